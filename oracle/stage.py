@@ -1,0 +1,274 @@
+"""One pipeline stage's training step under XPipe, in fp64 numpy.
+
+TEST INFRASTRUCTURE ONLY (the CPU oracle; see oracle/__init__.py).
+
+The step per mini-batch follows Sec. III-A and III-B: the forward bellwether
+predicts W_hat_f with its version difference (Eq. 1, Eq. 3), all T
+micro-batches run the forward on the cached W_hat_f; the backward bellwether
+predicts W_hat_b (Eq. 2, Eq. 3) and all T micro-batches run the backward on
+it, each backward first recomputing its forward (Sec. IV-C, recomputation
+during the backward pass); gradients are summed over the T micro-batches and
+the weights are updated once, after the T-th backward (Sec. III-A).
+
+Storage precision.  The oracle computes in fp64.  The GPU path stores
+activations, activation gradients and the optimizer state in a narrower
+format (fp32, or bf16 for activations in its bf16 variant).  Where a stored
+value decides an integer (a max-pool argmax, a ReLU mask), both sides must
+take the decision on values of the same precision, so the oracle can round
+(to nearest, ties to even) exactly the tensors that the GPU path stores:
+  storage="f32"   activations and gradients rounded to fp32;
+  storage="bf16"  activations and gradients rounded to bf16, conv/linear
+                  weights multiplied as bf16 (the fp32 prediction, rounded);
+in both, the predicted weights, the master weights, both moments and the
+gradient accumulator are rounded to fp32 each time they are written.
+Rounded activations are the outputs of conv, linear, relu, maxpool2, avgpool3
+and gap layers.  BN and residual-add outputs are never stored on their own
+(a ReLU always follows them in these stages) and are not rounded.  Every
+activation gradient is rounded each time a contribution is added to it;
+contributions arrive in reverse layer order.  storage="f64" rounds nothing.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import List, Optional
+
+import numpy as np
+
+from . import layers as ly
+from .method import adam_update, predict, PRED_EQ3
+
+
+def _round_f32(a):
+    """Round to the nearest fp32 value, as fp64."""
+    return np.asarray(a, np.float64).astype(np.float32).astype(np.float64)
+
+
+def _round_bf16(a):
+    """Round to the nearest bfloat16 value (ties to even) via fp32, as fp64."""
+    f = np.ascontiguousarray(np.asarray(a, np.float64).astype(np.float32))
+    u = f.view(np.uint32).astype(np.uint64)
+    r = (((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16).astype(np.uint32)
+    return r.view(np.float32).astype(np.float64)
+
+
+class Stage:
+    """A stage given as a layer list (see the workloads module for the format)."""
+
+    def __init__(self, layer_list: List[dict], storage: str = "f64"):
+        self.layers = layer_list
+        if storage not in ("f64", "f32", "bf16"):
+            raise ValueError(storage)
+        self.storage = storage
+        # parameter tensor indices owned by each layer
+        self.pidx = []
+        k = 0
+        for L in layer_list:
+            n = 0
+            if L["kind"] in ("linear", "conv"):
+                n = 2 if L["bias"] else 1
+            elif L["kind"] == "bn":
+                n = 2
+            self.pidx.append(list(range(k, k + n)))
+            k += n
+        self.n_params = k
+
+    # storage rounding: activations / gradients (q), conv and linear weight
+    # operands (qw), fp32 state (qs)
+    def q(self, a):
+        if self.storage == "bf16":
+            return _round_bf16(a)
+        if self.storage == "f32":
+            return _round_f32(a)
+        return a
+
+    def qw(self, a):
+        return self.q(a)
+
+    def qs(self, a):
+        return a if self.storage == "f64" else _round_f32(a)
+
+    @property
+    def has_loss(self):
+        return self.layers[-1]["kind"] == "softmax_ce"
+
+    # ------------------------------------------------------------ forward
+    def forward(self, params, x, labels=None, N=None):
+        """Returns (y, loss, saved): y is the stage output (the logits for a
+        stage ending in a loss), loss the CE sum / N or None."""
+        P = [np.asarray(p, np.float64) for p in params]
+        outs = {-1: np.asarray(x, np.float64)}
+        saved = {}
+        loss = None
+        for i, L in enumerate(self.layers):
+            k = L["kind"]
+            a = outs[L["inputs"][0]]
+            pi = self.pidx[i]
+            if k == "conv":
+                b = P[pi[1]] if L["bias"] else None
+                outs[i] = self.q(ly.conv2d(a, self.qw(P[pi[0]]), b))
+            elif k == "linear":
+                b = P[pi[1]] if L["bias"] else None
+                outs[i] = self.q(ly.linear(a, self.qw(P[pi[0]]), b))
+            elif k == "bn":
+                y, xhat, rstd = ly.batchnorm(a, P[pi[0]], P[pi[1]])
+                outs[i] = y
+                saved[i] = (xhat, rstd)
+            elif k == "relu":
+                outs[i] = self.q(ly.relu(a))
+            elif k == "add":
+                outs[i] = a + outs[L["inputs"][1]]
+            elif k == "maxpool2":
+                y, idx = ly.maxpool2(a)
+                outs[i] = y
+                saved[i] = idx
+            elif k == "avgpool3":
+                outs[i] = self.q(ly.avgpool3(a))
+            elif k == "gap":
+                outs[i] = self.q(ly.gap(a))
+            elif k == "concat":
+                outs[i] = np.concatenate([outs[j] for j in L["inputs"]], axis=-1)
+            elif k == "softmax_ce":
+                loss, dz = ly.softmax_ce(a, labels, N)
+                outs[i] = a
+                saved[i] = dz
+            else:
+                raise ValueError(k)
+        y = outs[len(self.layers) - 1]
+        return y, loss, (outs, saved)
+
+    # ------------------------------------------------------------ backward
+    def backward(self, params, x, dy=None, labels=None, N=None, need_dx=True):
+        """Recompute the forward at params, then the VJP.  Returns
+        (dx or None, [grad per parameter tensor], loss)."""
+        P = [np.asarray(p, np.float64) for p in params]
+        _, loss, (outs, saved) = self.forward(P, x, labels, N)
+        grads = [None] * self.n_params
+        g = {}
+
+        def acc(j, c):
+            g[j] = self.q(c) if j not in g else self.q(g[j] + c)
+
+        last = len(self.layers) - 1
+        if self.has_loss:
+            acc(self.layers[last]["inputs"][0], saved[last])
+        else:
+            g[last] = np.asarray(dy, np.float64)
+        for i in range(last, -1, -1):
+            L = self.layers[i]
+            k = L["kind"]
+            if k == "softmax_ce" or i not in g:
+                continue
+            gi = g[i]
+            src = L["inputs"][0]
+            a = outs[src]
+            pi = self.pidx[i]
+            want_dx = need_dx or src != -1
+            if k == "conv":
+                dx, dw, db = ly.conv2d_vjp(a, self.qw(P[pi[0]]), gi, want_dx, L["bias"])
+                grads[pi[0]] = dw
+                if L["bias"]:
+                    grads[pi[1]] = db
+                if want_dx:
+                    acc(src, dx)
+            elif k == "linear":
+                dx, dw, db = ly.linear_vjp(a, self.qw(P[pi[0]]), gi, want_dx, L["bias"])
+                grads[pi[0]] = dw
+                if L["bias"]:
+                    grads[pi[1]] = db
+                if want_dx:
+                    acc(src, dx)
+            elif k == "bn":
+                xhat, rstd = saved[i]
+                dz, dgamma, dbeta = ly.batchnorm_vjp(xhat, rstd, P[pi[0]], gi)
+                grads[pi[0]] = dgamma
+                grads[pi[1]] = dbeta
+                acc(src, dz)
+            elif k == "relu":
+                acc(src, ly.relu_vjp(outs[i], gi))
+            elif k == "add":
+                acc(src, gi)
+                acc(L["inputs"][1], gi)
+            elif k == "maxpool2":
+                acc(src, ly.maxpool2_vjp(a.shape, saved[i], gi))
+            elif k == "avgpool3":
+                acc(src, ly.avgpool3_vjp(gi))
+            elif k == "gap":
+                acc(src, ly.gap_vjp(a.shape, gi))
+            elif k == "concat":
+                c0 = 0
+                for j in L["inputs"]:
+                    cj = outs[j].shape[-1]
+                    acc(j, gi[..., c0:c0 + cj])
+                    c0 += cj
+            else:
+                raise ValueError(k)
+        dx = g.get(-1) if need_dx else None
+        return dx, grads, loss
+
+
+@dataclasses.dataclass
+class Hyper:
+    lr: float = 1e-3
+    beta1: float = 0.9
+    beta2: float = 0.999
+    eps: float = 1e-8
+    mode: str = PRED_EQ3
+
+
+@dataclasses.dataclass
+class MinibatchRecord:
+    t_before: int
+    w_pred_fwd: List[np.ndarray]
+    w_pred_bwd: List[np.ndarray]
+    ys: List[np.ndarray]
+    losses: List[Optional[float]]
+    dxs: List[Optional[np.ndarray]]
+    grad: List[np.ndarray]          # accumulated over the T micro-batches
+    W: List[np.ndarray]             # after the update
+    m: List[np.ndarray]
+    v: List[np.ndarray]
+
+
+def train_stage(stage: Stage, params, m, v, xs, s_fwd: int, s_bwd: int, hp: Hyper,
+                labels=None, dys=None, need_dx=True, minibatches=None,
+                t0: int = 0) -> List[MinibatchRecord]:
+    """Run mini-batches through one stage.  xs[j][i] is micro-batch i of
+    mini-batch j; labels or dys likewise.  params/m/v are per-tensor lists."""
+    qs = stage.qs
+    W = [qs(np.asarray(p, np.float64)) for p in params]
+    m = [qs(np.asarray(a, np.float64)) for a in m]
+    v = [qs(np.asarray(a, np.float64)) for a in v]
+    t = t0
+    J = len(xs) if minibatches is None else minibatches
+    T = len(xs[0])
+    N = T * xs[0][0].shape[0]
+    out = []
+    for j in range(J):
+        # forward bellwether: Eq. 1 version difference, Eq. 3 prediction, cached
+        Wf = [qs(predict(W[k], m[k], v[k], t, s_fwd, hp.lr, hp.beta1, hp.beta2, hp.eps, hp.mode))
+              for k in range(len(W))]
+        ys, losses = [], []
+        for i in range(T):
+            y, loss, _ = stage.forward(Wf, xs[j][i], None if labels is None else labels[j][i], N)
+            ys.append(y)
+            losses.append(loss)
+        # backward bellwether: Eq. 2 version difference, Eq. 3 prediction, cached
+        Wb = [qs(predict(W[k], m[k], v[k], t, s_bwd, hp.lr, hp.beta1, hp.beta2, hp.eps, hp.mode))
+              for k in range(len(W))]
+        G = [np.zeros_like(a) for a in W]
+        dxs = []
+        for i in range(T):
+            dx, gs, _ = stage.backward(Wb, xs[j][i], None if dys is None else dys[j][i],
+                                       None if labels is None else labels[j][i], N, need_dx)
+            for k in range(len(G)):
+                G[k] = qs(G[k] + gs[k])
+            dxs.append(dx)
+        # update at the T-th backward (Sec. III-A), Adam with Eq. 4's moments
+        t += 1
+        new = [adam_update(W[k], m[k], v[k], G[k], t, hp.lr, hp.beta1, hp.beta2, hp.eps)
+               for k in range(len(W))]
+        W = [qs(a[0]) for a in new]
+        m = [qs(a[1]) for a in new]
+        v = [qs(a[2]) for a in new]
+        out.append(MinibatchRecord(t - 1, Wf, Wb, ys, losses, dxs, G, W, m, v))
+    return out

@@ -1,0 +1,161 @@
+"""Pins for the oracle's stage step: forward/VJP against torch float64
+autograd on every stage architecture, gradient accumulation over
+micro-batches, and the reduction to plain Adam training when there is no
+pipeline (one stage, T = 1, s = 0)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wl
+from conftest import rel_l2
+import torch_ref
+
+SMALL = {
+    "tiny_mlp": dict(micro_batch=6),
+    "vgg16_stage0": dict(micro_batch=2, spatial=(12, 12)),
+    "resnet101_mid_stage": dict(micro_batch=2, spatial=(5, 6),
+                                layers=wl.resnet_stage_layers(blocks=2, c=24, mid=8),
+                                in_shape=(5, 6, 24)),
+    "inception_v3_stage": dict(micro_batch=2, spatial=(7, 7),
+                               layers=wl.inception_stage_layers(modules=2, cin=256, classes=12),
+                               in_shape=(7, 7, 256)),
+}
+
+
+def _small(name, **over):
+    kw = dict(SMALL[name])
+    kw.update(over)
+    return wl.shrink(wl.WORKLOADS[name](), **kw)
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_stage_forward_backward_matches_torch(name):
+    w = _small(name)
+    inp = wl.stage_inputs(w)
+    st = oracle.Stage(w.layers)
+    N = w.T * w.micro_batch
+    lab = None if inp.labels is None else inp.labels[0][0]
+    dy = None if inp.dys is None else inp.dys[0][0]
+    y, loss, _ = st.forward(inp.params, inp.xs[0][0], lab, N)
+    dx, grads, loss2 = st.backward(inp.params, inp.xs[0][0], dy, lab, N)
+    yt, losst, dxt, gt = torch_ref.fwd_bwd(w.layers, inp.params, inp.xs[0][0], dy, lab, N)
+    assert rel_l2(y, yt) < 1e-12
+    if loss is not None:
+        assert abs(loss - losst) < 1e-12 and loss2 == loss
+    assert rel_l2(dx, dxt) < 1e-11
+    for a, b in zip(grads, gt):
+        assert rel_l2(a, b) < 1e-11
+
+
+@pytest.mark.parametrize("name", ["tiny_mlp", "vgg16_stage0"])
+def test_accumulated_gradient_equals_full_minibatch_gradient(name):
+    """Sec. III-A: gradients accumulated over the T micro-batches of a mini-batch
+    equal the gradient of the whole mini-batch (no BN here, so the micro-batch
+    split does not change the function)."""
+    w = _small(name, T=3)
+    inp = wl.stage_inputs(w)
+    st = oracle.Stage(w.layers)
+    N = w.T * w.micro_batch
+    G = [np.zeros(p.shape) for p in inp.params]
+    for i in range(w.T):
+        lab = None if inp.labels is None else inp.labels[0][i]
+        dy = None if inp.dys is None else inp.dys[0][i]
+        _, g, _ = st.backward(inp.params, inp.xs[0][i], dy, lab, N)
+        G = [a + b for a, b in zip(G, g)]
+    x_all = np.concatenate(inp.xs[0])
+    lab_all = None if inp.labels is None else np.concatenate(inp.labels[0])
+    dy_all = None if inp.dys is None else np.concatenate(inp.dys[0])
+    _, g_all, _ = st.backward(inp.params, x_all, dy_all, lab_all, N)
+    for a, b in zip(G, g_all):
+        assert rel_l2(a, b) < 1e-12
+
+
+@pytest.mark.parametrize("name", ["tiny_mlp", "inception_v3_stage"])
+def test_no_pipeline_reduces_to_plain_adam_training(name):
+    """One stage, T = 1 and s = 0 (Eq. 1 and Eq. 2 both give 0 on one GPU):
+    the step is ordinary Adam training of the stage.  Compared with a torch
+    float64 model trained by torch.optim.Adam."""
+    w = _small(name, T=1, minibatches=3)
+    inp = wl.stage_inputs(w)
+    st = oracle.Stage(w.layers)
+    s_f = oracle.version_difference_fwd(1, 1, 0)
+    s_b = oracle.version_difference_bwd(1, 1, 0)
+    assert s_f == 0 and s_b == 0
+    hp = oracle.Hyper()
+    recs = oracle.train_stage(st, inp.params, inp.m, inp.v, inp.xs, s_f, s_b, hp,
+                              labels=inp.labels, dys=inp.dys)
+    P = [torch.tensor(np.asarray(p, np.float64), requires_grad=True) for p in inp.params]
+    opt = torch.optim.Adam(P, lr=hp.lr, betas=(hp.beta1, hp.beta2), eps=hp.eps)
+    N = w.micro_batch
+    for j in range(w.minibatches):
+        opt.zero_grad()
+        xt = torch.tensor(np.asarray(inp.xs[j][0], np.float64))
+        y, loss = torch_ref.forward(w.layers, P, xt, inp.labels[j][0] if inp.labels else None, N)
+        if loss is not None:
+            loss.backward()
+        else:
+            y.backward(torch.tensor(np.asarray(inp.dys[j][0], np.float64)))
+        opt.step()
+        for a, b in zip(recs[j].W, P):
+            np.testing.assert_allclose(a, b.detach().numpy(), rtol=0, atol=1e-13)
+
+
+def test_prediction_changes_the_step_once_moments_exist():
+    """t = 0 makes both predictions equal W (no update has happened yet); from
+    the second mini-batch on, s > 0 moves the predicted weights by s times the
+    Adam direction."""
+    w = _small("tiny_mlp", T=2, minibatches=2)
+    inp = wl.stage_inputs(w)
+    st = oracle.Stage(w.layers)
+    hp = oracle.Hyper()
+    recs = oracle.train_stage(st, inp.params, inp.m, inp.v, inp.xs, 2, 1, hp, labels=inp.labels)
+    for a, b in zip(recs[0].w_pred_fwd, inp.params):
+        assert np.array_equal(a, b)
+    r1 = recs[1]
+    for Wf, Wb, W, m, v in zip(r1.w_pred_fwd, r1.w_pred_bwd, recs[0].W, recs[0].m, recs[0].v):
+        np.testing.assert_allclose(Wf - W, 2 * (Wb - W), rtol=1e-9, atol=1e-18)
+        assert np.array_equal(Wf, oracle.predict(W, m, v, 1, 2, hp.lr, hp.beta1, hp.beta2, hp.eps))
+
+
+def test_f32_storage_stays_close_to_exact():
+    """Rounding activations, gradients and state to fp32 perturbs the step by
+    about fp32 precision; ReLU masks that flip where a pre-activation is within
+    rounding of zero add a little more (about 1e-4 here), nothing larger."""
+    w = _small("vgg16_stage0", T=2, minibatches=2)
+    inp = wl.stage_inputs(w)
+    hp = oracle.Hyper()
+    ref = oracle.train_stage(oracle.Stage(w.layers), inp.params, inp.m, inp.v, inp.xs, 2, 1, hp,
+                             dys=inp.dys)
+    got = oracle.train_stage(oracle.Stage(w.layers, "f32"), inp.params, inp.m, inp.v, inp.xs,
+                             2, 1, hp, dys=inp.dys)
+    for j in range(2):
+        for a, b in zip(got[j].ys, ref[j].ys):
+            assert rel_l2(a, b) < 1e-5
+        for a, b in zip(got[j].grad, ref[j].grad):
+            assert rel_l2(a, b) < 1e-3
+    y = got[0].ys[0]
+    assert np.array_equal(y, y.astype(np.float32).astype(np.float64))
+
+
+def test_bf16_storage_forward_close_to_exact():
+    """bf16 storage keeps the forward within bf16 precision of the exact one.
+    (Its backward is not close to the exact one: max-pool windows whose top two
+    values round to the same bf16 value route the gradient differently, which
+    is why the bf16 variant is checked against this storage mode.)"""
+    w = _small("vgg16_stage0", T=2, minibatches=1)
+    inp = wl.stage_inputs(w, act_dtype="bf16")
+    hp = oracle.Hyper()
+    ref = oracle.train_stage(oracle.Stage(w.layers), inp.params, inp.m, inp.v, inp.xs, 2, 1, hp,
+                             dys=inp.dys)
+    got = oracle.train_stage(oracle.Stage(w.layers, "bf16"), inp.params, inp.m, inp.v, inp.xs,
+                             2, 1, hp, dys=inp.dys)
+    for a, b in zip(got[0].ys, ref[0].ys):
+        assert rel_l2(a, b) < 1e-2
+    y = got[0].ys[0]
+    assert np.array_equal(y, ostage_round(y))
+
+
+def ostage_round(a):
+    from oracle.stage import _round_bf16
+    return _round_bf16(a)

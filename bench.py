@@ -1,0 +1,240 @@
+"""Benchmark of XPipe's one-stage training step on one MI355X.
+
+One step = one mini-batch of the stage: T forward micro-batches on the
+cached forward prediction, T backward micro-batches (each recomputing its
+forward) on the cached backward prediction, and the Adam update fused with
+emitting the next mini-batch's two predictions.  Inputs are seeded synthetic
+tensors already resident in HBM.
+
+Prints ONE JSON line: stage samples/s (value), the predict / Adam HBM rates
+of the 1e8-parameter sweep, the roofline of the dominant kernel, and the CPU
+oracle timed on a bounded sample.
+
+usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--dtype bf16|f32]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+PEAK_TFLOPS = {"bf16": 2500.0, "f64": 78.6, "f32": 157.3}
+CLASS_NAMES = {0: "conv/linear forward-type GEMM (fwd, recompute, data gradient)",
+               1: "weight-gradient GEMM", 2: "prediction / Adam", 3: "other layer kernels"}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="inception_v3_stage")
+    ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"])
+    ap.add_argument("--sweep-n", type=int, default=100_000_000)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true")
+    return ap.parse_args()
+
+
+def time_stage(args):
+    import torch
+    import paper_1911_04610_amd as xp
+    import workloads as wl
+    w = wl.WORKLOADS[args.workload]()
+    dt = xp.BF16 if args.dtype == "bf16" else xp.F32
+    tdt = torch.bfloat16 if dt == xp.BF16 else torch.float32
+    inp = wl.stage_inputs(w, act_dtype=args.dtype if args.dtype == "bf16" else "f32",
+                          moment_init="paper")
+    st = xp.Stage(w.layers, w.micro_batch, w.T, w.in_shape, dt)
+    st.set_flat(st.W, inp.params)
+    st.set_flat(st.m, inp.m)
+    st.set_flat(st.v, inp.v)
+
+    def dev(a):
+        return torch.from_numpy(a).cuda().to(tdt)
+
+    # three distinct mini-batches resident in HBM, reused round-robin
+    xs = [[dev(x) for x in row] for row in inp.xs]
+    labels = None if inp.labels is None else [[torch.from_numpy(l).cuda() for l in row]
+                                              for row in inp.labels]
+    dys = None if inp.dys is None else [[dev(d) for d in row] for row in inp.dys]
+    n, H, W_, C = st.out_shape
+    y = torch.empty((n, H, W_, C), dtype=tdt, device="cuda")
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    need_dx = w.rank > 0
+    dx = torch.empty((w.micro_batch,) + tuple(w.in_shape), dtype=tdt, device="cuda") if need_dx else None
+    hp = xp.Hyper()
+    state = {"t": 0}
+    st.xpipe_predict_weights(xp.FWD, w.s_fwd, hp, 0)
+    st.xpipe_predict_weights(xp.BWD, w.s_bwd, hp, 0)
+
+    def step(j):
+        J = len(xs)
+        for i in range(w.T):
+            st.xpipe_stage_fwd(xs[j % J][i], y, None if labels is None else labels[j % J][i],
+                               loss if w.has_loss else None)
+        for i in range(w.T):
+            st.xpipe_stage_bwd(xs[j % J][i], None if dys is None else dys[j % J][i],
+                               None if labels is None else labels[j % J][i], dx)
+        st.xpipe_adam_step(hp, state["t"], w.s_fwd, w.s_bwd, emit_pred=True)
+        state["t"] += 1
+
+    for j in range(args.warmup):
+        step(j)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for j in range(args.steps):
+        step(j)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / args.steps
+    # per-kernel-class durations with HIP events around every launch, over the
+    # same number of steps
+    st.set_timing(True)
+    for j in range(args.steps):
+        step(j)
+    torch.cuda.synchronize()
+    classes = {c: st.timing(c) for c in range(4)}
+    st.set_timing(False)
+    torch.cuda.synchronize()
+    fin = bool(torch.isfinite(st.W).all().item()) and (not w.has_loss or bool(torch.isfinite(loss).all().item()))
+    return w, ms, wall, classes, fin
+
+
+def time_sweep(n, steps):
+    """Prediction and Adam over n flat fp32 parameters at t = 100."""
+    import numpy as np
+    import torch
+    import paper_1911_04610_amd as xp
+    import workloads as wl
+    s = wl.flat_state(n)
+    W, m, v, G = (torch.from_numpy(a).cuda() for a in (s.W, s.m, s.v, s.G))
+    out = torch.empty_like(W)
+    pf, pb = torch.empty_like(W), torch.empty_like(W)
+    hp = xp.Hyper()
+    res = {}
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    reps = max(3, steps)
+    for sv in (0, 1, 2, 3, 7):
+        ms = timed(lambda: xp.xpipe_predict_flat(W, m, v, out, None, sv, hp, 100), reps)
+        res[f"predict_s{sv}"] = {"ms": ms, "GB_s": 16.0 * n / ms / 1e6}
+    ms = timed(lambda: xp.xpipe_adam_flat(W, m, v, G, hp, 100, False), reps)
+    res["adam"] = {"ms": ms, "GB_s": 28.0 * n / ms / 1e6}
+    ms = timed(lambda: xp.xpipe_adam_flat(W, m, v, G, hp, 100, True, pf, 2, pb, 1), reps)
+    res["adam_zero_grad_2pred"] = {"ms": ms, "GB_s": 40.0 * n / ms / 1e6}
+    del W, m, v, G, out, pf, pb
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(w, dtype):
+    """The oracle as it stands, on the host: one micro-batch's forward plus
+    its backward with recomputation, and the prediction + Adam over the
+    stage's parameters (a bounded sample of one step: 1 of T micro-batches)."""
+    import numpy as np
+    import oracle
+    import workloads as wl
+    threads = os.cpu_count()
+    try:
+        from threadpoolctl import threadpool_info
+        info = threadpool_info()
+        if info:
+            threads = max(i.get("num_threads", 0) for i in info) or threads
+    except Exception:
+        pass
+    inp = wl.stage_inputs(w, act_dtype="bf16" if dtype == "bf16" else "f32")
+    st = oracle.Stage(w.layers, "bf16" if dtype == "bf16" else "f32")
+    N = w.T * w.micro_batch
+    t0 = time.perf_counter()
+    lab = None if inp.labels is None else inp.labels[0][0]
+    dy = None if inp.dys is None else inp.dys[0][0]
+    st.forward(inp.params, inp.xs[0][0], lab, N)
+    st.backward(inp.params, inp.xs[0][0], dy, lab, N, need_dx=w.rank > 0)
+    hp = oracle.Hyper()
+    for p, m, v in zip(inp.params, inp.m, inp.v):
+        oracle.predict(p, m, v, 1, w.s_fwd, hp.lr, hp.beta1, hp.beta2, hp.eps)
+        oracle.adam_update(p, m, v, p, 1, hp.lr, hp.beta1, hp.beta2, hp.eps)
+    sec = time.perf_counter() - t0
+    return {"value": w.micro_batch / sec, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"1 of {w.T} micro-batches ({w.micro_batch} samples): forward + backward with "
+                       f"recompute in fp64 numpy ({dtype} storage rounding), plus prediction and Adam "
+                       f"over all {sum(p.size for p in inp.params)} parameters; {sec:.1f} s")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs one pipeline stage on one GPU; --gpus must be 1 "
+                                   "(each pipeline stage would run as its own one-GPU process)"}))
+        sys.exit(2)
+    import torch
+    import paper_1911_04610_amd as xp
+    torch.cuda.set_device(0)
+    w, ms, wall, classes, finite = time_stage(args)
+    samples = w.T * w.micro_batch
+    value = samples / (ms / 1e3)
+    peak_key = "bf16" if args.dtype == "bf16" else "f64"
+    dom = max((0, 1), key=lambda c: classes[c][0])
+    c_ms, c_n, c_work = classes[dom]
+    achieved = c_work / (c_ms / 1e3) / 1e12 if c_ms > 0 else 0.0
+    gemm_ms = classes[0][0] + classes[1][0]
+    gemm_work = classes[0][2] + classes[1][2]
+    out = {
+        "metric": "stage samples/sec (predict+fwd+bwd+Adam); predict/Adam HBM GB/s; MFMA util",
+        "value": round(value, 2),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": args.dtype,
+        "data": "synthetic (seeded N(0,1) inputs, Kaiming-uniform weights, paper moment init)",
+        "config": {"workload": w.name, "micro_batch": w.micro_batch, "T": w.T,
+                   "mini_batch": samples, "input_hwc": list(w.in_shape), "s_fwd": w.s_fwd,
+                   "s_bwd": w.s_bwd, "rank": w.rank, "size": w.size,
+                   "update": "adam fused with next predictions", "parallelism": "one stage, 1 GPU"},
+        "roofline": {"bound": "mfma", "kernel": CLASS_NAMES[dom], "achieved": round(achieved, 3),
+                     "peak": PEAK_TFLOPS[peak_key], "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_TFLOPS[peak_key], 5), "traffic": None,
+                     "launches": c_n, "avg_launch_us": round(1e3 * c_ms / max(c_n, 1), 3)},
+        "mfma_util_all_gemm": round(gemm_work / (gemm_ms / 1e3) / 1e12 / PEAK_TFLOPS[peak_key], 5)
+        if gemm_ms > 0 else None,
+        "kernel_classes_ms_per_step": {CLASS_NAMES[c]: round(classes[c][0] / args.steps, 4)
+                                       for c in range(4)},
+        "finite": finite,
+    }
+    if not args.no_sweep:
+        sw = time_sweep(args.sweep_n, args.steps)
+        out["predict_adam_sweep"] = {"n_params": args.sweep_n, "t": 100,
+                                     **{k: {"ms": round(v["ms"], 4), "GB_s": round(v["GB_s"], 1),
+                                            "frac_hbm": round(v["GB_s"] / HBM_PEAK_GBS, 4)}
+                                        for k, v in sw.items()}}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.dtype)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

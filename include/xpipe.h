@@ -1,0 +1,226 @@
+/*
+ * xpipe.h -- C ABI of libxpipe, one pipeline stage's training step under
+ * XPipe's asynchronous pipelining with Adam-based weight prediction
+ * (arXiv:1911.04610), on one AMD Instinct MI355X (gfx950).
+ *
+ * The step for one mini-batch of T micro-batches (Sec. III-A, III-B):
+ *   xpipe_predict_weights(FWD, s_f)   bellwether prediction, Eq. 3, cached
+ *   T x xpipe_stage_fwd(x_i)          forward on the cached forward prediction
+ *   xpipe_predict_weights(BWD, s_b)   bellwether prediction, Eq. 3, cached
+ *   T x xpipe_stage_bwd(x_i, dy_i)    recompute the forward, then the VJP;
+ *                                     weight gradients accumulate (Sec. III-A)
+ *   xpipe_adam_step(...)              update after the T-th backward (Eq. 4),
+ *                                     optionally emitting the next predictions
+ * s_f and s_b come from Eq. 1 and Eq. 2 (xpipe_version_difference).
+ *
+ * Conventions shared by every entry point:
+ *   - Device buffers and the HIP stream are owned by the caller.  A stage
+ *     handle keeps host-side descriptors and non-owning device pointers; it
+ *     allocates no device memory.
+ *   - Calls that touch the device enqueue work on the stage's stream and
+ *     return; results (including the loss) are in device memory once the
+ *     stream has been synchronised by the caller.
+ *   - Arguments are checked on the host before anything is enqueued.  A
+ *     failed check returns XPIPE_EINVAL (bad argument) or XPIPE_ESTATE (call
+ *     out of order) and leaves the device untouched.  A failed launch
+ *     returns XPIPE_EHIP.  xpipe_last_error() gives a message for the last
+ *     non-OK status of the calling thread.  No C++ exception crosses the ABI.
+ *   - Names follow the paper; its first moment v (decay gamma) and second
+ *     moment m (decay lambda) of Eq. 4 are called m (beta1) and v (beta2)
+ *     here, as in Adam.
+ */
+#ifndef XPIPE_H
+#define XPIPE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  XPIPE_OK = 0,
+  XPIPE_EINVAL = 1,       /* invalid argument, shape or layer list */
+  XPIPE_ESTATE = 2,       /* call out of order (see each entry point) */
+  XPIPE_EHIP = 3,         /* a HIP runtime call or kernel launch failed */
+  XPIPE_EUNSUPPORTED = 4  /* valid but not supported by this build */
+} xpipe_status;
+
+/* Storage format of activations and activation gradients.  Master weights,
+ * moments, gradient accumulator and predictions are fp32 in both.
+ *   XPIPE_F32:  fp32 storage; every contraction and reduction is computed in
+ *               fp64 (fp64 MFMA) and rounded once, on store.
+ *   XPIPE_BF16: bf16 storage; convolutions and linear layers multiply bf16
+ *               operands (the fp32 prediction rounded to nearest even) on
+ *               MFMA with fp32 accumulation; other layers compute in fp64. */
+typedef enum { XPIPE_F32 = 0, XPIPE_BF16 = 1 } xpipe_dtype;
+
+typedef enum { XPIPE_FWD = 0, XPIPE_BWD = 1 } xpipe_dir;
+
+/* Prediction direction of Eq. 3 (the paper prints eps inside the root and
+ * bias corrections without the power t; see XPIPE_PRED_LITERAL). */
+typedef enum {
+  XPIPE_PRED_EQ3 = 0,     /* m_hat / sqrt(v_hat + eps), m_hat = m/(1-beta1^t), v_hat = v/(1-beta2^t) */
+  XPIPE_PRED_ADAMDIR = 1, /* m_hat / (sqrt(v_hat) + eps): Adam's own update direction */
+  XPIPE_PRED_LITERAL = 2  /* (m/(1-beta1)) / sqrt(v/(1-beta2) + eps): Eq. 4 as printed */
+} xpipe_pred_mode;
+
+/* Tie rule for the "round" of Eq. 1 and Eq. 2 (undefined in the paper). */
+typedef enum {
+  XPIPE_ROUND_HALF_UP = 0,   /* ties away from zero (default reading) */
+  XPIPE_ROUND_HALF_EVEN = 1,
+  XPIPE_ROUND_HALF_DOWN = 2
+} xpipe_rounding;
+
+/* Layer kinds of a stage (Sec. IV-C's VGG-16, ResNet-101, Inception-V3).
+ * Activations are NHWC; a [n, C] tensor is NHWC with H = W = 1. */
+typedef enum {
+  XPIPE_LINEAR = 0,     /* y = x W^T + b; W [cout][cin]; input must have H = W = 1 */
+  XPIPE_CONV = 1,       /* k x k, stride 1, zero padding k/2, cross-correlation;
+                           W [cout][k][k][cin] (KRSC) */
+  XPIPE_BN = 2,         /* batch norm with the micro-batch's mean and biased
+                           variance, eps 1e-5; params gamma[C], beta[C] */
+  XPIPE_RELU = 3,       /* max(x, 0); derivative 0 at 0 */
+  XPIPE_ADD = 4,        /* inputs[0] + inputs[1] (same shape) */
+  XPIPE_MAXPOOL2 = 5,   /* 2x2 window, stride 2, floor; gradient to the first
+                           maximum in row-major window order */
+  XPIPE_AVGPOOL3 = 6,   /* 3x3 window, stride 1, zero padding 1, divisor 9 */
+  XPIPE_GAP = 7,        /* mean over H and W: [n,H,W,C] -> [n,1,1,C] */
+  XPIPE_CONCAT = 8,     /* channel concatenation of 2..4 inputs, in order */
+  XPIPE_SOFTMAX_CE = 9  /* loss = sum over the micro-batch of -log softmax(x)[label],
+                           divided by the mini-batch size N = T * micro_batch;
+                           must be the last layer */
+} xpipe_layer_kind;
+
+#define XPIPE_MAX_INPUTS 4
+
+typedef struct {
+  int32_t kind;                       /* xpipe_layer_kind */
+  int32_t n_inputs;                   /* 1, or 2 (ADD), or 2..4 (CONCAT) */
+  int32_t inputs[XPIPE_MAX_INPUTS];   /* producer layer indices (< own index); -1 = stage input */
+  int32_t cin, cout;                  /* LINEAR, CONV; BN uses cout as its channel count */
+  int32_t k;                          /* CONV kernel size (odd, 1..7) */
+  int32_t has_bias;                   /* LINEAR, CONV */
+  int32_t classes;                    /* SOFTMAX_CE: number of classes (= its input channels) */
+} xpipe_layer_desc;
+
+/* Optimizer and prediction hyper-parameters (Sec. IV-C: gamma 0.9,
+ * lambda 0.999, eps 1e-8).  t is the number of completed updates. */
+typedef struct {
+  double lr, beta1, beta2, eps;
+  int64_t t;
+  int32_t mode;                       /* xpipe_pred_mode */
+} xpipe_hparams;
+
+typedef struct xpipe_stage* xpipe_stage_t;
+
+/* Eq. 1 (dir = XPIPE_FWD): s = round((size + T - rank/2 - 2) / T);
+ * Eq. 2 (dir = XPIPE_BWD): s = round((T + floor(rank/2) - 1) / T).
+ * rounding selects the tie rule; ceil_half_rank != 0 reads Eq. 1's rank/2 as
+ * ceil(rank/2).  Host only.  EINVAL unless size >= 1, T >= 1, 0 <= rank < size. */
+xpipe_status xpipe_version_difference(int32_t size, int32_t T, int32_t rank, int32_t dir,
+                                      int32_t rounding, int32_t ceil_half_rank, int32_t* s_out);
+
+/* Validates a layer list for micro-batch shape [micro_batch, H, W, C] and
+ * reports the flat parameter count (each tensor zero-padded to a multiple of
+ * 64 elements) and the workspace size in bytes.  Host only. */
+xpipe_status xpipe_stage_query(const xpipe_layer_desc* layers, int32_t n_layers,
+                               int32_t micro_batch, int32_t H, int32_t W, int32_t C,
+                               int32_t dtype, int64_t* n_params_padded, size_t* workspace_bytes);
+
+/* Creates a stage.  W, m, v, grad, w_pred_fwd, w_pred_bwd are caller-owned
+ * fp32 device buffers of n_params_padded elements (layout: layers in order,
+ * weight then bias (CONV/LINEAR) or gamma then beta (BN), each tensor at a
+ * 64-element-aligned offset, padding zero).  workspace is caller-owned device
+ * memory of at least the queried size, 256-byte aligned.  T >= 1 is the
+ * number of micro-batches per mini-batch.  hip_stream is a hipStream_t (NULL
+ * = default stream).  grad is zeroed on the stream.  Nothing is predicted
+ * yet: call xpipe_predict_weights before the first forward. */
+xpipe_status xpipe_stage_create(const xpipe_layer_desc* layers, int32_t n_layers,
+                                int32_t micro_batch, int32_t T, int32_t H, int32_t W, int32_t C,
+                                int32_t dtype, void* hip_stream,
+                                float* W_, float* m, float* v, float* grad,
+                                float* w_pred_fwd, float* w_pred_bwd,
+                                void* workspace, size_t workspace_bytes, xpipe_stage_t* out);
+
+/* Number of parameter tensors, and offset/count (elements) of tensor idx. */
+xpipe_status xpipe_stage_num_param_tensors(xpipe_stage_t st, int32_t* n);
+xpipe_status xpipe_stage_param_layout(xpipe_stage_t st, int32_t tensor_idx,
+                                      int64_t* offset, int64_t* count);
+
+/* Stage output shape per micro-batch (for a stage ending in SOFTMAX_CE: the
+ * logits, [micro_batch, 1, 1, classes]). */
+xpipe_status xpipe_stage_output_shape(xpipe_stage_t st, int32_t* n, int32_t* H, int32_t* W,
+                                      int32_t* C);
+
+/* Bellwether prediction (Sec. III-B, Eq. 3 with Eq. 4's moments after hp->t
+ * completed updates): w_pred_{fwd|bwd} = W - s * lr * dir(m, v).  s >= 0.
+ * s = 0, or hp->t = 0 with a bias-corrected mode, gives W exactly.  The
+ * result is cached for the mini-batch's other T-1 micro-batches. */
+xpipe_status xpipe_predict_weights(xpipe_stage_t st, int32_t which, int32_t s,
+                                   const xpipe_hparams* hp);
+
+/* Forward of one micro-batch on the cached forward prediction.
+ * x: [micro_batch, H, W, C] in the stage dtype (fp32 or bf16), read only.
+ * y: stage output (logits for a loss stage), written.  labels: int32
+ * [micro_batch] in [0, classes), required iff the stage ends in SOFTMAX_CE;
+ * loss (fp32 scalar, may be NULL) receives this micro-batch's share of the
+ * mini-batch loss.  ESTATE before the first forward prediction. */
+xpipe_status xpipe_stage_fwd(xpipe_stage_t st, const void* x, void* y, const int32_t* labels,
+                             float* loss);
+
+/* Backward of one micro-batch on the cached backward prediction: the forward
+ * is recomputed from x (Sec. IV-C), then the vector-Jacobian product with dy
+ * (stage-output gradient, same dtype and shape as y; NULL for a loss stage,
+ * which uses labels).  Weight gradients are added into grad.  dx (input
+ * gradient, shape of x) is written unless NULL.  ESTATE before the first
+ * backward prediction. */
+xpipe_status xpipe_stage_bwd(xpipe_stage_t st, const void* x, const void* dy,
+                             const int32_t* labels, void* dx);
+
+/* Adam update at the mini-batch boundary (Sec. III-A; Kingma and Ba's update
+ * with Eq. 4's moments and bias correction for update number hp->t + 1, eps
+ * outside the root), then grad = 0.  With emit_pred != 0 the same pass also
+ * writes the next mini-batch's forward and backward predictions (version
+ * differences s_fwd_next, s_bwd_next, moments after hp->t + 1 updates), so
+ * the next mini-batch needs no xpipe_predict_weights.  ESTATE when no
+ * backward ran since the last update. */
+xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t s_fwd_next,
+                             int32_t s_bwd_next, int32_t emit_pred);
+
+xpipe_status xpipe_stage_destroy(xpipe_stage_t st);
+
+/* Flat-buffer forms of the two bandwidth-bound kernels, on n fp32 elements
+ * (any n >= 0; no alignment needed beyond 4 bytes, 16 bytes is faster).
+ * xpipe_predict_flat: out = W - s * lr * dir(m, v) (Eq. 3); out_bf16 (may be
+ * NULL) receives the same values rounded to bf16 (uint16 bit patterns).
+ * xpipe_adam_flat: W, m, v updated in place from G (update hp->t + 1); G is
+ * zeroed when zero_grad != 0; when pred_fwd / pred_bwd are not NULL they
+ * receive predictions with s_fwd / s_bwd from the updated state. */
+xpipe_status xpipe_predict_flat(const float* W, const float* m, const float* v, float* out,
+                                uint16_t* out_bf16, int64_t n, int32_t s, const xpipe_hparams* hp,
+                                void* hip_stream);
+xpipe_status xpipe_adam_flat(float* W, float* m, float* v, float* G, int64_t n,
+                             const xpipe_hparams* hp, int32_t zero_grad,
+                             float* pred_fwd, int32_t s_fwd, float* pred_bwd, int32_t s_bwd,
+                             void* hip_stream);
+
+/* Optional per-kernel timing: when enabled, hipEvents bracket every launch
+ * of the classes below on the stage stream; xpipe_stage_timing reports their
+ * summed duration (ms, after the caller synchronised), launch count and
+ * algorithmic work (flops for GEMM classes, bytes for the others).
+ * Classes: 0 conv/linear forward-type GEMM (forward, recompute, data
+ * gradient), 1 weight-gradient GEMM, 2 prediction/Adam, 3 everything else. */
+xpipe_status xpipe_stage_set_timing(xpipe_stage_t st, int32_t enable);
+xpipe_status xpipe_stage_timing(xpipe_stage_t st, int32_t kernel_class, double* ms,
+                                int64_t* launches, double* work);
+
+/* Message for the last non-OK status returned on the calling thread. */
+const char* xpipe_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* XPIPE_H */

@@ -1,0 +1,655 @@
+// Implicit-GEMM engine for convolution and linear layers on CDNA4 MFMA.
+//
+// Two precisions share one structure:
+//   bf16 storage: operands are bf16, v_mfma_f32_16x16x32_bf16, fp32 accumulators;
+//   fp32 storage: operands are fp32, widened to fp64 and multiplied with
+//                 v_mfma_f64_16x16x4f64 (fp64 accumulators), so every output is
+//                 the nearest fp32 of an (almost) exact dot product.
+// A 256-thread workgroup (4 wave64s) owns a BM x BN output tile.  Operand
+// tiles are staged through LDS in 16-byte chunks, double-buffered: the global
+// loads of step k+1 are in flight while the MFMAs of step k run.
+//
+// Forward-type GEMM (k_conv_gemm): rows m = output pixels, columns n = output
+// channels, reduction over (r, s, c) of the zero-padded input window.  The
+// A tile is gathered straight from the NHWC input (implicit im2col); with a
+// channel count that is a multiple of the 16-byte chunk, a reduction step
+// covers one (r, s) tap and a run of channels, otherwise every element is
+// gathered on its own ("flat" mode, used by 3-channel image inputs).
+//
+// Weight-gradient GEMM (k_wgrad): rows = output channels, columns = (r, s, c),
+// reduction over the pixels of the micro-batch.  The pixel range is split
+// over blockIdx.z; each split writes its partial tile to a workspace and a
+// second kernel adds the splits in a fixed order into the fp32 gradient
+// accumulator (deterministic, no atomics).
+#include "xp_device.h"
+#include "xp_kernels.h"
+
+namespace xp {
+
+template <typename T> struct MT;
+template <> struct MT<bf16_t> {
+  static constexpr int VEC = 8;     // elements per 16-byte chunk
+  static constexpr int BK = 32;     // reduction depth of one step (one MFMA)
+  static constexpr int PITCH = 40;  // LDS row pitch (elements), [row][k] layout
+  typedef f32x4_t acc_t;
+  typedef float part_t;
+  static XP_DEV int out_row(int lane, int q) { return 4 * (lane >> 4) + q; }
+};
+template <> struct MT<float> {
+  static constexpr int VEC = 4;
+  static constexpr int BK = 16;     // four 16x16x4 MFMA steps
+  static constexpr int PITCH = 20;  // 20 words: 16-byte aligned rows, conflict-free column reads
+  typedef f64x4_t acc_t;
+  typedef double part_t;
+  static XP_DEV int out_row(int lane, int q) { return (lane >> 4) + 4 * q; }
+};
+
+template <typename T>
+XP_DEV T zero_elem() { return T(0); }
+
+// pack VEC scalars (as raw bits) into a 16-byte chunk
+template <typename T>
+XP_DEV uint4 pack_chunk(const T* v);
+template <>
+XP_DEV uint4 pack_chunk<bf16_t>(const bf16_t* v) {
+  uint4 r;
+  r.x = (uint32_t)v[0] | ((uint32_t)v[1] << 16);
+  r.y = (uint32_t)v[2] | ((uint32_t)v[3] << 16);
+  r.z = (uint32_t)v[4] | ((uint32_t)v[5] << 16);
+  r.w = (uint32_t)v[6] | ((uint32_t)v[7] << 16);
+  return r;
+}
+template <>
+XP_DEV uint4 pack_chunk<float>(const float* v) {
+  uint4 r;
+  r.x = __float_as_uint(v[0]);
+  r.y = __float_as_uint(v[1]);
+  r.z = __float_as_uint(v[2]);
+  r.w = __float_as_uint(v[3]);
+  return r;
+}
+
+// ============================================================================
+// forward-type implicit GEMM
+// ============================================================================
+template <typename T, int BM, int BN, int WM, int WN, bool FLAT>
+__global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
+  using MTT = MT<T>;
+  constexpr int VEC = MTT::VEC, BK = MTT::BK, PITCH = MTT::PITCH;
+  constexpr int CPR = BK / VEC;  // chunks per tile row per step
+  constexpr int A_CH = BM * CPR, B_CH = BN * CPR;
+  constexpr int A_PER = (A_CH + 255) / 256, B_PER = (B_CH + 255) / 256;
+  constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
+  static_assert(WM * WN == 4, "four waves");
+  static_assert(TM >= 1 && TN >= 1, "wave tile");
+  __shared__ __align__(16) T sA[2][BM * PITCH];
+  __shared__ __align__(16) T sB[2][BN * PITCH];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int H = a.H, W = a.W, C = a.C, S = a.S, pad = a.pad;
+  const int M = a.nb * H * W;
+  const int K = a.R * S * C;
+  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  const T* __restrict__ x = (const T*)a.x;
+  const T* __restrict__ w = (const T*)a.w;
+
+  // fixed per-thread chunk slots
+  int a_row[A_PER], a_kc[A_PER], a_img[A_PER], a_h[A_PER], a_w[A_PER];
+  bool a_slot[A_PER], a_valid[A_PER];
+#pragma unroll
+  for (int i = 0; i < A_PER; ++i) {
+    int q = tid + i * 256;
+    a_slot[i] = q < A_CH;
+    a_row[i] = q / CPR;
+    a_kc[i] = q % CPR;
+    int m = m0 + a_row[i];
+    a_valid[i] = a_slot[i] && m < M;
+    int mm = a_valid[i] ? m : 0;
+    a_img[i] = mm / (H * W);
+    int rem = mm - a_img[i] * H * W;
+    a_h[i] = rem / W;
+    a_w[i] = rem - a_h[i] * W;
+  }
+  int b_row[B_PER], b_kc[B_PER];
+  bool b_slot[B_PER], b_valid[B_PER];
+#pragma unroll
+  for (int i = 0; i < B_PER; ++i) {
+    int q = tid + i * 256;
+    b_slot[i] = q < B_CH;
+    b_row[i] = q / CPR;
+    b_kc[i] = q % CPR;
+    b_valid[i] = b_slot[i] && (n0 + b_row[i]) < a.N;
+  }
+
+  const int nCB = FLAT ? 1 : (C + BK - 1) / BK;
+  const int nk = FLAT ? (K + BK - 1) / BK : a.R * S * nCB;
+
+  uint4 ra[A_PER], rb[B_PER];
+
+  auto gload = [&](int kb) {
+    if constexpr (!FLAT) {
+      int rs = kb / nCB, cb = kb - rs * nCB;
+      int r = rs / S, s = rs - r * S;
+#pragma unroll
+      for (int i = 0; i < A_PER; ++i) {
+        uint4 v = make_uint4(0, 0, 0, 0);
+        int c = cb * BK + a_kc[i] * VEC;
+        int hh = a_h[i] + r - pad, ww = a_w[i] + s - pad;
+        if (a_valid[i] && c < C && hh >= 0 && hh < H && ww >= 0 && ww < W)
+          v = *reinterpret_cast<const uint4*>(x + ((size_t)(a_img[i] * H + hh) * W + ww) * a.ldx + c);
+        ra[i] = v;
+      }
+#pragma unroll
+      for (int i = 0; i < B_PER; ++i) {
+        uint4 v = make_uint4(0, 0, 0, 0);
+        int c = cb * BK + b_kc[i] * VEC;
+        if (b_valid[i] && c < C)
+          v = *reinterpret_cast<const uint4*>(w + (size_t)(n0 + b_row[i]) * K + rs * C + c);
+        rb[i] = v;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < A_PER; ++i) {
+        T vals[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          int k = kb * BK + a_kc[i] * VEC + e;
+          T val = zero_elem<T>();
+          if (a_valid[i] && k < K) {
+            int rs = k / C, c = k - rs * C;
+            int r = rs / S, s = rs - r * S;
+            int hh = a_h[i] + r - pad, ww = a_w[i] + s - pad;
+            if (hh >= 0 && hh < H && ww >= 0 && ww < W)
+              val = x[((size_t)(a_img[i] * H + hh) * W + ww) * a.ldx + c];
+          }
+          vals[e] = val;
+        }
+        ra[i] = pack_chunk<T>(vals);
+      }
+#pragma unroll
+      for (int i = 0; i < B_PER; ++i) {
+        T vals[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          int k = kb * BK + b_kc[i] * VEC + e;
+          vals[e] = (b_valid[i] && k < K) ? w[(size_t)(n0 + b_row[i]) * K + k] : zero_elem<T>();
+        }
+        rb[i] = pack_chunk<T>(vals);
+      }
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < A_PER; ++i)
+      if (a_slot[i]) *reinterpret_cast<uint4*>(&sA[buf][a_row[i] * PITCH + a_kc[i] * VEC]) = ra[i];
+#pragma unroll
+    for (int i = 0; i < B_PER; ++i)
+      if (b_slot[i]) *reinterpret_cast<uint4*>(&sB[buf][b_row[i] * PITCH + b_kc[i] * VEC]) = rb[i];
+  };
+
+  typename MTT::acc_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[i][j][q] = 0;
+
+  auto compute = [&](int buf) {
+    const T* A = sA[buf];
+    const T* B = sB[buf];
+    if constexpr (sizeof(T) == 2) {
+      bf16x8_t af[TM], bfv[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        af[i] = *reinterpret_cast<const bf16x8_t*>(&A[(wm * WTM + i * 16 + (lane & 15)) * PITCH + (lane >> 4) * 8]);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        bfv[j] = *reinterpret_cast<const bf16x8_t*>(&B[(wn * WTN + j * 16 + (lane & 15)) * PITCH + (lane >> 4) * 8]);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfv[j], acc[i][j], 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        double af[TM], bfv[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          af[i] = (double)A[(wm * WTM + i * 16 + (lane & 15)) * PITCH + kk * 4 + (lane >> 4)];
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          bfv[j] = (double)B[(wn * WTN + j * 16 + (lane & 15)) * PITCH + kk * 4 + (lane >> 4)];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[i], bfv[j], acc[i][j], 0, 0, 0);
+      }
+    }
+  };
+
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int kb = 0; kb < nk; ++kb) {
+    const bool more = kb + 1 < nk;
+    if (more) gload(kb + 1);
+    compute(kb & 1);
+    if (more) lstore((kb + 1) & 1);
+    __syncthreads();
+  }
+
+  // epilogue: bias, ReLU, mask, accumulate, round once on store
+  T* __restrict__ y = (T*)a.y;
+  const T* __restrict__ mask = (const T*)a.mask;
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        int m = m0 + wm * WTM + i * 16 + MTT::out_row(lane, q);
+        int n = n0 + wn * WTN + j * 16 + (lane & 15);
+        if (m < M && n < a.N) {
+          double v = (double)acc[i][j][q];
+          if (a.bias) v += (double)a.bias[n];
+          if (a.relu) v = v > 0.0 ? v : 0.0;
+          if (mask && !(ldd(mask + (size_t)m * a.ldm + n) > 0.0)) v = 0.0;
+          T* p = y + (size_t)m * a.ldy + n;
+          if (a.accumulate) v += ldd(p);
+          std_(p, v);
+        }
+      }
+}
+
+// ============================================================================
+// weight-gradient GEMM with split reduction over pixels
+// ============================================================================
+// bf16: LDS tiles are [row][pixel] (pixel-contiguous) so the MFMA operand
+// fragments are 16-byte reads; the global chunks run along channels, so each
+// thread loads two pixels and interleaves them into 32-bit pairs on the way in.
+// fp32/fp64: one element per lane per MFMA, so the natural [pixel][row] layout
+// is read directly.
+template <typename T> struct WG;
+template <> struct WG<bf16_t> {
+  static constexpr int BKm = 32;
+};
+template <> struct WG<float> {
+  static constexpr int BKm = 16;
+};
+
+template <typename T, int BM, int BN, int WM, int WN, bool FLAT>
+__global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
+  using MTT = MT<T>;
+  constexpr int VEC = MTT::VEC;
+  constexpr int BKm = WG<T>::BKm;
+  constexpr bool BF = sizeof(T) == 2;
+  // LDS geometry
+  constexpr int PA = BF ? (BKm + 8) : (BM + 16);  // pitch of A tile rows
+  constexpr int PB = BF ? (BKm + 8) : (BN + 16);
+  constexpr int SA = BF ? BM * PA : BKm * PA;     // elements per buffer
+  constexpr int SB = BF ? BN * PB : BKm * PB;
+  __shared__ __align__(16) T sA[2][SA];
+  __shared__ __align__(16) T sB[2][SB];
+  constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
+  static_assert(WM * WN == 4, "four waves");
+  // load tasks: bf16: (pixel pair, 8-channel chunk); fp32: (pixel, 4-channel chunk)
+  constexpr int A_T = BF ? (BKm / 2) * (BM / VEC) : BKm * (BM / VEC);
+  constexpr int B_T = BF ? (BKm / 2) * (BN / VEC) : BKm * (BN / VEC);
+  constexpr int A_PER = (A_T + 255) / 256, B_PER = (B_T + 255) / 256;
+  constexpr int RPT = BF ? 2 : 1;  // pixels per task
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int H = a.H, W = a.W, C = a.C, S = a.S, pad = a.pad, N = a.N;
+  const int HW = H * W;
+  const int M = a.nb * HW;
+  const int K = a.R * S * C;
+  const int n0 = blockIdx.x * BM, k0 = blockIdx.y * BN;
+  const int mps = ((M + a.splits - 1) / a.splits + BKm - 1) / BKm * BKm;
+  const int mbeg = blockIdx.z * mps;
+  const int mend = min(M, mbeg + mps);
+  const T* __restrict__ dz = (const T*)a.dz;
+  const T* __restrict__ x = (const T*)a.x;
+  const bool dz_vec = (a.lddz % VEC) == 0 && (reinterpret_cast<uintptr_t>(a.dz) % 16) == 0;
+
+  // task geometry (fixed over the pixel loop)
+  int a_p[A_PER], a_c[A_PER];
+  bool a_slot[A_PER];
+#pragma unroll
+  for (int i = 0; i < A_PER; ++i) {
+    int q = tid + i * 256;
+    a_slot[i] = q < A_T;
+    a_c[i] = q % (BM / VEC);   // channel chunk (output-channel dim)
+    a_p[i] = q / (BM / VEC);   // pixel (pair) index
+  }
+  int b_p[B_PER], b_c[B_PER], b_r[B_PER], b_s[B_PER], b_ch[B_PER];
+  bool b_slot[B_PER], b_kok[B_PER];
+#pragma unroll
+  for (int i = 0; i < B_PER; ++i) {
+    int q = tid + i * 256;
+    b_slot[i] = q < B_T;
+    b_c[i] = q % (BN / VEC);
+    b_p[i] = q / (BN / VEC);
+    int kk = k0 + b_c[i] * VEC;
+    b_kok[i] = kk < K;
+    int rs = FLAT ? 0 : kk / C;
+    b_ch[i] = FLAT ? 0 : kk - rs * C;
+    b_r[i] = FLAT ? 0 : rs / S;
+    b_s[i] = FLAT ? 0 : rs - b_r[i] * S;
+  }
+
+  uint4 ra[A_PER][RPT], rb[B_PER][RPT];
+
+  auto gload = [&](int mb) {
+#pragma unroll
+    for (int i = 0; i < A_PER; ++i)
+#pragma unroll
+      for (int u = 0; u < RPT; ++u) {
+        int m = mb + a_p[i] * RPT + u;
+        int n = n0 + a_c[i] * VEC;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (a_slot[i] && m < mend && n < N) {
+          const T* src = dz + (size_t)m * a.lddz + n;
+          if (dz_vec && n + VEC <= N) {
+            v = *reinterpret_cast<const uint4*>(src);
+          } else {
+            T vals[VEC];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) vals[e] = (n + e < N) ? src[e] : zero_elem<T>();
+            v = pack_chunk<T>(vals);
+          }
+        }
+        ra[i][u] = v;
+      }
+#pragma unroll
+    for (int i = 0; i < B_PER; ++i)
+#pragma unroll
+      for (int u = 0; u < RPT; ++u) {
+        int m = mb + b_p[i] * RPT + u;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (b_slot[i] && m < mend) {
+          int img = m / HW, rem = m - img * HW, h = rem / W, ww0 = rem - h * W;
+          if constexpr (!FLAT) {
+            int hh = h + b_r[i] - pad, ww = ww0 + b_s[i] - pad;
+            if (b_kok[i] && hh >= 0 && hh < H && ww >= 0 && ww < W)
+              v = *reinterpret_cast<const uint4*>(x + ((size_t)(img * H + hh) * W + ww) * a.ldx + b_ch[i]);
+          } else {
+            T vals[VEC];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+              int k = k0 + b_c[i] * VEC + e;
+              T val = zero_elem<T>();
+              if (k < K) {
+                int rs = k / C, c = k - rs * C, r = rs / S, s = rs - r * S;
+                int hh = h + r - pad, ww = ww0 + s - pad;
+                if (hh >= 0 && hh < H && ww >= 0 && ww < W)
+                  val = x[((size_t)(img * H + hh) * W + ww) * a.ldx + c];
+              }
+              vals[e] = val;
+            }
+            v = pack_chunk<T>(vals);
+          }
+        }
+        rb[i][u] = v;
+      }
+  };
+
+  auto lstore = [&](int buf) {
+    if constexpr (BF) {
+      // interleave two pixels: word e of row (chunk*8 + e) holds (pixel 2p, pixel 2p+1)
+#pragma unroll
+      for (int i = 0; i < A_PER; ++i) {
+        if (!a_slot[i]) continue;
+        const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&ra[i][0]);
+        const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&ra[i][1]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          uint32_t lo = (r0[j] & 0xffffu) | (r1[j] << 16);
+          uint32_t hi = (r0[j] >> 16) | (r1[j] & 0xffff0000u);
+          int row = a_c[i] * VEC + 2 * j;
+          *reinterpret_cast<uint32_t*>(&sA[buf][row * PA + 2 * a_p[i]]) = lo;
+          *reinterpret_cast<uint32_t*>(&sA[buf][(row + 1) * PA + 2 * a_p[i]]) = hi;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < B_PER; ++i) {
+        if (!b_slot[i]) continue;
+        const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&rb[i][0]);
+        const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&rb[i][1]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          uint32_t lo = (r0[j] & 0xffffu) | (r1[j] << 16);
+          uint32_t hi = (r0[j] >> 16) | (r1[j] & 0xffff0000u);
+          int row = b_c[i] * VEC + 2 * j;
+          *reinterpret_cast<uint32_t*>(&sB[buf][row * PB + 2 * b_p[i]]) = lo;
+          *reinterpret_cast<uint32_t*>(&sB[buf][(row + 1) * PB + 2 * b_p[i]]) = hi;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < A_PER; ++i)
+        if (a_slot[i]) *reinterpret_cast<uint4*>(&sA[buf][a_p[i] * PA + a_c[i] * VEC]) = ra[i][0];
+#pragma unroll
+      for (int i = 0; i < B_PER; ++i)
+        if (b_slot[i]) *reinterpret_cast<uint4*>(&sB[buf][b_p[i] * PB + b_c[i] * VEC]) = rb[i][0];
+    }
+  };
+
+  typename MTT::acc_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[i][j][q] = 0;
+
+  auto compute = [&](int buf) {
+    const T* A = sA[buf];
+    const T* B = sB[buf];
+    if constexpr (BF) {
+      bf16x8_t af[TM], bfv[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        af[i] = *reinterpret_cast<const bf16x8_t*>(&A[(wm * WTM + i * 16 + (lane & 15)) * PA + (lane >> 4) * 8]);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        bfv[j] = *reinterpret_cast<const bf16x8_t*>(&B[(wn * WTN + j * 16 + (lane & 15)) * PB + (lane >> 4) * 8]);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfv[j], acc[i][j], 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        double af[TM], bfv[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          af[i] = (double)A[(kk * 4 + (lane >> 4)) * PA + wm * WTM + i * 16 + (lane & 15)];
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          bfv[j] = (double)B[(kk * 4 + (lane >> 4)) * PB + wn * WTN + j * 16 + (lane & 15)];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[i], bfv[j], acc[i][j], 0, 0, 0);
+      }
+    }
+  };
+
+  const int nsteps = mend > mbeg ? (mend - mbeg + BKm - 1) / BKm : 0;
+  if (nsteps > 0) {
+    gload(mbeg);
+    lstore(0);
+  }
+  __syncthreads();
+  for (int st = 0; st < nsteps; ++st) {
+    const bool more = st + 1 < nsteps;
+    if (more) gload(mbeg + (st + 1) * BKm);
+    compute(st & 1);
+    if (more) lstore((st + 1) & 1);
+    __syncthreads();
+  }
+
+  typename MTT::part_t* part = (typename MTT::part_t*)a.part + (size_t)blockIdx.z * N * K;
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        int n = n0 + wm * WTM + i * 16 + MTT::out_row(lane, q);
+        int k = k0 + wn * WTN + j * 16 + (lane & 15);
+        if (n < N && k < K) part[(size_t)n * K + k] = acc[i][j][q];
+      }
+}
+
+template <typename P>
+__global__ __launch_bounds__(256) void k_split_reduce(const P* __restrict__ part, int splits,
+                                                       int64_t count, float* __restrict__ grad) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    double s = 0.0;
+    for (int z = 0; z < splits; ++z) s += (double)part[(size_t)z * count + i];
+    grad[i] = (float)((double)grad[i] + s);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_flip(const T* __restrict__ w, T* __restrict__ wd, int N,
+                                               int R, int S, int C) {
+  int64_t total = (int64_t)N * R * S * C;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    // i indexes wd[c][r][s][n]
+    int n = (int)(i % N);
+    int64_t t = i / N;
+    int s = (int)(t % S);
+    t /= S;
+    int r = (int)(t % R);
+    int c = (int)(t / R);
+    wd[i] = w[(((int64_t)n * R + (R - 1 - r)) * S + (S - 1 - s)) * C + c];
+  }
+}
+
+// ============================================================================
+// host launchers
+// ============================================================================
+static int pick_bn(int N) {
+  // smallest padded width among 32 / 64 / 128; ties go to the wider tile
+  int best = 128, best_pad = ((N + 127) / 128) * 128;
+  int pad64 = ((N + 63) / 64) * 64, pad32 = ((N + 31) / 32) * 32;
+  if (pad64 < best_pad) { best = 64; best_pad = pad64; }
+  if (pad32 < best_pad) { best = 32; best_pad = pad32; }
+  return best;
+}
+
+template <typename T, int BM, int BN, int WM, int WN>
+static hipError_t conv_go(const ConvArgs& a, bool flat, hipStream_t s) {
+  int M = a.nb * a.H * a.W;
+  dim3 grid((M + BM - 1) / BM, (a.N + BN - 1) / BN);
+  if (flat)
+    hipLaunchKernelGGL((k_conv_gemm<T, BM, BN, WM, WN, true>), grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_conv_gemm<T, BM, BN, WM, WN, false>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t conv_dispatch(const ConvArgs& a, hipStream_t s) {
+  constexpr int VEC = MT<T>::VEC;
+  bool flat = (a.C % VEC) != 0 || (a.ldx % VEC) != 0 ||
+              (reinterpret_cast<uintptr_t>(a.x) % 16) != 0 ||
+              (reinterpret_cast<uintptr_t>(a.w) % 16) != 0;
+  int M = a.nb * a.H * a.W;
+  int bn = pick_bn(a.N);
+  // small problems: shorter row tiles give more workgroups
+  int tiles128 = ((M + 127) / 128) * ((a.N + bn - 1) / bn);
+  bool bm64 = tiles128 < 512;
+  if (!bm64) {
+    if (bn == 128) return conv_go<T, 128, 128, 2, 2>(a, flat, s);
+    if (bn == 64) return conv_go<T, 128, 64, 2, 2>(a, flat, s);
+    return conv_go<T, 128, 32, 4, 1>(a, flat, s);
+  }
+  if (bn == 128) return conv_go<T, 64, 128, 2, 2>(a, flat, s);
+  if (bn == 64) return conv_go<T, 64, 64, 2, 2>(a, flat, s);
+  return conv_go<T, 64, 32, 2, 2>(a, flat, s);
+}
+
+hipError_t launch_conv_gemm(int dtype, const ConvArgs& a, hipStream_t s) {
+  if (a.nb * a.H * a.W <= 0 || a.N <= 0) return hipSuccess;
+  return dtype == DT_BF16 ? conv_dispatch<bf16_t>(a, s) : conv_dispatch<float>(a, s);
+}
+
+int wgrad_pick_splits(int M, int N, int K) {
+  int bm = N <= 64 ? 64 : 128;
+  int bn = K <= 64 ? 64 : 128;
+  int tiles = ((N + bm - 1) / bm) * ((K + bn - 1) / bn);
+  int want = (512 + tiles - 1) / tiles;
+  int maxs = (M + 127) / 128;  // keep at least ~128 pixels per split
+  if (want > maxs) want = maxs;
+  if (want < 1) want = 1;
+  return want;
+}
+
+size_t wgrad_part_bytes(int dtype, int N, int K, int splits) {
+  return (size_t)splits * N * K * (dtype == DT_BF16 ? sizeof(float) : sizeof(double));
+}
+
+template <typename T, int BM, int BN, int WM, int WN>
+static hipError_t wgrad_go(const WgradArgs& a, bool flat, hipStream_t s) {
+  int K = a.R * a.S * a.C;
+  dim3 grid((a.N + BM - 1) / BM, (K + BN - 1) / BN, a.splits);
+  if (flat)
+    hipLaunchKernelGGL((k_wgrad<T, BM, BN, WM, WN, true>), grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_wgrad<T, BM, BN, WM, WN, false>), grid, dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  int64_t count = (int64_t)a.N * K;
+  int blocks = (int)((count + 255) / 256);
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_split_reduce<typename MT<T>::part_t>, dim3(blocks), dim3(256), 0, s,
+                     (const typename MT<T>::part_t*)a.part, a.splits, count, a.grad);
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t wgrad_dispatch(const WgradArgs& a, hipStream_t s) {
+  constexpr int VEC = MT<T>::VEC;
+  bool flat = (a.C % VEC) != 0 || (a.ldx % VEC) != 0 ||
+              (reinterpret_cast<uintptr_t>(a.x) % 16) != 0;
+  int K = a.R * a.S * a.C;
+  bool n64 = a.N <= 64, k64 = K <= 64;
+  if (n64 && k64) return wgrad_go<T, 64, 64, 2, 2>(a, flat, s);
+  if (n64) return wgrad_go<T, 64, 128, 2, 2>(a, flat, s);
+  if (k64) return wgrad_go<T, 128, 64, 2, 2>(a, flat, s);
+  return wgrad_go<T, 128, 128, 2, 2>(a, flat, s);
+}
+
+hipError_t launch_wgrad(int dtype, const WgradArgs& a, hipStream_t s) {
+  if (a.N <= 0) return hipSuccess;
+  return dtype == DT_BF16 ? wgrad_dispatch<bf16_t>(a, s) : wgrad_dispatch<float>(a, s);
+}
+
+hipError_t launch_flip_weights(int dtype, const void* w, void* wd, int N, int R, int S, int C,
+                               hipStream_t s) {
+  int64_t total = (int64_t)N * R * S * C;
+  int blocks = (int)((total + 255) / 256);
+  if (blocks > 4096) blocks = 4096;
+  if (total <= 0) return hipSuccess;
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(k_flip<bf16_t>, dim3(blocks), dim3(256), 0, s, (const bf16_t*)w,
+                       (bf16_t*)wd, N, R, S, C);
+  else
+    hipLaunchKernelGGL(k_flip<float>, dim3(blocks), dim3(256), 0, s, (const float*)w,
+                       (float*)wd, N, R, S, C);
+  return hipGetLastError();
+}
+
+}  // namespace xp

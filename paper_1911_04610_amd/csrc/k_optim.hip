@@ -1,0 +1,189 @@
+// Weight prediction (Eq. 3) and the Adam update (Eq. 4 moments, Kingma-Ba
+// step) over flat fp32 buffers: bandwidth-bound streaming kernels.
+//
+// Each thread moves 16-byte vectors (global_load_dwordx4) with non-temporal
+// hints (the buffers are read once per call and far exceed the caches at
+// production sizes); no LDS.  Arithmetic is done in fp64 and rounded once to
+// fp32 on store, so a stored value is the nearest fp32 of the exact formula
+// evaluated on the stored inputs.
+#include "xp_device.h"
+#include "xp_kernels.h"
+
+namespace xp {
+
+XP_DEV double pred_dir(double m, double v, const PredCoef& c) {
+  double mh = m * c.c1, vh = v * c.c2;
+  return c.eps_outside ? mh / (sqrt(vh) + c.eps) : mh / sqrt(vh + c.eps);
+}
+
+// s = 0 (or t = 0 with bias correction) is the identity: W is returned bit for bit
+XP_DEV float predict1(float w, float m, float v, const PredCoef& c) {
+  if (c.coef == 0.0) return w;
+  return (float)((double)w - c.coef * pred_dir((double)m, (double)v, c));
+}
+
+typedef float nf4 __attribute__((ext_vector_type(4)));
+typedef uint32_t nu2 __attribute__((ext_vector_type(2)));
+
+// streaming (non-temporal) 16-byte / 8-byte accesses
+XP_DEV float4 ldnt(const float4* p) {
+  nf4 v = __builtin_nontemporal_load(reinterpret_cast<const nf4*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+XP_DEV void stnt(float4* p, float4 v) {
+  nf4 r = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(r, reinterpret_cast<nf4*>(p));
+}
+XP_DEV void stnt(uint2* p, uint2 v) {
+  nu2 r = {v.x, v.y};
+  __builtin_nontemporal_store(r, reinterpret_cast<nu2*>(p));
+}
+
+// ---------------------------------------------------------------- predict
+__global__ __launch_bounds__(256) void k_predict(const float* __restrict__ W,
+                                                  const float* __restrict__ m,
+                                                  const float* __restrict__ v,
+                                                  float* __restrict__ out,
+                                                  bf16_t* __restrict__ out_bf, int64_t n,
+                                                  PredCoef c) {
+  const int64_t nv = n >> 2;  // float4 chunks (buffers are 16-byte aligned)
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const float4* W4 = reinterpret_cast<const float4*>(W);
+  const float4* m4 = reinterpret_cast<const float4*>(m);
+  const float4* v4 = reinterpret_cast<const float4*>(v);
+  float4* o4 = reinterpret_cast<float4*>(out);
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nv; i += stride) {
+    float4 w = ldnt(W4 + i), mm = ldnt(m4 + i), vv = ldnt(v4 + i);
+    float4 r;
+    r.x = predict1(w.x, mm.x, vv.x, c);
+    r.y = predict1(w.y, mm.y, vv.y, c);
+    r.z = predict1(w.z, mm.z, vv.z, c);
+    r.w = predict1(w.w, mm.w, vv.w, c);
+    stnt(o4 + i, r);
+    if (out_bf) {
+      uint2 b;
+      b.x = (uint32_t)f32_to_bf16(r.x) | ((uint32_t)f32_to_bf16(r.y) << 16);
+      b.y = (uint32_t)f32_to_bf16(r.z) | ((uint32_t)f32_to_bf16(r.w) << 16);
+      stnt(reinterpret_cast<uint2*>(out_bf) + i, b);
+    }
+  }
+  // scalar tail
+  int64_t t = (nv << 2) + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < n) {
+    float r = predict1(W[t], m[t], v[t], c);
+    out[t] = r;
+    if (out_bf) out_bf[t] = f32_to_bf16(r);
+  }
+}
+
+// ---------------------------------------------------------------- adam (+zero grad, +predictions)
+struct AdamElem {
+  float w, m, v;
+};
+
+// The moment recurrences are evaluated operation by operation (no fused
+// multiply-add) in the order beta*m + ((1-beta)*g) and beta*v + (((1-beta)*g)*g):
+// for fp32 inputs the exact result often falls exactly halfway between two
+// fp32 values, and only an identical sequence of roundings settles such ties
+// the same way as a reference evaluated in that order.
+XP_DEV AdamElem adam1(float w, float m, float v, float g, const AdamCoef& a) {
+#pragma clang fp contract(off)
+  double gd = (double)g;
+  double mn = a.beta1 * (double)m + a.one_m_beta1 * gd;
+  double vn = a.beta2 * (double)v + (a.one_m_beta2 * gd) * gd;
+  double wn = (double)w - a.lr * (mn * a.bc1) / (sqrt(vn * a.bc2) + a.eps);
+  return AdamElem{(float)wn, (float)mn, (float)vn};
+}
+
+__global__ __launch_bounds__(256) void k_adam(float* __restrict__ W, float* __restrict__ m,
+                                               float* __restrict__ v, float* __restrict__ G,
+                                               int64_t n, AdamCoef a, int zero_grad,
+                                               float* __restrict__ pf, bf16_t* __restrict__ pf_bf,
+                                               PredCoef cf, float* __restrict__ pb,
+                                               bf16_t* __restrict__ pb_bf, PredCoef cb) {
+  const int64_t nv = n >> 2;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  float4* W4 = reinterpret_cast<float4*>(W);
+  float4* m4 = reinterpret_cast<float4*>(m);
+  float4* v4 = reinterpret_cast<float4*>(v);
+  float4* G4 = reinterpret_cast<float4*>(G);
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nv; i += stride) {
+    float4 w = ldnt(W4 + i), mm = ldnt(m4 + i), vv = ldnt(v4 + i), g = ldnt(G4 + i);
+    AdamElem e0 = adam1(w.x, mm.x, vv.x, g.x, a);
+    AdamElem e1 = adam1(w.y, mm.y, vv.y, g.y, a);
+    AdamElem e2 = adam1(w.z, mm.z, vv.z, g.z, a);
+    AdamElem e3 = adam1(w.w, mm.w, vv.w, g.w, a);
+    stnt(W4 + i, make_float4(e0.w, e1.w, e2.w, e3.w));
+    stnt(m4 + i, make_float4(e0.m, e1.m, e2.m, e3.m));
+    stnt(v4 + i, make_float4(e0.v, e1.v, e2.v, e3.v));
+    if (zero_grad) stnt(G4 + i, make_float4(0.f, 0.f, 0.f, 0.f));
+    if (pf) {
+      float4 r = make_float4(predict1(e0.w, e0.m, e0.v, cf), predict1(e1.w, e1.m, e1.v, cf),
+                             predict1(e2.w, e2.m, e2.v, cf), predict1(e3.w, e3.m, e3.v, cf));
+      stnt(reinterpret_cast<float4*>(pf) + i, r);
+      if (pf_bf) {
+        uint2 b;
+        b.x = (uint32_t)f32_to_bf16(r.x) | ((uint32_t)f32_to_bf16(r.y) << 16);
+        b.y = (uint32_t)f32_to_bf16(r.z) | ((uint32_t)f32_to_bf16(r.w) << 16);
+        stnt(reinterpret_cast<uint2*>(pf_bf) + i, b);
+      }
+    }
+    if (pb) {
+      float4 r = make_float4(predict1(e0.w, e0.m, e0.v, cb), predict1(e1.w, e1.m, e1.v, cb),
+                             predict1(e2.w, e2.m, e2.v, cb), predict1(e3.w, e3.m, e3.v, cb));
+      stnt(reinterpret_cast<float4*>(pb) + i, r);
+      if (pb_bf) {
+        uint2 b;
+        b.x = (uint32_t)f32_to_bf16(r.x) | ((uint32_t)f32_to_bf16(r.y) << 16);
+        b.y = (uint32_t)f32_to_bf16(r.z) | ((uint32_t)f32_to_bf16(r.w) << 16);
+        stnt(reinterpret_cast<uint2*>(pb_bf) + i, b);
+      }
+    }
+  }
+  int64_t t = (nv << 2) + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < n) {
+    AdamElem e = adam1(W[t], m[t], v[t], G[t], a);
+    W[t] = e.w;
+    m[t] = e.m;
+    v[t] = e.v;
+    if (zero_grad) G[t] = 0.f;
+    if (pf) {
+      float r = predict1(e.w, e.m, e.v, cf);
+      pf[t] = r;
+      if (pf_bf) pf_bf[t] = f32_to_bf16(r);
+    }
+    if (pb) {
+      float r = predict1(e.w, e.m, e.v, cb);
+      pb[t] = r;
+      if (pb_bf) pb_bf[t] = f32_to_bf16(r);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+static int stream_grid(int64_t n) {
+  // enough waves in flight to saturate HBM: 256 CUs x 8 blocks of 256 threads
+  int64_t nv = (n >> 2) + 1;
+  int64_t blocks = (nv + 255) / 256;
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  return (int)blocks;
+}
+
+hipError_t launch_predict(const float* W, const float* m, const float* v, float* out,
+                          bf16_t* out_bf, int64_t n, const PredCoef& c, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_predict, dim3(stream_grid(n)), dim3(256), 0, s, W, m, v, out, out_bf, n, c);
+  return hipGetLastError();
+}
+
+hipError_t launch_adam(float* W, float* m, float* v, float* G, int64_t n, const AdamCoef& a,
+                       int zero_grad, float* pf, bf16_t* pf_bf, const PredCoef& cf, float* pb,
+                       bf16_t* pb_bf, const PredCoef& cb, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_adam, dim3(stream_grid(n)), dim3(256), 0, s, W, m, v, G, n, a, zero_grad,
+                     pf, pf_bf, cf, pb, pb_bf, cb);
+  return hipGetLastError();
+}
+
+}  // namespace xp

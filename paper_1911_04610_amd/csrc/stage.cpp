@@ -1,0 +1,1272 @@
+// libxpipe host runtime: stage planning, launch sequencing and the C ABI.
+//
+// A stage is a layer list (see include/xpipe.h).  At creation the runtime
+//   - checks every layer and infers NHWC shapes,
+//   - lays out the flat parameter buffer (64-element aligned tensors),
+//   - groups layers into fused launches: conv/linear (+ReLU in the epilogue),
+//     BN (+residual add) (+ReLU), add (+ReLU), pools, GAP, softmax-CE; a
+//     concatenation costs nothing: its inputs are produced straight into
+//     channel slices of its buffer,
+//   - gives every group output an activation buffer and a gradient buffer in
+//     the caller's workspace.  A gradient buffer of a ReLU output holds the
+//     gradient of the pre-activation: every producer multiplies by the mask
+//     (output > 0) as it writes.
+//   - fixes, for each gradient buffer, which producer writes first and which
+//     ones add (reverse layer order), so the backward is deterministic.
+// Each call then only enqueues kernels on the stage's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/xpipe.h"
+#include "xp_kernels.h"
+
+using namespace xp;
+
+namespace {
+
+thread_local std::string g_err;
+
+xpipe_status fail(xpipe_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+#define XP_HIP(call)                                                                     \
+  do {                                                                                   \
+    hipError_t e_ = (call);                                                              \
+    if (e_ != hipSuccess)                                                                \
+      return fail(XPIPE_EHIP, std::string(#call) + ": " + hipGetErrorString(e_));        \
+  } while (0)
+
+constexpr int64_t PARAM_ALIGN = 64;  // elements
+constexpr size_t WS_ALIGN = 256;     // bytes
+constexpr double BN_EPS = 1e-5;
+
+int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+struct Shape {
+  int n = 0, H = 0, W = 0, C = 0;
+  int64_t rows() const { return (int64_t)n * H * W; }
+  int64_t elems() const { return rows() * C; }
+};
+
+enum OpKind { OP_GEMM, OP_BN, OP_ELT, OP_MAXPOOL, OP_AVGPOOL, OP_GAP, OP_CONCAT, OP_CE };
+
+struct Tensor {
+  Shape sh;
+  int owner = -1;        // owning tensor id for a concat member view, else -1
+  int coff = 0;          // channel offset in the owner
+  int64_t act_off = -1;  // workspace byte offset of the owner's activation buffer
+  int64_t grad_off = -1; // workspace byte offset of the owner's gradient buffer
+  bool masked = false;   // values are ReLU outputs
+  int consumers = 0;
+};
+
+struct Op {
+  OpKind kind = OP_ELT;
+  int layer = -1;      // primary layer
+  int in = -1;         // input tensor
+  int in2 = -1;        // residual / second add operand tensor
+  int out = -1;        // output tensor (-1 for CE)
+  bool relu = false;
+  // GEMM
+  int cin = 0, cout = 0, k = 1;
+  int64_t w_off = -1, b_off = -1;   // parameter offsets (elements)
+  int64_t wd_off = -1;              // workspace bytes: flipped weights for the data gradient
+  // BN
+  int64_t g_off = -1, be_off = -1;  // gamma / beta parameter offsets
+  int64_t stat_off = -1;            // workspace bytes: mean, rstd, dbeta, dgamma (doubles)
+  // backward bookkeeping: first producer writes, later ones add
+  bool in_acc = false, in2_acc = false;
+};
+
+struct ParamT {
+  int64_t off, count;
+};
+
+struct TimeRec {
+  hipEvent_t a, b;
+  int cls;
+  double work;
+};
+
+}  // namespace
+
+struct xpipe_stage {
+  std::vector<xpipe_layer_desc> layers;
+  int mb = 0, T = 1, dtype = DT_F32;
+  Shape in_shape;
+  hipStream_t stream = nullptr;
+  float *W = nullptr, *m = nullptr, *v = nullptr, *grad = nullptr;
+  float *wpf = nullptr, *wpb = nullptr;
+  char* ws = nullptr;
+  size_t ws_bytes = 0;
+  int64_t P = 0;
+  std::vector<ParamT> params;
+  std::vector<Tensor> tensors;  // [0] = stage input
+  std::vector<Op> ops;
+  int out_tensor = -1;          // stage output tensor (logits for a loss stage)
+  bool has_loss = false;
+  int classes = 0;
+  int64_t bf_f_off = -1, bf_b_off = -1;  // bf16 shadows of the predictions
+  int64_t colpart_off = -1, wpart_off = -1;
+  // call-order state
+  bool pred_valid[2] = {false, false};
+  bool wd_valid = false;
+  int64_t bwd_since_step = 0;
+  // timing
+  bool timing = false;
+  std::vector<TimeRec> pending;
+  std::vector<hipEvent_t> pool;
+  double t_ms[4] = {0, 0, 0, 0};
+  double t_work[4] = {0, 0, 0, 0};
+  int64_t t_n[4] = {0, 0, 0, 0};
+
+  size_t esz() const { return dtype == DT_BF16 ? 2 : 4; }
+};
+
+namespace {
+
+// ============================================================================
+// planning
+// ============================================================================
+struct Plan {
+  std::vector<ParamT> params;
+  std::vector<Tensor> tensors;
+  std::vector<Op> ops;
+  int out_tensor = -1;
+  bool has_loss = false;
+  int classes = 0;
+  int64_t P = 0;
+  size_t ws = 0;
+  int64_t bf_f_off = -1, bf_b_off = -1, colpart_off = -1, wpart_off = -1;
+};
+
+xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, int C, int dtype,
+                        Plan& p) {
+  if (!L || n <= 0) return fail(XPIPE_EINVAL, "empty layer list");
+  if (mb <= 0 || H <= 0 || W <= 0 || C <= 0) return fail(XPIPE_EINVAL, "bad input shape");
+  if (dtype != DT_F32 && dtype != DT_BF16) return fail(XPIPE_EINVAL, "bad dtype");
+  if ((int64_t)mb * H * W > (int64_t)1 << 30) return fail(XPIPE_EINVAL, "micro-batch too large");
+  const size_t esz = dtype == DT_BF16 ? 2 : 4;
+
+  // ---- shapes and parameters
+  std::vector<Shape> sh(n);
+  std::vector<int> consumers(n + 1, 0);  // index i+1 for layer i, 0 for the input
+  Shape in{mb, H, W, C};
+  auto shape_of = [&](int idx) -> Shape { return idx < 0 ? in : sh[idx]; };
+  int64_t P = 0;
+  std::vector<int64_t> poff(n, -1), poff2(n, -1);
+  for (int i = 0; i < n; ++i) {
+    const xpipe_layer_desc& d = L[i];
+    char where[64];
+    snprintf(where, sizeof where, "layer %d: ", i);
+    int ni = d.n_inputs;
+    int need = (d.kind == XPIPE_ADD) ? 2 : (d.kind == XPIPE_CONCAT ? -1 : 1);
+    if (need > 0 && ni != need) return fail(XPIPE_EINVAL, std::string(where) + "wrong input count");
+    if (d.kind == XPIPE_CONCAT && (ni < 2 || ni > XPIPE_MAX_INPUTS))
+      return fail(XPIPE_EINVAL, std::string(where) + "concat takes 2..4 inputs");
+    for (int j = 0; j < ni; ++j) {
+      if (d.inputs[j] < -1 || d.inputs[j] >= i)
+        return fail(XPIPE_EINVAL, std::string(where) + "input index out of order");
+      consumers[d.inputs[j] + 1]++;
+    }
+    Shape s = shape_of(d.inputs[0]);
+    switch (d.kind) {
+      case XPIPE_LINEAR:
+      case XPIPE_CONV: {
+        int k = d.kind == XPIPE_LINEAR ? 1 : d.k;
+        if (d.kind == XPIPE_LINEAR && (s.H != 1 || s.W != 1))
+          return fail(XPIPE_EINVAL, std::string(where) + "linear input must have H = W = 1");
+        if (k < 1 || k > 7 || (k % 2) == 0) return fail(XPIPE_EINVAL, std::string(where) + "bad kernel size");
+        if (d.cin != s.C || d.cout <= 0) return fail(XPIPE_EINVAL, std::string(where) + "channel mismatch");
+        poff[i] = P;
+        P += align_up((int64_t)d.cout * k * k * d.cin, PARAM_ALIGN);
+        if (d.has_bias) {
+          poff2[i] = P;
+          P += align_up(d.cout, PARAM_ALIGN);
+        }
+        s.C = d.cout;
+        break;
+      }
+      case XPIPE_BN:
+        if (d.cout != s.C) return fail(XPIPE_EINVAL, std::string(where) + "bn channel mismatch");
+        poff[i] = P;
+        P += align_up(s.C, PARAM_ALIGN);
+        poff2[i] = P;
+        P += align_up(s.C, PARAM_ALIGN);
+        break;
+      case XPIPE_RELU:
+        break;
+      case XPIPE_ADD: {
+        Shape s2 = shape_of(d.inputs[1]);
+        if (s2.n != s.n || s2.H != s.H || s2.W != s.W || s2.C != s.C)
+          return fail(XPIPE_EINVAL, std::string(where) + "add shape mismatch");
+        break;
+      }
+      case XPIPE_MAXPOOL2:
+        if (s.H < 2 || s.W < 2) return fail(XPIPE_EINVAL, std::string(where) + "maxpool input too small");
+        s.H /= 2;
+        s.W /= 2;
+        break;
+      case XPIPE_AVGPOOL3:
+        break;
+      case XPIPE_GAP:
+        s.H = 1;
+        s.W = 1;
+        break;
+      case XPIPE_CONCAT: {
+        int c = 0;
+        for (int j = 0; j < ni; ++j) {
+          Shape sj = shape_of(d.inputs[j]);
+          if (sj.n != s.n || sj.H != s.H || sj.W != s.W)
+            return fail(XPIPE_EINVAL, std::string(where) + "concat spatial mismatch");
+          c += sj.C;
+        }
+        s.C = c;
+        break;
+      }
+      case XPIPE_SOFTMAX_CE:
+        if (i != n - 1) return fail(XPIPE_EINVAL, std::string(where) + "softmax_ce must be last");
+        if (s.H != 1 || s.W != 1 || d.classes != s.C || s.C <= 0)
+          return fail(XPIPE_EINVAL, std::string(where) + "softmax_ce needs [n, classes] logits");
+        if (s.n > 1024) return fail(XPIPE_EINVAL, std::string(where) + "micro-batch above 1024");
+        break;
+      default:
+        return fail(XPIPE_EINVAL, std::string(where) + "unknown layer kind");
+    }
+    sh[i] = s;
+  }
+  for (int i = 0; i < n - 1; ++i)
+    if (consumers[i + 1] == 0)
+      return fail(XPIPE_EINVAL, "layer " + std::to_string(i) + " output is never used");
+  if (consumers[0] == 0) return fail(XPIPE_EINVAL, "stage input is never used");
+
+  // parameter table
+  for (int i = 0; i < n; ++i) {
+    const xpipe_layer_desc& d = L[i];
+    if (d.kind == XPIPE_LINEAR || d.kind == XPIPE_CONV) {
+      int k = d.kind == XPIPE_LINEAR ? 1 : d.k;
+      p.params.push_back({poff[i], (int64_t)d.cout * k * k * d.cin});
+      if (d.has_bias) p.params.push_back({poff2[i], d.cout});
+    } else if (d.kind == XPIPE_BN) {
+      p.params.push_back({poff[i], d.cout});
+      p.params.push_back({poff2[i], d.cout});
+    }
+  }
+  p.P = P;
+
+  // ---- grouping
+  auto single_consumer = [&](int i, int kind) -> int {
+    // index of the only consumer of layer i if it has the given kind, else -1
+    if (consumers[i + 1] != 1) return -1;
+    for (int j = i + 1; j < n; ++j)
+      for (int q = 0; q < L[j].n_inputs; ++q)
+        if (L[j].inputs[q] == i) return L[j].kind == kind ? j : -1;
+    return -1;
+  };
+  std::vector<int> tensor_of(n, -1);  // layer -> tensor holding its (group's) output
+  std::vector<bool> absorbed(n, false);
+  p.tensors.clear();
+  Tensor tin;
+  tin.sh = in;
+  p.tensors.push_back(tin);  // tensor 0: stage input
+  auto tens = [&](int layer) -> int { return layer < 0 ? 0 : tensor_of[layer]; };
+  auto new_tensor = [&](Shape s) -> int {
+    Tensor t;
+    t.sh = s;
+    p.tensors.push_back(t);
+    return (int)p.tensors.size() - 1;
+  };
+
+  for (int i = 0; i < n; ++i) {
+    if (absorbed[i]) continue;
+    const xpipe_layer_desc& d = L[i];
+    Op op;
+    op.layer = i;
+    op.in = tens(d.inputs[0]);
+    if (op.in < 0) return fail(XPIPE_EINVAL, "layer " + std::to_string(i) + " reads a fused intermediate");
+    int last = i;
+    switch (d.kind) {
+      case XPIPE_LINEAR:
+      case XPIPE_CONV: {
+        op.kind = OP_GEMM;
+        op.cin = d.cin;
+        op.cout = d.cout;
+        op.k = d.kind == XPIPE_LINEAR ? 1 : d.k;
+        op.w_off = poff[i];
+        op.b_off = d.has_bias ? poff2[i] : -1;
+        int r = single_consumer(i, XPIPE_RELU);
+        if (r >= 0) {
+          op.relu = true;
+          absorbed[r] = true;
+          last = r;
+        }
+        break;
+      }
+      case XPIPE_BN: {
+        op.kind = OP_BN;
+        op.g_off = poff[i];
+        op.be_off = poff2[i];
+        int a = single_consumer(i, XPIPE_ADD);
+        int other = a >= 0 ? (L[a].inputs[0] == i ? L[a].inputs[1] : L[a].inputs[0]) : -2;
+        // the residual must already exist when the BN group runs
+        if (a >= 0 && (other == i || other >= i)) a = -1;
+        if (a >= 0) {
+          op.in2 = tens(other);
+          if (op.in2 < 0) return fail(XPIPE_EINVAL, "residual reads a fused intermediate");
+          absorbed[a] = true;
+          last = a;
+        }
+        int r = single_consumer(last, XPIPE_RELU);
+        if (r >= 0) {
+          op.relu = true;
+          absorbed[r] = true;
+          last = r;
+        }
+        break;
+      }
+      case XPIPE_ADD:
+      case XPIPE_RELU: {
+        op.kind = OP_ELT;
+        if (d.kind == XPIPE_ADD) {
+          op.in2 = tens(d.inputs[1]);
+          if (op.in2 < 0) return fail(XPIPE_EINVAL, "add reads a fused intermediate");
+        } else {
+          op.relu = true;
+        }
+        if (d.kind == XPIPE_ADD) {
+          int r = single_consumer(i, XPIPE_RELU);
+          if (r >= 0) {
+            op.relu = true;
+            absorbed[r] = true;
+            last = r;
+          }
+        }
+        break;
+      }
+      case XPIPE_MAXPOOL2: op.kind = OP_MAXPOOL; break;
+      case XPIPE_AVGPOOL3: op.kind = OP_AVGPOOL; break;
+      case XPIPE_GAP: op.kind = OP_GAP; break;
+      case XPIPE_CONCAT: op.kind = OP_CONCAT; break;
+      case XPIPE_SOFTMAX_CE: op.kind = OP_CE; break;
+    }
+    if (op.kind != OP_CE) {
+      int t = new_tensor(sh[last]);
+      p.tensors[t].masked = op.relu;
+      for (int q = i; q <= last; ++q)
+        if (q == i || absorbed[q]) tensor_of[q] = t;
+      op.out = t;
+    }
+    p.ops.push_back(op);
+  }
+
+  // consumer counts per tensor (by op inputs)
+  for (const Op& op : p.ops) {
+    if (op.kind == OP_CONCAT) {
+      for (int q = 0; q < L[op.layer].n_inputs; ++q) p.tensors[tens(L[op.layer].inputs[q])].consumers++;
+      continue;
+    }
+    p.tensors[op.in].consumers++;
+    if (op.in2 >= 0) p.tensors[op.in2].consumers++;
+  }
+
+  // ---- concat views
+  for (const Op& op : p.ops) {
+    if (op.kind != OP_CONCAT) continue;
+    int coff = 0;
+    bool all_masked = true;
+    for (int q = 0; q < L[op.layer].n_inputs; ++q) {
+      int t = tens(L[op.layer].inputs[q]);
+      Tensor& m = p.tensors[t];
+      if (t == 0 || m.owner >= 0 || m.consumers != 1)
+        return fail(XPIPE_EUNSUPPORTED, "concat inputs must be layer outputs used only by the concat");
+      m.owner = op.out;
+      m.coff = coff;
+      coff += m.sh.C;
+      all_masked = all_masked && m.masked;
+    }
+    p.tensors[op.out].masked = all_masked;
+  }
+  // concat-of-concat: resolve owners transitively
+  for (size_t t = 0; t < p.tensors.size(); ++t) {
+    int o = p.tensors[t].owner;
+    while (o >= 0 && p.tensors[o].owner >= 0) {
+      p.tensors[t].coff += p.tensors[o].coff;
+      o = p.tensors[o].owner;
+    }
+    p.tensors[t].owner = o;
+  }
+
+  const Op& lastop = p.ops.back();
+  if (lastop.kind == OP_CE) {
+    p.has_loss = true;
+    p.classes = L[n - 1].classes;
+    p.out_tensor = lastop.in;
+    if (p.tensors[p.out_tensor].consumers != 1 || p.tensors[p.out_tensor].masked ||
+        p.tensors[p.out_tensor].owner >= 0 || p.out_tensor == 0)
+      return fail(XPIPE_EUNSUPPORTED, "softmax_ce input must be a linear/conv output used only by it");
+  } else {
+    p.out_tensor = lastop.out;
+  }
+
+  // ---- backward accumulation order: walk ops in reverse; first contribution writes
+  {
+    std::vector<bool> written(p.tensors.size(), false);
+    auto claim = [&](int t) -> bool {
+      int o = p.tensors[t].owner >= 0 ? p.tensors[t].owner : t;
+      // concat members are disjoint slices of their owner: track per member
+      int key = p.tensors[t].owner >= 0 ? t : o;
+      bool acc = written[key];
+      written[key] = true;
+      return acc;
+    };
+    for (int i = (int)p.ops.size() - 1; i >= 0; --i) {
+      Op& op = p.ops[i];
+      if (op.kind == OP_CONCAT) {
+        // the gradient of the concat is, slice by slice, the gradient of its members
+        for (int q = 0; q < L[op.layer].n_inputs; ++q) claim(tens(L[op.layer].inputs[q]));
+        continue;
+      }
+      op.in_acc = claim(op.in);
+      if (op.in2 >= 0) op.in2_acc = claim(op.in2);
+    }
+  }
+
+  // ---- workspace layout
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> int64_t {
+    off = (size_t)align_up((int64_t)off, WS_ALIGN);
+    int64_t at = (int64_t)off;
+    off += bytes;
+    return at;
+  };
+  if (dtype == DT_BF16) {
+    p.bf_f_off = take((size_t)P * 2);
+    p.bf_b_off = take((size_t)P * 2);
+  }
+  size_t colpart = 0, wpart = 0;
+  for (Op& op : p.ops) {
+    const Tensor& tin_ = p.tensors[op.in];
+    if (op.kind == OP_GEMM) {
+      op.wd_off = take((size_t)op.cout * op.k * op.k * op.cin * esz);
+      int M = (int)tin_.sh.rows();
+      int K = op.k * op.k * op.cin;
+      int splits = wgrad_pick_splits(M, op.cout, K);
+      wpart = std::max(wpart, wgrad_part_bytes(dtype, op.cout, K, splits));
+      if (op.b_off >= 0) colpart = std::max(colpart, col_partial_bytes(M, op.cout));
+    } else if (op.kind == OP_BN) {
+      op.stat_off = take((size_t)4 * tin_.sh.C * sizeof(double));
+      colpart = std::max(colpart, col_partial_bytes((int)tin_.sh.rows(), tin_.sh.C));
+    }
+  }
+  for (size_t t = 1; t < p.tensors.size(); ++t) {
+    Tensor& tt = p.tensors[t];
+    if (tt.owner >= 0) continue;
+    tt.act_off = take((size_t)tt.sh.elems() * esz);
+    tt.grad_off = take((size_t)tt.sh.elems() * esz);
+  }
+  p.colpart_off = take(std::max<size_t>(colpart, 64));
+  p.wpart_off = take(std::max<size_t>(wpart, 64));
+  p.ws = (size_t)align_up((int64_t)off, WS_ALIGN);
+  return XPIPE_OK;
+}
+
+// ============================================================================
+// execution helpers
+// ============================================================================
+struct View {
+  char* p;
+  int ld;
+};
+
+struct Ctx {
+  const void* x = nullptr;  // stage input
+  void* y = nullptr;        // stage output override (forward)
+  void* dx = nullptr;       // stage input gradient (backward), may be null
+};
+
+View act(xpipe_stage* st, int t, const Ctx& c) {
+  const Tensor& tt = st->tensors[t];
+  if (t == 0) return View{(char*)c.x, tt.sh.C};
+  int o = tt.owner >= 0 ? tt.owner : t;
+  const Tensor& ot = st->tensors[o];
+  char* base = (c.y && o == st->out_tensor) ? (char*)c.y : st->ws + ot.act_off;
+  return View{base + (size_t)tt.coff * st->esz(), ot.sh.C};
+}
+
+View gradv(xpipe_stage* st, int t, const Ctx& c) {
+  const Tensor& tt = st->tensors[t];
+  if (t == 0) return View{(char*)c.dx, tt.sh.C};
+  int o = tt.owner >= 0 ? tt.owner : t;
+  const Tensor& ot = st->tensors[o];
+  return View{st->ws + ot.grad_off + (size_t)tt.coff * st->esz(), ot.sh.C};
+}
+
+hipEvent_t take_event(xpipe_stage* st) {
+  if (!st->pool.empty()) {
+    hipEvent_t e = st->pool.back();
+    st->pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// brackets a launch with events when timing is on
+struct Timed {
+  xpipe_stage* st;
+  int cls;
+  double work;
+  hipEvent_t a = nullptr;
+  Timed(xpipe_stage* s, int c, double w) : st(s), cls(c), work(w) {
+    if (st->timing) {
+      a = take_event(st);
+      if (a) (void)hipEventRecord(a, st->stream);
+    }
+  }
+  ~Timed() {
+    if (st->timing && a) {
+      hipEvent_t b = take_event(st);
+      if (b) {
+        (void)hipEventRecord(b, st->stream);
+        st->pending.push_back(TimeRec{a, b, cls, work});
+      } else {
+        st->pool.push_back(a);
+      }
+    }
+  }
+};
+
+const void* gemm_weights(xpipe_stage* st, const Op& op, int dir) {
+  if (st->dtype == DT_BF16) {
+    int64_t off = dir == XPIPE_FWD ? st->bf_f_off : st->bf_b_off;
+    return st->ws + off + (size_t)op.w_off * 2;
+  }
+  return (dir == XPIPE_FWD ? st->wpf : st->wpb) + op.w_off;
+}
+
+const float* fp32_param(xpipe_stage* st, int64_t off, int dir) {
+  return (dir == XPIPE_FWD ? st->wpf : st->wpb) + off;
+}
+
+double gemm_flops(const Tensor& tin, const Op& op) {
+  return 2.0 * (double)tin.sh.rows() * op.cout * (double)op.k * op.k * op.cin;
+}
+
+// ---------------------------------------------------------------- forward
+xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* labels,
+                         float* loss) {
+  hipStream_t s = st->stream;
+  const int dt = st->dtype;
+  for (const Op& op : st->ops) {
+    const Tensor& tin = st->tensors[op.in];
+    View x = act(st, op.in, c);
+    switch (op.kind) {
+      case OP_GEMM: {
+        View y = act(st, op.out, c);
+        ConvArgs a{};
+        a.x = x.p;
+        a.ldx = x.ld;
+        a.w = gemm_weights(st, op, dir);
+        a.y = y.p;
+        a.ldy = y.ld;
+        a.bias = op.b_off >= 0 ? fp32_param(st, op.b_off, dir) : nullptr;
+        a.nb = tin.sh.n;
+        a.H = tin.sh.H;
+        a.W = tin.sh.W;
+        a.C = op.cin;
+        a.N = op.cout;
+        a.R = a.S = op.k;
+        a.pad = op.k / 2;
+        a.relu = op.relu;
+        Timed tm(st, 0, gemm_flops(tin, op));
+        XP_HIP(launch_conv_gemm(dt, a, s));
+        break;
+      }
+      case OP_BN: {
+        double* stats = (double*)(st->ws + op.stat_off);
+        ColArgs ca{};
+        ca.mode = COL_STATS;
+        ca.a = x.p;
+        ca.lda = x.ld;
+        ca.M = (int)tin.sh.rows();
+        ca.C = tin.sh.C;
+        ca.partial = (double*)(st->ws + st->colpart_off);
+        ca.row_blocks = col_row_blocks(ca.M, ca.C);
+        ca.out0 = stats;
+        ca.out1 = stats + tin.sh.C;
+        ca.eps = BN_EPS;
+        {
+          Timed tm(st, 3, (double)tin.sh.elems() * st->esz());
+          XP_HIP(launch_colreduce(dt, ca, s));
+        }
+        View y = act(st, op.out, c);
+        BnApplyArgs b{};
+        b.z = x.p;
+        b.ldz = x.ld;
+        b.mean = stats;
+        b.rstd = stats + tin.sh.C;
+        b.gamma = fp32_param(st, op.g_off, dir);
+        b.beta = fp32_param(st, op.be_off, dir);
+        if (op.in2 >= 0) {
+          View r = act(st, op.in2, c);
+          b.res = r.p;
+          b.ldres = r.ld;
+        }
+        b.y = y.p;
+        b.ldy = y.ld;
+        b.M = ca.M;
+        b.C = ca.C;
+        b.relu = op.relu;
+        Timed tm(st, 3, (double)tin.sh.elems() * st->esz() * (op.in2 >= 0 ? 3 : 2));
+        XP_HIP(launch_bn_apply(dt, b, s));
+        break;
+      }
+      case OP_ELT: {
+        View y = act(st, op.out, c);
+        EltArgs e{};
+        e.a = x.p;
+        e.lda = x.ld;
+        if (op.in2 >= 0) {
+          View b = act(st, op.in2, c);
+          e.b = b.p;
+          e.ldb = b.ld;
+        }
+        e.y = y.p;
+        e.ldy = y.ld;
+        e.M = (int)tin.sh.rows();
+        e.C = tin.sh.C;
+        e.relu = op.relu;
+        Timed tm(st, 3, (double)tin.sh.elems() * st->esz() * (op.in2 >= 0 ? 3 : 2));
+        XP_HIP(launch_elementwise(dt, e, s));
+        break;
+      }
+      case OP_MAXPOOL:
+      case OP_AVGPOOL:
+      case OP_GAP: {
+        View y = act(st, op.out, c);
+        PoolArgs pa{};
+        pa.x = x.p;
+        pa.ldx = x.ld;
+        pa.out = y.p;
+        pa.ldo = y.ld;
+        pa.nb = tin.sh.n;
+        pa.H = tin.sh.H;
+        pa.W = tin.sh.W;
+        pa.C = tin.sh.C;
+        Timed tm(st, 3, (double)(tin.sh.elems() + st->tensors[op.out].sh.elems()) * st->esz());
+        if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_fwd(dt, pa, s));
+        else if (op.kind == OP_AVGPOOL) XP_HIP(launch_avgpool_fwd(dt, pa, s));
+        else XP_HIP(launch_gap_fwd(dt, pa, s));
+        break;
+      }
+      case OP_CONCAT:
+        break;
+      case OP_CE: {
+        if (!loss) break;  // the forward of a loss stage needs no more than the logits
+        CeArgs ce{};
+        ce.z = x.p;
+        ce.ldz = x.ld;
+        ce.labels = labels;
+        ce.n = tin.sh.n;
+        ce.classes = st->classes;
+        ce.inv_N = 1.0 / ((double)st->T * st->mb);
+        ce.loss = loss;
+        Timed tm(st, 3, (double)tin.sh.elems() * st->esz());
+        XP_HIP(launch_softmax_ce(dt, ce, s));
+        break;
+      }
+    }
+  }
+  return XPIPE_OK;
+}
+
+// ---------------------------------------------------------------- backward
+xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const int32_t* labels) {
+  hipStream_t s = st->stream;
+  const int dt = st->dtype;
+  const int dir = XPIPE_BWD;
+  const size_t esz = st->esz();
+  auto want_grad = [&](int t) { return t != 0 || c.dx != nullptr; };
+  auto mask_of = [&](int t, const void*& mp, int& ld) {
+    mp = nullptr;
+    ld = 0;
+    if (st->tensors[t].masked) {
+      View v = act(st, t, c);
+      mp = v.p;
+      ld = v.ld;
+    }
+  };
+
+  // seed: the gradient of the stage output
+  if (!st->has_loss) {
+    const Tensor& to = st->tensors[st->out_tensor];
+    View g = gradv(st, st->out_tensor, c);
+    EltArgs e{};
+    e.a = dy;
+    e.lda = to.sh.C;
+    mask_of(st->out_tensor, e.mask, e.ldm);
+    e.y = g.p;
+    e.ldy = g.ld;
+    e.M = (int)to.sh.rows();
+    e.C = to.sh.C;
+    Timed tm(st, 3, (double)to.sh.elems() * esz * 2);
+    XP_HIP(launch_elementwise(dt, e, s));
+  }
+
+  for (int i = (int)st->ops.size() - 1; i >= 0; --i) {
+    const Op& op = st->ops[i];
+    const Tensor& tin = st->tensors[op.in];
+    View x = act(st, op.in, c);
+    switch (op.kind) {
+      case OP_CE: {
+        View g = gradv(st, op.in, c);
+        CeArgs ce{};
+        ce.z = x.p;
+        ce.ldz = x.ld;
+        ce.labels = labels;
+        ce.n = tin.sh.n;
+        ce.classes = st->classes;
+        ce.inv_N = 1.0 / ((double)st->T * st->mb);
+        ce.dz = g.p;
+        ce.lddz = g.ld;
+        Timed tm(st, 3, (double)tin.sh.elems() * esz * 2);
+        XP_HIP(launch_softmax_ce(dt, ce, s));
+        break;
+      }
+      case OP_GEMM: {
+        View g = gradv(st, op.out, c);
+        const int M = (int)tin.sh.rows();
+        const int K = op.k * op.k * op.cin;
+        // weight gradient, accumulated into grad
+        WgradArgs w{};
+        w.dz = g.p;
+        w.lddz = g.ld;
+        w.x = x.p;
+        w.ldx = x.ld;
+        w.part = st->ws + st->wpart_off;
+        w.grad = st->grad + op.w_off;
+        w.nb = tin.sh.n;
+        w.H = tin.sh.H;
+        w.W = tin.sh.W;
+        w.C = op.cin;
+        w.N = op.cout;
+        w.R = w.S = op.k;
+        w.pad = op.k / 2;
+        w.splits = wgrad_pick_splits(M, op.cout, K);
+        {
+          Timed tm(st, 1, gemm_flops(tin, op));
+          XP_HIP(launch_wgrad(dt, w, s));
+        }
+        if (op.b_off >= 0) {
+          ColArgs ca{};
+          ca.mode = COL_BIAS;
+          ca.a = g.p;
+          ca.lda = g.ld;
+          ca.M = M;
+          ca.C = op.cout;
+          ca.partial = (double*)(st->ws + st->colpart_off);
+          ca.row_blocks = col_row_blocks(M, op.cout);
+          ca.grad0 = st->grad + op.b_off;
+          Timed tm(st, 3, (double)M * op.cout * esz);
+          XP_HIP(launch_colreduce(dt, ca, s));
+        }
+        if (want_grad(op.in)) {
+          View dx = gradv(st, op.in, c);
+          ConvArgs a{};
+          a.x = g.p;
+          a.ldx = g.ld;
+          a.w = st->ws + op.wd_off;
+          a.y = dx.p;
+          a.ldy = dx.ld;
+          mask_of(op.in, a.mask, a.ldm);
+          a.nb = tin.sh.n;
+          a.H = tin.sh.H;
+          a.W = tin.sh.W;
+          a.C = op.cout;
+          a.N = op.cin;
+          a.R = a.S = op.k;
+          a.pad = op.k / 2;
+          a.accumulate = op.in_acc;
+          Timed tm(st, 0, gemm_flops(tin, op));
+          XP_HIP(launch_conv_gemm(dt, a, s));
+        }
+        break;
+      }
+      case OP_BN: {
+        View g = gradv(st, op.out, c);
+        double* stats = (double*)(st->ws + op.stat_off);
+        const int M = (int)tin.sh.rows(), C = tin.sh.C;
+        ColArgs ca{};
+        ca.mode = COL_BNBWD;
+        ca.a = g.p;
+        ca.lda = g.ld;
+        ca.z = x.p;
+        ca.ldz = x.ld;
+        ca.mean = stats;
+        ca.rstd = stats + C;
+        ca.M = M;
+        ca.C = C;
+        ca.partial = (double*)(st->ws + st->colpart_off);
+        ca.row_blocks = col_row_blocks(M, C);
+        ca.out0 = stats + 2 * C;
+        ca.out1 = stats + 3 * C;
+        ca.grad0 = st->grad + op.g_off;
+        ca.grad1 = st->grad + op.be_off;
+        {
+          Timed tm(st, 3, (double)tin.sh.elems() * esz * 2);
+          XP_HIP(launch_colreduce(dt, ca, s));
+        }
+        BnBwdArgs b{};
+        b.g = g.p;
+        b.ldg = g.ld;
+        b.z = x.p;
+        b.ldz = x.ld;
+        b.mean = stats;
+        b.rstd = stats + C;
+        b.dbeta = stats + 2 * C;
+        b.dgamma = stats + 3 * C;
+        b.gamma = fp32_param(st, op.g_off, dir);
+        bool need_dz = want_grad(op.in);
+        View dz = gradv(st, op.in, c);
+        b.dz = need_dz ? dz.p : nullptr;
+        b.lddz = dz.ld;
+        mask_of(op.in, b.dzmask, b.ldzm);
+        b.dz_accumulate = op.in_acc;
+        if (op.in2 >= 0 && want_grad(op.in2)) {
+          View dr = gradv(st, op.in2, c);
+          b.dres = dr.p;
+          b.lddres = dr.ld;
+          mask_of(op.in2, b.resmask, b.ldrm);
+          b.res_accumulate = op.in2_acc;
+        }
+        b.M = M;
+        b.C = C;
+        if (!need_dz) {
+          // no BN-input gradient wanted (stage input without dx): only the
+          // residual part, as a masked copy
+          if (b.dres) {
+            EltArgs e{};
+            e.a = g.p;
+            e.lda = g.ld;
+            e.mask = b.resmask;
+            e.ldm = b.ldrm;
+            e.y = b.dres;
+            e.ldy = b.lddres;
+            e.M = M;
+            e.C = C;
+            e.accumulate = b.res_accumulate;
+            Timed tm(st, 3, (double)tin.sh.elems() * esz * 3);
+            XP_HIP(launch_elementwise(dt, e, s));
+          }
+          break;
+        }
+        Timed tm(st, 3, (double)tin.sh.elems() * esz * (b.dres ? 5 : 3));
+        XP_HIP(launch_bn_bwd(dt, b, s));
+        break;
+      }
+      case OP_ELT: {
+        View g = gradv(st, op.out, c);
+        int ins[2] = {op.in, op.in2};
+        bool accs[2] = {op.in_acc, op.in2_acc};
+        for (int q = 0; q < 2; ++q) {
+          if (ins[q] < 0 || !want_grad(ins[q])) continue;
+          View d = gradv(st, ins[q], c);
+          EltArgs e{};
+          e.a = g.p;
+          e.lda = g.ld;
+          mask_of(ins[q], e.mask, e.ldm);
+          e.y = d.p;
+          e.ldy = d.ld;
+          e.M = (int)tin.sh.rows();
+          e.C = tin.sh.C;
+          e.accumulate = accs[q];
+          Timed tm(st, 3, (double)tin.sh.elems() * esz * 3);
+          XP_HIP(launch_elementwise(dt, e, s));
+        }
+        break;
+      }
+      case OP_MAXPOOL:
+      case OP_AVGPOOL:
+      case OP_GAP: {
+        if (!want_grad(op.in)) break;
+        View g = gradv(st, op.out, c);
+        View d = gradv(st, op.in, c);
+        PoolArgs pa{};
+        pa.x = x.p;
+        pa.ldx = x.ld;
+        pa.dy = g.p;
+        pa.lddy = g.ld;
+        pa.out = d.p;
+        pa.ldo = d.ld;
+        mask_of(op.in, pa.mask, pa.ldm);
+        pa.accumulate = op.in_acc;
+        pa.nb = tin.sh.n;
+        pa.H = tin.sh.H;
+        pa.W = tin.sh.W;
+        pa.C = tin.sh.C;
+        Timed tm(st, 3, (double)tin.sh.elems() * esz * 3);
+        if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_bwd(dt, pa, s));
+        else if (op.kind == OP_AVGPOOL) XP_HIP(launch_avgpool_bwd(dt, pa, s));
+        else XP_HIP(launch_gap_bwd(dt, pa, s));
+        break;
+      }
+      case OP_CONCAT:
+        break;
+    }
+  }
+  return XPIPE_OK;
+}
+
+// ---------------------------------------------------------------- coefficients
+xpipe_status check_hp(const xpipe_hparams* hp) {
+  if (!hp) return fail(XPIPE_EINVAL, "null hparams");
+  if (!(hp->lr >= 0) || !(hp->beta1 >= 0 && hp->beta1 < 1) || !(hp->beta2 >= 0 && hp->beta2 < 1) ||
+      !(hp->eps > 0) || hp->t < 0 || hp->mode < 0 || hp->mode > 2)
+    return fail(XPIPE_EINVAL, "bad hparams");
+  return XPIPE_OK;
+}
+
+PredCoef pred_coef(const xpipe_hparams* hp, int64_t t, int s) {
+  PredCoef c{};
+  c.eps = hp->eps;
+  c.eps_outside = hp->mode == XPIPE_PRED_ADAMDIR;
+  bool identity = s == 0 || (t == 0 && hp->mode != XPIPE_PRED_LITERAL);
+  if (identity) return c;  // coef = c1 = c2 = 0: W - 0 * 0 = W
+  c.coef = (double)s * hp->lr;
+  if (hp->mode == XPIPE_PRED_LITERAL) {
+    c.c1 = 1.0 / (1.0 - hp->beta1);
+    c.c2 = 1.0 / (1.0 - hp->beta2);
+  } else {
+    c.c1 = 1.0 / (1.0 - std::pow(hp->beta1, (double)t));
+    c.c2 = 1.0 / (1.0 - std::pow(hp->beta2, (double)t));
+  }
+  return c;
+}
+
+AdamCoef adam_coef(const xpipe_hparams* hp) {
+  AdamCoef a{};
+  double t = (double)(hp->t + 1);
+  a.lr = hp->lr;
+  a.beta1 = hp->beta1;
+  a.beta2 = hp->beta2;
+  a.one_m_beta1 = 1.0 - hp->beta1;
+  a.one_m_beta2 = 1.0 - hp->beta2;
+  a.bc1 = 1.0 / (1.0 - std::pow(hp->beta1, t));
+  a.bc2 = 1.0 / (1.0 - std::pow(hp->beta2, t));
+  a.eps = hp->eps;
+  return a;
+}
+
+xpipe_status refresh_flipped(xpipe_stage* st) {
+  for (const Op& op : st->ops) {
+    if (op.kind != OP_GEMM) continue;
+    Timed tm(st, 3, (double)op.cout * op.k * op.k * op.cin * st->esz() * 2);
+    XP_HIP(launch_flip_weights(st->dtype, gemm_weights(st, op, XPIPE_BWD), st->ws + op.wd_off,
+                               op.cout, op.k, op.k, op.cin, st->stream));
+  }
+  st->wd_valid = true;
+  return XPIPE_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+}  // namespace
+
+// ============================================================================
+// C ABI
+// ============================================================================
+extern "C" {
+
+const char* xpipe_last_error(void) { return g_err.c_str(); }
+
+static int round_rule(double x, int rule) {
+  double lo = std::floor(x);
+  double frac = x - lo;
+  if (frac > 0.5) return (int)lo + 1;
+  if (frac < 0.5) return (int)lo;
+  if (rule == XPIPE_ROUND_HALF_UP) return (int)lo + 1;
+  if (rule == XPIPE_ROUND_HALF_DOWN) return (int)lo;
+  return ((int64_t)lo % 2 == 0) ? (int)lo : (int)lo + 1;
+}
+
+xpipe_status xpipe_version_difference(int32_t size, int32_t T, int32_t rank, int32_t dir,
+                                      int32_t rounding, int32_t ceil_half_rank, int32_t* s_out) {
+  if (!s_out) return fail(XPIPE_EINVAL, "null output");
+  if (size < 1 || T < 1 || rank < 0 || rank >= size) return fail(XPIPE_EINVAL, "need size >= 1, T >= 1, 0 <= rank < size");
+  if (dir != XPIPE_FWD && dir != XPIPE_BWD) return fail(XPIPE_EINVAL, "bad direction");
+  if (rounding < 0 || rounding > 2) return fail(XPIPE_EINVAL, "bad rounding rule");
+  double x;
+  if (dir == XPIPE_FWD) {
+    double half = ceil_half_rank ? (double)((rank + 1) / 2) : rank / 2.0;
+    x = ((double)size + T - half - 2.0) / T;
+  } else {
+    x = ((double)T + rank / 2 - 1.0) / T;
+  }
+  *s_out = round_rule(x, rounding);
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_query(const xpipe_layer_desc* layers, int32_t n_layers, int32_t micro_batch,
+                               int32_t H, int32_t W, int32_t C, int32_t dtype,
+                               int64_t* n_params_padded, size_t* workspace_bytes) {
+  if (!n_params_padded || !workspace_bytes) return fail(XPIPE_EINVAL, "null output");
+  Plan p;
+  xpipe_status s = build_plan(layers, n_layers, micro_batch, H, W, C, dtype, p);
+  if (s != XPIPE_OK) return s;
+  *n_params_padded = p.P;
+  *workspace_bytes = p.ws;
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_create(const xpipe_layer_desc* layers, int32_t n_layers, int32_t micro_batch,
+                                int32_t T, int32_t H, int32_t W, int32_t C, int32_t dtype,
+                                void* hip_stream, float* W_, float* m, float* v, float* grad,
+                                float* w_pred_fwd, float* w_pred_bwd, void* workspace,
+                                size_t workspace_bytes, xpipe_stage_t* out) {
+  if (!out) return fail(XPIPE_EINVAL, "null output handle");
+  *out = nullptr;
+  if (T < 1) return fail(XPIPE_EINVAL, "T must be >= 1");
+  Plan p;
+  xpipe_status s = build_plan(layers, n_layers, micro_batch, H, W, C, dtype, p);
+  if (s != XPIPE_OK) return s;
+  if (p.P > 0 && (!W_ || !m || !v || !grad || !w_pred_fwd || !w_pred_bwd))
+    return fail(XPIPE_EINVAL, "null device buffer");
+  if (!workspace) return fail(XPIPE_EINVAL, "null workspace");
+  if (workspace_bytes < p.ws) return fail(XPIPE_EINVAL, "workspace too small");
+  if ((reinterpret_cast<uintptr_t>(workspace) % WS_ALIGN) != 0)
+    return fail(XPIPE_EINVAL, "workspace must be 256-byte aligned");
+  if (!aligned16(W_) || !aligned16(m) || !aligned16(v) || !aligned16(grad) ||
+      !aligned16(w_pred_fwd) || !aligned16(w_pred_bwd))
+    return fail(XPIPE_EINVAL, "parameter buffers must be 16-byte aligned");
+  xpipe_stage* st = new (std::nothrow) xpipe_stage();
+  if (!st) return fail(XPIPE_EINVAL, "out of host memory");
+  st->layers.assign(layers, layers + n_layers);
+  st->mb = micro_batch;
+  st->T = T;
+  st->dtype = dtype;
+  st->in_shape = Shape{micro_batch, H, W, C};
+  st->stream = (hipStream_t)hip_stream;
+  st->W = W_;
+  st->m = m;
+  st->v = v;
+  st->grad = grad;
+  st->wpf = w_pred_fwd;
+  st->wpb = w_pred_bwd;
+  st->ws = (char*)workspace;
+  st->ws_bytes = workspace_bytes;
+  st->P = p.P;
+  st->params = p.params;
+  st->tensors = p.tensors;
+  st->ops = p.ops;
+  st->out_tensor = p.out_tensor;
+  st->has_loss = p.has_loss;
+  st->classes = p.classes;
+  st->bf_f_off = p.bf_f_off;
+  st->bf_b_off = p.bf_b_off;
+  st->colpart_off = p.colpart_off;
+  st->wpart_off = p.wpart_off;
+  hipError_t e = p.P > 0 ? hipMemsetAsync(grad, 0, (size_t)p.P * sizeof(float), st->stream)
+                         : hipSuccess;
+  if (e != hipSuccess) {
+    delete st;
+    return fail(XPIPE_EHIP, std::string("hipMemsetAsync: ") + hipGetErrorString(e));
+  }
+  *out = st;
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_num_param_tensors(xpipe_stage_t st, int32_t* n) {
+  if (!st || !n) return fail(XPIPE_EINVAL, "null argument");
+  *n = (int32_t)st->params.size();
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_param_layout(xpipe_stage_t st, int32_t idx, int64_t* offset, int64_t* count) {
+  if (!st || !offset || !count) return fail(XPIPE_EINVAL, "null argument");
+  if (idx < 0 || idx >= (int32_t)st->params.size()) return fail(XPIPE_EINVAL, "tensor index out of range");
+  *offset = st->params[idx].off;
+  *count = st->params[idx].count;
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_output_shape(xpipe_stage_t st, int32_t* n, int32_t* H, int32_t* W, int32_t* C) {
+  if (!st || !n || !H || !W || !C) return fail(XPIPE_EINVAL, "null argument");
+  const Shape& s = st->tensors[st->out_tensor].sh;
+  *n = s.n;
+  *H = s.H;
+  *W = s.W;
+  *C = s.C;
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_predict_weights(xpipe_stage_t st, int32_t which, int32_t s, const xpipe_hparams* hp) {
+  if (!st) return fail(XPIPE_EINVAL, "null stage");
+  if (which != XPIPE_FWD && which != XPIPE_BWD) return fail(XPIPE_EINVAL, "bad direction");
+  if (s < 0) return fail(XPIPE_EINVAL, "version difference must be >= 0");
+  xpipe_status hs = check_hp(hp);
+  if (hs != XPIPE_OK) return hs;
+  PredCoef c = pred_coef(hp, hp->t, s);
+  float* out = which == XPIPE_FWD ? st->wpf : st->wpb;
+  bf16_t* obf = nullptr;
+  if (st->dtype == DT_BF16) obf = (bf16_t*)(st->ws + (which == XPIPE_FWD ? st->bf_f_off : st->bf_b_off));
+  {
+    Timed tm(st, 2, (double)st->P * (obf ? 18 : 16));
+    XP_HIP(launch_predict(st->W, st->m, st->v, out, obf, st->P, c, st->stream));
+  }
+  st->pred_valid[which] = true;
+  if (which == XPIPE_BWD) {
+    xpipe_status r = refresh_flipped(st);
+    if (r != XPIPE_OK) return r;
+  }
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_fwd(xpipe_stage_t st, const void* x, void* y, const int32_t* labels, float* loss) {
+  if (!st) return fail(XPIPE_EINVAL, "null stage");
+  if (!x || !y) return fail(XPIPE_EINVAL, "null input or output");
+  if (st->has_loss && loss && !labels) return fail(XPIPE_EINVAL, "labels required for the loss");
+  if (!st->pred_valid[XPIPE_FWD]) return fail(XPIPE_ESTATE, "no forward prediction: call xpipe_predict_weights(FWD) first");
+  Ctx c;
+  c.x = x;
+  c.y = y;
+  return run_forward(st, XPIPE_FWD, c, labels, st->has_loss ? loss : nullptr);
+}
+
+xpipe_status xpipe_stage_bwd(xpipe_stage_t st, const void* x, const void* dy, const int32_t* labels, void* dx) {
+  if (!st) return fail(XPIPE_EINVAL, "null stage");
+  if (!x) return fail(XPIPE_EINVAL, "null input");
+  if (st->has_loss && !labels) return fail(XPIPE_EINVAL, "labels required for a loss stage");
+  if (!st->has_loss && !dy) return fail(XPIPE_EINVAL, "dy required for a stage without a loss");
+  if (!st->pred_valid[XPIPE_BWD] || !st->wd_valid)
+    return fail(XPIPE_ESTATE, "no backward prediction: call xpipe_predict_weights(BWD) first");
+  Ctx c;
+  c.x = x;
+  c.dx = dx;
+  xpipe_status s = run_forward(st, XPIPE_BWD, c, nullptr, nullptr);
+  if (s != XPIPE_OK) return s;
+  s = run_backward(st, c, dy, labels);
+  if (s != XPIPE_OK) return s;
+  st->bwd_since_step++;
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t s_fwd_next,
+                             int32_t s_bwd_next, int32_t emit_pred) {
+  if (!st) return fail(XPIPE_EINVAL, "null stage");
+  xpipe_status hs = check_hp(hp);
+  if (hs != XPIPE_OK) return hs;
+  if (emit_pred && (s_fwd_next < 0 || s_bwd_next < 0)) return fail(XPIPE_EINVAL, "version difference must be >= 0");
+  if (st->bwd_since_step == 0) return fail(XPIPE_ESTATE, "no backward since the last update");
+  AdamCoef a = adam_coef(hp);
+  PredCoef cf = pred_coef(hp, hp->t + 1, s_fwd_next);
+  PredCoef cb = pred_coef(hp, hp->t + 1, s_bwd_next);
+  bf16_t* ff = nullptr;
+  bf16_t* fb = nullptr;
+  if (emit_pred && st->dtype == DT_BF16) {
+    ff = (bf16_t*)(st->ws + st->bf_f_off);
+    fb = (bf16_t*)(st->ws + st->bf_b_off);
+  }
+  {
+    Timed tm(st, 2, (double)st->P * (emit_pred ? (ff ? 44 : 40) : 32));
+    XP_HIP(launch_adam(st->W, st->m, st->v, st->grad, st->P, a, 1, emit_pred ? st->wpf : nullptr, ff, cf,
+                       emit_pred ? st->wpb : nullptr, fb, cb, st->stream));
+  }
+  st->bwd_since_step = 0;
+  st->pred_valid[0] = st->pred_valid[1] = emit_pred != 0;
+  st->wd_valid = false;
+  if (emit_pred) return refresh_flipped(st);
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_destroy(xpipe_stage_t st) {
+  if (!st) return fail(XPIPE_EINVAL, "null stage");
+  for (auto& r : st->pending) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (auto e : st->pool) (void)hipEventDestroy(e);
+  delete st;
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_predict_flat(const float* W, const float* m, const float* v, float* out, uint16_t* out_bf16,
+                                int64_t n, int32_t s, const xpipe_hparams* hp, void* hip_stream) {
+  if (n < 0) return fail(XPIPE_EINVAL, "negative length");
+  if (s < 0) return fail(XPIPE_EINVAL, "version difference must be >= 0");
+  xpipe_status hs = check_hp(hp);
+  if (hs != XPIPE_OK) return hs;
+  if (n == 0) return XPIPE_OK;
+  if (!W || !m || !v || !out) return fail(XPIPE_EINVAL, "null buffer");
+  if (!aligned16(W) || !aligned16(m) || !aligned16(v) || !aligned16(out) ||
+      (out_bf16 && (reinterpret_cast<uintptr_t>(out_bf16) & 7) != 0))
+    return fail(XPIPE_EINVAL, "buffers must be 16-byte aligned (bf16 output 8-byte)");
+  XP_HIP(launch_predict(W, m, v, out, out_bf16, n, pred_coef(hp, hp->t, s), (hipStream_t)hip_stream));
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_adam_flat(float* W, float* m, float* v, float* G, int64_t n, const xpipe_hparams* hp,
+                             int32_t zero_grad, float* pred_fwd, int32_t s_fwd, float* pred_bwd, int32_t s_bwd,
+                             void* hip_stream) {
+  if (n < 0) return fail(XPIPE_EINVAL, "negative length");
+  xpipe_status hs = check_hp(hp);
+  if (hs != XPIPE_OK) return hs;
+  if ((pred_fwd && s_fwd < 0) || (pred_bwd && s_bwd < 0)) return fail(XPIPE_EINVAL, "version difference must be >= 0");
+  if (n == 0) return XPIPE_OK;
+  if (!W || !m || !v || !G) return fail(XPIPE_EINVAL, "null buffer");
+  if (!aligned16(W) || !aligned16(m) || !aligned16(v) || !aligned16(G) ||
+      (pred_fwd && !aligned16(pred_fwd)) || (pred_bwd && !aligned16(pred_bwd)))
+    return fail(XPIPE_EINVAL, "buffers must be 16-byte aligned");
+  XP_HIP(launch_adam(W, m, v, G, n, adam_coef(hp), zero_grad, pred_fwd, nullptr, pred_coef(hp, hp->t + 1, s_fwd),
+                     pred_bwd, nullptr, pred_coef(hp, hp->t + 1, s_bwd), (hipStream_t)hip_stream));
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_set_timing(xpipe_stage_t st, int32_t enable) {
+  if (!st) return fail(XPIPE_EINVAL, "null stage");
+  st->timing = enable != 0;
+  for (int i = 0; i < 4; ++i) {
+    st->t_ms[i] = 0;
+    st->t_work[i] = 0;
+    st->t_n[i] = 0;
+  }
+  for (auto& r : st->pending) {
+    st->pool.push_back(r.a);
+    st->pool.push_back(r.b);
+  }
+  st->pending.clear();
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_timing(xpipe_stage_t st, int32_t cls, double* ms, int64_t* launches, double* work) {
+  if (!st || !ms || !launches || !work) return fail(XPIPE_EINVAL, "null argument");
+  if (cls < 0 || cls > 3) return fail(XPIPE_EINVAL, "bad kernel class");
+  for (auto& r : st->pending) {
+    float e = 0.f;
+    hipError_t err = hipEventSynchronize(r.b);
+    if (err != hipSuccess) return fail(XPIPE_EHIP, std::string("hipEventSynchronize: ") + hipGetErrorString(err));
+    err = hipEventElapsedTime(&e, r.a, r.b);
+    if (err != hipSuccess) return fail(XPIPE_EHIP, std::string("hipEventElapsedTime: ") + hipGetErrorString(err));
+    st->t_ms[r.cls] += e;
+    st->t_work[r.cls] += r.work;
+    st->t_n[r.cls] += 1;
+    st->pool.push_back(r.a);
+    st->pool.push_back(r.b);
+  }
+  st->pending.clear();
+  *ms = st->t_ms[cls];
+  *launches = st->t_n[cls];
+  *work = st->t_work[cls];
+  return XPIPE_OK;
+}
+
+}  // extern "C"

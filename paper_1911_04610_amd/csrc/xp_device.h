@@ -1,0 +1,53 @@
+// Device-side helpers shared by the libxpipe HIP kernels (gfx950 / CDNA4).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define XP_DEV __device__ __forceinline__
+
+typedef uint16_t bf16_t;  // bf16 bit pattern
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- bf16
+XP_DEV float bf16_to_f32(bf16_t u) { return __uint_as_float((uint32_t)u << 16); }
+
+// fp32 -> bf16, round to nearest, ties to even; NaN stays a quiet NaN.
+XP_DEV bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+// ---------------------------------------------------------------- storage traits
+// Activations are stored as float (XPIPE_F32) or bf16 (XPIPE_BF16); element-
+// wise and reduction arithmetic is done in double and rounded once on store.
+template <typename T> struct Store;
+template <> struct Store<float> {
+  static XP_DEV double ld(const float* p) { return (double)*p; }
+  static XP_DEV void st(float* p, double v) { *p = (float)v; }
+};
+template <> struct Store<bf16_t> {
+  static XP_DEV double ld(const bf16_t* p) { return (double)bf16_to_f32(*p); }
+  // double -> fp32 (nearest) -> bf16 (nearest even), the storage model of the
+  // bf16 variant
+  static XP_DEV void st(bf16_t* p, double v) { *p = f32_to_bf16((float)v); }
+};
+
+template <typename T> XP_DEV double ldd(const T* p) { return Store<T>::ld(p); }
+template <typename T> XP_DEV void std_(T* p, double v) { Store<T>::st(p, v); }
+
+// ---------------------------------------------------------------- reductions
+XP_DEV double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+XP_DEV double wave_max(double v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
+  return v;
+}

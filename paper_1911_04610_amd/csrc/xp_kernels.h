@@ -1,0 +1,165 @@
+// Host-side interface of the libxpipe kernels: argument blocks and launchers.
+// Activation tensors are NHWC views: element (row m, channel c) of a view is
+// at ptr[m * ld + c], with m = (n * H + h) * W + w and ptr already offset to
+// the view's first channel.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace xp {
+
+typedef uint16_t bf16_t;
+
+enum Dtype { DT_F32 = 0, DT_BF16 = 1 };
+
+// ---------------------------------------------------------------- prediction / Adam
+struct PredCoef {
+  double coef;      // s * lr (0 for the identity)
+  double c1, c2;    // first / second moment scale (bias correction), 0 for the identity
+  double eps;
+  int eps_outside;  // Adam's direction: eps added after the root
+};
+
+struct AdamCoef {
+  double lr, beta1, beta2, one_m_beta1, one_m_beta2;
+  double bc1, bc2;  // 1 / (1 - beta^t) for this update
+  double eps;
+};
+
+hipError_t launch_predict(const float* W, const float* m, const float* v, float* out,
+                          bf16_t* out_bf, int64_t n, const PredCoef& c, hipStream_t s);
+hipError_t launch_adam(float* W, float* m, float* v, float* G, int64_t n, const AdamCoef& a,
+                       int zero_grad, float* pf, bf16_t* pf_bf, const PredCoef& cf, float* pb,
+                       bf16_t* pb_bf, const PredCoef& cb, hipStream_t s);
+
+// ---------------------------------------------------------------- GEMM engine
+// Forward-type implicit GEMM: y[m][n] = act(sum_{r,s,c} x[pix(m) + (r-pad, s-pad)][c] *
+// w[n][r][s][c] + bias[n]) over an nb x H x W image batch (stride 1, zero padding).
+// Serves conv forward, linear forward (H = W = R = S = 1) and the data gradient
+// (x = output gradient, w = flipped / transposed weights).
+struct ConvArgs {
+  const void* x;
+  int ldx;
+  const void* w;        // [N][R][S][C] contiguous, storage dtype
+  void* y;
+  int ldy;
+  const float* bias;    // [N] or null
+  const void* mask;     // optional view: y *= (mask > 0)
+  int ldm;
+  int nb, H, W, C, N, R, S, pad;
+  int relu;             // apply max(., 0) before storing
+  int accumulate;       // y = y + result (after mask)
+};
+
+// Weight gradient: part[split][n][k] = sum_{m in split} dz[m][n] * x~[m][k],
+// k = (r, s, c); then grad[n][k] += sum over splits (fixed order).
+struct WgradArgs {
+  const void* dz;
+  int lddz;
+  const void* x;
+  int ldx;
+  void* part;           // workspace: splits x N x K partial sums (fp32 or fp64)
+  float* grad;          // [N][K] fp32 accumulator
+  int nb, H, W, C, N, R, S, pad;
+  int splits;
+};
+
+// Work plan of one GEMM launch (tile shape picked on the host).
+hipError_t launch_conv_gemm(int dtype, const ConvArgs& a, hipStream_t s);
+size_t wgrad_part_bytes(int dtype, int N, int K, int splits);
+int wgrad_pick_splits(int M, int N, int K);
+hipError_t launch_wgrad(int dtype, const WgradArgs& a, hipStream_t s);
+
+// Flipped, transposed copy for the data gradient: wd[c][r][s][n] = w[n][R-1-r][S-1-s][c].
+hipError_t launch_flip_weights(int dtype, const void* w, void* wd, int N, int R, int S, int C,
+                               hipStream_t s);
+
+// ---------------------------------------------------------------- column reductions
+// Per-column sums over the rows of [M][C] views, two-level and fixed-order.
+enum ColMode { COL_STATS = 0, COL_BNBWD = 1, COL_BIAS = 2 };
+struct ColArgs {
+  int mode;
+  const void* a;        // STATS: z; BNBWD: g; BIAS: g
+  int lda;
+  const void* z;        // BNBWD: BN input
+  int ldz;
+  const double* mean;   // BNBWD
+  const double* rstd;   // BNBWD
+  int M, C;
+  double* partial;      // workspace [row blocks][2][C]
+  int row_blocks;
+  // finalize outputs
+  double* out0;         // STATS: mean; BNBWD: dbeta
+  double* out1;         // STATS: rstd; BNBWD: dgamma
+  float* grad0;         // BNBWD: grad of gamma; BIAS: grad of bias (accumulated)
+  float* grad1;         // BNBWD: grad of beta
+  double eps;
+};
+int col_row_blocks(int M, int C);
+size_t col_partial_bytes(int M, int C);
+hipError_t launch_colreduce(int dtype, const ColArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- element-wise
+struct BnApplyArgs {
+  const void* z; int ldz;
+  const double* mean; const double* rstd;
+  const float* gamma; const float* beta;
+  const void* res; int ldres;     // optional residual (added before the ReLU)
+  void* y; int ldy;
+  int M, C, relu;
+};
+hipError_t launch_bn_apply(int dtype, const BnApplyArgs& a, hipStream_t s);
+
+struct BnBwdArgs {
+  const void* g; int ldg;          // gradient at the BN(+add) output, masked
+  const void* z; int ldz;
+  const double* mean; const double* rstd;
+  const double* dbeta; const double* dgamma;
+  const float* gamma;
+  void* dz; int lddz;              // BN-input gradient
+  const void* dzmask; int ldzm;    // optional mask for dz
+  int dz_accumulate;
+  void* dres; int lddres;          // optional residual-source gradient
+  const void* resmask; int ldrm;   // optional mask for dres
+  int res_accumulate;
+  int M, C;
+};
+hipError_t launch_bn_bwd(int dtype, const BnBwdArgs& a, hipStream_t s);
+
+// y = relu?(a [+ b]), or mask mode: y = a * (m > 0)
+struct EltArgs {
+  const void* a; int lda;
+  const void* b; int ldb;          // optional second operand (add)
+  const void* mask; int ldm;       // optional mask
+  void* y; int ldy;
+  int M, C, relu, accumulate;
+};
+hipError_t launch_elementwise(int dtype, const EltArgs& a, hipStream_t s);
+
+struct PoolArgs {
+  const void* x; int ldx;          // pool input view
+  const void* y; int ldy;          // pool output view (forward result)
+  const void* dy; int lddy;        // backward: output gradient
+  void* out; int ldo;              // forward: y; backward: dx
+  const void* mask; int ldm;       // backward: mask for dx
+  int accumulate;
+  int nb, H, W, C;                 // input shape
+};
+hipError_t launch_maxpool_fwd(int dtype, const PoolArgs& a, hipStream_t s);
+hipError_t launch_maxpool_bwd(int dtype, const PoolArgs& a, hipStream_t s);
+hipError_t launch_avgpool_fwd(int dtype, const PoolArgs& a, hipStream_t s);
+hipError_t launch_avgpool_bwd(int dtype, const PoolArgs& a, hipStream_t s);
+hipError_t launch_gap_fwd(int dtype, const PoolArgs& a, hipStream_t s);
+hipError_t launch_gap_bwd(int dtype, const PoolArgs& a, hipStream_t s);
+
+struct CeArgs {
+  const void* z; int ldz;          // logits [n][classes]
+  const int32_t* labels;
+  int n, classes;
+  double inv_N;                    // 1 / mini-batch size
+  float* loss;                     // forward: loss share (may be null)
+  void* dz; int lddz;              // backward: dlogits (may be null)
+};
+hipError_t launch_softmax_ce(int dtype, const CeArgs& a, hipStream_t s);
+
+}  // namespace xp

@@ -1,0 +1,127 @@
+"""Host-side checks of the C ABI: the library loads, exports every declared
+entry point, and its host-only calls (version difference, layer-list
+validation, argument checks) behave as documented.  No GPU needed: none of
+these calls touches the device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_1911_04610_amd as xp
+import workloads as wl
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "xpipe.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(xpipe_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = xp.lib()
+    names = _declared()
+    assert "xpipe_stage_create" in names and "xpipe_adam_step" in names
+    for n in names:
+        assert hasattr(L, n), n
+
+
+RULES = {xp.ROUND_HALF_UP: oracle.HALF_UP, xp.ROUND_HALF_EVEN: oracle.HALF_EVEN,
+         xp.ROUND_HALF_DOWN: oracle.HALF_DOWN}
+
+
+@pytest.mark.parametrize("rounding", list(RULES))
+def test_version_difference_matches_oracle(rounding):
+    for size in (1, 2, 3, 4, 8, 16):
+        for T in (1, 2, 3, 4, 8):
+            for rank in range(size):
+                for ceil in (False, True):
+                    got = xp.xpipe_version_difference(size, T, rank, xp.FWD, rounding, ceil)
+                    want = oracle.version_difference_fwd(size, T, rank, RULES[rounding], ceil)
+                    assert got == want, (size, T, rank, ceil)
+                got = xp.xpipe_version_difference(size, T, rank, xp.BWD, rounding)
+                assert got == oracle.version_difference_bwd(size, T, rank, RULES[rounding])
+
+
+def test_version_difference_rejects_bad_arguments():
+    for args in [(0, 1, 0), (4, 0, 0), (4, 1, 4), (4, 1, -1)]:
+        with pytest.raises(xp.XPipeError) as e:
+            xp.xpipe_version_difference(*args, xp.FWD)
+        assert e.value.status == xp.EINVAL
+
+
+def test_workload_version_differences():
+    """The s values the stage workloads use are Eq. 1 / Eq. 2 at their rank."""
+    for name in ("vgg16_stage0", "resnet101_mid_stage", "inception_v3_stage"):
+        w = wl.WORKLOADS[name]()
+        assert xp.xpipe_version_difference(w.size, w.T, w.rank, xp.FWD) == w.s_fwd
+        assert xp.xpipe_version_difference(w.size, w.T, w.rank, xp.BWD) == w.s_bwd
+
+
+@pytest.mark.parametrize("name", list(wl.WORKLOADS))
+@pytest.mark.parametrize("dtype", [xp.F32, xp.BF16])
+def test_stage_query_param_count(name, dtype):
+    w = wl.WORKLOADS[name]()
+    P, ws = xp.xpipe_stage_query(w.layers, w.micro_batch, w.in_shape, dtype)
+    shapes = wl.param_shapes(w.layers)
+    assert P == sum((int(np.prod(s)) + 63) // 64 * 64 for s in shapes)
+    assert ws > 0 and ws % 256 == 0
+
+
+def _bad(layers, shape=(8, 8, 4), mb=2):
+    with pytest.raises(xp.XPipeError) as e:
+        xp.xpipe_stage_query(layers, mb, shape, xp.F32)
+    return e.value.status
+
+
+def test_stage_query_rejects_bad_layer_lists():
+    conv = dict(kind="conv", inputs=[-1], cin=4, cout=8, k=3, bias=False)
+    assert _bad([]) == xp.EINVAL
+    assert _bad([dict(conv, cin=5)]) == xp.EINVAL                       # channel mismatch
+    assert _bad([dict(conv, k=2)]) == xp.EINVAL                         # even kernel
+    assert _bad([dict(conv, inputs=[0])]) == xp.EINVAL                  # forward reference
+    assert _bad([conv, dict(kind="relu", inputs=[-1])]) == xp.EINVAL   # layer 0 unused
+    assert _bad([conv, dict(kind="softmax_ce", inputs=[0], classes=8)]) == xp.EINVAL  # not [n,C]
+    assert _bad([dict(kind="linear", inputs=[-1], cin=4, cout=3, bias=True)]) == xp.EINVAL
+    assert _bad([conv, dict(kind="add", inputs=[0, -1])]) == xp.EINVAL  # shape mismatch
+    assert _bad([conv], mb=0) == xp.EINVAL
+    assert _bad([dict(kind="concat", inputs=[-1])]) == xp.EINVAL
+    # concat of the stage input itself is not a layer output
+    assert _bad([dict(kind="concat", inputs=[-1, -1])], shape=(4, 4, 4)) in (xp.EINVAL, xp.EUNSUPPORTED)
+
+
+def test_stage_create_checks_arguments_before_touching_the_device():
+    w = wl.tiny_mlp()
+    d = xp.layer_descs(w.layers)
+    h = ctypes.c_void_p()
+    L = xp.lib()
+    # null device buffers
+    st = L.xpipe_stage_create(d, len(w.layers), 32, 4, 1, 1, 256, xp.F32, None, None, None, None,
+                              None, None, None, None, 0, ctypes.byref(h))
+    assert st == xp.EINVAL and not h.value
+    # T < 1
+    fake = 256
+    st = L.xpipe_stage_create(d, len(w.layers), 32, 0, 1, 1, 256, xp.F32, None, fake, fake, fake,
+                              fake, fake, fake, fake, 1 << 30, ctypes.byref(h))
+    assert st == xp.EINVAL and not h.value
+    # workspace too small
+    st = L.xpipe_stage_create(d, len(w.layers), 32, 4, 1, 1, 256, xp.F32, None, fake, fake, fake,
+                              fake, fake, fake, fake, 16, ctypes.byref(h))
+    assert st == xp.EINVAL and not h.value
+    assert b"workspace" in L.xpipe_last_error()
+
+
+def test_flat_entry_points_check_arguments_on_the_host():
+    L = xp.lib()
+    hp = xp.Hyper().c(1)
+    assert L.xpipe_predict_flat(None, None, None, None, None, -1, 1, ctypes.byref(hp), None) == xp.EINVAL
+    assert L.xpipe_predict_flat(None, None, None, None, None, 0, 1, ctypes.byref(hp), None) == xp.OK
+    bad = xp.Hyper(beta1=1.0).c(1)
+    assert L.xpipe_predict_flat(None, None, None, None, None, 0, 1, ctypes.byref(bad), None) == xp.EINVAL
+    assert L.xpipe_predict_flat(16, 16, 16, 16, None, 8, -1, ctypes.byref(hp), None) == xp.EINVAL
+    # misaligned buffers are refused before any launch
+    assert L.xpipe_predict_flat(20, 16, 16, 16, None, 8, 1, ctypes.byref(hp), None) == xp.EINVAL
+    assert L.xpipe_adam_flat(None, None, None, None, 0, ctypes.byref(hp), 1, None, 0, None, 0, None) == xp.OK

@@ -23,8 +23,6 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "f64": 78.6, "f32": 157.3}
-CLASS_NAMES = {0: "conv/linear forward-type GEMM (fwd, recompute, data gradient)",
-               1: "weight-gradient GEMM", 2: "prediction / Adam", 3: "other layer kernels"}
 
 
 def parse():
@@ -102,7 +100,7 @@ def time_stage(args):
     for j in range(args.steps):
         step(j)
     torch.cuda.synchronize()
-    classes = {c: st.timing(c) for c in range(4)}
+    classes = st.timing()
     st.set_timing(False)
     torch.cuda.synchronize()
     fin = bool(torch.isfinite(st.W).all().item()) and (not w.has_loss or bool(torch.isfinite(loss).all().item()))
@@ -147,10 +145,9 @@ def time_sweep(n, steps):
 
 
 def cpu_baseline(w, dtype):
-    """The oracle as it stands, on the host: one micro-batch's forward plus
-    its backward with recomputation, and the prediction + Adam over the
-    stage's parameters (a bounded sample of one step: 1 of T micro-batches)."""
-    import numpy as np
+    """The oracle as it stands, on the host, for one whole step of the same
+    stage: both predictions, T forwards, T backwards with recomputation and
+    the Adam update (the oracle's mini-batch driver, one mini-batch)."""
     import oracle
     import workloads as wl
     threads = os.cpu_count()
@@ -161,23 +158,19 @@ def cpu_baseline(w, dtype):
             threads = max(i.get("num_threads", 0) for i in info) or threads
     except Exception:
         pass
-    inp = wl.stage_inputs(w, act_dtype="bf16" if dtype == "bf16" else "f32")
-    st = oracle.Stage(w.layers, "bf16" if dtype == "bf16" else "f32")
-    N = w.T * w.micro_batch
+    storage = "bf16" if dtype == "bf16" else "f32"
+    inp = wl.stage_inputs(w, act_dtype=storage, moment_init="paper")
+    st = oracle.Stage(w.layers, storage)
     t0 = time.perf_counter()
-    lab = None if inp.labels is None else inp.labels[0][0]
-    dy = None if inp.dys is None else inp.dys[0][0]
-    st.forward(inp.params, inp.xs[0][0], lab, N)
-    st.backward(inp.params, inp.xs[0][0], dy, lab, N, need_dx=w.rank > 0)
-    hp = oracle.Hyper()
-    for p, m, v in zip(inp.params, inp.m, inp.v):
-        oracle.predict(p, m, v, 1, w.s_fwd, hp.lr, hp.beta1, hp.beta2, hp.eps)
-        oracle.adam_update(p, m, v, p, 1, hp.lr, hp.beta1, hp.beta2, hp.eps)
+    oracle.train_stage(st, inp.params, inp.m, inp.v, inp.xs, w.s_fwd, w.s_bwd, oracle.Hyper(),
+                       labels=inp.labels, dys=inp.dys, need_dx=w.rank > 0, minibatches=1, t0=1)
     sec = time.perf_counter() - t0
-    return {"value": w.micro_batch / sec, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
-            "sample": (f"1 of {w.T} micro-batches ({w.micro_batch} samples): forward + backward with "
-                       f"recompute in fp64 numpy ({dtype} storage rounding), plus prediction and Adam "
-                       f"over all {sum(p.size for p in inp.params)} parameters; {sec:.1f} s")}
+    samples = w.T * w.micro_batch
+    return {"value": round(samples / sec, 3), "unit": "samples/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": (f"one full step ({samples} samples: 2 predictions, {w.T} forwards, {w.T} "
+                       f"backwards with recompute, Adam) of the same stage in fp64 numpy with "
+                       f"{storage} storage rounding; {sec:.1f} s on {threads} threads")}
 
 
 def main():
@@ -193,11 +186,29 @@ def main():
     samples = w.T * w.micro_batch
     value = samples / (ms / 1e3)
     peak_key = "bf16" if args.dtype == "bf16" else "f64"
-    dom = max((0, 1), key=lambda c: classes[c][0])
-    c_ms, c_n, c_work = classes[dom]
-    achieved = c_work / (c_ms / 1e3) / 1e12 if c_ms > 0 else 0.0
-    gemm_ms = classes[0][0] + classes[1][0]
-    gemm_work = classes[0][2] + classes[1][2]
+
+    def is_gemm(name):
+        return name.startswith("k_conv_gemm") or name.startswith("k_wgrad")
+
+    def roof(name):
+        kms, kn, kwork = classes[name]
+        if is_gemm(name):
+            ach = kwork / (kms / 1e3) / 1e12
+            return {"bound": "mfma", "achieved": round(ach, 3), "peak": PEAK_TFLOPS[peak_key],
+                    "unit": "TFLOP/s", "frac": round(ach / PEAK_TFLOPS[peak_key], 5)}
+        ach = kwork / (kms / 1e3) / 1e9
+        return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4)}
+
+    dom = max(classes, key=lambda k: classes[k][0])
+    d_ms, d_n, d_work = classes[dom]
+    rf = roof(dom)
+    rf.update({"kernel": dom, "traffic": None, "launches_per_step": d_n / args.steps,
+               "avg_launch_us": round(1e3 * d_ms / max(d_n, 1), 3),
+               "work_per_launch": d_work / max(d_n, 1)})
+    gemm_ms = sum(v[0] for k, v in classes.items() if is_gemm(k))
+    gemm_work = sum(v[2] for k, v in classes.items() if is_gemm(k))
+    top = sorted(classes, key=lambda k: -classes[k][0])[:12]
     out = {
         "metric": "stage samples/sec (predict+fwd+bwd+Adam); predict/Adam HBM GB/s; MFMA util",
         "value": round(value, 2),
@@ -215,14 +226,15 @@ def main():
                    "mini_batch": samples, "input_hwc": list(w.in_shape), "s_fwd": w.s_fwd,
                    "s_bwd": w.s_bwd, "rank": w.rank, "size": w.size,
                    "update": "adam fused with next predictions", "parallelism": "one stage, 1 GPU"},
-        "roofline": {"bound": "mfma", "kernel": CLASS_NAMES[dom], "achieved": round(achieved, 3),
-                     "peak": PEAK_TFLOPS[peak_key], "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_TFLOPS[peak_key], 5), "traffic": None,
-                     "launches": c_n, "avg_launch_us": round(1e3 * c_ms / max(c_n, 1), 3)},
+        "roofline": rf,
         "mfma_util_all_gemm": round(gemm_work / (gemm_ms / 1e3) / 1e12 / PEAK_TFLOPS[peak_key], 5)
         if gemm_ms > 0 else None,
-        "kernel_classes_ms_per_step": {CLASS_NAMES[c]: round(classes[c][0] / args.steps, 4)
-                                       for c in range(4)},
+        "kernels_timed_sum_ms_per_step": round(sum(v[0] for v in classes.values()) / args.steps, 4),
+        "top_kernels": [{"kernel": k, "ms_per_step": round(classes[k][0] / args.steps, 4),
+                         "launches_per_step": classes[k][1] / args.steps,
+                         "avg_us": round(1e3 * classes[k][0] / max(classes[k][1], 1), 2),
+                         **{kk: vv for kk, vv in roof(k).items() if kk in ("achieved", "unit", "frac")}}
+                        for k in top],
         "finite": finite,
     }
     if not args.no_sweep:

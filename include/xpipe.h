@@ -206,15 +206,19 @@ xpipe_status xpipe_adam_flat(float* W, float* m, float* v, float* G, int64_t n,
                              float* pred_fwd, int32_t s_fwd, float* pred_bwd, int32_t s_bwd,
                              void* hip_stream);
 
-/* Optional per-kernel timing: when enabled, hipEvents bracket every launch
- * of the classes below on the stage stream; xpipe_stage_timing reports their
- * summed duration (ms, after the caller synchronised), launch count and
- * algorithmic work (flops for GEMM classes, bytes for the others).
- * Classes: 0 conv/linear forward-type GEMM (forward, recompute, data
- * gradient), 1 weight-gradient GEMM, 2 prediction/Adam, 3 everything else. */
+/* Optional per-kernel timing (measurement support, not part of the method):
+ * while enabled, hipEvents bracket every kernel the stage launches on its
+ * stream.  xpipe_stage_timing_count waits for the recorded launches and
+ * reports how many distinct kernels ran; xpipe_stage_timing_entry gives, for
+ * entry i (0 <= i < count, sorted by name), the kernel name (a static string
+ * owned by the library, valid until the stage is destroyed), the summed
+ * duration in ms, the launch count and the algorithmic work (flops for the
+ * GEMM kernels k_conv_gemm / k_wgrad, bytes moved for all others).
+ * Enabling (or re-enabling) clears the accumulated entries. */
 xpipe_status xpipe_stage_set_timing(xpipe_stage_t st, int32_t enable);
-xpipe_status xpipe_stage_timing(xpipe_stage_t st, int32_t kernel_class, double* ms,
-                                int64_t* launches, double* work);
+xpipe_status xpipe_stage_timing_count(xpipe_stage_t st, int32_t* n);
+xpipe_status xpipe_stage_timing_entry(xpipe_stage_t st, int32_t i, const char** kernel, double* ms,
+                                      int64_t* launches, double* work);
 
 /* Message for the last non-OK status returned on the calling thread. */
 const char* xpipe_last_error(void);

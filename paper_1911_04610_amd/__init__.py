@@ -83,8 +83,10 @@ _SIGS = {
     "xpipe_adam_flat": [_P, _P, _P, _P, _I64, ctypes.POINTER(HParams), _I32, _P, _I32, _P, _I32,
                         _P],
     "xpipe_stage_set_timing": [_P, _I32],
-    "xpipe_stage_timing": [_P, _I32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64),
-                           ctypes.POINTER(ctypes.c_double)],
+    "xpipe_stage_timing_count": [_P, ctypes.POINTER(_I32)],
+    "xpipe_stage_timing_entry": [_P, _I32, ctypes.POINTER(ctypes.c_char_p),
+                                 ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64),
+                                 ctypes.POINTER(ctypes.c_double)],
 }
 
 
@@ -240,11 +242,17 @@ class Stage:
     def set_timing(self, enable: bool):
         _check(lib().xpipe_stage_set_timing(self._h, int(enable)))
 
-    def timing(self, cls: int):
-        ms, n, work = ctypes.c_double(0), _I64(0), ctypes.c_double(0)
-        _check(lib().xpipe_stage_timing(self._h, cls, ctypes.byref(ms), ctypes.byref(n),
-                                        ctypes.byref(work)))
-        return ms.value, n.value, work.value
+    def timing(self):
+        """{kernel name: (ms, launches, work)} over the launches since set_timing(True)."""
+        n = _I32(0)
+        _check(lib().xpipe_stage_timing_count(self._h, ctypes.byref(n)))
+        out = {}
+        for i in range(n.value):
+            name, ms, cnt, work = ctypes.c_char_p(), ctypes.c_double(0), _I64(0), ctypes.c_double(0)
+            _check(lib().xpipe_stage_timing_entry(self._h, i, ctypes.byref(name), ctypes.byref(ms),
+                                                  ctypes.byref(cnt), ctypes.byref(work)))
+            out[name.value.decode()] = (ms.value, cnt.value, work.value)
+        return out
 
     def destroy(self):
         if self._h:

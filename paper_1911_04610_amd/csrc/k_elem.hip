@@ -11,6 +11,9 @@
 #include "xp_device.h"
 #include "xp_kernels.h"
 
+#include <initializer_list>
+#include <utility>
+
 namespace xp {
 
 __host__ __device__ static inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
@@ -25,8 +28,11 @@ static int row_blocks_for(int M, int C) {
 }
 
 int col_row_blocks(int M, int C) { return row_blocks_for(M, C); }
+int col_row_blocks_v(int M, int C, int N);
 size_t col_partial_bytes(int M, int C) {
-  return (size_t)row_blocks_for(M, C) * 2 * C * sizeof(double);
+  int rb = row_blocks_for(M, C);
+  if (rb < 128) rb = 128;  // the vectorised reduction uses at most 128 row blocks
+  return (size_t)rb * 2 * C * sizeof(double);
 }
 
 // ---------------------------------------------------------------- column reductions
@@ -70,41 +76,21 @@ __global__ __launch_bounds__(256) void k_colpart(ColArgs a) {
   }
 }
 
-__global__ __launch_bounds__(256) void k_colfinal(ColArgs a) {
-  const int col = blockIdx.x * blockDim.x + threadIdx.x;
-  if (col >= a.C) return;
-  double s0 = 0.0, s1 = 0.0;
-  for (int b = 0; b < a.row_blocks; ++b) {
-    s0 += a.partial[((size_t)b * 2 + 0) * a.C + col];
-    s1 += a.partial[((size_t)b * 2 + 1) * a.C + col];
-  }
-  if (a.mode == COL_STATS) {
-    double mean = s0 / a.M;
-    double var = s1 / a.M - mean * mean;
-    if (var < 0.0) var = 0.0;
-    a.out0[col] = mean;
-    a.out1[col] = 1.0 / sqrt(var + a.eps);
-  } else if (a.mode == COL_BNBWD) {
-    a.out0[col] = s0;  // dbeta
-    a.out1[col] = s1;  // dgamma
-    a.grad0[col] = (float)((double)a.grad0[col] + s1);
-    a.grad1[col] = (float)((double)a.grad1[col] + s0);
-  } else {
-    a.grad0[col] = (float)((double)a.grad0[col] + s0);
-  }
-}
+__global__ void k_colfinal_v(ColArgs a);
 
 template <typename T>
 static hipError_t colreduce_go(const ColArgs& a, hipStream_t s) {
   dim3 grid(ceil_div(a.C, 64), a.row_blocks);
-  hipLaunchKernelGGL(k_colpart<T>, grid, dim3(256), 0, s, a);
+  XP_LAUNCH("k_colpart", (double)a.M * a.C * sizeof(T) * (a.mode == COL_BNBWD ? 2 : 1), k_colpart<T>, grid,
+            dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_colfinal, dim3(ceil_div(a.C, 256)), dim3(256), 0, s, a);
+  XP_LAUNCH("k_colfinal", (double)a.row_blocks * 2 * a.C * 8, k_colfinal_v, dim3(ceil_div(a.C, 64)),
+            dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
-hipError_t launch_colreduce(int dtype, const ColArgs& a, hipStream_t s) {
+static hipError_t launch_colreduce_s(int dtype, const ColArgs& a, hipStream_t s) {
   if (a.C <= 0) return hipSuccess;
   return dtype == DT_BF16 ? colreduce_go<bf16_t>(a, s) : colreduce_go<float>(a, s);
 }
@@ -130,14 +116,14 @@ __global__ __launch_bounds__(256) void k_bn_apply(BnApplyArgs a, int row_blocks)
   }
 }
 
-hipError_t launch_bn_apply(int dtype, const BnApplyArgs& a, hipStream_t s) {
+static hipError_t launch_bn_apply_s(int dtype, const BnApplyArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.C <= 0) return hipSuccess;
   int rb = row_blocks_for(a.M, a.C);
   dim3 grid(ceil_div(a.C, 64), rb);
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(k_bn_apply<bf16_t>, grid, dim3(256), 0, s, a, rb);
+    XP_LAUNCH("k_bn_apply<bf16>", (double)a.M * a.C * 2 * (a.res ? 3 : 2), k_bn_apply<bf16_t>, grid, dim3(256), 0, s, a, rb);
   else
-    hipLaunchKernelGGL(k_bn_apply<float>, grid, dim3(256), 0, s, a, rb);
+    XP_LAUNCH("k_bn_apply<f32>", (double)a.M * a.C * 4 * (a.res ? 3 : 2), k_bn_apply<float>, grid, dim3(256), 0, s, a, rb);
   return hipGetLastError();
 }
 
@@ -174,14 +160,14 @@ __global__ __launch_bounds__(256) void k_bn_bwd(BnBwdArgs a, int row_blocks) {
   }
 }
 
-hipError_t launch_bn_bwd(int dtype, const BnBwdArgs& a, hipStream_t s) {
+static hipError_t launch_bn_bwd_s(int dtype, const BnBwdArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.C <= 0) return hipSuccess;
   int rb = row_blocks_for(a.M, a.C);
   dim3 grid(ceil_div(a.C, 64), rb);
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(k_bn_bwd<bf16_t>, grid, dim3(256), 0, s, a, rb);
+    XP_LAUNCH("k_bn_bwd<bf16>", (double)a.M * a.C * 2 * (a.dres ? 5 : 3), k_bn_bwd<bf16_t>, grid, dim3(256), 0, s, a, rb);
   else
-    hipLaunchKernelGGL(k_bn_bwd<float>, grid, dim3(256), 0, s, a, rb);
+    XP_LAUNCH("k_bn_bwd<f32>", (double)a.M * a.C * 4 * (a.dres ? 5 : 3), k_bn_bwd<float>, grid, dim3(256), 0, s, a, rb);
   return hipGetLastError();
 }
 
@@ -207,14 +193,14 @@ __global__ __launch_bounds__(256) void k_elt(EltArgs a, int row_blocks) {
   }
 }
 
-hipError_t launch_elementwise(int dtype, const EltArgs& a, hipStream_t s) {
+static hipError_t launch_elementwise_s(int dtype, const EltArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.C <= 0) return hipSuccess;
   int rb = row_blocks_for(a.M, a.C);
   dim3 grid(ceil_div(a.C, 64), rb);
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(k_elt<bf16_t>, grid, dim3(256), 0, s, a, rb);
+    XP_LAUNCH("k_elt<bf16>", (double)a.M * a.C * 2 * 3, k_elt<bf16_t>, grid, dim3(256), 0, s, a, rb);
   else
-    hipLaunchKernelGGL(k_elt<float>, grid, dim3(256), 0, s, a, rb);
+    XP_LAUNCH("k_elt<f32>", (double)a.M * a.C * 4 * 3, k_elt<float>, grid, dim3(256), 0, s, a, rb);
   return hipGetLastError();
 }
 
@@ -346,25 +332,25 @@ __global__ __launch_bounds__(256) void k_gap_bwd(PoolArgs a, int rows, int row_b
 }
 
 template <typename T>
-static void pool_launch_rows(void (*k)(PoolArgs, int, int), const PoolArgs& a, int rows,
-                             hipStream_t s) {
+static void pool_launch_rows(void (*k)(PoolArgs, int, int), const char* name, const PoolArgs& a,
+                             int rows, hipStream_t s) {
   int rb = row_blocks_for(rows, a.C);
-  hipLaunchKernelGGL(k, dim3(ceil_div(a.C, 64), rb), dim3(256), 0, s, a, rows, rb);
+  XP_LAUNCH(name, (double)rows * a.C * sizeof(T) * 3, k, dim3(ceil_div(a.C, 64), rb), dim3(256), 0, s, a, rows, rb);
 }
 
-hipError_t launch_maxpool_fwd(int dtype, const PoolArgs& a, hipStream_t s) {
+static hipError_t launch_maxpool_fwd_s(int dtype, const PoolArgs& a, hipStream_t s) {
   int rows = a.nb * (a.H / 2) * (a.W / 2);
   if (rows <= 0 || a.C <= 0) return hipSuccess;
-  if (dtype == DT_BF16) pool_launch_rows<bf16_t>(k_maxpool_fwd<bf16_t>, a, rows, s);
-  else pool_launch_rows<float>(k_maxpool_fwd<float>, a, rows, s);
+  if (dtype == DT_BF16) pool_launch_rows<bf16_t>(k_maxpool_fwd<bf16_t>, "k_maxpool_fwd<bf16>", a, rows, s);
+  else pool_launch_rows<float>(k_maxpool_fwd<float>, "k_maxpool_fwd<f32>", a, rows, s);
   return hipGetLastError();
 }
 
-hipError_t launch_maxpool_bwd(int dtype, const PoolArgs& a, hipStream_t s) {
+static hipError_t launch_maxpool_bwd_s(int dtype, const PoolArgs& a, hipStream_t s) {
   int rows = a.nb * a.H * a.W;
   if (rows <= 0 || a.C <= 0) return hipSuccess;
-  if (dtype == DT_BF16) pool_launch_rows<bf16_t>(k_maxpool_bwd<bf16_t>, a, rows, s);
-  else pool_launch_rows<float>(k_maxpool_bwd<float>, a, rows, s);
+  if (dtype == DT_BF16) pool_launch_rows<bf16_t>(k_maxpool_bwd<bf16_t>, "k_maxpool_bwd<bf16>", a, rows, s);
+  else pool_launch_rows<float>(k_maxpool_bwd<float>, "k_maxpool_bwd<f32>", a, rows, s);
   return hipGetLastError();
 }
 
@@ -373,33 +359,519 @@ static hipError_t avg_go(const PoolArgs& a, const void* src, int ld_src, hipStre
   int rows = a.nb * a.H * a.W;
   if (rows <= 0 || a.C <= 0) return hipSuccess;
   int rb = row_blocks_for(rows, a.C);
-  hipLaunchKernelGGL(k_avgpool3<T>, dim3(ceil_div(a.C, 64), rb), dim3(256), 0, s, a,
+  XP_LAUNCH("k_avgpool3", (double)rows * a.C * sizeof(T) * 2, k_avgpool3<T>, dim3(ceil_div(a.C, 64), rb), dim3(256), 0, s, a,
                      (const T*)src, ld_src, rows, rb);
   return hipGetLastError();
 }
 
-hipError_t launch_avgpool_fwd(int dtype, const PoolArgs& a, hipStream_t s) {
+static hipError_t launch_avgpool_fwd_s(int dtype, const PoolArgs& a, hipStream_t s) {
   return dtype == DT_BF16 ? avg_go<bf16_t>(a, a.x, a.ldx, s) : avg_go<float>(a, a.x, a.ldx, s);
 }
 
-hipError_t launch_avgpool_bwd(int dtype, const PoolArgs& a, hipStream_t s) {
+static hipError_t launch_avgpool_bwd_s(int dtype, const PoolArgs& a, hipStream_t s) {
   return dtype == DT_BF16 ? avg_go<bf16_t>(a, a.dy, a.lddy, s) : avg_go<float>(a, a.dy, a.lddy, s);
 }
 
-hipError_t launch_gap_fwd(int dtype, const PoolArgs& a, hipStream_t s) {
+static hipError_t launch_gap_fwd_s(int dtype, const PoolArgs& a, hipStream_t s) {
   if (a.nb <= 0 || a.C <= 0) return hipSuccess;
   dim3 grid(ceil_div(a.C, 64), a.nb);
-  if (dtype == DT_BF16) hipLaunchKernelGGL(k_gap_fwd<bf16_t>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(k_gap_fwd<float>, grid, dim3(256), 0, s, a);
+  double gb = (double)a.nb * a.H * a.W * a.C * (dtype == DT_BF16 ? 2 : 4);
+  if (dtype == DT_BF16) XP_LAUNCH("k_gap_fwd<bf16>", gb, k_gap_fwd<bf16_t>, grid, dim3(256), 0, s, a);
+  else XP_LAUNCH("k_gap_fwd<f32>", gb, k_gap_fwd<float>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
-hipError_t launch_gap_bwd(int dtype, const PoolArgs& a, hipStream_t s) {
+static hipError_t launch_gap_bwd_s(int dtype, const PoolArgs& a, hipStream_t s) {
   int rows = a.nb * a.H * a.W;
   if (rows <= 0 || a.C <= 0) return hipSuccess;
-  if (dtype == DT_BF16) pool_launch_rows<bf16_t>(k_gap_bwd<bf16_t>, a, rows, s);
-  else pool_launch_rows<float>(k_gap_bwd<float>, a, rows, s);
+  if (dtype == DT_BF16) pool_launch_rows<bf16_t>(k_gap_bwd<bf16_t>, "k_gap_bwd<bf16>", a, rows, s);
+  else pool_launch_rows<float>(k_gap_bwd<float>, "k_gap_bwd<f32>", a, rows, s);
   return hipGetLastError();
+}
+
+// ============================================================================
+// vectorised forms: each thread moves 16-byte chunks (8 bf16 or 4 fp32
+// channels).  Used whenever channel counts, row pitches and base pointers
+// allow 16-byte accesses (every layer of the stages measured here); the
+// per-channel kernels above remain for the other shapes.
+// ============================================================================
+template <typename T> struct VT;
+template <> struct VT<bf16_t> { static constexpr int N = 8; };
+template <> struct VT<float> { static constexpr int N = 4; };
+
+template <typename T>
+XP_DEV void vld(const T* p, double* v);
+template <>
+XP_DEV void vld<bf16_t>(const bf16_t* p, double* v) {
+  uint4 u = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = (double)__uint_as_float(w[i] << 16);
+    v[2 * i + 1] = (double)__uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+template <>
+XP_DEV void vld<float>(const float* p, double* v) {
+  float4 f = *reinterpret_cast<const float4*>(p);
+  v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+}
+template <typename T>
+XP_DEV void vst(T* p, const double* v);
+template <>
+XP_DEV void vst<bf16_t>(bf16_t* p, const double* v) {
+  uint4 u;
+  u.x = (uint32_t)f32_to_bf16((float)v[0]) | ((uint32_t)f32_to_bf16((float)v[1]) << 16);
+  u.y = (uint32_t)f32_to_bf16((float)v[2]) | ((uint32_t)f32_to_bf16((float)v[3]) << 16);
+  u.z = (uint32_t)f32_to_bf16((float)v[4]) | ((uint32_t)f32_to_bf16((float)v[5]) << 16);
+  u.w = (uint32_t)f32_to_bf16((float)v[6]) | ((uint32_t)f32_to_bf16((float)v[7]) << 16);
+  *reinterpret_cast<uint4*>(p) = u;
+}
+template <>
+XP_DEV void vst<float>(float* p, const double* v) {
+  *reinterpret_cast<float4*>(p) = make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
+}
+
+static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+template <typename T>
+static bool vec_ok(int C, std::initializer_list<std::pair<const void*, int>> views) {
+  constexpr int N = VT<T>::N;
+  if (C % N) return false;
+  for (auto& v : views)
+    if (v.first && (!al16(v.first) || (v.second % N))) return false;
+  return true;
+}
+
+static int grid_for(int64_t items) {
+  int64_t b = (items + 255) / 256;
+  if (b > 8192) b = 8192;
+  return (int)(b < 1 ? 1 : b);
+}
+
+// mask helper: zero lanes whose mask value is not > 0
+template <typename T>
+XP_DEV void vmask(const T* mk, double* v) {
+  constexpr int N = VT<T>::N;
+  double m[N];
+  vld(mk, m);
+#pragma unroll
+  for (int e = 0; e < N; ++e)
+    if (!(m[e] > 0.0)) v[e] = 0.0;
+}
+
+// ---------------------------------------------------------------- column reductions
+// Block: CL chunk-lanes x RG row groups; partials per (row block, column);
+// the row groups of a block are added in a fixed order in LDS.
+template <typename T>
+__global__ __launch_bounds__(256) void k_colpart_v(ColArgs a) {
+  constexpr int N = VT<T>::N;
+  __shared__ double sh[2][256][N];
+  const int chunks = a.C / N;
+  const int CL = chunks < 256 ? chunks : 256;
+  const int RG = 256 / CL;
+  const int cl = threadIdx.x % CL, g = threadIdx.x / CL;
+  const int chunk = blockIdx.x * CL + cl;
+  const int per = ceil_div(a.M, a.row_blocks);
+  const int r0 = blockIdx.y * per, r1 = min(a.M, r0 + per);
+  const T* A = (const T*)a.a;
+  const T* Z = (const T*)a.z;
+  double s0[N], s1[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) s0[e] = s1[e] = 0.0;
+  if (g < RG && chunk < chunks) {
+    const int c0 = chunk * N;
+    double mu[N], rs[N];
+    if (a.mode == COL_BNBWD) {
+#pragma unroll
+      for (int e = 0; e < N; ++e) { mu[e] = a.mean[c0 + e]; rs[e] = a.rstd[c0 + e]; }
+    }
+#pragma unroll 2
+    for (int r = r0 + g; r < r1; r += RG) {
+      double v[N];
+      vld(A + (size_t)r * a.lda + c0, v);
+      if (a.mode == COL_STATS) {
+#pragma unroll
+        for (int e = 0; e < N; ++e) { s0[e] += v[e]; s1[e] += v[e] * v[e]; }
+      } else if (a.mode == COL_BNBWD) {
+        double z[N];
+        vld(Z + (size_t)r * a.ldz + c0, z);
+#pragma unroll
+        for (int e = 0; e < N; ++e) { s0[e] += v[e]; s1[e] += v[e] * ((z[e] - mu[e]) * rs[e]); }
+      } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e) s0[e] += v[e];
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < N; ++e) { sh[0][threadIdx.x][e] = s0[e]; sh[1][threadIdx.x][e] = s1[e]; }
+  __syncthreads();
+  if (g == 0 && chunk < chunks) {
+    double t0[N], t1[N];
+#pragma unroll
+    for (int e = 0; e < N; ++e) t0[e] = t1[e] = 0.0;
+    for (int q = 0; q < RG; ++q)
+#pragma unroll
+      for (int e = 0; e < N; ++e) { t0[e] += sh[0][q * CL + cl][e]; t1[e] += sh[1][q * CL + cl][e]; }
+    const int c0 = chunk * N;
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+      a.partial[((size_t)blockIdx.y * 2 + 0) * a.C + c0 + e] = t0[e];
+      a.partial[((size_t)blockIdx.y * 2 + 1) * a.C + c0 + e] = t1[e];
+    }
+  }
+}
+
+// finalize: 64 columns x 4 row-block groups per workgroup, fixed-order sums
+__global__ __launch_bounds__(256) void k_colfinal_v(ColArgs a) {
+  __shared__ double sh[2][4][64];
+  const int lc = threadIdx.x & 63, g = threadIdx.x >> 6;
+  const int col = blockIdx.x * 64 + lc;
+  double s0 = 0.0, s1 = 0.0;
+  if (col < a.C) {
+#pragma unroll 4
+    for (int b = g; b < a.row_blocks; b += 4) {
+      s0 += a.partial[((size_t)b * 2 + 0) * a.C + col];
+      s1 += a.partial[((size_t)b * 2 + 1) * a.C + col];
+    }
+  }
+  sh[0][g][lc] = s0;
+  sh[1][g][lc] = s1;
+  __syncthreads();
+  if (g != 0 || col >= a.C) return;
+  s0 = ((sh[0][0][lc] + sh[0][1][lc]) + sh[0][2][lc]) + sh[0][3][lc];
+  s1 = ((sh[1][0][lc] + sh[1][1][lc]) + sh[1][2][lc]) + sh[1][3][lc];
+  if (a.mode == COL_STATS) {
+    double mean = s0 / a.M;
+    double var = s1 / a.M - mean * mean;
+    if (var < 0.0) var = 0.0;
+    a.out0[col] = mean;
+    a.out1[col] = 1.0 / sqrt(var + a.eps);
+  } else if (a.mode == COL_BNBWD) {
+    a.out0[col] = s0;
+    a.out1[col] = s1;
+    a.grad0[col] = (float)((double)a.grad0[col] + s1);
+    a.grad1[col] = (float)((double)a.grad1[col] + s0);
+  } else {
+    a.grad0[col] = (float)((double)a.grad0[col] + s0);
+  }
+}
+
+int col_row_blocks_v(int M, int C, int N) {
+  int chunks = C / N;
+  int CL = chunks < 256 ? chunks : 256;
+  int RG = 256 / CL;
+  int colblocks = ceil_div(chunks, CL);
+  int want = ceil_div(512, colblocks);          // ~512 workgroups
+  int maxrb = ceil_div(M, RG * 8);              // >= ~8 rows per thread
+  if (want > maxrb) want = maxrb;
+  if (want > 128) want = 128;
+  return want < 1 ? 1 : want;
+}
+
+template <typename T>
+static hipError_t colreduce_v(ColArgs a, hipStream_t s) {
+  constexpr int N = VT<T>::N;
+  int chunks = a.C / N;
+  int CL = chunks < 256 ? chunks : 256;
+  a.row_blocks = col_row_blocks_v(a.M, a.C, N);
+  XP_LAUNCH(sizeof(T) == 2 ? "k_colpart_v<bf16>" : "k_colpart_v<f32>",
+            (double)a.M * a.C * sizeof(T) * (a.mode == COL_BNBWD ? 2 : 1), k_colpart_v<T>,
+            dim3(ceil_div(chunks, CL), a.row_blocks), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  XP_LAUNCH("k_colfinal", (double)a.row_blocks * 2 * a.C * 8, k_colfinal_v, dim3(ceil_div(a.C, 64)),
+            dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- BN apply / backward
+template <typename T>
+__global__ __launch_bounds__(256) void k_bn_apply_v(BnApplyArgs a) {
+  constexpr int N = VT<T>::N;
+  const int chunks = a.C / N;
+  const int items = a.M * chunks;
+  const T* Z = (const T*)a.z;
+  const T* R = (const T*)a.res;
+  T* Y = (T*)a.y;
+  for (int it = blockIdx.x * blockDim.x + threadIdx.x; it < items; it += gridDim.x * blockDim.x) {
+    const int r = it / chunks, c0 = (it - r * chunks) * N;
+    double z[N], rr[N];
+    vld(Z + (size_t)r * a.ldz + c0, z);
+    if (R) vld(R + (size_t)r * a.ldres + c0, rr);
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+      double xh = (z[e] - a.mean[c0 + e]) * a.rstd[c0 + e];
+      double v = (double)a.gamma[c0 + e] * xh + (double)a.beta[c0 + e];
+      if (R) v += rr[e];
+      if (a.relu) v = v > 0.0 ? v : 0.0;
+      z[e] = v;
+    }
+    vst(Y + (size_t)r * a.ldy + c0, z);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_bn_bwd_v(BnBwdArgs a) {
+  constexpr int N = VT<T>::N;
+  const int chunks = a.C / N;
+  const int items = a.M * chunks;
+  const T* G = (const T*)a.g;
+  const T* Z = (const T*)a.z;
+  T* DZ = (T*)a.dz;
+  T* DR = (T*)a.dres;
+  const T* RM = (const T*)a.resmask;
+  const T* ZM = (const T*)a.dzmask;
+  for (int it = blockIdx.x * blockDim.x + threadIdx.x; it < items; it += gridDim.x * blockDim.x) {
+    const int r = it / chunks, c0 = (it - r * chunks) * N;
+    double g[N], z[N], d[N];
+    vld(G + (size_t)r * a.ldg + c0, g);
+    vld(Z + (size_t)r * a.ldz + c0, z);
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+      const int c = c0 + e;
+      double rs = a.rstd[c];
+      double xh = (z[e] - a.mean[c]) * rs;
+      d[e] = (double)a.gamma[c] * rs * (g[e] - a.dbeta[c] / a.M - xh * (a.dgamma[c] / a.M));
+    }
+    if (ZM) vmask(ZM + (size_t)r * a.ldzm + c0, d);
+    T* pz = DZ + (size_t)r * a.lddz + c0;
+    if (a.dz_accumulate) {
+      double o[N];
+      vld(pz, o);
+#pragma unroll
+      for (int e = 0; e < N; ++e) d[e] += o[e];
+    }
+    vst(pz, d);
+    if (DR) {
+      if (RM) vmask(RM + (size_t)r * a.ldrm + c0, g);
+      T* p = DR + (size_t)r * a.lddres + c0;
+      if (a.res_accumulate) {
+        double o[N];
+        vld(p, o);
+#pragma unroll
+        for (int e = 0; e < N; ++e) g[e] += o[e];
+      }
+      vst(p, g);
+    }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_elt_v(EltArgs a) {
+  constexpr int N = VT<T>::N;
+  const int chunks = a.C / N;
+  const int items = a.M * chunks;
+  const T* A = (const T*)a.a;
+  const T* B = (const T*)a.b;
+  const T* MK = (const T*)a.mask;
+  T* Y = (T*)a.y;
+  for (int it = blockIdx.x * blockDim.x + threadIdx.x; it < items; it += gridDim.x * blockDim.x) {
+    const int r = it / chunks, c0 = (it - r * chunks) * N;
+    double v[N];
+    vld(A + (size_t)r * a.lda + c0, v);
+    if (B) {
+      double b[N];
+      vld(B + (size_t)r * a.ldb + c0, b);
+#pragma unroll
+      for (int e = 0; e < N; ++e) v[e] += b[e];
+    }
+    if (a.relu) {
+#pragma unroll
+      for (int e = 0; e < N; ++e) v[e] = v[e] > 0.0 ? v[e] : 0.0;
+    }
+    if (MK) vmask(MK + (size_t)r * a.ldm + c0, v);
+    T* p = Y + (size_t)r * a.ldy + c0;
+    if (a.accumulate) {
+      double o[N];
+      vld(p, o);
+#pragma unroll
+      for (int e = 0; e < N; ++e) v[e] += o[e];
+    }
+    vst(p, v);
+  }
+}
+
+// ---------------------------------------------------------------- pooling
+template <typename T>
+__global__ __launch_bounds__(256) void k_maxpool_fwd_v(PoolArgs a) {
+  constexpr int N = VT<T>::N;
+  const int chunks = a.C / N, Ho = a.H / 2, Wo = a.W / 2;
+  const int items = a.nb * Ho * Wo * chunks;
+  const T* X = (const T*)a.x;
+  T* O = (T*)a.out;
+  for (int it = blockIdx.x * blockDim.x + threadIdx.x; it < items; it += gridDim.x * blockDim.x) {
+    const int r = it / chunks, c0 = (it - r * chunks) * N;
+    const int n = r / (Ho * Wo), rem = r - n * Ho * Wo, ho = rem / Wo, wo = rem - ho * Wo;
+    const T* base = X + ((size_t)(n * a.H + 2 * ho) * a.W + 2 * wo) * a.ldx + c0;
+    double b[N], q[N];
+    vld(base, b);
+    const T* others[3] = {base + a.ldx, base + (size_t)a.W * a.ldx, base + ((size_t)a.W + 1) * a.ldx};
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      vld(others[k], q);
+#pragma unroll
+      for (int e = 0; e < N; ++e)
+        if (q[e] > b[e]) b[e] = q[e];
+    }
+    vst(O + (size_t)r * a.ldo + c0, b);  // a max of stored values is stored exactly
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_maxpool_bwd_v(PoolArgs a) {
+  constexpr int N = VT<T>::N;
+  const int chunks = a.C / N, Ho = a.H / 2, Wo = a.W / 2;
+  const int items = a.nb * a.H * a.W * chunks;
+  const T* X = (const T*)a.x;
+  const T* DY = (const T*)a.dy;
+  const T* MK = (const T*)a.mask;
+  T* O = (T*)a.out;
+  for (int it = blockIdx.x * blockDim.x + threadIdx.x; it < items; it += gridDim.x * blockDim.x) {
+    const int r = it / chunks, c0 = (it - r * chunks) * N;
+    const int n = r / (a.H * a.W), rem = r - n * a.H * a.W, h = rem / a.W, w = rem - h * a.W;
+    const int ho = h >> 1, wo = w >> 1;
+    double d[N];
+#pragma unroll
+    for (int e = 0; e < N; ++e) d[e] = 0.0;
+    if (ho < Ho && wo < Wo) {
+      const T* base = X + ((size_t)(n * a.H + 2 * ho) * a.W + 2 * wo) * a.ldx + c0;
+      double v[4][N];
+      vld(base, v[0]);
+      vld(base + a.ldx, v[1]);
+      vld(base + (size_t)a.W * a.ldx, v[2]);
+      vld(base + ((size_t)a.W + 1) * a.ldx, v[3]);
+      double g[N];
+      vld(DY + ((size_t)(n * Ho + ho) * Wo + wo) * a.lddy + c0, g);
+      const int me = ((h & 1) << 1) + (w & 1);
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        int arg = 0;
+#pragma unroll
+        for (int q = 1; q < 4; ++q)
+          if (v[q][e] > v[arg][e]) arg = q;  // first maximum in row-major order wins ties
+        d[e] = arg == me ? g[e] : 0.0;
+      }
+    }
+    if (MK) vmask(MK + (size_t)r * a.ldm + c0, d);
+    T* p = O + (size_t)r * a.ldo + c0;
+    if (a.accumulate) {
+      double o[N];
+      vld(p, o);
+#pragma unroll
+      for (int e = 0; e < N; ++e) d[e] += o[e];
+    }
+    vst(p, d);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_avgpool3_v(PoolArgs a, const T* src, int ld_src) {
+  constexpr int N = VT<T>::N;
+  const int chunks = a.C / N;
+  const int items = a.nb * a.H * a.W * chunks;
+  const T* MK = (const T*)a.mask;
+  T* O = (T*)a.out;
+  for (int it = blockIdx.x * blockDim.x + threadIdx.x; it < items; it += gridDim.x * blockDim.x) {
+    const int r = it / chunks, c0 = (it - r * chunks) * N;
+    const int n = r / (a.H * a.W), rem = r - n * a.H * a.W, h = rem / a.W, w = rem - h * a.W;
+    double s[N], q[N];
+#pragma unroll
+    for (int e = 0; e < N; ++e) s[e] = 0.0;
+#pragma unroll
+    for (int dr = -1; dr <= 1; ++dr)
+#pragma unroll
+      for (int ds = -1; ds <= 1; ++ds) {
+        const int hh = h + dr, ww = w + ds;
+        if (hh >= 0 && hh < a.H && ww >= 0 && ww < a.W) {
+          vld(src + ((size_t)(n * a.H + hh) * a.W + ww) * ld_src + c0, q);
+#pragma unroll
+          for (int e = 0; e < N; ++e) s[e] += q[e];
+        }
+      }
+#pragma unroll
+    for (int e = 0; e < N; ++e) s[e] = s[e] / 9.0;
+    if (MK) vmask(MK + (size_t)r * a.ldm + c0, s);
+    T* p = O + (size_t)r * a.ldo + c0;
+    if (a.accumulate) {
+#pragma unroll
+      for (int e = 0; e < N; ++e) q[e] = 0.0;
+      vld(p, q);
+#pragma unroll
+      for (int e = 0; e < N; ++e) s[e] += q[e];
+    }
+    vst(p, s);
+  }
+}
+
+// global average pool: one workgroup of 512 threads per image, CL chunk-lanes
+// x RG row groups, fixed-order LDS reduction
+template <typename T>
+__global__ __launch_bounds__(512) void k_gap_fwd_v(PoolArgs a) {
+  constexpr int N = VT<T>::N;
+  __shared__ double sh[512][N];
+  const int chunks = a.C / N;
+  const int CL = chunks < 512 ? chunks : 512;
+  const int RG = 512 / CL;
+  const int cl = threadIdx.x % CL, g = threadIdx.x / CL;
+  const int n = blockIdx.y, chunk = blockIdx.x * CL + cl;
+  const int HW = a.H * a.W;
+  const T* X = (const T*)a.x;
+  double s[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) s[e] = 0.0;
+  if (g < RG && chunk < chunks) {
+#pragma unroll 4
+    for (int p = g; p < HW; p += RG) {
+      double q[N];
+      vld(X + ((size_t)n * HW + p) * a.ldx + chunk * N, q);
+#pragma unroll
+      for (int e = 0; e < N; ++e) s[e] += q[e];
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < N; ++e) sh[threadIdx.x][e] = s[e];
+  __syncthreads();
+  if (g == 0 && chunk < chunks) {
+    double t[N];
+#pragma unroll
+    for (int e = 0; e < N; ++e) t[e] = 0.0;
+    for (int q = 0; q < RG; ++q)
+#pragma unroll
+      for (int e = 0; e < N; ++e) t[e] += sh[q * CL + cl][e];
+#pragma unroll
+    for (int e = 0; e < N; ++e) t[e] = t[e] / HW;
+    vst((T*)a.out + (size_t)n * a.ldo + chunk * N, t);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_gap_bwd_v(PoolArgs a) {
+  constexpr int N = VT<T>::N;
+  const int chunks = a.C / N;
+  const int HW = a.H * a.W;
+  const int items = a.nb * HW * chunks;
+  const T* DY = (const T*)a.dy;
+  const T* MK = (const T*)a.mask;
+  T* O = (T*)a.out;
+  for (int it = blockIdx.x * blockDim.x + threadIdx.x; it < items; it += gridDim.x * blockDim.x) {
+    const int r = it / chunks, c0 = (it - r * chunks) * N;
+    const int n = r / HW;
+    double d[N];
+    vld(DY + (size_t)n * a.lddy + c0, d);
+#pragma unroll
+    for (int e = 0; e < N; ++e) d[e] = d[e] / HW;
+    if (MK) vmask(MK + (size_t)r * a.ldm + c0, d);
+    T* p = O + (size_t)r * a.ldo + c0;
+    if (a.accumulate) {
+      double o[N];
+      vld(p, o);
+#pragma unroll
+      for (int e = 0; e < N; ++e) d[e] += o[e];
+    }
+    vst(p, d);
+  }
 }
 
 // ---------------------------------------------------------------- softmax cross-entropy
@@ -440,9 +912,140 @@ __global__ __launch_bounds__(1024) void k_softmax_ce(CeArgs a) {
 
 hipError_t launch_softmax_ce(int dtype, const CeArgs& a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
-  if (dtype == DT_BF16) hipLaunchKernelGGL(k_softmax_ce<bf16_t>, dim3(1), dim3(1024), 0, s, a);
-  else hipLaunchKernelGGL(k_softmax_ce<float>, dim3(1), dim3(1024), 0, s, a);
+  double cb = (double)a.n * a.classes * (dtype == DT_BF16 ? 2 : 4) * (a.dz ? 2 : 1);
+  if (dtype == DT_BF16) XP_LAUNCH("k_softmax_ce<bf16>", cb, k_softmax_ce<bf16_t>, dim3(1), dim3(1024), 0, s, a);
+  else XP_LAUNCH("k_softmax_ce<f32>", cb, k_softmax_ce<float>, dim3(1), dim3(1024), 0, s, a);
   return hipGetLastError();
+}
+
+
+// ============================================================================
+// launchers: vectorised path when the views allow 16-byte accesses
+// ============================================================================
+template <typename T>
+static bool fits32(int64_t rows, int C) { return rows * (int64_t)(C / VT<T>::N) < (int64_t)1 << 31; }
+
+template <typename T>
+static hipError_t colreduce_t(const ColArgs& a, hipStream_t s) {
+  if (fits32<T>(a.M, a.C) && vec_ok<T>(a.C, {{a.a, a.lda}, {a.z, a.ldz}}))
+    return colreduce_v<T>(a, s);
+  return launch_colreduce_s(sizeof(T) == 2 ? DT_BF16 : DT_F32, a, s);
+}
+hipError_t launch_colreduce(int dtype, const ColArgs& a, hipStream_t s) {
+  if (a.C <= 0 || a.M <= 0) return hipSuccess;
+  return dtype == DT_BF16 ? colreduce_t<bf16_t>(a, s) : colreduce_t<float>(a, s);
+}
+
+// CHUNK_BYTES: algorithmic bytes moved per 16-byte chunk of the view
+#define XP_VEC_LAUNCH(KERNEL, items, CHUNK_BYTES, ...)                                  \
+  do {                                                                                   \
+    if (dtype == DT_BF16)                                                                \
+      XP_LAUNCH(#KERNEL "<bf16>", (double)(items) * (CHUNK_BYTES), KERNEL<bf16_t>,       \
+                dim3(grid_for(items)), dim3(256), 0, s, __VA_ARGS__);                    \
+    else                                                                                 \
+      XP_LAUNCH(#KERNEL "<f32>", (double)(items) * (CHUNK_BYTES), KERNEL<float>,         \
+                dim3(grid_for(items)), dim3(256), 0, s, __VA_ARGS__);                    \
+    return hipGetLastError();                                                            \
+  } while (0)
+
+static bool vec_dt(int dtype, int64_t rows, int C, std::initializer_list<std::pair<const void*, int>> v) {
+  return dtype == DT_BF16 ? (fits32<bf16_t>(rows, C) && vec_ok<bf16_t>(C, v))
+                          : (fits32<float>(rows, C) && vec_ok<float>(C, v));
+}
+static int vn(int dtype) { return dtype == DT_BF16 ? 8 : 4; }
+
+hipError_t launch_bn_apply(int dtype, const BnApplyArgs& a, hipStream_t s) {
+  if (a.M <= 0 || a.C <= 0) return hipSuccess;
+  if (vec_dt(dtype, a.M, a.C, {{a.z, a.ldz}, {a.res, a.ldres}, {a.y, a.ldy}}))
+    XP_VEC_LAUNCH(k_bn_apply_v, (int64_t)a.M * (a.C / vn(dtype)), vn(dtype) * (dtype == DT_BF16 ? 2 : 4) * (a.res ? 3 : 2), a);
+  return launch_bn_apply_s(dtype, a, s);
+}
+
+hipError_t launch_bn_bwd(int dtype, const BnBwdArgs& a, hipStream_t s) {
+  if (a.M <= 0 || a.C <= 0) return hipSuccess;
+  if (vec_dt(dtype, a.M, a.C, {{a.g, a.ldg}, {a.z, a.ldz}, {a.dz, a.lddz}, {a.dzmask, a.ldzm},
+                               {a.dres, a.lddres}, {a.resmask, a.ldrm}}))
+    XP_VEC_LAUNCH(k_bn_bwd_v, (int64_t)a.M * (a.C / vn(dtype)), vn(dtype) * (dtype == DT_BF16 ? 2 : 4) * (3 + (a.dres ? 2 : 0) + (a.dz_accumulate ? 1 : 0)), a);
+  return launch_bn_bwd_s(dtype, a, s);
+}
+
+hipError_t launch_elementwise(int dtype, const EltArgs& a, hipStream_t s) {
+  if (a.M <= 0 || a.C <= 0) return hipSuccess;
+  if (vec_dt(dtype, a.M, a.C, {{a.a, a.lda}, {a.b, a.ldb}, {a.mask, a.ldm}, {a.y, a.ldy}}))
+    XP_VEC_LAUNCH(k_elt_v, (int64_t)a.M * (a.C / vn(dtype)), vn(dtype) * (dtype == DT_BF16 ? 2 : 4) * (2 + (a.b ? 1 : 0) + (a.mask ? 1 : 0) + (a.accumulate ? 1 : 0)), a);
+  return launch_elementwise_s(dtype, a, s);
+}
+
+hipError_t launch_maxpool_fwd(int dtype, const PoolArgs& a, hipStream_t s) {
+  int64_t rows = (int64_t)a.nb * (a.H / 2) * (a.W / 2);
+  if (rows <= 0 || a.C <= 0) return hipSuccess;
+  if (vec_dt(dtype, (int64_t)a.nb * a.H * a.W, a.C, {{a.x, a.ldx}, {a.out, a.ldo}}))
+    XP_VEC_LAUNCH(k_maxpool_fwd_v, rows * (a.C / vn(dtype)), vn(dtype) * (dtype == DT_BF16 ? 2 : 4) * 5, a);
+  return launch_maxpool_fwd_s(dtype, a, s);
+}
+
+hipError_t launch_maxpool_bwd(int dtype, const PoolArgs& a, hipStream_t s) {
+  int64_t rows = (int64_t)a.nb * a.H * a.W;
+  if (rows <= 0 || a.C <= 0) return hipSuccess;
+  if (vec_dt(dtype, rows, a.C, {{a.x, a.ldx}, {a.dy, a.lddy}, {a.mask, a.ldm}, {a.out, a.ldo}}))
+    XP_VEC_LAUNCH(k_maxpool_bwd_v, rows * (a.C / vn(dtype)), vn(dtype) * (dtype == DT_BF16 ? 2 : 4) * (2.25 + (a.mask ? 1 : 0) + (a.accumulate ? 1 : 0)), a);
+  return launch_maxpool_bwd_s(dtype, a, s);
+}
+
+hipError_t launch_avgpool_fwd(int dtype, const PoolArgs& a, hipStream_t s) {
+  int64_t rows = (int64_t)a.nb * a.H * a.W;
+  if (rows <= 0 || a.C <= 0) return hipSuccess;
+  if (vec_dt(dtype, rows, a.C, {{a.x, a.ldx}, {a.mask, a.ldm}, {a.out, a.ldo}})) {
+    if (dtype == DT_BF16)
+      XP_LAUNCH("k_avgpool3_v<bf16>", (double)rows * a.C * 2 * (a.accumulate ? 3 : 2), k_avgpool3_v<bf16_t>,
+                dim3(grid_for(rows * (a.C / 8))), dim3(256), 0, s, a,
+                         (const bf16_t*)a.x, a.ldx);
+    else
+      XP_LAUNCH("k_avgpool3_v<f32>", (double)rows * a.C * 4 * (a.accumulate ? 3 : 2), k_avgpool3_v<float>,
+                dim3(grid_for(rows * (a.C / 4))), dim3(256), 0, s, a,
+                         (const float*)a.x, a.ldx);
+    return hipGetLastError();
+  }
+  return launch_avgpool_fwd_s(dtype, a, s);
+}
+
+hipError_t launch_avgpool_bwd(int dtype, const PoolArgs& a, hipStream_t s) {
+  int64_t rows = (int64_t)a.nb * a.H * a.W;
+  if (rows <= 0 || a.C <= 0) return hipSuccess;
+  if (vec_dt(dtype, rows, a.C, {{a.dy, a.lddy}, {a.mask, a.ldm}, {a.out, a.ldo}})) {
+    if (dtype == DT_BF16)
+      XP_LAUNCH("k_avgpool3_v<bf16>", (double)rows * a.C * 2 * (a.accumulate ? 3 : 2), k_avgpool3_v<bf16_t>,
+                dim3(grid_for(rows * (a.C / 8))), dim3(256), 0, s, a,
+                         (const bf16_t*)a.dy, a.lddy);
+    else
+      XP_LAUNCH("k_avgpool3_v<f32>", (double)rows * a.C * 4 * (a.accumulate ? 3 : 2), k_avgpool3_v<float>,
+                dim3(grid_for(rows * (a.C / 4))), dim3(256), 0, s, a,
+                         (const float*)a.dy, a.lddy);
+    return hipGetLastError();
+  }
+  return launch_avgpool_bwd_s(dtype, a, s);
+}
+
+hipError_t launch_gap_fwd(int dtype, const PoolArgs& a, hipStream_t s) {
+  if (a.nb <= 0 || a.C <= 0) return hipSuccess;
+  if (vec_dt(dtype, (int64_t)a.nb * a.H * a.W, a.C, {{a.x, a.ldx}, {a.out, a.ldo}})) {
+    int chunks = a.C / vn(dtype);
+    int CL = chunks < 512 ? chunks : 512;
+    dim3 grid(ceil_div(chunks, CL), a.nb);
+    double gb = (double)a.nb * a.H * a.W * a.C * (dtype == DT_BF16 ? 2 : 4);
+    if (dtype == DT_BF16) XP_LAUNCH("k_gap_fwd_v<bf16>", gb, k_gap_fwd_v<bf16_t>, grid, dim3(512), 0, s, a);
+    else XP_LAUNCH("k_gap_fwd_v<f32>", gb, k_gap_fwd_v<float>, grid, dim3(512), 0, s, a);
+    return hipGetLastError();
+  }
+  return launch_gap_fwd_s(dtype, a, s);
+}
+
+hipError_t launch_gap_bwd(int dtype, const PoolArgs& a, hipStream_t s) {
+  int64_t rows = (int64_t)a.nb * a.H * a.W;
+  if (rows <= 0 || a.C <= 0) return hipSuccess;
+  if (vec_dt(dtype, rows, a.C, {{a.dy, a.lddy}, {a.mask, a.ldm}, {a.out, a.ldo}}))
+    XP_VEC_LAUNCH(k_gap_bwd_v, rows * (a.C / vn(dtype)), vn(dtype) * (dtype == DT_BF16 ? 2 : 4) * (1 + (a.mask ? 1 : 0) + (a.accumulate ? 1 : 0)), a);
+  return launch_gap_bwd_s(dtype, a, s);
 }
 
 }  // namespace xp

@@ -24,6 +24,8 @@
 #include "xp_device.h"
 #include "xp_kernels.h"
 
+#include <cstdio>
+
 namespace xp {
 
 template <typename T> struct MT;
@@ -509,14 +511,33 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
       }
 }
 
+// grad[i] += sum over splits of part[z][i], splits added in order z = 0, 1, ...;
+// each thread owns four consecutive outputs so the partial reads are 16-32 B
 template <typename P>
 __global__ __launch_bounds__(256) void k_split_reduce(const P* __restrict__ part, int splits,
                                                        int64_t count, float* __restrict__ grad) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    double s = 0.0;
-    for (int z = 0; z < splits; ++z) s += (double)part[(size_t)z * count + i];
-    grad[i] = (float)((double)grad[i] + s);
+  const int64_t q = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (q >= count) return;
+  if (q + 4 <= count) {
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+#pragma unroll 4
+    for (int z = 0; z < splits; ++z) {
+      const P* p = part + (size_t)z * count + q;
+      s0 += (double)p[0];
+      s1 += (double)p[1];
+      s2 += (double)p[2];
+      s3 += (double)p[3];
+    }
+    grad[q] = (float)((double)grad[q] + s0);
+    grad[q + 1] = (float)((double)grad[q + 1] + s1);
+    grad[q + 2] = (float)((double)grad[q + 2] + s2);
+    grad[q + 3] = (float)((double)grad[q + 3] + s3);
+  } else {
+    for (int64_t i = q; i < count; ++i) {
+      double s = 0.0;
+      for (int z = 0; z < splits; ++z) s += (double)part[(size_t)z * count + i];
+      grad[i] = (float)((double)grad[i] + s);
+    }
   }
 }
 
@@ -549,14 +570,31 @@ static int pick_bn(int N) {
   return best;
 }
 
+template <typename T> static const char* tname() { return sizeof(T) == 2 ? "bf16" : "f32"; }
+
+template <typename T, int BM, int BN, int WM, int WN, bool FLAT>
+static const char* kname(const char* base) {
+  static char buf[96];
+  static bool init = false;
+  if (!init) {
+    snprintf(buf, sizeof buf, "%s<%s,%d,%d,%d,%d,%s>", base, tname<T>(), BM, BN, WM, WN,
+             FLAT ? "true" : "false");
+    init = true;
+  }
+  return buf;
+}
+
 template <typename T, int BM, int BN, int WM, int WN>
 static hipError_t conv_go(const ConvArgs& a, bool flat, hipStream_t s) {
   int M = a.nb * a.H * a.W;
   dim3 grid((M + BM - 1) / BM, (a.N + BN - 1) / BN);
+  double flops = 2.0 * M * (double)a.N * a.R * a.S * a.C;
   if (flat)
-    hipLaunchKernelGGL((k_conv_gemm<T, BM, BN, WM, WN, true>), grid, dim3(256), 0, s, a);
+    XP_LAUNCH((kname<T, BM, BN, WM, WN, true>("k_conv_gemm")), flops,
+              (k_conv_gemm<T, BM, BN, WM, WN, true>), grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((k_conv_gemm<T, BM, BN, WM, WN, false>), grid, dim3(256), 0, s, a);
+    XP_LAUNCH((kname<T, BM, BN, WM, WN, false>("k_conv_gemm")), flops,
+              (k_conv_gemm<T, BM, BN, WM, WN, false>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -590,9 +628,15 @@ int wgrad_pick_splits(int M, int N, int K) {
   int bm = N <= 64 ? 64 : 128;
   int bn = K <= 64 ? 64 : 128;
   int tiles = ((N + bm - 1) / bm) * ((K + bn - 1) / bn);
-  int want = (512 + tiles - 1) / tiles;
-  int maxs = (M + 127) / 128;  // keep at least ~128 pixels per split
+  int want = (512 + tiles - 1) / tiles;      // about two workgroups per CU
+  int maxs = (M + 255) / 256;                // at least ~256 pixels per split
+  // keep the partial sums (written and read back once) below the operands' bytes
+  int64_t op_bytes = (int64_t)M * (N + K / 1) * 2;
+  int64_t part_bytes = (int64_t)N * K * 4;
+  int64_t maxb = part_bytes > 0 ? op_bytes / part_bytes : want;
+  if (maxb < 4) maxb = 4;
   if (want > maxs) want = maxs;
+  if (want > maxb) want = (int)maxb;
   if (want < 1) want = 1;
   return want;
 }
@@ -605,17 +649,21 @@ template <typename T, int BM, int BN, int WM, int WN>
 static hipError_t wgrad_go(const WgradArgs& a, bool flat, hipStream_t s) {
   int K = a.R * a.S * a.C;
   dim3 grid((a.N + BM - 1) / BM, (K + BN - 1) / BN, a.splits);
+  double flops = 2.0 * a.nb * a.H * a.W * (double)a.N * K;
   if (flat)
-    hipLaunchKernelGGL((k_wgrad<T, BM, BN, WM, WN, true>), grid, dim3(256), 0, s, a);
+    XP_LAUNCH((kname<T, BM, BN, WM, WN, true>("k_wgrad")), flops, (k_wgrad<T, BM, BN, WM, WN, true>),
+              grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((k_wgrad<T, BM, BN, WM, WN, false>), grid, dim3(256), 0, s, a);
+    XP_LAUNCH((kname<T, BM, BN, WM, WN, false>("k_wgrad")), flops, (k_wgrad<T, BM, BN, WM, WN, false>),
+              grid, dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   int64_t count = (int64_t)a.N * K;
-  int blocks = (int)((count + 255) / 256);
-  if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(k_split_reduce<typename MT<T>::part_t>, dim3(blocks), dim3(256), 0, s,
-                     (const typename MT<T>::part_t*)a.part, a.splits, count, a.grad);
+  int blocks = (int)(((count + 3) / 4 + 255) / 256);
+  typedef typename MT<T>::part_t P;
+  XP_LAUNCH(sizeof(P) == 4 ? "k_split_reduce<float>" : "k_split_reduce<double>",
+            (double)count * (a.splits * sizeof(P) + 8), k_split_reduce<P>, dim3(blocks), dim3(256), 0, s,
+            (const P*)a.part, a.splits, count, a.grad);
   return hipGetLastError();
 }
 
@@ -644,11 +692,11 @@ hipError_t launch_flip_weights(int dtype, const void* w, void* wd, int N, int R,
   if (blocks > 4096) blocks = 4096;
   if (total <= 0) return hipSuccess;
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(k_flip<bf16_t>, dim3(blocks), dim3(256), 0, s, (const bf16_t*)w,
-                       (bf16_t*)wd, N, R, S, C);
+    XP_LAUNCH("k_flip<bf16>", (double)total * 4, k_flip<bf16_t>, dim3(blocks), dim3(256), 0, s,
+              (const bf16_t*)w, (bf16_t*)wd, N, R, S, C);
   else
-    hipLaunchKernelGGL(k_flip<float>, dim3(blocks), dim3(256), 0, s, (const float*)w,
-                       (float*)wd, N, R, S, C);
+    XP_LAUNCH("k_flip<f32>", (double)total * 8, k_flip<float>, dim3(blocks), dim3(256), 0, s,
+              (const float*)w, (float*)wd, N, R, S, C);
   return hipGetLastError();
 }
 

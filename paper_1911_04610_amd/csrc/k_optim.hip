@@ -11,6 +11,8 @@
 
 namespace xp {
 
+thread_local LaunchHook* g_hook = nullptr;
+
 XP_DEV double pred_dir(double m, double v, const PredCoef& c) {
   double mh = m * c.c1, vh = v * c.c2;
   return c.eps_outside ? mh / (sqrt(vh) + c.eps) : mh / sqrt(vh + c.eps);
@@ -173,7 +175,8 @@ static int stream_grid(int64_t n) {
 hipError_t launch_predict(const float* W, const float* m, const float* v, float* out,
                           bf16_t* out_bf, int64_t n, const PredCoef& c, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_predict, dim3(stream_grid(n)), dim3(256), 0, s, W, m, v, out, out_bf, n, c);
+  XP_LAUNCH("k_predict", (double)n * (out_bf ? 18 : 16), k_predict, dim3(stream_grid(n)), dim3(256), 0, s,
+            W, m, v, out, out_bf, n, c);
   return hipGetLastError();
 }
 
@@ -181,8 +184,10 @@ hipError_t launch_adam(float* W, float* m, float* v, float* G, int64_t n, const 
                        int zero_grad, float* pf, bf16_t* pf_bf, const PredCoef& cf, float* pb,
                        bf16_t* pb_bf, const PredCoef& cb, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_adam, dim3(stream_grid(n)), dim3(256), 0, s, W, m, v, G, n, a, zero_grad,
-                     pf, pf_bf, cf, pb, pb_bf, cb);
+  double bytes = (double)n * (28 + (zero_grad ? 4 : 0) + (pf ? 4 : 0) + (pb ? 4 : 0) +
+                              (pf_bf ? 2 : 0) + (pb_bf ? 2 : 0));
+  XP_LAUNCH("k_adam", bytes, k_adam, dim3(stream_grid(n)), dim3(256), 0, s, W, m, v, G, n, a, zero_grad,
+            pf, pf_bf, cf, pb, pb_bf, cb);
   return hipGetLastError();
 }
 

@@ -20,6 +20,8 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <iterator>
+#include <map>
 #include <new>
 #include <string>
 #include <vector>
@@ -93,8 +95,13 @@ struct ParamT {
 
 struct TimeRec {
   hipEvent_t a, b;
-  int cls;
+  const char* name;
   double work;
+};
+
+struct TimeAgg {
+  double ms = 0, work = 0;
+  int64_t n = 0;
 };
 
 }  // namespace
@@ -121,13 +128,17 @@ struct xpipe_stage {
   bool pred_valid[2] = {false, false};
   bool wd_valid = false;
   int64_t bwd_since_step = 0;
-  // timing
+  // timing: hipEvents around every launch, aggregated per kernel
+  struct Hook : xp::LaunchHook {
+    xpipe_stage* st = nullptr;
+    hipEvent_t a = nullptr;
+    void before() override;
+    void after(const char* name, double work) override;
+  } hook;
   bool timing = false;
   std::vector<TimeRec> pending;
   std::vector<hipEvent_t> pool;
-  double t_ms[4] = {0, 0, 0, 0};
-  double t_work[4] = {0, 0, 0, 0};
-  int64_t t_n[4] = {0, 0, 0, 0};
+  std::map<std::string, TimeAgg> agg;
 
   size_t esz() const { return dtype == DT_BF16 ? 2 : 4; }
 };
@@ -521,29 +532,32 @@ hipEvent_t take_event(xpipe_stage* st) {
   return e;
 }
 
-// brackets a launch with events when timing is on
-struct Timed {
-  xpipe_stage* st;
-  int cls;
-  double work;
-  hipEvent_t a = nullptr;
-  Timed(xpipe_stage* s, int c, double w) : st(s), cls(c), work(w) {
-    if (st->timing) {
-      a = take_event(st);
-      if (a) (void)hipEventRecord(a, st->stream);
-    }
+}  // namespace
+
+void xpipe_stage::Hook::before() {
+  a = take_event(st);
+  if (a) (void)hipEventRecord(a, st->stream);
+}
+
+void xpipe_stage::Hook::after(const char* name, double work) {
+  if (!a) return;
+  hipEvent_t b = take_event(st);
+  if (!b) {
+    st->pool.push_back(a);
+    a = nullptr;
+    return;
   }
-  ~Timed() {
-    if (st->timing && a) {
-      hipEvent_t b = take_event(st);
-      if (b) {
-        (void)hipEventRecord(b, st->stream);
-        st->pending.push_back(TimeRec{a, b, cls, work});
-      } else {
-        st->pool.push_back(a);
-      }
-    }
-  }
+  (void)hipEventRecord(b, st->stream);
+  st->pending.push_back(TimeRec{a, b, name, work});
+  a = nullptr;
+}
+
+namespace {
+
+// installs the stage's launch observer for the duration of one ABI call
+struct HookScope {
+  HookScope(xpipe_stage* st) { xp::g_hook = st->timing ? &st->hook : nullptr; }
+  ~HookScope() { xp::g_hook = nullptr; }
 };
 
 const void* gemm_weights(xpipe_stage* st, const Op& op, int dir) {
@@ -588,7 +602,6 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         a.R = a.S = op.k;
         a.pad = op.k / 2;
         a.relu = op.relu;
-        Timed tm(st, 0, gemm_flops(tin, op));
         XP_HIP(launch_conv_gemm(dt, a, s));
         break;
       }
@@ -606,7 +619,6 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         ca.out1 = stats + tin.sh.C;
         ca.eps = BN_EPS;
         {
-          Timed tm(st, 3, (double)tin.sh.elems() * st->esz());
           XP_HIP(launch_colreduce(dt, ca, s));
         }
         View y = act(st, op.out, c);
@@ -627,7 +639,6 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         b.M = ca.M;
         b.C = ca.C;
         b.relu = op.relu;
-        Timed tm(st, 3, (double)tin.sh.elems() * st->esz() * (op.in2 >= 0 ? 3 : 2));
         XP_HIP(launch_bn_apply(dt, b, s));
         break;
       }
@@ -646,7 +657,6 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         e.M = (int)tin.sh.rows();
         e.C = tin.sh.C;
         e.relu = op.relu;
-        Timed tm(st, 3, (double)tin.sh.elems() * st->esz() * (op.in2 >= 0 ? 3 : 2));
         XP_HIP(launch_elementwise(dt, e, s));
         break;
       }
@@ -663,7 +673,6 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         pa.H = tin.sh.H;
         pa.W = tin.sh.W;
         pa.C = tin.sh.C;
-        Timed tm(st, 3, (double)(tin.sh.elems() + st->tensors[op.out].sh.elems()) * st->esz());
         if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_fwd(dt, pa, s));
         else if (op.kind == OP_AVGPOOL) XP_HIP(launch_avgpool_fwd(dt, pa, s));
         else XP_HIP(launch_gap_fwd(dt, pa, s));
@@ -681,7 +690,6 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         ce.classes = st->classes;
         ce.inv_N = 1.0 / ((double)st->T * st->mb);
         ce.loss = loss;
-        Timed tm(st, 3, (double)tin.sh.elems() * st->esz());
         XP_HIP(launch_softmax_ce(dt, ce, s));
         break;
       }
@@ -719,7 +727,6 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
     e.ldy = g.ld;
     e.M = (int)to.sh.rows();
     e.C = to.sh.C;
-    Timed tm(st, 3, (double)to.sh.elems() * esz * 2);
     XP_HIP(launch_elementwise(dt, e, s));
   }
 
@@ -739,7 +746,6 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         ce.inv_N = 1.0 / ((double)st->T * st->mb);
         ce.dz = g.p;
         ce.lddz = g.ld;
-        Timed tm(st, 3, (double)tin.sh.elems() * esz * 2);
         XP_HIP(launch_softmax_ce(dt, ce, s));
         break;
       }
@@ -764,7 +770,6 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         w.pad = op.k / 2;
         w.splits = wgrad_pick_splits(M, op.cout, K);
         {
-          Timed tm(st, 1, gemm_flops(tin, op));
           XP_HIP(launch_wgrad(dt, w, s));
         }
         if (op.b_off >= 0) {
@@ -777,7 +782,6 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
           ca.partial = (double*)(st->ws + st->colpart_off);
           ca.row_blocks = col_row_blocks(M, op.cout);
           ca.grad0 = st->grad + op.b_off;
-          Timed tm(st, 3, (double)M * op.cout * esz);
           XP_HIP(launch_colreduce(dt, ca, s));
         }
         if (want_grad(op.in)) {
@@ -797,7 +801,6 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
           a.R = a.S = op.k;
           a.pad = op.k / 2;
           a.accumulate = op.in_acc;
-          Timed tm(st, 0, gemm_flops(tin, op));
           XP_HIP(launch_conv_gemm(dt, a, s));
         }
         break;
@@ -823,7 +826,6 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         ca.grad0 = st->grad + op.g_off;
         ca.grad1 = st->grad + op.be_off;
         {
-          Timed tm(st, 3, (double)tin.sh.elems() * esz * 2);
           XP_HIP(launch_colreduce(dt, ca, s));
         }
         BnBwdArgs b{};
@@ -865,12 +867,10 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
             e.M = M;
             e.C = C;
             e.accumulate = b.res_accumulate;
-            Timed tm(st, 3, (double)tin.sh.elems() * esz * 3);
             XP_HIP(launch_elementwise(dt, e, s));
           }
           break;
         }
-        Timed tm(st, 3, (double)tin.sh.elems() * esz * (b.dres ? 5 : 3));
         XP_HIP(launch_bn_bwd(dt, b, s));
         break;
       }
@@ -890,7 +890,6 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
           e.M = (int)tin.sh.rows();
           e.C = tin.sh.C;
           e.accumulate = accs[q];
-          Timed tm(st, 3, (double)tin.sh.elems() * esz * 3);
           XP_HIP(launch_elementwise(dt, e, s));
         }
         break;
@@ -914,7 +913,6 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         pa.H = tin.sh.H;
         pa.W = tin.sh.W;
         pa.C = tin.sh.C;
-        Timed tm(st, 3, (double)tin.sh.elems() * esz * 3);
         if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_bwd(dt, pa, s));
         else if (op.kind == OP_AVGPOOL) XP_HIP(launch_avgpool_bwd(dt, pa, s));
         else XP_HIP(launch_gap_bwd(dt, pa, s));
@@ -970,7 +968,6 @@ AdamCoef adam_coef(const xpipe_hparams* hp) {
 xpipe_status refresh_flipped(xpipe_stage* st) {
   for (const Op& op : st->ops) {
     if (op.kind != OP_GEMM) continue;
-    Timed tm(st, 3, (double)op.cout * op.k * op.k * op.cin * st->esz() * 2);
     XP_HIP(launch_flip_weights(st->dtype, gemm_weights(st, op, XPIPE_BWD), st->ws + op.wd_off,
                                op.cout, op.k, op.k, op.cin, st->stream));
   }
@@ -1075,6 +1072,7 @@ xpipe_status xpipe_stage_create(const xpipe_layer_desc* layers, int32_t n_layers
   st->bf_b_off = p.bf_b_off;
   st->colpart_off = p.colpart_off;
   st->wpart_off = p.wpart_off;
+  st->hook.st = st;
   hipError_t e = p.P > 0 ? hipMemsetAsync(grad, 0, (size_t)p.P * sizeof(float), st->stream)
                          : hipSuccess;
   if (e != hipSuccess) {
@@ -1115,12 +1113,12 @@ xpipe_status xpipe_predict_weights(xpipe_stage_t st, int32_t which, int32_t s, c
   if (s < 0) return fail(XPIPE_EINVAL, "version difference must be >= 0");
   xpipe_status hs = check_hp(hp);
   if (hs != XPIPE_OK) return hs;
+  HookScope hs_(st);
   PredCoef c = pred_coef(hp, hp->t, s);
   float* out = which == XPIPE_FWD ? st->wpf : st->wpb;
   bf16_t* obf = nullptr;
   if (st->dtype == DT_BF16) obf = (bf16_t*)(st->ws + (which == XPIPE_FWD ? st->bf_f_off : st->bf_b_off));
   {
-    Timed tm(st, 2, (double)st->P * (obf ? 18 : 16));
     XP_HIP(launch_predict(st->W, st->m, st->v, out, obf, st->P, c, st->stream));
   }
   st->pred_valid[which] = true;
@@ -1136,6 +1134,7 @@ xpipe_status xpipe_stage_fwd(xpipe_stage_t st, const void* x, void* y, const int
   if (!x || !y) return fail(XPIPE_EINVAL, "null input or output");
   if (st->has_loss && loss && !labels) return fail(XPIPE_EINVAL, "labels required for the loss");
   if (!st->pred_valid[XPIPE_FWD]) return fail(XPIPE_ESTATE, "no forward prediction: call xpipe_predict_weights(FWD) first");
+  HookScope hs_(st);
   Ctx c;
   c.x = x;
   c.y = y;
@@ -1149,6 +1148,7 @@ xpipe_status xpipe_stage_bwd(xpipe_stage_t st, const void* x, const void* dy, co
   if (!st->has_loss && !dy) return fail(XPIPE_EINVAL, "dy required for a stage without a loss");
   if (!st->pred_valid[XPIPE_BWD] || !st->wd_valid)
     return fail(XPIPE_ESTATE, "no backward prediction: call xpipe_predict_weights(BWD) first");
+  HookScope hs_(st);
   Ctx c;
   c.x = x;
   c.dx = dx;
@@ -1167,6 +1167,7 @@ xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t 
   if (hs != XPIPE_OK) return hs;
   if (emit_pred && (s_fwd_next < 0 || s_bwd_next < 0)) return fail(XPIPE_EINVAL, "version difference must be >= 0");
   if (st->bwd_since_step == 0) return fail(XPIPE_ESTATE, "no backward since the last update");
+  HookScope hs_(st);
   AdamCoef a = adam_coef(hp);
   PredCoef cf = pred_coef(hp, hp->t + 1, s_fwd_next);
   PredCoef cb = pred_coef(hp, hp->t + 1, s_bwd_next);
@@ -1177,7 +1178,6 @@ xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t 
     fb = (bf16_t*)(st->ws + st->bf_b_off);
   }
   {
-    Timed tm(st, 2, (double)st->P * (emit_pred ? (ff ? 44 : 40) : 32));
     XP_HIP(launch_adam(st->W, st->m, st->v, st->grad, st->P, a, 1, emit_pred ? st->wpf : nullptr, ff, cf,
                        emit_pred ? st->wpb : nullptr, fb, cb, st->stream));
   }
@@ -1234,11 +1234,7 @@ xpipe_status xpipe_adam_flat(float* W, float* m, float* v, float* G, int64_t n, 
 xpipe_status xpipe_stage_set_timing(xpipe_stage_t st, int32_t enable) {
   if (!st) return fail(XPIPE_EINVAL, "null stage");
   st->timing = enable != 0;
-  for (int i = 0; i < 4; ++i) {
-    st->t_ms[i] = 0;
-    st->t_work[i] = 0;
-    st->t_n[i] = 0;
-  }
+  st->agg.clear();
   for (auto& r : st->pending) {
     st->pool.push_back(r.a);
     st->pool.push_back(r.b);
@@ -1247,25 +1243,44 @@ xpipe_status xpipe_stage_set_timing(xpipe_stage_t st, int32_t enable) {
   return XPIPE_OK;
 }
 
-xpipe_status xpipe_stage_timing(xpipe_stage_t st, int32_t cls, double* ms, int64_t* launches, double* work) {
-  if (!st || !ms || !launches || !work) return fail(XPIPE_EINVAL, "null argument");
-  if (cls < 0 || cls > 3) return fail(XPIPE_EINVAL, "bad kernel class");
+static xpipe_status drain_timing(xpipe_stage* st) {
   for (auto& r : st->pending) {
     float e = 0.f;
     hipError_t err = hipEventSynchronize(r.b);
     if (err != hipSuccess) return fail(XPIPE_EHIP, std::string("hipEventSynchronize: ") + hipGetErrorString(err));
     err = hipEventElapsedTime(&e, r.a, r.b);
     if (err != hipSuccess) return fail(XPIPE_EHIP, std::string("hipEventElapsedTime: ") + hipGetErrorString(err));
-    st->t_ms[r.cls] += e;
-    st->t_work[r.cls] += r.work;
-    st->t_n[r.cls] += 1;
+    TimeAgg& g = st->agg[r.name];
+    g.ms += e;
+    g.work += r.work;
+    g.n += 1;
     st->pool.push_back(r.a);
     st->pool.push_back(r.b);
   }
   st->pending.clear();
-  *ms = st->t_ms[cls];
-  *launches = st->t_n[cls];
-  *work = st->t_work[cls];
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_timing_count(xpipe_stage_t st, int32_t* n) {
+  if (!st || !n) return fail(XPIPE_EINVAL, "null argument");
+  xpipe_status s = drain_timing(st);
+  if (s != XPIPE_OK) return s;
+  *n = (int32_t)st->agg.size();
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_timing_entry(xpipe_stage_t st, int32_t i, const char** kernel, double* ms,
+                                      int64_t* launches, double* work) {
+  if (!st || !kernel || !ms || !launches || !work) return fail(XPIPE_EINVAL, "null argument");
+  xpipe_status s = drain_timing(st);
+  if (s != XPIPE_OK) return s;
+  if (i < 0 || i >= (int32_t)st->agg.size()) return fail(XPIPE_EINVAL, "timing entry out of range");
+  auto it = st->agg.begin();
+  std::advance(it, i);
+  *kernel = it->first.c_str();
+  *ms = it->second.ms;
+  *launches = it->second.n;
+  *work = it->second.work;
   return XPIPE_OK;
 }
 

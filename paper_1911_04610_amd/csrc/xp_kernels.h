@@ -12,6 +12,24 @@ typedef uint16_t bf16_t;
 
 enum Dtype { DT_F32 = 0, DT_BF16 = 1 };
 
+// Optional per-launch observer (kernel timing).  Every launch goes through
+// XP_LAUNCH, which calls before() / after(name, work) around it when a hook is
+// installed for the calling thread.  work = algorithmic flops for GEMM
+// kernels, algorithmic bytes for the others.
+struct LaunchHook {
+  virtual void before() = 0;
+  virtual void after(const char* name, double work) = 0;
+  virtual ~LaunchHook() {}
+};
+extern thread_local LaunchHook* g_hook;
+
+#define XP_LAUNCH(NAME, WORK, KERNEL, GRID, BLOCK, SHM, STREAM, ...)   \
+  do {                                                                  \
+    if (::xp::g_hook) ::xp::g_hook->before();                           \
+    hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHM, STREAM, __VA_ARGS__);  \
+    if (::xp::g_hook) ::xp::g_hook->after(NAME, WORK);                  \
+  } while (0)
+
 // ---------------------------------------------------------------- prediction / Adam
 struct PredCoef {
   double coef;      // s * lr (0 for the identity)

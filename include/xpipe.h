@@ -135,8 +135,10 @@ xpipe_status xpipe_stage_query(const xpipe_layer_desc* layers, int32_t n_layers,
  * 64-element-aligned offset, padding zero).  workspace is caller-owned device
  * memory of at least the queried size, 256-byte aligned.  T >= 1 is the
  * number of micro-batches per mini-batch.  hip_stream is a hipStream_t (NULL
- * = default stream).  grad is zeroed on the stream.  Nothing is predicted
- * yet: call xpipe_predict_weights before the first forward. */
+ * = default stream).  grad is zeroed on the stream.  The workspace belongs
+ * to the stage until destroy, and calls on one stage must not overlap in time
+ * (they share it), which one stream guarantees.  Nothing is predicted yet:
+ * call xpipe_predict_weights before the first forward. */
 xpipe_status xpipe_stage_create(const xpipe_layer_desc* layers, int32_t n_layers,
                                 int32_t micro_batch, int32_t T, int32_t H, int32_t W, int32_t C,
                                 int32_t dtype, void* hip_stream,

@@ -11,6 +11,7 @@
 #include "xp_device.h"
 #include "xp_kernels.h"
 
+#include <algorithm>
 #include <initializer_list>
 #include <utility>
 
@@ -29,9 +30,11 @@ static int row_blocks_for(int M, int C) {
 
 int col_row_blocks(int M, int C) { return row_blocks_for(M, C); }
 int col_row_blocks_v(int M, int C, int N);
+// the vectorised reduction uses at most this many row blocks
+constexpr int COL_MAX_ROW_BLOCKS_V = 1024;
 size_t col_partial_bytes(int M, int C) {
   int rb = row_blocks_for(M, C);
-  if (rb < 128) rb = 128;  // the vectorised reduction uses at most 128 row blocks
+  if (rb < COL_MAX_ROW_BLOCKS_V) rb = COL_MAX_ROW_BLOCKS_V;
   return (size_t)rb * 2 * C * sizeof(double);
 }
 
@@ -71,12 +74,12 @@ __global__ __launch_bounds__(256) void k_colpart(ColArgs a) {
   if (rg == 0 && col < a.C) {
     double t0 = ((sh[0][0][lanec] + sh[0][1][lanec]) + sh[0][2][lanec]) + sh[0][3][lanec];
     double t1 = ((sh[1][0][lanec] + sh[1][1][lanec]) + sh[1][2][lanec]) + sh[1][3][lanec];
-    a.partial[((size_t)blockIdx.y * 2 + 0) * a.C + col] = t0;
-    a.partial[((size_t)blockIdx.y * 2 + 1) * a.C + col] = t1;
+    a.partial[((size_t)col * 2 + 0) * a.row_blocks + blockIdx.y] = t0;
+    a.partial[((size_t)col * 2 + 1) * a.row_blocks + blockIdx.y] = t1;
   }
 }
 
-__global__ void k_colfinal_v(ColArgs a);
+hipError_t launch_colfinal(const ColArgs& a, hipStream_t s);
 
 template <typename T>
 static hipError_t colreduce_go(const ColArgs& a, hipStream_t s) {
@@ -85,9 +88,7 @@ static hipError_t colreduce_go(const ColArgs& a, hipStream_t s) {
             dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  XP_LAUNCH("k_colfinal", (double)a.row_blocks * 2 * a.C * 8, k_colfinal_v, dim3(ceil_div(a.C, 64)),
-            dim3(256), 0, s, a);
-  return hipGetLastError();
+  return launch_colfinal(a, s);
 }
 
 static hipError_t launch_colreduce_s(int dtype, const ColArgs& a, hipStream_t s) {
@@ -461,6 +462,20 @@ XP_DEV void vmask(const T* mk, double* v) {
 }
 
 // ---------------------------------------------------------------- column reductions
+// the finished column sums of one column, by mode
+XP_DEV void col_finish_one(const ColArgs& a, int col, double s0, double s1) {
+  if (a.mode == COL_STATS) {
+    bn_stats_from_sums(s0, s1, a.M, a.eps, a.out0 + col, a.out1 + col);
+  } else if (a.mode == COL_BNBWD) {
+    a.out0[col] = s0;
+    a.out1[col] = s1;
+    a.grad0[col] = (float)((double)a.grad0[col] + s1);
+    a.grad1[col] = (float)((double)a.grad1[col] + s0);
+  } else {
+    a.grad0[col] = (float)((double)a.grad0[col] + s0);
+  }
+}
+
 // Block: CL chunk-lanes x RG row groups; partials per (row block, column);
 // the row groups of a block are added in a fixed order in LDS.
 template <typename T>
@@ -486,7 +501,7 @@ __global__ __launch_bounds__(256) void k_colpart_v(ColArgs a) {
 #pragma unroll
       for (int e = 0; e < N; ++e) { mu[e] = a.mean[c0 + e]; rs[e] = a.rstd[c0 + e]; }
     }
-#pragma unroll 2
+#pragma unroll 4
     for (int r = r0 + g; r < r1; r += RG) {
       double v[N];
       vld(A + (size_t)r * a.lda + c0, v);
@@ -517,45 +532,44 @@ __global__ __launch_bounds__(256) void k_colpart_v(ColArgs a) {
     const int c0 = chunk * N;
 #pragma unroll
     for (int e = 0; e < N; ++e) {
-      a.partial[((size_t)blockIdx.y * 2 + 0) * a.C + c0 + e] = t0[e];
-      a.partial[((size_t)blockIdx.y * 2 + 1) * a.C + c0 + e] = t1[e];
+      a.partial[((size_t)(c0 + e) * 2 + 0) * a.row_blocks + blockIdx.y] = t0[e];
+      a.partial[((size_t)(c0 + e) * 2 + 1) * a.row_blocks + blockIdx.y] = t1[e];
     }
   }
 }
 
-// finalize: 64 columns x 4 row-block groups per workgroup, fixed-order sums
+// finalize: one workgroup per column; the partials of a column are contiguous,
+// each thread adds a fixed stride of them, then the waves and the block add in
+// a fixed order
 __global__ __launch_bounds__(256) void k_colfinal_v(ColArgs a) {
-  __shared__ double sh[2][4][64];
-  const int lc = threadIdx.x & 63, g = threadIdx.x >> 6;
-  const int col = blockIdx.x * 64 + lc;
+  __shared__ double sh[2][4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = blockIdx.x;
+  const double* p0 = a.partial + (size_t)col * 2 * a.row_blocks;
+  const double* p1 = p0 + a.row_blocks;
   double s0 = 0.0, s1 = 0.0;
-  if (col < a.C) {
 #pragma unroll 4
-    for (int b = g; b < a.row_blocks; b += 4) {
-      s0 += a.partial[((size_t)b * 2 + 0) * a.C + col];
-      s1 += a.partial[((size_t)b * 2 + 1) * a.C + col];
-    }
+  for (int b = threadIdx.x; b < a.row_blocks; b += 256) {
+    s0 += p0[b];
+    s1 += p1[b];
   }
-  sh[0][g][lc] = s0;
-  sh[1][g][lc] = s1;
+  s0 = wave_sum(s0);
+  s1 = wave_sum(s1);
+  if (lane == 0) {
+    sh[0][wave] = s0;
+    sh[1][wave] = s1;
+  }
   __syncthreads();
-  if (g != 0 || col >= a.C) return;
-  s0 = ((sh[0][0][lc] + sh[0][1][lc]) + sh[0][2][lc]) + sh[0][3][lc];
-  s1 = ((sh[1][0][lc] + sh[1][1][lc]) + sh[1][2][lc]) + sh[1][3][lc];
-  if (a.mode == COL_STATS) {
-    double mean = s0 / a.M;
-    double var = s1 / a.M - mean * mean;
-    if (var < 0.0) var = 0.0;
-    a.out0[col] = mean;
-    a.out1[col] = 1.0 / sqrt(var + a.eps);
-  } else if (a.mode == COL_BNBWD) {
-    a.out0[col] = s0;
-    a.out1[col] = s1;
-    a.grad0[col] = (float)((double)a.grad0[col] + s1);
-    a.grad1[col] = (float)((double)a.grad1[col] + s0);
-  } else {
-    a.grad0[col] = (float)((double)a.grad0[col] + s0);
-  }
+  if (threadIdx.x == 0)
+    col_finish_one(a, col, ((sh[0][0] + sh[0][1]) + sh[0][2]) + sh[0][3],
+                   ((sh[1][0] + sh[1][1]) + sh[1][2]) + sh[1][3]);
+}
+
+hipError_t launch_colfinal(const ColArgs& a, hipStream_t s) {
+  if (a.C <= 0) return hipSuccess;
+  XP_LAUNCH("k_colfinal", (double)a.row_blocks * 2 * a.C * 8, k_colfinal_v, dim3(a.C),
+            dim3(256), 0, s, a);
+  return hipGetLastError();
 }
 
 int col_row_blocks_v(int M, int C, int N) {
@@ -563,10 +577,10 @@ int col_row_blocks_v(int M, int C, int N) {
   int CL = chunks < 256 ? chunks : 256;
   int RG = 256 / CL;
   int colblocks = ceil_div(chunks, CL);
-  int want = ceil_div(512, colblocks);          // ~512 workgroups
-  int maxrb = ceil_div(M, RG * 8);              // >= ~8 rows per thread
+  int want = ceil_div(1024, colblocks);         // ~1024 workgroups: every CU busy
+  int maxrb = ceil_div(M, RG * 4);              // >= ~4 rows per thread
   if (want > maxrb) want = maxrb;
-  if (want > 128) want = 128;
+  if (want > COL_MAX_ROW_BLOCKS_V) want = COL_MAX_ROW_BLOCKS_V;
   return want < 1 ? 1 : want;
 }
 
@@ -581,10 +595,9 @@ static hipError_t colreduce_v(ColArgs a, hipStream_t s) {
             dim3(ceil_div(chunks, CL), a.row_blocks), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  XP_LAUNCH("k_colfinal", (double)a.row_blocks * 2 * a.C * 8, k_colfinal_v, dim3(ceil_div(a.C, 64)),
-            dim3(256), 0, s, a);
-  return hipGetLastError();
+  return launch_colfinal(a, s);
 }
+
 
 // ---------------------------------------------------------------- BN apply / backward
 template <typename T>

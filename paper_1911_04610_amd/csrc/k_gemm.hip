@@ -31,16 +31,12 @@ namespace xp {
 template <typename T> struct MT;
 template <> struct MT<bf16_t> {
   static constexpr int VEC = 8;     // elements per 16-byte chunk
-  static constexpr int BK = 32;     // reduction depth of one step (one MFMA)
-  static constexpr int PITCH = 40;  // LDS row pitch (elements), [row][k] layout
   typedef f32x4_t acc_t;
   typedef float part_t;
   static XP_DEV int out_row(int lane, int q) { return 4 * (lane >> 4) + q; }
 };
 template <> struct MT<float> {
   static constexpr int VEC = 4;
-  static constexpr int BK = 16;     // four 16x16x4 MFMA steps
-  static constexpr int PITCH = 20;  // 20 words: 16-byte aligned rows, conflict-free column reads
   typedef f64x4_t acc_t;
   typedef double part_t;
   static XP_DEV int out_row(int lane, int q) { return (lane >> 4) + 4 * q; }
@@ -74,10 +70,16 @@ XP_DEV uint4 pack_chunk<float>(const float* v) {
 // ============================================================================
 // forward-type implicit GEMM
 // ============================================================================
-template <typename T, int BM, int BN, int WM, int WN, bool FLAT>
+// KS sets the stage depth BK = KS x 32 (bf16: one v_mfma_f32_16x16x32_bf16 per
+// 32) or KS x 16 (fp32 storage: four v_mfma_f64_16x16x4f64 per 16); deeper
+// stages keep more bytes in flight per barrier.
+template <typename T, int BM, int BN, int WM, int WN, bool FLAT, int KS>
 __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   using MTT = MT<T>;
-  constexpr int VEC = MTT::VEC, BK = MTT::BK, PITCH = MTT::PITCH;
+  constexpr int VEC = MTT::VEC;
+  constexpr int SUB = sizeof(T) == 2 ? 32 : 16;
+  constexpr int BK = KS * SUB;
+  constexpr int PITCH = BK + (sizeof(T) == 2 ? 8 : 4);
   constexpr int CPR = BK / VEC;  // chunks per tile row per step
   constexpr int A_CH = BM * CPR, B_CH = BN * CPR;
   constexpr int A_PER = (A_CH + 255) / 256, B_PER = (B_CH + 255) / 256;
@@ -202,21 +204,26 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     const T* A = sA[buf];
     const T* B = sB[buf];
     if constexpr (sizeof(T) == 2) {
-      bf16x8_t af[TM], bfv[TN];
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_t*>(&A[(wm * WTM + i * 16 + (lane & 15)) * PITCH + (lane >> 4) * 8]);
+      for (int ks = 0; ks < KS; ++ks) {
+        bf16x8_t af[TM], bfv[TN];
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bfv[j] = *reinterpret_cast<const bf16x8_t*>(&B[(wn * WTN + j * 16 + (lane & 15)) * PITCH + (lane >> 4) * 8]);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i)
+          af[i] = *reinterpret_cast<const bf16x8_t*>(
+              &A[(wm * WTM + i * 16 + (lane & 15)) * PITCH + ks * 32 + (lane >> 4) * 8]);
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfv[j], acc[i][j], 0, 0, 0);
+          bfv[j] = *reinterpret_cast<const bf16x8_t*>(
+              &B[(wn * WTN + j * 16 + (lane & 15)) * PITCH + ks * 32 + (lane >> 4) * 8]);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfv[j], acc[i][j], 0, 0, 0);
+      }
     } else {
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
+      for (int kk = 0; kk < BK / 4; ++kk) {
         double af[TM], bfv[TN];
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -247,6 +254,9 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   // epilogue: bias, ReLU, mask, accumulate, round once on store
   T* __restrict__ y = (T*)a.y;
   const T* __restrict__ mask = (const T*)a.mask;
+  double cs[TN], cq[TN];  // column sums of the stored values (batch-norm statistics)
+#pragma unroll
+  for (int j = 0; j < TN; ++j) cs[j] = cq[j] = 0.0;
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -263,8 +273,44 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
           T* p = y + (size_t)m * a.ldy + n;
           if (a.accumulate) v += ldd(p);
           std_(p, v);
+          if (a.stat_part) {
+            double sv = ldd(p);  // the stored (rounded) value, as the statistics see it
+            cs[j] += sv;
+            cq[j] += sv * sv;
+          }
         }
       }
+  if (a.stat_part) {
+    // lanes l, l+16, l+32, l+48 share a column: fixed-order butterfly
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      cs[j] += __shfl_xor(cs[j], 16, 64);
+      cq[j] += __shfl_xor(cq[j], 16, 64);
+      cs[j] += __shfl_xor(cs[j], 32, 64);
+      cq[j] += __shfl_xor(cq[j], 32, 64);
+    }
+    __shared__ double red[WM][2][BN];
+    if (lane < 16) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        red[wm][0][wn * WTN + j * 16 + lane] = cs[j];
+        red[wm][1][wn * WTN + j * 16 + lane] = cq[j];
+      }
+    }
+    __syncthreads();
+    for (int col = tid; col < BN; col += 256) {
+      int n = n0 + col;
+      if (n >= a.N) continue;
+      double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+      for (int w = 0; w < WM; ++w) {
+        s0 += red[w][0][col];
+        s1 += red[w][1][col];
+      }
+      a.stat_part[((size_t)n * 2 + 0) * gridDim.x + blockIdx.x] = s0;
+      a.stat_part[((size_t)n * 2 + 1) * gridDim.x + blockIdx.x] = s1;
+    }
+  }
 }
 
 // ============================================================================
@@ -561,68 +607,96 @@ __global__ __launch_bounds__(256) void k_flip(const T* __restrict__ w, T* __rest
 // ============================================================================
 // host launchers
 // ============================================================================
-static int pick_bn(int N) {
-  // smallest padded width among 32 / 64 / 128; ties go to the wider tile
-  int best = 128, best_pad = ((N + 127) / 128) * 128;
-  int pad64 = ((N + 63) / 64) * 64, pad32 = ((N + 31) / 32) * 32;
-  if (pad64 < best_pad) { best = 64; best_pad = pad64; }
-  if (pad32 < best_pad) { best = 32; best_pad = pad32; }
+// Tile choice, from a sweep of the stage shapes on MI355X: 64 columns (32 when
+// N <= 32); 32 or 64 rows depending on the stage depth (see conv_dispatch); the
+// bf16 stage depth minimises the zero padding of each tap's channel run while
+// keeping at least four pipeline stages when possible.
+static int pick_ks_bf16(int C, int taps) {
+  // score: (at least 4 stages, least padding, then larger KS if >= 4 stages,
+  // else more stages)
+  int best = 1, b_ok = -1, b_pad = 0, b_tie = 0;
+  for (int ks : {4, 2, 1}) {
+    int bk = 32 * ks;
+    int per_tap = (C + bk - 1) / bk;
+    int pad = per_tap * bk;
+    int ok = per_tap * taps >= 4;
+    int tie = ok ? ks : -ks;
+    if (ok > b_ok || (ok == b_ok && (pad < b_pad || (pad == b_pad && tie > b_tie)))) {
+      best = ks;
+      b_ok = ok;
+      b_pad = pad;
+      b_tie = tie;
+    }
+  }
   return best;
 }
 
 template <typename T> static const char* tname() { return sizeof(T) == 2 ? "bf16" : "f32"; }
 
-template <typename T, int BM, int BN, int WM, int WN, bool FLAT>
+template <typename T, int BM, int BN, int WM, int WN, bool FLAT, int KS = 0>
 static const char* kname(const char* base) {
   static char buf[96];
   static bool init = false;
   if (!init) {
-    snprintf(buf, sizeof buf, "%s<%s,%d,%d,%d,%d,%s>", base, tname<T>(), BM, BN, WM, WN,
-             FLAT ? "true" : "false");
+    if (KS)
+      snprintf(buf, sizeof buf, "%s<%s,%d,%d,%d,%d,%s,%d>", base, tname<T>(), BM, BN, WM, WN,
+               FLAT ? "true" : "false", KS);
+    else
+      snprintf(buf, sizeof buf, "%s<%s,%d,%d,%d,%d,%s>", base, tname<T>(), BM, BN, WM, WN,
+               FLAT ? "true" : "false");
     init = true;
   }
   return buf;
 }
 
-template <typename T, int BM, int BN, int WM, int WN>
-static hipError_t conv_go(const ConvArgs& a, bool flat, hipStream_t s) {
+template <typename T, int BM, int BN, int WM, int WN, int KS>
+static hipError_t conv_go(const ConvArgs& a, bool flat, hipStream_t s, int* grid_rows = nullptr) {
   int M = a.nb * a.H * a.W;
   dim3 grid((M + BM - 1) / BM, (a.N + BN - 1) / BN);
+  if (grid_rows) *grid_rows = (int)grid.x;
   double flops = 2.0 * M * (double)a.N * a.R * a.S * a.C;
   if (flat)
-    XP_LAUNCH((kname<T, BM, BN, WM, WN, true>("k_conv_gemm")), flops,
-              (k_conv_gemm<T, BM, BN, WM, WN, true>), grid, dim3(256), 0, s, a);
+    XP_LAUNCH((kname<T, BM, BN, WM, WN, true, KS>("k_conv_gemm")), flops,
+              (k_conv_gemm<T, BM, BN, WM, WN, true, KS>), grid, dim3(256), 0, s, a);
   else
-    XP_LAUNCH((kname<T, BM, BN, WM, WN, false>("k_conv_gemm")), flops,
-              (k_conv_gemm<T, BM, BN, WM, WN, false>), grid, dim3(256), 0, s, a);
+    XP_LAUNCH((kname<T, BM, BN, WM, WN, false, KS>("k_conv_gemm")), flops,
+              (k_conv_gemm<T, BM, BN, WM, WN, false, KS>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 template <typename T>
-static hipError_t conv_dispatch(const ConvArgs& a, hipStream_t s) {
+static hipError_t conv_dispatch(const ConvArgs& a, hipStream_t s, int* gr) {
   constexpr int VEC = MT<T>::VEC;
   bool flat = (a.C % VEC) != 0 || (a.ldx % VEC) != 0 ||
               (reinterpret_cast<uintptr_t>(a.x) % 16) != 0 ||
               (reinterpret_cast<uintptr_t>(a.w) % 16) != 0;
-  int M = a.nb * a.H * a.W;
-  int bn = pick_bn(a.N);
-  // small problems: shorter row tiles give more workgroups
-  int tiles128 = ((M + 127) / 128) * ((a.N + bn - 1) / bn);
-  bool bm64 = tiles128 < 512;
-  if (!bm64) {
-    if (bn == 128) return conv_go<T, 128, 128, 2, 2>(a, flat, s);
-    if (bn == 64) return conv_go<T, 128, 64, 2, 2>(a, flat, s);
-    return conv_go<T, 128, 32, 4, 1>(a, flat, s);
+  const bool narrow = a.N <= 32;
+  if constexpr (sizeof(T) == 2) {
+    // one-stage depth (KS = 1) runs best with 64-row tiles; deeper stages with
+    // 32-row tiles, which double the workgroups in flight for these skinny layers
+    const int ks = flat ? 1 : pick_ks_bf16(a.C, a.R * a.S);
+    if (narrow) {
+      if (ks == 4) return conv_go<T, 32, 32, 2, 2, 4>(a, flat, s, gr);
+      if (ks == 2) return conv_go<T, 32, 32, 2, 2, 2>(a, flat, s, gr);
+      return conv_go<T, 64, 32, 2, 2, 1>(a, flat, s, gr);
+    }
+    if (ks == 4) return conv_go<T, 32, 64, 2, 2, 4>(a, flat, s, gr);
+    if (ks == 2) return conv_go<T, 32, 64, 2, 2, 2>(a, flat, s, gr);
+    return conv_go<T, 64, 64, 2, 2, 1>(a, flat, s, gr);
+  } else {
+    if (narrow) return conv_go<T, 64, 32, 2, 2, 1>(a, flat, s, gr);
+    return conv_go<T, 64, 64, 2, 2, 1>(a, flat, s, gr);
   }
-  if (bn == 128) return conv_go<T, 64, 128, 2, 2>(a, flat, s);
-  if (bn == 64) return conv_go<T, 64, 64, 2, 2>(a, flat, s);
-  return conv_go<T, 64, 32, 2, 2>(a, flat, s);
 }
 
-hipError_t launch_conv_gemm(int dtype, const ConvArgs& a, hipStream_t s) {
+hipError_t launch_conv_gemm(int dtype, const ConvArgs& a, hipStream_t s, int* grid_rows) {
+  if (grid_rows) *grid_rows = 0;
   if (a.nb * a.H * a.W <= 0 || a.N <= 0) return hipSuccess;
-  return dtype == DT_BF16 ? conv_dispatch<bf16_t>(a, s) : conv_dispatch<float>(a, s);
+  return dtype == DT_BF16 ? conv_dispatch<bf16_t>(a, s, grid_rows)
+                          : conv_dispatch<float>(a, s, grid_rows);
 }
+
+int conv_max_row_tiles(int M) { return (M + 31) / 32; }
 
 int wgrad_pick_splits(int M, int N, int K) {
   int bm = N <= 64 ? 64 : 128;

@@ -87,6 +87,9 @@ struct Op {
   int64_t stat_off = -1;            // workspace bytes: mean, rstd, dbeta, dgamma (doubles)
   // backward bookkeeping: first producer writes, later ones add
   bool in_acc = false, in2_acc = false;
+  // batch-norm statistics computed in the producing GEMM's epilogue
+  int stats_for = -1;        // GEMM: index of the BN op whose statistics it produces
+  bool stats_fused = false;  // BN: statistics come from the producing GEMM
 };
 
 struct ParamT {
@@ -428,6 +431,21 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     p.out_tensor = lastop.out;
   }
 
+  // ---- batch-norm statistics fused into the producing conv / linear epilogue
+  for (size_t i = 0; i < p.ops.size(); ++i) {
+    Op& bn = p.ops[i];
+    if (bn.kind != OP_BN || bn.in == 0) continue;
+    const Tensor& z = p.tensors[bn.in];
+    if (z.owner >= 0 || z.consumers != 1) continue;
+    for (size_t j = 0; j < i; ++j) {
+      Op& g = p.ops[j];
+      if (g.kind == OP_GEMM && g.out == bn.in && !g.relu) {
+        g.stats_for = (int)i;
+        bn.stats_fused = true;
+      }
+    }
+  }
+
   // ---- backward accumulation order: walk ops in reverse; first contribution writes
   {
     std::vector<bool> written(p.tensors.size(), false);
@@ -473,6 +491,8 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
       int splits = wgrad_pick_splits(M, op.cout, K);
       wpart = std::max(wpart, wgrad_part_bytes(dtype, op.cout, K, splits));
       if (op.b_off >= 0) colpart = std::max(colpart, col_partial_bytes(M, op.cout));
+      if (op.stats_for >= 0)
+        colpart = std::max(colpart, (size_t)conv_max_row_tiles(M) * 2 * op.cout * sizeof(double));
     } else if (op.kind == OP_BN) {
       op.stat_off = take((size_t)4 * tin_.sh.C * sizeof(double));
       colpart = std::max(colpart, col_partial_bytes((int)tin_.sh.rows(), tin_.sh.C));
@@ -602,7 +622,24 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         a.R = a.S = op.k;
         a.pad = op.k / 2;
         a.relu = op.relu;
-        XP_HIP(launch_conv_gemm(dt, a, s));
+        int rows_tiles = 0;
+        if (op.stats_for >= 0) a.stat_part = (double*)(st->ws + st->colpart_off);
+        XP_HIP(launch_conv_gemm(dt, a, s, &rows_tiles));
+        if (op.stats_for >= 0) {
+          // the following BN's batch statistics from the epilogue's column sums
+          const Op& bn = st->ops[op.stats_for];
+          double* stats = (double*)(st->ws + bn.stat_off);
+          ColArgs ca{};
+          ca.mode = COL_STATS;
+          ca.M = (int)tin.sh.rows();
+          ca.C = op.cout;
+          ca.partial = a.stat_part;
+          ca.row_blocks = rows_tiles;
+          ca.out0 = stats;
+          ca.out1 = stats + op.cout;
+          ca.eps = BN_EPS;
+          XP_HIP(launch_colfinal(ca, s));
+        }
         break;
       }
       case OP_BN: {
@@ -618,7 +655,7 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         ca.out0 = stats;
         ca.out1 = stats + tin.sh.C;
         ca.eps = BN_EPS;
-        {
+        if (!op.stats_fused) {
           XP_HIP(launch_colreduce(dt, ca, s));
         }
         View y = act(st, op.out, c);

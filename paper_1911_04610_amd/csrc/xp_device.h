@@ -51,3 +51,14 @@ XP_DEV double wave_max(double v) {
   for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
   return v;
 }
+
+// ---------------------------------------------------------------- batch-norm statistics
+// mean and 1/sqrt(biased variance + eps) from the column sum and sum of squares
+XP_DEV void bn_stats_from_sums(double s0, double s1, int M, double eps, double* mean,
+                               double* rstd) {
+  const double mu = s0 / M;
+  double var = s1 / M - mu * mu;
+  if (var < 0.0) var = 0.0;
+  *mean = mu;
+  *rstd = 1.0 / sqrt(var + eps);
+}

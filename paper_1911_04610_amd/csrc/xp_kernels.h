@@ -67,6 +67,8 @@ struct ConvArgs {
   int nb, H, W, C, N, R, S, pad;
   int relu;             // apply max(., 0) before storing
   int accumulate;       // y = y + result (after mask)
+  double* stat_part;    // optional: per row tile, column sums of the stored y and of its
+                        // squares, at stat_part[(n * 2 + {0,1}) * row_tiles + tile]
 };
 
 // Weight gradient: part[split][n][k] = sum_{m in split} dz[m][n] * x~[m][k],
@@ -83,7 +85,10 @@ struct WgradArgs {
 };
 
 // Work plan of one GEMM launch (tile shape picked on the host).
-hipError_t launch_conv_gemm(int dtype, const ConvArgs& a, hipStream_t s);
+// grid_rows (optional) receives the number of row tiles of the launch
+hipError_t launch_conv_gemm(int dtype, const ConvArgs& a, hipStream_t s, int* grid_rows = nullptr);
+// row tiles the forward-type GEMM uses for M rows (upper bound over tile choices)
+int conv_max_row_tiles(int M);
 size_t wgrad_part_bytes(int dtype, int N, int K, int splits);
 int wgrad_pick_splits(int M, int N, int K);
 hipError_t launch_wgrad(int dtype, const WgradArgs& a, hipStream_t s);
@@ -104,7 +109,7 @@ struct ColArgs {
   const double* mean;   // BNBWD
   const double* rstd;   // BNBWD
   int M, C;
-  double* partial;      // workspace [row blocks][2][C]
+  double* partial;      // workspace [C][2][row blocks]
   int row_blocks;
   // finalize outputs
   double* out0;         // STATS: mean; BNBWD: dbeta
@@ -116,6 +121,8 @@ struct ColArgs {
 int col_row_blocks(int M, int C);
 size_t col_partial_bytes(int M, int C);
 hipError_t launch_colreduce(int dtype, const ColArgs& a, hipStream_t s);
+// second level only: sums a.row_blocks partials per column and finalises (a.mode)
+hipError_t launch_colfinal(const ColArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- element-wise
 struct BnApplyArgs {

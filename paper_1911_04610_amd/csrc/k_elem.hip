@@ -779,64 +779,91 @@ __global__ __launch_bounds__(256) void k_maxpool_bwd_v(PoolArgs a) {
   }
 }
 
+// 3x3 / stride 1 / zero-padded average (padding counted): each thread slides
+// along a run of AVG_SEG outputs of one image row and one 16-byte channel
+// chunk, keeping the vertical three-row sums of the previous, current and next
+// column, so each input chunk is loaded three times instead of nine.
+// out(h, w) = (v(w-1) + v(w)) + v(w+1) with v(w) = (x(h-1, w) + x(h, w)) + x(h+1, w).
+constexpr int AVG_SEG = 7;
 template <typename T>
 __global__ __launch_bounds__(256) void k_avgpool3_v(PoolArgs a, const T* src, int ld_src) {
   constexpr int N = VT<T>::N;
   const int chunks = a.C / N;
-  const int items = a.nb * a.H * a.W * chunks;
+  const int nseg = ceil_div(a.W, AVG_SEG);
+  int it = blockIdx.x * blockDim.x + threadIdx.x;
+  if (it >= a.nb * a.H * nseg * chunks) return;
+  const int chunk = it % chunks;
+  it /= chunks;
+  const int seg = it % nseg;
+  it /= nseg;
+  const int h = it % a.H, n = it / a.H;
+  const int c0 = chunk * N;
+  const int w0 = seg * AVG_SEG, w1 = min(a.W, w0 + AVG_SEG);
+  auto vsum = [&](int w, double* v) {
+#pragma unroll
+    for (int e = 0; e < N; ++e) v[e] = 0.0;
+    if (w < 0 || w >= a.W) return;
+#pragma unroll
+    for (int dr = -1; dr <= 1; ++dr) {
+      const int hh = h + dr;
+      if (hh < 0 || hh >= a.H) continue;
+      double q[N];
+      vld(src + ((size_t)(n * a.H + hh) * a.W + w) * ld_src + c0, q);
+#pragma unroll
+      for (int e = 0; e < N; ++e) v[e] += q[e];
+    }
+  };
   const T* MK = (const T*)a.mask;
   T* O = (T*)a.out;
-  for (int it = blockIdx.x * blockDim.x + threadIdx.x; it < items; it += gridDim.x * blockDim.x) {
-    const int r = it / chunks, c0 = (it - r * chunks) * N;
-    const int n = r / (a.H * a.W), rem = r - n * a.H * a.W, h = rem / a.W, w = rem - h * a.W;
-    double s[N], q[N];
+  double vp[N], vc[N], vn[N];
+  vsum(w0 - 1, vp);
+  vsum(w0, vc);
+  for (int w = w0; w < w1; ++w) {
+    vsum(w + 1, vn);
+    double s[N];
 #pragma unroll
-    for (int e = 0; e < N; ++e) s[e] = 0.0;
-#pragma unroll
-    for (int dr = -1; dr <= 1; ++dr)
-#pragma unroll
-      for (int ds = -1; ds <= 1; ++ds) {
-        const int hh = h + dr, ww = w + ds;
-        if (hh >= 0 && hh < a.H && ww >= 0 && ww < a.W) {
-          vld(src + ((size_t)(n * a.H + hh) * a.W + ww) * ld_src + c0, q);
-#pragma unroll
-          for (int e = 0; e < N; ++e) s[e] += q[e];
-        }
-      }
-#pragma unroll
-    for (int e = 0; e < N; ++e) s[e] = s[e] / 9.0;
-    if (MK) vmask(MK + (size_t)r * a.ldm + c0, s);
-    T* p = O + (size_t)r * a.ldo + c0;
+    for (int e = 0; e < N; ++e) s[e] = ((vp[e] + vc[e]) + vn[e]) / 9.0;
+    const size_t r = (size_t)(n * a.H + h) * a.W + w;
+    if (MK) vmask(MK + r * a.ldm + c0, s);
+    T* p = O + r * a.ldo + c0;
     if (a.accumulate) {
-#pragma unroll
-      for (int e = 0; e < N; ++e) q[e] = 0.0;
+      double q[N];
       vld(p, q);
 #pragma unroll
       for (int e = 0; e < N; ++e) s[e] += q[e];
     }
     vst(p, s);
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+      vp[e] = vc[e];
+      vc[e] = vn[e];
+    }
   }
 }
 
-// global average pool: one workgroup of 512 threads per image, CL chunk-lanes
-// x RG row groups, fixed-order LDS reduction
+// Global average pool, two launches: per (image, pixel split) partial sums of
+// every channel (fixed order: strided per thread, then the row groups in
+// order), then per (image, channel) the splits in order, divided by H*W.
 template <typename T>
-__global__ __launch_bounds__(512) void k_gap_fwd_v(PoolArgs a) {
+__global__ __launch_bounds__(256) void k_gap_part_v(PoolArgs a, int splits) {
   constexpr int N = VT<T>::N;
-  __shared__ double sh[512][N];
+  __shared__ double sh[256][N];
   const int chunks = a.C / N;
-  const int CL = chunks < 512 ? chunks : 512;
-  const int RG = 512 / CL;
+  const int CL = chunks < 256 ? chunks : 256;
+  const int RG = 256 / CL;
   const int cl = threadIdx.x % CL, g = threadIdx.x / CL;
-  const int n = blockIdx.y, chunk = blockIdx.x * CL + cl;
+  const int chunk = blockIdx.z * CL + cl;
+  const int split = blockIdx.x, n = blockIdx.y;
   const int HW = a.H * a.W;
+  const int per = ceil_div(HW, splits);
+  const int p0 = split * per, p1 = min(HW, p0 + per);
   const T* X = (const T*)a.x;
   double s[N];
 #pragma unroll
   for (int e = 0; e < N; ++e) s[e] = 0.0;
   if (g < RG && chunk < chunks) {
 #pragma unroll 4
-    for (int p = g; p < HW; p += RG) {
+    for (int p = p0 + g; p < p1; p += RG) {
       double q[N];
       vld(X + ((size_t)n * HW + p) * a.ldx + chunk * N, q);
 #pragma unroll
@@ -853,10 +880,31 @@ __global__ __launch_bounds__(512) void k_gap_fwd_v(PoolArgs a) {
     for (int q = 0; q < RG; ++q)
 #pragma unroll
       for (int e = 0; e < N; ++e) t[e] += sh[q * CL + cl][e];
+    double* P = a.part + ((size_t)n * splits + split) * a.C + chunk * N;
 #pragma unroll
-    for (int e = 0; e < N; ++e) t[e] = t[e] / HW;
-    vst((T*)a.out + (size_t)n * a.ldo + chunk * N, t);
+    for (int e = 0; e < N; ++e) P[e] = t[e];
   }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_gap_fin_v(PoolArgs a, int splits) {
+  constexpr int N = VT<T>::N;
+  const int chunks = a.C / N;
+  const int it = blockIdx.x * blockDim.x + threadIdx.x;
+  if (it >= a.nb * chunks) return;
+  const int n = it / chunks, c0 = (it - n * chunks) * N;
+  double t[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) t[e] = 0.0;
+  for (int q = 0; q < splits; ++q) {
+    const double* P = a.part + ((size_t)n * splits + q) * a.C + c0;
+#pragma unroll
+    for (int e = 0; e < N; ++e) t[e] += P[e];
+  }
+  const int HW = a.H * a.W;
+#pragma unroll
+  for (int e = 0; e < N; ++e) t[e] = t[e] / HW;
+  vst((T*)a.out + (size_t)n * a.ldo + c0, t);
 }
 
 template <typename T>
@@ -1005,18 +1053,21 @@ hipError_t launch_maxpool_bwd(int dtype, const PoolArgs& a, hipStream_t s) {
   return launch_maxpool_bwd_s(dtype, a, s);
 }
 
+static int avg_blocks(const PoolArgs& a, int n) {
+  return ceil_div(a.nb * a.H * ceil_div(a.W, AVG_SEG) * (a.C / n), 256);
+}
+
 hipError_t launch_avgpool_fwd(int dtype, const PoolArgs& a, hipStream_t s) {
   int64_t rows = (int64_t)a.nb * a.H * a.W;
   if (rows <= 0 || a.C <= 0) return hipSuccess;
   if (vec_dt(dtype, rows, a.C, {{a.x, a.ldx}, {a.mask, a.ldm}, {a.out, a.ldo}})) {
+    const int blocks = avg_blocks(a, vn(dtype));
     if (dtype == DT_BF16)
       XP_LAUNCH("k_avgpool3_v<bf16>", (double)rows * a.C * 2 * (a.accumulate ? 3 : 2), k_avgpool3_v<bf16_t>,
-                dim3(grid_for(rows * (a.C / 8))), dim3(256), 0, s, a,
-                         (const bf16_t*)a.x, a.ldx);
+                dim3(blocks), dim3(256), 0, s, a, (const bf16_t*)a.x, a.ldx);
     else
       XP_LAUNCH("k_avgpool3_v<f32>", (double)rows * a.C * 4 * (a.accumulate ? 3 : 2), k_avgpool3_v<float>,
-                dim3(grid_for(rows * (a.C / 4))), dim3(256), 0, s, a,
-                         (const float*)a.x, a.ldx);
+                dim3(blocks), dim3(256), 0, s, a, (const float*)a.x, a.ldx);
     return hipGetLastError();
   }
   return launch_avgpool_fwd_s(dtype, a, s);
@@ -1026,28 +1077,51 @@ hipError_t launch_avgpool_bwd(int dtype, const PoolArgs& a, hipStream_t s) {
   int64_t rows = (int64_t)a.nb * a.H * a.W;
   if (rows <= 0 || a.C <= 0) return hipSuccess;
   if (vec_dt(dtype, rows, a.C, {{a.dy, a.lddy}, {a.mask, a.ldm}, {a.out, a.ldo}})) {
+    const int blocks = avg_blocks(a, vn(dtype));
     if (dtype == DT_BF16)
       XP_LAUNCH("k_avgpool3_v<bf16>", (double)rows * a.C * 2 * (a.accumulate ? 3 : 2), k_avgpool3_v<bf16_t>,
-                dim3(grid_for(rows * (a.C / 8))), dim3(256), 0, s, a,
-                         (const bf16_t*)a.dy, a.lddy);
+                dim3(blocks), dim3(256), 0, s, a, (const bf16_t*)a.dy, a.lddy);
     else
       XP_LAUNCH("k_avgpool3_v<f32>", (double)rows * a.C * 4 * (a.accumulate ? 3 : 2), k_avgpool3_v<float>,
-                dim3(grid_for(rows * (a.C / 4))), dim3(256), 0, s, a,
-                         (const float*)a.dy, a.lddy);
+                dim3(blocks), dim3(256), 0, s, a, (const float*)a.dy, a.lddy);
     return hipGetLastError();
   }
   return launch_avgpool_bwd_s(dtype, a, s);
 }
 
+// pixel splits of the GAP partial sums: about 1024 workgroups, >= ~4 pixels per thread
+static int gap_splits(int nb, int HW, int C, int n) {
+  const int chunks = C / n;
+  const int CL = chunks < 256 ? chunks : 256;
+  const int RG = 256 / CL;
+  int want = ceil_div(1024, nb * ceil_div(chunks, CL));
+  const int maxs = ceil_div(HW, RG * 4);
+  if (want > maxs) want = maxs;
+  if (want > 64) want = 64;
+  return want < 1 ? 1 : want;
+}
+size_t gap_partial_bytes(int nb, int H, int W, int C) {
+  return (size_t)nb * 64 * C * sizeof(double);
+}
+
 hipError_t launch_gap_fwd(int dtype, const PoolArgs& a, hipStream_t s) {
   if (a.nb <= 0 || a.C <= 0) return hipSuccess;
-  if (vec_dt(dtype, (int64_t)a.nb * a.H * a.W, a.C, {{a.x, a.ldx}, {a.out, a.ldo}})) {
-    int chunks = a.C / vn(dtype);
-    int CL = chunks < 512 ? chunks : 512;
-    dim3 grid(ceil_div(chunks, CL), a.nb);
-    double gb = (double)a.nb * a.H * a.W * a.C * (dtype == DT_BF16 ? 2 : 4);
-    if (dtype == DT_BF16) XP_LAUNCH("k_gap_fwd_v<bf16>", gb, k_gap_fwd_v<bf16_t>, grid, dim3(512), 0, s, a);
-    else XP_LAUNCH("k_gap_fwd_v<f32>", gb, k_gap_fwd_v<float>, grid, dim3(512), 0, s, a);
+  if (a.part && vec_dt(dtype, (int64_t)a.nb * a.H * a.W, a.C, {{a.x, a.ldx}, {a.out, a.ldo}})) {
+    const int chunks = a.C / vn(dtype);
+    const int CL = chunks < 256 ? chunks : 256;
+    const int colblocks = ceil_div(chunks, CL);
+    const int splits = gap_splits(a.nb, a.H * a.W, a.C, vn(dtype));
+    dim3 grid(splits, a.nb, colblocks);
+    const double gb = (double)a.nb * a.H * a.W * a.C * (dtype == DT_BF16 ? 2 : 4);
+    const double fb = (double)a.nb * splits * a.C * 8;
+    const int fblocks = ceil_div(a.nb * chunks, 256);
+    if (dtype == DT_BF16) {
+      XP_LAUNCH("k_gap_part_v<bf16>", gb, k_gap_part_v<bf16_t>, grid, dim3(256), 0, s, a, splits);
+      XP_LAUNCH("k_gap_fin_v<bf16>", fb, k_gap_fin_v<bf16_t>, dim3(fblocks), dim3(256), 0, s, a, splits);
+    } else {
+      XP_LAUNCH("k_gap_part_v<f32>", gb, k_gap_part_v<float>, grid, dim3(256), 0, s, a, splits);
+      XP_LAUNCH("k_gap_fin_v<f32>", fb, k_gap_fin_v<float>, dim3(fblocks), dim3(256), 0, s, a, splits);
+    }
     return hipGetLastError();
   }
   return launch_gap_fwd_s(dtype, a, s);

@@ -559,12 +559,29 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
 
 // grad[i] += sum over splits of part[z][i], splits added in order z = 0, 1, ...;
 // each thread owns four consecutive outputs so the partial reads are 16-32 B
+// Destination rows of the weight gradient: one accumulator, or several
+// consecutive row ranges each with its own (sibling layers sharing a launch).
+struct GradDst {
+  int nseg;
+  int64_t base[GATHER_MAX_SEGS + 1];  // flat element index where segment j starts
+  float* ptr[GATHER_MAX_SEGS];
+};
+
+XP_DEV float* grad_at(const GradDst& d, int64_t i, int64_t* seg_end) {
+  int j = 0;
+  while (j + 1 < d.nseg && i >= d.base[j + 1]) ++j;
+  *seg_end = d.base[j + 1];
+  return d.ptr[j] + (i - d.base[j]);
+}
+
 template <typename P>
 __global__ __launch_bounds__(256) void k_split_reduce(const P* __restrict__ part, int splits,
-                                                       int64_t count, float* __restrict__ grad) {
+                                                       int64_t count, GradDst dst) {
   const int64_t q = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (q >= count) return;
-  if (q + 4 <= count) {
+  int64_t seg_end = 0;
+  float* g = grad_at(dst, q, &seg_end);
+  if (q + 4 <= seg_end) {
     double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
 #pragma unroll 4
     for (int z = 0; z < splits; ++z) {
@@ -574,16 +591,30 @@ __global__ __launch_bounds__(256) void k_split_reduce(const P* __restrict__ part
       s2 += (double)p[2];
       s3 += (double)p[3];
     }
-    grad[q] = (float)((double)grad[q] + s0);
-    grad[q + 1] = (float)((double)grad[q + 1] + s1);
-    grad[q + 2] = (float)((double)grad[q + 2] + s2);
-    grad[q + 3] = (float)((double)grad[q + 3] + s3);
+    g[0] = (float)((double)g[0] + s0);
+    g[1] = (float)((double)g[1] + s1);
+    g[2] = (float)((double)g[2] + s2);
+    g[3] = (float)((double)g[3] + s3);
   } else {
-    for (int64_t i = q; i < count; ++i) {
+    for (int64_t i = q; i < count && i < q + 4; ++i) {
       double s = 0.0;
       for (int z = 0; z < splits; ++z) s += (double)part[(size_t)z * count + i];
-      grad[i] = (float)((double)grad[i] + s);
+      float* gi = grad_at(dst, i, &seg_end);
+      *gi = (float)((double)*gi + s);
     }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_gather(GatherArgs a) {
+  int64_t base = 0;
+  for (int j = 0; j < a.nseg; ++j) {
+    const T* src = (const T*)a.src[j];
+    T* dst = (T*)a.dst + base;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < a.count[j];
+         i += (int64_t)gridDim.x * blockDim.x)
+      dst[i] = src[i];
+    base += a.count[j];
   }
 }
 
@@ -735,9 +766,20 @@ static hipError_t wgrad_go(const WgradArgs& a, bool flat, hipStream_t s) {
   int64_t count = (int64_t)a.N * K;
   int blocks = (int)(((count + 3) / 4 + 255) / 256);
   typedef typename MT<T>::part_t P;
+  GradDst d{};
+  if (a.nseg > 0) {
+    d.nseg = a.nseg;
+    for (int j = 0; j <= a.nseg; ++j) d.base[j] = (int64_t)a.seg_row0[j] * K;
+    for (int j = 0; j < a.nseg; ++j) d.ptr[j] = a.seg_grad[j];
+  } else {
+    d.nseg = 1;
+    d.base[0] = 0;
+    d.base[1] = count;
+    d.ptr[0] = a.grad;
+  }
   XP_LAUNCH(sizeof(P) == 4 ? "k_split_reduce<float>" : "k_split_reduce<double>",
             (double)count * (a.splits * sizeof(P) + 8), k_split_reduce<P>, dim3(blocks), dim3(256), 0, s,
-            (const P*)a.part, a.splits, count, a.grad);
+            (const P*)a.part, a.splits, count, d);
   return hipGetLastError();
 }
 
@@ -757,6 +799,22 @@ static hipError_t wgrad_dispatch(const WgradArgs& a, hipStream_t s) {
 hipError_t launch_wgrad(int dtype, const WgradArgs& a, hipStream_t s) {
   if (a.N <= 0) return hipSuccess;
   return dtype == DT_BF16 ? wgrad_dispatch<bf16_t>(a, s) : wgrad_dispatch<float>(a, s);
+}
+
+hipError_t launch_gather(int dtype, const GatherArgs& a, hipStream_t s) {
+  int64_t total = 0, longest = 0;
+  for (int j = 0; j < a.nseg; ++j) {
+    total += a.count[j];
+    longest = a.count[j] > longest ? a.count[j] : longest;
+  }
+  if (total <= 0) return hipSuccess;
+  int blocks = (int)((longest + 255) / 256);
+  if (blocks > 1024) blocks = 1024;
+  if (dtype == DT_BF16)
+    XP_LAUNCH("k_gather<bf16>", (double)total * 4, k_gather<bf16_t>, dim3(blocks), dim3(256), 0, s, a);
+  else
+    XP_LAUNCH("k_gather<f32>", (double)total * 8, k_gather<float>, dim3(blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_flip_weights(int dtype, const void* w, void* wd, int N, int R, int S, int C,

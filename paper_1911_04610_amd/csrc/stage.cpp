@@ -82,14 +82,21 @@ struct Op {
   int cin = 0, cout = 0, k = 1;
   int64_t w_off = -1, b_off = -1;   // parameter offsets (elements)
   int64_t wd_off = -1;              // workspace bytes: flipped weights for the data gradient
+  // GEMM over sibling layers that read the same input (merged launch): their
+  // weight tensors (parameter offset, output channels) in output-channel order
+  std::vector<std::pair<int64_t, int>> segs;
+  int64_t wg_off[2] = {-1, -1};     // workspace bytes: gathered predicted weights per direction
   // BN
   int64_t g_off = -1, be_off = -1;  // gamma / beta parameter offsets
-  int64_t stat_off = -1;            // workspace bytes: mean, rstd, dbeta, dgamma (doubles)
+  int64_t stat_off = -1;            // workspace bytes: mean, rstd, dbeta, dgamma (doubles) ...
+  int stat_ld = 0;                  // ... arrays stat_ld doubles apart
   // backward bookkeeping: first producer writes, later ones add
   bool in_acc = false, in2_acc = false;
   // batch-norm statistics computed in the producing GEMM's epilogue
-  int stats_for = -1;        // GEMM: index of the BN op whose statistics it produces
-  bool stats_fused = false;  // BN: statistics come from the producing GEMM
+  bool stats = false;          // GEMM: writes mean / rstd of every output column ...
+  int64_t stat_block = -1;     // ... to this workspace block ([2][cout] doubles, then dbeta/dgamma)
+  bool stats_fused = false;    // BN: statistics come from the producing GEMM
+  int stats_from = -1;         // BN: index of that GEMM op (during planning)
 };
 
 struct ParamT {
@@ -396,7 +403,7 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
   for (const Op& op : p.ops) {
     if (op.kind != OP_CONCAT) continue;
     int coff = 0;
-    bool all_masked = true;
+    bool all_masked = true, any_masked = false;
     for (int q = 0; q < L[op.layer].n_inputs; ++q) {
       int t = tens(L[op.layer].inputs[q]);
       Tensor& m = p.tensors[t];
@@ -406,7 +413,12 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
       m.coff = coff;
       coff += m.sh.C;
       all_masked = all_masked && m.masked;
+      any_masked = any_masked || m.masked;
     }
+    if (!all_masked && any_masked)
+      return fail(XPIPE_EUNSUPPORTED,
+                  "concat inputs must be all ReLU outputs or all not: the gradient of the concat "
+                  "is masked as one tensor");
     p.tensors[op.out].masked = all_masked;
   }
   // concat-of-concat: resolve owners transitively
@@ -431,18 +443,66 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     p.out_tensor = lastop.out;
   }
 
+  // The merge below is exact in real arithmetic and leaves every forward
+  // value bit for bit as the layer-by-layer launches give it, but the merged
+  // data gradient adds the siblings' contributions before rounding once.  The
+  // bf16 variant takes it; the fp32 variant keeps the rounding points of the
+  // layer-by-layer definition.
+  const bool rewrite = dtype == DT_BF16;
+
+  // ---- sibling merge: convolutions with the same input and kernel size (no
+  // bias, no fused ReLU, outputs not in a concat) become one GEMM launch whose
+  // output is a buffer the siblings' outputs are channel slices of: the input
+  // is read once, and the backward takes one data-gradient and one
+  // weight-gradient launch for all of them
+  for (size_t i = 0; rewrite && i < p.ops.size(); ++i) {
+    auto mergeable = [&](const Op& o) {
+      const Tensor& t = p.tensors[o.out];
+      return o.kind == OP_GEMM && o.segs.empty() && o.b_off < 0 && !o.relu && t.owner < 0 &&
+             o.out != p.out_tensor;
+    };
+    if (!mergeable(p.ops[i])) continue;
+    std::vector<size_t> sib{i};
+    for (size_t j = i + 1; j < p.ops.size() && sib.size() < (size_t)GATHER_MAX_SEGS; ++j)
+      if (mergeable(p.ops[j]) && p.ops[j].in == p.ops[i].in && p.ops[j].k == p.ops[i].k)
+        sib.push_back(j);
+    if (sib.size() < 2) continue;
+    Op m = p.ops[i];
+    m.w_off = -1;
+    m.cout = 0;
+    for (size_t q : sib) m.cout += p.ops[q].cout;
+    Shape ms = p.tensors[m.out].sh;
+    ms.C = m.cout;
+    const int owner = new_tensor(ms);
+    p.tensors[owner].consumers = 1;
+    int coff = 0;
+    for (size_t q : sib) {
+      const Op& o = p.ops[q];
+      m.segs.push_back({o.w_off, o.cout});
+      p.tensors[o.out].owner = owner;
+      p.tensors[o.out].coff = coff;
+      coff += o.cout;
+    }
+    m.out = owner;
+    for (size_t k = sib.size() - 1; k >= 1; --k) p.ops.erase(p.ops.begin() + sib[k]);
+    p.ops[i] = m;
+  }
+
   // ---- batch-norm statistics fused into the producing conv / linear epilogue
   for (size_t i = 0; i < p.ops.size(); ++i) {
     Op& bn = p.ops[i];
     if (bn.kind != OP_BN || bn.in == 0) continue;
     const Tensor& z = p.tensors[bn.in];
-    if (z.owner >= 0 || z.consumers != 1) continue;
+    if (z.consumers != 1) continue;
+    const int src = z.owner >= 0 ? z.owner : bn.in;
     for (size_t j = 0; j < i; ++j) {
       Op& g = p.ops[j];
-      if (g.kind == OP_GEMM && g.out == bn.in && !g.relu) {
-        g.stats_for = (int)i;
-        bn.stats_fused = true;
-      }
+      if (g.kind != OP_GEMM || g.out != src || g.relu) continue;
+      // a view is only fed by a merged GEMM
+      if (z.owner >= 0 && g.segs.empty()) continue;
+      g.stats = true;
+      bn.stats_fused = true;
+      bn.stats_from = (int)j;
     }
   }
 
@@ -486,16 +546,30 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     const Tensor& tin_ = p.tensors[op.in];
     if (op.kind == OP_GEMM) {
       op.wd_off = take((size_t)op.cout * op.k * op.k * op.cin * esz);
+      if (!op.segs.empty())
+        for (int d = 0; d < 2; ++d)
+          op.wg_off[d] = take((size_t)op.cout * op.k * op.k * op.cin * esz);
+      if (op.stats) op.stat_block = take((size_t)4 * op.cout * sizeof(double));
       int M = (int)tin_.sh.rows();
       int K = op.k * op.k * op.cin;
       int splits = wgrad_pick_splits(M, op.cout, K);
       wpart = std::max(wpart, wgrad_part_bytes(dtype, op.cout, K, splits));
       if (op.b_off >= 0) colpart = std::max(colpart, col_partial_bytes(M, op.cout));
-      if (op.stats_for >= 0)
+      if (op.stats)
         colpart = std::max(colpart, (size_t)conv_max_row_tiles(M) * 2 * op.cout * sizeof(double));
     } else if (op.kind == OP_BN) {
-      op.stat_off = take((size_t)4 * tin_.sh.C * sizeof(double));
+      if (op.stats_fused) {
+        // the GEMM's statistics block, at this BN's channels
+        const Op& g = p.ops[op.stats_from];
+        op.stat_off = g.stat_block + (int64_t)tin_.coff * (int64_t)sizeof(double);
+        op.stat_ld = g.cout;
+      } else {
+        op.stat_off = take((size_t)4 * tin_.sh.C * sizeof(double));
+        op.stat_ld = tin_.sh.C;
+      }
       colpart = std::max(colpart, col_partial_bytes((int)tin_.sh.rows(), tin_.sh.C));
+    } else if (op.kind == OP_GAP) {
+      colpart = std::max(colpart, gap_partial_bytes(tin_.sh.n, tin_.sh.H, tin_.sh.W, tin_.sh.C));
     }
   }
   for (size_t t = 1; t < p.tensors.size(); ++t) {
@@ -581,6 +655,7 @@ struct HookScope {
 };
 
 const void* gemm_weights(xpipe_stage* st, const Op& op, int dir) {
+  if (!op.segs.empty()) return st->ws + op.wg_off[dir];
   if (st->dtype == DT_BF16) {
     int64_t off = dir == XPIPE_FWD ? st->bf_f_off : st->bf_b_off;
     return st->ws + off + (size_t)op.w_off * 2;
@@ -623,12 +698,11 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         a.pad = op.k / 2;
         a.relu = op.relu;
         int rows_tiles = 0;
-        if (op.stats_for >= 0) a.stat_part = (double*)(st->ws + st->colpart_off);
+        if (op.stats) a.stat_part = (double*)(st->ws + st->colpart_off);
         XP_HIP(launch_conv_gemm(dt, a, s, &rows_tiles));
-        if (op.stats_for >= 0) {
-          // the following BN's batch statistics from the epilogue's column sums
-          const Op& bn = st->ops[op.stats_for];
-          double* stats = (double*)(st->ws + bn.stat_off);
+        if (op.stats) {
+          // the following BNs' batch statistics from the epilogue's column sums
+          double* stats = (double*)(st->ws + op.stat_block);
           ColArgs ca{};
           ca.mode = COL_STATS;
           ca.M = (int)tin.sh.rows();
@@ -653,7 +727,7 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         ca.partial = (double*)(st->ws + st->colpart_off);
         ca.row_blocks = col_row_blocks(ca.M, ca.C);
         ca.out0 = stats;
-        ca.out1 = stats + tin.sh.C;
+        ca.out1 = stats + op.stat_ld;
         ca.eps = BN_EPS;
         if (!op.stats_fused) {
           XP_HIP(launch_colreduce(dt, ca, s));
@@ -663,7 +737,7 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         b.z = x.p;
         b.ldz = x.ld;
         b.mean = stats;
-        b.rstd = stats + tin.sh.C;
+        b.rstd = stats + op.stat_ld;
         b.gamma = fp32_param(st, op.g_off, dir);
         b.beta = fp32_param(st, op.be_off, dir);
         if (op.in2 >= 0) {
@@ -710,6 +784,7 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         pa.H = tin.sh.H;
         pa.W = tin.sh.W;
         pa.C = tin.sh.C;
+        pa.part = (double*)(st->ws + st->colpart_off);
         if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_fwd(dt, pa, s));
         else if (op.kind == OP_AVGPOOL) XP_HIP(launch_avgpool_fwd(dt, pa, s));
         else XP_HIP(launch_gap_fwd(dt, pa, s));
@@ -797,7 +872,18 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         w.x = x.p;
         w.ldx = x.ld;
         w.part = st->ws + st->wpart_off;
-        w.grad = st->grad + op.w_off;
+        if (op.segs.empty()) {
+          w.grad = st->grad + op.w_off;
+        } else {
+          w.nseg = (int)op.segs.size();
+          int r0 = 0;
+          for (int q = 0; q < w.nseg; ++q) {
+            w.seg_row0[q] = r0;
+            w.seg_grad[q] = st->grad + op.segs[q].first;
+            r0 += op.segs[q].second;
+          }
+          w.seg_row0[w.nseg] = r0;
+        }
         w.nb = tin.sh.n;
         w.H = tin.sh.H;
         w.W = tin.sh.W;
@@ -852,14 +938,15 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         ca.lda = g.ld;
         ca.z = x.p;
         ca.ldz = x.ld;
+        const int ld = op.stat_ld;
         ca.mean = stats;
-        ca.rstd = stats + C;
+        ca.rstd = stats + ld;
         ca.M = M;
         ca.C = C;
         ca.partial = (double*)(st->ws + st->colpart_off);
         ca.row_blocks = col_row_blocks(M, C);
-        ca.out0 = stats + 2 * C;
-        ca.out1 = stats + 3 * C;
+        ca.out0 = stats + 2 * ld;
+        ca.out1 = stats + 3 * ld;
         ca.grad0 = st->grad + op.g_off;
         ca.grad1 = st->grad + op.be_off;
         {
@@ -871,9 +958,9 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         b.z = x.p;
         b.ldz = x.ld;
         b.mean = stats;
-        b.rstd = stats + C;
-        b.dbeta = stats + 2 * C;
-        b.dgamma = stats + 3 * C;
+        b.rstd = stats + ld;
+        b.dbeta = stats + 2 * ld;
+        b.dgamma = stats + 3 * ld;
         b.gamma = fp32_param(st, op.g_off, dir);
         bool need_dz = want_grad(op.in);
         View dz = gradv(st, op.in, c);
@@ -1000,6 +1087,27 @@ AdamCoef adam_coef(const xpipe_hparams* hp) {
   a.bc2 = 1.0 / (1.0 - std::pow(hp->beta2, t));
   a.eps = hp->eps;
   return a;
+}
+
+// the merged GEMMs' weights, gathered from the prediction of direction dir
+xpipe_status refresh_gathered(xpipe_stage* st, int dir) {
+  for (const Op& op : st->ops) {
+    if (op.segs.empty()) continue;
+    GatherArgs g{};
+    g.nseg = (int)op.segs.size();
+    const int64_t K = (int64_t)op.k * op.k * op.cin;
+    for (int q = 0; q < g.nseg; ++q) {
+      const int64_t off = op.segs[q].first;
+      if (st->dtype == DT_BF16)
+        g.src[q] = st->ws + (dir == XPIPE_FWD ? st->bf_f_off : st->bf_b_off) + (size_t)off * 2;
+      else
+        g.src[q] = (dir == XPIPE_FWD ? st->wpf : st->wpb) + off;
+      g.count[q] = K * op.segs[q].second;
+    }
+    g.dst = st->ws + op.wg_off[dir];
+    XP_HIP(launch_gather(st->dtype, g, st->stream));
+  }
+  return XPIPE_OK;
 }
 
 xpipe_status refresh_flipped(xpipe_stage* st) {
@@ -1158,9 +1266,11 @@ xpipe_status xpipe_predict_weights(xpipe_stage_t st, int32_t which, int32_t s, c
   {
     XP_HIP(launch_predict(st->W, st->m, st->v, out, obf, st->P, c, st->stream));
   }
+  xpipe_status r = refresh_gathered(st, which);
+  if (r != XPIPE_OK) return r;
   st->pred_valid[which] = true;
   if (which == XPIPE_BWD) {
-    xpipe_status r = refresh_flipped(st);
+    r = refresh_flipped(st);
     if (r != XPIPE_OK) return r;
   }
   return XPIPE_OK;
@@ -1221,8 +1331,12 @@ xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t 
   st->bwd_since_step = 0;
   st->pred_valid[0] = st->pred_valid[1] = emit_pred != 0;
   st->wd_valid = false;
-  if (emit_pred) return refresh_flipped(st);
-  return XPIPE_OK;
+  if (!emit_pred) return XPIPE_OK;
+  for (int d = 0; d < 2; ++d) {
+    xpipe_status r = refresh_gathered(st, d);
+    if (r != XPIPE_OK) return r;
+  }
+  return refresh_flipped(st);
 }
 
 xpipe_status xpipe_stage_destroy(xpipe_stage_t st) {

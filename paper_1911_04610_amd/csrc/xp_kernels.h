@@ -50,6 +50,18 @@ hipError_t launch_adam(float* W, float* m, float* v, float* G, int64_t n, const 
                        int zero_grad, float* pf, bf16_t* pf_bf, const PredCoef& cf, float* pb,
                        bf16_t* pb_bf, const PredCoef& cb, hipStream_t s);
 
+// ---------------------------------------------------------------- weight gather
+// Copies nseg blocks of elements (storage dtype) back to back into dst: the
+// weights of sibling layers that share one GEMM launch.
+constexpr int GATHER_MAX_SEGS = 4;
+struct GatherArgs {
+  int nseg;
+  const void* src[GATHER_MAX_SEGS];
+  int64_t count[GATHER_MAX_SEGS];
+  void* dst;
+};
+hipError_t launch_gather(int dtype, const GatherArgs& a, hipStream_t s);
+
 // ---------------------------------------------------------------- GEMM engine
 // Forward-type implicit GEMM: y[m][n] = act(sum_{r,s,c} x[pix(m) + (r-pad, s-pad)][c] *
 // w[n][r][s][c] + bias[n]) over an nb x H x W image batch (stride 1, zero padding).
@@ -82,6 +94,11 @@ struct WgradArgs {
   float* grad;          // [N][K] fp32 accumulator
   int nb, H, W, C, N, R, S, pad;
   int splits;
+  // optional (nseg > 0): the N rows go to nseg accumulators in order, rows
+  // [seg_row0[j], seg_row0[j + 1]) to seg_grad[j] (seg_row0[0] = 0, seg_row0[nseg] = N)
+  int nseg;
+  int seg_row0[GATHER_MAX_SEGS + 1];
+  float* seg_grad[GATHER_MAX_SEGS];
 };
 
 // Work plan of one GEMM launch (tile shape picked on the host).
@@ -169,7 +186,9 @@ struct PoolArgs {
   const void* mask; int ldm;       // backward: mask for dx
   int accumulate;
   int nb, H, W, C;                 // input shape
+  double* part;                    // GAP forward: workspace, gap_partial_bytes
 };
+size_t gap_partial_bytes(int nb, int H, int W, int C);
 hipError_t launch_maxpool_fwd(int dtype, const PoolArgs& a, hipStream_t s);
 hipError_t launch_maxpool_bwd(int dtype, const PoolArgs& a, hipStream_t s);
 hipError_t launch_avgpool_fwd(int dtype, const PoolArgs& a, hipStream_t s);

@@ -91,6 +91,11 @@ def test_stage_query_rejects_bad_layer_lists():
     assert _bad([dict(kind="concat", inputs=[-1])]) == xp.EINVAL
     # concat of the stage input itself is not a layer output
     assert _bad([dict(kind="concat", inputs=[-1, -1])], shape=(4, 4, 4)) in (xp.EINVAL, xp.EUNSUPPORTED)
+    # a concat of a ReLU output and a plain conv output: its gradient would need
+    # the mask on some channels only
+    c1 = dict(conv, k=1)
+    assert _bad([c1, dict(kind="relu", inputs=[0]), c1,
+                 dict(kind="concat", inputs=[1, 2])]) == xp.EUNSUPPORTED
 
 
 def test_stage_create_checks_arguments_before_touching_the_device():

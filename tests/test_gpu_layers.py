@@ -38,6 +38,17 @@ LAYER_CASES = {
     "maxpool_even": ([dict(kind="maxpool2", inputs=[-1])], (10, 12, 64), 2),
     "maxpool_odd": ([dict(kind="maxpool2", inputs=[-1])], (9, 11, 32), 2),
     "avgpool3": ([dict(kind="avgpool3", inputs=[-1])], (9, 9, 64), 2),
+    # rows of 15 = two full sliding-window runs of 7 and a ragged run of 1
+    "avgpool3_ragged_rows": ([dict(kind="avgpool3", inputs=[-1])], (5, 15, 32), 2),
+    "avgpool3_single_pixel": ([dict(kind="avgpool3", inputs=[-1])], (1, 1, 16), 3),
+    "avgpool3_after_concat": ([conv(-1, 32, 32, 1), conv(-1, 32, 16, 3),
+                               dict(kind="concat", inputs=[0, 1]),
+                               dict(kind="avgpool3", inputs=[2]), conv(3, 48, 32, 1)],
+                              (6, 8, 32), 2),
+    # 35 x 35 pixels: the average pool's partial sums split the pixels
+    "head_gap_many_pixels": ([dict(kind="gap", inputs=[-1]),
+                              dict(kind="linear", inputs=[0], cin=64, cout=10, bias=True),
+                              dict(kind="softmax_ce", inputs=[1], classes=10)], (35, 35, 64), 2),
     "head_gap_linear_ce": ([dict(kind="gap", inputs=[-1]),
                             dict(kind="linear", inputs=[0], cin=256, cout=200, bias=True),
                             dict(kind="softmax_ce", inputs=[1], classes=200)], (7, 7, 256), 4),
@@ -45,6 +56,15 @@ LAYER_CASES = {
                     dict(kind="softmax_ce", inputs=[0], classes=10)], (256,), 32),
     "concat_views": ([conv(-1, 64, 64, 1), conv(-1, 64, 32, 3),
                       dict(kind="concat", inputs=[0, 1]), conv(2, 96, 48, 1)], (8, 8, 64), 2),
+    # two 1x1 siblings on one input share a launch in bf16 (channel-slice outputs)
+    "siblings_merged_bn": ([conv(-1, 64, 32, 1), dict(kind="bn", inputs=[0], cin=32, cout=32),
+                            dict(kind="relu", inputs=[1]),
+                            conv(-1, 64, 16, 1), dict(kind="bn", inputs=[3], cin=16, cout=16),
+                            dict(kind="relu", inputs=[4]), conv(5, 16, 24, 3),
+                            dict(kind="relu", inputs=[6]),
+                            dict(kind="avgpool3", inputs=[-1]), conv(8, 64, 8, 1),
+                            dict(kind="bn", inputs=[9], cin=8, cout=8), dict(kind="relu", inputs=[10]),
+                            dict(kind="concat", inputs=[2, 7, 11])], (7, 9, 64), 2),
     "add_relu_elementwise": ([conv(-1, 32, 32, 1), dict(kind="add", inputs=[0, -1]),
                               dict(kind="relu", inputs=[1])], (6, 7, 32), 2),
     "pool_then_relu": ([dict(kind="maxpool2", inputs=[-1]), dict(kind="relu", inputs=[0])],

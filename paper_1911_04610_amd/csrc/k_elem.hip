@@ -886,25 +886,27 @@ __global__ __launch_bounds__(256) void k_gap_part_v(PoolArgs a, int splits) {
   }
 }
 
+// one wave per (image, channel chunk): lane q holds split q, the wave adds the
+// splits in a fixed butterfly order
 template <typename T>
 __global__ __launch_bounds__(256) void k_gap_fin_v(PoolArgs a, int splits) {
   constexpr int N = VT<T>::N;
   const int chunks = a.C / N;
-  const int it = blockIdx.x * blockDim.x + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int it = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (it >= a.nb * chunks) return;
   const int n = it / chunks, c0 = (it - n * chunks) * N;
   double t[N];
 #pragma unroll
   for (int e = 0; e < N; ++e) t[e] = 0.0;
-  for (int q = 0; q < splits; ++q) {
-    const double* P = a.part + ((size_t)n * splits + q) * a.C + c0;
+  if (lane < splits) {
+    const double* P = a.part + ((size_t)n * splits + lane) * a.C + c0;
 #pragma unroll
-    for (int e = 0; e < N; ++e) t[e] += P[e];
+    for (int e = 0; e < N; ++e) t[e] = P[e];
   }
-  const int HW = a.H * a.W;
 #pragma unroll
-  for (int e = 0; e < N; ++e) t[e] = t[e] / HW;
-  vst((T*)a.out + (size_t)n * a.ldo + c0, t);
+  for (int e = 0; e < N; ++e) t[e] = wave_sum(t[e]) / (a.H * a.W);
+  if (lane == 0) vst((T*)a.out + (size_t)n * a.ldo + c0, t);
 }
 
 template <typename T>
@@ -1114,7 +1116,7 @@ hipError_t launch_gap_fwd(int dtype, const PoolArgs& a, hipStream_t s) {
     dim3 grid(splits, a.nb, colblocks);
     const double gb = (double)a.nb * a.H * a.W * a.C * (dtype == DT_BF16 ? 2 : 4);
     const double fb = (double)a.nb * splits * a.C * 8;
-    const int fblocks = ceil_div(a.nb * chunks, 256);
+    const int fblocks = ceil_div(a.nb * chunks, 4);
     if (dtype == DT_BF16) {
       XP_LAUNCH("k_gap_part_v<bf16>", gb, k_gap_part_v<bf16_t>, grid, dim3(256), 0, s, a, splits);
       XP_LAUNCH("k_gap_fin_v<bf16>", fb, k_gap_fin_v<bf16_t>, dim3(fblocks), dim3(256), 0, s, a, splits);

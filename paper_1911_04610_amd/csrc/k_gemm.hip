@@ -22,6 +22,7 @@
 // second kernel adds the splits in a fixed order into the fp32 gradient
 // accumulator (deterministic, no atomics).
 #include "xp_device.h"
+#include <type_traits>
 #include "xp_kernels.h"
 
 #include <cstdio>
@@ -73,13 +74,27 @@ XP_DEV uint4 pack_chunk<float>(const float* v) {
 // KS sets the stage depth BK = KS x 32 (bf16: one v_mfma_f32_16x16x32_bf16 per
 // 32) or KS x 16 (fp32 storage: four v_mfma_f64_16x16x4f64 per 16); deeper
 // stages keep more bytes in flight per barrier.
-template <typename T, int BM, int BN, int WM, int WN, bool FLAT, int KS>
+// LDS row padding of the bf16 operand tiles, in elements
+#ifndef XP_GEMM_LDS_PAD_BF16
+#define XP_GEMM_LDS_PAD_BF16 16
+#endif
+
+// calls f(integral_constant<int, I>) for I = B .. E-1
+template <int B, int E, typename F>
+XP_DEV void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+template <typename T, int BM, int BN, int WM, int WN, bool FLAT, int KS, int PF>
 __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   using MTT = MT<T>;
   constexpr int VEC = MTT::VEC;
   constexpr int SUB = sizeof(T) == 2 ? 32 : 16;
   constexpr int BK = KS * SUB;
-  constexpr int PITCH = BK + (sizeof(T) == 2 ? 8 : 4);
+  constexpr int PITCH = BK + (sizeof(T) == 2 ? XP_GEMM_LDS_PAD_BF16 : 4);
   constexpr int CPR = BK / VEC;  // chunks per tile row per step
   constexpr int A_CH = BM * CPR, B_CH = BN * CPR;
   constexpr int A_PER = (A_CH + 255) / 256, B_PER = (B_CH + 255) / 256;
@@ -126,31 +141,79 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     b_valid[i] = b_slot[i] && (n0 + b_row[i]) < a.N;
   }
 
+  // Buffer-load addressing (16-byte chunk path): the input and weight views
+  // are raw buffer resources whose loads return zeros past num_records, so a
+  // chunk outside the image or past the channels is read from offset
+  // OUT_OF_RANGE instead of being branched around.  Per thread: the byte
+  // offset of each chunk's pixel, and one bit per filter row (column) telling
+  // whether that row (column) of taps lands inside the image.
+  constexpr uint32_t OUT_OF_RANGE = 0x80000000u;
+  uint32_t a_off[A_PER], b_off[B_PER], a_hm[A_PER], a_wm[A_PER];
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)x, (short)0, (int)((((size_t)(M - 1)) * a.ldx + C) * sizeof(T)), 0x00020000);
+  const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)w, (short)0, (int)((size_t)a.N * K * sizeof(T)), 0x00020000);
+  if constexpr (!FLAT) {
+#pragma unroll
+    for (int i = 0; i < A_PER; ++i) {
+      a_off[i] = (uint32_t)((((size_t)(a_img[i] * H + a_h[i]) * W + a_w[i]) * a.ldx + a_kc[i] * VEC) *
+                            sizeof(T));
+      uint32_t hm = 0, wm = 0;
+      if (a_valid[i]) {
+        for (int r = 0; r < a.R; ++r)
+          hm |= (uint32_t)((unsigned)(a_h[i] + r - pad) < (unsigned)H) << r;
+        for (int q = 0; q < S; ++q)
+          wm |= (uint32_t)((unsigned)(a_w[i] + q - pad) < (unsigned)W) << q;
+      }
+      a_hm[i] = hm;
+      a_wm[i] = wm;
+    }
+#pragma unroll
+    for (int i = 0; i < B_PER; ++i)
+      b_off[i] = b_valid[i] ? (uint32_t)(((size_t)(n0 + b_row[i]) * K + b_kc[i] * VEC) * sizeof(T))
+                            : OUT_OF_RANGE;
+  }
+
   const int nCB = FLAT ? 1 : (C + BK - 1) / BK;
   const int nk = FLAT ? (K + BK - 1) / BK : a.R * S * nCB;
 
-  uint4 ra[A_PER], rb[B_PER];
+  // PF register slots: the global loads of PF k-tiles are in flight at once.
+  uint4 ra[PF][A_PER], rb[PF][B_PER];
+  // position of the next k-tile to load (16-byte chunk path): filter row lr,
+  // column lq, channel block lcb; advanced once per load, held at the last tile
+  int lr = 0, lq = 0, lcb = 0, lrs = 0, loaded = 0;
 
-  auto gload = [&](int kb) {
+  // slot indices are compile-time constants so the register ring is not spilled
+  auto gload = [&](int kb, auto SLOT) __attribute__((always_inline)) {
+    constexpr int slot = decltype(SLOT)::value;
     if constexpr (!FLAT) {
-      int rs = kb / nCB, cb = kb - rs * nCB;
-      int r = rs / S, s = rs - r * S;
+      (void)kb;
+      const int crem = C - lcb * BK;  // channels left in this tap from this block on
+      const int dx = (((lr - pad) * W + (lq - pad)) * a.ldx + lcb * BK) * (int)sizeof(T);
+      const uint32_t dw = (uint32_t)((lrs * C + lcb * BK) * (int)sizeof(T));
 #pragma unroll
       for (int i = 0; i < A_PER; ++i) {
-        uint4 v = make_uint4(0, 0, 0, 0);
-        int c = cb * BK + a_kc[i] * VEC;
-        int hh = a_h[i] + r - pad, ww = a_w[i] + s - pad;
-        if (a_valid[i] && c < C && hh >= 0 && hh < H && ww >= 0 && ww < W)
-          v = *reinterpret_cast<const uint4*>(x + ((size_t)(a_img[i] * H + hh) * W + ww) * a.ldx + c);
-        ra[i] = v;
+        const bool ok = ((a_hm[i] >> lr) & (a_wm[i] >> lq) & 1u) && a_kc[i] * VEC < crem;
+        const uint32_t off = ok ? a_off[i] + (uint32_t)dx : OUT_OF_RANGE;
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(xr, (int)off, 0, 0);
+        ra[slot][i] = make_uint4(v[0], v[1], v[2], v[3]);
       }
 #pragma unroll
       for (int i = 0; i < B_PER; ++i) {
-        uint4 v = make_uint4(0, 0, 0, 0);
-        int c = cb * BK + b_kc[i] * VEC;
-        if (b_valid[i] && c < C)
-          v = *reinterpret_cast<const uint4*>(w + (size_t)(n0 + b_row[i]) * K + rs * C + c);
-        rb[i] = v;
+        const bool ok = b_kc[i] * VEC < crem;
+        const uint32_t off = ok ? b_off[i] + dw : OUT_OF_RANGE;
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0);
+        rb[slot][i] = make_uint4(v[0], v[1], v[2], v[3]);
+      }
+      if (++loaded < nk) {
+        if (++lcb == nCB) {
+          lcb = 0;
+          ++lrs;
+          if (++lq == S) {
+            lq = 0;
+            ++lr;
+          }
+        }
       }
     } else {
 #pragma unroll
@@ -169,7 +232,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
           }
           vals[e] = val;
         }
-        ra[i] = pack_chunk<T>(vals);
+        ra[slot][i] = pack_chunk<T>(vals);
       }
 #pragma unroll
       for (int i = 0; i < B_PER; ++i) {
@@ -179,17 +242,18 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
           int k = kb * BK + b_kc[i] * VEC + e;
           vals[e] = (b_valid[i] && k < K) ? w[(size_t)(n0 + b_row[i]) * K + k] : zero_elem<T>();
         }
-        rb[i] = pack_chunk<T>(vals);
+        rb[slot][i] = pack_chunk<T>(vals);
       }
     }
   };
-  auto lstore = [&](int buf) {
+  auto lstore = [&](auto SLOT, int buf) __attribute__((always_inline)) {
+    constexpr int slot = decltype(SLOT)::value;
 #pragma unroll
     for (int i = 0; i < A_PER; ++i)
-      if (a_slot[i]) *reinterpret_cast<uint4*>(&sA[buf][a_row[i] * PITCH + a_kc[i] * VEC]) = ra[i];
+      if (a_slot[i]) *reinterpret_cast<uint4*>(&sA[buf][a_row[i] * PITCH + a_kc[i] * VEC]) = ra[slot][i];
 #pragma unroll
     for (int i = 0; i < B_PER; ++i)
-      if (b_slot[i]) *reinterpret_cast<uint4*>(&sB[buf][b_row[i] * PITCH + b_kc[i] * VEC]) = rb[i];
+      if (b_slot[i]) *reinterpret_cast<uint4*>(&sB[buf][b_row[i] * PITCH + b_kc[i] * VEC]) = rb[slot][i];
   };
 
   typename MTT::acc_t acc[TM][TN];
@@ -200,7 +264,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) acc[i][j][q] = 0;
 
-  auto compute = [&](int buf) {
+  auto compute = [&](int buf) __attribute__((always_inline)) {
     const T* A = sA[buf];
     const T* B = sB[buf];
     if constexpr (sizeof(T) == 2) {
@@ -240,16 +304,36 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     }
   };
 
-  gload(0);
-  lstore(0);
+  // k-tile j is loaded into register slot j % PF, PF tiles ahead of its use,
+  // and staged into LDS buffer j & 1 one step ahead
+  // Loads are issued unconditionally (the last tile is re-read past the end)
+  // so that the only waits are for the tile about to be staged.
+  static_for<0, PF>([&](auto J) __attribute__((always_inline)) {
+    gload(min((int)decltype(J)::value, nk - 1), J);
+  });
+  lstore(std::integral_constant<int, 0>{}, 0);
   __syncthreads();
-  for (int kb = 0; kb < nk; ++kb) {
-    const bool more = kb + 1 < nk;
-    if (more) gload(kb + 1);
-    compute(kb & 1);
-    if (more) lstore((kb + 1) & 1);
-    __syncthreads();
+  int kb0 = 0;
+  for (; kb0 + PF <= nk; kb0 += PF) {
+    static_for<0, PF>([&](auto U) __attribute__((always_inline)) {
+      constexpr int u = decltype(U)::value;
+      const int kb = kb0 + u;
+      // slot u held tile kb, already in LDS
+      gload(min(kb + PF, nk - 1), U);
+      compute(kb & 1);
+      if (kb + 1 < nk) lstore(std::integral_constant<int, (u + 1) % PF>{}, (kb + 1) & 1);
+      __syncthreads();
+    });
   }
+  static_for<0, PF>([&](auto U) __attribute__((always_inline)) {
+    constexpr int u = decltype(U)::value;
+    const int kb = kb0 + u;
+    if (kb < nk) {
+      compute(kb & 1);
+      if (kb + 1 < nk) lstore(std::integral_constant<int, (u + 1) % PF>{}, (kb + 1) & 1);
+      __syncthreads();
+    }
+  });
 
   // epilogue: bias, ReLU, mask, accumulate, round once on store
   T* __restrict__ y = (T*)a.y;
@@ -495,7 +579,7 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) acc[i][j][q] = 0;
 
-  auto compute = [&](int buf) {
+  auto compute = [&](int buf) __attribute__((always_inline)) {
     const T* A = sA[buf];
     const T* B = sB[buf];
     if constexpr (BF) {
@@ -638,10 +722,8 @@ __global__ __launch_bounds__(256) void k_flip(const T* __restrict__ w, T* __rest
 // ============================================================================
 // host launchers
 // ============================================================================
-// Tile choice, from a sweep of the stage shapes on MI355X: 64 columns (32 when
-// N <= 32); 32 or 64 rows depending on the stage depth (see conv_dispatch); the
-// bf16 stage depth minimises the zero padding of each tap's channel run while
-// keeping at least four pipeline stages when possible.
+// The bf16 stage depth minimises the zero padding of each tap's channel run
+// while keeping at least four pipeline stages when possible.
 static int pick_ks_bf16(int C, int taps) {
   // score: (at least 4 stages, least padding, then larger KS if >= 4 stages,
   // else more stages)
@@ -664,14 +746,14 @@ static int pick_ks_bf16(int C, int taps) {
 
 template <typename T> static const char* tname() { return sizeof(T) == 2 ? "bf16" : "f32"; }
 
-template <typename T, int BM, int BN, int WM, int WN, bool FLAT, int KS = 0>
+template <typename T, int BM, int BN, int WM, int WN, bool FLAT, int KS = 0, int PF = 0>
 static const char* kname(const char* base) {
   static char buf[96];
   static bool init = false;
   if (!init) {
     if (KS)
-      snprintf(buf, sizeof buf, "%s<%s,%d,%d,%d,%d,%s,%d>", base, tname<T>(), BM, BN, WM, WN,
-               FLAT ? "true" : "false", KS);
+      snprintf(buf, sizeof buf, "%s<%s,%d,%d,%d,%d,%s,%d,%d>", base, tname<T>(), BM, BN, WM, WN,
+               FLAT ? "true" : "false", KS, PF);
     else
       snprintf(buf, sizeof buf, "%s<%s,%d,%d,%d,%d,%s>", base, tname<T>(), BM, BN, WM, WN,
                FLAT ? "true" : "false");
@@ -680,18 +762,18 @@ static const char* kname(const char* base) {
   return buf;
 }
 
-template <typename T, int BM, int BN, int WM, int WN, int KS>
+template <typename T, int BM, int BN, int WM, int WN, int KS, int PF = 1>
 static hipError_t conv_go(const ConvArgs& a, bool flat, hipStream_t s, int* grid_rows = nullptr) {
   int M = a.nb * a.H * a.W;
   dim3 grid((M + BM - 1) / BM, (a.N + BN - 1) / BN);
   if (grid_rows) *grid_rows = (int)grid.x;
   double flops = 2.0 * M * (double)a.N * a.R * a.S * a.C;
   if (flat)
-    XP_LAUNCH((kname<T, BM, BN, WM, WN, true, KS>("k_conv_gemm")), flops,
-              (k_conv_gemm<T, BM, BN, WM, WN, true, KS>), grid, dim3(256), 0, s, a);
+    XP_LAUNCH((kname<T, BM, BN, WM, WN, true, KS, PF>("k_conv_gemm")), flops,
+              (k_conv_gemm<T, BM, BN, WM, WN, true, KS, PF>), grid, dim3(256), 0, s, a);
   else
-    XP_LAUNCH((kname<T, BM, BN, WM, WN, false, KS>("k_conv_gemm")), flops,
-              (k_conv_gemm<T, BM, BN, WM, WN, false, KS>), grid, dim3(256), 0, s, a);
+    XP_LAUNCH((kname<T, BM, BN, WM, WN, false, KS, PF>("k_conv_gemm")), flops,
+              (k_conv_gemm<T, BM, BN, WM, WN, false, KS, PF>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -703,17 +785,27 @@ static hipError_t conv_dispatch(const ConvArgs& a, hipStream_t s, int* gr) {
               (reinterpret_cast<uintptr_t>(a.w) % 16) != 0;
   const bool narrow = a.N <= 32;
   if constexpr (sizeof(T) == 2) {
-    // one-stage depth (KS = 1) runs best with 64-row tiles; deeper stages with
-    // 32-row tiles, which double the workgroups in flight for these skinny layers
-    const int ks = flat ? 1 : pick_ks_bf16(a.C, a.R * a.S);
+    // From a sweep of the stage shapes on MI355X (tile, stage depth KS,
+    // register prefetch depth PF)
+    const int taps = a.R * a.S;
+    const int ks = flat ? 1 : pick_ks_bf16(a.C, taps);
     if (narrow) {
-      if (ks == 4) return conv_go<T, 32, 32, 2, 2, 4>(a, flat, s, gr);
-      if (ks == 2) return conv_go<T, 32, 32, 2, 2, 2>(a, flat, s, gr);
-      return conv_go<T, 64, 32, 2, 2, 1>(a, flat, s, gr);
+      if (ks == 4) return conv_go<T, 32, 32, 2, 2, 4, 3>(a, flat, s, gr);
+      if (ks == 2) return conv_go<T, 32, 32, 2, 2, 2, 3>(a, flat, s, gr);
+      return conv_go<T, 64, 32, 2, 2, 1, 2>(a, flat, s, gr);
     }
-    if (ks == 4) return conv_go<T, 32, 64, 2, 2, 4>(a, flat, s, gr);
-    if (ks == 2) return conv_go<T, 32, 64, 2, 2, 2>(a, flat, s, gr);
-    return conv_go<T, 64, 64, 2, 2, 1>(a, flat, s, gr);
+    if (!flat && taps > 1 && taps < 25 && a.N > 64)
+      return conv_go<T, 128, 64, 4, 1, 1, 4>(a, flat, s, gr);
+    if (ks == 1) {
+      if (taps > 1) return conv_go<T, 128, 64, 4, 1, 1, 4>(a, flat, s, gr);
+      return conv_go<T, 64, 64, 2, 2, 1, 2>(a, flat, s, gr);
+    }
+    if (taps >= 25) {
+      if (ks == 4) return conv_go<T, 64, 64, 2, 2, 4, 2>(a, flat, s, gr);
+      return conv_go<T, 64, 64, 2, 2, 2, 2>(a, flat, s, gr);
+    }
+    if (ks == 4) return conv_go<T, 32, 64, 2, 2, 4, 2>(a, flat, s, gr);
+    return conv_go<T, 32, 64, 2, 2, 2, 2>(a, flat, s, gr);
   } else {
     if (narrow) return conv_go<T, 64, 32, 2, 2, 1>(a, flat, s, gr);
     return conv_go<T, 64, 64, 2, 2, 1>(a, flat, s, gr);

@@ -641,6 +641,224 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
       }
 }
 
+// bf16 weight gradient, 16-byte chunk path (channels, output channels and row
+// strides multiples of 8, views below 2 GiB).  Same tiles and LDS layout as
+// k_wgrad; the operands load through raw buffer resources (out-of-range
+// offsets read zeros), addresses advance by a scalar per step, each thread
+// tracks the image row / column of its pixels incrementally, and PF steps of
+// loads are in flight.
+template <int BM, int BN, int WM, int WN, int PF>
+__global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
+  using T = bf16_t;
+  constexpr int VEC = 8, BKm = 32, RPT = 2;
+  constexpr int PA = BKm + 8, PB = BKm + 8;
+  __shared__ __align__(16) T sA[2][BM * PA];
+  __shared__ __align__(16) T sB[2][BN * PB];
+  constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
+  static_assert(WM * WN == 4, "four waves");
+  constexpr int A_T = (BKm / 2) * (BM / VEC), B_T = (BKm / 2) * (BN / VEC);
+  constexpr int A_PER = (A_T + 255) / 256, B_PER = (B_T + 255) / 256;
+  constexpr uint32_t OUT_OF_RANGE = 0x80000000u;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int H = a.H, W = a.W, C = a.C, S = a.S, pad = a.pad, N = a.N;
+  const int M = a.nb * H * W;
+  const int K = a.R * S * C;
+  const int n0 = blockIdx.x * BM, k0 = blockIdx.y * BN;
+  const int mps = ((M + a.splits - 1) / a.splits + BKm - 1) / BKm * BKm;
+  const int mbeg = blockIdx.z * mps;
+  const int mend = min(M, mbeg + mps);
+  const __amdgpu_buffer_rsrc_t dr = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)a.dz, (short)0, (int)((((size_t)(M - 1)) * a.lddz + N) * sizeof(T)), 0x00020000);
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)a.x, (short)0, (int)((((size_t)(M - 1)) * a.ldx + C) * sizeof(T)), 0x00020000);
+
+  // A tasks (dz): pixel pair p, output-channel chunk c
+  int a_p[A_PER], a_c[A_PER];
+  uint32_t a_off[A_PER];
+  bool a_slot[A_PER], a_nok[A_PER];
+#pragma unroll
+  for (int i = 0; i < A_PER; ++i) {
+    const int q = tid + i * 256;
+    a_slot[i] = q < A_T;
+    a_c[i] = q % (BM / VEC);
+    a_p[i] = q / (BM / VEC);
+    const int n = n0 + a_c[i] * VEC;
+    a_nok[i] = a_slot[i] && n < N;
+    a_off[i] = (uint32_t)((((size_t)mbeg + a_p[i] * RPT) * a.lddz + n) * sizeof(T));
+  }
+  // B tasks (x): pixel pair p, reduction chunk (tap r, s, channel ch)
+  int b_p[B_PER], b_c[B_PER], b_r[B_PER], b_s[B_PER];
+  int b_h[B_PER][RPT], b_w[B_PER][RPT];
+  uint32_t b_off[B_PER];
+  bool b_slot[B_PER], b_kok[B_PER];
+#pragma unroll
+  for (int i = 0; i < B_PER; ++i) {
+    const int q = tid + i * 256;
+    b_slot[i] = q < B_T;
+    b_c[i] = q % (BN / VEC);
+    b_p[i] = q / (BN / VEC);
+    const int kk = k0 + b_c[i] * VEC;
+    b_kok[i] = b_slot[i] && kk < K;
+    const int rs = b_kok[i] ? kk / C : 0, ch = b_kok[i] ? kk - rs * C : 0;
+    b_r[i] = rs / S;
+    b_s[i] = rs - b_r[i] * S;
+    // byte offset of (first pixel of the pair at step 0, shifted by the tap)
+    const long long pix = (long long)mbeg + b_p[i] * RPT + (b_r[i] - pad) * W + (b_s[i] - pad);
+    b_off[i] = (uint32_t)((pix * a.ldx + ch) * (long long)sizeof(T));
+#pragma unroll
+    for (int u = 0; u < RPT; ++u) {
+      const int m = mbeg + b_p[i] * RPT + u;
+      const int rem = m % (H * W);
+      b_h[i][u] = rem / W;
+      b_w[i][u] = rem - b_h[i][u] * W;
+    }
+  }
+
+  uint4 ra[PF][A_PER][RPT], rb[PF][B_PER][RPT];
+  int loaded = 0;  // steps loaded so far
+
+  auto gload = [&](auto SLOT) __attribute__((always_inline)) {
+    constexpr int slot = decltype(SLOT)::value;
+    const int mb = loaded * BKm;  // pixel offset of this step from mbeg
+    const int left = mend - mbeg - mb;
+#pragma unroll
+    for (int i = 0; i < A_PER; ++i)
+#pragma unroll
+      for (int u = 0; u < RPT; ++u) {
+        const bool ok = a_nok[i] && a_p[i] * RPT + u < left;
+        const uint32_t off =
+            ok ? a_off[i] + (uint32_t)(((size_t)mb + u) * a.lddz * sizeof(T)) : OUT_OF_RANGE;
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(dr, (int)off, 0, 0);
+        ra[slot][i][u] = make_uint4(v[0], v[1], v[2], v[3]);
+      }
+#pragma unroll
+    for (int i = 0; i < B_PER; ++i)
+#pragma unroll
+      for (int u = 0; u < RPT; ++u) {
+        const int hh = b_h[i][u] + b_r[i] - pad, ww = b_w[i][u] + b_s[i] - pad;
+        const bool ok = b_kok[i] && b_p[i] * RPT + u < left && (unsigned)hh < (unsigned)H &&
+                        (unsigned)ww < (unsigned)W;
+        const uint32_t off =
+            ok ? b_off[i] + (uint32_t)(((size_t)mb + u) * a.ldx * sizeof(T)) : OUT_OF_RANGE;
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(xr, (int)off, 0, 0);
+        rb[slot][i][u] = make_uint4(v[0], v[1], v[2], v[3]);
+        // advance this pixel by one step
+        int w2 = b_w[i][u] + BKm, h2 = b_h[i][u];
+        while (w2 >= W) {
+          w2 -= W;
+          if (++h2 == H) h2 = 0;
+        }
+        b_w[i][u] = w2;
+        b_h[i][u] = h2;
+      }
+    ++loaded;
+  };
+
+  auto lstore = [&](auto SLOT, int buf) __attribute__((always_inline)) {
+    constexpr int slot = decltype(SLOT)::value;
+    // interleave two pixels: word e of row (chunk*8 + e) holds (pixel 2p, pixel 2p+1)
+#pragma unroll
+    for (int i = 0; i < A_PER; ++i) {
+      if (!a_slot[i]) continue;
+      const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&ra[slot][i][0]);
+      const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&ra[slot][i][1]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t lo = __builtin_amdgcn_perm(r1[j], r0[j], 0x05040100u);
+        const uint32_t hi = __builtin_amdgcn_perm(r1[j], r0[j], 0x07060302u);
+        const int row = a_c[i] * VEC + 2 * j;
+        *reinterpret_cast<uint32_t*>(&sA[buf][row * PA + 2 * a_p[i]]) = lo;
+        *reinterpret_cast<uint32_t*>(&sA[buf][(row + 1) * PA + 2 * a_p[i]]) = hi;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < B_PER; ++i) {
+      if (!b_slot[i]) continue;
+      const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&rb[slot][i][0]);
+      const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&rb[slot][i][1]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t lo = __builtin_amdgcn_perm(r1[j], r0[j], 0x05040100u);
+        const uint32_t hi = __builtin_amdgcn_perm(r1[j], r0[j], 0x07060302u);
+        const int row = b_c[i] * VEC + 2 * j;
+        *reinterpret_cast<uint32_t*>(&sB[buf][row * PB + 2 * b_p[i]]) = lo;
+        *reinterpret_cast<uint32_t*>(&sB[buf][(row + 1) * PB + 2 * b_p[i]]) = hi;
+      }
+    }
+  };
+
+  f32x4_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[i][j][q] = 0.f;
+
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+    const T* A = sA[buf];
+    const T* B = sB[buf];
+    bf16x8_t af[TM], bfv[TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+      af[i] = *reinterpret_cast<const bf16x8_t*>(&A[(wm * WTM + i * 16 + (lane & 15)) * PA + (lane >> 4) * 8]);
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      bfv[j] = *reinterpret_cast<const bf16x8_t*>(&B[(wn * WTN + j * 16 + (lane & 15)) * PB + (lane >> 4) * 8]);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfv[j], acc[i][j], 0, 0, 0);
+  };
+
+  const int nsteps = mend > mbeg ? (mend - mbeg + BKm - 1) / BKm : 0;
+  if (nsteps > 0) {
+    // step j loads into slot j % PF; the last step is re-read past the end
+    static_for<0, PF>([&](auto J) __attribute__((always_inline)) {
+      if (decltype(J)::value >= nsteps) loaded = nsteps - 1;
+      gload(J);
+    });
+    lstore(std::integral_constant<int, 0>{}, 0);
+    __syncthreads();
+    int st0 = 0;
+    for (; st0 + PF <= nsteps; st0 += PF) {
+      static_for<0, PF>([&](auto U) __attribute__((always_inline)) {
+        constexpr int u = decltype(U)::value;
+        const int st = st0 + u;
+        if (st + PF >= nsteps) loaded = nsteps - 1;
+        gload(U);
+        compute(st & 1);
+        if (st + 1 < nsteps) lstore(std::integral_constant<int, (u + 1) % PF>{}, (st + 1) & 1);
+        __syncthreads();
+      });
+    }
+    static_for<0, PF>([&](auto U) __attribute__((always_inline)) {
+      constexpr int u = decltype(U)::value;
+      const int st = st0 + u;
+      if (st < nsteps) {
+        compute(st & 1);
+        if (st + 1 < nsteps) lstore(std::integral_constant<int, (u + 1) % PF>{}, (st + 1) & 1);
+        __syncthreads();
+      }
+    });
+  }
+
+  float* part = (float*)a.part + (size_t)blockIdx.z * N * K;
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int n = n0 + wm * WTM + i * 16 + MT<T>::out_row(lane, q);
+        const int k = k0 + wn * WTN + j * 16 + (lane & 15);
+        if (n < N && k < K) part[(size_t)n * K + k] = acc[i][j][q];
+      }
+}
+
 // grad[i] += sum over splits of part[z][i], splits added in order z = 0, 1, ...;
 // each thread owns four consecutive outputs so the partial reads are 16-32 B
 // Destination rows of the weight gradient: one accumulator, or several
@@ -780,9 +998,13 @@ static hipError_t conv_go(const ConvArgs& a, bool flat, hipStream_t s, int* grid
 template <typename T>
 static hipError_t conv_dispatch(const ConvArgs& a, hipStream_t s, int* gr) {
   constexpr int VEC = MT<T>::VEC;
+  const size_t M = (size_t)a.nb * a.H * a.W;
+  // the 16-byte chunk path addresses both operands with 32-bit buffer offsets
+  const bool spans = ((M - 1) * a.ldx + a.C) * sizeof(T) < ((size_t)1 << 31) &&
+                     (size_t)a.N * a.R * a.S * a.C * sizeof(T) < ((size_t)1 << 31);
   bool flat = (a.C % VEC) != 0 || (a.ldx % VEC) != 0 ||
               (reinterpret_cast<uintptr_t>(a.x) % 16) != 0 ||
-              (reinterpret_cast<uintptr_t>(a.w) % 16) != 0;
+              (reinterpret_cast<uintptr_t>(a.w) % 16) != 0 || !spans;
   const bool narrow = a.N <= 32;
   if constexpr (sizeof(T) == 2) {
     // From a sweep of the stage shapes on MI355X (tile, stage depth KS,
@@ -842,19 +1064,12 @@ size_t wgrad_part_bytes(int dtype, int N, int K, int splits) {
   return (size_t)splits * N * K * (dtype == DT_BF16 ? sizeof(float) : sizeof(double));
 }
 
-template <typename T, int BM, int BN, int WM, int WN>
-static hipError_t wgrad_go(const WgradArgs& a, bool flat, hipStream_t s) {
-  int K = a.R * a.S * a.C;
-  dim3 grid((a.N + BM - 1) / BM, (K + BN - 1) / BN, a.splits);
-  double flops = 2.0 * a.nb * a.H * a.W * (double)a.N * K;
-  if (flat)
-    XP_LAUNCH((kname<T, BM, BN, WM, WN, true>("k_wgrad")), flops, (k_wgrad<T, BM, BN, WM, WN, true>),
-              grid, dim3(256), 0, s, a);
-  else
-    XP_LAUNCH((kname<T, BM, BN, WM, WN, false>("k_wgrad")), flops, (k_wgrad<T, BM, BN, WM, WN, false>),
-              grid, dim3(256), 0, s, a);
+// grad (+)= the fixed-order sum of the launch's split partials
+template <typename T>
+static hipError_t wgrad_reduce(const WgradArgs& a, hipStream_t s) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const int K = a.R * a.S * a.C;
   int64_t count = (int64_t)a.N * K;
   int blocks = (int)(((count + 3) / 4 + 255) / 256);
   typedef typename MT<T>::part_t P;
@@ -875,6 +1090,30 @@ static hipError_t wgrad_go(const WgradArgs& a, bool flat, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <typename T, int BM, int BN, int WM, int WN>
+static hipError_t wgrad_go(const WgradArgs& a, bool flat, hipStream_t s) {
+  int K = a.R * a.S * a.C;
+  dim3 grid((a.N + BM - 1) / BM, (K + BN - 1) / BN, a.splits);
+  double flops = 2.0 * a.nb * a.H * a.W * (double)a.N * K;
+  if (flat)
+    XP_LAUNCH((kname<T, BM, BN, WM, WN, true>("k_wgrad")), flops, (k_wgrad<T, BM, BN, WM, WN, true>),
+              grid, dim3(256), 0, s, a);
+  else
+    XP_LAUNCH((kname<T, BM, BN, WM, WN, false>("k_wgrad")), flops, (k_wgrad<T, BM, BN, WM, WN, false>),
+              grid, dim3(256), 0, s, a);
+  return wgrad_reduce<T>(a, s);
+}
+
+template <int BM, int BN, int WM, int WN, int PF>
+static hipError_t wgrad_b_go(const WgradArgs& a, hipStream_t s) {
+  int K = a.R * a.S * a.C;
+  dim3 grid((a.N + BM - 1) / BM, (K + BN - 1) / BN, a.splits);
+  double flops = 2.0 * a.nb * a.H * a.W * (double)a.N * K;
+  XP_LAUNCH((kname<bf16_t, BM, BN, WM, WN, false, 1, PF>("k_wgrad_b")), flops,
+            (k_wgrad_b<BM, BN, WM, WN, PF>), grid, dim3(256), 0, s, a);
+  return wgrad_reduce<bf16_t>(a, s);
+}
+
 template <typename T>
 static hipError_t wgrad_dispatch(const WgradArgs& a, hipStream_t s) {
   constexpr int VEC = MT<T>::VEC;
@@ -882,6 +1121,19 @@ static hipError_t wgrad_dispatch(const WgradArgs& a, hipStream_t s) {
               (reinterpret_cast<uintptr_t>(a.x) % 16) != 0;
   int K = a.R * a.S * a.C;
   bool n64 = a.N <= 64, k64 = K <= 64;
+  if constexpr (sizeof(T) == 2) {
+    const int M = a.nb * a.H * a.W;
+    const bool chunks = !flat && (a.N % VEC) == 0 && (a.lddz % VEC) == 0 &&
+                        (reinterpret_cast<uintptr_t>(a.dz) % 16) == 0 &&
+                        (((size_t)(M - 1)) * a.lddz + a.N) * sizeof(T) < ((size_t)1 << 31) &&
+                        (((size_t)(M - 1)) * a.ldx + a.C) * sizeof(T) < ((size_t)1 << 31);
+    if (chunks) {
+      if (n64 && k64) return wgrad_b_go<64, 64, 2, 2, 2>(a, s);
+      if (n64) return wgrad_b_go<64, 128, 2, 2, 2>(a, s);
+      if (k64) return wgrad_b_go<128, 64, 2, 2, 2>(a, s);
+      return wgrad_b_go<128, 128, 2, 2, 2>(a, s);
+    }
+  }
   if (n64 && k64) return wgrad_go<T, 64, 64, 2, 2>(a, flat, s);
   if (n64) return wgrad_go<T, 64, 128, 2, 2>(a, flat, s);
   if (k64) return wgrad_go<T, 128, 64, 2, 2>(a, flat, s);

@@ -19,6 +19,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <iterator>
 #include <map>
@@ -50,6 +51,9 @@ xpipe_status fail(xpipe_status s, const std::string& msg) {
 constexpr int64_t PARAM_ALIGN = 64;  // elements
 constexpr size_t WS_ALIGN = 256;     // bytes
 constexpr double BN_EPS = 1e-5;
+// launch lanes: the stage's stream plus auxiliary streams on which independent
+// branches of the layer graph run concurrently
+constexpr int NLANES = 4;
 
 int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 
@@ -97,6 +101,12 @@ struct Op {
   int64_t stat_block = -1;     // ... to this workspace block ([2][cout] doubles, then dbeta/dgamma)
   bool stats_fused = false;    // BN: statistics come from the producing GEMM
   int stats_from = -1;         // BN: index of that GEMM op (during planning)
+  // launch lanes, per pass (0 forward, 1 backward): the lane this op runs on,
+  // the ops (same pass) on other lanes it waits for, and whether later ops on
+  // other lanes wait for it
+  int lane[2] = {0, 0};
+  std::vector<int> waits[2];
+  bool record[2] = {false, false};
 };
 
 struct ParamT {
@@ -133,7 +143,10 @@ struct xpipe_stage {
   bool has_loss = false;
   int classes = 0;
   int64_t bf_f_off = -1, bf_b_off = -1;  // bf16 shadows of the predictions
-  int64_t colpart_off = -1, wpart_off = -1;
+  int64_t colpart_off[NLANES] = {}, wpart_off[NLANES] = {};  // per-lane scratch
+  hipStream_t lane_stream[NLANES] = {};  // [0] = the stage's stream
+  std::vector<hipEvent_t> op_ev[2];      // per op, per pass
+  hipEvent_t fork_ev = nullptr, join_ev[NLANES] = {};
   // call-order state
   bool pred_valid[2] = {false, false};
   bool wd_valid = false;
@@ -167,8 +180,101 @@ struct Plan {
   int classes = 0;
   int64_t P = 0;
   size_t ws = 0;
-  int64_t bf_f_off = -1, bf_b_off = -1, colpart_off = -1, wpart_off = -1;
+  int64_t bf_f_off = -1, bf_b_off = -1, colpart_off[NLANES] = {}, wpart_off[NLANES] = {};
 };
+
+// Channel range a tensor occupies in its buffer: (buffer tensor, first, end).
+struct Region {
+  int base, c0, c1;
+};
+Region region_of(const Plan& p, int t) {
+  const Tensor& tt = p.tensors[t];
+  const int b = tt.owner >= 0 ? tt.owner : t;
+  return Region{b, tt.coff, tt.coff + tt.sh.C};
+}
+bool overlap(const Region& a, const Region& b) {
+  return a.base == b.base && a.c0 < b.c1 && b.c0 < a.c1;
+}
+
+// Assigns every op a lane per pass and the cross-lane waits that keep the
+// launch order's data dependencies.  Forward: an op depends on the ops that
+// wrote what it reads.  Backward (ops in reverse): an op depends on the ops
+// that wrote the gradient it reads and on the earlier writers of the gradient
+// it writes (the fixed accumulation order).  An op continues the lane of a
+// dependency that is still that lane's last op, else takes the next lane in
+// turn; waits on same-lane dependencies are implied by stream order.
+void plan_lanes(Plan& p) {
+  const int n = (int)p.ops.size();
+  auto writes_fwd = [&](int j) -> int { return p.ops[j].kind == OP_CE ? -1 : p.ops[j].out; };
+  for (int pass = 0; pass < 2; ++pass) {
+    std::vector<std::vector<int>> deps(n);
+    for (int i = 0; i < n; ++i) {
+      const Op& op = p.ops[i];
+      if (op.kind == OP_CONCAT) continue;
+      if (pass == 0) {
+        for (int r : {op.in, op.in2}) {
+          if (r <= 0) continue;  // the stage input is ready before the pass
+          const Region rr = region_of(p, r);
+          for (int j = 0; j < i; ++j) {
+            const int w = writes_fwd(j);
+            if (w >= 0 && p.ops[j].kind != OP_CONCAT && overlap(region_of(p, w), rr))
+              deps[i].push_back(j);
+          }
+        }
+      } else {
+        // backward order is n-1 .. 0: "earlier" means a larger index
+        auto grad_writes = [&](int j, const Region& rr) {
+          const Op& o = p.ops[j];
+          if (o.kind == OP_CONCAT) return false;
+          // (tensor 0 is the stage input: its gradient is the caller's dx)
+          for (int t : {o.in, o.in2})
+            if (t >= 0 && overlap(region_of(p, t), rr)) return true;
+          return false;
+        };
+        std::vector<Region> rs;
+        if (op.kind != OP_CE) rs.push_back(region_of(p, op.out));
+        for (int t : {op.in, op.in2})
+          if (t >= 0) rs.push_back(region_of(p, t));
+        for (int j = n - 1; j > i; --j)
+          for (const Region& rr : rs)
+            if (grad_writes(j, rr)) {
+              deps[i].push_back(j);
+              break;
+            }
+      }
+    }
+    std::vector<int> tail(NLANES, -1), tail_q(NLANES, -1);
+    for (int q = 0; q < n; ++q) {
+      const int i = pass == 0 ? q : n - 1 - q;
+      Op& op = p.ops[i];
+      op.waits[pass].clear();
+      if (op.kind == OP_CONCAT) continue;
+      // continue the chain of the most recent dependency that ends its lane,
+      // else start on the lane that has been idle longest
+      int lane = -1, best_q = -1;
+      for (int j : deps[i]) {
+        const int l = p.ops[j].lane[pass];
+        if (tail[l] == j && tail_q[l] > best_q) {
+          lane = l;
+          best_q = tail_q[l];
+        }
+      }
+      if (lane < 0) {
+        lane = 0;
+        for (int l = 1; l < NLANES; ++l)
+          if (tail_q[l] < tail_q[lane]) lane = l;
+      }
+      op.lane[pass] = lane;
+      tail[lane] = i;
+      tail_q[lane] = q;
+      for (int j : deps[i])
+        if (p.ops[j].lane[pass] != lane) {
+          op.waits[pass].push_back(j);
+          p.ops[j].record[pass] = true;
+        }
+    }
+  }
+}
 
 xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, int C, int dtype,
                         Plan& p) {
@@ -529,6 +635,21 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     }
   }
 
+  // ---- launch lanes
+  plan_lanes(p);
+  if (const char* tr = std::getenv("XPIPE_TRACE_PLAN"); tr && *tr == '1') {
+    static const char* kn[] = {"gemm", "bn", "elt", "maxpool", "avgpool", "gap", "concat", "ce"};
+    for (size_t i = 0; i < p.ops.size(); ++i) {
+      const Op& o = p.ops[i];
+      std::fprintf(stderr, "op %2zu %-7s layer %2d in %2d out %2d cout %3d segs %zu | fwd lane %d waits",
+                   i, kn[o.kind], o.layer, o.in, o.out, o.cout, o.segs.size(), o.lane[0]);
+      for (int j : o.waits[0]) std::fprintf(stderr, " %d", j);
+      std::fprintf(stderr, " | bwd lane %d waits", o.lane[1]);
+      for (int j : o.waits[1]) std::fprintf(stderr, " %d", j);
+      std::fprintf(stderr, "\n");
+    }
+  }
+
   // ---- workspace layout
   size_t off = 0;
   auto take = [&](size_t bytes) -> int64_t {
@@ -578,8 +699,10 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     tt.act_off = take((size_t)tt.sh.elems() * esz);
     tt.grad_off = take((size_t)tt.sh.elems() * esz);
   }
-  p.colpart_off = take(std::max<size_t>(colpart, 64));
-  p.wpart_off = take(std::max<size_t>(wpart, 64));
+  for (int l = 0; l < NLANES; ++l) {
+    p.colpart_off[l] = take(std::max<size_t>(colpart, 64));
+    p.wpart_off[l] = take(std::max<size_t>(wpart, 64));
+  }
   p.ws = (size_t)align_up((int64_t)off, WS_ALIGN);
   return XPIPE_OK;
 }
@@ -671,12 +794,64 @@ double gemm_flops(const Tensor& tin, const Op& op) {
   return 2.0 * (double)tin.sh.rows() * op.cout * (double)op.k * op.k * op.cin;
 }
 
+// ---------------------------------------------------------------- lanes
+// One pass (forward or backward) over the ops, spread over the launch lanes.
+// With per-launch timing on, everything runs on the stage's stream.
+struct Lanes {
+  xpipe_stage* st;
+  int pass;
+  bool used[NLANES] = {};
+  bool forked = false;
+  Lanes(xpipe_stage* st_, int pass_) : st(st_), pass(pass_) {}
+  bool single() const { return st->timing; }
+  // stream for op i after its waits; the first use of an auxiliary lane in
+  // the pass waits for the work enqueued on the stage's stream before it
+  xpipe_status begin(int i, hipStream_t& s, int& lane) {
+    const Op& op = st->ops[i];
+    lane = single() ? 0 : op.lane[pass];
+    s = st->lane_stream[lane];
+    if (lane > 0 && !used[lane]) {
+      if (!forked) XP_HIP(hipEventRecord(st->fork_ev, st->stream));
+      forked = true;
+      XP_HIP(hipStreamWaitEvent(s, st->fork_ev, 0));
+    }
+    used[lane] = true;
+    if (!single())
+      for (int j : op.waits[pass]) XP_HIP(hipStreamWaitEvent(s, st->op_ev[pass][j], 0));
+    return XPIPE_OK;
+  }
+  xpipe_status end(int i, hipStream_t s) {
+    if (!single() && st->ops[i].record[pass]) XP_HIP(hipEventRecord(st->op_ev[pass][i], s));
+    return XPIPE_OK;
+  }
+  // the stage's stream waits for every auxiliary lane used in the pass
+  xpipe_status join() {
+    for (int l = 1; l < NLANES; ++l)
+      if (used[l]) {
+        XP_HIP(hipEventRecord(st->join_ev[l], st->lane_stream[l]));
+        XP_HIP(hipStreamWaitEvent(st->stream, st->join_ev[l], 0));
+      }
+    return XPIPE_OK;
+  }
+};
+
+#define XP_OK(call)                        \
+  do {                                     \
+    xpipe_status s_ = (call);              \
+    if (s_ != XPIPE_OK) return s_;         \
+  } while (0)
+
 // ---------------------------------------------------------------- forward
 xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* labels,
                          float* loss) {
-  hipStream_t s = st->stream;
   const int dt = st->dtype;
-  for (const Op& op : st->ops) {
+  Lanes lanes(st, 0);
+  for (int i = 0; i < (int)st->ops.size(); ++i) {
+    const Op& op = st->ops[i];
+    if (op.kind == OP_CONCAT) continue;
+    hipStream_t s;
+    int lane;
+    XP_OK(lanes.begin(i, s, lane));
     const Tensor& tin = st->tensors[op.in];
     View x = act(st, op.in, c);
     switch (op.kind) {
@@ -698,7 +873,7 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         a.pad = op.k / 2;
         a.relu = op.relu;
         int rows_tiles = 0;
-        if (op.stats) a.stat_part = (double*)(st->ws + st->colpart_off);
+        if (op.stats) a.stat_part = (double*)(st->ws + st->colpart_off[lane]);
         XP_HIP(launch_conv_gemm(dt, a, s, &rows_tiles));
         if (op.stats) {
           // the following BNs' batch statistics from the epilogue's column sums
@@ -724,7 +899,7 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         ca.lda = x.ld;
         ca.M = (int)tin.sh.rows();
         ca.C = tin.sh.C;
-        ca.partial = (double*)(st->ws + st->colpart_off);
+        ca.partial = (double*)(st->ws + st->colpart_off[lane]);
         ca.row_blocks = col_row_blocks(ca.M, ca.C);
         ca.out0 = stats;
         ca.out1 = stats + op.stat_ld;
@@ -784,7 +959,7 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         pa.H = tin.sh.H;
         pa.W = tin.sh.W;
         pa.C = tin.sh.C;
-        pa.part = (double*)(st->ws + st->colpart_off);
+        pa.part = (double*)(st->ws + st->colpart_off[lane]);
         if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_fwd(dt, pa, s));
         else if (op.kind == OP_AVGPOOL) XP_HIP(launch_avgpool_fwd(dt, pa, s));
         else XP_HIP(launch_gap_fwd(dt, pa, s));
@@ -806,13 +981,15 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         break;
       }
     }
+    XP_OK(lanes.end(i, s));
   }
-  return XPIPE_OK;
+  return lanes.join();
 }
 
 // ---------------------------------------------------------------- backward
 xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const int32_t* labels) {
   hipStream_t s = st->stream;
+  int lane = 0;
   const int dt = st->dtype;
   const int dir = XPIPE_BWD;
   const size_t esz = st->esz();
@@ -842,8 +1019,11 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
     XP_HIP(launch_elementwise(dt, e, s));
   }
 
+  Lanes lanes(st, 1);
   for (int i = (int)st->ops.size() - 1; i >= 0; --i) {
     const Op& op = st->ops[i];
+    if (op.kind == OP_CONCAT) continue;
+    XP_OK(lanes.begin(i, s, lane));
     const Tensor& tin = st->tensors[op.in];
     View x = act(st, op.in, c);
     switch (op.kind) {
@@ -871,7 +1051,7 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         w.lddz = g.ld;
         w.x = x.p;
         w.ldx = x.ld;
-        w.part = st->ws + st->wpart_off;
+        w.part = st->ws + st->wpart_off[lane];
         if (op.segs.empty()) {
           w.grad = st->grad + op.w_off;
         } else {
@@ -902,7 +1082,7 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
           ca.lda = g.ld;
           ca.M = M;
           ca.C = op.cout;
-          ca.partial = (double*)(st->ws + st->colpart_off);
+          ca.partial = (double*)(st->ws + st->colpart_off[lane]);
           ca.row_blocks = col_row_blocks(M, op.cout);
           ca.grad0 = st->grad + op.b_off;
           XP_HIP(launch_colreduce(dt, ca, s));
@@ -943,7 +1123,7 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         ca.rstd = stats + ld;
         ca.M = M;
         ca.C = C;
-        ca.partial = (double*)(st->ws + st->colpart_off);
+        ca.partial = (double*)(st->ws + st->colpart_off[lane]);
         ca.row_blocks = col_row_blocks(M, C);
         ca.out0 = stats + 2 * ld;
         ca.out1 = stats + 3 * ld;
@@ -1045,8 +1225,9 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
       case OP_CONCAT:
         break;
     }
+    XP_OK(lanes.end(i, s));
   }
-  return XPIPE_OK;
+  return lanes.join();
 }
 
 // ---------------------------------------------------------------- coefficients
@@ -1121,6 +1302,17 @@ xpipe_status refresh_flipped(xpipe_stage* st) {
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+void release_lanes(xpipe_stage* st) {
+  for (int pass = 0; pass < 2; ++pass)
+    for (hipEvent_t e : st->op_ev[pass])
+      if (e) (void)hipEventDestroy(e);
+  if (st->fork_ev) (void)hipEventDestroy(st->fork_ev);
+  for (int l = 1; l < NLANES; ++l) {
+    if (st->join_ev[l]) (void)hipEventDestroy(st->join_ev[l]);
+    if (st->lane_stream[l]) (void)hipStreamDestroy(st->lane_stream[l]);
+  }
+}
 
 }  // namespace
 
@@ -1215,12 +1407,33 @@ xpipe_status xpipe_stage_create(const xpipe_layer_desc* layers, int32_t n_layers
   st->classes = p.classes;
   st->bf_f_off = p.bf_f_off;
   st->bf_b_off = p.bf_b_off;
-  st->colpart_off = p.colpart_off;
-  st->wpart_off = p.wpart_off;
+  for (int l = 0; l < NLANES; ++l) {
+    st->colpart_off[l] = p.colpart_off[l];
+    st->wpart_off[l] = p.wpart_off[l];
+  }
   st->hook.st = st;
-  hipError_t e = p.P > 0 ? hipMemsetAsync(grad, 0, (size_t)p.P * sizeof(float), st->stream)
-                         : hipSuccess;
+  hipError_t e = hipSuccess;
+  // auxiliary launch lanes (default priority) and their events
+  st->lane_stream[0] = st->stream;
+  for (int l = 1; l < NLANES && e == hipSuccess; ++l)
+    e = hipStreamCreateWithFlags(&st->lane_stream[l], hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&st->fork_ev, hipEventDisableTiming);
+  for (int l = 1; l < NLANES && e == hipSuccess; ++l)
+    e = hipEventCreateWithFlags(&st->join_ev[l], hipEventDisableTiming);
+  for (int pass = 0; pass < 2 && e == hipSuccess; ++pass) {
+    st->op_ev[pass].assign(st->ops.size(), nullptr);
+    for (size_t i = 0; i < st->ops.size() && e == hipSuccess; ++i)
+      if (st->ops[i].record[pass])
+        e = hipEventCreateWithFlags(&st->op_ev[pass][i], hipEventDisableTiming);
+  }
   if (e != hipSuccess) {
+    release_lanes(st);
+    delete st;
+    return fail(XPIPE_EHIP, std::string("stream / event creation: ") + hipGetErrorString(e));
+  }
+  e = p.P > 0 ? hipMemsetAsync(grad, 0, (size_t)p.P * sizeof(float), st->stream) : hipSuccess;
+  if (e != hipSuccess) {
+    release_lanes(st);
     delete st;
     return fail(XPIPE_EHIP, std::string("hipMemsetAsync: ") + hipGetErrorString(e));
   }
@@ -1341,6 +1554,10 @@ xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t 
 
 xpipe_status xpipe_stage_destroy(xpipe_stage_t st) {
   if (!st) return fail(XPIPE_EINVAL, "null stage");
+  // auxiliary lanes finish their work before their streams go away
+  for (int l = 1; l < NLANES; ++l)
+    if (st->lane_stream[l]) (void)hipStreamSynchronize(st->lane_stream[l]);
+  release_lanes(st);
   for (auto& r : st->pending) {
     (void)hipEventDestroy(r.a);
     (void)hipEventDestroy(r.b);

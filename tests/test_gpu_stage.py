@@ -148,6 +148,23 @@ def test_repeat_runs_are_bitwise_identical():
         assert np.array_equal(x, y)
 
 
+@pytest.mark.parametrize("name,dtype", [("inception_v3_stage", xp.BF16),
+                                        ("inception_v3_stage", xp.F32),
+                                        ("resnet101_mid_stage", xp.BF16)])
+def test_concurrent_lanes_match_single_lane(name, dtype):
+    """Independent branches run on several streams; with per-launch timing on
+    everything runs on one stream.  Both orders give the same bits."""
+    w = CASES[name]()
+    inp = wl.stage_inputs(w, act_dtype="bf16" if dtype == xp.BF16 else "f32")
+    one = xp.Stage(w.layers, w.micro_batch, w.T, w.in_shape, dtype)
+    one.set_timing(True)
+    a, _ = run_stage(w, inp, dtype, xp.Hyper(), 1, 1, minibatches=2, stage=one)
+    b, _ = run_stage(w, inp, dtype, xp.Hyper(), 1, 1, minibatches=2)
+    for ra, rb in zip(a, b):
+        for x, y in zip(ra.grad + ra.ys + ra.dxs, rb.grad + rb.ys + rb.dxs):
+            assert np.array_equal(x, y)
+
+
 def test_call_order_is_enforced():
     import torch
     w = wl.tiny_mlp()

@@ -422,10 +422,10 @@ XP_DEV void vst(T* p, const double* v);
 template <>
 XP_DEV void vst<bf16_t>(bf16_t* p, const double* v) {
   uint4 u;
-  u.x = (uint32_t)f32_to_bf16((float)v[0]) | ((uint32_t)f32_to_bf16((float)v[1]) << 16);
-  u.y = (uint32_t)f32_to_bf16((float)v[2]) | ((uint32_t)f32_to_bf16((float)v[3]) << 16);
-  u.z = (uint32_t)f32_to_bf16((float)v[4]) | ((uint32_t)f32_to_bf16((float)v[5]) << 16);
-  u.w = (uint32_t)f32_to_bf16((float)v[6]) | ((uint32_t)f32_to_bf16((float)v[7]) << 16);
+  u.x = f32x2_to_bf16x2((float)v[0], (float)v[1]);
+  u.y = f32x2_to_bf16x2((float)v[2], (float)v[3]);
+  u.z = f32x2_to_bf16x2((float)v[4], (float)v[5]);
+  u.w = f32x2_to_bf16x2((float)v[6], (float)v[7]);
   *reinterpret_cast<uint4*>(p) = u;
 }
 template <>

@@ -64,8 +64,8 @@ __global__ __launch_bounds__(256) void k_predict(const float* __restrict__ W,
     stnt(o4 + i, r);
     if (out_bf) {
       uint2 b;
-      b.x = (uint32_t)f32_to_bf16(r.x) | ((uint32_t)f32_to_bf16(r.y) << 16);
-      b.y = (uint32_t)f32_to_bf16(r.z) | ((uint32_t)f32_to_bf16(r.w) << 16);
+      b.x = f32x2_to_bf16x2(r.x, r.y);
+      b.y = f32x2_to_bf16x2(r.z, r.w);
       stnt(reinterpret_cast<uint2*>(out_bf) + i, b);
     }
   }
@@ -125,8 +125,8 @@ __global__ __launch_bounds__(256) void k_adam(float* __restrict__ W, float* __re
       stnt(reinterpret_cast<float4*>(pf) + i, r);
       if (pf_bf) {
         uint2 b;
-        b.x = (uint32_t)f32_to_bf16(r.x) | ((uint32_t)f32_to_bf16(r.y) << 16);
-        b.y = (uint32_t)f32_to_bf16(r.z) | ((uint32_t)f32_to_bf16(r.w) << 16);
+        b.x = f32x2_to_bf16x2(r.x, r.y);
+        b.y = f32x2_to_bf16x2(r.z, r.w);
         stnt(reinterpret_cast<uint2*>(pf_bf) + i, b);
       }
     }
@@ -136,8 +136,8 @@ __global__ __launch_bounds__(256) void k_adam(float* __restrict__ W, float* __re
       stnt(reinterpret_cast<float4*>(pb) + i, r);
       if (pb_bf) {
         uint2 b;
-        b.x = (uint32_t)f32_to_bf16(r.x) | ((uint32_t)f32_to_bf16(r.y) << 16);
-        b.y = (uint32_t)f32_to_bf16(r.z) | ((uint32_t)f32_to_bf16(r.w) << 16);
+        b.x = f32x2_to_bf16x2(r.x, r.y);
+        b.y = f32x2_to_bf16x2(r.z, r.w);
         stnt(reinterpret_cast<uint2*>(pb_bf) + i, b);
       }
     }

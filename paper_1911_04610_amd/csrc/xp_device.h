@@ -13,12 +13,15 @@ typedef double f64x4_t __attribute__((ext_vector_type(4)));
 // ---------------------------------------------------------------- bf16
 XP_DEV float bf16_to_f32(bf16_t u) { return __uint_as_float((uint32_t)u << 16); }
 
-// fp32 -> bf16, round to nearest, ties to even; NaN stays a quiet NaN.
-XP_DEV bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
+// fp32 -> bf16, round to nearest, ties to even (the gfx950 conversion
+// instruction); NaN stays a NaN.
+XP_DEV bf16_t f32_to_bf16(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
+
+// two fp32 -> two bf16 packed low, high (one conversion instruction)
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+XP_DEV uint32_t f32x2_to_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
 }
 
 // ---------------------------------------------------------------- storage traits

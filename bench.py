@@ -35,10 +35,101 @@ def parse():
     ap.add_argument("--sweep-n", type=int, default=100_000_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--traffic-run", action="store_true",
+                    help="a few stage steps plus a 256 MiB calibration copy, for rocprofv3 --pmc "
+                         "FETCH_SIZE / WRITE_SIZE runs")
+    ap.add_argument("--traffic-summarize", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn the two counter_collection.csv files into profiles/traffic.json")
     return ap.parse_args()
 
 
-def time_stage(args):
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "traffic.json")
+CALIB_BYTES = 256 << 20
+
+
+def source_hash():
+    """Hash of the kernel sources: stored HBM-traffic figures apply only to the
+    kernels they were measured on."""
+    import hashlib
+    h = hashlib.sha1()
+    d = os.path.join(ROOT, "paper_1911_04610_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".h", ".cpp")):
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def kernel_key(name):
+    """Common key for rocprofv3's demangled kernel names and the library's
+    launch names: no namespace or arguments, storage types as bf16 / f32."""
+    n = name.split("(")[0].replace("void ", "").replace("xp::", "")
+    n = n.replace("unsigned short", "bf16").replace(" ", "")
+    return n.replace("<float", "<f32").replace(",float", ",f32")
+
+
+def traffic_run(args):
+    import torch
+    w, ms, wall, classes, fin = time_stage(args, timing_pass=False)
+    a = torch.empty(CALIB_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"traffic_run": w.name, "steps": args.steps, "ms_per_step": ms}))
+
+
+def traffic_summarize(fetch_csv, write_csv):
+    import csv
+    from collections import defaultdict
+
+    def load(path, counter):
+        per = defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            per[r["Kernel_Name"]].append(float(r["Counter_Value"]) * 1024.0)  # KiB -> B
+        return per
+
+    fe, wr = load(fetch_csv, "FETCH_SIZE"), load(write_csv, "WRITE_SIZE")
+    copy = [k for k in fe if "copy" in k.lower()]
+    calib_name = max(copy, key=lambda k: max(fe[k]))
+    f_fac = max(fe[calib_name]) / CALIB_BYTES
+    w_fac = max(wr[calib_name]) / CALIB_BYTES
+    kernels = {}
+    for k in fe:
+        if not k.startswith("void xp::") and not k.startswith("xp::"):
+            continue
+        f = sum(fe[k]) / len(fe[k]) / f_fac
+        wv = sum(wr.get(k, [0.0])) / max(len(wr.get(k, [])), 1) / w_fac
+        key = kernel_key(k)
+        kernels[key] = {"fetch_bytes": round(f), "write_bytes": round(wv),
+                        "traffic_bytes": round(f + wv), "dispatches": len(fe[k])}
+    out = {"source_hash": source_hash(), "unit": "bytes per launch (HBM, calibrated)",
+           "calibration": {"kernel": kernel_key(calib_name), "bytes_each_way": CALIB_BYTES,
+                           "fetch_factor": round(f_fac, 4), "write_factor": round(w_fac, 4)},
+           "kernels": kernels}
+    with open(TRAFFIC_JSON, "w") as fh:
+        json.dump(out, fh, indent=1, sort_keys=True)
+    print(json.dumps({"written": TRAFFIC_JSON, "kernels": len(kernels),
+                      "fetch_factor": f_fac, "write_factor": w_fac}))
+
+
+def stored_traffic(kernel):
+    """Calibrated HBM bytes per launch of `kernel` from profiles/traffic.json,
+    or None when absent or taken on other kernel sources."""
+    try:
+        with open(TRAFFIC_JSON) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_hash") != source_hash():
+        return None
+    k = t.get("kernels", {}).get(kernel_key(kernel))
+    return None if k is None else k["traffic_bytes"]
+
+
+def time_stage(args, timing_pass=True):
     import torch
     import paper_1911_04610_amd as xp
     import workloads as wl
@@ -94,6 +185,8 @@ def time_stage(args):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms = e0.elapsed_time(e1) / args.steps
+    if not timing_pass:
+        return w, ms, wall, {}, True
     # per-kernel durations with HIP events around every launch, over the same
     # number of steps
     st.set_timing(True)
@@ -209,9 +302,15 @@ def main():
         print(json.dumps({"error": "this build runs one pipeline stage on one GPU; --gpus must be 1 "
                                    "(each pipeline stage would run as its own one-GPU process)"}))
         sys.exit(2)
+    if args.traffic_summarize:
+        traffic_summarize(*args.traffic_summarize)
+        return
     import torch
     import paper_1911_04610_amd as xp
     torch.cuda.set_device(0)
+    if args.traffic_run:
+        traffic_run(args)
+        return
     w, ms, wall, classes, finite = time_stage(args)
     samples = w.T * w.micro_batch
     value = samples / (ms / 1e3)
@@ -236,7 +335,8 @@ def main():
     dom = max(classes, key=lambda k: classes[k][0])
     d_ms, d_n, d_work = classes[dom]
     rf = roof(dom)
-    rf.update({"kernel": dom, "traffic": None, "launches_per_step": d_n / args.steps,
+    rf.update({"kernel": dom, "traffic": stored_traffic(dom), "traffic_unit": "bytes per launch",
+               "launches_per_step": d_n / args.steps,
                "avg_launch_us": round(1e3 * d_ms / max(d_n, 1) - off_us, 3),
                "avg_launch_us_raw_events": round(1e3 * d_ms / max(d_n, 1), 3),
                "event_offset_us": round(off_us, 3),

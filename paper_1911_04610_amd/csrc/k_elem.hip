@@ -84,7 +84,7 @@ hipError_t launch_colfinal(const ColArgs& a, hipStream_t s);
 template <typename T>
 static hipError_t colreduce_go(const ColArgs& a, hipStream_t s) {
   dim3 grid(ceil_div(a.C, 64), a.row_blocks);
-  XP_LAUNCH("k_colpart", (double)a.M * a.C * sizeof(T) * (a.mode == COL_BNBWD ? 2 : 1), k_colpart<T>, grid,
+  XP_LAUNCH(sizeof(T) == 2 ? "k_colpart<bf16>" : "k_colpart<f32>", (double)a.M * a.C * sizeof(T) * (a.mode == COL_BNBWD ? 2 : 1), k_colpart<T>, grid,
             dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -567,7 +567,7 @@ __global__ __launch_bounds__(256) void k_colfinal_v(ColArgs a) {
 
 hipError_t launch_colfinal(const ColArgs& a, hipStream_t s) {
   if (a.C <= 0) return hipSuccess;
-  XP_LAUNCH("k_colfinal", (double)a.row_blocks * 2 * a.C * 8, k_colfinal_v, dim3(a.C),
+  XP_LAUNCH("k_colfinal_v", (double)a.row_blocks * 2 * a.C * 8, k_colfinal_v, dim3(a.C),
             dim3(256), 0, s, a);
   return hipGetLastError();
 }

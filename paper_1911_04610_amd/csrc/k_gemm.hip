@@ -1109,7 +1109,9 @@ static hipError_t wgrad_b_go(const WgradArgs& a, hipStream_t s) {
   int K = a.R * a.S * a.C;
   dim3 grid((a.N + BM - 1) / BM, (K + BN - 1) / BN, a.splits);
   double flops = 2.0 * a.nb * a.H * a.W * (double)a.N * K;
-  XP_LAUNCH((kname<bf16_t, BM, BN, WM, WN, false, 1, PF>("k_wgrad_b")), flops,
+  static char name[64];
+  snprintf(name, sizeof name, "k_wgrad_b<%d,%d,%d,%d,%d>", BM, BN, WM, WN, PF);
+  XP_LAUNCH(name, flops,
             (k_wgrad_b<BM, BN, WM, WN, PF>), grid, dim3(256), 0, s, a);
   return wgrad_reduce<bf16_t>(a, s);
 }

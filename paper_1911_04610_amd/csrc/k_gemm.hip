@@ -1016,12 +1016,17 @@ static hipError_t conv_dispatch(const ConvArgs& a, hipStream_t s, int* gr) {
       if (ks == 2) return conv_go<T, 32, 32, 2, 2, 2, 3>(a, flat, s, gr);
       return conv_go<T, 64, 32, 2, 2, 1, 2>(a, flat, s, gr);
     }
-    if (!flat && taps > 1 && taps < 25 && a.N > 64)
+    if (!flat && taps > 1 && taps < 25 && a.N > 64) {
+      // one 96-column tile reads the input once and wastes no MFMA columns
+      if (a.N <= 96) return conv_go<T, 64, 96, 2, 2, 1, 2>(a, flat, s, gr);
       return conv_go<T, 128, 64, 4, 1, 1, 4>(a, flat, s, gr);
+    }
     if (ks == 1) {
       if (taps > 1) return conv_go<T, 128, 64, 4, 1, 1, 4>(a, flat, s, gr);
       return conv_go<T, 64, 64, 2, 2, 1, 2>(a, flat, s, gr);
     }
+    // wide 1x1 (merged siblings): 64-row tiles, one channel block per step
+    if (!flat && taps == 1 && a.N > 96) return conv_go<T, 64, 64, 2, 2, 1, 2>(a, flat, s, gr);
     if (taps >= 25) {
       if (ks == 4) return conv_go<T, 64, 64, 2, 2, 4, 2>(a, flat, s, gr);
       return conv_go<T, 64, 64, 2, 2, 2, 2>(a, flat, s, gr);
@@ -1043,11 +1048,16 @@ hipError_t launch_conv_gemm(int dtype, const ConvArgs& a, hipStream_t s, int* gr
 
 int conv_max_row_tiles(int M) { return (M + 31) / 32; }
 
-int wgrad_pick_splits(int M, int N, int K) {
-  int bm = N <= 64 ? 64 : 128;
-  int bn = K <= 64 ? 64 : 128;
+int wgrad_pick_splits(int dtype, int M, int N, int K, int taps) {
+  // bf16: 64x64 tiles, about 512 workgroups (1x1) or 1024 (larger filters),
+  // from a sweep of the stage shapes; fp32/fp64: the tile of wgrad_dispatch
+  // and about 512 workgroups
+  const bool bf = dtype == DT_BF16;
+  int bm = bf ? 64 : (N <= 64 ? 64 : 128);
+  int bn = bf ? 64 : (K <= 64 ? 64 : 128);
   int tiles = ((N + bm - 1) / bm) * ((K + bn - 1) / bn);
-  int want = (512 + tiles - 1) / tiles;      // about two workgroups per CU
+  int target = bf && taps > 1 ? 1024 : 512;
+  int want = (target + tiles - 1) / tiles;
   int maxs = (M + 255) / 256;                // at least ~256 pixels per split
   // keep the partial sums (written and read back once) below the operands' bytes
   int64_t op_bytes = (int64_t)M * (N + K / 1) * 2;
@@ -1059,7 +1069,6 @@ int wgrad_pick_splits(int M, int N, int K) {
   if (want < 1) want = 1;
   return want;
 }
-
 size_t wgrad_part_bytes(int dtype, int N, int K, int splits) {
   return (size_t)splits * N * K * (dtype == DT_BF16 ? sizeof(float) : sizeof(double));
 }
@@ -1129,12 +1138,7 @@ static hipError_t wgrad_dispatch(const WgradArgs& a, hipStream_t s) {
                         (reinterpret_cast<uintptr_t>(a.dz) % 16) == 0 &&
                         (((size_t)(M - 1)) * a.lddz + a.N) * sizeof(T) < ((size_t)1 << 31) &&
                         (((size_t)(M - 1)) * a.ldx + a.C) * sizeof(T) < ((size_t)1 << 31);
-    if (chunks) {
-      if (n64 && k64) return wgrad_b_go<64, 64, 2, 2, 2>(a, s);
-      if (n64) return wgrad_b_go<64, 128, 2, 2, 2>(a, s);
-      if (k64) return wgrad_b_go<128, 64, 2, 2, 2>(a, s);
-      return wgrad_b_go<128, 128, 2, 2, 2>(a, s);
-    }
+    if (chunks) return wgrad_b_go<64, 64, 2, 2, 2>(a, s);
   }
   if (n64 && k64) return wgrad_go<T, 64, 64, 2, 2>(a, flat, s);
   if (n64) return wgrad_go<T, 64, 128, 2, 2>(a, flat, s);

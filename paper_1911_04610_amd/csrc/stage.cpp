@@ -673,7 +673,7 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
       if (op.stats) op.stat_block = take((size_t)4 * op.cout * sizeof(double));
       int M = (int)tin_.sh.rows();
       int K = op.k * op.k * op.cin;
-      int splits = wgrad_pick_splits(M, op.cout, K);
+      int splits = wgrad_pick_splits(dtype, M, op.cout, K, op.k * op.k);
       wpart = std::max(wpart, wgrad_part_bytes(dtype, op.cout, K, splits));
       if (op.b_off >= 0) colpart = std::max(colpart, col_partial_bytes(M, op.cout));
       if (op.stats)
@@ -1071,7 +1071,7 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         w.N = op.cout;
         w.R = w.S = op.k;
         w.pad = op.k / 2;
-        w.splits = wgrad_pick_splits(M, op.cout, K);
+        w.splits = wgrad_pick_splits(dt, M, op.cout, K, op.k * op.k);
         {
           XP_HIP(launch_wgrad(dt, w, s));
         }

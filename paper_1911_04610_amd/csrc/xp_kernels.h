@@ -107,7 +107,8 @@ hipError_t launch_conv_gemm(int dtype, const ConvArgs& a, hipStream_t s, int* gr
 // row tiles the forward-type GEMM uses for M rows (upper bound over tile choices)
 int conv_max_row_tiles(int M);
 size_t wgrad_part_bytes(int dtype, int N, int K, int splits);
-int wgrad_pick_splits(int M, int N, int K);
+// pixel splits of the weight gradient (R*S = taps filter positions)
+int wgrad_pick_splits(int dtype, int M, int N, int K, int taps);
 hipError_t launch_wgrad(int dtype, const WgradArgs& a, hipStream_t s);
 
 // Flipped, transposed copy for the data gradient: wd[c][r][s][n] = w[n][R-1-r][S-1-s][c].

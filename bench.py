@@ -267,6 +267,37 @@ def time_sweep(n, steps):
     return res
 
 
+def measured_peaks():
+    """Attainable peaks on this GPU from the library's probes: a 1 GiB 16-byte
+    copy (read + write bytes) and back-to-back bf16 MFMAs on registers."""
+    import torch
+    import paper_1911_04610_amd as xp
+
+    def timed(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    n = 1 << 30
+    src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    ms = timed(lambda: xp.xpipe_probe_copy(src, dst))
+    copy_gbs = 2.0 * n / (ms / 1e3) / 1e9
+    del src, dst
+    waves, iters = 256 * 4 * 2, 4096
+    out = torch.empty(waves, dtype=torch.float32, device="cuda")
+    ms = timed(lambda: xp.xpipe_probe_mfma(out, iters))
+    tflops = waves * iters * 8 * 32768.0 / (ms / 1e3) / 1e12
+    return {"hbm_copy_GB_s": round(copy_gbs, 1), "mfma_bf16_TFLOP_s": round(tflops, 1),
+            "copy_bytes": 2 * n, "mfma": "v_mfma_f32_32x32x16_bf16, %d waves x %d x 8" % (waves, iters)}
+
+
 def cpu_baseline(w, dtype):
     """The oracle as it stands, on the host, for one whole step of the same
     stage: both predictions, T forwards, T backwards with recomputation and
@@ -372,11 +403,18 @@ def main():
                         for k in top],
         "finite": finite,
     }
+    pk = measured_peaks()
+    out["peaks_measured"] = pk
+    if rf["unit"] == "TFLOP/s" and peak_key == "bf16":
+        rf["frac_of_measured_peak"] = round(rf["achieved"] / pk["mfma_bf16_TFLOP_s"], 5)
+    elif rf["unit"] == "GB/s":
+        rf["frac_of_measured_peak"] = round(rf["achieved"] / pk["hbm_copy_GB_s"], 4)
     if not args.no_sweep:
         sw = time_sweep(args.sweep_n, args.steps)
         out["predict_adam_sweep"] = {"n_params": args.sweep_n, "t": 100,
                                      **{k: {"ms": round(v["ms"], 4), "GB_s": round(v["GB_s"], 1),
-                                            "frac_hbm": round(v["GB_s"] / HBM_PEAK_GBS, 4)}
+                                            "frac_hbm": round(v["GB_s"] / HBM_PEAK_GBS, 4),
+                                            "frac_measured_copy": round(v["GB_s"] / pk["hbm_copy_GB_s"], 4)}
                                         for k, v in sw.items()}}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.dtype)

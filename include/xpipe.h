@@ -222,6 +222,17 @@ xpipe_status xpipe_stage_timing_count(xpipe_stage_t st, int32_t* n);
 xpipe_status xpipe_stage_timing_entry(xpipe_stage_t st, int32_t i, const char** kernel, double* ms,
                                       int64_t* launches, double* work);
 
+/* Measurement probes (not part of the method): the attainable peaks the
+ * benchmark reports next to the published ones.
+ * xpipe_probe_copy: dst[i] = src[i] for `bytes` bytes (a multiple of 16; both
+ * 16-byte aligned, not overlapping), one 16-byte chunk per thread.
+ * xpipe_probe_mfma: every wave of `waves` runs `iters` rounds of eight
+ * independent v_mfma_f32_32x32x16_bf16 (32768 flops each) on register
+ * operands and writes one float per wave to out[waves] (so the work is kept);
+ * flops = waves * iters * 8 * 32768.  Both enqueue on hip_stream. */
+xpipe_status xpipe_probe_copy(const void* src, void* dst, int64_t bytes, void* hip_stream);
+xpipe_status xpipe_probe_mfma(float* out, int32_t waves, int32_t iters, void* hip_stream);
+
 /* Message for the last non-OK status returned on the calling thread. */
 const char* xpipe_last_error(void);
 

@@ -82,6 +82,8 @@ _SIGS = {
     "xpipe_predict_flat": [_P, _P, _P, _P, _P, _I64, _I32, ctypes.POINTER(HParams), _P],
     "xpipe_adam_flat": [_P, _P, _P, _P, _I64, ctypes.POINTER(HParams), _I32, _P, _I32, _P, _I32,
                         _P],
+    "xpipe_probe_copy": [_P, _P, _I64, _P],
+    "xpipe_probe_mfma": [_P, _I32, _I32, _P],
     "xpipe_stage_set_timing": [_P, _I32],
     "xpipe_stage_timing_count": [_P, ctypes.POINTER(_I32)],
     "xpipe_stage_timing_entry": [_P, _I32, ctypes.POINTER(ctypes.c_char_p),
@@ -270,6 +272,19 @@ def xpipe_predict_flat(W, m, v, out, out_bf16, s: int, hp: Hyper, t: int, stream
     c = hp.c(t)
     _check(lib().xpipe_predict_flat(_ptr(W), _ptr(m), _ptr(v), _ptr(out), _ptr(out_bf16),
                                     W.numel(), s, ctypes.byref(c), _stream_ptr(stream)))
+
+
+def xpipe_probe_copy(src, dst, stream=None):
+    """dst[:] = src[:] (same byte size, multiple of 16) with the library's copy probe."""
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("src and dst must have the same byte size")
+    _check(lib().xpipe_probe_copy(_ptr(src), _ptr(dst), nbytes, _stream_ptr(stream)))
+
+
+def xpipe_probe_mfma(out, iters: int, stream=None):
+    """One wave per element of the float32 tensor `out`, `iters` rounds of 8 MFMAs each."""
+    _check(lib().xpipe_probe_mfma(_ptr(out), out.numel(), int(iters), _stream_ptr(stream)))
 
 
 def xpipe_adam_flat(W, m, v, G, hp: Hyper, t: int, zero_grad=True, pred_fwd=None, s_fwd=0,

@@ -92,13 +92,18 @@ template <typename T, int BM, int BN, int WM, int WN, bool FLAT, int KS, int PF>
 __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   using MTT = MT<T>;
   constexpr int VEC = MTT::VEC;
-  constexpr int SUB = sizeof(T) == 2 ? 32 : 16;
+  constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
+  // bf16 wave tiles that are multiples of 32 use v_mfma_f32_32x32x16_bf16,
+  // which on gfx950 has twice the throughput of the 16x16x32 form, and step
+  // through K in multiples of 16 (KS counts 16-deep slices); otherwise KS
+  // counts 32-deep slices (bf16, 16x16x32) or 16-deep (fp32 storage, f64 MFMA)
+  constexpr bool M32 = sizeof(T) == 2 && WTM % 32 == 0 && WTN % 32 == 0;
+  constexpr int SUB = (sizeof(T) == 2 && !M32) ? 32 : 16;
   constexpr int BK = KS * SUB;
   constexpr int PITCH = BK + (sizeof(T) == 2 ? XP_GEMM_LDS_PAD_BF16 : 4);
   constexpr int CPR = BK / VEC;  // chunks per tile row per step
   constexpr int A_CH = BM * CPR, B_CH = BN * CPR;
   constexpr int A_PER = (A_CH + 255) / 256, B_PER = (B_CH + 255) / 256;
-  constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
   static_assert(WM * WN == 4, "four waves");
   static_assert(TM >= 1 && TN >= 1, "wave tile");
   __shared__ __align__(16) T sA[2][BM * PITCH];
@@ -256,18 +261,48 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
       if (b_slot[i]) *reinterpret_cast<uint4*>(&sB[buf][b_row[i] * PITCH + b_kc[i] * VEC]) = rb[slot][i];
   };
 
-  typename MTT::acc_t acc[TM][TN];
+  constexpr int TM2 = M32 ? WTM / 32 : 1, TN2 = M32 ? WTN / 32 : 1;
+  typename MTT::acc_t acc[M32 ? 1 : TM][M32 ? 1 : TN];
+  f32x16_t acc2[TM2][TN2];
+  if constexpr (M32) {
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM2; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+      for (int j = 0; j < TN2; ++j)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) acc[i][j][q] = 0;
+        for (int q = 0; q < 16; ++q) acc2[i][j][q] = 0.f;
+  } else {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[i][j][q] = 0;
+  }
 
   auto compute = [&](int buf) __attribute__((always_inline)) {
     const T* A = sA[buf];
     const T* B = sB[buf];
-    if constexpr (sizeof(T) == 2) {
+    if constexpr (M32) {
+      // A fragment: lane l holds row l % 32, k = 8 * (l / 32) .. + 8 of a 16-deep step
+#pragma unroll
+      for (int kk = 0; kk < BK / 16; ++kk) {
+        bf16x8_t af[TM2], bfv[TN2];
+#pragma unroll
+        for (int i = 0; i < TM2; ++i)
+          af[i] = *reinterpret_cast<const bf16x8_t*>(
+              &A[(wm * WTM + i * 32 + (lane & 31)) * PITCH + kk * 16 + (lane >> 5) * 8]);
+#pragma unroll
+        for (int j = 0; j < TN2; ++j)
+          bfv[j] = *reinterpret_cast<const bf16x8_t*>(
+              &B[(wn * WTN + j * 32 + (lane & 31)) * PITCH + kk * 16 + (lane >> 5) * 8]);
+#pragma unroll
+        for (int i = 0; i < TM2; ++i)
+#pragma unroll
+          for (int j = 0; j < TN2; ++j)
+            acc2[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfv[j], acc2[i][j], 0, 0, 0);
+      }
+    } else if constexpr (sizeof(T) == 2) {
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         bf16x8_t af[TM], bfv[TN];
@@ -338,47 +373,64 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   // epilogue: bias, ReLU, mask, accumulate, round once on store
   T* __restrict__ y = (T*)a.y;
   const T* __restrict__ mask = (const T*)a.mask;
-  double cs[TN], cq[TN];  // column sums of the stored values (batch-norm statistics)
+  constexpr int NCOL = M32 ? TN2 : TN;  // column groups per lane
+  double cs[NCOL], cq[NCOL];  // column sums of the stored values (batch-norm statistics)
 #pragma unroll
-  for (int j = 0; j < TN; ++j) cs[j] = cq[j] = 0.0;
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        int m = m0 + wm * WTM + i * 16 + MTT::out_row(lane, q);
-        int n = n0 + wn * WTN + j * 16 + (lane & 15);
-        if (m < M && n < a.N) {
-          double v = (double)acc[i][j][q];
-          if (a.bias) v += (double)a.bias[n];
-          if (a.relu) v = v > 0.0 ? v : 0.0;
-          if (mask && !(ldd(mask + (size_t)m * a.ldm + n) > 0.0)) v = 0.0;
-          T* p = y + (size_t)m * a.ldy + n;
-          if (a.accumulate) v += ldd(p);
-          std_(p, v);
-          if (a.stat_part) {
-            double sv = ldd(p);  // the stored (rounded) value, as the statistics see it
-            cs[j] += sv;
-            cq[j] += sv * sv;
-          }
-        }
+  for (int j = 0; j < NCOL; ++j) cs[j] = cq[j] = 0.0;
+  auto emit = [&](double acc_v, int m, int n, int j) __attribute__((always_inline)) {
+    if (m < M && n < a.N) {
+      double v = acc_v;
+      if (a.bias) v += (double)a.bias[n];
+      if (a.relu) v = v > 0.0 ? v : 0.0;
+      if (mask && !(ldd(mask + (size_t)m * a.ldm + n) > 0.0)) v = 0.0;
+      T* p = y + (size_t)m * a.ldy + n;
+      if (a.accumulate) v += ldd(p);
+      std_(p, v);
+      if (a.stat_part) {
+        double sv = ldd(p);  // the stored (rounded) value, as the statistics see it
+        cs[j] += sv;
+        cq[j] += sv * sv;
       }
-  if (a.stat_part) {
-    // lanes l, l+16, l+32, l+48 share a column: fixed-order butterfly
+    }
+  };
+  if constexpr (M32) {
+    // 32x32 result: lane l, register r holds row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      cs[j] += __shfl_xor(cs[j], 16, 64);
-      cq[j] += __shfl_xor(cq[j], 16, 64);
+    for (int i = 0; i < TM2; ++i)
+#pragma unroll
+      for (int j = 0; j < TN2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          emit((double)acc2[i][j][r], m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3),
+               n0 + wn * WTN + j * 32 + (lane & 31), j);
+  } else {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          emit((double)acc[i][j][q], m0 + wm * WTM + i * 16 + MTT::out_row(lane, q),
+               n0 + wn * WTN + j * 16 + (lane & 15), j);
+  }
+  if (a.stat_part) {
+    // lanes that hold the same column add in a fixed butterfly order
+    constexpr int CW = M32 ? 32 : 16;  // columns per group
+#pragma unroll
+    for (int j = 0; j < NCOL; ++j) {
+      if constexpr (!M32) {
+        cs[j] += __shfl_xor(cs[j], 16, 64);
+        cq[j] += __shfl_xor(cq[j], 16, 64);
+      }
       cs[j] += __shfl_xor(cs[j], 32, 64);
       cq[j] += __shfl_xor(cq[j], 32, 64);
     }
     __shared__ double red[WM][2][BN];
-    if (lane < 16) {
+    if (lane < CW) {
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        red[wm][0][wn * WTN + j * 16 + lane] = cs[j];
-        red[wm][1][wn * WTN + j * 16 + lane] = cq[j];
+      for (int j = 0; j < NCOL; ++j) {
+        red[wm][0][wn * WTN + j * CW + lane] = cs[j];
+        red[wm][1][wn * WTN + j * CW + lane] = cq[j];
       }
     }
     __syncthreads();
@@ -789,17 +841,47 @@ __global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
     }
   };
 
-  f32x4_t acc[TM][TN];
+  // wave tiles that are multiples of 32 use v_mfma_f32_32x32x16_bf16
+  constexpr bool M32 = WTM % 32 == 0 && WTN % 32 == 0;
+  constexpr int TM2 = M32 ? WTM / 32 : 1, TN2 = M32 ? WTN / 32 : 1;
+  f32x4_t acc[M32 ? 1 : TM][M32 ? 1 : TN];
+  f32x16_t acc2[TM2][TN2];
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < (M32 ? 1 : TM); ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+    for (int j = 0; j < (M32 ? 1 : TN); ++j)
 #pragma unroll
       for (int q = 0; q < 4; ++q) acc[i][j][q] = 0.f;
+#pragma unroll
+  for (int i = 0; i < TM2; ++i)
+#pragma unroll
+    for (int j = 0; j < TN2; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc2[i][j][q] = 0.f;
 
   auto compute = [&](int buf) __attribute__((always_inline)) {
     const T* A = sA[buf];
     const T* B = sB[buf];
+    if constexpr (M32) {
+#pragma unroll
+      for (int kk = 0; kk < BKm / 16; ++kk) {
+        bf16x8_t af[TM2], bfv[TN2];
+#pragma unroll
+        for (int i = 0; i < TM2; ++i)
+          af[i] = *reinterpret_cast<const bf16x8_t*>(
+              &A[(wm * WTM + i * 32 + (lane & 31)) * PA + kk * 16 + (lane >> 5) * 8]);
+#pragma unroll
+        for (int j = 0; j < TN2; ++j)
+          bfv[j] = *reinterpret_cast<const bf16x8_t*>(
+              &B[(wn * WTN + j * 32 + (lane & 31)) * PB + kk * 16 + (lane >> 5) * 8]);
+#pragma unroll
+        for (int i = 0; i < TM2; ++i)
+#pragma unroll
+          for (int j = 0; j < TN2; ++j)
+            acc2[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfv[j], acc2[i][j], 0, 0, 0);
+      }
+      return;
+    }
     bf16x8_t af[TM], bfv[TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -847,16 +929,29 @@ __global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
   }
 
   float* part = (float*)a.part + (size_t)blockIdx.z * N * K;
+  if constexpr (M32) {
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM2; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+      for (int j = 0; j < TN2; ++j)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int n = n0 + wm * WTM + i * 16 + MT<T>::out_row(lane, q);
-        const int k = k0 + wn * WTN + j * 16 + (lane & 15);
-        if (n < N && k < K) part[(size_t)n * K + k] = acc[i][j][q];
-      }
+        for (int r = 0; r < 16; ++r) {
+          const int n = n0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          const int k = k0 + wn * WTN + j * 32 + (lane & 31);
+          if (n < N && k < K) part[(size_t)n * K + k] = acc2[i][j][r];
+        }
+  } else {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int n = n0 + wm * WTM + i * 16 + MT<T>::out_row(lane, q);
+          const int k = k0 + wn * WTN + j * 16 + (lane & 15);
+          if (n < N && k < K) part[(size_t)n * K + k] = acc[i][j][q];
+        }
+  }
 }
 
 // grad[i] += sum over splits of part[z][i], splits added in order z = 0, 1, ...;
@@ -1011,25 +1106,27 @@ static hipError_t conv_dispatch(const ConvArgs& a, hipStream_t s, int* gr) {
     // register prefetch depth PF)
     const int taps = a.R * a.S;
     const int ks = flat ? 1 : pick_ks_bf16(a.C, taps);
+    // KS counts 32-deep slices for the 16x16 MFMA tiles and 16-deep slices
+    // for the 32x32 ones (64x64 on 2x2 waves), so 64x64 KS 2 has BK = 32.
     if (narrow) {
       if (ks == 4) return conv_go<T, 32, 32, 2, 2, 4, 3>(a, flat, s, gr);
       if (ks == 2) return conv_go<T, 32, 32, 2, 2, 2, 3>(a, flat, s, gr);
       return conv_go<T, 64, 32, 2, 2, 1, 2>(a, flat, s, gr);
     }
-    if (!flat && taps > 1 && taps < 25 && a.N > 64) {
-      // one 96-column tile reads the input once and wastes no MFMA columns
-      if (a.N <= 96) return conv_go<T, 64, 96, 2, 2, 1, 2>(a, flat, s, gr);
-      return conv_go<T, 128, 64, 4, 1, 1, 4>(a, flat, s, gr);
-    }
-    if (ks == 1) {
-      if (taps > 1) return conv_go<T, 128, 64, 4, 1, 1, 4>(a, flat, s, gr);
-      return conv_go<T, 64, 64, 2, 2, 1, 2>(a, flat, s, gr);
-    }
-    // wide 1x1 (merged siblings): 64-row tiles, one channel block per step
-    if (!flat && taps == 1 && a.N > 96) return conv_go<T, 64, 64, 2, 2, 1, 2>(a, flat, s, gr);
-    if (taps >= 25) {
-      if (ks == 4) return conv_go<T, 64, 64, 2, 2, 4, 2>(a, flat, s, gr);
+    // one 96-column tile reads the input once and wastes no MFMA columns
+    if (!flat && taps > 1 && taps < 25 && a.N > 64 && a.N <= 96)
+      return conv_go<T, 64, 96, 2, 2, 1, 2>(a, flat, s, gr);
+    if (ks == 1) return conv_go<T, 64, 64, 2, 2, 2, 2>(a, flat, s, gr);
+    if (!flat && taps == 1 && a.N > 96 && M >= 16384) {
+      // wide 1x1 (merged siblings) over many rows: 64-row tiles, the column
+      // tile that pads N least
+      if ((a.N + 95) / 96 * 96 <= (a.N + 63) / 64 * 64)
+        return conv_go<T, 64, 96, 2, 2, 1, 2>(a, flat, s, gr);
       return conv_go<T, 64, 64, 2, 2, 2, 2>(a, flat, s, gr);
+    }
+    if (taps >= 25 && a.N > 48) {
+      if (ks == 4) return conv_go<T, 64, 64, 2, 2, 8, 2>(a, flat, s, gr);
+      return conv_go<T, 64, 64, 2, 2, 4, 2>(a, flat, s, gr);
     }
     if (ks == 4) return conv_go<T, 32, 64, 2, 2, 4, 2>(a, flat, s, gr);
     return conv_go<T, 32, 64, 2, 2, 2, 2>(a, flat, s, gr);

@@ -193,4 +193,52 @@ hipError_t launch_adam(float* W, float* m, float* v, float* G, int64_t n, const 
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- measurement probes
+__global__ __launch_bounds__(256) void k_probe_copy(const uint4* __restrict__ src,
+                                                     uint4* __restrict__ dst, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[i];
+}
+
+__global__ __launch_bounds__(256) void k_probe_mfma(float* out, int waves, int iters) {
+  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  bf16x8_t a, b;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    a[e] = (__bf16)(float)((lane + e) & 7);
+    b[e] = (__bf16)(float)((lane * 3 + e) & 7);
+  }
+  f32x16_t acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s += acc[j][r];
+  if (lane == 0 && wave < waves) out[wave] = s;
+}
+
+hipError_t launch_probe_copy(const void* src, void* dst, int64_t bytes, hipStream_t s) {
+  const int64_t n = bytes / 16;
+  if (n <= 0) return hipSuccess;
+  XP_LAUNCH("k_probe_copy", (double)bytes * 2, k_probe_copy, dim3((unsigned)((n + 255) / 256)),
+            dim3(256), 0, s, (const uint4*)src, (uint4*)dst, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_probe_mfma(float* out, int waves, int iters, hipStream_t s) {
+  if (waves <= 0 || iters <= 0) return hipSuccess;
+  XP_LAUNCH("k_probe_mfma", (double)waves * iters * 8 * 32768.0, k_probe_mfma,
+            dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, out, waves, iters);
+  return hipGetLastError();
+}
+
 }  // namespace xp

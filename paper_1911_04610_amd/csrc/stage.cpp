@@ -1599,6 +1599,23 @@ xpipe_status xpipe_adam_flat(float* W, float* m, float* v, float* G, int64_t n, 
   return XPIPE_OK;
 }
 
+xpipe_status xpipe_probe_copy(const void* src, void* dst, int64_t bytes, void* hip_stream) {
+  if (bytes < 0 || (bytes % 16) != 0) return fail(XPIPE_EINVAL, "bytes must be a multiple of 16");
+  if (bytes == 0) return XPIPE_OK;
+  if (!src || !dst) return fail(XPIPE_EINVAL, "null buffer");
+  if (!aligned16(src) || !aligned16(dst)) return fail(XPIPE_EINVAL, "buffers must be 16-byte aligned");
+  XP_HIP(launch_probe_copy(src, dst, bytes, (hipStream_t)hip_stream));
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_probe_mfma(float* out, int32_t waves, int32_t iters, void* hip_stream) {
+  if (waves < 0 || iters < 0) return fail(XPIPE_EINVAL, "negative size");
+  if (waves == 0 || iters == 0) return XPIPE_OK;
+  if (!out) return fail(XPIPE_EINVAL, "null output");
+  XP_HIP(launch_probe_mfma(out, waves, iters, (hipStream_t)hip_stream));
+  return XPIPE_OK;
+}
+
 xpipe_status xpipe_stage_set_timing(xpipe_stage_t st, int32_t enable) {
   if (!st) return fail(XPIPE_EINVAL, "null stage");
   st->timing = enable != 0;

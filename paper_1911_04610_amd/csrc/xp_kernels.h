@@ -207,4 +207,8 @@ struct CeArgs {
 };
 hipError_t launch_softmax_ce(int dtype, const CeArgs& a, hipStream_t s);
 
+// ---------------------------------------------------------------- measurement probes
+hipError_t launch_probe_copy(const void* src, void* dst, int64_t bytes, hipStream_t s);
+hipError_t launch_probe_mfma(float* out, int waves, int iters, hipStream_t s);
+
 }  // namespace xp

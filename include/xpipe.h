@@ -218,6 +218,18 @@ xpipe_status xpipe_adam_flat(float* W, float* m, float* v, float* G, int64_t n,
  * GEMM kernels k_conv_gemm / k_wgrad, bytes moved for all others).
  * Enabling (or re-enabling) clears the accumulated entries. */
 xpipe_status xpipe_stage_set_timing(xpipe_stage_t st, int32_t enable);
+
+/* Recorded passes (on by default; the environment variable XPIPE_GRAPHS=0
+ * turns them off at creation).  xpipe_stage_fwd and xpipe_stage_bwd capture
+ * each distinct combination of their pointer arguments once into a HIP graph
+ * (all launch lanes, same kernels and arguments as the eager launches) and
+ * replay it on later calls, so a pass costs one graph launch on the host.  At
+ * most 64 graphs are kept (least recently used are dropped).  Results are
+ * identical with or without graphs.  A pointer argument must keep describing
+ * the same buffer between calls that pass it (a freed and reallocated buffer
+ * of the same size at the same address is fine).  Timing mode runs eagerly.
+ * xpipe_stage_set_graphs turns recording on or off and drops the kept graphs. */
+xpipe_status xpipe_stage_set_graphs(xpipe_stage_t st, int32_t enable);
 xpipe_status xpipe_stage_timing_count(xpipe_stage_t st, int32_t* n);
 xpipe_status xpipe_stage_timing_entry(xpipe_stage_t st, int32_t i, const char** kernel, double* ms,
                                       int64_t* launches, double* work);

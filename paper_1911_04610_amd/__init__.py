@@ -85,6 +85,7 @@ _SIGS = {
     "xpipe_probe_copy": [_P, _P, _I64, _P],
     "xpipe_probe_mfma": [_P, _I32, _I32, _P],
     "xpipe_stage_set_timing": [_P, _I32],
+    "xpipe_stage_set_graphs": [_P, _I32],
     "xpipe_stage_timing_count": [_P, ctypes.POINTER(_I32)],
     "xpipe_stage_timing_entry": [_P, _I32, ctypes.POINTER(ctypes.c_char_p),
                                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64),
@@ -243,6 +244,9 @@ class Stage:
 
     def set_timing(self, enable: bool):
         _check(lib().xpipe_stage_set_timing(self._h, int(enable)))
+
+    def set_graphs(self, enable: bool):
+        _check(lib().xpipe_stage_set_graphs(self._h, int(enable)))
 
     def timing(self):
         """{kernel name: (ms, launches, work)} over the launches since set_timing(True)."""

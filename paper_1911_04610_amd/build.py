@@ -28,7 +28,9 @@ def _flags():
     return ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
             "-Wall", "-Wno-unused-function", "-Wno-unused-result",
             # keep the compiler away from packed fp32 math (v_pk_*_f32)
-            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            # MFMA accumulators in ordinary VGPRs: no AGPR copies in the GEMM loops
+            "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 
 
 def build(verbose=False):

@@ -106,8 +106,14 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   constexpr int A_PER = (A_CH + 255) / 256, B_PER = (B_CH + 255) / 256;
   static_assert(WM * WN == 4, "four waves");
   static_assert(TM >= 1 && TN >= 1, "wave tile");
-  __shared__ __align__(16) T sA[2][BM * PITCH];
-  __shared__ __align__(16) T sB[2][BN * PITCH];
+  // bf16: the epilogue stages the fp32 result tile in the same LDS, rows
+  // padded so that the accumulator layouts write it without bank conflicts
+  constexpr int OPITCH = BN + (M32 ? 8 : 4);
+  constexpr int STAGE_BYTES = 2 * (BM + BN) * PITCH * (int)sizeof(T);
+  constexpr int OUT_BYTES = sizeof(T) == 2 ? BM * OPITCH * 4 : 0;
+  __shared__ __align__(16) unsigned char smem[STAGE_BYTES > OUT_BYTES ? STAGE_BYTES : OUT_BYTES];
+  T (*sA)[BM * PITCH] = reinterpret_cast<T (*)[BM * PITCH]>(smem);
+  T (*sB)[BN * PITCH] = reinterpret_cast<T (*)[BN * PITCH]>(smem + 2 * BM * PITCH * sizeof(T));
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -210,16 +216,14 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
         const auto v = __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0);
         rb[slot][i] = make_uint4(v[0], v[1], v[2], v[3]);
       }
-      if (++loaded < nk) {
-        if (++lcb == nCB) {
-          lcb = 0;
-          ++lrs;
-          if (++lq == S) {
-            lq = 0;
-            ++lr;
-          }
-        }
-      }
+      // advance the cursor without branches (the loop body stays one block)
+      const bool adv = ++loaded < nk;
+      const bool wc = adv && lcb + 1 == nCB;
+      const bool wq = wc && lq + 1 == S;
+      lcb = wc ? 0 : lcb + (int)adv;
+      lrs += (int)wc;
+      lq = wq ? 0 : lq + (int)wc;
+      lr += (int)wq;
     } else {
 #pragma unroll
       for (int i = 0; i < A_PER; ++i) {
@@ -251,14 +255,21 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
       }
     }
   };
+  // LDS element offset of each slot's chunk; a slot past the tile writes into
+  // the row padding (never read), so the stores need no branches
+  int a_lds[A_PER], b_lds[B_PER];
+#pragma unroll
+  for (int i = 0; i < A_PER; ++i)
+    a_lds[i] = a_slot[i] ? a_row[i] * PITCH + a_kc[i] * VEC : ((tid + i * 256 - A_CH) % BM) * PITCH + BK;
+#pragma unroll
+  for (int i = 0; i < B_PER; ++i)
+    b_lds[i] = b_slot[i] ? b_row[i] * PITCH + b_kc[i] * VEC : ((tid + i * 256 - B_CH) % BN) * PITCH + BK;
   auto lstore = [&](auto SLOT, int buf) __attribute__((always_inline)) {
     constexpr int slot = decltype(SLOT)::value;
 #pragma unroll
-    for (int i = 0; i < A_PER; ++i)
-      if (a_slot[i]) *reinterpret_cast<uint4*>(&sA[buf][a_row[i] * PITCH + a_kc[i] * VEC]) = ra[slot][i];
+    for (int i = 0; i < A_PER; ++i) *reinterpret_cast<uint4*>(&sA[buf][a_lds[i]]) = ra[slot][i];
 #pragma unroll
-    for (int i = 0; i < B_PER; ++i)
-      if (b_slot[i]) *reinterpret_cast<uint4*>(&sB[buf][b_row[i] * PITCH + b_kc[i] * VEC]) = rb[slot][i];
+    for (int i = 0; i < B_PER; ++i) *reinterpret_cast<uint4*>(&sB[buf][b_lds[i]]) = rb[slot][i];
   };
 
   constexpr int TM2 = M32 ? WTM / 32 : 1, TN2 = M32 ? WTN / 32 : 1;
@@ -353,10 +364,12 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     static_for<0, PF>([&](auto U) __attribute__((always_inline)) {
       constexpr int u = decltype(U)::value;
       const int kb = kb0 + u;
-      // slot u held tile kb, already in LDS
-      gload(min(kb + PF, nk - 1), U);
+      // MFMAs on tile kb first, then refill slot u (tile kb, already in LDS)
+      // with tile kb + PF and stage tile kb + 1 into the other buffer (last
+      // read one step ago); past the end both repeat the last tile harmlessly
       compute(kb & 1);
-      if (kb + 1 < nk) lstore(std::integral_constant<int, (u + 1) % PF>{}, (kb + 1) & 1);
+      gload(min(kb + PF, nk - 1), U);
+      lstore(std::integral_constant<int, (u + 1) % PF>{}, (kb + 1) & 1);
       __syncthreads();
     });
   }
@@ -370,81 +383,261 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     }
   });
 
-  // epilogue: bias, ReLU, mask, accumulate, round once on store
   T* __restrict__ y = (T*)a.y;
   const T* __restrict__ mask = (const T*)a.mask;
-  constexpr int NCOL = M32 ? TN2 : TN;  // column groups per lane
-  double cs[NCOL], cq[NCOL];  // column sums of the stored values (batch-norm statistics)
+  if constexpr (sizeof(T) == 2) {
+    // epilogue (bf16): stage the fp32 tile in LDS, then each thread finishes
+    // 8-column chunks of a row (bias, ReLU, mask, accumulate, round once) with
+    // 16-byte loads and stores, and leaves the stored values in LDS for the
+    // batch-norm column statistics.  The main loop ended with a barrier, so
+    // the operand tiles are free.
+    float* ot = reinterpret_cast<float*>(smem);
+    if constexpr (M32) {
+      // 32x32 result: lane l, register r holds row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32
 #pragma unroll
-  for (int j = 0; j < NCOL; ++j) cs[j] = cq[j] = 0.0;
-  auto emit = [&](double acc_v, int m, int n, int j) __attribute__((always_inline)) {
-    if (m < M && n < a.N) {
-      double v = acc_v;
-      if (a.bias) v += (double)a.bias[n];
-      if (a.relu) v = v > 0.0 ? v : 0.0;
-      if (mask && !(ldd(mask + (size_t)m * a.ldm + n) > 0.0)) v = 0.0;
-      T* p = y + (size_t)m * a.ldy + n;
-      if (a.accumulate) v += ldd(p);
-      std_(p, v);
-      if (a.stat_part) {
-        double sv = ldd(p);  // the stored (rounded) value, as the statistics see it
-        cs[j] += sv;
-        cq[j] += sv * sv;
-      }
-    }
-  };
-  if constexpr (M32) {
-    // 32x32 result: lane l, register r holds row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32
+      for (int i = 0; i < TM2; ++i)
 #pragma unroll
-    for (int i = 0; i < TM2; ++i)
+        for (int j = 0; j < TN2; ++j)
 #pragma unroll
-      for (int j = 0; j < TN2; ++j)
+          for (int r = 0; r < 16; ++r)
+            ot[(wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * OPITCH + wn * WTN +
+               j * 32 + (lane & 31)] = acc2[i][j][r];
+    } else {
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          emit((double)acc2[i][j][r], m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3),
-               n0 + wn * WTN + j * 32 + (lane & 31), j);
-  } else {
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          emit((double)acc[i][j][q], m0 + wm * WTM + i * 16 + MTT::out_row(lane, q),
-               n0 + wn * WTN + j * 16 + (lane & 15), j);
-  }
-  if (a.stat_part) {
-    // lanes that hold the same column add in a fixed butterfly order
-    constexpr int CW = M32 ? 32 : 16;  // columns per group
-#pragma unroll
-    for (int j = 0; j < NCOL; ++j) {
-      if constexpr (!M32) {
-        cs[j] += __shfl_xor(cs[j], 16, 64);
-        cq[j] += __shfl_xor(cq[j], 16, 64);
-      }
-      cs[j] += __shfl_xor(cs[j], 32, 64);
-      cq[j] += __shfl_xor(cq[j], 32, 64);
-    }
-    __shared__ double red[WM][2][BN];
-    if (lane < CW) {
-#pragma unroll
-      for (int j = 0; j < NCOL; ++j) {
-        red[wm][0][wn * WTN + j * CW + lane] = cs[j];
-        red[wm][1][wn * WTN + j * CW + lane] = cq[j];
-      }
+          for (int q = 0; q < 4; ++q)
+            ot[(wm * WTM + i * 16 + MTT::out_row(lane, q)) * OPITCH + wn * WTN + j * 16 + (lane & 15)] =
+                acc[i][j][q];
     }
     __syncthreads();
-    for (int col = tid; col < BN; col += 256) {
-      int n = n0 + col;
-      if (n >= a.N) continue;
-      double s0 = 0.0, s1 = 0.0;
+    constexpr int CPRN = BN / 8;  // 8-column chunks per tile row
+    static_assert(BN % 8 == 0, "chunked epilogue");
+    // 16-byte global access needs 8-element aligned rows and base pointers
+    const bool vy = (a.ldy % 8) == 0 && (reinterpret_cast<uintptr_t>(y) % 16) == 0;
+    const bool vm = mask && (a.ldm % 8) == 0 && (reinterpret_cast<uintptr_t>(mask) % 16) == 0;
+    // all loads of the thread's chunks are issued before its first store (a
+    // load after a store waits for the store on this hardware); full chunks
+    // take 16-byte accesses, a ragged last chunk (N not a multiple of 8) or
+    // unaligned views an element loop
+    typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+    constexpr int NCH = (BM * CPRN + 255) / 256;  // chunks per thread
+    int c_ne[NCH];
+    u32x4_t c_mask[NCH], c_old[NCH];
+    f32x4_t c_b0[NCH], c_b1[NCH];
+    const bool vb = a.bias && (reinterpret_cast<uintptr_t>(a.bias + n0) % 16) == 0;
 #pragma unroll
-      for (int w = 0; w < WM; ++w) {
-        s0 += red[w][0][col];
-        s1 += red[w][1][col];
+    for (int k = 0; k < NCH; ++k) {
+      const int c = k * 256 + tid;
+      const int row = c / CPRN, cc = c - row * CPRN;
+      const int m = m0 + row, nb = n0 + cc * 8;
+      const bool live = ((BM * CPRN) % 256 == 0 || c < BM * CPRN) && m < M && nb < a.N;
+      const int ne = live ? (a.N - nb < 8 ? a.N - nb : 8) : 0;  // valid columns in this chunk
+      c_ne[k] = ne;
+      c_mask[k] = c_old[k] = (u32x4_t){0u, 0u, 0u, 0u};
+      c_b0[k] = c_b1[k] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+      if (ne == 8) {
+        if (vb) {
+          c_b0[k] = *reinterpret_cast<const f32x4_t*>(a.bias + nb);
+          c_b1[k] = *reinterpret_cast<const f32x4_t*>(a.bias + nb + 4);
+        }
+        if (vm) c_mask[k] = *reinterpret_cast<const u32x4_t*>(mask + (size_t)m * a.ldm + nb);
+        if (a.accumulate && vy) c_old[k] = *reinterpret_cast<const u32x4_t*>(y + (size_t)m * a.ldy + nb);
       }
-      a.stat_part[((size_t)n * 2 + 0) * gridDim.x + blockIdx.x] = s0;
-      a.stat_part[((size_t)n * 2 + 1) * gridDim.x + blockIdx.x] = s1;
+      if (ne > 0 && (ne < 8 || (a.bias && !vb) || (mask && !vm) || (a.accumulate && !vy))) {
+        float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        uint16_t mv[8] = {0, 0, 0, 0, 0, 0, 0, 0}, ov[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (int e = 0; e < ne; ++e) {
+          if (a.bias) bv[e] = a.bias[nb + e];
+          if (mask) mv[e] = mask[(size_t)m * a.ldm + nb + e];
+          if (a.accumulate) ov[e] = y[(size_t)m * a.ldy + nb + e];
+        }
+        c_b0[k] = (f32x4_t){bv[0], bv[1], bv[2], bv[3]};
+        c_b1[k] = (f32x4_t){bv[4], bv[5], bv[6], bv[7]};
+        c_mask[k] = *reinterpret_cast<const u32x4_t*>(mv);
+        c_old[k] = *reinterpret_cast<const u32x4_t*>(ov);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) {
+      const int c = k * 256 + tid;
+      if ((BM * CPRN) % 256 != 0 && c >= BM * CPRN) break;
+      const int row = c / CPRN, cc = c - row * CPRN;
+      const int ne = c_ne[k];
+      float* o = &ot[row * OPITCH + cc * 8];
+      if (ne > 0) {
+        const f32x4_t lo = *reinterpret_cast<const f32x4_t*>(o);
+        const f32x4_t hi = *reinterpret_cast<const f32x4_t*>(o + 4);
+        float f[8];
+        if (!a.accumulate) {
+          // one rounding to fp32 of acc + bias equals the rounding of their
+          // exact double sum (53 >= 2 * 24 + 2), and ReLU and the mask commute
+          // with rounding, so fp32 arithmetic stores the same values
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            f[e] = lo[e] + c_b0[k][e];
+            f[e + 4] = hi[e] + c_b1[k][e];
+          }
+        } else {
+          // y + result: added to the double value, rounded once
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            double v = (double)(e < 4 ? lo[e] : hi[e - 4]) + (double)(e < 4 ? c_b0[k][e] : c_b1[k][e - 4]);
+            if (a.relu) v = v > 0.0 ? v : 0.0;
+            const uint32_t mw = c_mask[k][e >> 1];
+            if (mask && !(__uint_as_float((e & 1) ? (mw & 0xffff0000u) : (mw << 16)) > 0.0f)) v = 0.0;
+            const uint32_t ow = c_old[k][e >> 1];
+            v += (double)__uint_as_float((e & 1) ? (ow & 0xffff0000u) : (ow << 16));
+            f[e] = (float)v;
+          }
+        }
+        if (!a.accumulate) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            if (a.relu) f[e] = f[e] > 0.f ? f[e] : 0.f;
+            const uint32_t mw = c_mask[k][e >> 1];
+            if (mask && !(__uint_as_float((e & 1) ? (mw & 0xffff0000u) : (mw << 16)) > 0.0f)) f[e] = 0.f;
+          }
+        }
+        u32x4_t pr;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) pr[q] = f32x2_to_bf16x2(f[2 * q], f[2 * q + 1]);
+        T* p = y + (size_t)(m0 + row) * a.ldy + n0 + cc * 8;
+        if (vy && ne == 8) {
+          *reinterpret_cast<u32x4_t*>(p) = pr;
+        } else {
+          for (int e = 0; e < ne; ++e) p[e] = (uint16_t)(pr[e >> 1] >> ((e & 1) * 16));
+        }
+        if (a.stat_part) {
+          f32x4_t s0, s1;
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            s0[2 * q] = 2 * q < ne ? __uint_as_float(pr[q] << 16) : 0.f;
+            s0[2 * q + 1] = 2 * q + 1 < ne ? __uint_as_float(pr[q] & 0xffff0000u) : 0.f;
+            s1[2 * q] = 2 * q + 4 < ne ? __uint_as_float(pr[q + 2] << 16) : 0.f;
+            s1[2 * q + 1] = 2 * q + 5 < ne ? __uint_as_float(pr[q + 2] & 0xffff0000u) : 0.f;
+          }
+          *reinterpret_cast<f32x4_t*>(o) = s0;
+          *reinterpret_cast<f32x4_t*>(o + 4) = s1;
+        }
+      } else if (a.stat_part) {
+        *reinterpret_cast<f32x4_t*>(o) = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+        *reinterpret_cast<f32x4_t*>(o + 4) = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    if (a.stat_part) {
+      // column sums of the stored values: RS row ranges per column, then a
+      // fixed-order sum of the ranges
+      constexpr int RS = 256 / BN > 0 ? 256 / BN : 1;
+      constexpr int RROWS = BM / RS;
+      static_assert(BM % RS == 0 && RROWS % 4 == 0, "row ranges");
+      __shared__ double sred[RS][2][BN];
+      __syncthreads();
+      if (tid < RS * BN) {
+        const int col = tid % BN, part = tid / BN;
+        const float* oc = ot + part * RROWS * OPITCH + col;
+        // four interleaved partial sums, added in a fixed order
+        double s0[4] = {0.0, 0.0, 0.0, 0.0}, s1[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int r = 0; r < RROWS; ++r) {
+          const double sv = (double)oc[r * OPITCH];
+          s0[r & 3] += sv;
+          s1[r & 3] += sv * sv;
+        }
+        sred[part][0][col] = (s0[0] + s0[1]) + (s0[2] + s0[3]);
+        sred[part][1][col] = (s1[0] + s1[1]) + (s1[2] + s1[3]);
+      }
+      __syncthreads();
+      for (int col = tid; col < BN; col += 256) {
+        const int n = n0 + col;
+        if (n >= a.N) continue;
+        double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+        for (int q = 0; q < RS; ++q) {
+          s0 += sred[q][0][col];
+          s1 += sred[q][1][col];
+        }
+        a.stat_part[((size_t)n * 2 + 0) * gridDim.x + blockIdx.x] = s0;
+        a.stat_part[((size_t)n * 2 + 1) * gridDim.x + blockIdx.x] = s1;
+      }
+    }
+  } else {
+    // epilogue (fp32 storage): bias, ReLU, mask, accumulate, round once on store
+    constexpr int NCOL = M32 ? TN2 : TN;  // column groups per lane
+    double cs[NCOL], cq[NCOL];  // column sums of the stored values (batch-norm statistics)
+#pragma unroll
+    for (int j = 0; j < NCOL; ++j) cs[j] = cq[j] = 0.0;
+    auto emit = [&](double acc_v, int m, int n, int j) __attribute__((always_inline)) {
+      if (m < M && n < a.N) {
+        double v = acc_v;
+        if (a.bias) v += (double)a.bias[n];
+        if (a.relu) v = v > 0.0 ? v : 0.0;
+        if (mask && !(ldd(mask + (size_t)m * a.ldm + n) > 0.0)) v = 0.0;
+        T* p = y + (size_t)m * a.ldy + n;
+        if (a.accumulate) v += ldd(p);
+        std_(p, v);
+        if (a.stat_part) {
+          double sv = ldd(p);  // the stored (rounded) value, as the statistics see it
+          cs[j] += sv;
+          cq[j] += sv * sv;
+        }
+      }
+    };
+    if constexpr (M32) {
+      // 32x32 result: lane l, register r holds row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32
+#pragma unroll
+      for (int i = 0; i < TM2; ++i)
+#pragma unroll
+        for (int j = 0; j < TN2; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            emit((double)acc2[i][j][r], m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3),
+                 n0 + wn * WTN + j * 32 + (lane & 31), j);
+    } else {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            emit((double)acc[i][j][q], m0 + wm * WTM + i * 16 + MTT::out_row(lane, q),
+                 n0 + wn * WTN + j * 16 + (lane & 15), j);
+    }
+    if (a.stat_part) {
+      // lanes that hold the same column add in a fixed butterfly order
+      constexpr int CW = M32 ? 32 : 16;  // columns per group
+#pragma unroll
+      for (int j = 0; j < NCOL; ++j) {
+        if constexpr (!M32) {
+          cs[j] += __shfl_xor(cs[j], 16, 64);
+          cq[j] += __shfl_xor(cq[j], 16, 64);
+        }
+        cs[j] += __shfl_xor(cs[j], 32, 64);
+        cq[j] += __shfl_xor(cq[j], 32, 64);
+      }
+      __shared__ double red[WM][2][BN];
+      if (lane < CW) {
+#pragma unroll
+        for (int j = 0; j < NCOL; ++j) {
+          red[wm][0][wn * WTN + j * CW + lane] = cs[j];
+          red[wm][1][wn * WTN + j * CW + lane] = cq[j];
+        }
+      }
+      __syncthreads();
+      for (int col = tid; col < BN; col += 256) {
+        int n = n0 + col;
+        if (n >= a.N) continue;
+        double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+        for (int w = 0; w < WM; ++w) {
+          s0 += red[w][0][col];
+          s1 += red[w][1][col];
+        }
+        a.stat_part[((size_t)n * 2 + 0) * gridDim.x + blockIdx.x] = s0;
+        a.stat_part[((size_t)n * 2 + 1) * gridDim.x + blockIdx.x] = s1;
+      }
     }
   }
 }

@@ -159,6 +159,20 @@ struct xpipe_stage {
     void after(const char* name, double work) override;
   } hook;
   bool timing = false;
+  // recorded passes: each distinct (pass, caller pointers) is captured once
+  // into a HIP graph on cap_stream and replayed on the stage's stream
+  struct PassGraph {
+    int kind;                // 0 forward, 1 backward
+    const void* ptr[5];      // the call's pointers
+    hipGraphExec_t exec;
+    uint64_t used;           // last use, for eviction
+  };
+  bool graphs = true;
+  bool capturing = false;  // a pass is being recorded on cap_stream
+  std::vector<int> rec_order[2];  // op order while recording (see Plan)
+  hipStream_t cap_stream = nullptr;
+  std::vector<PassGraph> pass_graphs;
+  uint64_t graph_clock = 0;
   std::vector<TimeRec> pending;
   std::vector<hipEvent_t> pool;
   std::map<std::string, TimeAgg> agg;
@@ -181,6 +195,10 @@ struct Plan {
   int64_t P = 0;
   size_t ws = 0;
   int64_t bf_f_off = -1, bf_b_off = -1, colpart_off[NLANES] = {}, wpart_off[NLANES] = {};
+  // per pass, the order in which a recorded pass captures its ops: a
+  // topological order of the lane plan that takes the lanes in turn, so the
+  // graph's launches interleave the independent branches
+  std::vector<int> rec_order[2];
 };
 
 // Channel range a tensor occupies in its buffer: (buffer tensor, first, end).
@@ -272,6 +290,40 @@ void plan_lanes(Plan& p) {
           op.waits[pass].push_back(j);
           p.ops[j].record[pass] = true;
         }
+    }
+    // recording order: an op is ready once the previous op of its lane (in
+    // pass order) and the ops it waits for are placed; among ready ops take
+    // the lane placed least recently, then pass order
+    std::vector<int> seq;  // pass order without concats
+    for (int q = 0; q < n; ++q) {
+      const int i = pass == 0 ? q : n - 1 - q;
+      if (p.ops[i].kind != OP_CONCAT) seq.push_back(i);
+    }
+    std::vector<int> prev(n, -1), last(NLANES, -1);
+    for (int i : seq) {
+      prev[i] = last[p.ops[i].lane[pass]];
+      last[p.ops[i].lane[pass]] = i;
+    }
+    std::vector<char> placed(n, 0);
+    std::vector<long> lane_used(NLANES, -1);
+    std::vector<int>& order = p.rec_order[pass];
+    order.clear();
+    for (long step = 0; order.size() < seq.size(); ++step) {
+      int pick = -1;
+      for (int i : seq) {
+        if (placed[i] || (prev[i] >= 0 && !placed[prev[i]])) continue;
+        bool ready = true;
+        for (int j : p.ops[i].waits[pass]) ready = ready && placed[j];
+        if (!ready) continue;
+        if (pick < 0 || lane_used[p.ops[i].lane[pass]] < lane_used[p.ops[pick].lane[pass]]) pick = i;
+      }
+      if (pick < 0) {  // cannot happen for a plan built above; keep pass order
+        order = seq;
+        break;
+      }
+      placed[pick] = 1;
+      lane_used[p.ops[pick].lane[pass]] = step;
+      order.push_back(pick);
     }
   }
 }
@@ -796,19 +848,63 @@ double gemm_flops(const Tensor& tin, const Op& op) {
 
 // ---------------------------------------------------------------- lanes
 // One pass (forward or backward) over the ops, spread over the launch lanes.
-// With per-launch timing on, everything runs on the stage's stream.
+#define XP_OK(call)                        \
+  do {                                     \
+    xpipe_status s_ = (call);              \
+    if (s_ != XPIPE_OK) return s_;         \
+  } while (0)
+
+// With per-launch timing on, everything runs on the stage's stream.  While a
+// pass is being recorded, every launch goes to the capture stream and the
+// lanes become graph edges instead of events: before an op's first launch the
+// capture's dependency set is replaced by the last nodes of the op's lane and
+// of the ops it waits for, so the recorded graph has the same ordering as the
+// multi-stream execution (per-lane scratch still follows the op's lane).
 struct Lanes {
+  typedef std::vector<hipGraphNode_t> Nodes;
   xpipe_stage* st;
   int pass;
   bool used[NLANES] = {};
   bool forked = false;
+  Nodes ltail[NLANES];        // recording: last nodes per lane
+  std::vector<Nodes> otail;  // recording: last nodes of each op
+  bool started = false;
   Lanes(xpipe_stage* st_, int pass_) : st(st_), pass(pass_) {}
+  // recording: every lane starts after everything captured so far (the
+  // graph itself starts after the work enqueued before its launch)
+  xpipe_status start() {
+    if (started) return XPIPE_OK;
+    started = true;
+    otail.resize(st->ops.size());
+    XP_OK(capture_tail(ltail[0]));
+    for (int l = 1; l < NLANES; ++l) ltail[l] = ltail[0];
+    return XPIPE_OK;
+  }
+  xpipe_status capture_tail(Nodes& out) {
+    hipStreamCaptureStatus cs;
+    const hipGraphNode_t* d = nullptr;
+    size_t nd = 0;
+    XP_HIP(hipStreamGetCaptureInfo_v2(st->cap_stream, &cs, nullptr, nullptr, &d, &nd));
+    out.assign(d, d + nd);
+    return XPIPE_OK;
+  }
   bool single() const { return st->timing; }
   // stream for op i after its waits; the first use of an auxiliary lane in
   // the pass waits for the work enqueued on the stage's stream before it
   xpipe_status begin(int i, hipStream_t& s, int& lane) {
     const Op& op = st->ops[i];
     lane = single() ? 0 : op.lane[pass];
+    if (st->capturing) {
+      XP_OK(start());
+      s = st->cap_stream;
+      used[lane] = true;
+      Nodes d = ltail[lane];
+      for (int j : op.waits[pass])
+        for (hipGraphNode_t n : otail[j])
+          if (std::find(d.begin(), d.end(), n) == d.end()) d.push_back(n);
+      XP_HIP(hipStreamUpdateCaptureDependencies(s, d.data(), d.size(), hipStreamSetCaptureDependencies));
+      return XPIPE_OK;
+    }
     s = st->lane_stream[lane];
     if (lane > 0 && !used[lane]) {
       if (!forked) XP_HIP(hipEventRecord(st->fork_ev, st->stream));
@@ -821,11 +917,28 @@ struct Lanes {
     return XPIPE_OK;
   }
   xpipe_status end(int i, hipStream_t s) {
+    if (st->capturing) {
+      (void)s;
+      XP_OK(capture_tail(otail[i]));
+      ltail[st->ops[i].lane[pass]] = otail[i];
+      return XPIPE_OK;
+    }
     if (!single() && st->ops[i].record[pass]) XP_HIP(hipEventRecord(st->op_ev[pass][i], s));
     return XPIPE_OK;
   }
   // the stage's stream waits for every auxiliary lane used in the pass
   xpipe_status join() {
+    if (st->capturing) {
+      if (!started) return XPIPE_OK;
+      Nodes all;
+      for (int l = 0; l < NLANES; ++l)
+        if (used[l] || l == 0)
+          for (hipGraphNode_t n : ltail[l])
+            if (std::find(all.begin(), all.end(), n) == all.end()) all.push_back(n);
+      XP_HIP(hipStreamUpdateCaptureDependencies(st->cap_stream, all.data(), all.size(),
+                                                hipStreamSetCaptureDependencies));
+      return XPIPE_OK;
+    }
     for (int l = 1; l < NLANES; ++l)
       if (used[l]) {
         XP_HIP(hipEventRecord(st->join_ev[l], st->lane_stream[l]));
@@ -835,18 +948,21 @@ struct Lanes {
   }
 };
 
-#define XP_OK(call)                        \
-  do {                                     \
-    xpipe_status s_ = (call);              \
-    if (s_ != XPIPE_OK) return s_;         \
-  } while (0)
+// op order of a pass: pass order, or the interleaved order while recording
+std::vector<int> pass_order(const xpipe_stage* st, int pass) {
+  if (st->capturing) return st->rec_order[pass];
+  const int n = (int)st->ops.size();
+  std::vector<int> o(n);
+  for (int q = 0; q < n; ++q) o[q] = pass == 0 ? q : n - 1 - q;
+  return o;
+}
 
 // ---------------------------------------------------------------- forward
 xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* labels,
                          float* loss) {
   const int dt = st->dtype;
   Lanes lanes(st, 0);
-  for (int i = 0; i < (int)st->ops.size(); ++i) {
+  for (int i : pass_order(st, 0)) {
     const Op& op = st->ops[i];
     if (op.kind == OP_CONCAT) continue;
     hipStream_t s;
@@ -1020,7 +1136,7 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
   }
 
   Lanes lanes(st, 1);
-  for (int i = (int)st->ops.size() - 1; i >= 0; --i) {
+  for (int i : pass_order(st, 1)) {
     const Op& op = st->ops[i];
     if (op.kind == OP_CONCAT) continue;
     XP_OK(lanes.begin(i, s, lane));
@@ -1303,7 +1419,14 @@ xpipe_status refresh_flipped(xpipe_stage* st) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
+void drop_graphs(xpipe_stage* st) {
+  for (auto& g : st->pass_graphs) (void)hipGraphExecDestroy(g.exec);
+  st->pass_graphs.clear();
+}
+
 void release_lanes(xpipe_stage* st) {
+  drop_graphs(st);
+  if (st->cap_stream) (void)hipStreamDestroy(st->cap_stream);
   for (int pass = 0; pass < 2; ++pass)
     for (hipEvent_t e : st->op_ev[pass])
       if (e) (void)hipEventDestroy(e);
@@ -1312,6 +1435,57 @@ void release_lanes(xpipe_stage* st) {
     if (st->join_ev[l]) (void)hipEventDestroy(st->join_ev[l]);
     if (st->lane_stream[l]) (void)hipStreamDestroy(st->lane_stream[l]);
   }
+}
+
+// Run one pass through its recorded graph: replay it if this (pass, pointers)
+// was seen before, else capture the pass's launches on cap_stream (the lanes
+// become graph edges), instantiate, keep, and replay.  The pass
+// reads only the call's pointers and the stage's own buffers, so a recorded
+// pass launches the same kernels with the same arguments as the eager one.
+// Timing mode runs eagerly.
+template <typename F>
+xpipe_status run_graphed(xpipe_stage* st, int kind, const void* const (&ptr)[5], F&& pass) {
+  if (!st->graphs || st->timing) return pass();
+  ++st->graph_clock;
+  for (auto& g : st->pass_graphs)
+    if (g.kind == kind && std::equal(ptr, ptr + 5, g.ptr)) {
+      g.used = st->graph_clock;
+      XP_HIP(hipGraphLaunch(g.exec, st->stream));
+      return XPIPE_OK;
+    }
+  hipStream_t caller = st->stream;
+  st->stream = st->lane_stream[0] = st->cap_stream;
+  st->capturing = true;
+  hipError_t e = hipStreamBeginCapture(st->cap_stream, hipStreamCaptureModeThreadLocal);
+  xpipe_status ps = e == hipSuccess ? pass() : XPIPE_OK;
+  hipGraph_t graph = nullptr;
+  hipError_t e2 = e == hipSuccess ? hipStreamEndCapture(st->cap_stream, &graph) : e;
+  st->capturing = false;
+  st->stream = st->lane_stream[0] = caller;
+  if (ps != XPIPE_OK || e != hipSuccess || e2 != hipSuccess) {
+    if (graph) (void)hipGraphDestroy(graph);
+    if (ps != XPIPE_OK) return ps;
+    return fail(XPIPE_EHIP, std::string("pass capture: ") + hipGetErrorString(e != hipSuccess ? e : e2));
+  }
+  hipGraphExec_t exec = nullptr;
+  e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(graph);
+  if (e != hipSuccess) return fail(XPIPE_EHIP, std::string("hipGraphInstantiate: ") + hipGetErrorString(e));
+  constexpr size_t MAX_GRAPHS = 64;
+  if (st->pass_graphs.size() >= MAX_GRAPHS) {
+    auto old = std::min_element(st->pass_graphs.begin(), st->pass_graphs.end(),
+                                [](const auto& a, const auto& b) { return a.used < b.used; });
+    (void)hipGraphExecDestroy(old->exec);
+    st->pass_graphs.erase(old);
+  }
+  xpipe_stage::PassGraph g{};
+  g.kind = kind;
+  std::copy(ptr, ptr + 5, g.ptr);
+  g.exec = exec;
+  g.used = st->graph_clock;
+  st->pass_graphs.push_back(g);
+  XP_HIP(hipGraphLaunch(exec, st->stream));
+  return XPIPE_OK;
 }
 
 }  // namespace
@@ -1402,6 +1576,8 @@ xpipe_status xpipe_stage_create(const xpipe_layer_desc* layers, int32_t n_layers
   st->params = p.params;
   st->tensors = p.tensors;
   st->ops = p.ops;
+  st->rec_order[0] = p.rec_order[0];
+  st->rec_order[1] = p.rec_order[1];
   st->out_tensor = p.out_tensor;
   st->has_loss = p.has_loss;
   st->classes = p.classes;
@@ -1417,6 +1593,8 @@ xpipe_status xpipe_stage_create(const xpipe_layer_desc* layers, int32_t n_layers
   st->lane_stream[0] = st->stream;
   for (int l = 1; l < NLANES && e == hipSuccess; ++l)
     e = hipStreamCreateWithFlags(&st->lane_stream[l], hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&st->cap_stream, hipStreamNonBlocking);
+  if (const char* g = std::getenv("XPIPE_GRAPHS"); g && *g == '0') st->graphs = false;
   if (e == hipSuccess) e = hipEventCreateWithFlags(&st->fork_ev, hipEventDisableTiming);
   for (int l = 1; l < NLANES && e == hipSuccess; ++l)
     e = hipEventCreateWithFlags(&st->join_ev[l], hipEventDisableTiming);
@@ -1498,7 +1676,9 @@ xpipe_status xpipe_stage_fwd(xpipe_stage_t st, const void* x, void* y, const int
   Ctx c;
   c.x = x;
   c.y = y;
-  return run_forward(st, XPIPE_FWD, c, labels, st->has_loss ? loss : nullptr);
+  float* ls = st->has_loss ? loss : nullptr;
+  const void* const key[5] = {x, y, labels, ls, nullptr};
+  return run_graphed(st, 0, key, [&] { return run_forward(st, XPIPE_FWD, c, labels, ls); });
 }
 
 xpipe_status xpipe_stage_bwd(xpipe_stage_t st, const void* x, const void* dy, const int32_t* labels, void* dx) {
@@ -1512,11 +1692,20 @@ xpipe_status xpipe_stage_bwd(xpipe_stage_t st, const void* x, const void* dy, co
   Ctx c;
   c.x = x;
   c.dx = dx;
-  xpipe_status s = run_forward(st, XPIPE_BWD, c, nullptr, nullptr);
-  if (s != XPIPE_OK) return s;
-  s = run_backward(st, c, dy, labels);
+  const void* const key[5] = {x, dy, labels, dx, nullptr};
+  xpipe_status s = run_graphed(st, 1, key, [&] {
+    xpipe_status r = run_forward(st, XPIPE_BWD, c, nullptr, nullptr);
+    return r != XPIPE_OK ? r : run_backward(st, c, dy, labels);
+  });
   if (s != XPIPE_OK) return s;
   st->bwd_since_step++;
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_set_graphs(xpipe_stage_t st, int32_t enable) {
+  if (!st) return fail(XPIPE_EINVAL, "null stage");
+  st->graphs = enable != 0;
+  drop_graphs(st);
   return XPIPE_OK;
 }
 

@@ -23,10 +23,11 @@ class GpuRecord:
 
 
 def run_stage(w, inp, dtype, hp, s_fwd, s_bwd, minibatches=None, fused=True, need_dx=True,
-              stage=None):
+              stage=None, reuse_inputs=False):
     """Mini-batch loop of the XPipe stage step on the GPU.  With fused=True the
     Adam step also emits the next mini-batch's predictions (no separate
-    predict calls after the first mini-batch)."""
+    predict calls after the first mini-batch).  reuse_inputs feeds mini-batch
+    0's buffers to every mini-batch (same pointers on every call)."""
     import torch
     J = len(inp.xs) if minibatches is None else minibatches
     st = stage or xp.Stage(w.layers, w.micro_batch, w.T, w.in_shape, dtype)
@@ -45,9 +46,10 @@ def run_stage(w, inp, dtype, hp, s_fwd, s_bwd, minibatches=None, fused=True, nee
     out_shape_oracle = (n, C) if (H == 1 and W_ == 1 and len(w.in_shape) == 1) or w.has_loss else (n, H, W_, C)
     recs = []
     t = 0
-    for j in range(J):
+    for jj in range(J):
+        j = 0 if reuse_inputs else jj
         r = GpuRecord()
-        if j == 0 or not fused:
+        if jj == 0 or not fused:
             st.xpipe_predict_weights(xp.FWD, s_fwd, hp, t)
         for i in range(w.T):
             st.xpipe_stage_fwd(xs[j][i], y, None if labels is None else labels[j][i],
@@ -55,7 +57,7 @@ def run_stage(w, inp, dtype, hp, s_fwd, s_bwd, minibatches=None, fused=True, nee
             r.ys.append(to_host(y).reshape(out_shape_oracle))
             r.losses.append(float(loss.item()) if w.has_loss else None)
         r.w_pred_fwd = st.get_tensors(st.w_pred_fwd)
-        if j == 0 or not fused:
+        if jj == 0 or not fused:
             st.xpipe_predict_weights(xp.BWD, s_bwd, hp, t)
         r.w_pred_bwd = st.get_tensors(st.w_pred_bwd)
         for i in range(w.T):

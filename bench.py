@@ -70,7 +70,9 @@ def kernel_key(name):
 
 def traffic_run(args):
     import torch
-    w, ms, wall, classes, fin = time_stage(args, timing_pass=False)
+    # eager launches: the counters are taken per dispatch (same kernels and
+    # arguments as the recorded passes)
+    w, ms, wall, classes, fin = time_stage(args, timing_pass=False, graphs=False)
     a = torch.empty(CALIB_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
     b = torch.empty_like(a)
     for _ in range(3):
@@ -129,7 +131,7 @@ def stored_traffic(kernel):
     return None if k is None else k["traffic_bytes"]
 
 
-def time_stage(args, timing_pass=True):
+def time_stage(args, timing_pass=True, graphs=True):
     import torch
     import paper_1911_04610_amd as xp
     import workloads as wl
@@ -139,6 +141,7 @@ def time_stage(args, timing_pass=True):
     inp = wl.stage_inputs(w, act_dtype=args.dtype if args.dtype == "bf16" else "f32",
                           moment_init="paper")
     st = xp.Stage(w.layers, w.micro_batch, w.T, w.in_shape, dt)
+    st.set_graphs(graphs)
     st.set_flat(st.W, inp.params)
     st.set_flat(st.m, inp.m)
     st.set_flat(st.v, inp.v)

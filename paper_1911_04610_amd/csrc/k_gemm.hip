@@ -88,6 +88,17 @@ XP_DEV void static_for(F&& f) {
   }
 }
 
+// Workgroups are dispatched to the 8 XCDs (each with its own L2) round-robin
+// by linear id.  Remap the linear id so that each XCD takes a contiguous run
+// of the logical tile order: neighbouring tiles (shared input rows, shared
+// pixel splits) then meet in one L2.  A bijection of [0, G).
+constexpr int XP_XCDS = 8;
+XP_DEV int xcd_tile(int l, int G) {
+  const int x = l % XP_XCDS, q = l / XP_XCDS;
+  const int per = G / XP_XCDS, rem = G % XP_XCDS;
+  return x * per + (x < rem ? x : rem) + q;
+}
+
 template <typename T, int BM, int BN, int WM, int WN, bool FLAT, int KS, int PF>
 __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   using MTT = MT<T>;
@@ -120,7 +131,10 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   const int H = a.H, W = a.W, C = a.C, S = a.S, pad = a.pad;
   const int M = a.nb * H * W;
   const int K = a.R * S * C;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  // logical tile (row tile tm, column tile tn), column tiles fastest
+  const int tlin = xcd_tile(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x * gridDim.y);
+  const int tm = tlin / gridDim.y, tn = tlin - tm * gridDim.y;
+  const int m0 = tm * BM, n0 = tn * BN;
   const T* __restrict__ x = (const T*)a.x;
   const T* __restrict__ w = (const T*)a.w;
 
@@ -559,8 +573,8 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
           s0 += sred[q][0][col];
           s1 += sred[q][1][col];
         }
-        a.stat_part[((size_t)n * 2 + 0) * gridDim.x + blockIdx.x] = s0;
-        a.stat_part[((size_t)n * 2 + 1) * gridDim.x + blockIdx.x] = s1;
+        a.stat_part[((size_t)n * 2 + 0) * gridDim.x + tm] = s0;
+        a.stat_part[((size_t)n * 2 + 1) * gridDim.x + tm] = s1;
       }
     }
   } else {
@@ -635,8 +649,8 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
           s0 += red[w][0][col];
           s1 += red[w][1][col];
         }
-        a.stat_part[((size_t)n * 2 + 0) * gridDim.x + blockIdx.x] = s0;
-        a.stat_part[((size_t)n * 2 + 1) * gridDim.x + blockIdx.x] = s1;
+        a.stat_part[((size_t)n * 2 + 0) * gridDim.x + tm] = s0;
+        a.stat_part[((size_t)n * 2 + 1) * gridDim.x + tm] = s1;
       }
     }
   }

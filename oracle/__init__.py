@@ -7,16 +7,21 @@ leg of bench.py may import or run anything here; the product path must never
 route through it.
 
 Contents:
-  method  Eq. 1 / Eq. 2 version difference, Eq. 3 / Eq. 4 prediction, Adam update
+  method  Eq. 1 / Eq. 2 version difference, Eq. 3 / Eq. 4 prediction, Adam update,
+          momentum-SGD and RMSProp updates that keep the prediction's Adam moments
   layers  layer forwards and VJPs (conv, linear, BN, ReLU, pools, GAP, CE)
   stage   a stage's forward, backward-with-recompute and the mini-batch driver
 """
 from .method import (HALF_DOWN, HALF_EVEN, HALF_UP, PRED_ADAMDIR, PRED_EQ3, PRED_LITERAL,
-                     adam_update, predict, version_difference_bwd, version_difference_fwd)
+                     RULE_ADAM, RULE_MOMENTUM_SGD, RULE_RMSPROP, adam_moments, adam_update,
+                     momentum_sgd_update, predict, rmsprop_update, version_difference_bwd,
+                     version_difference_fwd)
 from .stage import Hyper, MinibatchRecord, Stage, train_stage
 
 __all__ = [
     "HALF_DOWN", "HALF_EVEN", "HALF_UP", "PRED_ADAMDIR", "PRED_EQ3", "PRED_LITERAL",
-    "adam_update", "predict", "version_difference_bwd", "version_difference_fwd",
+    "RULE_ADAM", "RULE_MOMENTUM_SGD", "RULE_RMSPROP", "adam_moments", "adam_update",
+    "momentum_sgd_update", "predict", "rmsprop_update", "version_difference_bwd",
+    "version_difference_fwd",
     "Hyper", "MinibatchRecord", "Stage", "train_stage",
 ]

@@ -1,5 +1,6 @@
 """XPipe's method steps in plain fp64 numpy: version difference, weight
-prediction and the Adam update.
+prediction, the Adam update, and the other update rules the paper trains
+with while predicting from Adam moments (momentum SGD, RMSProp).
 
 TEST INFRASTRUCTURE ONLY.  This module is the CPU oracle that the GPU path is
 checked against; it is never part of the product path.  Only tests/,
@@ -106,3 +107,53 @@ def adam_update(W, m, v, G, t_next: int, lr: float, beta1: float, beta2: float,
     v_hat = v_new / (1.0 - beta2 ** t_next)
     W_new = W - lr * m_hat / (np.sqrt(v_hat) + eps)
     return W_new, m_new, v_new
+
+
+# update rules besides Adam; the prediction always uses Adam moments
+RULE_ADAM = "adam"
+RULE_MOMENTUM_SGD = "momentum_sgd"
+RULE_RMSPROP = "rmsprop"
+
+
+def adam_moments(m, v, g, beta1: float, beta2: float):
+    """Eq. 4's running averages of the gradient and of its square, the state
+    XPipe's prediction reads (Sec. III-B), advanced by one gradient g."""
+    m = np.asarray(m, np.float64)
+    v = np.asarray(v, np.float64)
+    g = np.asarray(g, np.float64)
+    return beta1 * m + (1.0 - beta1) * g, beta2 * v + (1.0 - beta2) * g * g
+
+
+def momentum_sgd_update(W, buf, m, v, G, lr: float, momentum: float, weight_decay: float,
+                        beta1: float, beta2: float):
+    """Momentum SGD with weight decay, the update rule of the paper's main
+    experiments (Sec. IV-B: momentum 0.9, weight decay 5e-4), with the Adam
+    moments that the prediction of Eq. 3 keeps (Sec. III-B) advanced by the same
+    gradient.  Heavy-ball form without dampening: g = G + wd * W,
+    buf = momentum * buf + g, W = W - lr * buf.  Returns (W, buf, m, v) in fp64."""
+    W = np.asarray(W, np.float64)
+    buf = np.asarray(buf, np.float64)
+    g = np.asarray(G, np.float64) + weight_decay * W
+    buf_new = momentum * buf + g
+    W_new = W - lr * buf_new
+    m_new, v_new = adam_moments(m, v, g, beta1, beta2)
+    return W_new, buf_new, m_new, v_new
+
+
+def rmsprop_update(W, buf, sq, m, v, G, lr: float, alpha: float, eps: float, momentum: float,
+                   weight_decay: float, beta1: float, beta2: float):
+    """RMSProp with momentum, the update rule of the robustness study (Sec. IV-D:
+    momentum 0.9), with the prediction's Adam moments advanced by the same
+    gradient.  Tieleman and Hinton's running mean of the squared gradient with
+    eps outside the root: g = G + wd * W, sq = alpha * sq + (1 - alpha) * g * g,
+    buf = momentum * buf + g / (sqrt(sq) + eps), W = W - lr * buf.
+    Returns (W, buf, sq, m, v) in fp64."""
+    W = np.asarray(W, np.float64)
+    buf = np.asarray(buf, np.float64)
+    sq = np.asarray(sq, np.float64)
+    g = np.asarray(G, np.float64) + weight_decay * W
+    sq_new = alpha * sq + (1.0 - alpha) * g * g
+    buf_new = momentum * buf + g / (np.sqrt(sq_new) + eps)
+    W_new = W - lr * buf_new
+    m_new, v_new = adam_moments(m, v, g, beta1, beta2)
+    return W_new, buf_new, sq_new, m_new, v_new

@@ -35,7 +35,8 @@ from typing import List, Optional
 import numpy as np
 
 from . import layers as ly
-from .method import adam_update, predict, PRED_EQ3
+from .method import (adam_update, momentum_sgd_update, predict, rmsprop_update, PRED_EQ3,
+                     RULE_ADAM, RULE_MOMENTUM_SGD, RULE_RMSPROP)
 
 
 def _round_f32(a):
@@ -213,6 +214,13 @@ class Hyper:
     beta2: float = 0.999
     eps: float = 1e-8
     mode: str = PRED_EQ3
+    # update rule at the mini-batch boundary (the prediction always uses the
+    # Adam moments m, v): Adam, momentum SGD (Sec. IV-B) or RMSProp (Sec. IV-D)
+    rule: str = RULE_ADAM
+    momentum: float = 0.9
+    weight_decay: float = 0.0
+    alpha: float = 0.99        # RMSProp's decay of the squared-gradient average
+    rms_eps: float = 1e-8      # RMSProp's eps, outside the root
 
 
 @dataclasses.dataclass
@@ -227,6 +235,8 @@ class MinibatchRecord:
     W: List[np.ndarray]             # after the update
     m: List[np.ndarray]
     v: List[np.ndarray]
+    buf: Optional[List[np.ndarray]] = None  # momentum buffer (momentum SGD, RMSProp)
+    sq: Optional[List[np.ndarray]] = None   # RMSProp's squared-gradient average
 
 
 def train_stage(stage: Stage, params, m, v, xs, s_fwd: int, s_bwd: int, hp: Hyper,
@@ -239,6 +249,8 @@ def train_stage(stage: Stage, params, m, v, xs, s_fwd: int, s_bwd: int, hp: Hype
     m = [qs(np.asarray(a, np.float64)) for a in m]
     v = [qs(np.asarray(a, np.float64)) for a in v]
     t = t0
+    buf = [np.zeros_like(a) for a in W]   # momentum buffer (momentum SGD, RMSProp)
+    sq = [np.zeros_like(a) for a in W]    # RMSProp's squared-gradient average
     J = len(xs) if minibatches is None else minibatches
     T = len(xs[0])
     N = T * xs[0][0].shape[0]
@@ -263,12 +275,28 @@ def train_stage(stage: Stage, params, m, v, xs, s_fwd: int, s_bwd: int, hp: Hype
             for k in range(len(G)):
                 G[k] = qs(G[k] + gs[k])
             dxs.append(dx)
-        # update at the T-th backward (Sec. III-A), Adam with Eq. 4's moments
+        # update at the T-th backward (Sec. III-A): Adam with Eq. 4's moments,
+        # or momentum SGD / RMSProp with the same moments kept for prediction
         t += 1
-        new = [adam_update(W[k], m[k], v[k], G[k], t, hp.lr, hp.beta1, hp.beta2, hp.eps)
-               for k in range(len(W))]
-        W = [qs(a[0]) for a in new]
-        m = [qs(a[1]) for a in new]
-        v = [qs(a[2]) for a in new]
-        out.append(MinibatchRecord(t - 1, Wf, Wb, ys, losses, dxs, G, W, m, v))
+        if hp.rule == RULE_ADAM:
+            new = [adam_update(W[k], m[k], v[k], G[k], t, hp.lr, hp.beta1, hp.beta2, hp.eps)
+                   for k in range(len(W))]
+            W = [qs(a[0]) for a in new]
+            m = [qs(a[1]) for a in new]
+            v = [qs(a[2]) for a in new]
+        elif hp.rule == RULE_MOMENTUM_SGD:
+            new = [momentum_sgd_update(W[k], buf[k], m[k], v[k], G[k], hp.lr, hp.momentum,
+                                       hp.weight_decay, hp.beta1, hp.beta2)
+                   for k in range(len(W))]
+            W, buf, m, v = ([qs(a[q]) for a in new] for q in range(4))
+        elif hp.rule == RULE_RMSPROP:
+            new = [rmsprop_update(W[k], buf[k], sq[k], m[k], v[k], G[k], hp.lr, hp.alpha,
+                                  hp.rms_eps, hp.momentum, hp.weight_decay, hp.beta1, hp.beta2)
+                   for k in range(len(W))]
+            W, buf, sq, m, v = ([qs(a[q]) for a in new] for q in range(5))
+        else:
+            raise ValueError(hp.rule)
+        out.append(MinibatchRecord(t - 1, Wf, Wb, ys, losses, dxs, G, W, m, v,
+                                   None if hp.rule == RULE_ADAM else list(buf),
+                                   list(sq) if hp.rule == RULE_RMSPROP else None))
     return out

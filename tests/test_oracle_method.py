@@ -186,3 +186,93 @@ def test_adam_zero_gradient_keeps_zero_state():
     z = np.zeros(8)
     W, m, v = om.adam_update(z, z, z, z, 5, **HP)
     assert not W.any() and not m.any() and not v.any()
+
+
+# ------------------------------------------------------------------ momentum SGD / RMSProp
+SGD = dict(lr=1e-2, momentum=0.9, weight_decay=5e-4)      # Sec. IV-B's settings
+RMS = dict(lr=1e-4, alpha=0.99, eps=1e-8, momentum=0.9, weight_decay=0.0)  # Sec. IV-D
+
+
+@pytest.mark.parametrize("wd", [0.0, 5e-4])
+def test_momentum_sgd_matches_torch_optim(wd):
+    """torch.optim.SGD (float64, CPU; momentum, no dampening, weight decay added
+    to the gradient) is an independent implementation of the same rule."""
+    rng = np.random.default_rng(11)
+    n = 500
+    W0 = rng.normal(0, 0.05, n)
+    grads = [rng.normal(0, 10 ** rng.uniform(-4, -1), n) for _ in range(6)]
+    p = torch.nn.Parameter(torch.tensor(W0, dtype=torch.float64))
+    opt = torch.optim.SGD([p], lr=SGD["lr"], momentum=SGD["momentum"], weight_decay=wd)
+    W, buf, m, v = W0.copy(), np.zeros(n), np.zeros(n), np.zeros(n)
+    for g in grads:
+        p.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        W, buf, m, v = om.momentum_sgd_update(W, buf, m, v, g, SGD["lr"], SGD["momentum"], wd,
+                                             HP["beta1"], HP["beta2"])
+        np.testing.assert_allclose(W, p.detach().numpy(), rtol=0, atol=1e-15)
+        np.testing.assert_allclose(buf, opt.state[p]["momentum_buffer"].numpy(), rtol=1e-13, atol=1e-18)
+
+
+@pytest.mark.parametrize("wd,mom", [(0.0, 0.9), (5e-4, 0.9), (0.0, 0.0)])
+def test_rmsprop_matches_torch_optim(wd, mom):
+    """torch.optim.RMSprop (float64, CPU; not centered, eps outside the root,
+    momentum buffer of the normalised gradient) is an independent implementation."""
+    rng = np.random.default_rng(12)
+    n = 500
+    W0 = rng.normal(0, 0.05, n)
+    grads = [rng.normal(0, 10 ** rng.uniform(-4, -1), n) for _ in range(6)]
+    p = torch.nn.Parameter(torch.tensor(W0, dtype=torch.float64))
+    opt = torch.optim.RMSprop([p], lr=RMS["lr"], alpha=RMS["alpha"], eps=RMS["eps"],
+                              momentum=mom, weight_decay=wd)
+    W, buf, sq, m, v = W0.copy(), np.zeros(n), np.zeros(n), np.zeros(n), np.zeros(n)
+    for g in grads:
+        p.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        W, buf, sq, m, v = om.rmsprop_update(W, buf, sq, m, v, g, RMS["lr"], RMS["alpha"], RMS["eps"],
+                                             mom, wd, HP["beta1"], HP["beta2"])
+        np.testing.assert_allclose(W, p.detach().numpy(), rtol=0, atol=1e-15)
+        np.testing.assert_allclose(sq, opt.state[p]["square_avg"].numpy(), rtol=1e-13, atol=1e-30)
+
+
+@pytest.mark.parametrize("k", [1, 2, 7])
+def test_momentum_sgd_constant_gradient_closed_form(k):
+    """Constant gradient c, no weight decay, from zero state: the buffer is the
+    geometric sum c (1 - mu^j) / (1 - mu) after j steps, W moves by lr times
+    the sum of the buffers, and the Adam moments are c (1 - beta1^k) and
+    c^2 (1 - beta2^k)."""
+    c = np.array([0.3, -1e-3, 2.0, 0.0])
+    mu, lr = SGD["momentum"], SGD["lr"]
+    W, buf, m, v = np.ones(4), np.zeros(4), np.zeros(4), np.zeros(4)
+    for _ in range(k):
+        W, buf, m, v = om.momentum_sgd_update(W, buf, m, v, c, lr, mu, 0.0, HP["beta1"], HP["beta2"])
+    bufs = [c * (1 - mu ** j) / (1 - mu) for j in range(1, k + 1)]
+    np.testing.assert_allclose(buf, bufs[-1], rtol=1e-13, atol=0)
+    np.testing.assert_allclose(W, 1.0 - lr * sum(bufs), rtol=1e-13, atol=0)
+    np.testing.assert_allclose(m, c * (1 - HP["beta1"] ** k), rtol=1e-13, atol=0)
+    np.testing.assert_allclose(v, c * c * (1 - HP["beta2"] ** k), rtol=1e-12, atol=0)
+
+
+@pytest.mark.parametrize("k", [1, 3])
+def test_rmsprop_constant_gradient_closed_form(k):
+    """Constant gradient c, no momentum, no weight decay: the squared average
+    is c^2 (1 - alpha^j) after j steps and each step moves W by
+    lr c / (|c| sqrt(1 - alpha^j) + eps)."""
+    c = np.array([0.5, -2e-2, 3.0])
+    a, e, lr = RMS["alpha"], RMS["eps"], RMS["lr"]
+    W, buf, sq, m, v = np.zeros(3), np.zeros(3), np.zeros(3), np.zeros(3), np.zeros(3)
+    for _ in range(k):
+        W, buf, sq, m, v = om.rmsprop_update(W, buf, sq, m, v, c, lr, a, e, 0.0, 0.0,
+                                             HP["beta1"], HP["beta2"])
+    np.testing.assert_allclose(sq, c * c * (1 - a ** k), rtol=1e-12, atol=0)
+    steps = [lr * c / (np.abs(c) * np.sqrt(1 - a ** j) + e) for j in range(1, k + 1)]
+    np.testing.assert_allclose(W, -sum(steps), rtol=1e-12, atol=0)
+
+
+def test_update_rules_weight_decay_reaches_the_moments():
+    """The prediction's moments track the gradient the rule steps on: with
+    G = 0 and weight decay wd they see wd * W."""
+    W = np.array([0.5, -1.0])
+    z = np.zeros(2)
+    _, _, m, v = om.momentum_sgd_update(W, z, z, z, z, 1e-2, 0.9, 1e-3, HP["beta1"], HP["beta2"])
+    np.testing.assert_allclose(m, (1 - HP["beta1"]) * 1e-3 * W, rtol=1e-15, atol=0)
+    np.testing.assert_allclose(v, (1 - HP["beta2"]) * (1e-3 * W) ** 2, rtol=1e-14, atol=0)

@@ -101,6 +101,36 @@ def test_no_pipeline_reduces_to_plain_adam_training(name):
             np.testing.assert_allclose(a, b.detach().numpy(), rtol=0, atol=1e-13)
 
 
+@pytest.mark.parametrize("rule", [oracle.RULE_MOMENTUM_SGD, oracle.RULE_RMSPROP])
+def test_no_pipeline_reduces_to_plain_training_other_rules(rule):
+    """One stage, T = 1, s = 0 with momentum SGD (weight decay 5e-4) or RMSProp
+    (momentum 0.9) as the update rule: ordinary training with torch.optim.SGD
+    or torch.optim.RMSprop of a torch float64 model."""
+    w = _small("tiny_mlp", T=1, minibatches=3)
+    inp = wl.stage_inputs(w)
+    st = oracle.Stage(w.layers)
+    if rule == oracle.RULE_MOMENTUM_SGD:
+        hp = oracle.Hyper(lr=1e-2, rule=rule, momentum=0.9, weight_decay=5e-4)
+    else:
+        hp = oracle.Hyper(lr=1e-4, rule=rule, momentum=0.9, alpha=0.99, rms_eps=1e-8)
+    recs = oracle.train_stage(st, inp.params, inp.m, inp.v, inp.xs, 0, 0, hp,
+                              labels=inp.labels, dys=inp.dys)
+    P = [torch.tensor(np.asarray(p, np.float64), requires_grad=True) for p in inp.params]
+    if rule == oracle.RULE_MOMENTUM_SGD:
+        opt = torch.optim.SGD(P, lr=hp.lr, momentum=hp.momentum, weight_decay=hp.weight_decay)
+    else:
+        opt = torch.optim.RMSprop(P, lr=hp.lr, alpha=hp.alpha, eps=hp.rms_eps, momentum=hp.momentum)
+    N = w.micro_batch
+    for j in range(w.minibatches):
+        opt.zero_grad()
+        xt = torch.tensor(np.asarray(inp.xs[j][0], np.float64))
+        y, loss = torch_ref.forward(w.layers, P, xt, inp.labels[j][0] if inp.labels else None, N)
+        loss.backward()
+        opt.step()
+        for a, b in zip(recs[j].W, P):
+            np.testing.assert_allclose(a, b.detach().numpy(), rtol=0, atol=1e-13)
+
+
 def test_prediction_changes_the_step_once_moments_exist():
     """t = 0 makes both predictions equal W (no update has happened yet); from
     the second mini-batch on, s > 0 moves the predicted weights by s times the

@@ -265,7 +265,17 @@ def time_sweep(n, steps):
     res["adam"] = {"ms": ms, "GB_s": 28.0 * n / ms / 1e6}
     ms = timed(lambda: xp.xpipe_adam_flat(W, m, v, G, hp, 100, True, pf, 2, pb, 1), reps)
     res["adam_zero_grad_2pred"] = {"ms": ms, "GB_s": 40.0 * n / ms / 1e6}
-    del W, m, v, G, out, pf, pb
+    # the other update rules with Adam-moment prediction, fused the same way:
+    # momentum SGD 36 B/param (W, buf, m, v, G in; W, buf, m, v out) + zero + 2 predictions
+    # = 48; RMSProp adds the squared average (44 + 12 = 56)
+    buf, sq = (torch.from_numpy(a).cuda() for a in wl.rule_state(n))
+    rule = xp.Rule(rule=xp.RULE_MOMENTUM_SGD, lr=1e-2, momentum=0.9, weight_decay=5e-4)
+    ms = timed(lambda: xp.xpipe_rule_flat(W, buf, None, m, v, G, rule, hp, 100, True, pf, 2, pb, 1), reps)
+    res["momentum_sgd_zero_grad_2pred"] = {"ms": ms, "GB_s": 48.0 * n / ms / 1e6}
+    rule = xp.Rule(rule=xp.RULE_RMSPROP, lr=1e-4, momentum=0.9, alpha=0.99, eps=1e-8)
+    ms = timed(lambda: xp.xpipe_rule_flat(W, buf, sq, m, v, G, rule, hp, 100, True, pf, 2, pb, 1), reps)
+    res["rmsprop_zero_grad_2pred"] = {"ms": ms, "GB_s": 56.0 * n / ms / 1e6}
+    del W, m, v, G, out, pf, pb, buf, sq
     torch.cuda.empty_cache()
     return res
 

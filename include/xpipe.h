@@ -191,6 +191,41 @@ xpipe_status xpipe_stage_bwd(xpipe_stage_t st, const void* x, const void* dy,
 xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t s_fwd_next,
                              int32_t s_bwd_next, int32_t emit_pred);
 
+/* Update rules of the paper's other settings, with the prediction still built
+ * from Adam moments (Sec. III-B): momentum SGD with weight decay (Sec. IV-B's
+ * experiments) and RMSProp with momentum (Sec. IV-D's robustness study).
+ * The gradient the rule steps on is g = grad + weight_decay * W; the Adam
+ * moments m, v (Eq. 4) advance by the same g in the same pass.
+ *   MOMENTUM_SGD: buf = momentum * buf + g;  W -= lr * buf
+ *   RMSPROP:      sq = alpha * sq + (1 - alpha) * g^2;
+ *                 buf = momentum * buf + g / (sqrt(sq) + eps);  W -= lr * buf
+ * (heavy-ball momentum without dampening; eps outside the root). */
+typedef enum { XPIPE_RULE_MOMENTUM_SGD = 1, XPIPE_RULE_RMSPROP = 2 } xpipe_rule;
+
+typedef struct {
+  int32_t rule;          /* xpipe_rule */
+  double lr;             /* the rule's step size */
+  double momentum;       /* in [0, 1) */
+  double weight_decay;   /* >= 0 */
+  double alpha;          /* RMSProp: decay of the squared-gradient average, in [0, 1) */
+  double eps;            /* RMSProp: > 0, added to the root */
+} xpipe_rule_hparams;
+
+/* The update at the mini-batch boundary with rule rp instead of Adam, then
+ * grad = 0.  buf (momentum buffer) and, for RMSProp, sq (squared-gradient
+ * average) are caller-owned fp32 device buffers of the stage's padded
+ * parameter count, zero before the first update and carried between calls
+ * (16-byte aligned; sq may be NULL for momentum SGD).  hp supplies the
+ * prediction: beta1, beta2 and eps of the Adam moments, the prediction's lr
+ * (the paper predicts with the rule's learning rate: pass the same value),
+ * the mode, and t = completed updates before this one.  With emit_pred != 0
+ * the same pass writes the next mini-batch's forward and backward predictions
+ * from the updated W and moments (update count hp->t + 1).  ESTATE when no
+ * backward ran since the last update. */
+xpipe_status xpipe_rule_step(xpipe_stage_t st, const xpipe_rule_hparams* rp, const xpipe_hparams* hp,
+                             float* buf, float* sq, int32_t s_fwd_next, int32_t s_bwd_next,
+                             int32_t emit_pred);
+
 xpipe_status xpipe_stage_destroy(xpipe_stage_t st);
 
 /* Flat-buffer forms of the two bandwidth-bound kernels, on n fp32 elements
@@ -205,6 +240,13 @@ xpipe_status xpipe_predict_flat(const float* W, const float* m, const float* v, 
                                 void* hip_stream);
 xpipe_status xpipe_adam_flat(float* W, float* m, float* v, float* G, int64_t n,
                              const xpipe_hparams* hp, int32_t zero_grad,
+                             float* pred_fwd, int32_t s_fwd, float* pred_bwd, int32_t s_bwd,
+                             void* hip_stream);
+/* xpipe_rule_flat: xpipe_rule_step's pass on flat buffers: W, buf, sq
+ * (RMSProp only; may be NULL otherwise), m, v updated in place from G; G
+ * zeroed when zero_grad != 0; predictions as in xpipe_adam_flat. */
+xpipe_status xpipe_rule_flat(float* W, float* buf, float* sq, float* m, float* v, float* G, int64_t n,
+                             const xpipe_rule_hparams* rp, const xpipe_hparams* hp, int32_t zero_grad,
                              float* pred_fwd, int32_t s_fwd, float* pred_bwd, int32_t s_bwd,
                              void* hip_stream);
 

@@ -8,8 +8,8 @@ missing the import of any entry point raises: there is no CPU fallback.
 Entry points (same names as the C ABI):
   xpipe_version_difference, xpipe_stage_query, Stage (xpipe_stage_create /
   _param_layout / _output_shape / xpipe_predict_weights / xpipe_stage_fwd /
-  xpipe_stage_bwd / xpipe_adam_step / xpipe_stage_destroy / timing),
-  xpipe_predict_flat, xpipe_adam_flat.
+  xpipe_stage_bwd / xpipe_adam_step / xpipe_rule_step / xpipe_stage_destroy /
+  timing / recorded passes), xpipe_predict_flat, xpipe_adam_flat, xpipe_rule_flat.
 """
 from __future__ import annotations
 
@@ -25,6 +25,7 @@ OK, EINVAL, ESTATE, EHIP, EUNSUPPORTED = 0, 1, 2, 3, 4
 F32, BF16 = 0, 1
 FWD, BWD = 0, 1
 PRED_EQ3, PRED_ADAMDIR, PRED_LITERAL = 0, 1, 2
+RULE_MOMENTUM_SGD, RULE_RMSPROP = 1, 2
 ROUND_HALF_UP, ROUND_HALF_EVEN, ROUND_HALF_DOWN = 0, 1, 2
 KINDS = {"linear": 0, "conv": 1, "bn": 2, "relu": 3, "add": 4, "maxpool2": 5, "avgpool3": 6,
          "gap": 7, "concat": 8, "softmax_ce": 9}
@@ -47,6 +48,25 @@ class LayerDesc(ctypes.Structure):
 class HParams(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_double), ("beta1", ctypes.c_double), ("beta2", ctypes.c_double),
                 ("eps", ctypes.c_double), ("t", ctypes.c_int64), ("mode", ctypes.c_int32)]
+
+
+class RuleParams(ctypes.Structure):
+    _fields_ = [("rule", ctypes.c_int32), ("lr", ctypes.c_double), ("momentum", ctypes.c_double),
+                ("weight_decay", ctypes.c_double), ("alpha", ctypes.c_double), ("eps", ctypes.c_double)]
+
+
+@dataclasses.dataclass
+class Rule:
+    """Update rule besides Adam (xpipe_rule_hparams)."""
+    rule: int = RULE_MOMENTUM_SGD
+    lr: float = 1e-2
+    momentum: float = 0.9
+    weight_decay: float = 0.0
+    alpha: float = 0.99
+    eps: float = 1e-8
+
+    def c(self) -> RuleParams:
+        return RuleParams(int(self.rule), self.lr, self.momentum, self.weight_decay, self.alpha, self.eps)
 
 
 @dataclasses.dataclass
@@ -78,6 +98,10 @@ _SIGS = {
     "xpipe_stage_fwd": [_P, _P, _P, _P, _P],
     "xpipe_stage_bwd": [_P, _P, _P, _P, _P],
     "xpipe_adam_step": [_P, ctypes.POINTER(HParams), _I32, _I32, _I32],
+    "xpipe_rule_step": [_P, ctypes.POINTER(RuleParams), ctypes.POINTER(HParams), _P, _P, _I32, _I32,
+                        _I32],
+    "xpipe_rule_flat": [_P, _P, _P, _P, _P, _P, _I64, ctypes.POINTER(RuleParams),
+                        ctypes.POINTER(HParams), _I32, _P, _I32, _P, _I32, _P],
     "xpipe_stage_destroy": [_P],
     "xpipe_predict_flat": [_P, _P, _P, _P, _P, _I64, _I32, ctypes.POINTER(HParams), _P],
     "xpipe_adam_flat": [_P, _P, _P, _P, _I64, ctypes.POINTER(HParams), _I32, _P, _I32, _P, _I32,
@@ -242,6 +266,14 @@ class Stage:
         _check(lib().xpipe_adam_step(self._h, ctypes.byref(c), s_fwd_next, s_bwd_next,
                                      int(emit_pred)))
 
+    def xpipe_rule_step(self, rule: Rule, hp: Hyper, t: int, buf, sq=None, s_fwd_next: int = 0,
+                        s_bwd_next: int = 0, emit_pred: bool = False):
+        """Update with momentum SGD or RMSProp; buf / sq are fp32 device tensors
+        of n_params elements carried between calls (zero before the first)."""
+        r, c = rule.c(), hp.c(t)
+        _check(lib().xpipe_rule_step(self._h, ctypes.byref(r), ctypes.byref(c), _ptr(buf), _ptr(sq),
+                                     s_fwd_next, s_bwd_next, int(emit_pred)))
+
     def set_timing(self, enable: bool):
         _check(lib().xpipe_stage_set_timing(self._h, int(enable)))
 
@@ -276,6 +308,14 @@ def xpipe_predict_flat(W, m, v, out, out_bf16, s: int, hp: Hyper, t: int, stream
     c = hp.c(t)
     _check(lib().xpipe_predict_flat(_ptr(W), _ptr(m), _ptr(v), _ptr(out), _ptr(out_bf16),
                                     W.numel(), s, ctypes.byref(c), _stream_ptr(stream)))
+
+
+def xpipe_rule_flat(W, buf, sq, m, v, G, rule: Rule, hp: Hyper, t: int, zero_grad=True, pred_fwd=None,
+                    s_fwd=0, pred_bwd=None, s_bwd=0, stream=None):
+    r, c = rule.c(), hp.c(t)
+    _check(lib().xpipe_rule_flat(_ptr(W), _ptr(buf), _ptr(sq), _ptr(m), _ptr(v), _ptr(G), W.numel(),
+                                 ctypes.byref(r), ctypes.byref(c), int(zero_grad), _ptr(pred_fwd), s_fwd,
+                                 _ptr(pred_bwd), s_bwd, _stream_ptr(stream)))
 
 
 def xpipe_probe_copy(src, dst, stream=None):

@@ -162,6 +162,103 @@ __global__ __launch_bounds__(256) void k_adam(float* __restrict__ W, float* __re
   }
 }
 
+// ---------------------------------------------------------------- momentum SGD / RMSProp
+// The update rules of the paper's other settings, each keeping the Adam
+// moments that the prediction reads, all advanced by the same gradient
+// g = G + wd * W.  Evaluated in fp64 in the order of the formulas (no fused
+// multiply-add), each stored value rounded once to fp32.
+struct RuleElem {
+  float w, b, q, m, v;  // weight, momentum buffer, squared average, moments
+};
+
+template <int RULE>
+XP_DEV RuleElem rule1(float w, float b, float q, float m, float v, float gr, const RuleCoef& c) {
+#pragma clang fp contract(off)
+  const double wd = (double)w;
+  const double g = (double)gr + c.wd * wd;
+  double qn = 0.0, bn;
+  if constexpr (RULE == RULE_MOMENTUM_SGD) {
+    bn = c.mu * (double)b + g;
+  } else {
+    qn = c.alpha * (double)q + (c.one_m_alpha * g) * g;
+    bn = c.mu * (double)b + g / (sqrt(qn) + c.eps);
+  }
+  const double wn = wd - c.lr * bn;
+  const double mn = c.beta1 * (double)m + c.one_m_beta1 * g;
+  const double vn = c.beta2 * (double)v + (c.one_m_beta2 * g) * g;
+  return RuleElem{(float)wn, (float)bn, (float)qn, (float)mn, (float)vn};
+}
+
+template <int RULE>
+__global__ __launch_bounds__(256) void k_rule(float* __restrict__ W, float* __restrict__ B,
+                                              float* __restrict__ Q, float* __restrict__ m,
+                                              float* __restrict__ v, float* __restrict__ G, int64_t n,
+                                              RuleCoef c, int zero_grad, float* __restrict__ pf,
+                                              bf16_t* __restrict__ pf_bf, PredCoef cf,
+                                              float* __restrict__ pb, bf16_t* __restrict__ pb_bf,
+                                              PredCoef cb) {
+  constexpr bool RMS = RULE == RULE_RMSPROP;
+  const int64_t nv = n >> 2;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  float4* W4 = reinterpret_cast<float4*>(W);
+  float4* B4 = reinterpret_cast<float4*>(B);
+  float4* Q4 = reinterpret_cast<float4*>(Q);
+  float4* m4 = reinterpret_cast<float4*>(m);
+  float4* v4 = reinterpret_cast<float4*>(v);
+  float4* G4 = reinterpret_cast<float4*>(G);
+  auto preds = [&](int64_t i, const RuleElem (&e)[4]) __attribute__((always_inline)) {
+    if (pf) {
+      float4 r = make_float4(predict1(e[0].w, e[0].m, e[0].v, cf), predict1(e[1].w, e[1].m, e[1].v, cf),
+                             predict1(e[2].w, e[2].m, e[2].v, cf), predict1(e[3].w, e[3].m, e[3].v, cf));
+      stnt(reinterpret_cast<float4*>(pf) + i, r);
+      if (pf_bf) stnt(reinterpret_cast<uint2*>(pf_bf) + i,
+                      make_uint2(f32x2_to_bf16x2(r.x, r.y), f32x2_to_bf16x2(r.z, r.w)));
+    }
+    if (pb) {
+      float4 r = make_float4(predict1(e[0].w, e[0].m, e[0].v, cb), predict1(e[1].w, e[1].m, e[1].v, cb),
+                             predict1(e[2].w, e[2].m, e[2].v, cb), predict1(e[3].w, e[3].m, e[3].v, cb));
+      stnt(reinterpret_cast<float4*>(pb) + i, r);
+      if (pb_bf) stnt(reinterpret_cast<uint2*>(pb_bf) + i,
+                      make_uint2(f32x2_to_bf16x2(r.x, r.y), f32x2_to_bf16x2(r.z, r.w)));
+    }
+  };
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nv; i += stride) {
+    const float4 w = ldnt(W4 + i), b = ldnt(B4 + i), mm = ldnt(m4 + i), vv = ldnt(v4 + i), g = ldnt(G4 + i);
+    const float4 q = RMS ? ldnt(Q4 + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    const RuleElem e[4] = {rule1<RULE>(w.x, b.x, q.x, mm.x, vv.x, g.x, c),
+                           rule1<RULE>(w.y, b.y, q.y, mm.y, vv.y, g.y, c),
+                           rule1<RULE>(w.z, b.z, q.z, mm.z, vv.z, g.z, c),
+                           rule1<RULE>(w.w, b.w, q.w, mm.w, vv.w, g.w, c)};
+    stnt(W4 + i, make_float4(e[0].w, e[1].w, e[2].w, e[3].w));
+    stnt(B4 + i, make_float4(e[0].b, e[1].b, e[2].b, e[3].b));
+    if (RMS) stnt(Q4 + i, make_float4(e[0].q, e[1].q, e[2].q, e[3].q));
+    stnt(m4 + i, make_float4(e[0].m, e[1].m, e[2].m, e[3].m));
+    stnt(v4 + i, make_float4(e[0].v, e[1].v, e[2].v, e[3].v));
+    if (zero_grad) stnt(G4 + i, make_float4(0.f, 0.f, 0.f, 0.f));
+    preds(i, e);
+  }
+  const int64_t t = (nv << 2) + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < n) {
+    const RuleElem e = rule1<RULE>(W[t], B[t], RMS ? Q[t] : 0.f, m[t], v[t], G[t], c);
+    W[t] = e.w;
+    B[t] = e.b;
+    if (RMS) Q[t] = e.q;
+    m[t] = e.m;
+    v[t] = e.v;
+    if (zero_grad) G[t] = 0.f;
+    if (pf) {
+      const float r = predict1(e.w, e.m, e.v, cf);
+      pf[t] = r;
+      if (pf_bf) pf_bf[t] = f32_to_bf16(r);
+    }
+    if (pb) {
+      const float r = predict1(e.w, e.m, e.v, cb);
+      pb[t] = r;
+      if (pb_bf) pb_bf[t] = f32_to_bf16(r);
+    }
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 static int stream_grid(int64_t n) {
   // one 16-byte vector per thread: every load of the pass is issued up front
@@ -190,6 +287,22 @@ hipError_t launch_adam(float* W, float* m, float* v, float* G, int64_t n, const 
                               (pf_bf ? 2 : 0) + (pb_bf ? 2 : 0));
   XP_LAUNCH("k_adam", bytes, k_adam, dim3(stream_grid(n)), dim3(256), 0, s, W, m, v, G, n, a, zero_grad,
             pf, pf_bf, cf, pb, pb_bf, cb);
+  return hipGetLastError();
+}
+
+hipError_t launch_rule(int rule, float* W, float* B, float* Q, float* m, float* v, float* G, int64_t n,
+                       const RuleCoef& c, int zero_grad, float* pf, bf16_t* pf_bf, const PredCoef& cf,
+                       float* pb, bf16_t* pb_bf, const PredCoef& cb, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const bool rms = rule == RULE_RMSPROP;
+  double bytes = (double)n * ((rms ? 44 : 36) + (zero_grad ? 4 : 0) + (pf ? 4 : 0) + (pb ? 4 : 0) +
+                              (pf_bf ? 2 : 0) + (pb_bf ? 2 : 0));
+  if (rms)
+    XP_LAUNCH("k_rule<rmsprop>", bytes, k_rule<RULE_RMSPROP>, dim3(stream_grid(n)), dim3(256), 0, s, W, B, Q,
+              m, v, G, n, c, zero_grad, pf, pf_bf, cf, pb, pb_bf, cb);
+  else
+    XP_LAUNCH("k_rule<momentum_sgd>", bytes, k_rule<RULE_MOMENTUM_SGD>, dim3(stream_grid(n)), dim3(256), 0, s,
+              W, B, Q, m, v, G, n, c, zero_grad, pf, pf_bf, cf, pb, pb_bf, cb);
   return hipGetLastError();
 }
 

@@ -1386,6 +1386,32 @@ AdamCoef adam_coef(const xpipe_hparams* hp) {
   return a;
 }
 
+xpipe_status check_rule(const xpipe_rule_hparams* rp) {
+  if (!rp) return fail(XPIPE_EINVAL, "null rule hparams");
+  if (rp->rule != XPIPE_RULE_MOMENTUM_SGD && rp->rule != XPIPE_RULE_RMSPROP)
+    return fail(XPIPE_EINVAL, "unknown update rule");
+  if (!(rp->lr >= 0) || !(rp->momentum >= 0 && rp->momentum < 1) || !(rp->weight_decay >= 0))
+    return fail(XPIPE_EINVAL, "bad rule hparams");
+  if (rp->rule == XPIPE_RULE_RMSPROP && (!(rp->alpha >= 0 && rp->alpha < 1) || !(rp->eps > 0)))
+    return fail(XPIPE_EINVAL, "bad RMSProp hparams");
+  return XPIPE_OK;
+}
+
+RuleCoef rule_coef(const xpipe_rule_hparams* rp, const xpipe_hparams* hp) {
+  RuleCoef c{};
+  c.lr = rp->lr;
+  c.mu = rp->momentum;
+  c.wd = rp->weight_decay;
+  c.alpha = rp->alpha;
+  c.one_m_alpha = 1.0 - rp->alpha;
+  c.eps = rp->eps;
+  c.beta1 = hp->beta1;
+  c.beta2 = hp->beta2;
+  c.one_m_beta1 = 1.0 - hp->beta1;
+  c.one_m_beta2 = 1.0 - hp->beta2;
+  return c;
+}
+
 // the merged GEMMs' weights, gathered from the prediction of direction dir
 xpipe_status refresh_gathered(xpipe_stage* st, int dir) {
   for (const Op& op : st->ops) {
@@ -1741,6 +1767,40 @@ xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t 
   return refresh_flipped(st);
 }
 
+xpipe_status xpipe_rule_step(xpipe_stage_t st, const xpipe_rule_hparams* rp, const xpipe_hparams* hp,
+                             float* buf, float* sq, int32_t s_fwd_next, int32_t s_bwd_next,
+                             int32_t emit_pred) {
+  if (!st) return fail(XPIPE_EINVAL, "null stage");
+  xpipe_status hs = check_hp(hp);
+  if (hs != XPIPE_OK) return hs;
+  hs = check_rule(rp);
+  if (hs != XPIPE_OK) return hs;
+  if (emit_pred && (s_fwd_next < 0 || s_bwd_next < 0)) return fail(XPIPE_EINVAL, "version difference must be >= 0");
+  if (!buf || (rp->rule == XPIPE_RULE_RMSPROP && !sq)) return fail(XPIPE_EINVAL, "null optimizer buffer");
+  if (!aligned16(buf) || (sq && !aligned16(sq))) return fail(XPIPE_EINVAL, "buffers must be 16-byte aligned");
+  if (st->bwd_since_step == 0) return fail(XPIPE_ESTATE, "no backward since the last update");
+  HookScope hs_(st);
+  PredCoef cf = pred_coef(hp, hp->t + 1, s_fwd_next);
+  PredCoef cb = pred_coef(hp, hp->t + 1, s_bwd_next);
+  bf16_t* ff = nullptr;
+  bf16_t* fb = nullptr;
+  if (emit_pred && st->dtype == DT_BF16) {
+    ff = (bf16_t*)(st->ws + st->bf_f_off);
+    fb = (bf16_t*)(st->ws + st->bf_b_off);
+  }
+  XP_HIP(launch_rule(rp->rule, st->W, buf, sq, st->m, st->v, st->grad, st->P, rule_coef(rp, hp), 1,
+                     emit_pred ? st->wpf : nullptr, ff, cf, emit_pred ? st->wpb : nullptr, fb, cb, st->stream));
+  st->bwd_since_step = 0;
+  st->pred_valid[0] = st->pred_valid[1] = emit_pred != 0;
+  st->wd_valid = false;
+  if (!emit_pred) return XPIPE_OK;
+  for (int d = 0; d < 2; ++d) {
+    xpipe_status r = refresh_gathered(st, d);
+    if (r != XPIPE_OK) return r;
+  }
+  return refresh_flipped(st);
+}
+
 xpipe_status xpipe_stage_destroy(xpipe_stage_t st) {
   if (!st) return fail(XPIPE_EINVAL, "null stage");
   // auxiliary lanes finish their work before their streams go away
@@ -1785,6 +1845,27 @@ xpipe_status xpipe_adam_flat(float* W, float* m, float* v, float* G, int64_t n, 
     return fail(XPIPE_EINVAL, "buffers must be 16-byte aligned");
   XP_HIP(launch_adam(W, m, v, G, n, adam_coef(hp), zero_grad, pred_fwd, nullptr, pred_coef(hp, hp->t + 1, s_fwd),
                      pred_bwd, nullptr, pred_coef(hp, hp->t + 1, s_bwd), (hipStream_t)hip_stream));
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_rule_flat(float* W, float* buf, float* sq, float* m, float* v, float* G, int64_t n,
+                             const xpipe_rule_hparams* rp, const xpipe_hparams* hp, int32_t zero_grad,
+                             float* pred_fwd, int32_t s_fwd, float* pred_bwd, int32_t s_bwd,
+                             void* hip_stream) {
+  if (n < 0) return fail(XPIPE_EINVAL, "negative length");
+  xpipe_status hs = check_hp(hp);
+  if (hs != XPIPE_OK) return hs;
+  hs = check_rule(rp);
+  if (hs != XPIPE_OK) return hs;
+  if ((pred_fwd && s_fwd < 0) || (pred_bwd && s_bwd < 0)) return fail(XPIPE_EINVAL, "version difference must be >= 0");
+  if (n == 0) return XPIPE_OK;
+  if (!W || !buf || !m || !v || !G || (rp->rule == XPIPE_RULE_RMSPROP && !sq)) return fail(XPIPE_EINVAL, "null buffer");
+  if (!aligned16(W) || !aligned16(buf) || (sq && !aligned16(sq)) || !aligned16(m) || !aligned16(v) ||
+      !aligned16(G) || (pred_fwd && !aligned16(pred_fwd)) || (pred_bwd && !aligned16(pred_bwd)))
+    return fail(XPIPE_EINVAL, "buffers must be 16-byte aligned");
+  XP_HIP(launch_rule(rp->rule, W, buf, sq, m, v, G, n, rule_coef(rp, hp), zero_grad, pred_fwd, nullptr,
+                     pred_coef(hp, hp->t + 1, s_fwd), pred_bwd, nullptr, pred_coef(hp, hp->t + 1, s_bwd),
+                     (hipStream_t)hip_stream));
   return XPIPE_OK;
 }
 

@@ -44,8 +44,20 @@ struct AdamCoef {
   double eps;
 };
 
+// update rules besides Adam (the prediction keeps reading Adam moments)
+constexpr int RULE_MOMENTUM_SGD = 1;
+constexpr int RULE_RMSPROP = 2;
+struct RuleCoef {
+  double lr, mu, wd;                        // step size, momentum, weight decay
+  double alpha, one_m_alpha, eps;           // RMSProp squared average and its eps
+  double beta1, beta2, one_m_beta1, one_m_beta2;  // the prediction's Adam moments
+};
+
 hipError_t launch_predict(const float* W, const float* m, const float* v, float* out,
                           bf16_t* out_bf, int64_t n, const PredCoef& c, hipStream_t s);
+hipError_t launch_rule(int rule, float* W, float* B, float* Q, float* m, float* v, float* G, int64_t n,
+                       const RuleCoef& c, int zero_grad, float* pf, bf16_t* pf_bf, const PredCoef& cf,
+                       float* pb, bf16_t* pb_bf, const PredCoef& cb, hipStream_t s);
 hipError_t launch_adam(float* W, float* m, float* v, float* G, int64_t n, const AdamCoef& a,
                        int zero_grad, float* pf, bf16_t* pf_bf, const PredCoef& cf, float* pb,
                        bf16_t* pb_bf, const PredCoef& cb, hipStream_t s);

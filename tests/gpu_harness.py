@@ -23,11 +23,12 @@ class GpuRecord:
 
 
 def run_stage(w, inp, dtype, hp, s_fwd, s_bwd, minibatches=None, fused=True, need_dx=True,
-              stage=None, reuse_inputs=False):
+              stage=None, reuse_inputs=False, rule=None):
     """Mini-batch loop of the XPipe stage step on the GPU.  With fused=True the
     Adam step also emits the next mini-batch's predictions (no separate
     predict calls after the first mini-batch).  reuse_inputs feeds mini-batch
-    0's buffers to every mini-batch (same pointers on every call)."""
+    0's buffers to every mini-batch (same pointers on every call).  rule (an
+    xp.Rule) updates with momentum SGD / RMSProp instead of Adam."""
     import torch
     J = len(inp.xs) if minibatches is None else minibatches
     st = stage or xp.Stage(w.layers, w.micro_batch, w.T, w.in_shape, dtype)
@@ -44,6 +45,8 @@ def run_stage(w, inp, dtype, hp, s_fwd, s_bwd, minibatches=None, fused=True, nee
     loss = torch.zeros(1, dtype=torch.float32, device="cuda")
     dx = torch.empty((w.micro_batch,) + tuple(w.in_shape), dtype=tdt, device="cuda") if need_dx else None
     out_shape_oracle = (n, C) if (H == 1 and W_ == 1 and len(w.in_shape) == 1) or w.has_loss else (n, H, W_, C)
+    buf = torch.zeros(st.P, dtype=torch.float32, device="cuda") if rule is not None else None
+    sq = torch.zeros(st.P, dtype=torch.float32, device="cuda") if rule is not None else None
     recs = []
     t = 0
     for jj in range(J):
@@ -65,7 +68,10 @@ def run_stage(w, inp, dtype, hp, s_fwd, s_bwd, minibatches=None, fused=True, nee
                                None if labels is None else labels[j][i], dx)
             r.dxs.append(to_host(dx).reshape(inp.xs[0][0].shape) if need_dx else None)
         r.grad = st.get_tensors(st.grad)
-        st.xpipe_adam_step(hp, t, s_fwd, s_bwd, emit_pred=fused)
+        if rule is None:
+            st.xpipe_adam_step(hp, t, s_fwd, s_bwd, emit_pred=fused)
+        else:
+            st.xpipe_rule_step(rule, hp, t, buf, sq, s_fwd, s_bwd, emit_pred=fused)
         t += 1
         r.W = st.get_tensors(st.W)
         r.m = st.get_tensors(st.m)

@@ -141,3 +141,57 @@ def test_full_size_sweep_sampled():
     _assert_rounded(_host(m[ti]), mn, "m")
     _assert_rounded(_host(v[ti]), vn, "v")
     assert float(G.abs().max()) == 0.0
+
+
+# ------------------------------------------------------------------ momentum SGD / RMSProp
+RULES = [(xp.RULE_MOMENTUM_SGD, dict(lr=1e-2, momentum=0.9, weight_decay=5e-4)),
+         (xp.RULE_RMSPROP, dict(lr=1e-4, momentum=0.9, weight_decay=5e-4, alpha=0.99, eps=1e-8))]
+
+
+@pytest.mark.parametrize("n", [5, 4096, 1000003])
+@pytest.mark.parametrize("rule,kw", RULES)
+def test_rule_flat_fused_matches_oracle(n, rule, kw):
+    """Momentum SGD / RMSProp with the prediction's Adam moments, fused with
+    zeroing the gradient and the next two predictions."""
+    import torch
+    st = wl.flat_state(n, seed=13)
+    b0, q0 = wl.rule_state(n)
+    r = xp.Rule(rule=rule, **kw)
+    hp = xp.Hyper(lr=r.lr)
+    for t in (0, 7):
+        W, m, v, G = _dev(st.W), _dev(st.m), _dev(st.v), _dev(st.G)
+        buf, sq = _dev(b0), _dev(q0)
+        pf, pb = torch.empty_like(W), torch.empty_like(W)
+        xp.xpipe_rule_flat(W, buf, sq if rule == xp.RULE_RMSPROP else None, m, v, G, r, hp, t, True,
+                           pf, 2, pb, 1)
+        torch.cuda.synchronize()
+        if rule == xp.RULE_MOMENTUM_SGD:
+            Wn, bn, mn, vn = oracle.momentum_sgd_update(st.W, b0, st.m, st.v, st.G, r.lr, r.momentum,
+                                                        r.weight_decay, hp.beta1, hp.beta2)
+        else:
+            Wn, bn, qn, mn, vn = oracle.rmsprop_update(st.W, b0, q0, st.m, st.v, st.G, r.lr, r.alpha,
+                                                       r.eps, r.momentum, r.weight_decay, hp.beta1,
+                                                       hp.beta2)
+            _assert_rounded(_host(sq), qn, "sq")
+        _assert_rounded(_host(W), Wn, "W")
+        _assert_rounded(_host(buf), bn, "buf")
+        _assert_rounded(_host(m), mn, "m")
+        _assert_rounded(_host(v), vn, "v")
+        assert not _host(G).any()
+        W32, m32, v32 = (a.astype(np.float32) for a in (Wn, mn, vn))
+        for out, s in ((pf, 2), (pb, 1)):
+            want = oracle.predict(W32, m32, v32, t + 1, s, hp.lr, hp.beta1, hp.beta2, hp.eps)
+            _assert_rounded(_host(out), want, f"pred s={s}")
+
+
+def test_rule_flat_rejects_bad_arguments():
+    import torch
+    W = torch.zeros(8, device="cuda")
+    with pytest.raises(xp.XPipeError) as e:      # RMSProp needs its squared average
+        xp.xpipe_rule_flat(W, W.clone(), None, W.clone(), W.clone(), W.clone(),
+                           xp.Rule(rule=xp.RULE_RMSPROP), xp.Hyper(), 0)
+    assert e.value.status == xp.EINVAL
+    with pytest.raises(xp.XPipeError) as e:      # momentum must be below 1
+        xp.xpipe_rule_flat(W, W.clone(), None, W.clone(), W.clone(), W.clone(),
+                           xp.Rule(momentum=1.0), xp.Hyper(), 0)
+    assert e.value.status == xp.EINVAL

@@ -70,6 +70,27 @@ def test_stage_step_fp32_matches_oracle(name):
     _compare(gpu, ref, TOL[xp.F32], f"{name}/f32")
 
 
+@pytest.mark.parametrize("name", ["tiny_mlp", "vgg16_stage0", "inception_v3_stage"])
+@pytest.mark.parametrize("rule", [xp.RULE_MOMENTUM_SGD, xp.RULE_RMSPROP])
+def test_stage_step_other_rules_fp32_match_oracle(name, rule):
+    """The paper's other update rules (momentum SGD with weight decay, Sec.
+    IV-B; RMSProp with momentum, Sec. IV-D) with Adam-moment prediction from
+    the paper's moment initialisation: fp32 storage, every tensor within 2e-4
+    of the oracle."""
+    w = CASES[name]()
+    inp = wl.stage_inputs(w, act_dtype="f32", moment_init="paper")
+    if rule == xp.RULE_MOMENTUM_SGD:
+        r = xp.Rule(rule=rule, lr=1e-2, momentum=0.9, weight_decay=5e-4)
+        ohp = oracle.Hyper(lr=r.lr, rule=oracle.RULE_MOMENTUM_SGD, momentum=0.9, weight_decay=5e-4)
+    else:
+        r = xp.Rule(rule=rule, lr=1e-4, momentum=0.9, alpha=0.99, eps=1e-8)
+        ohp = oracle.Hyper(lr=r.lr, rule=oracle.RULE_RMSPROP, momentum=0.9, alpha=0.99, rms_eps=1e-8)
+    gpu, _ = run_stage(w, inp, xp.F32, xp.Hyper(lr=r.lr), w.s_fwd, w.s_bwd, rule=r)
+    ref = oracle.train_stage(oracle.Stage(w.layers, "f32"), inp.params, inp.m, inp.v, inp.xs,
+                             w.s_fwd, w.s_bwd, ohp, labels=inp.labels, dys=inp.dys)
+    _compare(gpu, ref, TOL[xp.F32], f"{name}/f32/rule{rule}")
+
+
 def _all_errs(recs, ref):
     e = {}
     for j, (g, r) in enumerate(zip(recs, ref)):

@@ -346,3 +346,13 @@ def flat_state(n: int, seed: int = PAPER_SEED + 1) -> FlatState:
     v = rng.standard_normal(n, dtype=np.float32); np.abs(v, out=v); v *= np.float32(1e-6)
     G = rng.standard_normal(n, dtype=np.float32); G *= np.float32(1e-3)
     return FlatState(W, m, v, G)
+
+
+def rule_state(n: int, seed: int = PAPER_SEED + 6):
+    """Optimizer buffers of the momentum-SGD / RMSProp rules, continuing a run:
+    momentum buffer ~N(0,1e-3), squared-gradient average |N(0,1e-6)| (standard
+    deviations), drawn in that order.  Returns (buf, sq) fp32."""
+    rng = np.random.default_rng(seed)
+    buf = rng.standard_normal(n, dtype=np.float32); buf *= np.float32(1e-3)
+    sq = rng.standard_normal(n, dtype=np.float32); np.abs(sq, out=sq); sq *= np.float32(1e-6)
+    return buf, sq

@@ -186,8 +186,11 @@ xpipe_status xpipe_stage_bwd(xpipe_stage_t st, const void* x, const void* dy,
  * outside the root), then grad = 0.  With emit_pred != 0 the same pass also
  * writes the next mini-batch's forward and backward predictions (version
  * differences s_fwd_next, s_bwd_next, moments after hp->t + 1 updates), so
- * the next mini-batch needs no xpipe_predict_weights.  ESTATE when no
- * backward ran since the last update. */
+ * the next mini-batch needs no xpipe_predict_weights.  With
+ * emit_pred = XPIPE_KEEP_PRED the cached predictions stay valid (an interleaved
+ * schedule reuses a mini-batch's prediction across an update); with 0 they
+ * become invalid.  ESTATE when no backward ran since the last update. */
+#define XPIPE_KEEP_PRED 2
 xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t s_fwd_next,
                              int32_t s_bwd_next, int32_t emit_pred);
 
@@ -227,6 +230,65 @@ xpipe_status xpipe_rule_step(xpipe_stage_t st, const xpipe_rule_hparams* rp, con
                              int32_t emit_pred);
 
 xpipe_status xpipe_stage_destroy(xpipe_stage_t st);
+
+/* ---------------------------------------------------------------- schedule
+ * The pipeline schedule of Sec. III-A (Fig. 1) as a unit-time model, host
+ * only: on a `size`-GPU pipeline, GPU `rank` runs the forward pass of
+ * micro-batch i (1-based) at unit 2i + rank and its backward at
+ * 2i + 2 size - 1 - rank, which gives the warm-up, the one-forward-one-
+ * backward steady phase and the drain, and reproduces the orders the text
+ * walks through.  The weights are updated after the backward pass of every
+ * T-th micro-batch.  For a bellwether (the first micro-batch of a mini-batch,
+ * Sec. III-B) the event carries Eq. 1 / Eq. 2's version difference and the
+ * counted one: the updates on this GPU after the pass, up to the unit in which
+ * the mini-batch's T-th micro-batch completes its backward pass on GPU 0
+ * (s_incl; s_excl leaves out the mini-batch's own update). */
+typedef struct {
+  int32_t time;          /* pipeline unit */
+  int32_t kind;          /* XPIPE_FWD or XPIPE_BWD */
+  int32_t micro;         /* micro-batch index, 1-based */
+  int32_t mini;          /* mini-batch index, 1-based */
+  int32_t bellwether;    /* 1 for the first micro-batch of its mini-batch */
+  int32_t update_after;  /* 1 if the weights are updated right after this backward */
+  int32_t version;       /* updates applied on this GPU before the pass */
+  int32_t s_eq;          /* bellwether: Eq. 1 (forward) or Eq. 2 (backward) */
+  int32_t s_excl, s_incl;/* bellwether: counted version differences */
+} xpipe_sched_event;
+
+/* Events of GPU `rank` for `minibatches` mini-batches of T micro-batches, in
+ * time order: *count = 2 T minibatches.  With out = NULL only the count is
+ * returned; otherwise capacity must hold them.  rounding / ceil_half_rank as
+ * in xpipe_version_difference.  No device work. */
+xpipe_status xpipe_schedule(int32_t size, int32_t T, int32_t rank, int32_t minibatches, int32_t rounding,
+                            int32_t ceil_half_rank, xpipe_sched_event* out, int32_t capacity,
+                            int32_t* count);
+
+/* Host arrays (n_micro entries, indexed by micro-batch - 1) of device
+ * pointers for xpipe_stage_run. */
+typedef struct {
+  int32_t n_micro;
+  const void* const* x;           /* stage inputs (required) */
+  const void* const* dy;          /* upstream gradients; NULL for a loss stage */
+  const int32_t* const* labels;   /* NULL unless the stage ends in SOFTMAX_CE */
+  void* const* y;                 /* forward outputs (required) */
+  float* loss;                    /* device array [n_micro] of per-micro-batch losses, or NULL */
+  void* const* dx;                /* input gradients, or NULL */
+} xpipe_run_io;
+
+/* Runs a schedule's events on one stage in order, as GPU `rank` would: a
+ * bellwether's forward (backward) pass first predicts with its s_eq and caches
+ * the result (xpipe_predict_weights), the other micro-batches of the mini-batch
+ * reuse the cache even after an update in between (Sec. III-B), and the
+ * update (Adam, or rule when not NULL, with buf / sq as in xpipe_rule_step)
+ * follows every event with update_after, keeping both caches.  hp->t counts
+ * the updates before the run; hp's lr is the prediction's.  draft != 0 takes
+ * the variant of the draft text instead: a forward micro-batch that finds its
+ * mini-batch's cached prediction older than the latest update predicts again
+ * from the current weights with the bellwether's s reduced by the updates since
+ * (at least 0), and the later ones reuse that. */
+xpipe_status xpipe_stage_run(xpipe_stage_t st, const xpipe_sched_event* events, int32_t n_events,
+                             const xpipe_run_io* io, const xpipe_hparams* hp,
+                             const xpipe_rule_hparams* rule, float* buf, float* sq, int32_t draft);
 
 /* Flat-buffer forms of the two bandwidth-bound kernels, on n fp32 elements
  * (any n >= 0; no alignment needed beyond 4 bytes, 16 bytes is faster).

@@ -10,18 +10,22 @@ Contents:
   method  Eq. 1 / Eq. 2 version difference, Eq. 3 / Eq. 4 prediction, Adam update,
           momentum-SGD and RMSProp updates that keep the prediction's Adam moments
   layers  layer forwards and VJPs (conv, linear, BN, ReLU, pools, GAP, CE)
-  stage   a stage's forward, backward-with-recompute and the mini-batch driver
+  stage   a stage's forward, backward-with-recompute, the mini-batch driver and
+          the driver of one GPU's part of the interleaved schedule
+  schedule  the pipeline schedule as a unit-time model, with staleness counts
 """
 from .method import (HALF_DOWN, HALF_EVEN, HALF_UP, PRED_ADAMDIR, PRED_EQ3, PRED_LITERAL,
                      RULE_ADAM, RULE_MOMENTUM_SGD, RULE_RMSPROP, adam_moments, adam_update,
                      momentum_sgd_update, predict, rmsprop_update, version_difference_bwd,
                      version_difference_fwd)
-from .stage import Hyper, MinibatchRecord, Stage, train_stage
+from .stage import Hyper, MinibatchRecord, ScheduleRecord, Stage, train_schedule, train_stage
+from . import schedule
 
 __all__ = [
     "HALF_DOWN", "HALF_EVEN", "HALF_UP", "PRED_ADAMDIR", "PRED_EQ3", "PRED_LITERAL",
     "RULE_ADAM", "RULE_MOMENTUM_SGD", "RULE_RMSPROP", "adam_moments", "adam_update",
     "momentum_sgd_update", "predict", "rmsprop_update", "version_difference_bwd",
     "version_difference_fwd",
-    "Hyper", "MinibatchRecord", "Stage", "train_stage",
+    "Hyper", "MinibatchRecord", "ScheduleRecord", "Stage", "train_schedule", "train_stage",
+    "schedule",
 ]

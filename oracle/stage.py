@@ -300,3 +300,86 @@ def train_stage(stage: Stage, params, m, v, xs, s_fwd: int, s_bwd: int, hp: Hype
                                    None if hp.rule == RULE_ADAM else list(buf),
                                    list(sq) if hp.rule == RULE_RMSPROP else None))
     return out
+
+
+@dataclasses.dataclass
+class ScheduleRecord:
+    ys: List[np.ndarray]                 # forward output per micro-batch (index micro - 1)
+    losses: List[Optional[float]]
+    dxs: List[Optional[np.ndarray]]
+    predictions: List[tuple]             # (kind, micro, s, t) of every prediction made
+    W: List[np.ndarray]                  # after the last update
+    m: List[np.ndarray]
+    v: List[np.ndarray]
+
+
+def train_schedule(stage: Stage, params, m, v, xs, events, hp: Hyper, labels=None, dys=None,
+                   need_dx=True, t0: int = 0, draft: bool = False) -> ScheduleRecord:
+    """One GPU's part of the interleaved schedule (oracle.schedule events) on
+    one stage.  xs[k] / labels[k] / dys[k] belong to micro-batch k + 1; the
+    mini-batch size N = T * micro-batch follows from the events.
+
+    A bellwether predicts for its pass and caches the result (Eq. 3 with its
+    event's s); the mini-batch's other micro-batches reuse the cache even when
+    an update happened in between (Sec. III-B, final text).  draft=True takes
+    the draft text's variant for the forward pass: a micro-batch that finds
+    the cached prediction older than the latest update predicts again from the
+    current weights with s reduced by the updates since the bellwether."""
+    qs = stage.qs
+    W = [qs(np.asarray(p, np.float64)) for p in params]
+    m = [qs(np.asarray(a, np.float64)) for a in m]
+    v = [qs(np.asarray(a, np.float64)) for a in v]
+    buf = [np.zeros_like(a) for a in W]
+    sq = [np.zeros_like(a) for a in W]
+    n_micro = max(e.micro for e in events) if events else 0
+    T = next((e.micro for e in events if e.update_after), n_micro)
+    N = T * xs[0].shape[0]
+    t = t0
+    G = [np.zeros_like(a) for a in W]
+    Wf = Wb = None
+    bell_t = cache_t = -1
+    bell_s = 0
+    ys, losses, dxs = [None] * n_micro, [None] * n_micro, [None] * n_micro
+    preds = []
+
+    def pred(s):
+        return [qs(predict(W[k], m[k], v[k], t, s, hp.lr, hp.beta1, hp.beta2, hp.eps, hp.mode))
+                for k in range(len(W))]
+
+    for e in events:
+        k = e.micro - 1
+        lab = None if labels is None else labels[k]
+        if e.kind == 0:
+            if e.bellwether:
+                Wf, bell_s, bell_t, cache_t = pred(e.s_eq), e.s_eq, t, t
+                preds.append((0, e.micro, e.s_eq, t))
+            elif draft and cache_t != t:
+                s = max(bell_s - (t - bell_t), 0)
+                Wf, cache_t = pred(s), t
+                preds.append((0, e.micro, s, t))
+            ys[k], losses[k], _ = stage.forward(Wf, xs[k], lab, N)
+        else:
+            if e.bellwether:
+                Wb = pred(e.s_eq)
+                preds.append((1, e.micro, e.s_eq, t))
+            dx, gs, _ = stage.backward(Wb, xs[k], None if dys is None else dys[k], lab, N, need_dx)
+            dxs[k] = dx
+            for q in range(len(G)):
+                G[q] = qs(G[q] + gs[q])
+            if e.update_after:
+                t += 1
+                if hp.rule == RULE_ADAM:
+                    new = [adam_update(W[q], m[q], v[q], G[q], t, hp.lr, hp.beta1, hp.beta2, hp.eps)
+                           for q in range(len(W))]
+                    W, m, v = ([qs(a[i]) for a in new] for i in range(3))
+                elif hp.rule == RULE_MOMENTUM_SGD:
+                    new = [momentum_sgd_update(W[q], buf[q], m[q], v[q], G[q], hp.lr, hp.momentum,
+                                               hp.weight_decay, hp.beta1, hp.beta2) for q in range(len(W))]
+                    W, buf, m, v = ([qs(a[i]) for a in new] for i in range(4))
+                else:
+                    new = [rmsprop_update(W[q], buf[q], sq[q], m[q], v[q], G[q], hp.lr, hp.alpha,
+                                          hp.rms_eps, hp.momentum, hp.weight_decay, hp.beta1, hp.beta2)
+                           for q in range(len(W))]
+                    W, buf, sq, m, v = ([qs(a[i]) for a in new] for i in range(5))
+                G = [np.zeros_like(a) for a in W]
+    return ScheduleRecord(ys, losses, dxs, preds, W, m, v)

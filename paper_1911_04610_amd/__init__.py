@@ -9,7 +9,8 @@ Entry points (same names as the C ABI):
   xpipe_version_difference, xpipe_stage_query, Stage (xpipe_stage_create /
   _param_layout / _output_shape / xpipe_predict_weights / xpipe_stage_fwd /
   xpipe_stage_bwd / xpipe_adam_step / xpipe_rule_step / xpipe_stage_destroy /
-  timing / recorded passes), xpipe_predict_flat, xpipe_adam_flat, xpipe_rule_flat.
+  timing / recorded passes / xpipe_stage_run), xpipe_schedule, xpipe_predict_flat,
+  xpipe_adam_flat, xpipe_rule_flat.
 """
 from __future__ import annotations
 
@@ -24,6 +25,7 @@ LIB_PATH = os.path.join(HERE, "libxpipe.so")
 OK, EINVAL, ESTATE, EHIP, EUNSUPPORTED = 0, 1, 2, 3, 4
 F32, BF16 = 0, 1
 FWD, BWD = 0, 1
+KEEP_PRED = 2
 PRED_EQ3, PRED_ADAMDIR, PRED_LITERAL = 0, 1, 2
 RULE_MOMENTUM_SGD, RULE_RMSPROP = 1, 2
 ROUND_HALF_UP, ROUND_HALF_EVEN, ROUND_HALF_DOWN = 0, 1, 2
@@ -48,6 +50,17 @@ class LayerDesc(ctypes.Structure):
 class HParams(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_double), ("beta1", ctypes.c_double), ("beta2", ctypes.c_double),
                 ("eps", ctypes.c_double), ("t", ctypes.c_int64), ("mode", ctypes.c_int32)]
+
+
+class SchedEvent(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("time", "kind", "micro", "mini", "bellwether",
+                                             "update_after", "version", "s_eq", "s_excl", "s_incl")]
+
+
+class RunIO(ctypes.Structure):
+    _fields_ = [("n_micro", ctypes.c_int32), ("x", ctypes.c_void_p), ("dy", ctypes.c_void_p),
+                ("labels", ctypes.c_void_p), ("y", ctypes.c_void_p), ("loss", ctypes.c_void_p),
+                ("dx", ctypes.c_void_p)]
 
 
 class RuleParams(ctypes.Structure):
@@ -98,6 +111,8 @@ _SIGS = {
     "xpipe_stage_fwd": [_P, _P, _P, _P, _P],
     "xpipe_stage_bwd": [_P, _P, _P, _P, _P],
     "xpipe_adam_step": [_P, ctypes.POINTER(HParams), _I32, _I32, _I32],
+    "xpipe_schedule": [_I32, _I32, _I32, _I32, _I32, _I32, _P, _I32, ctypes.POINTER(_I32)],
+    "xpipe_stage_run": [_P, _P, _I32, ctypes.POINTER(RunIO), ctypes.POINTER(HParams), _P, _P, _P, _I32],
     "xpipe_rule_step": [_P, ctypes.POINTER(RuleParams), ctypes.POINTER(HParams), _P, _P, _I32, _I32,
                         _I32],
     "xpipe_rule_flat": [_P, _P, _P, _P, _P, _P, _I64, ctypes.POINTER(RuleParams),
@@ -274,6 +289,25 @@ class Stage:
         _check(lib().xpipe_rule_step(self._h, ctypes.byref(r), ctypes.byref(c), _ptr(buf), _ptr(sq),
                                      s_fwd_next, s_bwd_next, int(emit_pred)))
 
+    def xpipe_stage_run(self, events, x, y, hp: Hyper, t: int, dy=None, labels=None, loss=None,
+                        dx=None, rule: Optional[Rule] = None, buf=None, sq=None, draft=False):
+        """Run schedule events (from xpipe_schedule) on this stage.  x, y, dy,
+        labels, dx: lists of device tensors indexed by micro-batch - 1; loss: a
+        device fp32 tensor [n_micro] or None."""
+        n = len(x)
+        arr = lambda ts: None if ts is None else (ctypes.c_void_p * n)(*[_ptr(a) for a in ts])
+        keep = [arr(x), arr(dy), arr(labels), arr(y), arr(dx)]
+        io = RunIO(n, *(ctypes.cast(a, ctypes.c_void_p) if a is not None else None for a in keep[:3]),
+                   ctypes.cast(keep[3], ctypes.c_void_p), _ptr(loss),
+                   ctypes.cast(keep[4], ctypes.c_void_p) if keep[4] is not None else None)
+        ev = (SchedEvent * len(events))(*events)
+        c = hp.c(t)
+        r = rule.c() if rule is not None else None
+        _check(lib().xpipe_stage_run(self._h, ctypes.cast(ev, ctypes.c_void_p), len(events),
+                                     ctypes.byref(io), ctypes.byref(c),
+                                     ctypes.cast(ctypes.pointer(r), ctypes.c_void_p) if r is not None else None,
+                                     _ptr(buf), _ptr(sq), int(draft)))
+
     def set_timing(self, enable: bool):
         _check(lib().xpipe_stage_set_timing(self._h, int(enable)))
 
@@ -308,6 +342,18 @@ def xpipe_predict_flat(W, m, v, out, out_bf16, s: int, hp: Hyper, t: int, stream
     c = hp.c(t)
     _check(lib().xpipe_predict_flat(_ptr(W), _ptr(m), _ptr(v), _ptr(out), _ptr(out_bf16),
                                     W.numel(), s, ctypes.byref(c), _stream_ptr(stream)))
+
+
+def xpipe_schedule(size: int, T: int, rank: int, minibatches: int, rounding: int = 0,
+                   ceil_half_rank: bool = False) -> List[SchedEvent]:
+    """Events of GPU `rank` in the unit-time pipeline schedule (host only)."""
+    n = _I32(0)
+    _check(lib().xpipe_schedule(size, T, rank, minibatches, rounding, int(ceil_half_rank), None, 0,
+                                ctypes.byref(n)))
+    ev = (SchedEvent * max(n.value, 1))()
+    _check(lib().xpipe_schedule(size, T, rank, minibatches, rounding, int(ceil_half_rank),
+                                ctypes.cast(ev, ctypes.c_void_p), n.value, ctypes.byref(n)))
+    return list(ev)[:n.value]
 
 
 def xpipe_rule_flat(W, buf, sq, m, v, G, rule: Rule, hp: Hyper, t: int, zero_grad=True, pred_fwd=None,

@@ -1740,6 +1740,8 @@ xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t 
   if (!st) return fail(XPIPE_EINVAL, "null stage");
   xpipe_status hs = check_hp(hp);
   if (hs != XPIPE_OK) return hs;
+  const bool keep = emit_pred == XPIPE_KEEP_PRED;
+  if (keep) emit_pred = 0;
   if (emit_pred && (s_fwd_next < 0 || s_bwd_next < 0)) return fail(XPIPE_EINVAL, "version difference must be >= 0");
   if (st->bwd_since_step == 0) return fail(XPIPE_ESTATE, "no backward since the last update");
   HookScope hs_(st);
@@ -1757,6 +1759,7 @@ xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t 
                        emit_pred ? st->wpb : nullptr, fb, cb, st->stream));
   }
   st->bwd_since_step = 0;
+  if (keep) return XPIPE_OK;  // the cached predictions (and what derives from them) stay
   st->pred_valid[0] = st->pred_valid[1] = emit_pred != 0;
   st->wd_valid = false;
   if (!emit_pred) return XPIPE_OK;
@@ -1775,6 +1778,8 @@ xpipe_status xpipe_rule_step(xpipe_stage_t st, const xpipe_rule_hparams* rp, con
   if (hs != XPIPE_OK) return hs;
   hs = check_rule(rp);
   if (hs != XPIPE_OK) return hs;
+  const bool keep = emit_pred == XPIPE_KEEP_PRED;
+  if (keep) emit_pred = 0;
   if (emit_pred && (s_fwd_next < 0 || s_bwd_next < 0)) return fail(XPIPE_EINVAL, "version difference must be >= 0");
   if (!buf || (rp->rule == XPIPE_RULE_RMSPROP && !sq)) return fail(XPIPE_EINVAL, "null optimizer buffer");
   if (!aligned16(buf) || (sq && !aligned16(sq))) return fail(XPIPE_EINVAL, "buffers must be 16-byte aligned");
@@ -1791,6 +1796,7 @@ xpipe_status xpipe_rule_step(xpipe_stage_t st, const xpipe_rule_hparams* rp, con
   XP_HIP(launch_rule(rp->rule, st->W, buf, sq, st->m, st->v, st->grad, st->P, rule_coef(rp, hp), 1,
                      emit_pred ? st->wpf : nullptr, ff, cf, emit_pred ? st->wpb : nullptr, fb, cb, st->stream));
   st->bwd_since_step = 0;
+  if (keep) return XPIPE_OK;
   st->pred_valid[0] = st->pred_valid[1] = emit_pred != 0;
   st->wd_valid = false;
   if (!emit_pred) return XPIPE_OK;
@@ -1940,3 +1946,121 @@ xpipe_status xpipe_stage_timing_entry(xpipe_stage_t st, int32_t i, const char** 
 }
 
 }  // extern "C"
+
+// ============================================================================
+// Pipeline schedule (unit-time model, Sec. III-A) and the interleaved executor
+// ============================================================================
+xpipe_status xpipe_schedule(int32_t size, int32_t T, int32_t rank, int32_t minibatches, int32_t rounding,
+                            int32_t ceil_half_rank, xpipe_sched_event* out, int32_t capacity,
+                            int32_t* count) {
+  if (!count) return fail(XPIPE_EINVAL, "null output");
+  if (size < 1 || T < 1 || rank < 0 || rank >= size || minibatches < 0)
+    return fail(XPIPE_EINVAL, "need size >= 1, T >= 1, 0 <= rank < size, minibatches >= 0");
+  if ((int64_t)T * minibatches > (1 << 28)) return fail(XPIPE_EINVAL, "schedule too long");
+  const int32_t n = T * minibatches;
+  *count = 2 * n;
+  if (!out) return XPIPE_OK;
+  if (capacity < 2 * n) return fail(XPIPE_EINVAL, "capacity below the event count");
+  int32_t s_fwd = 0, s_bwd = 0;
+  xpipe_status st = xpipe_version_difference(size, T, rank, XPIPE_FWD, rounding, ceil_half_rank, &s_fwd);
+  if (st != XPIPE_OK) return st;
+  st = xpipe_version_difference(size, T, rank, XPIPE_BWD, rounding, ceil_half_rank, &s_bwd);
+  if (st != XPIPE_OK) return st;
+  const int64_t K = size;
+  auto fwd_time = [&](int64_t i) { return 2 * i + rank; };
+  auto bwd_time = [&](int64_t i, int64_t r) { return 2 * i + 2 * K - 1 - r; };
+  // forward and backward units have opposite parity, so the two ascending
+  // sequences merge without ties; the updates are the backward units of the
+  // T-th micro-batches, in ascending order
+  int64_t f = 1, b = 1, updates_before = 0;
+  for (int32_t q = 0; q < 2 * n; ++q) {
+    const bool take_f = f <= n && (b > n || fwd_time(f) < bwd_time(b, rank));
+    const int64_t i = take_f ? f++ : b++;
+    const int64_t time = take_f ? fwd_time(i) : bwd_time(i, rank);
+    // updates strictly before this unit
+    while (updates_before < minibatches && bwd_time(T * (updates_before + 1), rank) < time) ++updates_before;
+    xpipe_sched_event e{};
+    e.time = (int32_t)time;
+    e.kind = take_f ? XPIPE_FWD : XPIPE_BWD;
+    e.micro = (int32_t)i;
+    e.mini = (int32_t)((i - 1) / T + 1);
+    e.bellwether = (i - 1) % T == 0;
+    e.update_after = !take_f && i % T == 0;
+    e.version = (int32_t)updates_before;
+    if (e.bellwether) {
+      e.s_eq = take_f ? s_fwd : s_bwd;
+      const int64_t end = bwd_time((int64_t)T * e.mini, 0);     // round trip ends on GPU 0
+      const int64_t own = bwd_time((int64_t)T * e.mini, rank);  // this mini-batch's update here
+      int32_t incl = 0, excl = 0;
+      for (int64_t j = 1; j <= minibatches; ++j) {
+        const int64_t u = bwd_time(T * j, rank);
+        if (u > time && u <= end) {
+          ++incl;
+          if (u != own) ++excl;
+        }
+      }
+      e.s_incl = incl;
+      e.s_excl = excl;
+    }
+    out[q] = e;
+  }
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_run(xpipe_stage_t st, const xpipe_sched_event* events, int32_t n_events,
+                             const xpipe_run_io* io, const xpipe_hparams* hp,
+                             const xpipe_rule_hparams* rule, float* buf, float* sq, int32_t draft) {
+  if (!st) return fail(XPIPE_EINVAL, "null stage");
+  if (n_events < 0 || (n_events > 0 && !events)) return fail(XPIPE_EINVAL, "bad event list");
+  if (!io || !io->x || !io->y || io->n_micro < 0) return fail(XPIPE_EINVAL, "inputs and outputs required");
+  xpipe_status s = check_hp(hp);
+  if (s != XPIPE_OK) return s;
+  if (rule) {
+    s = check_rule(rule);
+    if (s != XPIPE_OK) return s;
+  }
+  if (st->has_loss && !io->labels) return fail(XPIPE_EINVAL, "labels required for a loss stage");
+  if (!st->has_loss && !io->dy) return fail(XPIPE_EINVAL, "dy required for a stage without a loss");
+  // every event is checked before the first launch
+  for (int32_t q = 0; q < n_events; ++q) {
+    const xpipe_sched_event& e = events[q];
+    if (e.micro < 1 || e.micro > io->n_micro || (e.kind != XPIPE_FWD && e.kind != XPIPE_BWD) ||
+        (e.bellwether && e.s_eq < 0))
+      return fail(XPIPE_EINVAL, "event " + std::to_string(q) + " out of range");
+  }
+  xpipe_hparams h = *hp;
+  int64_t bell_t = -1, cache_t = -1;  // update counts at the forward bellwether / cached forward prediction
+  int32_t bell_s = 0;
+  for (int32_t q = 0; q < n_events; ++q) {
+    const xpipe_sched_event& e = events[q];
+    const int32_t k = e.micro - 1;
+    if (e.kind == XPIPE_FWD) {
+      if (e.bellwether) {
+        s = xpipe_predict_weights(st, XPIPE_FWD, e.s_eq, &h);
+        bell_s = e.s_eq;
+        bell_t = cache_t = h.t;
+      } else if (draft && bell_t >= 0 && cache_t != h.t) {
+        const int64_t left = (int64_t)bell_s - (h.t - bell_t);
+        s = xpipe_predict_weights(st, XPIPE_FWD, (int32_t)(left > 0 ? left : 0), &h);
+        cache_t = h.t;
+      }
+      if (s != XPIPE_OK) return s;
+      s = xpipe_stage_fwd(st, io->x[k], io->y[k], io->labels ? io->labels[k] : nullptr,
+                          io->loss ? io->loss + k : nullptr);
+    } else {
+      if (e.bellwether) {
+        s = xpipe_predict_weights(st, XPIPE_BWD, e.s_eq, &h);
+        if (s != XPIPE_OK) return s;
+      }
+      s = xpipe_stage_bwd(st, io->x[k], io->dy ? io->dy[k] : nullptr, io->labels ? io->labels[k] : nullptr,
+                          io->dx ? io->dx[k] : nullptr);
+      if (s == XPIPE_OK && e.update_after) {
+        s = rule ? xpipe_rule_step(st, rule, &h, buf, sq, 0, 0, XPIPE_KEEP_PRED)
+                 : xpipe_adam_step(st, &h, 0, 0, XPIPE_KEEP_PRED);
+        ++h.t;
+      }
+    }
+    if (s != XPIPE_OK) return s;
+  }
+  return XPIPE_OK;
+}

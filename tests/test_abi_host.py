@@ -130,3 +130,28 @@ def test_flat_entry_points_check_arguments_on_the_host():
     # misaligned buffers are refused before any launch
     assert L.xpipe_predict_flat(20, 16, 16, 16, None, 8, 1, ctypes.byref(hp), None) == xp.EINVAL
     assert L.xpipe_adam_flat(None, None, None, None, 0, ctypes.byref(hp), 1, None, 0, None, 0, None) == xp.OK
+
+
+@pytest.mark.parametrize("rounding", [0, 2])
+def test_schedule_matches_oracle(rounding):
+    """The library's host schedule simulator gives the oracle's events."""
+    rule = {0: oracle.HALF_UP, 2: oracle.HALF_DOWN}[rounding]
+    fields = ("time", "kind", "micro", "mini", "bellwether", "update_after", "version", "s_eq",
+              "s_excl", "s_incl")
+    for K in (1, 2, 3, 4, 8):
+        for T in (1, 2, 3, 4):
+            for r in range(K):
+                got = xp.xpipe_schedule(K, T, r, 5, rounding)
+                want = oracle.schedule.schedule(K, T, r, 5, rule)
+                assert len(got) == len(want)
+                for g, w in zip(got, want):
+                    assert tuple(int(getattr(g, f)) for f in fields) == \
+                        tuple(int(getattr(w, f)) for f in fields), (K, T, r)
+
+
+def test_schedule_rejects_bad_arguments():
+    for args in ((0, 1, 0, 2), (4, 0, 0, 2), (4, 2, 4, 2), (4, 2, -1, 2), (4, 2, 0, -1)):
+        with pytest.raises(xp.XPipeError) as e:
+            xp.xpipe_schedule(*args)
+        assert e.value.status == xp.EINVAL
+    assert xp.xpipe_schedule(4, 2, 0, 0) == []

@@ -1,0 +1,106 @@
+"""One GPU's part of the interleaved pipeline schedule on the GPU library
+(xpipe_schedule + xpipe_stage_run, through the C ABI) against the oracle's
+driver of the same events: bellwether predictions cached across updates,
+updates after every T-th backward, optionally the draft text's re-prediction.
+fp32 storage: every output and the final state within 2e-4."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1911_04610_amd as xp
+import workloads as wl
+from conftest import rel_l2
+from gpu_harness import to_device, to_host
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-4
+
+
+def _small(name):
+    if name == "tiny_mlp":
+        return wl.shrink(wl.tiny_mlp(), minibatches=3)
+    if name == "vgg16_stage0":
+        return wl.shrink(wl.vgg_stage(), micro_batch=2, spatial=(12, 12), T=2, minibatches=3)
+    return wl.shrink(wl.inception_stage(), micro_batch=2, T=2, minibatches=3,
+                     layers=wl.inception_stage_layers(modules=1, classes=10), spatial=(9, 9))
+
+
+CASES = [  # (workload, size, rank, rule, draft)
+    ("tiny_mlp", 4, 0, None, False),
+    ("tiny_mlp", 4, 2, None, False),
+    ("tiny_mlp", 4, 2, None, True),
+    ("tiny_mlp", 4, 3, xp.RULE_MOMENTUM_SGD, False),
+    ("vgg16_stage0", 4, 0, xp.RULE_MOMENTUM_SGD, True),
+    ("inception_v3_stage", 4, 1, None, False),
+]
+
+
+@pytest.mark.parametrize("name,size,rank,rule,draft", CASES)
+def test_interleaved_schedule_matches_oracle(name, size, rank, rule, draft):
+    import torch
+    w = _small(name)
+    inp = wl.stage_inputs(w, act_dtype="f32", moment_init="paper")
+    J, T = len(inp.xs), len(inp.xs[0])
+    events = xp.xpipe_schedule(size, T, rank, J)
+    oev = oracle.schedule.schedule(size, T, rank, J)
+    flat = lambda rows: None if rows is None else [a for row in rows for a in row]
+    xs, labels, dys = flat(inp.xs), flat(inp.labels), flat(inp.dys)
+    if rule == xp.RULE_MOMENTUM_SGD:
+        r = xp.Rule(rule=rule, lr=1e-2, momentum=0.9, weight_decay=5e-4)
+        ohp = oracle.Hyper(lr=r.lr, rule=oracle.RULE_MOMENTUM_SGD, momentum=0.9, weight_decay=5e-4)
+    else:
+        r, ohp = None, oracle.Hyper()
+    hp = xp.Hyper(lr=ohp.lr)
+    need_dx = w.rank > 0 if name != "tiny_mlp" else True
+
+    st = xp.Stage(w.layers, w.micro_batch, T, w.in_shape, xp.F32)
+    st.set_flat(st.W, inp.params)
+    st.set_flat(st.m, inp.m)
+    st.set_flat(st.v, inp.v)
+    n, H, W_, C = st.out_shape
+    xd = [to_device(x, xp.F32) for x in xs]
+    yd = [torch.empty((n, H, W_, C), dtype=torch.float32, device="cuda") for _ in xs]
+    dxd = [torch.empty_like(x) for x in xd] if need_dx else None
+    lab = None if labels is None else [torch.from_numpy(l).cuda() for l in labels]
+    dyd = None if dys is None else [to_device(d, xp.F32) for d in dys]
+    loss = torch.zeros(len(xs), dtype=torch.float32, device="cuda") if w.has_loss else None
+    buf = torch.zeros(st.P, dtype=torch.float32, device="cuda")
+    st.xpipe_stage_run(events, xd, yd, hp, 0, dy=dyd, labels=lab, loss=loss, dx=dxd, rule=r,
+                       buf=buf, draft=draft)
+    torch.cuda.synchronize()
+
+    ref = oracle.train_schedule(oracle.Stage(w.layers, "f32"), inp.params, inp.m, inp.v, xs, oev, ohp,
+                                labels=labels, dys=dys, need_dx=need_dx, draft=draft)
+    errs = {}
+    oshape = lambda a: a.reshape(ref.ys[0].shape)
+    for k in range(len(xs)):
+        errs[f"y{k + 1}"] = rel_l2(oshape(to_host(yd[k])), ref.ys[k])
+        if need_dx:
+            errs[f"dx{k + 1}"] = rel_l2(to_host(dxd[k]).reshape(ref.dxs[k].shape), ref.dxs[k])
+        if loss is not None:
+            errs[f"loss{k + 1}"] = abs(float(loss[k]) - ref.losses[k]) / abs(ref.losses[k])
+    for field in ("W", "m", "v"):
+        got = st.get_tensors(getattr(st, field))
+        for q, (a, b) in enumerate(zip(got, getattr(ref, field))):
+            errs[f"{field}[{q}]"] = rel_l2(a, b)
+    worst = max(errs, key=errs.get)
+    print(f"{name} size {size} rank {rank} rule {rule} draft {draft}: worst {worst} = {errs[worst]:.2e}"
+          f", {len(ref.predictions)} predictions")
+    bad = {k: v for k, v in errs.items() if not v <= TOL}
+    assert not bad, bad
+    if draft and name == "tiny_mlp":
+        # the update between bellwether 5 and micro-batch 6 forces a re-prediction
+        assert any(p[0] == 0 and p[1] == 6 for p in ref.predictions)
+
+
+def test_run_rejects_events_out_of_range():
+    import torch
+    w = wl.tiny_mlp()
+    st = xp.Stage(w.layers, w.micro_batch, w.T, w.in_shape, xp.F32)
+    ev = xp.xpipe_schedule(2, 4, 0, 2)
+    x = [torch.zeros((w.micro_batch,) + tuple(w.in_shape), device="cuda") for _ in range(4)]  # 8 needed
+    y = [torch.zeros((w.micro_batch, 10), device="cuda") for _ in range(4)]
+    lab = [torch.zeros(w.micro_batch, dtype=torch.int32, device="cuda") for _ in range(4)]
+    with pytest.raises(xp.XPipeError) as e:
+        st.xpipe_stage_run(ev, x, y, xp.Hyper(), 0, labels=lab)
+    assert e.value.status == xp.EINVAL

@@ -203,6 +203,52 @@ def time_stage(args, timing_pass=True, graphs=True):
     return w, ms, wall, classes, fin
 
 
+def time_interleaved(args, minibatches=6):
+    """One GPU's part of the interleaved pipeline schedule (xpipe_schedule +
+    xpipe_stage_run) on the same stage: the workload's rank of its pipeline,
+    each micro-batch its own input buffer, bellwether predictions cached across
+    updates.  Returns samples/s over the run (after one untimed run that also
+    records the passes)."""
+    import torch
+    import paper_1911_04610_amd as xp
+    import workloads as wl
+    w = wl.WORKLOADS[args.workload]()
+    dt = xp.BF16 if args.dtype == "bf16" else xp.F32
+    tdt = torch.bfloat16 if dt == xp.BF16 else torch.float32
+    inp = wl.stage_inputs(w, act_dtype=args.dtype if args.dtype == "bf16" else "f32", moment_init="paper")
+    st = xp.Stage(w.layers, w.micro_batch, w.T, w.in_shape, dt)
+    st.set_flat(st.W, inp.params)
+    st.set_flat(st.m, inp.m)
+    st.set_flat(st.v, inp.v)
+    J = len(inp.xs)
+    n = w.T * minibatches
+    dev = lambda a: torch.from_numpy(a).cuda().to(tdt)
+    xs = [dev(inp.xs[(k // w.T) % J][k % w.T]) for k in range(n)]
+    labels = None if inp.labels is None else [torch.from_numpy(inp.labels[(k // w.T) % J][k % w.T]).cuda()
+                                              for k in range(n)]
+    dys = None if inp.dys is None else [dev(inp.dys[(k // w.T) % J][k % w.T]) for k in range(n)]
+    nb, H, W_, C = st.out_shape
+    ys = [torch.empty((nb, H, W_, C), dtype=tdt, device="cuda") for _ in range(n)]
+    dxs = [torch.empty_like(x) for x in xs] if w.rank > 0 else None
+    loss = torch.zeros(n, dtype=torch.float32, device="cuda") if w.has_loss else None
+    events = xp.xpipe_schedule(w.size, w.T, w.rank, minibatches)
+    hp = xp.Hyper()
+    run = lambda t: st.xpipe_stage_run(events, xs, ys, hp, t, dy=dys, labels=labels, loss=loss, dx=dxs)
+    run(0)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    run(minibatches)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    return {"size": w.size, "rank": w.rank, "T": w.T, "minibatches": minibatches,
+            "samples_per_s": round(n * w.micro_batch / (ms / 1e3), 2),
+            "ms_per_minibatch": round(ms / minibatches, 4),
+            "note": "interleaved one-forward-one-backward order of this rank; a prediction per "
+                    "bellwether and direction, updates kept separate from predictions"}
+
+
 def event_offset_us(reps=300):
     """Per-launch offset of a start/stop event pair around one kernel: the
     bracketed time of a ~10 us kernel minus its period when launched back to
@@ -429,6 +475,8 @@ def main():
                                             "frac_hbm": round(v["GB_s"] / HBM_PEAK_GBS, 4),
                                             "frac_measured_copy": round(v["GB_s"] / pk["hbm_copy_GB_s"], 4)}
                                         for k, v in sw.items()}}
+    if not args.no_sweep:
+        out["interleaved_schedule"] = time_interleaved(args)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.dtype)
     print(json.dumps(out))

@@ -100,7 +100,8 @@ XP_DEV int xcd_tile(int l, int G) {
 }
 
 template <typename T, int BM, int BN, int WM, int WN, bool FLAT, int KS, int PF>
-__global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
+__global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
+  constexpr int NT = WM * WN * 64;  // threads: one wave64 per wave tile
   using MTT = MT<T>;
   constexpr int VEC = MTT::VEC;
   constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
@@ -114,8 +115,8 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   constexpr int PITCH = BK + (sizeof(T) == 2 ? XP_GEMM_LDS_PAD_BF16 : 4);
   constexpr int CPR = BK / VEC;  // chunks per tile row per step
   constexpr int A_CH = BM * CPR, B_CH = BN * CPR;
-  constexpr int A_PER = (A_CH + 255) / 256, B_PER = (B_CH + 255) / 256;
-  static_assert(WM * WN == 4, "four waves");
+  constexpr int A_PER = (A_CH + NT - 1) / NT, B_PER = (B_CH + NT - 1) / NT;
+  static_assert(WM * WN >= 1 && WM * WN <= 8, "one to eight waves");
   static_assert(TM >= 1 && TN >= 1, "wave tile");
   // bf16: the epilogue stages the fp32 result tile in the same LDS, rows
   // padded so that the accumulator layouts write it without bank conflicts
@@ -143,7 +144,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   bool a_slot[A_PER], a_valid[A_PER];
 #pragma unroll
   for (int i = 0; i < A_PER; ++i) {
-    int q = tid + i * 256;
+    int q = tid + i * NT;
     a_slot[i] = q < A_CH;
     a_row[i] = q / CPR;
     a_kc[i] = q % CPR;
@@ -159,7 +160,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   bool b_slot[B_PER], b_valid[B_PER];
 #pragma unroll
   for (int i = 0; i < B_PER; ++i) {
-    int q = tid + i * 256;
+    int q = tid + i * NT;
     b_slot[i] = q < B_CH;
     b_row[i] = q / CPR;
     b_kc[i] = q % CPR;
@@ -274,10 +275,10 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   int a_lds[A_PER], b_lds[B_PER];
 #pragma unroll
   for (int i = 0; i < A_PER; ++i)
-    a_lds[i] = a_slot[i] ? a_row[i] * PITCH + a_kc[i] * VEC : ((tid + i * 256 - A_CH) % BM) * PITCH + BK;
+    a_lds[i] = a_slot[i] ? a_row[i] * PITCH + a_kc[i] * VEC : ((tid + i * NT - A_CH) % BM) * PITCH + BK;
 #pragma unroll
   for (int i = 0; i < B_PER; ++i)
-    b_lds[i] = b_slot[i] ? b_row[i] * PITCH + b_kc[i] * VEC : ((tid + i * 256 - B_CH) % BN) * PITCH + BK;
+    b_lds[i] = b_slot[i] ? b_row[i] * PITCH + b_kc[i] * VEC : ((tid + i * NT - B_CH) % BN) * PITCH + BK;
   auto lstore = [&](auto SLOT, int buf) __attribute__((always_inline)) {
     constexpr int slot = decltype(SLOT)::value;
 #pragma unroll
@@ -437,17 +438,17 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     // take 16-byte accesses, a ragged last chunk (N not a multiple of 8) or
     // unaligned views an element loop
     typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-    constexpr int NCH = (BM * CPRN + 255) / 256;  // chunks per thread
+    constexpr int NCH = (BM * CPRN + NT - 1) / NT;  // chunks per thread
     int c_ne[NCH];
     u32x4_t c_mask[NCH], c_old[NCH];
     f32x4_t c_b0[NCH], c_b1[NCH];
     const bool vb = a.bias && (reinterpret_cast<uintptr_t>(a.bias + n0) % 16) == 0;
 #pragma unroll
     for (int k = 0; k < NCH; ++k) {
-      const int c = k * 256 + tid;
+      const int c = k * NT + tid;
       const int row = c / CPRN, cc = c - row * CPRN;
       const int m = m0 + row, nb = n0 + cc * 8;
-      const bool live = ((BM * CPRN) % 256 == 0 || c < BM * CPRN) && m < M && nb < a.N;
+      const bool live = ((BM * CPRN) % NT == 0 || c < BM * CPRN) && m < M && nb < a.N;
       const int ne = live ? (a.N - nb < 8 ? a.N - nb : 8) : 0;  // valid columns in this chunk
       c_ne[k] = ne;
       c_mask[k] = c_old[k] = (u32x4_t){0u, 0u, 0u, 0u};
@@ -476,8 +477,8 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     }
 #pragma unroll
     for (int k = 0; k < NCH; ++k) {
-      const int c = k * 256 + tid;
-      if ((BM * CPRN) % 256 != 0 && c >= BM * CPRN) break;
+      const int c = k * NT + tid;
+      if ((BM * CPRN) % NT != 0 && c >= BM * CPRN) break;
       const int row = c / CPRN, cc = c - row * CPRN;
       const int ne = c_ne[k];
       float* o = &ot[row * OPITCH + cc * 8];
@@ -544,7 +545,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     if (a.stat_part) {
       // column sums of the stored values: RS row ranges per column, then a
       // fixed-order sum of the ranges
-      constexpr int RS = 256 / BN > 0 ? 256 / BN : 1;
+      constexpr int RS = NT / BN > 0 ? NT / BN : 1;
       constexpr int RROWS = BM / RS;
       static_assert(BM % RS == 0 && RROWS % 4 == 0, "row ranges");
       __shared__ double sred[RS][2][BN];
@@ -564,7 +565,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
         sred[part][1][col] = (s1[0] + s1[1]) + (s1[2] + s1[3]);
       }
       __syncthreads();
-      for (int col = tid; col < BN; col += 256) {
+      for (int col = tid; col < BN; col += NT) {
         const int n = n0 + col;
         if (n >= a.N) continue;
         double s0 = 0.0, s1 = 0.0;
@@ -640,7 +641,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
         }
       }
       __syncthreads();
-      for (int col = tid; col < BN; col += 256) {
+      for (int col = tid; col < BN; col += NT) {
         int n = n0 + col;
         if (n >= a.N) continue;
         double s0 = 0.0, s1 = 0.0;
@@ -1290,10 +1291,10 @@ static hipError_t conv_go(const ConvArgs& a, bool flat, hipStream_t s, int* grid
   double flops = 2.0 * M * (double)a.N * a.R * a.S * a.C;
   if (flat)
     XP_LAUNCH((kname<T, BM, BN, WM, WN, true, KS, PF>("k_conv_gemm")), flops,
-              (k_conv_gemm<T, BM, BN, WM, WN, true, KS, PF>), grid, dim3(256), 0, s, a);
+              (k_conv_gemm<T, BM, BN, WM, WN, true, KS, PF>), grid, dim3(WM * WN * 64), 0, s, a);
   else
     XP_LAUNCH((kname<T, BM, BN, WM, WN, false, KS, PF>("k_conv_gemm")), flops,
-              (k_conv_gemm<T, BM, BN, WM, WN, false, KS, PF>), grid, dim3(256), 0, s, a);
+              (k_conv_gemm<T, BM, BN, WM, WN, false, KS, PF>), grid, dim3(WM * WN * 64), 0, s, a);
   return hipGetLastError();
 }
 

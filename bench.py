@@ -249,6 +249,72 @@ def time_interleaved(args, minibatches=6):
                     "bellwether and direction, updates kept separate from predictions"}
 
 
+def time_partitioned(args, stages=4, steps=10, warmup=3):
+    """VGG-16 for 32x32 inputs split into `stages` stages by the paper's
+    partition rule (xpipe_partition), each stage trained on its own as its GPU
+    would (micro-batch 32, T = 4, bf16: T forwards, T backwards with
+    recomputation, Adam fused with the next predictions).  Reports each
+    stage's step time and the pipeline's steady-state throughput bound, the
+    slowest stage's (synthetic inputs and upstream gradients of each stage's
+    shapes)."""
+    import numpy as np
+    import torch
+    import paper_1911_04610_amd as xp
+    import workloads as wl
+    layers = wl.vgg16_layers()
+    first = xp.xpipe_partition(layers, stages)
+    parts = wl.split_layers(layers, first)
+    mb, T = 32, 4
+    rng = np.random.default_rng(wl.PAPER_SEED + 7)
+    in_shape = (32, 32, 3)
+    res = []
+    hp = xp.Hyper()
+    for k, p in enumerate(parts):
+        st = xp.Stage(p, mb, T, in_shape, xp.BF16)
+        st.set_flat(st.W, wl.init_params(p, rng))
+        n, H, W_, C = st.out_shape
+        last = k == len(parts) - 1
+        x = torch.from_numpy(rng.standard_normal((mb,) + in_shape).astype(np.float32)).cuda().to(torch.bfloat16)
+        y = torch.empty((n, H, W_, C), dtype=torch.bfloat16, device="cuda")
+        dy = None if last else torch.from_numpy(
+            (1e-2 * rng.standard_normal((n, H, W_, C))).astype(np.float32)).cuda().to(torch.bfloat16)
+        lab = torch.from_numpy(rng.integers(0, 10, mb).astype(np.int32)).cuda() if last else None
+        loss = torch.zeros(1, dtype=torch.float32, device="cuda") if last else None
+        dx = torch.empty_like(x) if k > 0 else None
+        st.xpipe_predict_weights(xp.FWD, 1, hp, 0)
+        st.xpipe_predict_weights(xp.BWD, 1, hp, 0)
+        state = {"t": 0}
+
+        def step():
+            for _ in range(T):
+                st.xpipe_stage_fwd(x, y, lab, loss)
+            for _ in range(T):
+                st.xpipe_stage_bwd(x, dy, lab, dx)
+            st.xpipe_adam_step(hp, state["t"], 1, 1, emit_pred=True)
+            state["t"] += 1
+
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            step()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        res.append({"layers": [first[k], first[k + 1]], "in_shape": list(in_shape),
+                    "params": int(st.P), "ms_per_step": round(ms, 4)})
+        in_shape = (H, W_, C)
+        del st
+    slow = max(r["ms_per_step"] for r in res)
+    return {"model": "vgg16 (32x32 inputs, 13 conv + linear)", "stages": stages, "micro_batch": mb, "T": T,
+            "dtype": "bf16", "per_stage": res,
+            "pipeline_samples_per_s_bound": round(mb * T / (slow / 1e3), 1),
+            "note": "each stage timed alone on this GPU as its pipeline GPU would run it; the "
+                    "pipeline's steady-state rate is bounded by its slowest stage"}
+
+
 def event_offset_us(reps=300):
     """Per-launch offset of a start/stop event pair around one kernel: the
     bracketed time of a ~10 us kernel minus its period when launched back to
@@ -477,6 +543,7 @@ def main():
                                         for k, v in sw.items()}}
     if not args.no_sweep:
         out["interleaved_schedule"] = time_interleaved(args)
+        out["vgg16_partitioned"] = time_partitioned(args)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.dtype)
     print(json.dumps(out))

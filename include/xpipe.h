@@ -231,6 +231,20 @@ xpipe_status xpipe_rule_step(xpipe_stage_t st, const xpipe_rule_hparams* rp, con
 
 xpipe_status xpipe_stage_destroy(xpipe_stage_t st);
 
+/* ---------------------------------------------------------------- partition
+ * The paper's model partition (Sec. IV-A): the layers are split across the
+ * GPUs into consecutive stages with roughly equal numbers of layers, the later
+ * GPUs taking slightly more.  Counted here are the layers with weights (LINEAR,
+ * CONV): with L of them over K stages, stage k gets L / K and the last L % K
+ * stages one more; a stage starts at its first weighted layer (activations,
+ * pools, normalisations and joins stay with the stage of the layer they follow).
+ * first[k] = index of stage k's first layer (first[0] = 0, first[K] = n;
+ * K + 1 entries).  Layer inputs are re-indexed by the caller: the previous
+ * stage's last layer becomes the stage input (-1).  EUNSUPPORTED when a layer
+ * reads a tensor of an earlier stage other than that one (a branch or skip
+ * connection cut by a boundary); EINVAL when K exceeds L.  Host only. */
+xpipe_status xpipe_partition(const xpipe_layer_desc* layers, int32_t n_layers, int32_t stages, int32_t* first);
+
 /* ---------------------------------------------------------------- schedule
  * The pipeline schedule of Sec. III-A (Fig. 1) as a unit-time model, host
  * only: on a `size`-GPU pipeline, GPU `rank` runs the forward pass of

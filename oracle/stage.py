@@ -39,6 +39,15 @@ from .method import (adam_update, momentum_sgd_update, predict, rmsprop_update, 
                      RULE_ADAM, RULE_MOMENTUM_SGD, RULE_RMSPROP)
 
 
+def _rows(a):
+    """A [n, 1, 1, C] activation (an NHWC map of one pixel, e.g. after the last
+    pooling) as the [n, C] rows a linear layer reads; [n, C] stays."""
+    if a.ndim == 4:
+        assert a.shape[1] == 1 and a.shape[2] == 1, "linear input must have H = W = 1"
+        return a.reshape(a.shape[0], a.shape[3])
+    return a
+
+
 def _round_f32(a):
     """Round to the nearest fp32 value, as fp64."""
     return np.asarray(a, np.float64).astype(np.float32).astype(np.float64)
@@ -109,7 +118,7 @@ class Stage:
                 outs[i] = self.q(ly.conv2d(a, self.qw(P[pi[0]]), b))
             elif k == "linear":
                 b = P[pi[1]] if L["bias"] else None
-                outs[i] = self.q(ly.linear(a, self.qw(P[pi[0]]), b))
+                outs[i] = self.q(ly.linear(_rows(a), self.qw(P[pi[0]]), b))
             elif k == "bn":
                 y, xhat, rstd = ly.batchnorm(a, P[pi[0]], P[pi[1]])
                 outs[i] = y
@@ -172,7 +181,9 @@ class Stage:
                 if want_dx:
                     acc(src, dx)
             elif k == "linear":
-                dx, dw, db = ly.linear_vjp(a, self.qw(P[pi[0]]), gi, want_dx, L["bias"])
+                dx, dw, db = ly.linear_vjp(_rows(a), self.qw(P[pi[0]]), _rows(gi), want_dx, L["bias"])
+                if dx is not None:
+                    dx = dx.reshape(a.shape)
                 grads[pi[0]] = dw
                 if L["bias"]:
                     grads[pi[1]] = db

@@ -111,6 +111,7 @@ _SIGS = {
     "xpipe_stage_fwd": [_P, _P, _P, _P, _P],
     "xpipe_stage_bwd": [_P, _P, _P, _P, _P],
     "xpipe_adam_step": [_P, ctypes.POINTER(HParams), _I32, _I32, _I32],
+    "xpipe_partition": [_P, _I32, _I32, ctypes.POINTER(_I32)],
     "xpipe_schedule": [_I32, _I32, _I32, _I32, _I32, _I32, _P, _I32, ctypes.POINTER(_I32)],
     "xpipe_stage_run": [_P, _P, _I32, ctypes.POINTER(RunIO), ctypes.POINTER(HParams), _P, _P, _P, _I32],
     "xpipe_rule_step": [_P, ctypes.POINTER(RuleParams), ctypes.POINTER(HParams), _P, _P, _I32, _I32,
@@ -342,6 +343,14 @@ def xpipe_predict_flat(W, m, v, out, out_bf16, s: int, hp: Hyper, t: int, stream
     c = hp.c(t)
     _check(lib().xpipe_predict_flat(_ptr(W), _ptr(m), _ptr(v), _ptr(out), _ptr(out_bf16),
                                     W.numel(), s, ctypes.byref(c), _stream_ptr(stream)))
+
+
+def xpipe_partition(layers, stages: int) -> List[int]:
+    """first layer index of each stage, and len(layers) (Sec. IV-A's partition)."""
+    arr = layer_descs(layers)
+    first = (_I32 * (stages + 1))()
+    _check(lib().xpipe_partition(arr, len(layers), stages, first))
+    return list(first)
 
 
 def xpipe_schedule(size: int, T: int, rank: int, minibatches: int, rounding: int = 0,

@@ -2064,3 +2064,38 @@ xpipe_status xpipe_stage_run(xpipe_stage_t st, const xpipe_sched_event* events, 
   }
   return XPIPE_OK;
 }
+
+// ============================================================================
+// Model partition (Sec. IV-A)
+// ============================================================================
+xpipe_status xpipe_partition(const xpipe_layer_desc* layers, int32_t n_layers, int32_t stages, int32_t* first) {
+  if (!layers || !first || n_layers <= 0 || stages < 1) return fail(XPIPE_EINVAL, "bad arguments");
+  std::vector<int32_t> wl;
+  for (int32_t i = 0; i < n_layers; ++i)
+    if (layers[i].kind == XPIPE_LINEAR || layers[i].kind == XPIPE_CONV) wl.push_back(i);
+  const int32_t L = (int32_t)wl.size();
+  if (stages > L) return fail(XPIPE_EINVAL, "more stages than layers with weights");
+  const int32_t base = L / stages, rem = L % stages;
+  int32_t w = 0;
+  first[0] = 0;
+  for (int32_t k = 0; k < stages; ++k) {
+    if (k > 0) first[k] = wl[w];
+    w += base + (k >= stages - rem ? 1 : 0);
+  }
+  first[stages] = n_layers;
+  // every layer reads only its own stage, or the previous stage's last layer
+  for (int32_t k = 0; k < stages; ++k)
+    for (int32_t i = first[k]; i < first[k + 1]; ++i) {
+      const xpipe_layer_desc& d = layers[i];
+      if (d.n_inputs < 1 || d.n_inputs > XPIPE_MAX_INPUTS) return fail(XPIPE_EINVAL, "bad input count");
+      for (int32_t q = 0; q < d.n_inputs; ++q) {
+        const int32_t j = d.inputs[q];
+        if (j >= i || j < -1) return fail(XPIPE_EINVAL, "layer inputs must precede the layer");
+        if (j >= first[k]) continue;
+        if (k == 0 ? j == -1 : j == first[k] - 1) continue;
+        return fail(XPIPE_EUNSUPPORTED, "layer " + std::to_string(i) + " of stage " + std::to_string(k) +
+                                            " reads layer " + std::to_string(j) + " across a stage boundary");
+      }
+    }
+  return XPIPE_OK;
+}

@@ -155,3 +155,37 @@ def test_schedule_rejects_bad_arguments():
             xp.xpipe_schedule(*args)
         assert e.value.status == xp.EINVAL
     assert xp.xpipe_schedule(4, 2, 0, 0) == []
+
+
+def test_partition_vgg16():
+    """Sec. IV-A's rule on VGG-16's 14 weighted layers over 4 GPUs: 3, 3, 4, 4
+    (the later GPUs take the remainder), each stage starting at a weighted
+    layer, trailing ReLUs and pools kept with the layer they follow."""
+    L = wl.vgg16_layers()
+    first = xp.xpipe_partition(L, 4)
+    assert first[0] == 0 and first[-1] == len(L)
+    weighted = lambda ls: sum(1 for l in ls if l["kind"] in ("conv", "linear"))
+    stages = wl.split_layers(L, first)
+    assert [weighted(s) for s in stages] == [3, 3, 4, 4]
+    for k, s in enumerate(stages):
+        if k:
+            assert s[0]["kind"] == "conv"
+        for i, l in enumerate(s):
+            assert all(-1 <= j < i for j in l["inputs"])
+    assert xp.xpipe_partition(L, 1) == [0, len(L)]
+    assert [weighted(s) for s in wl.split_layers(L, xp.xpipe_partition(L, 14))] == [1] * 14
+    with pytest.raises(xp.XPipeError) as e:
+        xp.xpipe_partition(L, 15)
+    assert e.value.status == xp.EINVAL
+
+
+def test_partition_refuses_cut_branches():
+    """ResNet bottlenecks split at block boundaries (the skip reads the previous
+    stage's output); Inception-A modules cut inside a module are refused."""
+    R = wl.resnet_stage_layers(blocks=8)
+    first = xp.xpipe_partition(R, 4)
+    for s in wl.split_layers(R, first):
+        assert sum(1 for l in s if l["kind"] == "conv") == 6
+    with pytest.raises(xp.XPipeError) as e:
+        xp.xpipe_partition(wl.inception_stage_layers(), 4)
+    assert e.value.status == xp.EUNSUPPORTED

@@ -1,0 +1,64 @@
+"""VGG-16 partitioned into four stages by Sec. IV-A's rule, run stage by stage
+on the GPU library (the activation of stage k is the input of stage k + 1,
+the input gradient of stage k + 1 the upstream gradient of stage k) against
+the oracle's forward and backward of the unpartitioned network.  fp32
+storage, s = 0: logits, loss and every weight gradient within 2e-4."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1911_04610_amd as xp
+import workloads as wl
+from conftest import rel_l2
+from gpu_harness import to_device, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+def test_partitioned_vgg16_matches_unpartitioned_oracle():
+    import torch
+    layers = wl.vgg16_layers()
+    w = wl.StageWorkload("vgg16_full", layers, 2, 1, (32, 32, 3), 4, 0, 0, 0, minibatches=1)
+    inp = wl.stage_inputs(w, act_dtype="f32")
+    x, labels = inp.xs[0][0], inp.labels[0][0]
+    first = xp.xpipe_partition(layers, 4)
+    parts = wl.split_layers(layers, first)
+    counts = [len(wl.param_shapes(p)) for p in parts]
+    offs = np.cumsum([0] + counts)
+    hp = xp.Hyper()
+    stages, ins, outs = [], [to_device(x, xp.F32)], []
+    lab = torch.from_numpy(labels).cuda()
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    in_shape = (32, 32, 3)
+    for k, p in enumerate(parts):
+        st = xp.Stage(p, w.micro_batch, 1, in_shape, xp.F32)
+        st.set_flat(st.W, inp.params[offs[k]:offs[k + 1]])
+        st.xpipe_predict_weights(xp.FWD, 0, hp, 0)
+        st.xpipe_predict_weights(xp.BWD, 0, hp, 0)
+        n, H, W_, C = st.out_shape
+        y = torch.empty((n, H, W_, C), dtype=torch.float32, device="cuda")
+        last = k == len(parts) - 1
+        st.xpipe_stage_fwd(ins[-1], y, lab if last else None, loss if last else None)
+        stages.append(st)
+        outs.append(y)
+        ins.append(y)
+        in_shape = (H, W_, C)
+    dy = None
+    for k in reversed(range(len(parts))):
+        st = stages[k]
+        dx = torch.empty_like(ins[k]) if k > 0 else None
+        st.xpipe_stage_bwd(ins[k], dy, lab if k == len(parts) - 1 else None, dx)
+        dy = dx
+    torch.cuda.synchronize()
+    grads = [g for st in stages for g in st.get_tensors(st.grad)]
+
+    ref = oracle.Stage(layers, "f32")
+    z, ref_loss, _ = ref.forward(inp.params, x, labels, w.micro_batch)
+    _, ref_grads, _ = ref.backward(inp.params, x, None, labels, w.micro_batch, False)
+    errs = {"logits": rel_l2(to_host(outs[-1]).reshape(z.shape), z),
+            "loss": abs(float(loss[0]) - ref_loss) / abs(ref_loss)}
+    for q, (a, b) in enumerate(zip(grads, ref_grads)):
+        errs[f"grad[{q}]"] = rel_l2(a, b)
+    worst = max(errs, key=errs.get)
+    print(f"partitioned VGG-16 {first}: worst {worst} = {errs[worst]:.2e}")
+    assert all(v <= 2e-4 for v in errs.values()), {k: v for k, v in errs.items() if v > 2e-4}

@@ -48,6 +48,24 @@ def test_stage_forward_backward_matches_torch(name):
         assert rel_l2(a, b) < 1e-11
 
 
+def test_full_vgg16_matches_torch():
+    """The whole VGG-16 (thirteen convolutions, five pools, the classifier on a
+    one-pixel map) against torch float64 autograd."""
+    layers = wl.vgg16_layers()
+    w = wl.StageWorkload("vgg16_full", layers, 2, 1, (32, 32, 3), 4, 0, 0, 0, minibatches=1)
+    inp = wl.stage_inputs(w)
+    st = oracle.Stage(layers)
+    x, lab = inp.xs[0][0], inp.labels[0][0]
+    y, loss, _ = st.forward(inp.params, x, lab, 2)
+    dx, grads, _ = st.backward(inp.params, x, None, lab, 2)
+    yt, losst, dxt, gt = torch_ref.fwd_bwd(layers, inp.params, x, None, lab, 2)
+    assert rel_l2(y.reshape(-1), np.asarray(yt).reshape(-1)) < 1e-12
+    assert abs(loss - losst) < 1e-12
+    assert rel_l2(dx, dxt) < 1e-11
+    for a, b in zip(grads, gt):
+        assert rel_l2(a, b) < 1e-11
+
+
 @pytest.mark.parametrize("name", ["tiny_mlp", "vgg16_stage0"])
 def test_accumulated_gradient_equals_full_minibatch_gradient(name):
     """Sec. III-A: gradients accumulated over the T micro-batches of a mini-batch

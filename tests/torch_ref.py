@@ -34,7 +34,8 @@ def forward(layers, P, x, labels=None, N=None):
             outs[i] = F.conv2d(a.permute(0, 3, 1, 2), P[pi[0]].permute(0, 3, 1, 2), b,
                                padding=L["k"] // 2).permute(0, 2, 3, 1)
         elif k == "linear":
-            outs[i] = F.linear(a, P[pi[0]], P[pi[1]] if L["bias"] else None)
+            a2 = a.reshape(a.shape[0], a.shape[-1]) if a.dim() == 4 else a   # [n,1,1,C] -> [n,C]
+            outs[i] = F.linear(a2, P[pi[0]], P[pi[1]] if L["bias"] else None)
         elif k == "bn":
             outs[i] = F.batch_norm(a.permute(0, 3, 1, 2), None, None, P[pi[0]], P[pi[1]],
                                    training=True, eps=1e-5).permute(0, 2, 3, 1)

@@ -79,6 +79,38 @@ def vgg_stage_layers() -> List[dict]:
     return b.layers
 
 
+def vgg16_layers(classes=10) -> List[dict]:
+    """VGG-16 for 32x32 inputs (Sec. IV-B's CIFAR-10 model): thirteen 3x3
+    convolutions with bias and ReLU in five blocks, each closed by a 2x2 max
+    pool (32 -> 1), then a linear classifier and the cross-entropy loss."""
+    b = _Builder()
+    x, cin = -1, 3
+    for widths in ((64, 64), (128, 128), (256, 256, 256), (512, 512, 512), (512, 512, 512)):
+        for c in widths:
+            x = b.relu(b.conv(x, cin, c, 3, bias=True))
+            cin = c
+        x = b.add(kind="maxpool2", inputs=[x])
+    z = b.linear(x, 512, classes)
+    b.add(kind="softmax_ce", inputs=[z], classes=classes)
+    return b.layers
+
+
+def split_layers(layers: List[dict], first: List[int]) -> List[List[dict]]:
+    """Per-stage layer lists for stage boundaries `first` (first[k] = stage k's
+    first layer, last entry = len(layers)): inputs re-indexed within the stage,
+    the previous stage's last layer becoming the stage input -1."""
+    out = []
+    for k in range(len(first) - 1):
+        a, b = first[k], first[k + 1]
+        stage = []
+        for L in layers[a:b]:
+            L = dict(L)
+            L["inputs"] = [-1 if (j == a - 1 or j == -1) else j - a for j in L["inputs"]]
+            stage.append(L)
+        out.append(stage)
+    return out
+
+
 def resnet_stage_layers(blocks=8, c=512, mid=128) -> List[dict]:
     """Middle ResNet-101 stage: bottlenecks with identity shortcut."""
     b = _Builder()

@@ -423,6 +423,71 @@ def measured_peaks():
             "copy_bytes": 2 * n, "mfma": "v_mfma_f32_32x32x16_bf16, %d waves x %d x 8" % (waves, iters)}
 
 
+def vendor_reference(reps=50):
+    """The stage's two most frequent convolution shapes (32 x 35 x 35 NHWC,
+    bf16) three ways, per launch, with HIP events over back-to-back launches:
+    this library's implicit GEMM (forward of a one-convolution stage: one
+    k_conv_gemm launch), MIOpen's convolution through torch (channels-last),
+    and hipBLASLt's plain GEMM of the same M x K x N through torch.mm (no
+    im2col: the library GEMM reads a ready K-major operand, which the
+    convolution does not have).  Context for the MFMA fraction of these skinny
+    shapes, not a dependency: the stage itself never calls the vendor
+    libraries."""
+    import numpy as np
+    import torch
+    import paper_1911_04610_amd as xp
+    import workloads as wl
+
+    def timed(fn):
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps * 1e3
+
+    torch.backends.cudnn.benchmark = True  # MIOpen picks its fastest algorithm per shape
+    out = []
+    nb, H, W = 32, 35, 35
+    for cin, cout, k in ((64, 96, 3), (96, 96, 3)):
+        b = wl._Builder()
+        b.conv(-1, cin, cout, k)
+        st = xp.Stage(b.layers, nb, 1, (H, W, cin), xp.BF16, stream=torch.cuda.current_stream())
+        rng = np.random.default_rng(wl.PAPER_SEED + 9)
+        st.set_flat(st.W, wl.init_params(b.layers, rng))
+        hp = xp.Hyper()
+        st.xpipe_predict_weights(xp.FWD, 0, hp, 0)
+        st.set_graphs(False)
+        x = torch.randn(nb, H, W, cin, device="cuda").to(torch.bfloat16)
+        y = torch.empty(nb, H, W, cout, device="cuda", dtype=torch.bfloat16)
+        ours = timed(lambda: st.xpipe_stage_fwd(x, y))
+        st.set_timing(True)
+        st.xpipe_stage_fwd(x, y)
+        torch.cuda.synchronize()
+        launched = sorted(st.timing())
+        st.set_timing(False)
+        xc = x.permute(0, 3, 1, 2)  # NCHW view of the NHWC data: channels-last
+        wt = torch.randn(cout, cin, k, k, device="cuda").to(torch.bfloat16).to(memory_format=torch.channels_last)
+        miopen = timed(lambda: torch.nn.functional.conv2d(xc, wt, padding=k // 2))
+        M, K = nb * H * W, k * k * cin
+        A = torch.randn(M, K, device="cuda").to(torch.bfloat16)
+        B = torch.randn(K, cout, device="cuda").to(torch.bfloat16)
+        blas = timed(lambda: A @ B)
+        fl = 2.0 * M * cout * K
+        out.append({"shape": f"conv {k}x{k} {cin}->{cout}, 32x35x35 NHWC bf16 (M={M}, N={cout}, K={K})",
+                    "ours_us": round(ours, 2), "ours_launches": launched, "miopen_conv_us": round(miopen, 2),
+                    "hipblaslt_gemm_us": round(blas, 2),
+                    "ours_TFLOP_s": round(fl / ours / 1e6, 1),
+                    "miopen_TFLOP_s": round(fl / miopen / 1e6, 1),
+                    "hipblaslt_TFLOP_s": round(fl / blas / 1e6, 1)})
+        del st
+    return out
+
+
 def cpu_baseline(w, dtype):
     """The oracle as it stands, on the host, for one whole step of the same
     stage: both predictions, T forwards, T backwards with recomputation and
@@ -544,6 +609,7 @@ def main():
     if not args.no_sweep:
         out["interleaved_schedule"] = time_interleaved(args)
         out["vgg16_partitioned"] = time_partitioned(args)
+        out["vendor_reference"] = vendor_reference()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.dtype)
     print(json.dumps(out))

@@ -400,11 +400,13 @@ template <typename T> struct VT;
 template <> struct VT<bf16_t> { static constexpr int N = 8; };
 template <> struct VT<float> { static constexpr int N = 4; };
 
+// a 16-byte chunk as raw bits, and its values widened to double
 template <typename T>
-XP_DEV void vld(const T* p, double* v);
+XP_DEV uint4 ld16(const T* p) { return *reinterpret_cast<const uint4*>(p); }
+template <typename T>
+XP_DEV void cvt16(uint4 u, double* v);
 template <>
-XP_DEV void vld<bf16_t>(const bf16_t* p, double* v) {
-  uint4 u = *reinterpret_cast<const uint4*>(p);
+XP_DEV void cvt16<bf16_t>(uint4 u, double* v) {
   const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -413,25 +415,31 @@ XP_DEV void vld<bf16_t>(const bf16_t* p, double* v) {
   }
 }
 template <>
-XP_DEV void vld<float>(const float* p, double* v) {
-  float4 f = *reinterpret_cast<const float4*>(p);
-  v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+XP_DEV void cvt16<float>(uint4 u, double* v) {
+  v[0] = __uint_as_float(u.x); v[1] = __uint_as_float(u.y);
+  v[2] = __uint_as_float(u.z); v[3] = __uint_as_float(u.w);
 }
 template <typename T>
-XP_DEV void vst(T* p, const double* v);
+XP_DEV void vld(const T* p, double* v) { cvt16<T>(ld16(p), v); }
+// a chunk of values rounded to the storage type, as raw bits
+template <typename T>
+XP_DEV uint4 pack16(const double* v);
 template <>
-XP_DEV void vst<bf16_t>(bf16_t* p, const double* v) {
+XP_DEV uint4 pack16<bf16_t>(const double* v) {
   uint4 u;
   u.x = f32x2_to_bf16x2((float)v[0], (float)v[1]);
   u.y = f32x2_to_bf16x2((float)v[2], (float)v[3]);
   u.z = f32x2_to_bf16x2((float)v[4], (float)v[5]);
   u.w = f32x2_to_bf16x2((float)v[6], (float)v[7]);
-  *reinterpret_cast<uint4*>(p) = u;
+  return u;
 }
 template <>
-XP_DEV void vst<float>(float* p, const double* v) {
-  *reinterpret_cast<float4*>(p) = make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
+XP_DEV uint4 pack16<float>(const double* v) {
+  return make_uint4(__float_as_uint((float)v[0]), __float_as_uint((float)v[1]),
+                    __float_as_uint((float)v[2]), __float_as_uint((float)v[3]));
 }
+template <typename T>
+XP_DEV void vst(T* p, const double* v) { *reinterpret_cast<uint4*>(p) = pack16<T>(v); }
 
 static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
@@ -452,13 +460,48 @@ static int grid_for(int64_t items) {
 
 // mask helper: zero lanes whose mask value is not > 0
 template <typename T>
-XP_DEV void vmask(const T* mk, double* v) {
+XP_DEV void vmask_raw(uint4 mk, double* v) {
   constexpr int N = VT<T>::N;
   double m[N];
-  vld(mk, m);
+  cvt16<T>(mk, m);
 #pragma unroll
   for (int e = 0; e < N; ++e)
     if (!(m[e] > 0.0)) v[e] = 0.0;
+}
+template <typename T>
+XP_DEV void vmask(const T* mk, double* v) { vmask_raw<T>(ld16(mk), v); }
+
+// Row kernels (BN apply / backward): a block holds CPB chunk columns x RPB
+// row lanes, each thread keeps its chunk's per-channel coefficients in
+// registers and walks rows with a grid-wide stride, U rows per trip, every
+// load of a trip issued before its arithmetic.
+struct RowMap {
+  int chunk, row0, stride;
+  bool live;
+};
+template <typename T>
+XP_DEV RowMap row_map(int C) {
+  constexpr int N = VT<T>::N;
+  const int chunks = C / N;
+  const int cpb = chunks < 256 ? chunks : 256;
+  const int rpb = 256 / cpb;
+  const int rl = threadIdx.x / cpb;
+  RowMap m;
+  m.chunk = blockIdx.y * cpb + (int)(threadIdx.x % cpb);
+  m.live = rl < rpb && m.chunk < chunks;
+  m.row0 = blockIdx.x * rpb + rl;
+  m.stride = gridDim.x * rpb;
+  return m;
+}
+// grid of a row kernel: about U rows per thread
+static dim3 row_grid(int64_t M, int C, int N, int U) {
+  const int chunks = C / N;
+  const int cpb = chunks < 256 ? chunks : 256;
+  const int rpb = 256 / cpb;
+  int64_t gx = (M + (int64_t)rpb * U - 1) / ((int64_t)rpb * U);
+  if (gx > 8192) gx = 8192;
+  if (gx < 1) gx = 1;
+  return dim3((unsigned)gx, (unsigned)((chunks + cpb - 1) / cpb));
 }
 
 // ---------------------------------------------------------------- column reductions
@@ -521,19 +564,27 @@ __global__ __launch_bounds__(256) void k_colpart_v(ColArgs a) {
   }
 #pragma unroll
   for (int e = 0; e < N; ++e) { sh[0][threadIdx.x][e] = s0[e]; sh[1][threadIdx.x][e] = s1[e]; }
-  __syncthreads();
+  // the RG row groups of a column are added pairwise in a fixed tree: at each
+  // level group g takes in group g + half
+  int half = 1;
+  while (2 * half < RG) half *= 2;
+  for (; half >= 1; half >>= 1) {
+    __syncthreads();
+    if (g < half && g + half < RG) {
+      const int o = (g + half) * CL + cl;
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        sh[0][threadIdx.x][e] += sh[0][o][e];
+        sh[1][threadIdx.x][e] += sh[1][o][e];
+      }
+    }
+  }
   if (g == 0 && chunk < chunks) {
-    double t0[N], t1[N];
-#pragma unroll
-    for (int e = 0; e < N; ++e) t0[e] = t1[e] = 0.0;
-    for (int q = 0; q < RG; ++q)
-#pragma unroll
-      for (int e = 0; e < N; ++e) { t0[e] += sh[0][q * CL + cl][e]; t1[e] += sh[1][q * CL + cl][e]; }
     const int c0 = chunk * N;
 #pragma unroll
     for (int e = 0; e < N; ++e) {
-      a.partial[((size_t)(c0 + e) * 2 + 0) * a.row_blocks + blockIdx.y] = t0[e];
-      a.partial[((size_t)(c0 + e) * 2 + 1) * a.row_blocks + blockIdx.y] = t1[e];
+      a.partial[((size_t)(c0 + e) * 2 + 0) * a.row_blocks + blockIdx.y] = sh[0][cl][e];
+      a.partial[((size_t)(c0 + e) * 2 + 1) * a.row_blocks + blockIdx.y] = sh[1][cl][e];
     }
   }
 }
@@ -600,73 +651,127 @@ static hipError_t colreduce_v(ColArgs a, hipStream_t s) {
 
 
 // ---------------------------------------------------------------- BN apply / backward
-template <typename T>
+template <typename T, int U>
 __global__ __launch_bounds__(256) void k_bn_apply_v(BnApplyArgs a) {
   constexpr int N = VT<T>::N;
-  const int chunks = a.C / N;
-  const int items = a.M * chunks;
+  const RowMap m = row_map<T>(a.C);
+  if (!m.live) return;
+  const int c0 = m.chunk * N;
+  double mu[N], rs[N], ga[N], be[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) {
+    mu[e] = a.mean[c0 + e];
+    rs[e] = a.rstd[c0 + e];
+    ga[e] = (double)a.gamma[c0 + e];
+    be[e] = (double)a.beta[c0 + e];
+  }
   const T* Z = (const T*)a.z;
   const T* R = (const T*)a.res;
   T* Y = (T*)a.y;
-  for (int it = blockIdx.x * blockDim.x + threadIdx.x; it < items; it += gridDim.x * blockDim.x) {
-    const int r = it / chunks, c0 = (it - r * chunks) * N;
-    double z[N], rr[N];
-    vld(Z + (size_t)r * a.ldz + c0, z);
-    if (R) vld(R + (size_t)r * a.ldres + c0, rr);
+  for (int r0 = m.row0; r0 < a.M; r0 += U * m.stride) {
+    uint4 zr[U], rr[U];
 #pragma unroll
-    for (int e = 0; e < N; ++e) {
-      double xh = (z[e] - a.mean[c0 + e]) * a.rstd[c0 + e];
-      double v = (double)a.gamma[c0 + e] * xh + (double)a.beta[c0 + e];
-      if (R) v += rr[e];
-      if (a.relu) v = v > 0.0 ? v : 0.0;
-      z[e] = v;
+    for (int u = 0; u < U; ++u) {
+      const int r = r0 + u * m.stride;
+      zr[u] = rr[u] = make_uint4(0u, 0u, 0u, 0u);
+      if (r < a.M) {
+        zr[u] = ld16(Z + (size_t)r * a.ldz + c0);
+        if (R) rr[u] = ld16(R + (size_t)r * a.ldres + c0);
+      }
     }
-    vst(Y + (size_t)r * a.ldy + c0, z);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int r = r0 + u * m.stride;
+      if (r >= a.M) break;
+      double z[N], q[N];
+      cvt16<T>(zr[u], z);
+      if (R) cvt16<T>(rr[u], q);
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        double xh = (z[e] - mu[e]) * rs[e];
+        double v = ga[e] * xh + be[e];
+        if (R) v += q[e];
+        if (a.relu) v = v > 0.0 ? v : 0.0;
+        z[e] = v;
+      }
+      vst(Y + (size_t)r * a.ldy + c0, z);
+    }
   }
 }
 
-template <typename T>
+template <typename T, int U>
 __global__ __launch_bounds__(256) void k_bn_bwd_v(BnBwdArgs a) {
   constexpr int N = VT<T>::N;
-  const int chunks = a.C / N;
-  const int items = a.M * chunks;
+  const RowMap m = row_map<T>(a.C);
+  if (!m.live) return;
+  const int c0 = m.chunk * N;
+  // d = gamma rstd (g - dbeta / M - xh dgamma / M), xh = (z - mean) rstd
+  double mu[N], rs[N], grs[N], db[N], dg[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) {
+    const int c = c0 + e;
+    mu[e] = a.mean[c];
+    rs[e] = a.rstd[c];
+    grs[e] = (double)a.gamma[c] * rs[e];
+    db[e] = a.dbeta[c] / a.M;
+    dg[e] = a.dgamma[c] / a.M;
+  }
   const T* G = (const T*)a.g;
   const T* Z = (const T*)a.z;
   T* DZ = (T*)a.dz;
   T* DR = (T*)a.dres;
   const T* RM = (const T*)a.resmask;
   const T* ZM = (const T*)a.dzmask;
-  for (int it = blockIdx.x * blockDim.x + threadIdx.x; it < items; it += gridDim.x * blockDim.x) {
-    const int r = it / chunks, c0 = (it - r * chunks) * N;
-    double g[N], z[N], d[N];
-    vld(G + (size_t)r * a.ldg + c0, g);
-    vld(Z + (size_t)r * a.ldz + c0, z);
+  const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+  // the residual source can be the BN input itself (its gradient accumulates
+  // onto the BN-input gradient just stored): then the stored chunk is reused
+  const bool res_is_dz = DR == DZ && a.lddres == a.lddz;
+  for (int r0 = m.row0; r0 < a.M; r0 += U * m.stride) {
+    uint4 gr[U], zr[U], zm[U], zo[U], rm[U], ro[U];
 #pragma unroll
-    for (int e = 0; e < N; ++e) {
-      const int c = c0 + e;
-      double rs = a.rstd[c];
-      double xh = (z[e] - a.mean[c]) * rs;
-      d[e] = (double)a.gamma[c] * rs * (g[e] - a.dbeta[c] / a.M - xh * (a.dgamma[c] / a.M));
-    }
-    if (ZM) vmask(ZM + (size_t)r * a.ldzm + c0, d);
-    T* pz = DZ + (size_t)r * a.lddz + c0;
-    if (a.dz_accumulate) {
-      double o[N];
-      vld(pz, o);
-#pragma unroll
-      for (int e = 0; e < N; ++e) d[e] += o[e];
-    }
-    vst(pz, d);
-    if (DR) {
-      if (RM) vmask(RM + (size_t)r * a.ldrm + c0, g);
-      T* p = DR + (size_t)r * a.lddres + c0;
-      if (a.res_accumulate) {
-        double o[N];
-        vld(p, o);
-#pragma unroll
-        for (int e = 0; e < N; ++e) g[e] += o[e];
+    for (int u = 0; u < U; ++u) {
+      const int r = r0 + u * m.stride;
+      gr[u] = zr[u] = zm[u] = zo[u] = rm[u] = ro[u] = zero;
+      if (r < a.M) {
+        gr[u] = ld16(G + (size_t)r * a.ldg + c0);
+        zr[u] = ld16(Z + (size_t)r * a.ldz + c0);
+        if (ZM) zm[u] = ld16(ZM + (size_t)r * a.ldzm + c0);
+        if (a.dz_accumulate) zo[u] = ld16(DZ + (size_t)r * a.lddz + c0);
+        if (DR && RM) rm[u] = ld16(RM + (size_t)r * a.ldrm + c0);
+        if (DR && a.res_accumulate && !res_is_dz) ro[u] = ld16(DR + (size_t)r * a.lddres + c0);
       }
-      vst(p, g);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int r = r0 + u * m.stride;
+      if (r >= a.M) break;
+      double g[N], z[N], d[N];
+      cvt16<T>(gr[u], g);
+      cvt16<T>(zr[u], z);
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        double xh = (z[e] - mu[e]) * rs[e];
+        d[e] = grs[e] * (g[e] - db[e] - xh * dg[e]);
+      }
+      if (ZM) vmask_raw<T>(zm[u], d);
+      if (a.dz_accumulate) {
+        double o[N];
+        cvt16<T>(zo[u], o);
+#pragma unroll
+        for (int e = 0; e < N; ++e) d[e] += o[e];
+      }
+      const uint4 dbits = pack16<T>(d);
+      *reinterpret_cast<uint4*>(DZ + (size_t)r * a.lddz + c0) = dbits;
+      if (DR) {
+        if (RM) vmask_raw<T>(rm[u], g);
+        if (a.res_accumulate) {
+          double o[N];
+          cvt16<T>(res_is_dz ? dbits : ro[u], o);
+#pragma unroll
+          for (int e = 0; e < N; ++e) g[e] += o[e];
+        }
+        vst(DR + (size_t)r * a.lddres + c0, g);
+      }
     }
   }
 }
@@ -779,15 +884,19 @@ __global__ __launch_bounds__(256) void k_maxpool_bwd_v(PoolArgs a) {
   }
 }
 
-// 3x3 / stride 1 / zero-padded average (padding counted): each thread slides
-// along a run of AVG_SEG outputs of one image row and one 16-byte channel
-// chunk, keeping the vertical three-row sums of the previous, current and next
-// column, so each input chunk is loaded three times instead of nine.
-// out(h, w) = (v(w-1) + v(w)) + v(w+1) with v(w) = (x(h-1, w) + x(h, w)) + x(h+1, w).
+// 3x3 / stride 1 / zero-padded average (padding counted): each thread owns a
+// run of AVG_SEG outputs of one image row and one 16-byte channel chunk.  It
+// issues every load of its 3 x (AVG_SEG + 2) input window (and of its mask and
+// accumulation operands) before any arithmetic, so a thread waits on memory
+// once, then slides along the run keeping the vertical three-row sums of the
+// previous, current and next column:
+// out(h, w) = ((v(w-1) + v(w)) + v(w+1)) / 9, v(w) = (x(h-1, w) + x(h, w)) + x(h+1, w),
+// with zeros outside the image.
 constexpr int AVG_SEG = 7;
 template <typename T>
 __global__ __launch_bounds__(256) void k_avgpool3_v(PoolArgs a, const T* src, int ld_src) {
   constexpr int N = VT<T>::N;
+  constexpr int WIN = AVG_SEG + 2;
   const int chunks = a.C / N;
   const int nseg = ceil_div(a.W, AVG_SEG);
   int it = blockIdx.x * blockDim.x + threadIdx.x;
@@ -798,41 +907,58 @@ __global__ __launch_bounds__(256) void k_avgpool3_v(PoolArgs a, const T* src, in
   it /= nseg;
   const int h = it % a.H, n = it / a.H;
   const int c0 = chunk * N;
-  const int w0 = seg * AVG_SEG, w1 = min(a.W, w0 + AVG_SEG);
-  auto vsum = [&](int w, double* v) {
+  const int w0 = seg * AVG_SEG;
+  const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+  uint4 win[3][WIN];
 #pragma unroll
-    for (int e = 0; e < N; ++e) v[e] = 0.0;
-    if (w < 0 || w >= a.W) return;
+  for (int dr = 0; dr < 3; ++dr) {
+    const int hh = h + dr - 1;
+    const bool rok = hh >= 0 && hh < a.H;
 #pragma unroll
-    for (int dr = -1; dr <= 1; ++dr) {
-      const int hh = h + dr;
-      if (hh < 0 || hh >= a.H) continue;
-      double q[N];
-      vld(src + ((size_t)(n * a.H + hh) * a.W + w) * ld_src + c0, q);
-#pragma unroll
-      for (int e = 0; e < N; ++e) v[e] += q[e];
+    for (int j = 0; j < WIN; ++j) {
+      const int w = w0 - 1 + j;
+      win[dr][j] = (rok && w >= 0 && w < a.W)
+                       ? ld16(src + ((size_t)(n * a.H + hh) * a.W + w) * ld_src + c0) : zero;
     }
-  };
+  }
   const T* MK = (const T*)a.mask;
   T* O = (T*)a.out;
+  const size_t rbase = (size_t)(n * a.H + h) * a.W;
+  uint4 mk[AVG_SEG], old[AVG_SEG];
+#pragma unroll
+  for (int j = 0; j < AVG_SEG; ++j) {
+    mk[j] = old[j] = zero;
+    if (w0 + j < a.W) {
+      if (MK) mk[j] = ld16(MK + (rbase + w0 + j) * a.ldm + c0);
+      if (a.accumulate) old[j] = ld16(O + (rbase + w0 + j) * a.ldo + c0);
+    }
+  }
+  auto vsum = [&](int j, double* v) {
+    double q0[N], q1[N], q2[N];
+    cvt16<T>(win[0][j], q0);
+    cvt16<T>(win[1][j], q1);
+    cvt16<T>(win[2][j], q2);
+#pragma unroll
+    for (int e = 0; e < N; ++e) v[e] = (q0[e] + q1[e]) + q2[e];
+  };
   double vp[N], vc[N], vn[N];
-  vsum(w0 - 1, vp);
-  vsum(w0, vc);
-  for (int w = w0; w < w1; ++w) {
-    vsum(w + 1, vn);
+  vsum(0, vp);
+  vsum(1, vc);
+#pragma unroll
+  for (int j = 0; j < AVG_SEG; ++j) {
+    if (w0 + j >= a.W) break;
+    vsum(j + 2, vn);
     double s[N];
 #pragma unroll
     for (int e = 0; e < N; ++e) s[e] = ((vp[e] + vc[e]) + vn[e]) / 9.0;
-    const size_t r = (size_t)(n * a.H + h) * a.W + w;
-    if (MK) vmask(MK + r * a.ldm + c0, s);
-    T* p = O + r * a.ldo + c0;
+    if (MK) vmask_raw<T>(mk[j], s);
     if (a.accumulate) {
       double q[N];
-      vld(p, q);
+      cvt16<T>(old[j], q);
 #pragma unroll
       for (int e = 0; e < N; ++e) s[e] += q[e];
     }
-    vst(p, s);
+    vst(O + (rbase + w0 + j) * a.ldo + c0, s);
 #pragma unroll
     for (int e = 0; e < N; ++e) {
       vp[e] = vc[e];
@@ -1017,18 +1143,38 @@ static bool vec_dt(int dtype, int64_t rows, int C, std::initializer_list<std::pa
 }
 static int vn(int dtype) { return dtype == DT_BF16 ? 8 : 4; }
 
+constexpr int BN_APPLY_U = 4, BN_BWD_U = 2;  // rows per trip of the row kernels
+
 hipError_t launch_bn_apply(int dtype, const BnApplyArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.C <= 0) return hipSuccess;
-  if (vec_dt(dtype, a.M, a.C, {{a.z, a.ldz}, {a.res, a.ldres}, {a.y, a.ldy}}))
-    XP_VEC_LAUNCH(k_bn_apply_v, (int64_t)a.M * (a.C / vn(dtype)), vn(dtype) * (dtype == DT_BF16 ? 2 : 4) * (a.res ? 3 : 2), a);
+  if (vec_dt(dtype, a.M, a.C, {{a.z, a.ldz}, {a.res, a.ldres}, {a.y, a.ldy}})) {
+    const int N = vn(dtype);
+    const dim3 grid = row_grid(a.M, a.C, N, BN_APPLY_U);
+    const double bytes = (double)a.M * a.C * (dtype == DT_BF16 ? 2 : 4) * (a.res ? 3 : 2);
+    if (dtype == DT_BF16)
+      XP_LAUNCH("k_bn_apply_v<bf16>", bytes, (k_bn_apply_v<bf16_t, BN_APPLY_U>), grid, dim3(256), 0, s, a);
+    else
+      XP_LAUNCH("k_bn_apply_v<f32>", bytes, (k_bn_apply_v<float, BN_APPLY_U>), grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
   return launch_bn_apply_s(dtype, a, s);
 }
 
 hipError_t launch_bn_bwd(int dtype, const BnBwdArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.C <= 0) return hipSuccess;
   if (vec_dt(dtype, a.M, a.C, {{a.g, a.ldg}, {a.z, a.ldz}, {a.dz, a.lddz}, {a.dzmask, a.ldzm},
-                               {a.dres, a.lddres}, {a.resmask, a.ldrm}}))
-    XP_VEC_LAUNCH(k_bn_bwd_v, (int64_t)a.M * (a.C / vn(dtype)), vn(dtype) * (dtype == DT_BF16 ? 2 : 4) * (3 + (a.dres ? 2 : 0) + (a.dz_accumulate ? 1 : 0)), a);
+                               {a.dres, a.lddres}, {a.resmask, a.ldrm}})) {
+    const int N = vn(dtype);
+    const dim3 grid = row_grid(a.M, a.C, N, BN_BWD_U);
+    const int tensors = 3 + (a.dzmask ? 1 : 0) + (a.dz_accumulate ? 1 : 0) +
+                        (a.dres ? 1 + (a.resmask ? 1 : 0) + (a.res_accumulate ? 1 : 0) : 0);
+    const double bytes = (double)a.M * a.C * (dtype == DT_BF16 ? 2 : 4) * tensors;
+    if (dtype == DT_BF16)
+      XP_LAUNCH("k_bn_bwd_v<bf16>", bytes, (k_bn_bwd_v<bf16_t, BN_BWD_U>), grid, dim3(256), 0, s, a);
+    else
+      XP_LAUNCH("k_bn_bwd_v<f32>", bytes, (k_bn_bwd_v<float, BN_BWD_U>), grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
   return launch_bn_bwd_s(dtype, a, s);
 }
 
@@ -1065,10 +1211,10 @@ hipError_t launch_avgpool_fwd(int dtype, const PoolArgs& a, hipStream_t s) {
   if (vec_dt(dtype, rows, a.C, {{a.x, a.ldx}, {a.mask, a.ldm}, {a.out, a.ldo}})) {
     const int blocks = avg_blocks(a, vn(dtype));
     if (dtype == DT_BF16)
-      XP_LAUNCH("k_avgpool3_v<bf16>", (double)rows * a.C * 2 * (a.accumulate ? 3 : 2), k_avgpool3_v<bf16_t>,
+      XP_LAUNCH("k_avgpool3_v<bf16>", (double)rows * a.C * 2 * ((a.accumulate ? 3 : 2) + (a.mask ? 1 : 0)), k_avgpool3_v<bf16_t>,
                 dim3(blocks), dim3(256), 0, s, a, (const bf16_t*)a.x, a.ldx);
     else
-      XP_LAUNCH("k_avgpool3_v<f32>", (double)rows * a.C * 4 * (a.accumulate ? 3 : 2), k_avgpool3_v<float>,
+      XP_LAUNCH("k_avgpool3_v<f32>", (double)rows * a.C * 4 * ((a.accumulate ? 3 : 2) + (a.mask ? 1 : 0)), k_avgpool3_v<float>,
                 dim3(blocks), dim3(256), 0, s, a, (const float*)a.x, a.ldx);
     return hipGetLastError();
   }
@@ -1081,10 +1227,10 @@ hipError_t launch_avgpool_bwd(int dtype, const PoolArgs& a, hipStream_t s) {
   if (vec_dt(dtype, rows, a.C, {{a.dy, a.lddy}, {a.mask, a.ldm}, {a.out, a.ldo}})) {
     const int blocks = avg_blocks(a, vn(dtype));
     if (dtype == DT_BF16)
-      XP_LAUNCH("k_avgpool3_v<bf16>", (double)rows * a.C * 2 * (a.accumulate ? 3 : 2), k_avgpool3_v<bf16_t>,
+      XP_LAUNCH("k_avgpool3_v<bf16>", (double)rows * a.C * 2 * ((a.accumulate ? 3 : 2) + (a.mask ? 1 : 0)), k_avgpool3_v<bf16_t>,
                 dim3(blocks), dim3(256), 0, s, a, (const bf16_t*)a.dy, a.lddy);
     else
-      XP_LAUNCH("k_avgpool3_v<f32>", (double)rows * a.C * 4 * (a.accumulate ? 3 : 2), k_avgpool3_v<float>,
+      XP_LAUNCH("k_avgpool3_v<f32>", (double)rows * a.C * 4 * ((a.accumulate ? 3 : 2) + (a.mask ? 1 : 0)), k_avgpool3_v<float>,
                 dim3(blocks), dim3(256), 0, s, a, (const float*)a.dy, a.lddy);
     return hipGetLastError();
   }

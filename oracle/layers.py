@@ -5,9 +5,11 @@ TEST INFRASTRUCTURE ONLY (the CPU oracle; see oracle/__init__.py).
 The paper runs stock framework layers (Sec. IV-A, IV-C) and defines none of
 them; each function below is the textbook definition written out.  Layouts:
 activations NHWC (or [n, C]), conv weights [K, R, S, C], linear weights
-[out, in].  Convolutions are stride 1 with zero padding k//2 (cross-
-correlation).  ReLU'(0) = 0.  Max pooling sends the gradient to the first
-maximum in row-major window order.  3x3 average pooling counts the zero
+[out, in].  Convolutions have zero padding k//2 and stride 1 or 2 (cross-
+correlation; output size floor((H - 1) / stride) + 1, the strided layers of
+ResNet-101).  ReLU'(0) = 0.  Max pooling sends the gradient to the first
+maximum in row-major window order (the 3x3 stride-2 pool of the ResNet stem
+pads with -inf).  3x3 average pooling counts the zero
 padding (divides by 9).  Batch normalisation uses the batch mean and the
 biased batch variance of the micro-batch, eps 1e-5.
 """
@@ -18,41 +20,55 @@ import numpy as np
 BN_EPS = 1e-5
 
 
-def _shifted(xp, r, s, H, W):
-    """The H x W window of padded input xp starting at (r, s), as [n*H*W, C]."""
-    return np.ascontiguousarray(xp[:, r:r + H, s:s + W, :]).reshape(-1, xp.shape[3])
+def _win(r, s, Ho, Wo, stride):
+    """Index of the Ho x Wo output grid's taps (r, s) in the padded input."""
+    return (slice(None), slice(r, r + stride * (Ho - 1) + 1, stride),
+            slice(s, s + stride * (Wo - 1) + 1, stride), slice(None))
+
+
+def _shifted(xp, r, s, Ho, Wo, stride=1):
+    """Tap (r, s) of every output position, from padded input xp, as [n*Ho*Wo, C]."""
+    return np.ascontiguousarray(xp[_win(r, s, Ho, Wo, stride)]).reshape(-1, xp.shape[3])
+
+
+def conv_out(H, k, stride=1):
+    """Output size of a zero-padded (k//2) convolution: floor((H + 2p - k) / stride) + 1."""
+    p = k // 2
+    return (H + 2 * p - k) // stride + 1
 
 
 # ---------------------------------------------------------------- conv / linear
-def conv2d(x, w, b=None):
-    """y[n,h,w,k] = sum_{r,s,c} x[n, h+r-p, w+s-p, c] * w[k,r,s,c] (+ b[k])."""
+def conv2d(x, w, b=None, stride=1):
+    """y[n,h,w,k] = sum_{r,s,c} x[n, h*st+r-p, w*st+s-p, c] * w[k,r,s,c] (+ b[k])."""
     n, H, W, C = x.shape
     K, R, S, _ = w.shape
     p = R // 2
+    Ho, Wo = conv_out(H, R, stride), conv_out(W, S, stride)
     xp = np.pad(x, ((0, 0), (p, p), (p, p), (0, 0)))
-    y = np.zeros((n * H * W, K))
+    y = np.zeros((n * Ho * Wo, K))
     for r in range(R):
         for s in range(S):
-            y += _shifted(xp, r, s, H, W) @ w[:, r, s, :].T
+            y += _shifted(xp, r, s, Ho, Wo, stride) @ w[:, r, s, :].T
     if b is not None:
         y += b
-    return y.reshape(n, H, W, K)
+    return y.reshape(n, Ho, Wo, K)
 
 
-def conv2d_vjp(x, w, dy, need_dx=True, has_bias=False):
+def conv2d_vjp(x, w, dy, need_dx=True, has_bias=False, stride=1):
     """Gradients of conv2d w.r.t. x, w and b for cotangent dy."""
     n, H, W, C = x.shape
     K, R, S, _ = w.shape
     p = R // 2
+    Ho, Wo = dy.shape[1], dy.shape[2]
     xp = np.pad(x, ((0, 0), (p, p), (p, p), (0, 0)))
     dy2 = dy.reshape(-1, K)
     dw = np.zeros_like(w)
     dxp = np.zeros_like(xp) if need_dx else None
     for r in range(R):
         for s in range(S):
-            dw[:, r, s, :] = dy2.T @ _shifted(xp, r, s, H, W)
+            dw[:, r, s, :] = dy2.T @ _shifted(xp, r, s, Ho, Wo, stride)
             if need_dx:
-                dxp[:, r:r + H, s:s + W, :] += (dy2 @ w[:, r, s, :]).reshape(n, H, W, C)
+                dxp[_win(r, s, Ho, Wo, stride)] += (dy2 @ w[:, r, s, :]).reshape(n, Ho, Wo, C)
     db = dy2.sum(axis=0) if has_bias else None
     dx = dxp[:, p:p + H, p:p + W, :] if need_dx else None
     return dx, dw, db
@@ -132,6 +148,31 @@ def maxpool2_vjp(x_shape, idx, dy):
     dx[:, :2 * Ho, :2 * Wo, :] = (win.reshape(n, Ho, Wo, 2, 2, C)
                                   .transpose(0, 1, 3, 2, 4, 5).reshape(n, 2 * Ho, 2 * Wo, C))
     return dx
+
+
+def maxpool3s2(x):
+    """3x3 max pooling, stride 2, padding 1 with -inf (never chosen: the window
+    centre is always inside).  Output floor((H - 1) / 2) + 1.  Returns (y,
+    argmax index 0..8 per output, the first maximum in row-major order)."""
+    n, H, W, C = x.shape
+    Ho, Wo = (H - 1) // 2 + 1, (W - 1) // 2 + 1
+    xp = np.pad(x, ((0, 0), (1, 1), (1, 1), (0, 0)), constant_values=-np.inf)
+    win = np.stack([xp[_win(r, s, Ho, Wo, 2)] for r in range(3) for s in range(3)], axis=3)
+    idx = np.argmax(win, axis=3)
+    y = np.take_along_axis(win, idx[:, :, :, None, :], axis=3)[:, :, :, 0, :]
+    return y, idx
+
+
+def maxpool3s2_vjp(x_shape, idx, dy):
+    """Each output's gradient goes to its window's first maximum; windows overlap,
+    so an input adds the gradients of every output that chose it."""
+    n, H, W, C = x_shape
+    Ho, Wo = dy.shape[1], dy.shape[2]
+    dxp = np.zeros((n, H + 2, W + 2, C))
+    for j in range(9):
+        r, s = divmod(j, 3)
+        dxp[_win(r, s, Ho, Wo, 2)] += np.where(idx == j, dy, 0.0)
+    return dxp[:, 1:H + 1, 1:W + 1, :]
 
 
 def avgpool3(x):

@@ -21,9 +21,13 @@ take the decision on values of the same precision, so the oracle can round
                   weights multiplied as bf16 (the fp32 prediction, rounded);
 in both, the predicted weights, the master weights, both moments and the
 gradient accumulator are rounded to fp32 each time they are written.
-Rounded activations are the outputs of conv, linear, relu, maxpool2, avgpool3
-and gap layers.  BN and residual-add outputs are never stored on their own
-(a ReLU always follows them in these stages) and are not rounded.  Every
+Rounded activations are the outputs of conv, linear, relu, avgpool3 and gap
+layers (max pools select stored values).  A BN output feeding only a ReLU, or
+only a residual add whose other operand comes earlier in the list, is fused
+into that consumer and not rounded; any other BN output (the projection
+shortcut of a ResNet block, added to the main path's BN) is a stored
+activation and is rounded.  Residual-add outputs are followed by a ReLU and
+are not rounded.  Every
 activation gradient is rounded each time a contribution is added to it;
 contributions arrive in reverse layer order.  storage="f64" rounds nothing.
 """
@@ -81,6 +85,21 @@ class Stage:
             self.pidx.append(list(range(k, k + n)))
             k += n
         self.n_params = k
+        # BN outputs that are stored on their own (not fused into their consumer)
+        cons = [[j for j, M in enumerate(layer_list) if i in M["inputs"]] for i in range(len(layer_list))]
+        self.bn_stored = {}
+        for i, L in enumerate(layer_list):
+            if L["kind"] != "bn":
+                continue
+            fused = False
+            if len(cons[i]) == 1:
+                c = layer_list[cons[i][0]]
+                if c["kind"] == "relu":
+                    fused = True
+                elif c["kind"] == "add":
+                    other = c["inputs"][1] if c["inputs"][0] == i else c["inputs"][0]
+                    fused = other < i
+            self.bn_stored[i] = not fused
 
     # storage rounding: activations / gradients (q), conv and linear weight
     # operands (qw), fp32 state (qs)
@@ -115,13 +134,13 @@ class Stage:
             pi = self.pidx[i]
             if k == "conv":
                 b = P[pi[1]] if L["bias"] else None
-                outs[i] = self.q(ly.conv2d(a, self.qw(P[pi[0]]), b))
+                outs[i] = self.q(ly.conv2d(a, self.qw(P[pi[0]]), b, L.get("stride", 1)))
             elif k == "linear":
                 b = P[pi[1]] if L["bias"] else None
                 outs[i] = self.q(ly.linear(_rows(a), self.qw(P[pi[0]]), b))
             elif k == "bn":
                 y, xhat, rstd = ly.batchnorm(a, P[pi[0]], P[pi[1]])
-                outs[i] = y
+                outs[i] = self.q(y) if self.bn_stored[i] else y
                 saved[i] = (xhat, rstd)
             elif k == "relu":
                 outs[i] = self.q(ly.relu(a))
@@ -129,6 +148,10 @@ class Stage:
                 outs[i] = a + outs[L["inputs"][1]]
             elif k == "maxpool2":
                 y, idx = ly.maxpool2(a)
+                outs[i] = y
+                saved[i] = idx
+            elif k == "maxpool3s2":
+                y, idx = ly.maxpool3s2(a)
                 outs[i] = y
                 saved[i] = idx
             elif k == "avgpool3":
@@ -174,7 +197,8 @@ class Stage:
             pi = self.pidx[i]
             want_dx = need_dx or src != -1
             if k == "conv":
-                dx, dw, db = ly.conv2d_vjp(a, self.qw(P[pi[0]]), gi, want_dx, L["bias"])
+                dx, dw, db = ly.conv2d_vjp(a, self.qw(P[pi[0]]), gi, want_dx, L["bias"],
+                                           L.get("stride", 1))
                 grads[pi[0]] = dw
                 if L["bias"]:
                     grads[pi[1]] = db
@@ -202,6 +226,8 @@ class Stage:
                 acc(L["inputs"][1], gi)
             elif k == "maxpool2":
                 acc(src, ly.maxpool2_vjp(a.shape, saved[i], gi))
+            elif k == "maxpool3s2":
+                acc(src, ly.maxpool3s2_vjp(a.shape, saved[i], gi))
             elif k == "avgpool3":
                 acc(src, ly.avgpool3_vjp(gi))
             elif k == "gap":

@@ -177,3 +177,76 @@ def test_bf16_rounding_matches_torch_and_ties_to_even():
     a = rng.standard_normal(100000) * 10.0 ** rng.uniform(-20, 20, 100000)
     want = torch.tensor(a, dtype=torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
     np.testing.assert_array_equal(ostage._round_bf16(a), want)
+
+
+@pytest.mark.parametrize("k,H,W", [(1, 8, 7), (3, 9, 8), (7, 12, 11)])
+def test_strided_conv_matches_torch(k, H, W):
+    """Stride 2 (ResNet-101's stem, first blocks and projections): values and
+    every gradient against torch's float64 convolution, odd and even sizes."""
+    rng = np.random.default_rng(20 + k)
+    x = rng.standard_normal((2, H, W, 5))
+    w = rng.standard_normal((6, k, k, 5))
+    b = rng.standard_normal(6)
+    xt = torch.tensor(x.transpose(0, 3, 1, 2), requires_grad=True)
+    wt = torch.tensor(w.transpose(0, 3, 1, 2), requires_grad=True)
+    bt = torch.tensor(b, requires_grad=True)
+    yt = F.conv2d(xt, wt, bt, stride=2, padding=k // 2)
+    assert yt.shape[2:] == (ly.conv_out(H, k, 2), ly.conv_out(W, k, 2)) == ((H - 1) // 2 + 1, (W - 1) // 2 + 1)
+    dy = rng.standard_normal(yt.shape)
+    yt.backward(torch.tensor(dy))
+    y = ly.conv2d(x, w, b, stride=2)
+    np.testing.assert_allclose(y, yt.detach().numpy().transpose(0, 2, 3, 1), rtol=1e-12, atol=1e-12)
+    dx, dw, db = ly.conv2d_vjp(x, w, dy.transpose(0, 2, 3, 1), True, True, stride=2)
+    np.testing.assert_allclose(dx, xt.grad.numpy().transpose(0, 2, 3, 1), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dw, wt.grad.numpy().transpose(0, 2, 3, 1), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(db, bt.grad.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_strided_conv_vjp_finite_differences():
+    rng = np.random.default_rng(31)
+    x = rng.standard_normal((1, 7, 6, 2))
+    w = rng.standard_normal((3, 3, 3, 2))
+    dy = rng.standard_normal((1, 4, 3, 3))
+    dx, dw, _ = ly.conv2d_vjp(x, w, dy, True, False, stride=2)
+    _fd_vs_vjp(lambda x_: ly.conv2d(x_, w, None, 2), [x], 0, dy, dx)
+    _fd_vs_vjp(lambda w_: ly.conv2d(x, w_, None, 2), [w], 0, dy, dw)
+
+
+@pytest.mark.parametrize("H,W", [(9, 8), (8, 7)])
+def test_maxpool3s2_matches_torch(H, W):
+    """3x3 window, stride 2, padding 1 (the ResNet stem's pool): overlapping
+    windows, so an input can take the gradient of up to four outputs."""
+    rng = np.random.default_rng(40 + H)
+    x = rng.permutation(2 * H * W * 3).reshape(2, H, W, 3).astype(np.float64) / 11.0  # distinct
+    y, idx = ly.maxpool3s2(x)
+    assert y.shape[1:3] == ((H - 1) // 2 + 1, (W - 1) // 2 + 1)
+    dy = rng.standard_normal(y.shape)
+    dx = ly.maxpool3s2_vjp(x.shape, idx, dy)
+    xt = torch.tensor(x.transpose(0, 3, 1, 2), requires_grad=True)
+    yt = F.max_pool2d(xt, 3, stride=2, padding=1)
+    yt.backward(torch.tensor(dy.transpose(0, 3, 1, 2)))
+    np.testing.assert_array_equal(y, yt.detach().numpy().transpose(0, 2, 3, 1))
+    np.testing.assert_allclose(dx, xt.grad.numpy().transpose(0, 2, 3, 1), rtol=1e-15, atol=1e-15)
+    _fd_vs_vjp(lambda x_: ly.maxpool3s2(x_)[0], [x], 0, dy, dx, h=1e-7)
+
+
+def test_maxpool3s2_ties_and_padding():
+    # output (0, 0) sees rows/cols -1..1: the padding never wins, even over negatives
+    # a 2x2 input has one output, whose window covers rows/cols -1..1
+    x = -np.ones((1, 2, 2, 2))
+    x[0, :, :, 1] = [[0.0, 2.0], [2.0, 0.0]]
+    y, idx = ly.maxpool3s2(x)
+    assert y.shape == (1, 1, 1, 2) and y[0, 0, 0].tolist() == [-1.0, 2.0]
+    # window positions are row-major over rows -1..1, cols -1..1: (0, 0) is index 4,
+    # (0, 1) index 5, (1, 0) index 7; channel 1 ties (0, 1) and (1, 0) -> (0, 1)
+    assert idx[0, 0, 0].tolist() == [4, 5]
+    dx = ly.maxpool3s2_vjp(x.shape, idx, np.ones(y.shape))
+    assert dx[0, :, :, 0].tolist() == [[1.0, 0.0], [0.0, 0.0]]
+    assert dx[0, :, :, 1].tolist() == [[0.0, 1.0], [0.0, 0.0]]
+    # overlapping windows: on a 3x3 input the pixel (0, 1) is in the windows of
+    # outputs (0, 0) and (0, 1), and takes both gradients when it is both maxima
+    x3 = np.zeros((1, 3, 3, 1))
+    x3[0, 0, 1, 0] = 5.0
+    y3, idx3 = ly.maxpool3s2(x3)
+    dx3 = ly.maxpool3s2_vjp(x3.shape, idx3, np.ones(y3.shape))
+    assert dx3[0, 0, 1, 0] == 2.0 and dx3.sum() == 4.0

@@ -66,6 +66,41 @@ def test_full_vgg16_matches_torch():
         assert rel_l2(a, b) < 1e-11
 
 
+def test_full_resnet101_matches_torch():
+    """The whole ResNet-101 (strided stem, 3x3 stride-2 pool, 33 bottlenecks
+    with strided first blocks and projection shortcuts, classifier) against
+    torch float64 autograd, at a 64 x 64 input.  (At 32 x 32 the last group's
+    BNs see two samples per channel and the 33 blocks amplify rounding-order
+    differences to ~1e-3: a conditioning effect, not a disagreement; every
+    shallower variant agrees to ~1e-12 at that size.)"""
+    layers = wl.resnet101_layers()
+    w = wl.StageWorkload("resnet101_full", layers, 2, 1, (64, 64, 3), 4, 0, 0, 0, minibatches=1)
+    inp = wl.stage_inputs(w)
+    st = oracle.Stage(layers)
+    x, lab = inp.xs[0][0], inp.labels[0][0]
+    y, loss, _ = st.forward(inp.params, x, lab, 2)
+    dx, grads, _ = st.backward(inp.params, x, None, lab, 2)
+    yt, losst, dxt, gt = torch_ref.fwd_bwd(layers, inp.params, x, None, lab, 2)
+    assert rel_l2(y.reshape(-1), np.asarray(yt).reshape(-1)) < 1e-10
+    assert abs(loss - losst) < 1e-10
+    assert rel_l2(dx, dxt) < 1e-10
+    worst = max(rel_l2(a, b) for a, b in zip(grads, gt))
+    assert worst < 1e-10, worst
+
+
+def test_projection_bn_output_is_stored():
+    """A BN output that is not fused into a ReLU or into a later residual add
+    (the projection shortcut's BN) is a stored activation: rounded to the
+    storage type; the main path's last BN, which takes in the shortcut, is not."""
+    layers = wl.resnet101_layers(blocks=(1, 1, 1, 1))
+    st = oracle.Stage(layers, "bf16")
+    stored = sorted(i for i, v in st.bn_stored.items() if v)
+    proj = [i for i, L in enumerate(layers) if L["kind"] == "bn" and layers[L["inputs"][0]]["kind"] == "conv"
+            and layers[L["inputs"][0]]["k"] == 1 and
+            any(M["kind"] == "add" and M["inputs"][1] == i for M in layers)]
+    assert stored == proj and len(proj) == 4
+
+
 @pytest.mark.parametrize("name", ["tiny_mlp", "vgg16_stage0"])
 def test_accumulated_gradient_equals_full_minibatch_gradient(name):
     """Sec. III-A: gradients accumulated over the T micro-batches of a mini-batch

@@ -46,8 +46,8 @@ class _Builder:
     def linear(self, x, cin, cout, bias=True):
         return self.add(kind="linear", inputs=[x], cin=cin, cout=cout, bias=bias)
 
-    def conv(self, x, cin, cout, k, bias=False):
-        return self.add(kind="conv", inputs=[x], cin=cin, cout=cout, k=k, bias=bias)
+    def conv(self, x, cin, cout, k, bias=False, stride=1):
+        return self.add(kind="conv", inputs=[x], cin=cin, cout=cout, k=k, bias=bias, stride=stride)
 
     def bn(self, x, c):
         return self.add(kind="bn", inputs=[x], cin=c, cout=c)
@@ -55,8 +55,8 @@ class _Builder:
     def relu(self, x):
         return self.add(kind="relu", inputs=[x])
 
-    def conv_bn_relu(self, x, cin, cout, k):
-        return self.relu(self.bn(self.conv(x, cin, cout, k), cout))
+    def conv_bn_relu(self, x, cin, cout, k, stride=1):
+        return self.relu(self.bn(self.conv(x, cin, cout, k, stride=stride), cout))
 
 
 def mlp_stage_layers(d_in=256, d_hidden=256, classes=10) -> List[dict]:
@@ -109,6 +109,37 @@ def split_layers(layers: List[dict], first: List[int]) -> List[List[dict]]:
             stage.append(L)
         out.append(stage)
     return out
+
+
+def resnet101_layers(classes=200, blocks=(3, 4, 23, 3)) -> List[dict]:
+    """ResNet-101 (Sec. IV-B's Tiny ImageNet model, inputs scaled to 224 x 224):
+    a 7x7 stride-2 stem convolution with BN and ReLU, a 3x3 stride-2 max pool,
+    four groups of bottleneck blocks (1x1, 3x3, 1x1 with 4x expansion; BN after
+    each convolution) whose first block strides by 2 on its 3x3 convolution
+    (groups 2-4) and adds a 1x1 projection with BN on the shortcut, then global
+    average pooling, the linear classifier and the cross-entropy loss.  Within
+    a block the projection comes before the third convolution, so that the
+    third BN takes in the shortcut (BN + add + ReLU)."""
+    b = _Builder()
+    x = b.conv_bn_relu(-1, 3, 64, 7, stride=2)
+    x = b.add(kind="maxpool3s2", inputs=[x])
+    cin = 64
+    for g, nblk in enumerate(blocks):
+        mid = 64 << g
+        for j in range(nblk):
+            stride = 2 if (j == 0 and g > 0) else 1
+            y = b.conv_bn_relu(x, cin, mid, 1)
+            y = b.conv_bn_relu(y, mid, mid, 3, stride=stride)
+            sc = x
+            if j == 0:
+                sc = b.bn(b.conv(x, cin, 4 * mid, 1, stride=stride), 4 * mid)
+            y = b.bn(b.conv(y, mid, 4 * mid, 1), 4 * mid)
+            x = b.relu(b.add(kind="add", inputs=[y, sc]))
+            cin = 4 * mid
+    g_ = b.add(kind="gap", inputs=[x])
+    z = b.linear(g_, cin, classes)
+    b.add(kind="softmax_ce", inputs=[z], classes=classes)
+    return b.layers
 
 
 def resnet_stage_layers(blocks=8, c=512, mid=128) -> List[dict]:

@@ -249,24 +249,29 @@ def time_interleaved(args, minibatches=6):
                     "bellwether and direction, updates kept separate from predictions"}
 
 
-def time_partitioned(args, stages=4, steps=10, warmup=3):
-    """VGG-16 for 32x32 inputs split into `stages` stages by the paper's
-    partition rule (xpipe_partition), each stage trained on its own as its GPU
-    would (micro-batch 32, T = 4, bf16: T forwards, T backwards with
-    recomputation, Adam fused with the next predictions).  Reports each
-    stage's step time and the pipeline's steady-state throughput bound, the
-    slowest stage's (synthetic inputs and upstream gradients of each stage's
-    shapes)."""
+def time_partitioned(args, net, stages=4, steps=10, warmup=3):
+    """A whole network split into `stages` stages by the paper's partition rule
+    (xpipe_partition), each stage trained on its own as its GPU would (T
+    forwards, T backwards with recomputation, Adam fused with the next
+    predictions; bf16).  Reports each stage's step time and the pipeline's
+    steady-state throughput bound, the slowest stage's (synthetic inputs and
+    upstream gradients of each stage's shapes).  VGG-16: CIFAR-10 images
+    (32 x 32), micro-batch 32, T = 4 (mini-batch 128).  ResNet-101: Tiny
+    ImageNet images scaled to 224 x 224, 200 classes, micro-batch 100 (the
+    paper's 4-GPU setting), T = 4."""
     import numpy as np
     import torch
     import paper_1911_04610_amd as xp
     import workloads as wl
-    layers = wl.vgg16_layers()
+    if net == "vgg16":
+        layers, in_shape, mb, T = wl.vgg16_layers(), (32, 32, 3), 32, 4
+        model = "vgg16 (32x32 inputs, 13 conv + linear)"
+    else:
+        layers, in_shape, mb, T = wl.resnet101_layers(), (224, 224, 3), 100, 4
+        model = "resnet101 (224x224 inputs, 200 classes, 104 conv + linear)"
     first = xp.xpipe_partition(layers, stages)
     parts = wl.split_layers(layers, first)
-    mb, T = 32, 4
     rng = np.random.default_rng(wl.PAPER_SEED + 7)
-    in_shape = (32, 32, 3)
     res = []
     hp = xp.Hyper()
     for k, p in enumerate(parts):
@@ -274,11 +279,10 @@ def time_partitioned(args, stages=4, steps=10, warmup=3):
         st.set_flat(st.W, wl.init_params(p, rng))
         n, H, W_, C = st.out_shape
         last = k == len(parts) - 1
-        x = torch.from_numpy(rng.standard_normal((mb,) + in_shape).astype(np.float32)).cuda().to(torch.bfloat16)
+        x = torch.randn((mb,) + tuple(in_shape), device="cuda").to(torch.bfloat16)
         y = torch.empty((n, H, W_, C), dtype=torch.bfloat16, device="cuda")
-        dy = None if last else torch.from_numpy(
-            (1e-2 * rng.standard_normal((n, H, W_, C))).astype(np.float32)).cuda().to(torch.bfloat16)
-        lab = torch.from_numpy(rng.integers(0, 10, mb).astype(np.int32)).cuda() if last else None
+        dy = None if last else (1e-2 * torch.randn((n, H, W_, C), device="cuda")).to(torch.bfloat16)
+        lab = torch.from_numpy(rng.integers(0, C if last else 10, mb).astype(np.int32)).cuda() if last else None
         loss = torch.zeros(1, dtype=torch.float32, device="cuda") if last else None
         dx = torch.empty_like(x) if k > 0 else None
         st.xpipe_predict_weights(xp.FWD, 1, hp, 0)
@@ -304,123 +308,17 @@ def time_partitioned(args, stages=4, steps=10, warmup=3):
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / steps
         res.append({"layers": [first[k], first[k + 1]], "in_shape": list(in_shape),
-                    "params": int(st.P), "ms_per_step": round(ms, 4)})
+                    "params": int(st.P), "ms_per_step": round(ms, 4),
+                    "samples_per_s": round(mb * T / (ms / 1e3), 1)})
         in_shape = (H, W_, C)
-        del st
+        del st, x, y, dy, dx
+        torch.cuda.empty_cache()
     slow = max(r["ms_per_step"] for r in res)
-    return {"model": "vgg16 (32x32 inputs, 13 conv + linear)", "stages": stages, "micro_batch": mb, "T": T,
+    return {"model": model, "stages": stages, "micro_batch": mb, "T": T,
             "dtype": "bf16", "per_stage": res,
             "pipeline_samples_per_s_bound": round(mb * T / (slow / 1e3), 1),
             "note": "each stage timed alone on this GPU as its pipeline GPU would run it; the "
                     "pipeline's steady-state rate is bounded by its slowest stage"}
-
-
-def event_offset_us(reps=300):
-    """Per-launch offset of a start/stop event pair around one kernel: the
-    bracketed time of a ~10 us kernel minus its period when launched back to
-    back (then the kernel's own duration, as it is longer than the launch
-    floor).  Subtracted from the per-kernel event averages so they measure
-    what the kernel-trace profiler reports."""
-    import torch
-    t = torch.zeros(1 << 23, device="cuda")
-    s = torch.cuda.current_stream()
-    for _ in range(20):
-        t.add_(1)
-    torch.cuda.synchronize()
-    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-             for _ in range(reps)]
-    for a, b in pairs:
-        a.record(s)
-        t.add_(1)
-        b.record(s)
-    torch.cuda.synchronize()
-    bracket = sum(a.elapsed_time(b) for a, b in pairs) / reps * 1e3
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record(s)
-    for _ in range(reps):
-        t.add_(1)
-    b.record(s)
-    torch.cuda.synchronize()
-    period = a.elapsed_time(b) / reps * 1e3
-    return max(0.0, bracket - period), bracket, period
-
-
-def time_sweep(n, steps):
-    """Prediction and Adam over n flat fp32 parameters at t = 100."""
-    import numpy as np
-    import torch
-    import paper_1911_04610_amd as xp
-    import workloads as wl
-    s = wl.flat_state(n)
-    W, m, v, G = (torch.from_numpy(a).cuda() for a in (s.W, s.m, s.v, s.G))
-    out = torch.empty_like(W)
-    pf, pb = torch.empty_like(W), torch.empty_like(W)
-    hp = xp.Hyper()
-    res = {}
-
-    def timed(fn, reps):
-        fn()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(reps):
-            fn()
-        b.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / reps
-
-    reps = max(3, steps)
-    for sv in (0, 1, 2, 3, 7):
-        ms = timed(lambda: xp.xpipe_predict_flat(W, m, v, out, None, sv, hp, 100), reps)
-        res[f"predict_s{sv}"] = {"ms": ms, "GB_s": 16.0 * n / ms / 1e6}
-    ms = timed(lambda: xp.xpipe_adam_flat(W, m, v, G, hp, 100, False), reps)
-    res["adam"] = {"ms": ms, "GB_s": 28.0 * n / ms / 1e6}
-    ms = timed(lambda: xp.xpipe_adam_flat(W, m, v, G, hp, 100, True, pf, 2, pb, 1), reps)
-    res["adam_zero_grad_2pred"] = {"ms": ms, "GB_s": 40.0 * n / ms / 1e6}
-    # the other update rules with Adam-moment prediction, fused the same way:
-    # momentum SGD 36 B/param (W, buf, m, v, G in; W, buf, m, v out) + zero + 2 predictions
-    # = 48; RMSProp adds the squared average (44 + 12 = 56)
-    buf, sq = (torch.from_numpy(a).cuda() for a in wl.rule_state(n))
-    rule = xp.Rule(rule=xp.RULE_MOMENTUM_SGD, lr=1e-2, momentum=0.9, weight_decay=5e-4)
-    ms = timed(lambda: xp.xpipe_rule_flat(W, buf, None, m, v, G, rule, hp, 100, True, pf, 2, pb, 1), reps)
-    res["momentum_sgd_zero_grad_2pred"] = {"ms": ms, "GB_s": 48.0 * n / ms / 1e6}
-    rule = xp.Rule(rule=xp.RULE_RMSPROP, lr=1e-4, momentum=0.9, alpha=0.99, eps=1e-8)
-    ms = timed(lambda: xp.xpipe_rule_flat(W, buf, sq, m, v, G, rule, hp, 100, True, pf, 2, pb, 1), reps)
-    res["rmsprop_zero_grad_2pred"] = {"ms": ms, "GB_s": 56.0 * n / ms / 1e6}
-    del W, m, v, G, out, pf, pb, buf, sq
-    torch.cuda.empty_cache()
-    return res
-
-
-def measured_peaks():
-    """Attainable peaks on this GPU from the library's probes: a 1 GiB 16-byte
-    copy (read + write bytes) and back-to-back bf16 MFMAs on registers."""
-    import torch
-    import paper_1911_04610_amd as xp
-
-    def timed(fn, reps=5):
-        fn()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(reps):
-            fn()
-        b.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / reps
-
-    n = 1 << 30
-    src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
-    dst = torch.empty_like(src)
-    ms = timed(lambda: xp.xpipe_probe_copy(src, dst))
-    copy_gbs = 2.0 * n / (ms / 1e3) / 1e9
-    del src, dst
-    waves, iters = 256 * 4 * 2, 4096
-    out = torch.empty(waves, dtype=torch.float32, device="cuda")
-    ms = timed(lambda: xp.xpipe_probe_mfma(out, iters))
-    tflops = waves * iters * 8 * 32768.0 / (ms / 1e3) / 1e12
-    return {"hbm_copy_GB_s": round(copy_gbs, 1), "mfma_bf16_TFLOP_s": round(tflops, 1),
-            "copy_bytes": 2 * n, "mfma": "v_mfma_f32_32x32x16_bf16, %d waves x %d x 8" % (waves, iters)}
 
 
 def vendor_reference(reps=50):
@@ -608,7 +506,8 @@ def main():
                                         for k, v in sw.items()}}
     if not args.no_sweep:
         out["interleaved_schedule"] = time_interleaved(args)
-        out["vgg16_partitioned"] = time_partitioned(args)
+        out["vgg16_partitioned"] = time_partitioned(args, "vgg16")
+        out["resnet101_partitioned"] = time_partitioned(args, "resnet101")
         out["vendor_reference"] = vendor_reference()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.dtype)

@@ -77,8 +77,8 @@ typedef enum {
  * Activations are NHWC; a [n, C] tensor is NHWC with H = W = 1. */
 typedef enum {
   XPIPE_LINEAR = 0,     /* y = x W^T + b; W [cout][cin]; input must have H = W = 1 */
-  XPIPE_CONV = 1,       /* k x k, stride 1, zero padding k/2, cross-correlation;
-                           W [cout][k][k][cin] (KRSC) */
+  XPIPE_CONV = 1,       /* k x k, stride 1 or 2, zero padding k/2, cross-correlation;
+                           output floor((H - 1) / stride) + 1; W [cout][k][k][cin] (KRSC) */
   XPIPE_BN = 2,         /* batch norm with the micro-batch's mean and biased
                            variance, eps 1e-5; params gamma[C], beta[C] */
   XPIPE_RELU = 3,       /* max(x, 0); derivative 0 at 0 */
@@ -88,9 +88,12 @@ typedef enum {
   XPIPE_AVGPOOL3 = 6,   /* 3x3 window, stride 1, zero padding 1, divisor 9 */
   XPIPE_GAP = 7,        /* mean over H and W: [n,H,W,C] -> [n,1,1,C] */
   XPIPE_CONCAT = 8,     /* channel concatenation of 2..4 inputs, in order */
-  XPIPE_SOFTMAX_CE = 9  /* loss = sum over the micro-batch of -log softmax(x)[label],
+  XPIPE_SOFTMAX_CE = 9, /* loss = sum over the micro-batch of -log softmax(x)[label],
                            divided by the mini-batch size N = T * micro_batch;
                            must be the last layer */
+  XPIPE_MAXPOOL3S2 = 10 /* 3x3 window, stride 2, padding 1 (never chosen), output
+                           floor((H - 1) / 2) + 1; gradient to the first maximum in
+                           row-major window order (ResNet-101's stem) */
 } xpipe_layer_kind;
 
 #define XPIPE_MAX_INPUTS 4
@@ -103,6 +106,7 @@ typedef struct {
   int32_t k;                          /* CONV kernel size (odd, 1..7) */
   int32_t has_bias;                   /* LINEAR, CONV */
   int32_t classes;                    /* SOFTMAX_CE: number of classes (= its input channels) */
+  int32_t stride;                     /* CONV: 1 or 2 (0 reads as 1); others 0 or 1 */
 } xpipe_layer_desc;
 
 /* Optimizer and prediction hyper-parameters (Sec. IV-C: gamma 0.9,

@@ -30,7 +30,7 @@ PRED_EQ3, PRED_ADAMDIR, PRED_LITERAL = 0, 1, 2
 RULE_MOMENTUM_SGD, RULE_RMSPROP = 1, 2
 ROUND_HALF_UP, ROUND_HALF_EVEN, ROUND_HALF_DOWN = 0, 1, 2
 KINDS = {"linear": 0, "conv": 1, "bn": 2, "relu": 3, "add": 4, "maxpool2": 5, "avgpool3": 6,
-         "gap": 7, "concat": 8, "softmax_ce": 9}
+         "gap": 7, "concat": 8, "softmax_ce": 9, "maxpool3s2": 10}
 MAX_INPUTS = 4
 
 
@@ -44,7 +44,7 @@ class LayerDesc(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("n_inputs", ctypes.c_int32),
                 ("inputs", ctypes.c_int32 * MAX_INPUTS), ("cin", ctypes.c_int32),
                 ("cout", ctypes.c_int32), ("k", ctypes.c_int32), ("has_bias", ctypes.c_int32),
-                ("classes", ctypes.c_int32)]
+                ("classes", ctypes.c_int32), ("stride", ctypes.c_int32)]
 
 
 class HParams(ctypes.Structure):
@@ -171,6 +171,7 @@ def layer_descs(layers: Sequence[dict]):
         d.k = int(L.get("k", 1))
         d.has_bias = int(bool(L.get("bias", False)))
         d.classes = int(L.get("classes", 0))
+        d.stride = int(L.get("stride", 1))
     return arr
 
 

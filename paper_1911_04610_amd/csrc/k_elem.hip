@@ -967,6 +967,156 @@ __global__ __launch_bounds__(256) void k_avgpool3_v(PoolArgs a, const T* src, in
   }
 }
 
+// 3x3 / stride 2 / padding 1 max pool over groups of N channels (16-byte
+// chunks, or single channels).  Padding is never chosen: the window centre
+// (2ho, 2wo) is always inside.  Ties go to the first maximum in row-major
+// window order (strict > while scanning).
+template <typename T, int N>
+XP_DEV void ldn(const T* p, double* v) {
+  if constexpr (N == VT<T>::N) vld(p, v);
+  else
+#pragma unroll
+    for (int e = 0; e < N; ++e) v[e] = ldd(p + e);
+}
+template <typename T, int N>
+XP_DEV void stn(T* p, const double* v) {
+  if constexpr (N == VT<T>::N) vst(p, v);
+  else
+#pragma unroll
+    for (int e = 0; e < N; ++e) std_(p + e, v[e]);
+}
+
+template <typename T, int N>
+__global__ __launch_bounds__(256) void k_maxpool3s2_fwd(PoolArgs a, int Ho, int Wo) {
+  const int groups = a.C / N;
+  int64_t it = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (it >= (int64_t)a.nb * Ho * Wo * groups) return;
+  const int g = (int)(it % groups);
+  it /= groups;
+  const int wo = (int)(it % Wo);
+  it /= Wo;
+  const int ho = (int)(it % Ho), n = (int)(it / Ho);
+  const int c0 = g * N;
+  const T* X = (const T*)a.x;
+  double best[N];
+  bool have = false;
+  for (int r = 0; r < 3; ++r) {
+    const int h = 2 * ho - 1 + r;
+    if (h < 0 || h >= a.H) continue;
+    for (int q = 0; q < 3; ++q) {
+      const int w = 2 * wo - 1 + q;
+      if (w < 0 || w >= a.W) continue;
+      double v[N];
+      ldn<T, N>(X + ((size_t)(n * a.H + h) * a.W + w) * a.ldx + c0, v);
+#pragma unroll
+      for (int e = 0; e < N; ++e)
+        if (!have || v[e] > best[e]) best[e] = v[e];
+      have = true;
+    }
+  }
+  stn<T, N>((T*)a.out + ((size_t)(n * Ho + ho) * Wo + wo) * a.ldo + c0, best);
+}
+
+// backward: each input pixel gathers, in (ho, wo) order, the output gradients
+// of the (at most four) windows that contain it and chose it
+template <typename T, int N>
+__global__ __launch_bounds__(256) void k_maxpool3s2_bwd(PoolArgs a, int Ho, int Wo) {
+  const int groups = a.C / N;
+  int64_t it = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (it >= (int64_t)a.nb * a.H * a.W * groups) return;
+  const int g = (int)(it % groups);
+  it /= groups;
+  const int w = (int)(it % a.W);
+  it /= a.W;
+  const int h = (int)(it % a.H), n = (int)(it / a.H);
+  const int c0 = g * N;
+  const T* X = (const T*)a.x;
+  const T* DY = (const T*)a.dy;
+  double acc[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) acc[e] = 0.0;
+  const int ho1 = min((h + 1) / 2, Ho - 1), wo1 = min((w + 1) / 2, Wo - 1);
+  for (int ho = h / 2; ho <= ho1; ++ho)
+    for (int wo = w / 2; wo <= wo1; ++wo) {
+      double best[N];
+      int arg[N];
+      bool have = false;
+      for (int r = 0; r < 3; ++r) {
+        const int hh = 2 * ho - 1 + r;
+        if (hh < 0 || hh >= a.H) continue;
+        for (int q = 0; q < 3; ++q) {
+          const int ww = 2 * wo - 1 + q;
+          if (ww < 0 || ww >= a.W) continue;
+          double v[N];
+          ldn<T, N>(X + ((size_t)(n * a.H + hh) * a.W + ww) * a.ldx + c0, v);
+#pragma unroll
+          for (int e = 0; e < N; ++e)
+            if (!have || v[e] > best[e]) {
+              best[e] = v[e];
+              arg[e] = hh * a.W + ww;
+            }
+          have = true;
+        }
+      }
+      double d[N];
+      ldn<T, N>(DY + ((size_t)(n * Ho + ho) * Wo + wo) * a.lddy + c0, d);
+#pragma unroll
+      for (int e = 0; e < N; ++e)
+        if (arg[e] == h * a.W + w) acc[e] += d[e];
+    }
+  const size_t r = (size_t)(n * a.H + h) * a.W + w;
+  if (a.mask) {
+    double m[N];
+    ldn<T, N>((const T*)a.mask + r * a.ldm + c0, m);
+#pragma unroll
+    for (int e = 0; e < N; ++e)
+      if (!(m[e] > 0.0)) acc[e] = 0.0;
+  }
+  T* p = (T*)a.out + r * a.ldo + c0;
+  if (a.accumulate) {
+    double o[N];
+    ldn<T, N>(p, o);
+#pragma unroll
+    for (int e = 0; e < N; ++e) acc[e] += o[e];
+  }
+  stn<T, N>(p, acc);
+}
+
+template <typename T>
+static hipError_t maxpool3s2_go(const PoolArgs& a, bool bwd, hipStream_t s) {
+  const int Ho = (a.H - 1) / 2 + 1, Wo = (a.W - 1) / 2 + 1;
+  constexpr int V = VT<T>::N;
+  const bool vec = vec_ok<T>(a.C, {{a.x, a.ldx}, {a.out, a.ldo}, {a.dy, a.lddy}, {a.mask, a.ldm}});
+  const int64_t pix = bwd ? (int64_t)a.nb * a.H * a.W : (int64_t)a.nb * Ho * Wo;
+  const int64_t threads = pix * (vec ? a.C / V : a.C);
+  const unsigned blocks = (unsigned)((threads + 255) / 256);
+  const double esz = sizeof(T);
+  // algorithmic bytes: forward reads x once and writes y; backward reads x, dy
+  // (and mask / old dx) and writes dx
+  const double in_b = (double)a.nb * a.H * a.W * a.C * esz, out_b = (double)a.nb * Ho * Wo * a.C * esz;
+  const double bytes = bwd ? 2 * in_b + out_b + (a.mask ? in_b : 0) + (a.accumulate ? in_b : 0)
+                           : in_b + out_b;
+  const char* name = bwd ? (sizeof(T) == 2 ? "k_maxpool3s2_bwd<bf16>" : "k_maxpool3s2_bwd<f32>")
+                         : (sizeof(T) == 2 ? "k_maxpool3s2_fwd<bf16>" : "k_maxpool3s2_fwd<f32>");
+  if (vec) {
+    if (bwd) XP_LAUNCH(name, bytes, (k_maxpool3s2_bwd<T, V>), dim3(blocks), dim3(256), 0, s, a, Ho, Wo);
+    else XP_LAUNCH(name, bytes, (k_maxpool3s2_fwd<T, V>), dim3(blocks), dim3(256), 0, s, a, Ho, Wo);
+  } else {
+    if (bwd) XP_LAUNCH(name, bytes, (k_maxpool3s2_bwd<T, 1>), dim3(blocks), dim3(256), 0, s, a, Ho, Wo);
+    else XP_LAUNCH(name, bytes, (k_maxpool3s2_fwd<T, 1>), dim3(blocks), dim3(256), 0, s, a, Ho, Wo);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_maxpool3s2_fwd(int dtype, const PoolArgs& a, hipStream_t s) {
+  if (a.nb <= 0 || a.H <= 0 || a.W <= 0 || a.C <= 0) return hipSuccess;
+  return dtype == DT_BF16 ? maxpool3s2_go<bf16_t>(a, false, s) : maxpool3s2_go<float>(a, false, s);
+}
+hipError_t launch_maxpool3s2_bwd(int dtype, const PoolArgs& a, hipStream_t s) {
+  if (a.nb <= 0 || a.H <= 0 || a.W <= 0 || a.C <= 0) return hipSuccess;
+  return dtype == DT_BF16 ? maxpool3s2_go<bf16_t>(a, true, s) : maxpool3s2_go<float>(a, true, s);
+}
+
 // Global average pool, two launches: per (image, pixel split) partial sums of
 // every channel (fixed order: strided per thread, then the row groups in
 // order), then per (image, channel) the splits in order, divided by H*W.

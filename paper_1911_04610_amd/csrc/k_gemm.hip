@@ -99,7 +99,9 @@ XP_DEV int xcd_tile(int l, int G) {
   return x * per + (x < rem ? x : rem) + q;
 }
 
-template <typename T, int BM, int BN, int WM, int WN, bool FLAT, int KS, int PF>
+// GM selects the gather: 0 stride 1 (rows = input grid), 1 strided forward,
+// 2 strided data gradient (see ConvArgs)
+template <typename T, int BM, int BN, int WM, int WN, bool FLAT, int KS, int PF, int GM>
 __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
   constexpr int NT = WM * WN * 64;  // threads: one wave64 per wave tile
   using MTT = MT<T>;
@@ -130,7 +132,11 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int H = a.H, W = a.W, C = a.C, S = a.S, pad = a.pad;
-  const int M = a.nb * H * W;
+  // the GEMM rows: the input grid for stride 1, else the Ho x Wo grid
+  const int Ho = GM ? a.Ho : H, Wo = GM ? a.Wo : W;
+  const int sd = GM ? a.stride : 1;
+  const int M = a.nb * Ho * Wo;
+  const int Min = a.nb * H * W;  // pixels of x
   const int K = a.R * S * C;
   // logical tile (row tile tm, column tile tn), column tiles fastest
   const int tlin = xcd_tile(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x * gridDim.y);
@@ -151,10 +157,10 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
     int m = m0 + a_row[i];
     a_valid[i] = a_slot[i] && m < M;
     int mm = a_valid[i] ? m : 0;
-    a_img[i] = mm / (H * W);
-    int rem = mm - a_img[i] * H * W;
-    a_h[i] = rem / W;
-    a_w[i] = rem - a_h[i] * W;
+    a_img[i] = mm / (Ho * Wo);
+    int rem = mm - a_img[i] * Ho * Wo;
+    a_h[i] = rem / Wo;
+    a_w[i] = rem - a_h[i] * Wo;
   }
   int b_row[B_PER], b_kc[B_PER];
   bool b_slot[B_PER], b_valid[B_PER];
@@ -176,20 +182,36 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
   constexpr uint32_t OUT_OF_RANGE = 0x80000000u;
   uint32_t a_off[A_PER], b_off[B_PER], a_hm[A_PER], a_wm[A_PER];
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)x, (short)0, (int)((((size_t)(M - 1)) * a.ldx + C) * sizeof(T)), 0x00020000);
+      (void*)x, (short)0, (int)((((size_t)(Min - 1)) * a.ldx + C) * sizeof(T)), 0x00020000);
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
       (void*)w, (short)0, (int)((size_t)a.N * K * sizeof(T)), 0x00020000);
   if constexpr (!FLAT) {
 #pragma unroll
     for (int i = 0; i < A_PER; ++i) {
-      a_off[i] = (uint32_t)((((size_t)(a_img[i] * H + a_h[i]) * W + a_w[i]) * a.ldx + a_kc[i] * VEC) *
+      // base pixel of the row's taps; a tap adds (r - pad, q - pad) (GM 0, 1) or
+      // (-(r / sd), -(q / sd)) (GM 2); 32-bit wrap-around makes a base one row
+      // past the image harmless, since only in-image taps use it
+      const int bh = GM == 2 ? (a_h[i] + pad) / sd : a_h[i] * sd;
+      const int bw = GM == 2 ? (a_w[i] + pad) / sd : a_w[i] * sd;
+      a_off[i] = (uint32_t)((((size_t)(a_img[i] * H + bh) * W + bw) * a.ldx + a_kc[i] * VEC) *
                             sizeof(T));
       uint32_t hm = 0, wm = 0;
       if (a_valid[i]) {
-        for (int r = 0; r < a.R; ++r)
-          hm |= (uint32_t)((unsigned)(a_h[i] + r - pad) < (unsigned)H) << r;
-        for (int q = 0; q < S; ++q)
-          wm |= (uint32_t)((unsigned)(a_w[i] + q - pad) < (unsigned)W) << q;
+        if constexpr (GM == 2) {
+          for (int r = 0; r < a.R; ++r) {
+            const int t = a_h[i] + pad - r;
+            hm |= (uint32_t)(t >= 0 && t % sd == 0 && t / sd < H) << r;
+          }
+          for (int q = 0; q < S; ++q) {
+            const int t = a_w[i] + pad - q;
+            wm |= (uint32_t)(t >= 0 && t % sd == 0 && t / sd < W) << q;
+          }
+        } else {
+          for (int r = 0; r < a.R; ++r)
+            hm |= (uint32_t)((unsigned)(bh + r - pad) < (unsigned)H) << r;
+          for (int q = 0; q < S; ++q)
+            wm |= (uint32_t)((unsigned)(bw + q - pad) < (unsigned)W) << q;
+        }
       }
       a_hm[i] = hm;
       a_wm[i] = wm;
@@ -215,7 +237,9 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
     if constexpr (!FLAT) {
       (void)kb;
       const int crem = C - lcb * BK;  // channels left in this tap from this block on
-      const int dx = (((lr - pad) * W + (lq - pad)) * a.ldx + lcb * BK) * (int)sizeof(T);
+      const int tr_ = GM == 2 ? -(lr / sd) : lr - pad;
+      const int tq_ = GM == 2 ? -(lq / sd) : lq - pad;
+      const int dx = ((tr_ * W + tq_) * a.ldx + lcb * BK) * (int)sizeof(T);
       const uint32_t dw = (uint32_t)((lrs * C + lcb * BK) * (int)sizeof(T));
 #pragma unroll
       for (int i = 0; i < A_PER; ++i) {
@@ -250,8 +274,19 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
           if (a_valid[i] && k < K) {
             int rs = k / C, c = k - rs * C;
             int r = rs / S, s = rs - r * S;
-            int hh = a_h[i] + r - pad, ww = a_w[i] + s - pad;
-            if (hh >= 0 && hh < H && ww >= 0 && ww < W)
+            int hh, ww;
+            bool in;
+            if constexpr (GM == 2) {
+              const int th = a_h[i] + pad - r, tw = a_w[i] + pad - s;
+              in = th >= 0 && tw >= 0 && th % sd == 0 && tw % sd == 0;
+              hh = th / sd;
+              ww = tw / sd;
+            } else {
+              hh = a_h[i] * sd + r - pad;
+              ww = a_w[i] * sd + s - pad;
+              in = true;
+            }
+            if (in && hh >= 0 && hh < H && ww >= 0 && ww < W)
               val = x[((size_t)(a_img[i] * H + hh) * W + ww) * a.ldx + c];
           }
           vals[e] = val;
@@ -697,7 +732,10 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int H = a.H, W = a.W, C = a.C, S = a.S, pad = a.pad, N = a.N;
-  const int HW = H * W;
+  // dz pixels: the input grid, or the Ho x Wo grid of a strided convolution
+  const int sd = a.stride > 1 ? a.stride : 1;
+  const int Wo = sd > 1 ? a.Wo : W;
+  const int HW = (sd > 1 ? a.Ho : H) * Wo;
   const int M = a.nb * HW;
   const int K = a.R * S * C;
   const int n0 = blockIdx.x * BM, k0 = blockIdx.y * BN;
@@ -764,7 +802,9 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
         int m = mb + b_p[i] * RPT + u;
         uint4 v = make_uint4(0, 0, 0, 0);
         if (b_slot[i] && m < mend) {
-          int img = m / HW, rem = m - img * HW, h = rem / W, ww0 = rem - h * W;
+          int img = m / HW, rem = m - img * HW, h = rem / Wo, ww0 = rem - h * Wo;
+          h *= sd;
+          ww0 *= sd;
           if constexpr (!FLAT) {
             int hh = h + b_r[i] - pad, ww = ww0 + b_s[i] - pad;
             if (b_kok[i] && hh >= 0 && hh < H && ww >= 0 && ww < W)
@@ -1225,7 +1265,7 @@ __global__ __launch_bounds__(256) void k_gather(GatherArgs a) {
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_flip(const T* __restrict__ w, T* __restrict__ wd, int N,
-                                               int R, int S, int C) {
+                                               int R, int S, int C, int flip) {
   int64_t total = (int64_t)N * R * S * C;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
        i += (int64_t)gridDim.x * blockDim.x) {
@@ -1236,7 +1276,8 @@ __global__ __launch_bounds__(256) void k_flip(const T* __restrict__ w, T* __rest
     t /= S;
     int r = (int)(t % R);
     int c = (int)(t / R);
-    wd[i] = w[(((int64_t)n * R + (R - 1 - r)) * S + (S - 1 - s)) * C + c];
+    const int rr = flip ? R - 1 - r : r, ss = flip ? S - 1 - s : s;
+    wd[i] = w[(((int64_t)n * R + rr) * S + ss) * C + c];
   }
 }
 
@@ -1267,12 +1308,15 @@ static int pick_ks_bf16(int C, int taps) {
 
 template <typename T> static const char* tname() { return sizeof(T) == 2 ? "bf16" : "f32"; }
 
-template <typename T, int BM, int BN, int WM, int WN, bool FLAT, int KS = 0, int PF = 0>
+template <typename T, int BM, int BN, int WM, int WN, bool FLAT, int KS = 0, int PF = 0, int GM = 0>
 static const char* kname(const char* base) {
   static char buf[96];
   static bool init = false;
   if (!init) {
-    if (KS)
+    if (KS && GM)
+      snprintf(buf, sizeof buf, "%s<%s,%d,%d,%d,%d,%s,%d,%d,%s>", base, tname<T>(), BM, BN, WM, WN,
+               FLAT ? "true" : "false", KS, PF, GM == 1 ? "strided" : "strided_dgrad");
+    else if (KS)
       snprintf(buf, sizeof buf, "%s<%s,%d,%d,%d,%d,%s,%d,%d>", base, tname<T>(), BM, BN, WM, WN,
                FLAT ? "true" : "false", KS, PF);
     else
@@ -1283,18 +1327,20 @@ static const char* kname(const char* base) {
   return buf;
 }
 
-template <typename T, int BM, int BN, int WM, int WN, int KS, int PF = 1>
+template <typename T, int BM, int BN, int WM, int WN, int KS, int PF = 1, int GM = 0>
 static hipError_t conv_go(const ConvArgs& a, bool flat, hipStream_t s, int* grid_rows = nullptr) {
-  int M = a.nb * a.H * a.W;
+  int M = a.nb * (GM ? a.Ho * a.Wo : a.H * a.W);
   dim3 grid((M + BM - 1) / BM, (a.N + BN - 1) / BN);
   if (grid_rows) *grid_rows = (int)grid.x;
-  double flops = 2.0 * M * (double)a.N * a.R * a.S * a.C;
+  // algorithmic work: every (row, tap) pair of the convolution once; a strided
+  // data gradient reads each output-gradient pixel once per tap
+  double flops = 2.0 * a.nb * (GM == 2 ? a.H * a.W : M / a.nb) * (double)a.N * a.R * a.S * a.C;
   if (flat)
-    XP_LAUNCH((kname<T, BM, BN, WM, WN, true, KS, PF>("k_conv_gemm")), flops,
-              (k_conv_gemm<T, BM, BN, WM, WN, true, KS, PF>), grid, dim3(WM * WN * 64), 0, s, a);
+    XP_LAUNCH((kname<T, BM, BN, WM, WN, true, KS, PF, GM>("k_conv_gemm")), flops,
+              (k_conv_gemm<T, BM, BN, WM, WN, true, KS, PF, GM>), grid, dim3(WM * WN * 64), 0, s, a);
   else
-    XP_LAUNCH((kname<T, BM, BN, WM, WN, false, KS, PF>("k_conv_gemm")), flops,
-              (k_conv_gemm<T, BM, BN, WM, WN, false, KS, PF>), grid, dim3(WM * WN * 64), 0, s, a);
+    XP_LAUNCH((kname<T, BM, BN, WM, WN, false, KS, PF, GM>("k_conv_gemm")), flops,
+              (k_conv_gemm<T, BM, BN, WM, WN, false, KS, PF, GM>), grid, dim3(WM * WN * 64), 0, s, a);
   return hipGetLastError();
 }
 
@@ -1309,6 +1355,24 @@ static hipError_t conv_dispatch(const ConvArgs& a, hipStream_t s, int* gr) {
               (reinterpret_cast<uintptr_t>(a.x) % 16) != 0 ||
               (reinterpret_cast<uintptr_t>(a.w) % 16) != 0 || !spans;
   const bool narrow = a.N <= 32;
+  if (a.tr || a.stride > 1) {
+    // strided layers (ResNet stem, first blocks, projections): general tiles
+    if constexpr (sizeof(T) == 2) {
+      if (a.tr) {
+        if (narrow) return conv_go<T, 64, 32, 2, 2, 1, 2, 2>(a, flat, s, gr);
+        return conv_go<T, 64, 64, 2, 2, 2, 2, 2>(a, flat, s, gr);
+      }
+      if (narrow) return conv_go<T, 64, 32, 2, 2, 1, 2, 1>(a, flat, s, gr);
+      return conv_go<T, 64, 64, 2, 2, 2, 2, 1>(a, flat, s, gr);
+    } else {
+      if (a.tr) {
+        if (narrow) return conv_go<T, 64, 32, 2, 2, 1, 1, 2>(a, flat, s, gr);
+        return conv_go<T, 64, 64, 2, 2, 1, 1, 2>(a, flat, s, gr);
+      }
+      if (narrow) return conv_go<T, 64, 32, 2, 2, 1, 1, 1>(a, flat, s, gr);
+      return conv_go<T, 64, 64, 2, 2, 1, 1, 1>(a, flat, s, gr);
+    }
+  }
   if constexpr (sizeof(T) == 2) {
     // From a sweep of the stage shapes on MI355X (tile, stage depth KS,
     // register prefetch depth PF)
@@ -1408,7 +1472,8 @@ template <typename T, int BM, int BN, int WM, int WN>
 static hipError_t wgrad_go(const WgradArgs& a, bool flat, hipStream_t s) {
   int K = a.R * a.S * a.C;
   dim3 grid((a.N + BM - 1) / BM, (K + BN - 1) / BN, a.splits);
-  double flops = 2.0 * a.nb * a.H * a.W * (double)a.N * K;
+  const int pix = a.stride > 1 ? a.Ho * a.Wo : a.H * a.W;
+  double flops = 2.0 * a.nb * pix * (double)a.N * K;
   if (flat)
     XP_LAUNCH((kname<T, BM, BN, WM, WN, true>("k_wgrad")), flops, (k_wgrad<T, BM, BN, WM, WN, true>),
               grid, dim3(256), 0, s, a);
@@ -1439,7 +1504,7 @@ static hipError_t wgrad_dispatch(const WgradArgs& a, hipStream_t s) {
   bool n64 = a.N <= 64, k64 = K <= 64;
   if constexpr (sizeof(T) == 2) {
     const int M = a.nb * a.H * a.W;
-    const bool chunks = !flat && (a.N % VEC) == 0 && (a.lddz % VEC) == 0 &&
+    const bool chunks = !flat && a.stride <= 1 && (a.N % VEC) == 0 && (a.lddz % VEC) == 0 &&
                         (reinterpret_cast<uintptr_t>(a.dz) % 16) == 0 &&
                         (((size_t)(M - 1)) * a.lddz + a.N) * sizeof(T) < ((size_t)1 << 31) &&
                         (((size_t)(M - 1)) * a.ldx + a.C) * sizeof(T) < ((size_t)1 << 31);
@@ -1473,17 +1538,17 @@ hipError_t launch_gather(int dtype, const GatherArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_flip_weights(int dtype, const void* w, void* wd, int N, int R, int S, int C,
-                               hipStream_t s) {
+                               hipStream_t s, int flip) {
   int64_t total = (int64_t)N * R * S * C;
   int blocks = (int)((total + 255) / 256);
   if (blocks > 4096) blocks = 4096;
   if (total <= 0) return hipSuccess;
   if (dtype == DT_BF16)
     XP_LAUNCH("k_flip<bf16>", (double)total * 4, k_flip<bf16_t>, dim3(blocks), dim3(256), 0, s,
-              (const bf16_t*)w, (bf16_t*)wd, N, R, S, C);
+              (const bf16_t*)w, (bf16_t*)wd, N, R, S, C, flip);
   else
     XP_LAUNCH("k_flip<f32>", (double)total * 8, k_flip<float>, dim3(blocks), dim3(256), 0, s,
-              (const float*)w, (float*)wd, N, R, S, C);
+              (const float*)w, (float*)wd, N, R, S, C, flip);
   return hipGetLastError();
 }
 

@@ -63,7 +63,7 @@ struct Shape {
   int64_t elems() const { return rows() * C; }
 };
 
-enum OpKind { OP_GEMM, OP_BN, OP_ELT, OP_MAXPOOL, OP_AVGPOOL, OP_GAP, OP_CONCAT, OP_CE };
+enum OpKind { OP_GEMM, OP_BN, OP_ELT, OP_MAXPOOL, OP_AVGPOOL, OP_GAP, OP_CONCAT, OP_CE, OP_MAXPOOL3 };
 
 struct Tensor {
   Shape sh;
@@ -83,7 +83,7 @@ struct Op {
   int out = -1;        // output tensor (-1 for CE)
   bool relu = false;
   // GEMM
-  int cin = 0, cout = 0, k = 1;
+  int cin = 0, cout = 0, k = 1, stride = 1;
   int64_t w_off = -1, b_off = -1;   // parameter offsets (elements)
   int64_t wd_off = -1;              // workspace bytes: flipped weights for the data gradient
   // GEMM over sibling layers that read the same input (merged launch): their
@@ -365,6 +365,8 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
         if (d.kind == XPIPE_LINEAR && (s.H != 1 || s.W != 1))
           return fail(XPIPE_EINVAL, std::string(where) + "linear input must have H = W = 1");
         if (k < 1 || k > 7 || (k % 2) == 0) return fail(XPIPE_EINVAL, std::string(where) + "bad kernel size");
+        if (d.stride < 0 || d.stride > 2 || (d.kind == XPIPE_LINEAR && d.stride > 1))
+          return fail(XPIPE_EINVAL, std::string(where) + "stride must be 1 or 2 (convolutions only)");
         if (d.cin != s.C || d.cout <= 0) return fail(XPIPE_EINVAL, std::string(where) + "channel mismatch");
         poff[i] = P;
         P += align_up((int64_t)d.cout * k * k * d.cin, PARAM_ALIGN);
@@ -373,6 +375,10 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
           P += align_up(d.cout, PARAM_ALIGN);
         }
         s.C = d.cout;
+        if (d.stride == 2) {
+          s.H = (s.H - 1) / 2 + 1;
+          s.W = (s.W - 1) / 2 + 1;
+        }
         break;
       }
       case XPIPE_BN:
@@ -396,6 +402,10 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
         s.W /= 2;
         break;
       case XPIPE_AVGPOOL3:
+        break;
+      case XPIPE_MAXPOOL3S2:
+        s.H = (s.H - 1) / 2 + 1;
+        s.W = (s.W - 1) / 2 + 1;
         break;
       case XPIPE_GAP:
         s.H = 1;
@@ -480,6 +490,7 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
         op.cin = d.cin;
         op.cout = d.cout;
         op.k = d.kind == XPIPE_LINEAR ? 1 : d.k;
+        op.stride = d.stride == 2 ? 2 : 1;
         op.w_off = poff[i];
         op.b_off = d.has_bias ? poff2[i] : -1;
         int r = single_consumer(i, XPIPE_RELU);
@@ -532,6 +543,7 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
         break;
       }
       case XPIPE_MAXPOOL2: op.kind = OP_MAXPOOL; break;
+      case XPIPE_MAXPOOL3S2: op.kind = OP_MAXPOOL3; break;
       case XPIPE_AVGPOOL3: op.kind = OP_AVGPOOL; break;
       case XPIPE_GAP: op.kind = OP_GAP; break;
       case XPIPE_CONCAT: op.kind = OP_CONCAT; break;
@@ -622,7 +634,8 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     if (!mergeable(p.ops[i])) continue;
     std::vector<size_t> sib{i};
     for (size_t j = i + 1; j < p.ops.size() && sib.size() < (size_t)GATHER_MAX_SEGS; ++j)
-      if (mergeable(p.ops[j]) && p.ops[j].in == p.ops[i].in && p.ops[j].k == p.ops[i].k)
+      if (mergeable(p.ops[j]) && p.ops[j].in == p.ops[i].in && p.ops[j].k == p.ops[i].k &&
+          p.ops[j].stride == p.ops[i].stride)
         sib.push_back(j);
     if (sib.size() < 2) continue;
     Op m = p.ops[i];
@@ -690,7 +703,7 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
   // ---- launch lanes
   plan_lanes(p);
   if (const char* tr = std::getenv("XPIPE_TRACE_PLAN"); tr && *tr == '1') {
-    static const char* kn[] = {"gemm", "bn", "elt", "maxpool", "avgpool", "gap", "concat", "ce"};
+    static const char* kn[] = {"gemm", "bn", "elt", "maxpool", "avgpool", "gap", "concat", "ce", "maxpool3"};
     for (size_t i = 0; i < p.ops.size(); ++i) {
       const Op& o = p.ops[i];
       std::fprintf(stderr, "op %2zu %-7s layer %2d in %2d out %2d cout %3d segs %zu | fwd lane %d waits",
@@ -723,7 +736,7 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
         for (int d = 0; d < 2; ++d)
           op.wg_off[d] = take((size_t)op.cout * op.k * op.k * op.cin * esz);
       if (op.stats) op.stat_block = take((size_t)4 * op.cout * sizeof(double));
-      int M = (int)tin_.sh.rows();
+      int M = (int)p.tensors[op.out].sh.rows();  // output pixels (the input's for stride 1)
       int K = op.k * op.k * op.cin;
       int splits = wgrad_pick_splits(dtype, M, op.cout, K, op.k * op.k);
       wpart = std::max(wpart, wgrad_part_bytes(dtype, op.cout, K, splits));
@@ -988,6 +1001,12 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         a.R = a.S = op.k;
         a.pad = op.k / 2;
         a.relu = op.relu;
+        const Tensor& tout = st->tensors[op.out];
+        if (op.stride > 1) {
+          a.stride = op.stride;
+          a.Ho = tout.sh.H;
+          a.Wo = tout.sh.W;
+        }
         int rows_tiles = 0;
         if (op.stats) a.stat_part = (double*)(st->ws + st->colpart_off[lane]);
         XP_HIP(launch_conv_gemm(dt, a, s, &rows_tiles));
@@ -996,7 +1015,7 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
           double* stats = (double*)(st->ws + op.stat_block);
           ColArgs ca{};
           ca.mode = COL_STATS;
-          ca.M = (int)tin.sh.rows();
+          ca.M = (int)tout.sh.rows();
           ca.C = op.cout;
           ca.partial = a.stat_part;
           ca.row_blocks = rows_tiles;
@@ -1063,6 +1082,7 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         break;
       }
       case OP_MAXPOOL:
+      case OP_MAXPOOL3:
       case OP_AVGPOOL:
       case OP_GAP: {
         View y = act(st, op.out, c);
@@ -1077,6 +1097,7 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         pa.C = tin.sh.C;
         pa.part = (double*)(st->ws + st->colpart_off[lane]);
         if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_fwd(dt, pa, s));
+        else if (op.kind == OP_MAXPOOL3) XP_HIP(launch_maxpool3s2_fwd(dt, pa, s));
         else if (op.kind == OP_AVGPOOL) XP_HIP(launch_avgpool_fwd(dt, pa, s));
         else XP_HIP(launch_gap_fwd(dt, pa, s));
         break;
@@ -1159,7 +1180,8 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
       }
       case OP_GEMM: {
         View g = gradv(st, op.out, c);
-        const int M = (int)tin.sh.rows();
+        const Tensor& tout = st->tensors[op.out];
+        const int M = (int)tout.sh.rows();  // output pixels
         const int K = op.k * op.k * op.cin;
         // weight gradient, accumulated into grad
         WgradArgs w{};
@@ -1187,6 +1209,11 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         w.N = op.cout;
         w.R = w.S = op.k;
         w.pad = op.k / 2;
+        if (op.stride > 1) {
+          w.stride = op.stride;
+          w.Ho = tout.sh.H;
+          w.Wo = tout.sh.W;
+        }
         w.splits = wgrad_pick_splits(dt, M, op.cout, K, op.k * op.k);
         {
           XP_HIP(launch_wgrad(dt, w, s));
@@ -1220,6 +1247,16 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
           a.R = a.S = op.k;
           a.pad = op.k / 2;
           a.accumulate = op.in_acc;
+          if (op.stride > 1) {
+            // rows: the input grid; gathered from the output gradient's grid,
+            // with the transposed (unflipped) weights
+            a.tr = 1;
+            a.stride = op.stride;
+            a.H = tout.sh.H;
+            a.W = tout.sh.W;
+            a.Ho = tin.sh.H;
+            a.Wo = tin.sh.W;
+          }
           XP_HIP(launch_conv_gemm(dt, a, s));
         }
         break;
@@ -1315,6 +1352,7 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         break;
       }
       case OP_MAXPOOL:
+      case OP_MAXPOOL3:
       case OP_AVGPOOL:
       case OP_GAP: {
         if (!want_grad(op.in)) break;
@@ -1334,6 +1372,7 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         pa.W = tin.sh.W;
         pa.C = tin.sh.C;
         if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_bwd(dt, pa, s));
+        else if (op.kind == OP_MAXPOOL3) XP_HIP(launch_maxpool3s2_bwd(dt, pa, s));
         else if (op.kind == OP_AVGPOOL) XP_HIP(launch_avgpool_bwd(dt, pa, s));
         else XP_HIP(launch_gap_bwd(dt, pa, s));
         break;
@@ -1436,8 +1475,10 @@ xpipe_status refresh_gathered(xpipe_stage* st, int dir) {
 xpipe_status refresh_flipped(xpipe_stage* st) {
   for (const Op& op : st->ops) {
     if (op.kind != OP_GEMM) continue;
+    // stride 1: flipped (the data gradient is a convolution of dy); strided:
+    // transposed only (the data gradient gathers dy tap by tap)
     XP_HIP(launch_flip_weights(st->dtype, gemm_weights(st, op, XPIPE_BWD), st->ws + op.wd_off,
-                               op.cout, op.k, op.k, op.cin, st->stream));
+                               op.cout, op.k, op.k, op.cin, st->stream, op.stride == 1));
   }
   st->wd_valid = true;
   return XPIPE_OK;
@@ -2071,31 +2112,51 @@ xpipe_status xpipe_stage_run(xpipe_stage_t st, const xpipe_sched_event* events, 
 xpipe_status xpipe_partition(const xpipe_layer_desc* layers, int32_t n_layers, int32_t stages, int32_t* first) {
   if (!layers || !first || n_layers <= 0 || stages < 1) return fail(XPIPE_EINVAL, "bad arguments");
   std::vector<int32_t> wl;
-  for (int32_t i = 0; i < n_layers; ++i)
-    if (layers[i].kind == XPIPE_LINEAR || layers[i].kind == XPIPE_CONV) wl.push_back(i);
+  for (int32_t i = 0; i < n_layers; ++i) {
+    const xpipe_layer_desc& d = layers[i];
+    if (d.n_inputs < 1 || d.n_inputs > XPIPE_MAX_INPUTS) return fail(XPIPE_EINVAL, "bad input count");
+    for (int32_t q = 0; q < d.n_inputs; ++q)
+      if (d.inputs[q] >= i || d.inputs[q] < -1) return fail(XPIPE_EINVAL, "layer inputs must precede the layer");
+    if (d.kind == XPIPE_LINEAR || d.kind == XPIPE_CONV) wl.push_back(i);
+  }
   const int32_t L = (int32_t)wl.size();
   if (stages > L) return fail(XPIPE_EINVAL, "more stages than layers with weights");
+  // a cut before layer c is valid when every layer from c on reads nothing
+  // older than layer c - 1 (the hand-off): suffix minimum of the inputs
+  std::vector<int32_t> sm(n_layers + 1, n_layers);
+  for (int32_t i = n_layers - 1; i >= 0; --i) {
+    int32_t m = sm[i + 1];
+    for (int32_t q = 0; q < layers[i].n_inputs; ++q) m = std::min(m, layers[i].inputs[q]);
+    sm[i] = m;
+  }
+  auto valid = [&](int32_t j) { return sm[wl[j]] >= wl[j] - 1; };
+  // stage k takes L / K weighted layers, the last L % K stages one more; a cut
+  // that would split a branch or a skip connection moves to the nearest valid
+  // cut (ties: the earlier one, so the later stage takes the extra layers)
   const int32_t base = L / stages, rem = L % stages;
-  int32_t w = 0;
   first[0] = 0;
-  for (int32_t k = 0; k < stages; ++k) {
-    if (k > 0) first[k] = wl[w];
-    w += base + (k >= stages - rem ? 1 : 0);
+  int32_t target = 0, prev = 0;
+  for (int32_t k = 1; k < stages; ++k) {
+    target += base + (k - 1 >= stages - rem ? 1 : 0);
+    const int32_t hi = L - (stages - k);  // leave a weighted layer for every later stage
+    int32_t best = -1;
+    for (int32_t j = prev + 1; j <= hi; ++j)
+      if (valid(j) && (best < 0 || std::abs(j - target) < std::abs(best - target))) best = j;
+    if (best < 0)
+      return fail(XPIPE_EUNSUPPORTED, "no valid cut for stage " + std::to_string(k) +
+                                          ": every cut in range splits a branch or a skip connection");
+    first[k] = wl[best];
+    prev = best;
   }
   first[stages] = n_layers;
   // every layer reads only its own stage, or the previous stage's last layer
   for (int32_t k = 0; k < stages; ++k)
-    for (int32_t i = first[k]; i < first[k + 1]; ++i) {
-      const xpipe_layer_desc& d = layers[i];
-      if (d.n_inputs < 1 || d.n_inputs > XPIPE_MAX_INPUTS) return fail(XPIPE_EINVAL, "bad input count");
-      for (int32_t q = 0; q < d.n_inputs; ++q) {
-        const int32_t j = d.inputs[q];
-        if (j >= i || j < -1) return fail(XPIPE_EINVAL, "layer inputs must precede the layer");
-        if (j >= first[k]) continue;
-        if (k == 0 ? j == -1 : j == first[k] - 1) continue;
+    for (int32_t i = first[k]; i < first[k + 1]; ++i)
+      for (int32_t q = 0; q < layers[i].n_inputs; ++q) {
+        const int32_t j = layers[i].inputs[q];
+        if (j >= first[k] || (k == 0 ? j == -1 : j == first[k] - 1)) continue;
         return fail(XPIPE_EUNSUPPORTED, "layer " + std::to_string(i) + " of stage " + std::to_string(k) +
                                             " reads layer " + std::to_string(j) + " across a stage boundary");
       }
-    }
   return XPIPE_OK;
 }

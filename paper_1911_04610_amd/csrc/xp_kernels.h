@@ -93,6 +93,12 @@ struct ConvArgs {
   int accumulate;       // y = y + result (after mask)
   double* stat_part;    // optional: per row tile, column sums of the stored y and of its
                         // squares, at stat_part[(n * 2 + {0,1}) * row_tiles + tile]
+  // strided convolution (stride > 1): the rows are an Ho x Wo grid per image.
+  // tr = 0: forward, row (ho, wo) reads x at (ho*stride + r - pad, wo*stride + q - pad);
+  // tr = 1: data gradient, x is the output gradient (H x W), the rows the
+  // input grid, and row (h, w) reads x at ((h + pad - r) / stride, ...) where
+  // stride divides h + pad - r, with the weights transposed but not flipped
+  int stride, Ho, Wo, tr;
 };
 
 // Weight gradient: part[split][n][k] = sum_{m in split} dz[m][n] * x~[m][k],
@@ -106,6 +112,9 @@ struct WgradArgs {
   float* grad;          // [N][K] fp32 accumulator
   int nb, H, W, C, N, R, S, pad;
   int splits;
+  // stride > 1: dz has Ho x Wo pixels per image, pixel (ho, wo) pairs with x at
+  // (ho*stride + r - pad, wo*stride + q - pad)
+  int stride, Ho, Wo;
   // optional (nseg > 0): the N rows go to nseg accumulators in order, rows
   // [seg_row0[j], seg_row0[j + 1]) to seg_grad[j] (seg_row0[0] = 0, seg_row0[nseg] = N)
   int nseg;
@@ -123,9 +132,10 @@ size_t wgrad_part_bytes(int dtype, int N, int K, int splits);
 int wgrad_pick_splits(int dtype, int M, int N, int K, int taps);
 hipError_t launch_wgrad(int dtype, const WgradArgs& a, hipStream_t s);
 
-// Flipped, transposed copy for the data gradient: wd[c][r][s][n] = w[n][R-1-r][S-1-s][c].
+// Transposed copy for the data gradient, flipped for stride 1:
+// wd[c][r][s][n] = w[n][R-1-r][S-1-s][c] (flip != 0) or w[n][r][s][c] (flip == 0).
 hipError_t launch_flip_weights(int dtype, const void* w, void* wd, int N, int R, int S, int C,
-                               hipStream_t s);
+                               hipStream_t s, int flip = 1);
 
 // ---------------------------------------------------------------- column reductions
 // Per-column sums over the rows of [M][C] views, two-level and fixed-order.
@@ -204,6 +214,10 @@ struct PoolArgs {
 size_t gap_partial_bytes(int nb, int H, int W, int C);
 hipError_t launch_maxpool_fwd(int dtype, const PoolArgs& a, hipStream_t s);
 hipError_t launch_maxpool_bwd(int dtype, const PoolArgs& a, hipStream_t s);
+// 3x3 / stride 2 / padding 1 max pool (padding never chosen; ties to the first
+// maximum in row-major window order); backward recomputes each window's choice
+hipError_t launch_maxpool3s2_fwd(int dtype, const PoolArgs& a, hipStream_t s);
+hipError_t launch_maxpool3s2_bwd(int dtype, const PoolArgs& a, hipStream_t s);
 hipError_t launch_avgpool_fwd(int dtype, const PoolArgs& a, hipStream_t s);
 hipError_t launch_avgpool_bwd(int dtype, const PoolArgs& a, hipStream_t s);
 hipError_t launch_gap_fwd(int dtype, const PoolArgs& a, hipStream_t s);

@@ -179,13 +179,45 @@ def test_partition_vgg16():
     assert e.value.status == xp.EINVAL
 
 
-def test_partition_refuses_cut_branches():
-    """ResNet bottlenecks split at block boundaries (the skip reads the previous
-    stage's output); Inception-A modules cut inside a module are refused."""
+def _check_cuts(L, first):
+    """Every stage reads only itself and the previous stage's last layer."""
+    for k in range(len(first) - 1):
+        for i in range(first[k], first[k + 1]):
+            for j in L[i]["inputs"]:
+                assert j >= first[k] or j == (first[k] - 1 if k else -1), (k, i, j)
+
+
+def test_partition_moves_cuts_to_block_boundaries():
+    """A cut that would split a residual block or an Inception module moves to
+    the nearest valid cut (ties: the earlier one).  ResNet bottlenecks with
+    identity skips split exactly; the ResNet-101 cuts fall on block starts; the
+    Inception-A stage splits at module boundaries."""
     R = wl.resnet_stage_layers(blocks=8)
     first = xp.xpipe_partition(R, 4)
     for s in wl.split_layers(R, first):
         assert sum(1 for l in s if l["kind"] == "conv") == 6
+    R101 = wl.resnet101_layers()
+    f101 = xp.xpipe_partition(R101, 4)
+    _check_cuts(R101, f101)
+    weighted = [i for i, l in enumerate(R101) if l["kind"] in ("conv", "linear")]
+    # 105 weighted layers: ideal cuts before weighted layers 26, 52, 78; block
+    # starts nearest to them are 24 (tie with 28, the earlier wins), 52 and 79
+    assert [weighted.index(c) for c in f101[1:-1]] == [24, 52, 79]
+    I = wl.inception_stage_layers()
+    fi = xp.xpipe_partition(I, 3)
+    _check_cuts(I, fi)
+    assert [sum(1 for l in s if l["kind"] == "concat") for s in wl.split_layers(I, fi)] == [1, 1, 1]
+
+
+def test_partition_refuses_when_no_valid_cut():
+    """A skip connection from the stage input to the last layer leaves no valid cut."""
+    b = wl._Builder()
+    x = b.relu(b.conv(-1, 8, 8, 3))
+    y = b.relu(b.conv(x, 8, 8, 3))
+    z = b.conv(y, 8, 8, 3)
+    b.add(kind="add", inputs=[z, -1])
+    L = b.layers
+    assert xp.xpipe_partition(L, 1) == [0, len(L)]
     with pytest.raises(xp.XPipeError) as e:
-        xp.xpipe_partition(wl.inception_stage_layers(), 4)
+        xp.xpipe_partition(L, 2)
     assert e.value.status == xp.EUNSUPPORTED

@@ -20,8 +20,12 @@ from gpu_harness import run_stage
 pytestmark = pytest.mark.gpu
 
 
-def conv(x, cin, cout, k, bias=False):
-    return dict(kind="conv", inputs=[x], cin=cin, cout=cout, k=k, bias=bias)
+def conv(x, cin, cout, k, bias=False, stride=1):
+    return dict(kind="conv", inputs=[x], cin=cin, cout=cout, k=k, bias=bias, stride=stride)
+
+
+def bn(x, c):
+    return dict(kind="bn", inputs=[x], cin=c, cout=c)
 
 
 LAYER_CASES = {
@@ -69,6 +73,29 @@ LAYER_CASES = {
                               dict(kind="relu", inputs=[1])], (6, 7, 32), 2),
     "pool_then_relu": ([dict(kind="maxpool2", inputs=[-1]), dict(kind="relu", inputs=[0])],
                        (8, 8, 64), 2),
+    # stride 2 (ResNet-101): odd and even sizes, ragged row tiles; the data
+    # gradient gathers the output gradient tap by tap
+    "conv3x3_s2": ([conv(-1, 64, 128, 3, stride=2)], (15, 14, 64), 2),
+    "conv1x1_s2_projection": ([conv(-1, 64, 128, 1, stride=2)], (14, 13, 64), 2),
+    "conv3x3_s2_narrow": ([conv(-1, 32, 32, 3, True, stride=2)], (9, 10, 32), 3),
+    # 12 channels: element-gather forward and data gradient in bf16
+    "conv3x3_s2_c12_flat": ([conv(-1, 12, 12, 3, stride=2)], (11, 7, 12), 2),
+    "conv7x7_s2_stem": ([conv(-1, 3, 64, 7, stride=2)], (23, 22, 3), 2),
+    "maxpool3s2_even": ([dict(kind="maxpool3s2", inputs=[-1])], (12, 10, 64), 2),
+    "maxpool3s2_odd": ([dict(kind="maxpool3s2", inputs=[-1])], (11, 9, 24), 2),
+    "maxpool3s2_c20": ([dict(kind="maxpool3s2", inputs=[-1])], (9, 8, 20), 2),
+    # ResNet-101 stem: strided conv with BN statistics in its epilogue, ReLU,
+    # the 3x3 stride-2 pool (its gradient masked by the ReLU)
+    "resnet_stem": ([conv(-1, 3, 64, 7, stride=2), bn(0, 64), dict(kind="relu", inputs=[1]),
+                     dict(kind="maxpool3s2", inputs=[2])], (30, 28, 3), 2),
+    # first bottleneck of a group: strided 3x3, projection shortcut with BN
+    # (stored), the last BN taking in the shortcut with the ReLU
+    "resnet_block_projection": ([conv(-1, 64, 32, 1), bn(0, 32), dict(kind="relu", inputs=[1]),
+                                 conv(2, 32, 32, 3, stride=2), bn(3, 32), dict(kind="relu", inputs=[4]),
+                                 conv(-1, 64, 128, 1, stride=2), bn(6, 128),
+                                 conv(5, 32, 128, 1), bn(8, 128),
+                                 dict(kind="add", inputs=[9, 7]), dict(kind="relu", inputs=[10])],
+                                (10, 9, 64), 2),
 }
 
 
@@ -98,7 +125,7 @@ def test_layer_kernels_match_oracle(name, dtype):
     act = "bf16" if dtype == xp.BF16 else "f32"
     inp = wl.stage_inputs(w, act_dtype=act)
     gpu, _ = run_stage(w, inp, dtype, xp.Hyper(), 0, 0, minibatches=1)
-    decisions = any(L["kind"] in ("relu", "maxpool2") for L in w.layers)
+    decisions = any(L["kind"] in ("relu", "maxpool2", "maxpool3s2") for L in w.layers)
     refs = {act: oracle.train_stage(oracle.Stage(w.layers, act), inp.params, inp.m, inp.v, inp.xs,
                                     0, 0, oracle.Hyper(), labels=inp.labels, dys=inp.dys)[0]}
     if dtype == xp.BF16 and not decisions:

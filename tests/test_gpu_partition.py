@@ -1,8 +1,11 @@
-"""VGG-16 partitioned into four stages by Sec. IV-A's rule, run stage by stage
-on the GPU library (the activation of stage k is the input of stage k + 1,
-the input gradient of stage k + 1 the upstream gradient of stage k) against
-the oracle's forward and backward of the unpartitioned network.  fp32
-storage, s = 0: logits, loss and every weight gradient within 2e-4."""
+"""Whole networks partitioned into four stages by Sec. IV-A's rule, run
+stage by stage on the GPU library (the activation of stage k is the input of
+stage k + 1, the input gradient of stage k + 1 the upstream gradient of stage
+k) against the oracle's forward and backward of the unpartitioned network.
+fp32 storage, s = 0: logits, loss and every weight gradient within 2e-4.
+VGG-16 at 32 x 32 (CIFAR-10); ResNet-101 at 64 x 64 (its strided stem, pool,
+projections and 33 bottlenecks; 2 x 2 maps in the last group keep the
+micro-batch BNs well conditioned)."""
 import numpy as np
 import pytest
 
@@ -15,10 +18,15 @@ from gpu_harness import to_device, to_host
 pytestmark = pytest.mark.gpu
 
 
-def test_partitioned_vgg16_matches_unpartitioned_oracle():
+NETS = {"vgg16": (wl.vgg16_layers, (32, 32, 3)), "resnet101": (wl.resnet101_layers, (64, 64, 3))}
+
+
+@pytest.mark.parametrize("net", list(NETS))
+def test_partitioned_network_matches_unpartitioned_oracle(net):
     import torch
-    layers = wl.vgg16_layers()
-    w = wl.StageWorkload("vgg16_full", layers, 2, 1, (32, 32, 3), 4, 0, 0, 0, minibatches=1)
+    build, in_shape = NETS[net]
+    layers = build()
+    w = wl.StageWorkload(net + "_full", layers, 2, 1, in_shape, 4, 0, 0, 0, minibatches=1)
     inp = wl.stage_inputs(w, act_dtype="f32")
     x, labels = inp.xs[0][0], inp.labels[0][0]
     first = xp.xpipe_partition(layers, 4)
@@ -29,7 +37,6 @@ def test_partitioned_vgg16_matches_unpartitioned_oracle():
     stages, ins, outs = [], [to_device(x, xp.F32)], []
     lab = torch.from_numpy(labels).cuda()
     loss = torch.zeros(1, dtype=torch.float32, device="cuda")
-    in_shape = (32, 32, 3)
     for k, p in enumerate(parts):
         st = xp.Stage(p, w.micro_batch, 1, in_shape, xp.F32)
         st.set_flat(st.W, inp.params[offs[k]:offs[k + 1]])
@@ -60,5 +67,5 @@ def test_partitioned_vgg16_matches_unpartitioned_oracle():
     for q, (a, b) in enumerate(zip(grads, ref_grads)):
         errs[f"grad[{q}]"] = rel_l2(a, b)
     worst = max(errs, key=errs.get)
-    print(f"partitioned VGG-16 {first}: worst {worst} = {errs[worst]:.2e}")
+    print(f"partitioned {net} {first}: worst {worst} = {errs[worst]:.2e}")
     assert all(v <= 2e-4 for v in errs.values()), {k: v for k, v in errs.items() if v > 2e-4}

@@ -378,9 +378,12 @@ def stage_output_shape(w: StageWorkload) -> tuple:
         if k in ("linear",):
             shapes[i] = s[:-1] + (L["cout"],)
         elif k == "conv":
-            shapes[i] = s[:-1] + (L["cout"],)
+            st = L.get("stride", 1)
+            shapes[i] = (s[0], (s[1] - 1) // st + 1, (s[2] - 1) // st + 1, L["cout"])
         elif k == "maxpool2":
             shapes[i] = (s[0], s[1] // 2, s[2] // 2, s[3])
+        elif k == "maxpool3s2":
+            shapes[i] = (s[0], (s[1] - 1) // 2 + 1, (s[2] - 1) // 2 + 1, s[3])
         elif k == "gap":
             shapes[i] = (s[0], s[3])
         elif k == "concat":

@@ -5,11 +5,12 @@ TEST INFRASTRUCTURE ONLY (the CPU oracle; see oracle/__init__.py).
 The paper runs stock framework layers (Sec. IV-A, IV-C) and defines none of
 them; each function below is the textbook definition written out.  Layouts:
 activations NHWC (or [n, C]), conv weights [K, R, S, C], linear weights
-[out, in].  Convolutions have zero padding k//2 and stride 1 or 2 (cross-
-correlation; output size floor((H - 1) / stride) + 1, the strided layers of
-ResNet-101).  ReLU'(0) = 0.  Max pooling sends the gradient to the first
-maximum in row-major window order (the 3x3 stride-2 pool of the ResNet stem
-pads with -inf).  3x3 average pooling counts the zero
+[out, in].  Convolutions (cross-correlation) have an R x S kernel (square, or
+Inception-V3's 1 x n / n x 1), stride 1 or 2, and either "same" zero padding
+(R//2, S//2) or none ("valid", Inception-V3's stem and grid reductions); output
+size floor((H + 2p - R) / stride) + 1.  ReLU'(0) = 0.  Max pooling sends the
+gradient to the first maximum in row-major window order (the 3x3 stride-2 pool
+pads with -inf, or not at all when "valid").  3x3 average pooling counts the zero
 padding (divides by 9).  Batch normalisation uses the batch mean and the
 biased batch variance of the micro-batch, eps 1e-5.
 """
@@ -31,20 +32,21 @@ def _shifted(xp, r, s, Ho, Wo, stride=1):
     return np.ascontiguousarray(xp[_win(r, s, Ho, Wo, stride)]).reshape(-1, xp.shape[3])
 
 
-def conv_out(H, k, stride=1):
-    """Output size of a zero-padded (k//2) convolution: floor((H + 2p - k) / stride) + 1."""
-    p = k // 2
+def conv_out(H, k, stride=1, valid=False):
+    """Output size of a convolution: floor((H + 2p - k) / stride) + 1, p = k//2 or 0."""
+    p = 0 if valid else k // 2
     return (H + 2 * p - k) // stride + 1
 
 
 # ---------------------------------------------------------------- conv / linear
-def conv2d(x, w, b=None, stride=1):
-    """y[n,h,w,k] = sum_{r,s,c} x[n, h*st+r-p, w*st+s-p, c] * w[k,r,s,c] (+ b[k])."""
+def conv2d(x, w, b=None, stride=1, valid=False):
+    """y[n,h,w,k] = sum_{r,s,c} x[n, h*st+r-ph, w*st+s-pw, c] * w[k,r,s,c] (+ b[k]),
+    (ph, pw) = (R//2, S//2), or (0, 0) when valid."""
     n, H, W, C = x.shape
     K, R, S, _ = w.shape
-    p = R // 2
-    Ho, Wo = conv_out(H, R, stride), conv_out(W, S, stride)
-    xp = np.pad(x, ((0, 0), (p, p), (p, p), (0, 0)))
+    ph, pw = (0, 0) if valid else (R // 2, S // 2)
+    Ho, Wo = conv_out(H, R, stride, valid), conv_out(W, S, stride, valid)
+    xp = np.pad(x, ((0, 0), (ph, ph), (pw, pw), (0, 0)))
     y = np.zeros((n * Ho * Wo, K))
     for r in range(R):
         for s in range(S):
@@ -54,13 +56,13 @@ def conv2d(x, w, b=None, stride=1):
     return y.reshape(n, Ho, Wo, K)
 
 
-def conv2d_vjp(x, w, dy, need_dx=True, has_bias=False, stride=1):
+def conv2d_vjp(x, w, dy, need_dx=True, has_bias=False, stride=1, valid=False):
     """Gradients of conv2d w.r.t. x, w and b for cotangent dy."""
     n, H, W, C = x.shape
     K, R, S, _ = w.shape
-    p = R // 2
+    ph, pw = (0, 0) if valid else (R // 2, S // 2)
     Ho, Wo = dy.shape[1], dy.shape[2]
-    xp = np.pad(x, ((0, 0), (p, p), (p, p), (0, 0)))
+    xp = np.pad(x, ((0, 0), (ph, ph), (pw, pw), (0, 0)))
     dy2 = dy.reshape(-1, K)
     dw = np.zeros_like(w)
     dxp = np.zeros_like(xp) if need_dx else None
@@ -70,7 +72,7 @@ def conv2d_vjp(x, w, dy, need_dx=True, has_bias=False, stride=1):
             if need_dx:
                 dxp[_win(r, s, Ho, Wo, stride)] += (dy2 @ w[:, r, s, :]).reshape(n, Ho, Wo, C)
     db = dy2.sum(axis=0) if has_bias else None
-    dx = dxp[:, p:p + H, p:p + W, :] if need_dx else None
+    dx = dxp[:, ph:ph + H, pw:pw + W, :] if need_dx else None
     return dx, dw, db
 
 
@@ -150,29 +152,32 @@ def maxpool2_vjp(x_shape, idx, dy):
     return dx
 
 
-def maxpool3s2(x):
+def maxpool3s2(x, valid=False):
     """3x3 max pooling, stride 2, padding 1 with -inf (never chosen: the window
-    centre is always inside).  Output floor((H - 1) / 2) + 1.  Returns (y,
-    argmax index 0..8 per output, the first maximum in row-major order)."""
+    centre is always inside), or no padding when valid.  Output
+    floor((H + 2p - 3) / 2) + 1.  Returns (y, argmax index 0..8 per output, the
+    first maximum in row-major order)."""
     n, H, W, C = x.shape
-    Ho, Wo = (H - 1) // 2 + 1, (W - 1) // 2 + 1
-    xp = np.pad(x, ((0, 0), (1, 1), (1, 1), (0, 0)), constant_values=-np.inf)
+    p = 0 if valid else 1
+    Ho, Wo = (H + 2 * p - 3) // 2 + 1, (W + 2 * p - 3) // 2 + 1
+    xp = np.pad(x, ((0, 0), (p, p), (p, p), (0, 0)), constant_values=-np.inf)
     win = np.stack([xp[_win(r, s, Ho, Wo, 2)] for r in range(3) for s in range(3)], axis=3)
     idx = np.argmax(win, axis=3)
     y = np.take_along_axis(win, idx[:, :, :, None, :], axis=3)[:, :, :, 0, :]
     return y, idx
 
 
-def maxpool3s2_vjp(x_shape, idx, dy):
+def maxpool3s2_vjp(x_shape, idx, dy, valid=False):
     """Each output's gradient goes to its window's first maximum; windows overlap,
     so an input adds the gradients of every output that chose it."""
     n, H, W, C = x_shape
+    p = 0 if valid else 1
     Ho, Wo = dy.shape[1], dy.shape[2]
-    dxp = np.zeros((n, H + 2, W + 2, C))
+    dxp = np.zeros((n, H + 2 * p, W + 2 * p, C))
     for j in range(9):
         r, s = divmod(j, 3)
         dxp[_win(r, s, Ho, Wo, 2)] += np.where(idx == j, dy, 0.0)
-    return dxp[:, 1:H + 1, 1:W + 1, :]
+    return dxp[:, p:p + H, p:p + W, :]
 
 
 def avgpool3(x):

@@ -134,7 +134,8 @@ class Stage:
             pi = self.pidx[i]
             if k == "conv":
                 b = P[pi[1]] if L["bias"] else None
-                outs[i] = self.q(ly.conv2d(a, self.qw(P[pi[0]]), b, L.get("stride", 1)))
+                outs[i] = self.q(ly.conv2d(a, self.qw(P[pi[0]]), b, L.get("stride", 1),
+                                           L.get("pad", "same") == "valid"))
             elif k == "linear":
                 b = P[pi[1]] if L["bias"] else None
                 outs[i] = self.q(ly.linear(_rows(a), self.qw(P[pi[0]]), b))
@@ -151,7 +152,7 @@ class Stage:
                 outs[i] = y
                 saved[i] = idx
             elif k == "maxpool3s2":
-                y, idx = ly.maxpool3s2(a)
+                y, idx = ly.maxpool3s2(a, L.get("pad", "same") == "valid")
                 outs[i] = y
                 saved[i] = idx
             elif k == "avgpool3":
@@ -198,7 +199,7 @@ class Stage:
             want_dx = need_dx or src != -1
             if k == "conv":
                 dx, dw, db = ly.conv2d_vjp(a, self.qw(P[pi[0]]), gi, want_dx, L["bias"],
-                                           L.get("stride", 1))
+                                           L.get("stride", 1), L.get("pad", "same") == "valid")
                 grads[pi[0]] = dw
                 if L["bias"]:
                     grads[pi[1]] = db
@@ -227,7 +228,7 @@ class Stage:
             elif k == "maxpool2":
                 acc(src, ly.maxpool2_vjp(a.shape, saved[i], gi))
             elif k == "maxpool3s2":
-                acc(src, ly.maxpool3s2_vjp(a.shape, saved[i], gi))
+                acc(src, ly.maxpool3s2_vjp(a.shape, saved[i], gi, L.get("pad", "same") == "valid"))
             elif k == "avgpool3":
                 acc(src, ly.avgpool3_vjp(gi))
             elif k == "gap":

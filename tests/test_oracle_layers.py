@@ -250,3 +250,44 @@ def test_maxpool3s2_ties_and_padding():
     y3, idx3 = ly.maxpool3s2(x3)
     dx3 = ly.maxpool3s2_vjp(x3.shape, idx3, np.ones(y3.shape))
     assert dx3[0, 0, 1, 0] == 2.0 and dx3.sum() == 4.0
+
+
+@pytest.mark.parametrize("R,S,stride,valid", [(1, 7, 1, False), (7, 1, 1, False), (1, 3, 1, False),
+                                              (3, 1, 1, False), (3, 3, 1, True), (3, 3, 2, True),
+                                              (5, 3, 2, True)])
+def test_general_conv_matches_torch(R, S, stride, valid):
+    """Inception-V3's convolutions: 1 x n / n x 1 kernels with "same" padding
+    (R//2, S//2), and unpadded ("valid") ones, strided or not."""
+    rng = np.random.default_rng(50 + R * 7 + S + stride)
+    x = rng.standard_normal((2, 11, 10, 4))
+    w = rng.standard_normal((5, R, S, 4))
+    b = rng.standard_normal(5)
+    xt = torch.tensor(x.transpose(0, 3, 1, 2), requires_grad=True)
+    wt = torch.tensor(w.transpose(0, 3, 1, 2), requires_grad=True)
+    bt = torch.tensor(b, requires_grad=True)
+    yt = F.conv2d(xt, wt, bt, stride=stride, padding=(0, 0) if valid else (R // 2, S // 2))
+    assert yt.shape[2:] == (ly.conv_out(11, R, stride, valid), ly.conv_out(10, S, stride, valid))
+    dy = rng.standard_normal(yt.shape)
+    yt.backward(torch.tensor(dy))
+    y = ly.conv2d(x, w, b, stride, valid)
+    np.testing.assert_allclose(y, yt.detach().numpy().transpose(0, 2, 3, 1), rtol=1e-12, atol=1e-12)
+    dx, dw, db = ly.conv2d_vjp(x, w, dy.transpose(0, 2, 3, 1), True, True, stride, valid)
+    np.testing.assert_allclose(dx, xt.grad.numpy().transpose(0, 2, 3, 1), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dw, wt.grad.numpy().transpose(0, 2, 3, 1), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(db, bt.grad.numpy(), rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("H,W", [(9, 8), (8, 7)])
+def test_maxpool3s2_valid_matches_torch(H, W):
+    """The unpadded 3x3 stride-2 pool of Inception-V3 (output floor((H - 3) / 2) + 1)."""
+    rng = np.random.default_rng(60 + H)
+    x = rng.permutation(2 * H * W * 3).reshape(2, H, W, 3).astype(np.float64) / 13.0
+    y, idx = ly.maxpool3s2(x, valid=True)
+    assert y.shape[1:3] == ((H - 3) // 2 + 1, (W - 3) // 2 + 1)
+    dy = rng.standard_normal(y.shape)
+    dx = ly.maxpool3s2_vjp(x.shape, idx, dy, valid=True)
+    xt = torch.tensor(x.transpose(0, 3, 1, 2), requires_grad=True)
+    yt = F.max_pool2d(xt, 3, stride=2)
+    yt.backward(torch.tensor(dy.transpose(0, 3, 1, 2)))
+    np.testing.assert_array_equal(y, yt.detach().numpy().transpose(0, 2, 3, 1))
+    np.testing.assert_allclose(dx, xt.grad.numpy().transpose(0, 2, 3, 1), rtol=1e-15, atol=1e-15)

@@ -88,6 +88,26 @@ def test_full_resnet101_matches_torch():
     assert worst < 1e-10, worst
 
 
+def test_full_inception_v3_matches_torch():
+    """The whole Inception-V3 (unpadded stem, three A modules, grid reductions B
+    and D with their max-pool branches, four C modules with 1x7 / 7x1
+    factorisations, two E modules with nested concats, classifier) against
+    torch float64 autograd, at a 139 x 139 input (3 x 3 maps in the last modules)."""
+    layers = wl.inception_v3_layers()
+    w = wl.StageWorkload("inception_v3_full", layers, 2, 1, (139, 139, 3), 4, 0, 0, 0, minibatches=1)
+    inp = wl.stage_inputs(w)
+    st = oracle.Stage(layers)
+    x, lab = inp.xs[0][0], inp.labels[0][0]
+    y, loss, _ = st.forward(inp.params, x, lab, 2)
+    dx, grads, _ = st.backward(inp.params, x, None, lab, 2)
+    yt, losst, dxt, gt = torch_ref.fwd_bwd(layers, inp.params, x, None, lab, 2)
+    assert rel_l2(y.reshape(-1), np.asarray(yt).reshape(-1)) < 1e-10
+    assert abs(loss - losst) < 1e-10
+    assert rel_l2(dx, dxt) < 1e-10
+    worst = max(rel_l2(a, b) for a, b in zip(grads, gt))
+    assert worst < 1e-10, worst
+
+
 def test_projection_bn_output_is_stored():
     """A BN output that is not fused into a ReLU or into a later residual add
     (the projection shortcut's BN) is a stored activation: rounded to the

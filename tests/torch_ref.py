@@ -31,8 +31,10 @@ def forward(layers, P, x, labels=None, N=None):
         pi = own[i]
         if k == "conv":
             b = P[pi[1]] if L["bias"] else None
-            outs[i] = F.conv2d(a.permute(0, 3, 1, 2), P[pi[0]].permute(0, 3, 1, 2), b,
-                               stride=L.get("stride", 1), padding=L["k"] // 2).permute(0, 2, 3, 1)
+            wk = P[pi[0]]
+            pad = (0, 0) if L.get("pad", "same") == "valid" else (wk.shape[1] // 2, wk.shape[2] // 2)
+            outs[i] = F.conv2d(a.permute(0, 3, 1, 2), wk.permute(0, 3, 1, 2), b,
+                               stride=L.get("stride", 1), padding=pad).permute(0, 2, 3, 1)
         elif k == "linear":
             a2 = a.reshape(a.shape[0], a.shape[-1]) if a.dim() == 4 else a   # [n,1,1,C] -> [n,C]
             outs[i] = F.linear(a2, P[pi[0]], P[pi[1]] if L["bias"] else None)
@@ -46,7 +48,8 @@ def forward(layers, P, x, labels=None, N=None):
         elif k == "maxpool2":
             outs[i] = F.max_pool2d(a.permute(0, 3, 1, 2), 2).permute(0, 2, 3, 1)
         elif k == "maxpool3s2":
-            outs[i] = F.max_pool2d(a.permute(0, 3, 1, 2), 3, stride=2, padding=1).permute(0, 2, 3, 1)
+            outs[i] = F.max_pool2d(a.permute(0, 3, 1, 2), 3, stride=2,
+                                   padding=0 if L.get("pad", "same") == "valid" else 1).permute(0, 2, 3, 1)
         elif k == "avgpool3":
             outs[i] = F.avg_pool2d(a.permute(0, 3, 1, 2), 3, 1, 1,
                                    count_include_pad=True).permute(0, 2, 3, 1)

@@ -46,8 +46,14 @@ class _Builder:
     def linear(self, x, cin, cout, bias=True):
         return self.add(kind="linear", inputs=[x], cin=cin, cout=cout, bias=bias)
 
-    def conv(self, x, cin, cout, k, bias=False, stride=1):
-        return self.add(kind="conv", inputs=[x], cin=cin, cout=cout, k=k, bias=bias, stride=stride)
+    def conv(self, x, cin, cout, k, bias=False, stride=1, kw=None, pad="same"):
+        """k x kw kernel (kw defaults to k); pad "same" (k//2, kw//2) or "valid" (none)."""
+        L = dict(kind="conv", inputs=[x], cin=cin, cout=cout, k=k, bias=bias, stride=stride)
+        if kw is not None and kw != k:
+            L["kw"] = kw
+        if pad != "same":
+            L["pad"] = pad
+        return self.add(**L)
 
     def bn(self, x, c):
         return self.add(kind="bn", inputs=[x], cin=c, cout=c)
@@ -55,8 +61,8 @@ class _Builder:
     def relu(self, x):
         return self.add(kind="relu", inputs=[x])
 
-    def conv_bn_relu(self, x, cin, cout, k, stride=1):
-        return self.relu(self.bn(self.conv(x, cin, cout, k, stride=stride), cout))
+    def conv_bn_relu(self, x, cin, cout, k, stride=1, kw=None, pad="same"):
+        return self.relu(self.bn(self.conv(x, cin, cout, k, stride=stride, kw=kw, pad=pad), cout))
 
 
 def mlp_stage_layers(d_in=256, d_hidden=256, classes=10) -> List[dict]:
@@ -142,6 +148,70 @@ def resnet101_layers(classes=200, blocks=(3, 4, 23, 3)) -> List[dict]:
     return b.layers
 
 
+def inception_v3_layers(classes=200) -> List[dict]:
+    """Inception-V3 (Sec. IV-B's Tiny ImageNet model, inputs scaled to 224 x
+    224), as defined by its authors: every convolution followed by BN and ReLU;
+    an unpadded stem (3x3 stride 2, 3x3, padded 3x3, 3x3 stride-2 max pool,
+    1x1, 3x3, 3x3 stride-2 max pool); three Inception-A modules (1x1 | 1x1 ->
+    5x5 | 1x1 -> 3x3 -> 3x3 | 3x3 average pool -> 1x1); the grid reduction B;
+    four Inception-C modules with factorised 1x7 / 7x1 convolutions; the grid
+    reduction D; two Inception-E modules whose 3x3 branches end in parallel
+    1x3 and 3x1 convolutions; global average pooling, the classifier and the
+    cross-entropy loss (no auxiliary head)."""
+    b = _Builder()
+    cbr = b.conv_bn_relu
+    x = cbr(-1, 3, 32, 3, stride=2, pad="valid")
+    x = cbr(x, 32, 32, 3, pad="valid")
+    x = cbr(x, 32, 64, 3)
+    x = b.add(kind="maxpool3s2", inputs=[x], pad="valid")
+    x = cbr(x, 64, 80, 1)
+    x = cbr(x, 80, 192, 3, pad="valid")
+    x = b.add(kind="maxpool3s2", inputs=[x], pad="valid")
+    cin = 192
+    for pool_f in (32, 64, 64):                       # Inception-A
+        b1 = cbr(x, cin, 64, 1)
+        b2 = cbr(cbr(x, cin, 48, 1), 48, 64, 5)
+        b3 = cbr(cbr(cbr(x, cin, 64, 1), 64, 96, 3), 96, 96, 3)
+        b4 = cbr(b.add(kind="avgpool3", inputs=[x]), cin, pool_f, 1)
+        x = b.add(kind="concat", inputs=[b1, b2, b3, b4])
+        cin = 64 + 64 + 96 + pool_f
+    b1 = cbr(x, cin, 384, 3, stride=2, pad="valid")   # grid reduction B
+    b2 = cbr(cbr(cbr(x, cin, 64, 1), 64, 96, 3), 96, 96, 3, stride=2, pad="valid")
+    b3 = b.add(kind="maxpool3s2", inputs=[x], pad="valid")
+    x = b.add(kind="concat", inputs=[b1, b2, b3])
+    cin = 384 + 96 + cin
+    for c7 in (128, 160, 160, 192):                   # Inception-C
+        b1 = cbr(x, cin, 192, 1)
+        b2 = cbr(cbr(cbr(x, cin, c7, 1), c7, c7, 1, kw=7), c7, 192, 7, kw=1)
+        b3 = cbr(x, cin, c7, 1)
+        b3 = cbr(b3, c7, c7, 7, kw=1)
+        b3 = cbr(b3, c7, c7, 1, kw=7)
+        b3 = cbr(b3, c7, c7, 7, kw=1)
+        b3 = cbr(b3, c7, 192, 1, kw=7)
+        b4 = cbr(b.add(kind="avgpool3", inputs=[x]), cin, 192, 1)
+        x = b.add(kind="concat", inputs=[b1, b2, b3, b4])
+        cin = 768
+    b1 = cbr(cbr(x, cin, 192, 1), 192, 320, 3, stride=2, pad="valid")   # grid reduction D
+    b2 = cbr(cbr(cbr(cbr(x, cin, 192, 1), 192, 192, 1, kw=7), 192, 192, 7, kw=1),
+             192, 192, 3, stride=2, pad="valid")
+    b3 = b.add(kind="maxpool3s2", inputs=[x], pad="valid")
+    x = b.add(kind="concat", inputs=[b1, b2, b3])
+    cin = 320 + 192 + cin
+    for _ in range(2):                                # Inception-E
+        b1 = cbr(x, cin, 320, 1)
+        t = cbr(x, cin, 384, 1)
+        b2 = b.add(kind="concat", inputs=[cbr(t, 384, 384, 1, kw=3), cbr(t, 384, 384, 3, kw=1)])
+        t = cbr(cbr(x, cin, 448, 1), 448, 384, 3)
+        b3 = b.add(kind="concat", inputs=[cbr(t, 384, 384, 1, kw=3), cbr(t, 384, 384, 3, kw=1)])
+        b4 = cbr(b.add(kind="avgpool3", inputs=[x]), cin, 192, 1)
+        x = b.add(kind="concat", inputs=[b1, b2, b3, b4])
+        cin = 2048
+    g_ = b.add(kind="gap", inputs=[x])
+    z = b.linear(g_, cin, classes)
+    b.add(kind="softmax_ce", inputs=[z], classes=classes)
+    return b.layers
+
+
 def resnet_stage_layers(blocks=8, c=512, mid=128) -> List[dict]:
     """Middle ResNet-101 stage: bottlenecks with identity shortcut."""
     b = _Builder()
@@ -183,7 +253,7 @@ def param_shapes(layers: List[dict]) -> List[tuple]:
             if L["bias"]:
                 shapes.append((L["cout"],))
         elif L["kind"] == "conv":
-            shapes.append((L["cout"], L["k"], L["k"], L["cin"]))
+            shapes.append((L["cout"], L["k"], L.get("kw", L["k"]), L["cin"]))
             if L["bias"]:
                 shapes.append((L["cout"],))
         elif L["kind"] == "bn":
@@ -378,12 +448,14 @@ def stage_output_shape(w: StageWorkload) -> tuple:
         if k in ("linear",):
             shapes[i] = s[:-1] + (L["cout"],)
         elif k == "conv":
-            st = L.get("stride", 1)
-            shapes[i] = (s[0], (s[1] - 1) // st + 1, (s[2] - 1) // st + 1, L["cout"])
+            st, kh, kw = L.get("stride", 1), L["k"], L.get("kw", L["k"])
+            ph, pw = (0, 0) if L.get("pad", "same") == "valid" else (kh // 2, kw // 2)
+            shapes[i] = (s[0], (s[1] + 2 * ph - kh) // st + 1, (s[2] + 2 * pw - kw) // st + 1, L["cout"])
         elif k == "maxpool2":
             shapes[i] = (s[0], s[1] // 2, s[2] // 2, s[3])
         elif k == "maxpool3s2":
-            shapes[i] = (s[0], (s[1] - 1) // 2 + 1, (s[2] - 1) // 2 + 1, s[3])
+            p = 0 if L.get("pad", "same") == "valid" else 1
+            shapes[i] = (s[0], (s[1] + 2 * p - 3) // 2 + 1, (s[2] + 2 * p - 3) // 2 + 1, s[3])
         elif k == "gap":
             shapes[i] = (s[0], s[3])
         elif k == "concat":

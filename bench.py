@@ -256,9 +256,9 @@ def time_partitioned(args, net, stages=4, steps=10, warmup=3):
     predictions; bf16).  Reports each stage's step time and the pipeline's
     steady-state throughput bound, the slowest stage's (synthetic inputs and
     upstream gradients of each stage's shapes).  VGG-16: CIFAR-10 images
-    (32 x 32), micro-batch 32, T = 4 (mini-batch 128).  ResNet-101: Tiny
-    ImageNet images scaled to 224 x 224, 200 classes, micro-batch 100 (the
-    paper's 4-GPU setting), T = 4."""
+    (32 x 32), micro-batch 32, T = 4 (mini-batch 128).  ResNet-101 and
+    Inception-V3: Tiny ImageNet images scaled to 224 x 224, 200 classes,
+    micro-batch 100 (the paper's 4-GPU setting), T = 4."""
     import numpy as np
     import torch
     import paper_1911_04610_amd as xp
@@ -266,9 +266,12 @@ def time_partitioned(args, net, stages=4, steps=10, warmup=3):
     if net == "vgg16":
         layers, in_shape, mb, T = wl.vgg16_layers(), (32, 32, 3), 32, 4
         model = "vgg16 (32x32 inputs, 13 conv + linear)"
-    else:
+    elif net == "resnet101":
         layers, in_shape, mb, T = wl.resnet101_layers(), (224, 224, 3), 100, 4
         model = "resnet101 (224x224 inputs, 200 classes, 104 conv + linear)"
+    else:
+        layers, in_shape, mb, T = wl.inception_v3_layers(), (224, 224, 3), 100, 4
+        model = "inception_v3 (224x224 inputs, 200 classes, 94 conv + linear, no auxiliary head)"
     first = xp.xpipe_partition(layers, stages)
     parts = wl.split_layers(layers, first)
     rng = np.random.default_rng(wl.PAPER_SEED + 7)
@@ -508,6 +511,7 @@ def main():
         out["interleaved_schedule"] = time_interleaved(args)
         out["vgg16_partitioned"] = time_partitioned(args, "vgg16")
         out["resnet101_partitioned"] = time_partitioned(args, "resnet101")
+        out["inception_v3_partitioned"] = time_partitioned(args, "inception_v3")
         out["vendor_reference"] = vendor_reference()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.dtype)

@@ -77,8 +77,9 @@ typedef enum {
  * Activations are NHWC; a [n, C] tensor is NHWC with H = W = 1. */
 typedef enum {
   XPIPE_LINEAR = 0,     /* y = x W^T + b; W [cout][cin]; input must have H = W = 1 */
-  XPIPE_CONV = 1,       /* k x k, stride 1 or 2, zero padding k/2, cross-correlation;
-                           output floor((H - 1) / stride) + 1; W [cout][k][k][cin] (KRSC) */
+  XPIPE_CONV = 1,       /* k x kw kernel, stride 1 or 2, zero padding (k/2, kw/2) or
+                           none (pad = 1), cross-correlation; output
+                           floor((H + 2 ph - k) / stride) + 1; W [cout][k][kw][cin] (KRSC) */
   XPIPE_BN = 2,         /* batch norm with the micro-batch's mean and biased
                            variance, eps 1e-5; params gamma[C], beta[C] */
   XPIPE_RELU = 3,       /* max(x, 0); derivative 0 at 0 */
@@ -91,9 +92,10 @@ typedef enum {
   XPIPE_SOFTMAX_CE = 9, /* loss = sum over the micro-batch of -log softmax(x)[label],
                            divided by the mini-batch size N = T * micro_batch;
                            must be the last layer */
-  XPIPE_MAXPOOL3S2 = 10 /* 3x3 window, stride 2, padding 1 (never chosen), output
-                           floor((H - 1) / 2) + 1; gradient to the first maximum in
-                           row-major window order (ResNet-101's stem) */
+  XPIPE_MAXPOOL3S2 = 10 /* 3x3 window, stride 2, padding 1 (never chosen) or none
+                           (pad = 1), output floor((H + 2p - 3) / 2) + 1; gradient to
+                           the first maximum in row-major window order (ResNet-101's
+                           stem, Inception-V3's stem and grid reductions) */
 } xpipe_layer_kind;
 
 #define XPIPE_MAX_INPUTS 4
@@ -103,10 +105,13 @@ typedef struct {
   int32_t n_inputs;                   /* 1, or 2 (ADD), or 2..4 (CONCAT) */
   int32_t inputs[XPIPE_MAX_INPUTS];   /* producer layer indices (< own index); -1 = stage input */
   int32_t cin, cout;                  /* LINEAR, CONV; BN uses cout as its channel count */
-  int32_t k;                          /* CONV kernel size (odd, 1..7) */
+  int32_t k;                          /* CONV kernel height (odd, 1..7) */
   int32_t has_bias;                   /* LINEAR, CONV */
   int32_t classes;                    /* SOFTMAX_CE: number of classes (= its input channels) */
   int32_t stride;                     /* CONV: 1 or 2 (0 reads as 1); others 0 or 1 */
+  int32_t kw;                         /* CONV kernel width (odd, 1..7; 0 reads as k) */
+  int32_t pad;                        /* CONV, MAXPOOL3S2: 0 zero padding ("same": k/2, kw/2;
+                                         1 for the pool), 1 none ("valid") */
 } xpipe_layer_desc;
 
 /* Optimizer and prediction hyper-parameters (Sec. IV-C: gamma 0.9,

@@ -44,7 +44,8 @@ class LayerDesc(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("n_inputs", ctypes.c_int32),
                 ("inputs", ctypes.c_int32 * MAX_INPUTS), ("cin", ctypes.c_int32),
                 ("cout", ctypes.c_int32), ("k", ctypes.c_int32), ("has_bias", ctypes.c_int32),
-                ("classes", ctypes.c_int32), ("stride", ctypes.c_int32)]
+                ("classes", ctypes.c_int32), ("stride", ctypes.c_int32), ("kw", ctypes.c_int32),
+                ("pad", ctypes.c_int32)]
 
 
 class HParams(ctypes.Structure):
@@ -172,6 +173,8 @@ def layer_descs(layers: Sequence[dict]):
         d.has_bias = int(bool(L.get("bias", False)))
         d.classes = int(L.get("classes", 0))
         d.stride = int(L.get("stride", 1))
+        d.kw = int(L.get("kw", d.k))
+        d.pad = {"same": 0, "valid": 1}[L.get("pad", "same")]
     return arr
 
 

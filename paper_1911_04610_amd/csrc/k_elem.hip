@@ -967,10 +967,10 @@ __global__ __launch_bounds__(256) void k_avgpool3_v(PoolArgs a, const T* src, in
   }
 }
 
-// 3x3 / stride 2 / padding 1 max pool over groups of N channels (16-byte
-// chunks, or single channels).  Padding is never chosen: the window centre
-// (2ho, 2wo) is always inside.  Ties go to the first maximum in row-major
-// window order (strict > while scanning).
+// 3x3 / stride 2 max pool, padding p = 1 (never chosen: the window centre
+// (2ho, 2wo) is always inside) or 0 (valid), over groups of N channels
+// (16-byte chunks, or single channels).  Ties go to the first maximum in
+// row-major window order (strict > while scanning).
 template <typename T, int N>
 XP_DEV void ldn(const T* p, double* v) {
   if constexpr (N == VT<T>::N) vld(p, v);
@@ -998,13 +998,14 @@ __global__ __launch_bounds__(256) void k_maxpool3s2_fwd(PoolArgs a, int Ho, int 
   const int ho = (int)(it % Ho), n = (int)(it / Ho);
   const int c0 = g * N;
   const T* X = (const T*)a.x;
+  const int p = a.valid ? 0 : 1;
   double best[N];
   bool have = false;
   for (int r = 0; r < 3; ++r) {
-    const int h = 2 * ho - 1 + r;
+    const int h = 2 * ho - p + r;
     if (h < 0 || h >= a.H) continue;
     for (int q = 0; q < 3; ++q) {
-      const int w = 2 * wo - 1 + q;
+      const int w = 2 * wo - p + q;
       if (w < 0 || w >= a.W) continue;
       double v[N];
       ldn<T, N>(X + ((size_t)(n * a.H + h) * a.W + w) * a.ldx + c0, v);
@@ -1032,20 +1033,23 @@ __global__ __launch_bounds__(256) void k_maxpool3s2_bwd(PoolArgs a, int Ho, int 
   const int c0 = g * N;
   const T* X = (const T*)a.x;
   const T* DY = (const T*)a.dy;
+  const int pd = a.valid ? 0 : 1;
   double acc[N];
 #pragma unroll
   for (int e = 0; e < N; ++e) acc[e] = 0.0;
-  const int ho1 = min((h + 1) / 2, Ho - 1), wo1 = min((w + 1) / 2, Wo - 1);
-  for (int ho = h / 2; ho <= ho1; ++ho)
-    for (int wo = w / 2; wo <= wo1; ++wo) {
+  // windows 2ho - p .. 2ho - p + 2 that contain row h: ho from ceil((h + p - 2) / 2)
+  const int ho0 = max(0, (h + pd - 1) / 2), wo0 = max(0, (w + pd - 1) / 2);
+  const int ho1 = min((h + pd) / 2, Ho - 1), wo1 = min((w + pd) / 2, Wo - 1);
+  for (int ho = ho0; ho <= ho1; ++ho)
+    for (int wo = wo0; wo <= wo1; ++wo) {
       double best[N];
       int arg[N];
       bool have = false;
       for (int r = 0; r < 3; ++r) {
-        const int hh = 2 * ho - 1 + r;
+        const int hh = 2 * ho - pd + r;
         if (hh < 0 || hh >= a.H) continue;
         for (int q = 0; q < 3; ++q) {
-          const int ww = 2 * wo - 1 + q;
+          const int ww = 2 * wo - pd + q;
           if (ww < 0 || ww >= a.W) continue;
           double v[N];
           ldn<T, N>(X + ((size_t)(n * a.H + hh) * a.W + ww) * a.ldx + c0, v);
@@ -1084,7 +1088,9 @@ __global__ __launch_bounds__(256) void k_maxpool3s2_bwd(PoolArgs a, int Ho, int 
 
 template <typename T>
 static hipError_t maxpool3s2_go(const PoolArgs& a, bool bwd, hipStream_t s) {
-  const int Ho = (a.H - 1) / 2 + 1, Wo = (a.W - 1) / 2 + 1;
+  const int p = a.valid ? 0 : 1;
+  const int Ho = (a.H + 2 * p - 3) / 2 + 1, Wo = (a.W + 2 * p - 3) / 2 + 1;
+  if (Ho <= 0 || Wo <= 0) return hipErrorInvalidValue;
   constexpr int V = VT<T>::N;
   const bool vec = vec_ok<T>(a.C, {{a.x, a.ldx}, {a.out, a.ldo}, {a.dy, a.lddy}, {a.mask, a.ldm}});
   const int64_t pix = bwd ? (int64_t)a.nb * a.H * a.W : (int64_t)a.nb * Ho * Wo;

@@ -131,8 +131,8 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int H = a.H, W = a.W, C = a.C, S = a.S, pad = a.pad;
-  // the GEMM rows: the input grid for stride 1, else the Ho x Wo grid
+  const int H = a.H, W = a.W, C = a.C, S = a.S, pad = a.pad, padw = a.padw;
+  // the GEMM rows: the input grid for GM 0, else the Ho x Wo grid
   const int Ho = GM ? a.Ho : H, Wo = GM ? a.Wo : W;
   const int sd = GM ? a.stride : 1;
   const int M = a.nb * Ho * Wo;
@@ -192,7 +192,7 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
       // (-(r / sd), -(q / sd)) (GM 2); 32-bit wrap-around makes a base one row
       // past the image harmless, since only in-image taps use it
       const int bh = GM == 2 ? (a_h[i] + pad) / sd : a_h[i] * sd;
-      const int bw = GM == 2 ? (a_w[i] + pad) / sd : a_w[i] * sd;
+      const int bw = GM == 2 ? (a_w[i] + padw) / sd : a_w[i] * sd;
       a_off[i] = (uint32_t)((((size_t)(a_img[i] * H + bh) * W + bw) * a.ldx + a_kc[i] * VEC) *
                             sizeof(T));
       uint32_t hm = 0, wm = 0;
@@ -203,14 +203,14 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
             hm |= (uint32_t)(t >= 0 && t % sd == 0 && t / sd < H) << r;
           }
           for (int q = 0; q < S; ++q) {
-            const int t = a_w[i] + pad - q;
+            const int t = a_w[i] + padw - q;
             wm |= (uint32_t)(t >= 0 && t % sd == 0 && t / sd < W) << q;
           }
         } else {
           for (int r = 0; r < a.R; ++r)
             hm |= (uint32_t)((unsigned)(bh + r - pad) < (unsigned)H) << r;
           for (int q = 0; q < S; ++q)
-            wm |= (uint32_t)((unsigned)(bw + q - pad) < (unsigned)W) << q;
+            wm |= (uint32_t)((unsigned)(bw + q - padw) < (unsigned)W) << q;
         }
       }
       a_hm[i] = hm;
@@ -238,7 +238,7 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
       (void)kb;
       const int crem = C - lcb * BK;  // channels left in this tap from this block on
       const int tr_ = GM == 2 ? -(lr / sd) : lr - pad;
-      const int tq_ = GM == 2 ? -(lq / sd) : lq - pad;
+      const int tq_ = GM == 2 ? -(lq / sd) : lq - padw;
       const int dx = ((tr_ * W + tq_) * a.ldx + lcb * BK) * (int)sizeof(T);
       const uint32_t dw = (uint32_t)((lrs * C + lcb * BK) * (int)sizeof(T));
 #pragma unroll
@@ -277,13 +277,13 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
             int hh, ww;
             bool in;
             if constexpr (GM == 2) {
-              const int th = a_h[i] + pad - r, tw = a_w[i] + pad - s;
+              const int th = a_h[i] + pad - r, tw = a_w[i] + padw - s;
               in = th >= 0 && tw >= 0 && th % sd == 0 && tw % sd == 0;
               hh = th / sd;
               ww = tw / sd;
             } else {
               hh = a_h[i] * sd + r - pad;
-              ww = a_w[i] * sd + s - pad;
+              ww = a_w[i] * sd + s - padw;
               in = true;
             }
             if (in && hh >= 0 && hh < H && ww >= 0 && ww < W)
@@ -731,11 +731,12 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int H = a.H, W = a.W, C = a.C, S = a.S, pad = a.pad, N = a.N;
-  // dz pixels: the input grid, or the Ho x Wo grid of a strided convolution
+  const int H = a.H, W = a.W, C = a.C, S = a.S, pad = a.pad, padw = a.padw, N = a.N;
+  // dz pixels: the input grid, or the Ho x Wo grid of a strided or unpadded
+  // convolution
   const int sd = a.stride > 1 ? a.stride : 1;
-  const int Wo = sd > 1 ? a.Wo : W;
-  const int HW = (sd > 1 ? a.Ho : H) * Wo;
+  const int Wo = a.Ho > 0 ? a.Wo : W;
+  const int HW = (a.Ho > 0 ? a.Ho : H) * Wo;
   const int M = a.nb * HW;
   const int K = a.R * S * C;
   const int n0 = blockIdx.x * BM, k0 = blockIdx.y * BN;
@@ -806,7 +807,7 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
           h *= sd;
           ww0 *= sd;
           if constexpr (!FLAT) {
-            int hh = h + b_r[i] - pad, ww = ww0 + b_s[i] - pad;
+            int hh = h + b_r[i] - pad, ww = ww0 + b_s[i] - padw;
             if (b_kok[i] && hh >= 0 && hh < H && ww >= 0 && ww < W)
               v = *reinterpret_cast<const uint4*>(x + ((size_t)(img * H + hh) * W + ww) * a.ldx + b_ch[i]);
           } else {
@@ -817,7 +818,7 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
               T val = zero_elem<T>();
               if (k < K) {
                 int rs = k / C, c = k - rs * C, r = rs / S, s = rs - r * S;
-                int hh = h + r - pad, ww = ww0 + s - pad;
+                int hh = h + r - pad, ww = ww0 + s - padw;
                 if (hh >= 0 && hh < H && ww >= 0 && ww < W)
                   val = x[((size_t)(img * H + hh) * W + ww) * a.ldx + c];
               }
@@ -1329,6 +1330,7 @@ static const char* kname(const char* base) {
 
 template <typename T, int BM, int BN, int WM, int WN, int KS, int PF = 1, int GM = 0>
 static hipError_t conv_go(const ConvArgs& a, bool flat, hipStream_t s, int* grid_rows = nullptr) {
+  static_assert(GM >= 0 && GM <= 2, "gather mode");
   int M = a.nb * (GM ? a.Ho * a.Wo : a.H * a.W);
   dim3 grid((M + BM - 1) / BM, (a.N + BN - 1) / BN);
   if (grid_rows) *grid_rows = (int)grid.x;
@@ -1345,8 +1347,10 @@ static hipError_t conv_go(const ConvArgs& a, bool flat, hipStream_t s, int* grid
 }
 
 template <typename T>
-static hipError_t conv_dispatch(const ConvArgs& a, hipStream_t s, int* gr) {
+static hipError_t conv_dispatch(const ConvArgs& a0, hipStream_t s, int* gr) {
   constexpr int VEC = MT<T>::VEC;
+  ConvArgs a = a0;
+  if (a.stride < 1) a.stride = 1;
   const size_t M = (size_t)a.nb * a.H * a.W;
   // the 16-byte chunk path addresses both operands with 32-bit buffer offsets
   const bool spans = ((M - 1) * a.ldx + a.C) * sizeof(T) < ((size_t)1 << 31) &&
@@ -1355,8 +1359,9 @@ static hipError_t conv_dispatch(const ConvArgs& a, hipStream_t s, int* gr) {
               (reinterpret_cast<uintptr_t>(a.x) % 16) != 0 ||
               (reinterpret_cast<uintptr_t>(a.w) % 16) != 0 || !spans;
   const bool narrow = a.N <= 32;
-  if (a.tr || a.stride > 1) {
-    // strided layers (ResNet stem, first blocks, projections): general tiles
+  if (a.tr || a.Ho > 0) {
+    // strided or unpadded layers (ResNet-101 stem, first blocks, projections;
+    // Inception-V3 stem and grid reductions): general tiles
     if constexpr (sizeof(T) == 2) {
       if (a.tr) {
         if (narrow) return conv_go<T, 64, 32, 2, 2, 1, 2, 2>(a, flat, s, gr);
@@ -1472,7 +1477,7 @@ template <typename T, int BM, int BN, int WM, int WN>
 static hipError_t wgrad_go(const WgradArgs& a, bool flat, hipStream_t s) {
   int K = a.R * a.S * a.C;
   dim3 grid((a.N + BM - 1) / BM, (K + BN - 1) / BN, a.splits);
-  const int pix = a.stride > 1 ? a.Ho * a.Wo : a.H * a.W;
+  const int pix = a.Ho > 0 ? a.Ho * a.Wo : a.H * a.W;
   double flops = 2.0 * a.nb * pix * (double)a.N * K;
   if (flat)
     XP_LAUNCH((kname<T, BM, BN, WM, WN, true>("k_wgrad")), flops, (k_wgrad<T, BM, BN, WM, WN, true>),
@@ -1504,7 +1509,8 @@ static hipError_t wgrad_dispatch(const WgradArgs& a, hipStream_t s) {
   bool n64 = a.N <= 64, k64 = K <= 64;
   if constexpr (sizeof(T) == 2) {
     const int M = a.nb * a.H * a.W;
-    const bool chunks = !flat && a.stride <= 1 && (a.N % VEC) == 0 && (a.lddz % VEC) == 0 &&
+    // the pixel-pair kernel assumes the same grid and square padding
+    const bool chunks = !flat && a.Ho <= 0 && a.pad == a.padw && (a.N % VEC) == 0 && (a.lddz % VEC) == 0 &&
                         (reinterpret_cast<uintptr_t>(a.dz) % 16) == 0 &&
                         (((size_t)(M - 1)) * a.lddz + a.N) * sizeof(T) < ((size_t)1 << 31) &&
                         (((size_t)(M - 1)) * a.ldx + a.C) * sizeof(T) < ((size_t)1 << 31);

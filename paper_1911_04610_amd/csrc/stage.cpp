@@ -84,6 +84,9 @@ struct Op {
   bool relu = false;
   // GEMM
   int cin = 0, cout = 0, k = 1, stride = 1;
+  int kw = 1, ph = 0, pw = 0;       // kernel width, row / column zero padding
+  bool grid = false;                // output grid differs from the input's (strided or unpadded)
+  bool valid = false;               // 3x3 stride-2 max pool without padding
   int64_t w_off = -1, b_off = -1;   // parameter offsets (elements)
   int64_t wd_off = -1;              // workspace bytes: flipped weights for the data gradient
   // GEMM over sibling layers that read the same input (merged launch): their
@@ -361,23 +364,33 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     switch (d.kind) {
       case XPIPE_LINEAR:
       case XPIPE_CONV: {
-        int k = d.kind == XPIPE_LINEAR ? 1 : d.k;
-        if (d.kind == XPIPE_LINEAR && (s.H != 1 || s.W != 1))
+        const bool lin = d.kind == XPIPE_LINEAR;
+        int k = lin ? 1 : d.k;
+        int kw = lin ? 1 : (d.kw > 0 ? d.kw : d.k);
+        if (lin && (s.H != 1 || s.W != 1))
           return fail(XPIPE_EINVAL, std::string(where) + "linear input must have H = W = 1");
-        if (k < 1 || k > 7 || (k % 2) == 0) return fail(XPIPE_EINVAL, std::string(where) + "bad kernel size");
-        if (d.stride < 0 || d.stride > 2 || (d.kind == XPIPE_LINEAR && d.stride > 1))
+        if (k < 1 || k > 7 || (k % 2) == 0 || kw < 1 || kw > 7 || (kw % 2) == 0)
+          return fail(XPIPE_EINVAL, std::string(where) + "bad kernel size");
+        if (d.stride < 0 || d.stride > 2 || (lin && d.stride > 1))
           return fail(XPIPE_EINVAL, std::string(where) + "stride must be 1 or 2 (convolutions only)");
+        if (d.pad < 0 || d.pad > 1 || (lin && d.pad != 0))
+          return fail(XPIPE_EINVAL, std::string(where) + "pad must be 0 (same) or 1 (none), convolutions only");
         if (d.cin != s.C || d.cout <= 0) return fail(XPIPE_EINVAL, std::string(where) + "channel mismatch");
         poff[i] = P;
-        P += align_up((int64_t)d.cout * k * k * d.cin, PARAM_ALIGN);
+        P += align_up((int64_t)d.cout * k * kw * d.cin, PARAM_ALIGN);
         if (d.has_bias) {
           poff2[i] = P;
           P += align_up(d.cout, PARAM_ALIGN);
         }
         s.C = d.cout;
-        if (d.stride == 2) {
-          s.H = (s.H - 1) / 2 + 1;
-          s.W = (s.W - 1) / 2 + 1;
+        {
+          const int st_ = d.stride == 2 ? 2 : 1;
+          const int ph = d.pad ? 0 : k / 2, pw = d.pad ? 0 : kw / 2;
+          const int Ho = (s.H + 2 * ph - k) / st_ + 1, Wo = (s.W + 2 * pw - kw) / st_ + 1;
+          if (s.H + 2 * ph < k || s.W + 2 * pw < kw || Ho < 1 || Wo < 1)
+            return fail(XPIPE_EINVAL, std::string(where) + "input smaller than the kernel");
+          s.H = Ho;
+          s.W = Wo;
         }
         break;
       }
@@ -403,10 +416,15 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
         break;
       case XPIPE_AVGPOOL3:
         break;
-      case XPIPE_MAXPOOL3S2:
-        s.H = (s.H - 1) / 2 + 1;
-        s.W = (s.W - 1) / 2 + 1;
+      case XPIPE_MAXPOOL3S2: {
+        if (d.pad < 0 || d.pad > 1) return fail(XPIPE_EINVAL, std::string(where) + "bad pool padding");
+        const int p_ = d.pad ? 0 : 1;
+        if (s.H + 2 * p_ < 3 || s.W + 2 * p_ < 3)
+          return fail(XPIPE_EINVAL, std::string(where) + "maxpool input too small");
+        s.H = (s.H + 2 * p_ - 3) / 2 + 1;
+        s.W = (s.W + 2 * p_ - 3) / 2 + 1;
         break;
+      }
       case XPIPE_GAP:
         s.H = 1;
         s.W = 1;
@@ -442,8 +460,9 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
   for (int i = 0; i < n; ++i) {
     const xpipe_layer_desc& d = L[i];
     if (d.kind == XPIPE_LINEAR || d.kind == XPIPE_CONV) {
-      int k = d.kind == XPIPE_LINEAR ? 1 : d.k;
-      p.params.push_back({poff[i], (int64_t)d.cout * k * k * d.cin});
+      const int k = d.kind == XPIPE_LINEAR ? 1 : d.k;
+      const int kw = d.kind == XPIPE_LINEAR ? 1 : (d.kw > 0 ? d.kw : d.k);
+      p.params.push_back({poff[i], (int64_t)d.cout * k * kw * d.cin});
       if (d.has_bias) p.params.push_back({poff2[i], d.cout});
     } else if (d.kind == XPIPE_BN) {
       p.params.push_back({poff[i], d.cout});
@@ -490,7 +509,11 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
         op.cin = d.cin;
         op.cout = d.cout;
         op.k = d.kind == XPIPE_LINEAR ? 1 : d.k;
+        op.kw = d.kind == XPIPE_LINEAR ? 1 : (d.kw > 0 ? d.kw : d.k);
         op.stride = d.stride == 2 ? 2 : 1;
+        op.ph = d.pad ? 0 : op.k / 2;
+        op.pw = d.pad ? 0 : op.kw / 2;
+        op.grid = op.stride > 1 || d.pad != 0;
         op.w_off = poff[i];
         op.b_off = d.has_bias ? poff2[i] : -1;
         int r = single_consumer(i, XPIPE_RELU);
@@ -543,7 +566,10 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
         break;
       }
       case XPIPE_MAXPOOL2: op.kind = OP_MAXPOOL; break;
-      case XPIPE_MAXPOOL3S2: op.kind = OP_MAXPOOL3; break;
+      case XPIPE_MAXPOOL3S2:
+        op.kind = OP_MAXPOOL3;
+        op.valid = d.pad != 0;
+        break;
       case XPIPE_AVGPOOL3: op.kind = OP_AVGPOOL; break;
       case XPIPE_GAP: op.kind = OP_GAP; break;
       case XPIPE_CONCAT: op.kind = OP_CONCAT; break;
@@ -569,8 +595,14 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     if (op.in2 >= 0) p.tensors[op.in2].consumers++;
   }
 
-  // ---- concat views
+  // ---- concat views.  A max pool of ReLU outputs counts as masked: where its
+  // output is 0 the whole window is 0, so masking its gradient there changes
+  // nothing below the pool (the pooled ReLU outputs mask it anyway).
   for (const Op& op : p.ops) {
+    if (op.kind == OP_MAXPOOL || op.kind == OP_MAXPOOL3) {
+      p.tensors[op.out].masked = p.tensors[op.in].masked;
+      continue;
+    }
     if (op.kind != OP_CONCAT) continue;
     int coff = 0;
     bool all_masked = true, any_masked = false;
@@ -635,7 +667,8 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     std::vector<size_t> sib{i};
     for (size_t j = i + 1; j < p.ops.size() && sib.size() < (size_t)GATHER_MAX_SEGS; ++j)
       if (mergeable(p.ops[j]) && p.ops[j].in == p.ops[i].in && p.ops[j].k == p.ops[i].k &&
-          p.ops[j].stride == p.ops[i].stride)
+          p.ops[j].kw == p.ops[i].kw && p.ops[j].stride == p.ops[i].stride &&
+          p.ops[j].grid == p.ops[i].grid)
         sib.push_back(j);
     if (sib.size() < 2) continue;
     Op m = p.ops[i];
@@ -731,14 +764,14 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
   for (Op& op : p.ops) {
     const Tensor& tin_ = p.tensors[op.in];
     if (op.kind == OP_GEMM) {
-      op.wd_off = take((size_t)op.cout * op.k * op.k * op.cin * esz);
+      op.wd_off = take((size_t)op.cout * op.k * op.kw * op.cin * esz);
       if (!op.segs.empty())
         for (int d = 0; d < 2; ++d)
-          op.wg_off[d] = take((size_t)op.cout * op.k * op.k * op.cin * esz);
+          op.wg_off[d] = take((size_t)op.cout * op.k * op.kw * op.cin * esz);
       if (op.stats) op.stat_block = take((size_t)4 * op.cout * sizeof(double));
       int M = (int)p.tensors[op.out].sh.rows();  // output pixels (the input's for stride 1)
-      int K = op.k * op.k * op.cin;
-      int splits = wgrad_pick_splits(dtype, M, op.cout, K, op.k * op.k);
+      int K = op.k * op.kw * op.cin;
+      int splits = wgrad_pick_splits(dtype, M, op.cout, K, op.k * op.kw);
       wpart = std::max(wpart, wgrad_part_bytes(dtype, op.cout, K, splits));
       if (op.b_off >= 0) colpart = std::max(colpart, col_partial_bytes(M, op.cout));
       if (op.stats)
@@ -855,9 +888,6 @@ const float* fp32_param(xpipe_stage* st, int64_t off, int dir) {
   return (dir == XPIPE_FWD ? st->wpf : st->wpb) + off;
 }
 
-double gemm_flops(const Tensor& tin, const Op& op) {
-  return 2.0 * (double)tin.sh.rows() * op.cout * (double)op.k * op.k * op.cin;
-}
 
 // ---------------------------------------------------------------- lanes
 // One pass (forward or backward) over the ops, spread over the launch lanes.
@@ -998,12 +1028,14 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         a.W = tin.sh.W;
         a.C = op.cin;
         a.N = op.cout;
-        a.R = a.S = op.k;
-        a.pad = op.k / 2;
+        a.R = op.k;
+        a.S = op.kw;
+        a.pad = op.ph;
+        a.padw = op.pw;
         a.relu = op.relu;
         const Tensor& tout = st->tensors[op.out];
-        if (op.stride > 1) {
-          a.stride = op.stride;
+        a.stride = op.stride;
+        if (op.grid) {
           a.Ho = tout.sh.H;
           a.Wo = tout.sh.W;
         }
@@ -1095,6 +1127,7 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         pa.H = tin.sh.H;
         pa.W = tin.sh.W;
         pa.C = tin.sh.C;
+        pa.valid = op.valid;
         pa.part = (double*)(st->ws + st->colpart_off[lane]);
         if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_fwd(dt, pa, s));
         else if (op.kind == OP_MAXPOOL3) XP_HIP(launch_maxpool3s2_fwd(dt, pa, s));
@@ -1182,7 +1215,7 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         View g = gradv(st, op.out, c);
         const Tensor& tout = st->tensors[op.out];
         const int M = (int)tout.sh.rows();  // output pixels
-        const int K = op.k * op.k * op.cin;
+        const int K = op.k * op.kw * op.cin;
         // weight gradient, accumulated into grad
         WgradArgs w{};
         w.dz = g.p;
@@ -1207,14 +1240,16 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         w.W = tin.sh.W;
         w.C = op.cin;
         w.N = op.cout;
-        w.R = w.S = op.k;
-        w.pad = op.k / 2;
-        if (op.stride > 1) {
-          w.stride = op.stride;
+        w.R = op.k;
+        w.S = op.kw;
+        w.pad = op.ph;
+        w.padw = op.pw;
+        w.stride = op.stride;
+        if (op.grid) {
           w.Ho = tout.sh.H;
           w.Wo = tout.sh.W;
         }
-        w.splits = wgrad_pick_splits(dt, M, op.cout, K, op.k * op.k);
+        w.splits = wgrad_pick_splits(dt, M, op.cout, K, op.k * op.kw);
         {
           XP_HIP(launch_wgrad(dt, w, s));
         }
@@ -1244,10 +1279,12 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
           a.W = tin.sh.W;
           a.C = op.cout;
           a.N = op.cin;
-          a.R = a.S = op.k;
-          a.pad = op.k / 2;
+          a.R = op.k;
+          a.S = op.kw;
+          a.pad = op.ph;
+          a.padw = op.pw;
           a.accumulate = op.in_acc;
-          if (op.stride > 1) {
+          if (op.grid) {
             // rows: the input grid; gathered from the output gradient's grid,
             // with the transposed (unflipped) weights
             a.tr = 1;
@@ -1371,6 +1408,7 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         pa.H = tin.sh.H;
         pa.W = tin.sh.W;
         pa.C = tin.sh.C;
+        pa.valid = op.valid;
         if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_bwd(dt, pa, s));
         else if (op.kind == OP_MAXPOOL3) XP_HIP(launch_maxpool3s2_bwd(dt, pa, s));
         else if (op.kind == OP_AVGPOOL) XP_HIP(launch_avgpool_bwd(dt, pa, s));
@@ -1457,7 +1495,7 @@ xpipe_status refresh_gathered(xpipe_stage* st, int dir) {
     if (op.segs.empty()) continue;
     GatherArgs g{};
     g.nseg = (int)op.segs.size();
-    const int64_t K = (int64_t)op.k * op.k * op.cin;
+    const int64_t K = (int64_t)op.k * op.kw * op.cin;
     for (int q = 0; q < g.nseg; ++q) {
       const int64_t off = op.segs[q].first;
       if (st->dtype == DT_BF16)
@@ -1475,10 +1513,10 @@ xpipe_status refresh_gathered(xpipe_stage* st, int dir) {
 xpipe_status refresh_flipped(xpipe_stage* st) {
   for (const Op& op : st->ops) {
     if (op.kind != OP_GEMM) continue;
-    // stride 1: flipped (the data gradient is a convolution of dy); strided:
-    // transposed only (the data gradient gathers dy tap by tap)
+    // same grid: flipped (the data gradient is a convolution of dy); strided or
+    // unpadded: transposed only (the data gradient gathers dy tap by tap)
     XP_HIP(launch_flip_weights(st->dtype, gemm_weights(st, op, XPIPE_BWD), st->ws + op.wd_off,
-                               op.cout, op.k, op.k, op.cin, st->stream, op.stride == 1));
+                               op.cout, op.k, op.kw, op.cin, st->stream, !op.grid));
   }
   st->wd_valid = true;
   return XPIPE_OK;

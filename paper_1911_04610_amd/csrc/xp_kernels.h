@@ -88,17 +88,19 @@ struct ConvArgs {
   const float* bias;    // [N] or null
   const void* mask;     // optional view: y *= (mask > 0)
   int ldm;
-  int nb, H, W, C, N, R, S, pad;
+  int nb, H, W, C, N, R, S, pad;  // pad: rows (and columns when padw is unset)
   int relu;             // apply max(., 0) before storing
   int accumulate;       // y = y + result (after mask)
   double* stat_part;    // optional: per row tile, column sums of the stored y and of its
                         // squares, at stat_part[(n * 2 + {0,1}) * row_tiles + tile]
-  // strided convolution (stride > 1): the rows are an Ho x Wo grid per image.
-  // tr = 0: forward, row (ho, wo) reads x at (ho*stride + r - pad, wo*stride + q - pad);
+  // general grid (Ho > 0: strided, or unpadded): the rows are an Ho x Wo grid
+  // per image, stride >= 1.
+  // tr = 0: forward, row (ho, wo) reads x at (ho*stride + r - pad, wo*stride + q - padw);
   // tr = 1: data gradient, x is the output gradient (H x W), the rows the
   // input grid, and row (h, w) reads x at ((h + pad - r) / stride, ...) where
   // stride divides h + pad - r, with the weights transposed but not flipped
   int stride, Ho, Wo, tr;
+  int padw;             // column padding
 };
 
 // Weight gradient: part[split][n][k] = sum_{m in split} dz[m][n] * x~[m][k],
@@ -112,9 +114,10 @@ struct WgradArgs {
   float* grad;          // [N][K] fp32 accumulator
   int nb, H, W, C, N, R, S, pad;
   int splits;
-  // stride > 1: dz has Ho x Wo pixels per image, pixel (ho, wo) pairs with x at
-  // (ho*stride + r - pad, wo*stride + q - pad)
+  // general grid (Ho > 0): dz has Ho x Wo pixels per image, pixel (ho, wo)
+  // pairs with x at (ho*stride + r - pad, wo*stride + q - padw)
   int stride, Ho, Wo;
+  int padw;             // column padding
   // optional (nseg > 0): the N rows go to nseg accumulators in order, rows
   // [seg_row0[j], seg_row0[j + 1]) to seg_grad[j] (seg_row0[0] = 0, seg_row0[nseg] = N)
   int nseg;
@@ -210,6 +213,7 @@ struct PoolArgs {
   int accumulate;
   int nb, H, W, C;                 // input shape
   double* part;                    // GAP forward: workspace, gap_partial_bytes
+  int valid;                       // 3x3 stride-2 max pool: no padding
 };
 size_t gap_partial_bytes(int nb, int H, int W, int C);
 hipError_t launch_maxpool_fwd(int dtype, const PoolArgs& a, hipStream_t s);

@@ -203,6 +203,11 @@ def test_partition_moves_cuts_to_block_boundaries():
     # 105 weighted layers: ideal cuts before weighted layers 26, 52, 78; block
     # starts nearest to them are 24 (tie with 28, the earlier wins), 52 and 79
     assert [weighted.index(c) for c in f101[1:-1]] == [24, 52, 79]
+    V3 = wl.inception_v3_layers()
+    fv = xp.xpipe_partition(V3, 4)
+    _check_cuts(V3, fv)
+    # every cut falls between modules: right after a concat (or the stem's pool)
+    assert all(V3[c - 1]["kind"] in ("concat", "maxpool3s2") for c in fv[1:-1])
     I = wl.inception_stage_layers()
     fi = xp.xpipe_partition(I, 3)
     _check_cuts(I, fi)

@@ -20,12 +20,38 @@ from gpu_harness import run_stage
 pytestmark = pytest.mark.gpu
 
 
-def conv(x, cin, cout, k, bias=False, stride=1):
-    return dict(kind="conv", inputs=[x], cin=cin, cout=cout, k=k, bias=bias, stride=stride)
+def conv(x, cin, cout, k, bias=False, stride=1, kw=None, pad="same"):
+    L = dict(kind="conv", inputs=[x], cin=cin, cout=cout, k=k, bias=bias, stride=stride)
+    if kw is not None:
+        L["kw"] = kw
+    if pad != "same":
+        L["pad"] = pad
+    return L
 
 
 def bn(x, c):
     return dict(kind="bn", inputs=[x], cin=c, cout=c)
+
+
+def _module(kind):
+    """Small Inception-V3 grid-reduction B or E module after a conv + BN + ReLU."""
+    b = wl._Builder()
+    x = b.conv_bn_relu(-1, 16, 32, 1)
+    if kind == "B":
+        b1 = b.conv_bn_relu(x, 32, 24, 3, stride=2, pad="valid")
+        b2 = b.conv_bn_relu(b.conv_bn_relu(b.conv_bn_relu(x, 32, 16, 1), 16, 24, 3), 24, 24, 3,
+                            stride=2, pad="valid")
+        b3 = b.add(kind="maxpool3s2", inputs=[x], pad="valid")
+        b.add(kind="concat", inputs=[b1, b2, b3])
+    else:
+        b1 = b.conv_bn_relu(x, 32, 16, 1)
+        t = b.conv_bn_relu(x, 32, 24, 1)
+        b2 = b.add(kind="concat", inputs=[b.conv_bn_relu(t, 24, 16, 1, kw=3), b.conv_bn_relu(t, 24, 16, 3, kw=1)])
+        t = b.conv_bn_relu(b.conv_bn_relu(x, 32, 24, 1), 24, 16, 3)
+        b3 = b.add(kind="concat", inputs=[b.conv_bn_relu(t, 16, 16, 1, kw=3), b.conv_bn_relu(t, 16, 16, 3, kw=1)])
+        b4 = b.conv_bn_relu(b.add(kind="avgpool3", inputs=[x]), 32, 8, 1)
+        b.add(kind="concat", inputs=[b1, b2, b3, b4])
+    return b.layers
 
 
 LAYER_CASES = {
@@ -88,6 +114,20 @@ LAYER_CASES = {
     # the 3x3 stride-2 pool (its gradient masked by the ReLU)
     "resnet_stem": ([conv(-1, 3, 64, 7, stride=2), bn(0, 64), dict(kind="relu", inputs=[1]),
                      dict(kind="maxpool3s2", inputs=[2])], (30, 28, 3), 2),
+    # Inception-V3: factorised 1 x n / n x 1 kernels (same grid, padding on one
+    # axis), unpadded convolutions with and without stride, the unpadded pool
+    "conv1x7": ([conv(-1, 32, 48, 1, kw=7)], (9, 10, 32), 2),
+    "conv7x1": ([conv(-1, 48, 32, 7, kw=1)], (10, 9, 48), 2),
+    "conv1x3_bias": ([conv(-1, 64, 40, 1, True, kw=3)], (7, 8, 64), 2),
+    "conv3x3_valid": ([conv(-1, 32, 64, 3, pad="valid")], (11, 10, 32), 2),
+    "conv3x3_s2_valid": ([conv(-1, 64, 96, 3, stride=2, pad="valid")], (13, 12, 64), 2),
+    "conv3x3_s2_valid_c3_stem": ([conv(-1, 3, 32, 3, stride=2, pad="valid")], (23, 21, 3), 2),
+    "maxpool3s2_valid": ([dict(kind="maxpool3s2", inputs=[-1], pad="valid")], (13, 12, 64), 2),
+    "maxpool3s2_valid_c20": ([dict(kind="maxpool3s2", inputs=[-1], pad="valid")], (12, 11, 20), 2),
+    # grid reduction B: strided unpadded branches and a max-pool branch in one concat
+    "inception_b_module": (_module("B"), (11, 10, 16), 2),
+    # Inception-E: parallel 1x3 / 3x1 convolutions concatenated inside the module concat
+    "inception_e_module": (_module("E"), (6, 7, 16), 2),
     # first bottleneck of a group: strided 3x3, projection shortcut with BN
     # (stored), the last BN taking in the shortcut with the ReLU
     "resnet_block_projection": ([conv(-1, 64, 32, 1), bn(0, 32), dict(kind="relu", inputs=[1]),

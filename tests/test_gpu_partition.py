@@ -5,7 +5,8 @@ k) against the oracle's forward and backward of the unpartitioned network.
 fp32 storage, s = 0: logits, loss and every weight gradient within 2e-4.
 VGG-16 at 32 x 32 (CIFAR-10); ResNet-101 at 64 x 64 (its strided stem, pool,
 projections and 33 bottlenecks; 2 x 2 maps in the last group keep the
-micro-batch BNs well conditioned)."""
+micro-batch BNs well conditioned); Inception-V3 at 139 x 139 (3 x 3 maps in the
+last modules)."""
 import numpy as np
 import pytest
 
@@ -18,7 +19,8 @@ from gpu_harness import to_device, to_host
 pytestmark = pytest.mark.gpu
 
 
-NETS = {"vgg16": (wl.vgg16_layers, (32, 32, 3)), "resnet101": (wl.resnet101_layers, (64, 64, 3))}
+NETS = {"vgg16": (wl.vgg16_layers, (32, 32, 3)), "resnet101": (wl.resnet101_layers, (64, 64, 3)),
+        "inception_v3": (wl.inception_v3_layers, (139, 139, 3))}
 
 
 @pytest.mark.parametrize("net", list(NETS))

@@ -104,7 +104,19 @@ def vgg16_layers(classes=10) -> List[dict]:
 def split_layers(layers: List[dict], first: List[int]) -> List[List[dict]]:
     """Per-stage layer lists for stage boundaries `first` (first[k] = stage k's
     first layer, last entry = len(layers)): inputs re-indexed within the stage,
-    the previous stage's last layer becoming the stage input -1."""
+    the previous stage's last layer becoming the stage input -1.
+
+    A stage whose max pool reads the stage input, when the previous stage ends
+    in ReLU outputs (a ReLU or a concat of them), starts with a ReLU on its
+    input: the identity on those values, it marks the input as a ReLU output so
+    that a concat of the pool with ReLU branches (Inception-V3's grid
+    reductions) is masked as one tensor.  It changes no value and no weight
+    gradient; only the stage-input gradient at the input's zeros, which the
+    previous stage's ReLU zeroes anyway."""
+    def relu_out(j):
+        L = layers[j]
+        return L["kind"] == "relu" or (L["kind"] == "concat" and all(relu_out(q) for q in L["inputs"]))
+
     out = []
     for k in range(len(first) - 1):
         a, b = first[k], first[k + 1]
@@ -113,6 +125,14 @@ def split_layers(layers: List[dict], first: List[int]) -> List[List[dict]]:
             L = dict(L)
             L["inputs"] = [-1 if (j == a - 1 or j == -1) else j - a for j in L["inputs"]]
             stage.append(L)
+        pools_input = any(L["kind"] in ("maxpool2", "maxpool3s2") and L["inputs"] == [-1] for L in stage)
+        if a > 0 and pools_input and relu_out(a - 1):
+            shifted = [dict(kind="relu", inputs=[-1])]
+            for L in stage:
+                L = dict(L)
+                L["inputs"] = [j + 1 for j in L["inputs"]]  # -1 -> 0: the ReLU
+                shifted.append(L)
+            stage = shifted
         out.append(stage)
     return out
 

@@ -128,6 +128,14 @@ LAYER_CASES = {
     "inception_b_module": (_module("B"), (11, 10, 16), 2),
     # Inception-E: parallel 1x3 / 3x1 convolutions concatenated inside the module concat
     "inception_e_module": (_module("E"), (6, 7, 16), 2),
+    # degenerate cases: BN over one sample per channel (variance exactly 0,
+    # x_hat = 0, zero input gradient), micro-batch 1, a 7x7 kernel on a 2x2
+    # map (padding dominates), strided and unpadded layers down to 1x1 maps
+    "bn_single_sample": ([conv(-1, 16, 16, 1), bn(0, 16), dict(kind="relu", inputs=[1])], (1, 1, 16), 1),
+    "micro_batch_1": ([conv(-1, 32, 32, 3), bn(0, 32), dict(kind="relu", inputs=[1])], (5, 4, 32), 1),
+    "conv7x7_on_2x2": ([conv(-1, 16, 24, 7, True)], (2, 2, 16), 2),
+    "to_1x1_maps": ([conv(-1, 16, 32, 3, stride=2), conv(0, 32, 32, 3, pad="valid"),
+                     dict(kind="maxpool3s2", inputs=[1])], (5, 6, 16), 2),
     # first bottleneck of a group: strided 3x3, projection shortcut with BN
     # (stored), the last BN taking in the shortcut with the ReLU
     "resnet_block_projection": ([conv(-1, 64, 32, 1), bn(0, 32), dict(kind="relu", inputs=[1]),

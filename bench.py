@@ -421,7 +421,7 @@ def cpu_baseline(w, dtype):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs one pipeline stage on one GPU; --gpus must be 1 "
+        print(json.dumps({"error": "this library runs one pipeline stage on one GPU; --gpus must be 1 "
                                    "(each pipeline stage would run as its own one-GPU process)"}))
         sys.exit(2)
     if args.traffic_summarize:

@@ -44,7 +44,7 @@ typedef enum {
   XPIPE_EINVAL = 1,       /* invalid argument, shape or layer list */
   XPIPE_ESTATE = 2,       /* call out of order (see each entry point) */
   XPIPE_EHIP = 3,         /* a HIP runtime call or kernel launch failed */
-  XPIPE_EUNSUPPORTED = 4  /* valid but not supported by this build */
+  XPIPE_EUNSUPPORTED = 4  /* valid but not supported by this library */
 } xpipe_status;
 
 /* Storage format of activations and activation gradients.  Master weights,

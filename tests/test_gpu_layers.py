@@ -5,7 +5,7 @@ Each case runs one mini-batch of T = 2 micro-batches (forward, then backward
 with recomputation) and compares the stage output, the input gradient and
 the accumulated weight gradient with the oracle on identical inputs.  These
 stages have no chain of ReLU / max-pool decisions, so the bf16 variant is
-held to the spec bf16 bar (2e-2) against the oracle's bf16-storage
+held to the bf16 bar (relative L2 2e-2) against the oracle's bf16-storage
 model, and, where the stage has no ReLU or max-pool at all, against the exact
 (fp64) oracle too; the fp32
 variant is held to 2e-4 against the oracle's fp32-storage model."""

@@ -5,7 +5,7 @@ predictions) against the oracle, through the C ABI.
 The kernels compute in fp64 and round once to fp32, so each result must be
 the fp32 nearest to the oracle's fp64 value: at most 1 ulp apart, and only
 where the exact value lies within fp64 rounding of an fp32 tie.  The
-spec bar (relative L2 <= 2e-4) is asserted as well."""
+fp32 bar (relative L2 <= 2e-4) is asserted as well."""
 import numpy as np
 import pytest
 

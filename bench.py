@@ -324,6 +324,114 @@ def time_partitioned(args, net, stages=4, steps=10, warmup=3):
                     "pipeline's steady-state rate is bounded by its slowest stage"}
 
 
+def event_offset_us(reps=300):
+    """Per-launch offset of a start/stop event pair around one kernel: the
+    bracketed time of a ~10 us kernel minus its period when launched back to
+    back (then the kernel's own duration, as it is longer than the launch
+    floor).  Subtracted from the per-kernel event averages so they measure
+    what the kernel-trace profiler reports."""
+    import torch
+    t = torch.zeros(1 << 23, device="cuda")
+    s = torch.cuda.current_stream()
+    for _ in range(20):
+        t.add_(1)
+    torch.cuda.synchronize()
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(reps)]
+    for a, b in pairs:
+        a.record(s)
+        t.add_(1)
+        b.record(s)
+    torch.cuda.synchronize()
+    bracket = sum(a.elapsed_time(b) for a, b in pairs) / reps * 1e3
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(s)
+    for _ in range(reps):
+        t.add_(1)
+    b.record(s)
+    torch.cuda.synchronize()
+    period = a.elapsed_time(b) / reps * 1e3
+    return max(0.0, bracket - period), bracket, period
+
+
+def time_sweep(n, steps):
+    """Prediction and Adam over n flat fp32 parameters at t = 100."""
+    import numpy as np
+    import torch
+    import paper_1911_04610_amd as xp
+    import workloads as wl
+    s = wl.flat_state(n)
+    W, m, v, G = (torch.from_numpy(a).cuda() for a in (s.W, s.m, s.v, s.G))
+    out = torch.empty_like(W)
+    pf, pb = torch.empty_like(W), torch.empty_like(W)
+    hp = xp.Hyper()
+    res = {}
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    reps = max(3, steps)
+    for sv in (0, 1, 2, 3, 7):
+        ms = timed(lambda: xp.xpipe_predict_flat(W, m, v, out, None, sv, hp, 100), reps)
+        res[f"predict_s{sv}"] = {"ms": ms, "GB_s": 16.0 * n / ms / 1e6}
+    ms = timed(lambda: xp.xpipe_adam_flat(W, m, v, G, hp, 100, False), reps)
+    res["adam"] = {"ms": ms, "GB_s": 28.0 * n / ms / 1e6}
+    ms = timed(lambda: xp.xpipe_adam_flat(W, m, v, G, hp, 100, True, pf, 2, pb, 1), reps)
+    res["adam_zero_grad_2pred"] = {"ms": ms, "GB_s": 40.0 * n / ms / 1e6}
+    # the other update rules with Adam-moment prediction, fused the same way:
+    # momentum SGD 36 B/param (W, buf, m, v, G in; W, buf, m, v out) + zero + 2 predictions
+    # = 48; RMSProp adds the squared average (44 + 12 = 56)
+    buf, sq = (torch.from_numpy(a).cuda() for a in wl.rule_state(n))
+    rule = xp.Rule(rule=xp.RULE_MOMENTUM_SGD, lr=1e-2, momentum=0.9, weight_decay=5e-4)
+    ms = timed(lambda: xp.xpipe_rule_flat(W, buf, None, m, v, G, rule, hp, 100, True, pf, 2, pb, 1), reps)
+    res["momentum_sgd_zero_grad_2pred"] = {"ms": ms, "GB_s": 48.0 * n / ms / 1e6}
+    rule = xp.Rule(rule=xp.RULE_RMSPROP, lr=1e-4, momentum=0.9, alpha=0.99, eps=1e-8)
+    ms = timed(lambda: xp.xpipe_rule_flat(W, buf, sq, m, v, G, rule, hp, 100, True, pf, 2, pb, 1), reps)
+    res["rmsprop_zero_grad_2pred"] = {"ms": ms, "GB_s": 56.0 * n / ms / 1e6}
+    del W, m, v, G, out, pf, pb, buf, sq
+    torch.cuda.empty_cache()
+    return res
+
+
+def measured_peaks():
+    """Attainable peaks on this GPU from the library's probes: a 1 GiB 16-byte
+    copy (read + write bytes) and back-to-back bf16 MFMAs on registers."""
+    import torch
+    import paper_1911_04610_amd as xp
+
+    def timed(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    n = 1 << 30
+    src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    ms = timed(lambda: xp.xpipe_probe_copy(src, dst))
+    copy_gbs = 2.0 * n / (ms / 1e3) / 1e9
+    del src, dst
+    waves, iters = 256 * 4 * 2, 4096
+    out = torch.empty(waves, dtype=torch.float32, device="cuda")
+    ms = timed(lambda: xp.xpipe_probe_mfma(out, iters))
+    tflops = waves * iters * 8 * 32768.0 / (ms / 1e3) / 1e12
+    return {"hbm_copy_GB_s": round(copy_gbs, 1), "mfma_bf16_TFLOP_s": round(tflops, 1),
+            "copy_bytes": 2 * n, "mfma": "v_mfma_f32_32x32x16_bf16, %d waves x %d x 8" % (waves, iters)}
+
+
 def vendor_reference(reps=50):
     """The stage's two most frequent convolution shapes (32 x 35 x 35 NHWC,
     bf16) three ways, per launch, with HIP events over back-to-back launches:

@@ -544,21 +544,38 @@ __global__ __launch_bounds__(256) void k_colpart_v(ColArgs a) {
 #pragma unroll
       for (int e = 0; e < N; ++e) { mu[e] = a.mean[c0 + e]; rs[e] = a.rstd[c0 + e]; }
     }
-#pragma unroll 4
-    for (int r = r0 + g; r < r1; r += RG) {
-      double v[N];
-      vld(A + (size_t)r * a.lda + c0, v);
-      if (a.mode == COL_STATS) {
+    // rows r0 + g, r0 + g + RG, ... in order, four per trip with the trip's
+    // loads issued first
+    constexpr int U = 4;
+    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+    for (int rb = r0 + g; rb < r1; rb += U * RG) {
+      uint4 av[U], zv[U];
 #pragma unroll
-        for (int e = 0; e < N; ++e) { s0[e] += v[e]; s1[e] += v[e] * v[e]; }
-      } else if (a.mode == COL_BNBWD) {
-        double z[N];
-        vld(Z + (size_t)r * a.ldz + c0, z);
+      for (int u = 0; u < U; ++u) {
+        const int r = rb + u * RG;
+        av[u] = zv[u] = zero;
+        if (r < r1) {
+          av[u] = ld16(A + (size_t)r * a.lda + c0);
+          if (a.mode == COL_BNBWD) zv[u] = ld16(Z + (size_t)r * a.ldz + c0);
+        }
+      }
 #pragma unroll
-        for (int e = 0; e < N; ++e) { s0[e] += v[e]; s1[e] += v[e] * ((z[e] - mu[e]) * rs[e]); }
-      } else {
+      for (int u = 0; u < U; ++u) {
+        if (rb + u * RG >= r1) break;
+        double v[N];
+        cvt16<T>(av[u], v);
+        if (a.mode == COL_STATS) {
 #pragma unroll
-        for (int e = 0; e < N; ++e) s0[e] += v[e];
+          for (int e = 0; e < N; ++e) { s0[e] += v[e]; s1[e] += v[e] * v[e]; }
+        } else if (a.mode == COL_BNBWD) {
+          double z[N];
+          cvt16<T>(zv[u], z);
+#pragma unroll
+          for (int e = 0; e < N; ++e) { s0[e] += v[e]; s1[e] += v[e] * ((z[e] - mu[e]) * rs[e]); }
+        } else {
+#pragma unroll
+          for (int e = 0; e < N; ++e) s0[e] += v[e];
+        }
       }
     }
   }

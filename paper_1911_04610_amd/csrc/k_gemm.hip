@@ -1220,33 +1220,50 @@ XP_DEV float* grad_at(const GradDst& d, int64_t i, int64_t* seg_end) {
   return d.ptr[j] + (i - d.base[j]);
 }
 
+// Threads are (quad, split group): the G groups of a quad of 4 consecutive
+// elements add splits g, g + G, g + 2G, ... in order, then the first group
+// adds the G group sums in group order and accumulates into grad (fixed order
+// throughout: bit-reproducible).
+constexpr int SPLIT_GROUPS = 8;
 template <typename P>
 __global__ __launch_bounds__(256) void k_split_reduce(const P* __restrict__ part, int splits,
                                                        int64_t count, GradDst dst) {
-  const int64_t q = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (q >= count) return;
-  int64_t seg_end = 0;
-  float* g = grad_at(dst, q, &seg_end);
-  if (q + 4 <= seg_end) {
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+  constexpr int G = SPLIT_GROUPS, QPB = 256 / G;
+  __shared__ double sh[G][QPB][4];
+  const int qi = threadIdx.x % QPB, g = threadIdx.x / QPB;
+  const int64_t q = ((int64_t)blockIdx.x * QPB + qi) * 4;
+  double s[4] = {0.0, 0.0, 0.0, 0.0};
+  if (q + 4 <= count) {
 #pragma unroll 4
-    for (int z = 0; z < splits; ++z) {
+    for (int z = g; z < splits; z += G) {
       const P* p = part + (size_t)z * count + q;
-      s0 += (double)p[0];
-      s1 += (double)p[1];
-      s2 += (double)p[2];
-      s3 += (double)p[3];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s[e] += (double)p[e];
     }
-    g[0] = (float)((double)g[0] + s0);
-    g[1] = (float)((double)g[1] + s1);
-    g[2] = (float)((double)g[2] + s2);
-    g[3] = (float)((double)g[3] + s3);
+  } else if (q < count) {
+    for (int z = g; z < splits; z += G)
+      for (int e = 0; q + e < count; ++e) s[e] += (double)part[(size_t)z * count + q + e];
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) sh[g][qi][e] = s[e];
+  __syncthreads();
+  if (g != 0 || q >= count) return;
+  double t[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    t[e] = sh[0][qi][e];
+#pragma unroll
+    for (int k = 1; k < G; ++k) t[e] += sh[k][qi][e];
+  }
+  int64_t seg_end = 0;
+  float* gp = grad_at(dst, q, &seg_end);
+  if (q + 4 <= seg_end) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) gp[e] = (float)((double)gp[e] + t[e]);
   } else {
-    for (int64_t i = q; i < count && i < q + 4; ++i) {
-      double s = 0.0;
-      for (int z = 0; z < splits; ++z) s += (double)part[(size_t)z * count + i];
-      float* gi = grad_at(dst, i, &seg_end);
-      *gi = (float)((double)*gi + s);
+    for (int e = 0; e < 4 && q + e < count; ++e) {
+      float* gi = grad_at(dst, q + e, &seg_end);
+      *gi = (float)((double)*gi + t[e]);
     }
   }
 }
@@ -1454,7 +1471,7 @@ static hipError_t wgrad_reduce(const WgradArgs& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   const int K = a.R * a.S * a.C;
   int64_t count = (int64_t)a.N * K;
-  int blocks = (int)(((count + 3) / 4 + 255) / 256);
+  int blocks = (int)(((count + 3) / 4 + (256 / SPLIT_GROUPS) - 1) / (256 / SPLIT_GROUPS));
   typedef typename MT<T>::part_t P;
   GradDst d{};
   if (a.nseg > 0) {

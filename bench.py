@@ -62,10 +62,20 @@ def source_hash():
 
 def kernel_key(name):
     """Common key for rocprofv3's demangled kernel names and the library's
-    launch names: no namespace or arguments, storage types as bf16 / f32."""
+    launch names: no namespace or arguments, storage types as bf16 / f32, and
+    without the template arguments only the compiler's name shows (the GEMM's
+    gather mode, named by the library only when not 0; the row kernels' rows
+    per trip; the pools' channels per thread)."""
+    import re
     n = name.split("(")[0].replace("void ", "").replace("xp::", "")
     n = n.replace("unsigned short", "bf16").replace(" ", "")
-    return n.replace("<float", "<f32").replace(",float", ",f32")
+    n = n.replace("<float", "<f32").replace(",float", ",f32")
+    m = re.match(r"^k_conv_gemm<((?:[^,>]+,){7}[^,>]+),(\d)>$", n)
+    if m:
+        gm = int(m.group(2))
+        n = "k_conv_gemm<" + m.group(1) + ("" if gm == 0 else "," + ("strided", "strided_dgrad")[gm - 1]) + ">"
+    return re.sub(r"^(k_bn_apply_v|k_bn_bwd_v|k_maxpool3s2_fwd|k_maxpool3s2_bwd)<(bf16|f32),\d+>$",
+                  r"\1<\2>", n)
 
 
 def traffic_run(args):

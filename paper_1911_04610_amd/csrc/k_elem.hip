@@ -1036,7 +1036,10 @@ __global__ __launch_bounds__(256) void k_maxpool3s2_fwd(PoolArgs a, int Ho, int 
 }
 
 // backward: each input pixel gathers, in (ho, wo) order, the output gradients
-// of the (at most four) windows that contain it and chose it
+// of the (at most four) windows that contain it and chose it.  A window chose
+// the pixel when the pixel holds the window's maximum (the stored forward
+// output y) and no position before it in row-major window order does; the
+// earlier positions are read only when some channel of the chunk ties.
 template <typename T, int N>
 __global__ __launch_bounds__(256) void k_maxpool3s2_bwd(PoolArgs a, int Ho, int Wo) {
   const int groups = a.C / N;
@@ -1049,41 +1052,53 @@ __global__ __launch_bounds__(256) void k_maxpool3s2_bwd(PoolArgs a, int Ho, int 
   const int h = (int)(it % a.H), n = (int)(it / a.H);
   const int c0 = g * N;
   const T* X = (const T*)a.x;
+  const T* Y = (const T*)a.y;
   const T* DY = (const T*)a.dy;
   const int pd = a.valid ? 0 : 1;
-  double acc[N];
+  double xv[N], acc[N];
+  ldn<T, N>(X + ((size_t)(n * a.H + h) * a.W + w) * a.ldx + c0, xv);
 #pragma unroll
   for (int e = 0; e < N; ++e) acc[e] = 0.0;
-  // windows 2ho - p .. 2ho - p + 2 that contain row h: ho from ceil((h + p - 2) / 2)
+  // windows 2ho - pd .. 2ho - pd + 2 that contain row h: ho from ceil((h + pd - 2) / 2)
   const int ho0 = max(0, (h + pd - 1) / 2), wo0 = max(0, (w + pd - 1) / 2);
   const int ho1 = min((h + pd) / 2, Ho - 1), wo1 = min((w + pd) / 2, Wo - 1);
   for (int ho = ho0; ho <= ho1; ++ho)
     for (int wo = wo0; wo <= wo1; ++wo) {
-      double best[N];
-      int arg[N];
-      bool have = false;
-      for (int r = 0; r < 3; ++r) {
-        const int hh = 2 * ho - pd + r;
-        if (hh < 0 || hh >= a.H) continue;
+      const size_t o = (size_t)(n * Ho + ho) * Wo + wo;
+      double yv[N];
+      ldn<T, N>(Y + o * a.ldy + c0, yv);
+      bool cand[N], any = false;
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        cand[e] = xv[e] == yv[e];
+        any = any || cand[e];
+      }
+      if (!any) continue;
+      // an earlier position holding the maximum takes it instead
+      const int hs = 2 * ho - pd, ws = 2 * wo - pd;
+      for (int r = 0; r < 3 && any; ++r) {
+        const int hh = hs + r;
+        if (hh < 0 || hh >= a.H || hh > h) continue;
         for (int q = 0; q < 3; ++q) {
-          const int ww = 2 * wo - pd + q;
-          if (ww < 0 || ww >= a.W) continue;
+          const int ww = ws + q;
+          if (ww < 0 || ww >= a.W || (hh == h && ww >= w)) continue;
           double v[N];
           ldn<T, N>(X + ((size_t)(n * a.H + hh) * a.W + ww) * a.ldx + c0, v);
+          any = false;
 #pragma unroll
-          for (int e = 0; e < N; ++e)
-            if (!have || v[e] > best[e]) {
-              best[e] = v[e];
-              arg[e] = hh * a.W + ww;
-            }
-          have = true;
+          for (int e = 0; e < N; ++e) {
+            cand[e] = cand[e] && !(v[e] == yv[e]);
+            any = any || cand[e];
+          }
+          if (!any) break;
         }
       }
+      if (!any) continue;
       double d[N];
-      ldn<T, N>(DY + ((size_t)(n * Ho + ho) * Wo + wo) * a.lddy + c0, d);
+      ldn<T, N>(DY + o * a.lddy + c0, d);
 #pragma unroll
       for (int e = 0; e < N; ++e)
-        if (arg[e] == h * a.W + w) acc[e] += d[e];
+        if (cand[e]) acc[e] += d[e];
     }
   const size_t r = (size_t)(n * a.H + h) * a.W + w;
   if (a.mask) {
@@ -1109,7 +1124,9 @@ static hipError_t maxpool3s2_go(const PoolArgs& a, bool bwd, hipStream_t s) {
   const int Ho = (a.H + 2 * p - 3) / 2 + 1, Wo = (a.W + 2 * p - 3) / 2 + 1;
   if (Ho <= 0 || Wo <= 0) return hipErrorInvalidValue;
   constexpr int V = VT<T>::N;
-  const bool vec = vec_ok<T>(a.C, {{a.x, a.ldx}, {a.out, a.ldo}, {a.dy, a.lddy}, {a.mask, a.ldm}});
+  const bool vec = vec_ok<T>(a.C, {{a.x, a.ldx}, {a.out, a.ldo}, {a.dy, a.lddy}, {a.mask, a.ldm},
+                                   {a.y, a.ldy}});
+  if (bwd && !a.y) return hipErrorInvalidValue;  // the backward reads the forward output
   const int64_t pix = bwd ? (int64_t)a.nb * a.H * a.W : (int64_t)a.nb * Ho * Wo;
   const int64_t threads = pix * (vec ? a.C / V : a.C);
   const unsigned blocks = (unsigned)((threads + 255) / 256);

@@ -267,13 +267,14 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
 #pragma unroll
       for (int i = 0; i < A_PER; ++i) {
         T vals[VEC];
+        // (r, s, c) of the chunk's first k, then stepped element by element
+        const int kbase = kb * BK + a_kc[i] * VEC;
+        int r = kbase / (S * C), s = (kbase / C) % S, c = kbase % C;
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
-          int k = kb * BK + a_kc[i] * VEC + e;
+          const int k = kbase + e;
           T val = zero_elem<T>();
           if (a_valid[i] && k < K) {
-            int rs = k / C, c = k - rs * C;
-            int r = rs / S, s = rs - r * S;
             int hh, ww;
             bool in;
             if constexpr (GM == 2) {
@@ -290,6 +291,13 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
               val = x[((size_t)(a_img[i] * H + hh) * W + ww) * a.ldx + c];
           }
           vals[e] = val;
+          if (++c == C) {
+            c = 0;
+            if (++s == S) {
+              s = 0;
+              ++r;
+            }
+          }
         }
         ra[slot][i] = pack_chunk<T>(vals);
       }
@@ -767,10 +775,12 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
     b_p[i] = q / (BN / VEC);
     int kk = k0 + b_c[i] * VEC;
     b_kok[i] = kk < K;
-    int rs = FLAT ? 0 : kk / C;
-    b_ch[i] = FLAT ? 0 : kk - rs * C;
-    b_r[i] = FLAT ? 0 : rs / S;
-    b_s[i] = FLAT ? 0 : rs - b_r[i] * S;
+    // filter position and channel of the chunk's first k (the flat gather
+    // steps through the chunk from there)
+    int rs = kk / C;
+    b_ch[i] = kk - rs * C;
+    b_r[i] = rs / S;
+    b_s[i] = rs - b_r[i] * S;
   }
 
   uint4 ra[A_PER][RPT], rb[B_PER][RPT];
@@ -812,17 +822,24 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
               v = *reinterpret_cast<const uint4*>(x + ((size_t)(img * H + hh) * W + ww) * a.ldx + b_ch[i]);
           } else {
             T vals[VEC];
+            int r = b_r[i], s = b_s[i], c = b_ch[i];
 #pragma unroll
             for (int e = 0; e < VEC; ++e) {
               int k = k0 + b_c[i] * VEC + e;
               T val = zero_elem<T>();
               if (k < K) {
-                int rs = k / C, c = k - rs * C, r = rs / S, s = rs - r * S;
                 int hh = h + r - pad, ww = ww0 + s - padw;
                 if (hh >= 0 && hh < H && ww >= 0 && ww < W)
                   val = x[((size_t)(img * H + hh) * W + ww) * a.ldx + c];
               }
               vals[e] = val;
+              if (++c == C) {
+                c = 0;
+                if (++s == S) {
+                  s = 0;
+                  ++r;
+                }
+              }
             }
             v = pack_chunk<T>(vals);
           }

@@ -1409,6 +1409,13 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         pa.W = tin.sh.W;
         pa.C = tin.sh.C;
         pa.valid = op.valid;
+        if (op.kind == OP_MAXPOOL3) {
+          // the pool's output from the recomputed forward: a pixel takes a
+          // window's gradient when it holds the window's value first
+          View yv = act(st, op.out, c);
+          pa.y = yv.p;
+          pa.ldy = yv.ld;
+        }
         if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_bwd(dt, pa, s));
         else if (op.kind == OP_MAXPOOL3) XP_HIP(launch_maxpool3s2_bwd(dt, pa, s));
         else if (op.kind == OP_AVGPOOL) XP_HIP(launch_avgpool_bwd(dt, pa, s));

@@ -908,7 +908,12 @@ __global__ __launch_bounds__(256) void k_maxpool_bwd_v(PoolArgs a) {
 // once, then slides along the run keeping the vertical three-row sums of the
 // previous, current and next column:
 // out(h, w) = ((v(w-1) + v(w)) + v(w+1)) / 9, v(w) = (x(h-1, w) + x(h, w)) + x(h+1, w),
-// with zeros outside the image.
+// with zeros outside the image.  The kernel is bound by its arithmetic, not by
+// memory: fp32 storage computes in fp64 (one rounding on store, as everywhere
+// in that variant); bf16 storage computes in fp32, like the bf16 variant's
+// accumulations, at twice the rate and without conversions to fp64.
+template <typename T> struct AvgAcc { typedef double t; };
+template <> struct AvgAcc<bf16_t> { typedef float t; };
 constexpr int AVG_SEG = 7;
 template <typename T>
 __global__ __launch_bounds__(256) void k_avgpool3_v(PoolArgs a, const T* src, int ld_src) {
@@ -950,15 +955,28 @@ __global__ __launch_bounds__(256) void k_avgpool3_v(PoolArgs a, const T* src, in
       if (a.accumulate) old[j] = ld16(O + (rbase + w0 + j) * a.ldo + c0);
     }
   }
-  auto vsum = [&](int j, double* v) {
-    double q0[N], q1[N], q2[N];
-    cvt16<T>(win[0][j], q0);
-    cvt16<T>(win[1][j], q1);
-    cvt16<T>(win[2][j], q2);
+  typedef typename AvgAcc<T>::t A;
+  auto cvt = [&](uint4 u, A* v) {
+    if constexpr (sizeof(T) == 2) {
+      const uint32_t wd[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v[2 * i] = __uint_as_float(wd[i] << 16);
+        v[2 * i + 1] = __uint_as_float(wd[i] & 0xffff0000u);
+      }
+    } else {
+      cvt16<T>(u, v);
+    }
+  };
+  auto vsum = [&](int j, A* v) {
+    A q0[N], q1[N], q2[N];
+    cvt(win[0][j], q0);
+    cvt(win[1][j], q1);
+    cvt(win[2][j], q2);
 #pragma unroll
     for (int e = 0; e < N; ++e) v[e] = (q0[e] + q1[e]) + q2[e];
   };
-  double vp[N], vc[N], vn[N];
+  A vp[N], vc[N], vn[N];
   vsum(0, vp);
   vsum(1, vc);
 #pragma unroll
@@ -967,7 +985,7 @@ __global__ __launch_bounds__(256) void k_avgpool3_v(PoolArgs a, const T* src, in
     vsum(j + 2, vn);
     double s[N];
 #pragma unroll
-    for (int e = 0; e < N; ++e) s[e] = ((vp[e] + vc[e]) + vn[e]) / 9.0;
+    for (int e = 0; e < N; ++e) s[e] = (double)(((vp[e] + vc[e]) + vn[e]) / (A)9);
     if (MK) vmask_raw<T>(mk[j], s);
     if (a.accumulate) {
       double q[N];

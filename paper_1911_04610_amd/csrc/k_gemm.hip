@@ -965,7 +965,10 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
 // offsets read zeros), addresses advance by a scalar per step, each thread
 // tracks the image row / column of its pixels incrementally, and PF steps of
 // loads are in flight.
-template <int BM, int BN, int WM, int WN, int PF>
+// GRID: dz lives on the Ho x Wo grid of a strided or unpadded convolution (or
+// the rows and columns pad differently); each pixel then tracks its image, row
+// and column and addresses x at (ho*stride + r - pad, wo*stride + q - padw)
+template <int BM, int BN, int WM, int WN, int PF, bool GRID>
 __global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
   using T = bf16_t;
   constexpr int VEC = 8, BKm = 32, RPT = 2;
@@ -981,7 +984,11 @@ __global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int H = a.H, W = a.W, C = a.C, S = a.S, pad = a.pad, N = a.N;
-  const int M = a.nb * H * W;
+  const int padw = GRID ? a.padw : pad;
+  const int sd = GRID && a.stride > 1 ? a.stride : 1;
+  const int Ho = GRID && a.Ho > 0 ? a.Ho : H, Wo = GRID && a.Ho > 0 ? a.Wo : W;
+  const int M = a.nb * Ho * Wo;    // dz pixels
+  const int Min = a.nb * H * W;    // x pixels
   const int K = a.R * S * C;
   const int n0 = blockIdx.x * BM, k0 = blockIdx.y * BN;
   const int mps = ((M + a.splits - 1) / a.splits + BKm - 1) / BKm * BKm;
@@ -990,7 +997,7 @@ __global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
   const __amdgpu_buffer_rsrc_t dr = __builtin_amdgcn_make_buffer_rsrc(
       (void*)a.dz, (short)0, (int)((((size_t)(M - 1)) * a.lddz + N) * sizeof(T)), 0x00020000);
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)a.x, (short)0, (int)((((size_t)(M - 1)) * a.ldx + C) * sizeof(T)), 0x00020000);
+      (void*)a.x, (short)0, (int)((((size_t)(Min - 1)) * a.ldx + C) * sizeof(T)), 0x00020000);
 
   // A tasks (dz): pixel pair p, output-channel chunk c
   int a_p[A_PER], a_c[A_PER];
@@ -1007,8 +1014,8 @@ __global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
     a_off[i] = (uint32_t)((((size_t)mbeg + a_p[i] * RPT) * a.lddz + n) * sizeof(T));
   }
   // B tasks (x): pixel pair p, reduction chunk (tap r, s, channel ch)
-  int b_p[B_PER], b_c[B_PER], b_r[B_PER], b_s[B_PER];
-  int b_h[B_PER][RPT], b_w[B_PER][RPT];
+  int b_p[B_PER], b_c[B_PER], b_r[B_PER], b_s[B_PER], b_ch[B_PER];
+  int b_h[B_PER][RPT], b_w[B_PER][RPT], b_img[B_PER][RPT];
   uint32_t b_off[B_PER];
   bool b_slot[B_PER], b_kok[B_PER];
 #pragma unroll
@@ -1022,15 +1029,17 @@ __global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
     const int rs = b_kok[i] ? kk / C : 0, ch = b_kok[i] ? kk - rs * C : 0;
     b_r[i] = rs / S;
     b_s[i] = rs - b_r[i] * S;
+    b_ch[i] = ch;
     // byte offset of (first pixel of the pair at step 0, shifted by the tap)
     const long long pix = (long long)mbeg + b_p[i] * RPT + (b_r[i] - pad) * W + (b_s[i] - pad);
-    b_off[i] = (uint32_t)((pix * a.ldx + ch) * (long long)sizeof(T));
+    b_off[i] = GRID ? 0u : (uint32_t)((pix * a.ldx + ch) * (long long)sizeof(T));
 #pragma unroll
     for (int u = 0; u < RPT; ++u) {
       const int m = mbeg + b_p[i] * RPT + u;
-      const int rem = m % (H * W);
-      b_h[i][u] = rem / W;
-      b_w[i][u] = rem - b_h[i][u] * W;
+      const int rem = m % (Ho * Wo);
+      b_img[i][u] = m / (Ho * Wo);
+      b_h[i][u] = rem / Wo;
+      b_w[i][u] = rem - b_h[i][u] * Wo;
     }
   }
 
@@ -1055,18 +1064,25 @@ __global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
     for (int i = 0; i < B_PER; ++i)
 #pragma unroll
       for (int u = 0; u < RPT; ++u) {
-        const int hh = b_h[i][u] + b_r[i] - pad, ww = b_w[i][u] + b_s[i] - pad;
+        const int hh = b_h[i][u] * sd + b_r[i] - pad, ww = b_w[i][u] * sd + b_s[i] - padw;
         const bool ok = b_kok[i] && b_p[i] * RPT + u < left && (unsigned)hh < (unsigned)H &&
                         (unsigned)ww < (unsigned)W;
-        const uint32_t off =
-            ok ? b_off[i] + (uint32_t)(((size_t)mb + u) * a.ldx * sizeof(T)) : OUT_OF_RANGE;
+        uint32_t off;
+        if constexpr (GRID)
+          off = ok ? (uint32_t)(((((size_t)b_img[i][u] * H + hh) * W + ww) * a.ldx + b_ch[i]) * sizeof(T))
+                   : OUT_OF_RANGE;
+        else
+          off = ok ? b_off[i] + (uint32_t)(((size_t)mb + u) * a.ldx * sizeof(T)) : OUT_OF_RANGE;
         const auto v = __builtin_amdgcn_raw_buffer_load_b128(xr, (int)off, 0, 0);
         rb[slot][i][u] = make_uint4(v[0], v[1], v[2], v[3]);
         // advance this pixel by one step
         int w2 = b_w[i][u] + BKm, h2 = b_h[i][u];
-        while (w2 >= W) {
-          w2 -= W;
-          if (++h2 == H) h2 = 0;
+        while (w2 >= Wo) {
+          w2 -= Wo;
+          if (++h2 == Ho) {
+            h2 = 0;
+            if constexpr (GRID) ++b_img[i][u];
+          }
         }
         b_w[i][u] = w2;
         b_h[i][u] = h2;
@@ -1522,15 +1538,17 @@ static hipError_t wgrad_go(const WgradArgs& a, bool flat, hipStream_t s) {
   return wgrad_reduce<T>(a, s);
 }
 
-template <int BM, int BN, int WM, int WN, int PF>
+template <int BM, int BN, int WM, int WN, int PF, bool GRID = false>
 static hipError_t wgrad_b_go(const WgradArgs& a, hipStream_t s) {
   int K = a.R * a.S * a.C;
   dim3 grid((a.N + BM - 1) / BM, (K + BN - 1) / BN, a.splits);
-  double flops = 2.0 * a.nb * a.H * a.W * (double)a.N * K;
+  const int pix = a.Ho > 0 ? a.Ho * a.Wo : a.H * a.W;
+  double flops = 2.0 * a.nb * pix * (double)a.N * K;
   static char name[64];
-  snprintf(name, sizeof name, "k_wgrad_b<%d,%d,%d,%d,%d>", BM, BN, WM, WN, PF);
+  snprintf(name, sizeof name, GRID ? "k_wgrad_b<%d,%d,%d,%d,%d,grid>" : "k_wgrad_b<%d,%d,%d,%d,%d>", BM, BN,
+           WM, WN, PF);
   XP_LAUNCH(name, flops,
-            (k_wgrad_b<BM, BN, WM, WN, PF>), grid, dim3(256), 0, s, a);
+            (k_wgrad_b<BM, BN, WM, WN, PF, GRID>), grid, dim3(256), 0, s, a);
   return wgrad_reduce<bf16_t>(a, s);
 }
 
@@ -1542,13 +1560,15 @@ static hipError_t wgrad_dispatch(const WgradArgs& a, hipStream_t s) {
   int K = a.R * a.S * a.C;
   bool n64 = a.N <= 64, k64 = K <= 64;
   if constexpr (sizeof(T) == 2) {
-    const int M = a.nb * a.H * a.W;
-    // the pixel-pair kernel assumes the same grid and square padding
-    const bool chunks = !flat && a.Ho <= 0 && a.pad == a.padw && (a.N % VEC) == 0 && (a.lddz % VEC) == 0 &&
+    const int M = a.nb * (a.Ho > 0 ? a.Ho * a.Wo : a.H * a.W), Min = a.nb * a.H * a.W;
+    const bool chunks = !flat && (a.N % VEC) == 0 && (a.lddz % VEC) == 0 &&
                         (reinterpret_cast<uintptr_t>(a.dz) % 16) == 0 &&
                         (((size_t)(M - 1)) * a.lddz + a.N) * sizeof(T) < ((size_t)1 << 31) &&
-                        (((size_t)(M - 1)) * a.ldx + a.C) * sizeof(T) < ((size_t)1 << 31);
-    if (chunks) return wgrad_b_go<64, 64, 2, 2, 2>(a, s);
+                        (((size_t)(Min - 1)) * a.ldx + a.C) * sizeof(T) < ((size_t)1 << 31);
+    // same grid and square padding: pixel offsets shift with the pixel index;
+    // otherwise each pixel addresses x from its own row and column
+    if (chunks && a.Ho <= 0 && a.pad == a.padw) return wgrad_b_go<64, 64, 2, 2, 2>(a, s);
+    if (chunks) return wgrad_b_go<64, 64, 2, 2, 2, true>(a, s);
   }
   if (n64 && k64) return wgrad_go<T, 64, 64, 2, 2>(a, flat, s);
   if (n64) return wgrad_go<T, 64, 128, 2, 2>(a, flat, s);

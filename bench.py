@@ -64,8 +64,9 @@ def kernel_key(name):
     """Common key for rocprofv3's demangled kernel names and the library's
     launch names: no namespace or arguments, storage types as bf16 / f32, and
     without the template arguments only the compiler's name shows (the GEMM's
-    gather mode, named by the library only when not 0; the row kernels' rows
-    per trip; the pools' channels per thread)."""
+    gather mode, named by the library only when not 0; the weight gradient's
+    grid flag, named only when set; the row kernels' rows per trip; the
+    pools' channels per thread)."""
     import re
     n = name.split("(")[0].replace("void ", "").replace("xp::", "")
     n = n.replace("unsigned short", "bf16").replace(" ", "")
@@ -74,6 +75,9 @@ def kernel_key(name):
     if m:
         gm = int(m.group(2))
         n = "k_conv_gemm<" + m.group(1) + ("" if gm == 0 else "," + ("strided", "strided_dgrad")[gm - 1]) + ">"
+    m = re.match(r"^k_wgrad_b<((?:\d+,){4}\d+),(true|false)>$", n)
+    if m:
+        n = "k_wgrad_b<" + m.group(1) + (",grid>" if m.group(2) == "true" else ">")
     return re.sub(r"^(k_bn_apply_v|k_bn_bwd_v|k_maxpool3s2_fwd|k_maxpool3s2_bwd)<(bf16|f32),\d+>$",
                   r"\1<\2>", n)
 

@@ -13,6 +13,9 @@ namespace xp {
 
 thread_local LaunchHook* g_hook = nullptr;
 
+// threads per workgroup of the streaming passes (prediction, updates)
+constexpr int STREAM_BLOCK = 256;
+
 XP_DEV double pred_dir(double m, double v, const PredCoef& c) {
   double mh = m * c.c1, vh = v * c.c2;
   return c.eps_outside ? mh / (sqrt(vh) + c.eps) : mh / sqrt(vh + c.eps);
@@ -22,6 +25,21 @@ XP_DEV double pred_dir(double m, double v, const PredCoef& c) {
 XP_DEV float predict1(float w, float m, float v, const PredCoef& c) {
   if (c.coef == 0.0) return w;
   return (float)((double)w - c.coef * pred_dir((double)m, (double)v, c));
+}
+
+// both predictions of the fused update: one direction when the two
+// coefficient sets share it (same moments' scales and eps, s differs), the
+// same fp64 operations as two separate predict1 calls
+XP_DEV void predict2(float w, float m, float v, const PredCoef& cf, const PredCoef& cb, bool shared,
+                     float& rf, float& rb) {
+  if (!shared) {
+    rf = predict1(w, m, v, cf);
+    rb = predict1(w, m, v, cb);
+    return;
+  }
+  const double d = (cf.coef == 0.0 && cb.coef == 0.0) ? 0.0 : pred_dir((double)m, (double)v, cf);
+  rf = cf.coef == 0.0 ? w : (float)((double)w - cf.coef * d);
+  rb = cb.coef == 0.0 ? w : (float)((double)w - cb.coef * d);
 }
 
 typedef float nf4 __attribute__((ext_vector_type(4)));
@@ -42,7 +60,7 @@ XP_DEV void stnt(uint2* p, uint2 v) {
 }
 
 // ---------------------------------------------------------------- predict
-__global__ __launch_bounds__(256) void k_predict(const float* __restrict__ W,
+__global__ __launch_bounds__(STREAM_BLOCK) void k_predict(const float* __restrict__ W,
                                                   const float* __restrict__ m,
                                                   const float* __restrict__ v,
                                                   float* __restrict__ out,
@@ -97,7 +115,7 @@ XP_DEV AdamElem adam1(float w, float m, float v, float g, const AdamCoef& a) {
   return AdamElem{(float)wn, (float)mn, (float)vn};
 }
 
-__global__ __launch_bounds__(256) void k_adam(float* __restrict__ W, float* __restrict__ m,
+__global__ __launch_bounds__(STREAM_BLOCK) void k_adam(float* __restrict__ W, float* __restrict__ m,
                                                float* __restrict__ v, float* __restrict__ G,
                                                int64_t n, AdamCoef a, int zero_grad,
                                                float* __restrict__ pf, bf16_t* __restrict__ pf_bf,
@@ -105,6 +123,7 @@ __global__ __launch_bounds__(256) void k_adam(float* __restrict__ W, float* __re
                                                bf16_t* __restrict__ pb_bf, PredCoef cb) {
   const int64_t nv = n >> 2;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const bool shared = cf.c1 == cb.c1 && cf.c2 == cb.c2 && cf.eps == cb.eps && cf.eps_outside == cb.eps_outside;
   float4* W4 = reinterpret_cast<float4*>(W);
   float4* m4 = reinterpret_cast<float4*>(m);
   float4* v4 = reinterpret_cast<float4*>(v);
@@ -119,26 +138,38 @@ __global__ __launch_bounds__(256) void k_adam(float* __restrict__ W, float* __re
     stnt(m4 + i, make_float4(e0.m, e1.m, e2.m, e3.m));
     stnt(v4 + i, make_float4(e0.v, e1.v, e2.v, e3.v));
     if (zero_grad) stnt(G4 + i, make_float4(0.f, 0.f, 0.f, 0.f));
-    if (pf) {
-      float4 r = make_float4(predict1(e0.w, e0.m, e0.v, cf), predict1(e1.w, e1.m, e1.v, cf),
-                             predict1(e2.w, e2.m, e2.v, cf), predict1(e3.w, e3.m, e3.v, cf));
-      stnt(reinterpret_cast<float4*>(pf) + i, r);
+    if (pf && pb) {
+      float4 rf, rb;
+      predict2(e0.w, e0.m, e0.v, cf, cb, shared, rf.x, rb.x);
+      predict2(e1.w, e1.m, e1.v, cf, cb, shared, rf.y, rb.y);
+      predict2(e2.w, e2.m, e2.v, cf, cb, shared, rf.z, rb.z);
+      predict2(e3.w, e3.m, e3.v, cf, cb, shared, rf.w, rb.w);
+      stnt(reinterpret_cast<float4*>(pf) + i, rf);
+      stnt(reinterpret_cast<float4*>(pb) + i, rb);
       if (pf_bf) {
         uint2 b;
-        b.x = f32x2_to_bf16x2(r.x, r.y);
-        b.y = f32x2_to_bf16x2(r.z, r.w);
+        b.x = f32x2_to_bf16x2(rf.x, rf.y);
+        b.y = f32x2_to_bf16x2(rf.z, rf.w);
         stnt(reinterpret_cast<uint2*>(pf_bf) + i, b);
       }
-    }
-    if (pb) {
-      float4 r = make_float4(predict1(e0.w, e0.m, e0.v, cb), predict1(e1.w, e1.m, e1.v, cb),
-                             predict1(e2.w, e2.m, e2.v, cb), predict1(e3.w, e3.m, e3.v, cb));
-      stnt(reinterpret_cast<float4*>(pb) + i, r);
       if (pb_bf) {
+        uint2 b;
+        b.x = f32x2_to_bf16x2(rb.x, rb.y);
+        b.y = f32x2_to_bf16x2(rb.z, rb.w);
+        stnt(reinterpret_cast<uint2*>(pb_bf) + i, b);
+      }
+    } else if (pf || pb) {
+      const PredCoef& c = pf ? cf : cb;
+      float* o = pf ? pf : pb;
+      bf16_t* ob = pf ? pf_bf : pb_bf;
+      float4 r = make_float4(predict1(e0.w, e0.m, e0.v, c), predict1(e1.w, e1.m, e1.v, c),
+                             predict1(e2.w, e2.m, e2.v, c), predict1(e3.w, e3.m, e3.v, c));
+      stnt(reinterpret_cast<float4*>(o) + i, r);
+      if (ob) {
         uint2 b;
         b.x = f32x2_to_bf16x2(r.x, r.y);
         b.y = f32x2_to_bf16x2(r.z, r.w);
-        stnt(reinterpret_cast<uint2*>(pb_bf) + i, b);
+        stnt(reinterpret_cast<uint2*>(ob) + i, b);
       }
     }
   }
@@ -190,7 +221,7 @@ XP_DEV RuleElem rule1(float w, float b, float q, float m, float v, float gr, con
 }
 
 template <int RULE>
-__global__ __launch_bounds__(256) void k_rule(float* __restrict__ W, float* __restrict__ B,
+__global__ __launch_bounds__(STREAM_BLOCK) void k_rule(float* __restrict__ W, float* __restrict__ B,
                                               float* __restrict__ Q, float* __restrict__ m,
                                               float* __restrict__ v, float* __restrict__ G, int64_t n,
                                               RuleCoef c, int zero_grad, float* __restrict__ pf,
@@ -206,7 +237,22 @@ __global__ __launch_bounds__(256) void k_rule(float* __restrict__ W, float* __re
   float4* m4 = reinterpret_cast<float4*>(m);
   float4* v4 = reinterpret_cast<float4*>(v);
   float4* G4 = reinterpret_cast<float4*>(G);
+  const bool shared = cf.c1 == cb.c1 && cf.c2 == cb.c2 && cf.eps == cb.eps && cf.eps_outside == cb.eps_outside;
   auto preds = [&](int64_t i, const RuleElem (&e)[4]) __attribute__((always_inline)) {
+    if (pf && pb) {
+      float4 rf, rb;
+      predict2(e[0].w, e[0].m, e[0].v, cf, cb, shared, rf.x, rb.x);
+      predict2(e[1].w, e[1].m, e[1].v, cf, cb, shared, rf.y, rb.y);
+      predict2(e[2].w, e[2].m, e[2].v, cf, cb, shared, rf.z, rb.z);
+      predict2(e[3].w, e[3].m, e[3].v, cf, cb, shared, rf.w, rb.w);
+      stnt(reinterpret_cast<float4*>(pf) + i, rf);
+      stnt(reinterpret_cast<float4*>(pb) + i, rb);
+      if (pf_bf) stnt(reinterpret_cast<uint2*>(pf_bf) + i,
+                      make_uint2(f32x2_to_bf16x2(rf.x, rf.y), f32x2_to_bf16x2(rf.z, rf.w)));
+      if (pb_bf) stnt(reinterpret_cast<uint2*>(pb_bf) + i,
+                      make_uint2(f32x2_to_bf16x2(rb.x, rb.y), f32x2_to_bf16x2(rb.z, rb.w)));
+      return;
+    }
     if (pf) {
       float4 r = make_float4(predict1(e[0].w, e[0].m, e[0].v, cf), predict1(e[1].w, e[1].m, e[1].v, cf),
                              predict1(e[2].w, e[2].m, e[2].v, cf), predict1(e[3].w, e[3].m, e[3].v, cf));
@@ -263,9 +309,11 @@ __global__ __launch_bounds__(256) void k_rule(float* __restrict__ W, float* __re
 static int stream_grid(int64_t n) {
   // one 16-byte vector per thread: every load of the pass is issued up front
   // (measured on MI355X at 1e8 parameters: 6.35 TB/s for the prediction versus
-  // 5.3 TB/s with a 2048-workgroup grid-stride loop)
+  // 5.3 TB/s with a 2048-workgroup grid-stride loop; 1024-thread workgroups
+  // gain ~1.5% on a bare three-read one-write stream but lose more on the
+  // passes with fp64 square roots and divides)
   int64_t nv = (n >> 2) + 1;
-  int64_t blocks = (nv + 255) / 256;
+  int64_t blocks = (nv + STREAM_BLOCK - 1) / STREAM_BLOCK;
   if (blocks > ((int64_t)1 << 30)) blocks = (int64_t)1 << 30;
   if (blocks < 1) blocks = 1;
   return (int)blocks;
@@ -274,7 +322,7 @@ static int stream_grid(int64_t n) {
 hipError_t launch_predict(const float* W, const float* m, const float* v, float* out,
                           bf16_t* out_bf, int64_t n, const PredCoef& c, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  XP_LAUNCH("k_predict", (double)n * (out_bf ? 18 : 16), k_predict, dim3(stream_grid(n)), dim3(256), 0, s,
+  XP_LAUNCH("k_predict", (double)n * (out_bf ? 18 : 16), k_predict, dim3(stream_grid(n)), dim3(STREAM_BLOCK), 0, s,
             W, m, v, out, out_bf, n, c);
   return hipGetLastError();
 }
@@ -285,7 +333,7 @@ hipError_t launch_adam(float* W, float* m, float* v, float* G, int64_t n, const 
   if (n <= 0) return hipSuccess;
   double bytes = (double)n * (28 + (zero_grad ? 4 : 0) + (pf ? 4 : 0) + (pb ? 4 : 0) +
                               (pf_bf ? 2 : 0) + (pb_bf ? 2 : 0));
-  XP_LAUNCH("k_adam", bytes, k_adam, dim3(stream_grid(n)), dim3(256), 0, s, W, m, v, G, n, a, zero_grad,
+  XP_LAUNCH("k_adam", bytes, k_adam, dim3(stream_grid(n)), dim3(STREAM_BLOCK), 0, s, W, m, v, G, n, a, zero_grad,
             pf, pf_bf, cf, pb, pb_bf, cb);
   return hipGetLastError();
 }
@@ -298,10 +346,10 @@ hipError_t launch_rule(int rule, float* W, float* B, float* Q, float* m, float* 
   double bytes = (double)n * ((rms ? 44 : 36) + (zero_grad ? 4 : 0) + (pf ? 4 : 0) + (pb ? 4 : 0) +
                               (pf_bf ? 2 : 0) + (pb_bf ? 2 : 0));
   if (rms)
-    XP_LAUNCH("k_rule<rmsprop>", bytes, k_rule<RULE_RMSPROP>, dim3(stream_grid(n)), dim3(256), 0, s, W, B, Q,
+    XP_LAUNCH("k_rule<rmsprop>", bytes, k_rule<RULE_RMSPROP>, dim3(stream_grid(n)), dim3(STREAM_BLOCK), 0, s, W, B, Q,
               m, v, G, n, c, zero_grad, pf, pf_bf, cf, pb, pb_bf, cb);
   else
-    XP_LAUNCH("k_rule<momentum_sgd>", bytes, k_rule<RULE_MOMENTUM_SGD>, dim3(stream_grid(n)), dim3(256), 0, s,
+    XP_LAUNCH("k_rule<momentum_sgd>", bytes, k_rule<RULE_MOMENTUM_SGD>, dim3(stream_grid(n)), dim3(STREAM_BLOCK), 0, s,
               W, B, Q, m, v, G, n, c, zero_grad, pf, pf_bf, cf, pb, pb_bf, cb);
   return hipGetLastError();
 }

@@ -971,7 +971,9 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
 template <int BM, int BN, int WM, int WN, int PF, bool GRID>
 __global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
   using T = bf16_t;
-  constexpr int VEC = 8, BKm = 32, RPT = 2;
+  // 64 pixels per step: four 32x32x16 MFMAs per wave between barriers (32 took
+  // 4-8% longer on the stage shapes)
+  constexpr int VEC = 8, BKm = 64, RPT = 2;
   constexpr int PA = BKm + 8, PB = BKm + 8;
   __shared__ __align__(16) T sA[2][BM * PA];
   __shared__ __align__(16) T sB[2][BN * PB];
@@ -1164,18 +1166,23 @@ __global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
       }
       return;
     }
-    bf16x8_t af[TM], bfv[TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
-      af[i] = *reinterpret_cast<const bf16x8_t*>(&A[(wm * WTM + i * 16 + (lane & 15)) * PA + (lane >> 4) * 8]);
+    for (int ks = 0; ks < BKm / 32; ++ks) {
+      bf16x8_t af[TM], bfv[TN];
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
-      bfv[j] = *reinterpret_cast<const bf16x8_t*>(&B[(wn * WTN + j * 16 + (lane & 15)) * PB + (lane >> 4) * 8]);
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < TM; ++i)
+        af[i] = *reinterpret_cast<const bf16x8_t*>(
+            &A[(wm * WTM + i * 16 + (lane & 15)) * PA + ks * 32 + (lane >> 4) * 8]);
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfv[j], acc[i][j], 0, 0, 0);
+        bfv[j] = *reinterpret_cast<const bf16x8_t*>(
+            &B[(wn * WTN + j * 16 + (lane & 15)) * PB + ks * 32 + (lane >> 4) * 8]);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfv[j], acc[i][j], 0, 0, 0);
+    }
   };
 
   const int nsteps = mend > mbeg ? (mend - mbeg + BKm - 1) / BKm : 0;
@@ -1567,8 +1574,8 @@ static hipError_t wgrad_dispatch(const WgradArgs& a, hipStream_t s) {
                         (((size_t)(Min - 1)) * a.ldx + a.C) * sizeof(T) < ((size_t)1 << 31);
     // same grid and square padding: pixel offsets shift with the pixel index;
     // otherwise each pixel addresses x from its own row and column
-    if (chunks && a.Ho <= 0 && a.pad == a.padw) return wgrad_b_go<64, 64, 2, 2, 2>(a, s);
-    if (chunks) return wgrad_b_go<64, 64, 2, 2, 2, true>(a, s);
+    if (chunks && a.Ho <= 0 && a.pad == a.padw) return wgrad_b_go<64, 64, 2, 2, 1>(a, s);
+    if (chunks) return wgrad_b_go<64, 64, 2, 2, 1, true>(a, s);
   }
   if (n64 && k64) return wgrad_go<T, 64, 64, 2, 2>(a, flat, s);
   if (n64) return wgrad_go<T, 64, 128, 2, 2>(a, flat, s);

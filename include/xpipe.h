@@ -247,11 +247,14 @@ xpipe_status xpipe_stage_destroy(xpipe_stage_t st);
  * CONV): with L of them over K stages, stage k gets L / K and the last L % K
  * stages one more; a stage starts at its first weighted layer (activations,
  * pools, normalisations and joins stay with the stage of the layer they follow).
+ * A cut is valid only where the previous stage's last layer is the one tensor
+ * crossing it.  A cut that would split a branch or a skip connection (an
+ * Inception module, a residual block) moves to the nearest valid cut at a
+ * weighted layer, ties to the earlier one, keeping the cuts in order.
  * first[k] = index of stage k's first layer (first[0] = 0, first[K] = n;
  * K + 1 entries).  Layer inputs are re-indexed by the caller: the previous
- * stage's last layer becomes the stage input (-1).  EUNSUPPORTED when a layer
- * reads a tensor of an earlier stage other than that one (a branch or skip
- * connection cut by a boundary); EINVAL when K exceeds L.  Host only. */
+ * stage's last layer becomes the stage input (-1).  EUNSUPPORTED when some cut
+ * has no valid position left; EINVAL when K exceeds L.  Host only. */
 xpipe_status xpipe_partition(const xpipe_layer_desc* layers, int32_t n_layers, int32_t stages, int32_t* first);
 
 /* ---------------------------------------------------------------- schedule

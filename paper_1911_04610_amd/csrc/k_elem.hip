@@ -1035,6 +1035,7 @@ __global__ __launch_bounds__(256) void k_maxpool3s2_fwd(PoolArgs a, int Ho, int 
   const T* X = (const T*)a.x;
   const int p = a.valid ? 0 : 1;
   double best[N];
+  uint32_t pos[N];  // window position of the first maximum
   bool have = false;
   for (int r = 0; r < 3; ++r) {
     const int h = 2 * ho - p + r;
@@ -1046,11 +1047,34 @@ __global__ __launch_bounds__(256) void k_maxpool3s2_fwd(PoolArgs a, int Ho, int 
       ldn<T, N>(X + ((size_t)(n * a.H + h) * a.W + w) * a.ldx + c0, v);
 #pragma unroll
       for (int e = 0; e < N; ++e)
-        if (!have || v[e] > best[e]) best[e] = v[e];
+        if (!have || v[e] > best[e]) {
+          best[e] = v[e];
+          pos[e] = (uint32_t)(r * 3 + q);
+        }
       have = true;
     }
   }
-  stn<T, N>((T*)a.out + ((size_t)(n * Ho + ho) * Wo + wo) * a.ldo + c0, best);
+  const size_t o = (size_t)(n * Ho + ho) * Wo + wo;
+  stn<T, N>((T*)a.out + o * a.ldo + c0, best);
+  if (a.idx) {
+    // a NaN maximum chooses no position (the comparison in the backward
+    // without indices never matches it either)
+#pragma unroll
+    for (int e = 0; e < N; ++e)
+      if (best[e] != best[e]) pos[e] = 0xffu;
+    uint8_t* ip = a.idx + o * a.ldi + c0;
+    if constexpr (N == 8) {
+      uint2 v;
+      v.x = pos[0] | (pos[1] << 8) | (pos[2] << 16) | (pos[3] << 24);
+      v.y = pos[4] | (pos[5] << 8) | (pos[6] << 16) | (pos[7] << 24);
+      *reinterpret_cast<uint2*>(ip) = v;
+    } else if constexpr (N == 4) {
+      *reinterpret_cast<uint32_t*>(ip) = pos[0] | (pos[1] << 8) | (pos[2] << 16) | (pos[3] << 24);
+    } else {
+#pragma unroll
+      for (int e = 0; e < N; ++e) ip[e] = (uint8_t)pos[e];
+    }
+  }
 }
 
 // backward: each input pixel gathers, in (ho, wo) order, the output gradients
@@ -1073,13 +1097,44 @@ __global__ __launch_bounds__(256) void k_maxpool3s2_bwd(PoolArgs a, int Ho, int 
   const T* Y = (const T*)a.y;
   const T* DY = (const T*)a.dy;
   const int pd = a.valid ? 0 : 1;
-  double xv[N], acc[N];
-  ldn<T, N>(X + ((size_t)(n * a.H + h) * a.W + w) * a.ldx + c0, xv);
+  double acc[N];
 #pragma unroll
   for (int e = 0; e < N; ++e) acc[e] = 0.0;
   // windows 2ho - pd .. 2ho - pd + 2 that contain row h: ho from ceil((h + pd - 2) / 2)
   const int ho0 = max(0, (h + pd - 1) / 2), wo0 = max(0, (w + pd - 1) / 2);
   const int ho1 = min((h + pd) / 2, Ho - 1), wo1 = min((w + pd) / 2, Wo - 1);
+  if (a.idx) {
+    // the forward's choice: this pixel's position in each covering window
+    for (int ho = ho0; ho <= ho1; ++ho)
+      for (int wo = wo0; wo <= wo1; ++wo) {
+        const size_t o = (size_t)(n * Ho + ho) * Wo + wo;
+        const uint32_t me = (uint32_t)((h - (2 * ho - pd)) * 3 + (w - (2 * wo - pd)));
+        const uint8_t* ip = a.idx + o * a.ldi + c0;
+        uint32_t pos[N];
+        if constexpr (N == 8) {
+          const uint2 v = *reinterpret_cast<const uint2*>(ip);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            pos[e] = (v.x >> (8 * e)) & 0xffu;
+            pos[e + 4] = (v.y >> (8 * e)) & 0xffu;
+          }
+        } else if constexpr (N == 4) {
+          const uint32_t v = *reinterpret_cast<const uint32_t*>(ip);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) pos[e] = (v >> (8 * e)) & 0xffu;
+        } else {
+#pragma unroll
+          for (int e = 0; e < N; ++e) pos[e] = ip[e];
+        }
+        double d[N];
+        ldn<T, N>(DY + o * a.lddy + c0, d);
+#pragma unroll
+        for (int e = 0; e < N; ++e)
+          if (pos[e] == me) acc[e] += d[e];
+      }
+  } else {
+  double xv[N];
+  ldn<T, N>(X + ((size_t)(n * a.H + h) * a.W + w) * a.ldx + c0, xv);
   for (int ho = ho0; ho <= ho1; ++ho)
     for (int wo = wo0; wo <= wo1; ++wo) {
       const size_t o = (size_t)(n * Ho + ho) * Wo + wo;
@@ -1118,6 +1173,7 @@ __global__ __launch_bounds__(256) void k_maxpool3s2_bwd(PoolArgs a, int Ho, int 
       for (int e = 0; e < N; ++e)
         if (cand[e]) acc[e] += d[e];
     }
+  }
   const size_t r = (size_t)(n * a.H + h) * a.W + w;
   if (a.mask) {
     double m[N];
@@ -1144,7 +1200,12 @@ static hipError_t maxpool3s2_go(const PoolArgs& a, bool bwd, hipStream_t s) {
   constexpr int V = VT<T>::N;
   const bool vec = vec_ok<T>(a.C, {{a.x, a.ldx}, {a.out, a.ldo}, {a.dy, a.lddy}, {a.mask, a.ldm},
                                    {a.y, a.ldy}});
-  if (bwd && !a.y) return hipErrorInvalidValue;  // the backward reads the forward output
+  // the backward reads the forward's choices or its output
+  if (bwd && !a.y && !a.idx) return hipErrorInvalidValue;
+  // indices are stored as one byte per channel, N-byte groups aligned
+  if (a.idx && (a.ldi < a.C || (vec && ((a.ldi % VT<T>::N) != 0 ||
+                                       (reinterpret_cast<uintptr_t>(a.idx) % VT<T>::N) != 0))))
+    return hipErrorInvalidValue;
   const int64_t pix = bwd ? (int64_t)a.nb * a.H * a.W : (int64_t)a.nb * Ho * Wo;
   const int64_t threads = pix * (vec ? a.C / V : a.C);
   const unsigned blocks = (unsigned)((threads + 255) / 256);

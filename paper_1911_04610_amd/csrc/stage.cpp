@@ -93,6 +93,10 @@ struct Op {
   // weight tensors (parameter offset, output channels) in output-channel order
   std::vector<std::pair<int64_t, int>> segs;
   int64_t wg_off[2] = {-1, -1};     // workspace bytes: gathered predicted weights per direction
+  // 3x3 stride-2 max pool: workspace bytes of the first-maximum positions (one
+  // byte per output element), written by the forward that the backward
+  // recomputes and read by the pool's backward
+  int64_t idx_off = -1;
   // BN
   int64_t g_off = -1, be_off = -1;  // gamma / beta parameter offsets
   int64_t stat_off = -1;            // workspace bytes: mean, rstd, dbeta, dgamma (doubles) ...
@@ -789,6 +793,8 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
       colpart = std::max(colpart, col_partial_bytes((int)tin_.sh.rows(), tin_.sh.C));
     } else if (op.kind == OP_GAP) {
       colpart = std::max(colpart, gap_partial_bytes(tin_.sh.n, tin_.sh.H, tin_.sh.W, tin_.sh.C));
+    } else if (op.kind == OP_MAXPOOL3) {
+      op.idx_off = take((size_t)p.tensors[op.out].sh.elems());
     }
   }
   for (size_t t = 1; t < p.tensors.size(); ++t) {
@@ -1129,6 +1135,11 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         pa.C = tin.sh.C;
         pa.valid = op.valid;
         pa.part = (double*)(st->ws + st->colpart_off[lane]);
+        if (op.kind == OP_MAXPOOL3 && dir == XPIPE_BWD) {
+          // the backward that follows this recomputation takes the choices
+          pa.idx = (uint8_t*)(st->ws + op.idx_off);
+          pa.ldi = tin.sh.C;
+        }
         if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_fwd(dt, pa, s));
         else if (op.kind == OP_MAXPOOL3) XP_HIP(launch_maxpool3s2_fwd(dt, pa, s));
         else if (op.kind == OP_AVGPOOL) XP_HIP(launch_avgpool_fwd(dt, pa, s));
@@ -1410,11 +1421,13 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         pa.C = tin.sh.C;
         pa.valid = op.valid;
         if (op.kind == OP_MAXPOOL3) {
-          // the pool's output from the recomputed forward: a pixel takes a
-          // window's gradient when it holds the window's value first
+          // a pixel takes a window's gradient when it holds the window's
+          // maximum first: the recomputed forward recorded that position
           View yv = act(st, op.out, c);
           pa.y = yv.p;
           pa.ldy = yv.ld;
+          pa.idx = (uint8_t*)(st->ws + op.idx_off);
+          pa.ldi = tin.sh.C;
         }
         if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_bwd(dt, pa, s));
         else if (op.kind == OP_MAXPOOL3) XP_HIP(launch_maxpool3s2_bwd(dt, pa, s));

@@ -9,6 +9,7 @@ held to the bf16 bar (relative L2 2e-2) against the oracle's bf16-storage
 model, and, where the stage has no ReLU or max-pool at all, against the exact
 (fp64) oracle too; the fp32
 variant is held to 2e-4 against the oracle's fp32-storage model."""
+import numpy as np
 import pytest
 
 import oracle
@@ -189,3 +190,30 @@ def test_layer_kernels_match_oracle(name, dtype):
         print(f"{name}/{act} vs oracle-{mode}: worst {worst} = {e[worst]:.2e}")
         bad = {k: v for k, v in e.items() if not v <= tol}
         assert not bad, f"vs oracle-{mode}: " + ", ".join(f"{k}={v:.2e}" for k, v in bad.items())
+
+
+@pytest.mark.parametrize("dtype", [xp.F32, xp.BF16])
+@pytest.mark.parametrize("pad,shape", [(None, (13, 11, 16)), ("valid", (12, 13, 16)),
+                                       (None, (9, 10, 20))])
+def test_maxpool3s2_ties_match_oracle_exactly(pad, shape, dtype):
+    """Inputs on five levels, so most windows hold their maximum more than once:
+    the output is that maximum and each window's gradient goes to its first
+    holder in row-major window order, as the oracle routes it.  Both are exact
+    (the gradient sums at most four upstream values), so the comparison is bit
+    for bit; C = 20 takes the element-wise kernels."""
+    L = dict(kind="maxpool3s2", inputs=[-1])
+    if pad:
+        L["pad"] = pad
+    w = wl.StageWorkload("maxpool3s2_ties", [L], 2, 2, shape, 1, 0, 0, 0, minibatches=1, seed=23)
+    act = "bf16" if dtype == xp.BF16 else "f32"
+    inp = wl.stage_inputs(w, act_dtype=act, x_levels=5)
+    gpu, _ = run_stage(w, inp, dtype, xp.Hyper(), 0, 0, minibatches=1)
+    ref = oracle.train_stage(oracle.Stage(w.layers, act), inp.params, inp.m, inp.v, inp.xs, 0, 0,
+                             oracle.Hyper(), labels=inp.labels, dys=inp.dys)[0]
+    x = inp.xs[0][0]
+    assert len(np.unique(x)) <= 5
+    for i in range(w.T):
+        np.testing.assert_array_equal(np.asarray(gpu[0].ys[i], np.float64).reshape(ref.ys[i].shape),
+                                      np.asarray(ref.ys[i], np.float64))
+        np.testing.assert_array_equal(np.asarray(gpu[0].dxs[i], np.float64).reshape(ref.dxs[i].shape),
+                                      np.asarray(ref.dxs[i], np.float64))

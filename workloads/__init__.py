@@ -427,12 +427,14 @@ class StageInputs:
 
 
 def stage_inputs(w: StageWorkload, act_dtype: str = "f32", moment_init: str = "zeros",
-                 seed: Optional[int] = None) -> StageInputs:
+                 seed: Optional[int] = None, x_levels: Optional[int] = None) -> StageInputs:
     """Draw params, moments, inputs, labels/dy in that fixed order from PCG64(seed).
 
     act_dtype "bf16" rounds inputs and upstream gradients to bf16 values (the
     storage format of that variant); parameters stay fp32 masters.
     moment_init "paper" draws both moments as 1e-4 * U(0, 1) (Sec. IV-C).
+    x_levels = L draws the inputs as integers uniform in [-(L // 2), L // 2]
+    instead of N(0, 1) (exact in either format; equal values are common).
     """
     rng = np.random.default_rng(w.seed if seed is None else seed)
     params = init_params(w.layers, rng)
@@ -446,8 +448,11 @@ def stage_inputs(w: StageWorkload, act_dtype: str = "f32", moment_init: str = "z
         raise ValueError(moment_init)
     conv = (lambda a: round_to_bf16(a)) if act_dtype == "bf16" else (lambda a: a)
     shape = (w.micro_batch,) + tuple(w.in_shape)
-    xs = [[conv(rng.standard_normal(shape).astype(np.float32)) for _ in range(w.T)]
-          for _ in range(w.minibatches)]
+    if x_levels:
+        draw = lambda: rng.integers(-(x_levels // 2), x_levels // 2 + 1, size=shape).astype(np.float32)
+    else:
+        draw = lambda: rng.standard_normal(shape).astype(np.float32)
+    xs = [[conv(draw()) for _ in range(w.T)] for _ in range(w.minibatches)]
     labels = dys = None
     if w.has_loss:
         labels = [[rng.integers(0, w.classes, size=w.micro_batch).astype(np.int32)

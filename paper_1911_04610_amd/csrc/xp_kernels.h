@@ -123,6 +123,9 @@ struct WgradArgs {
   int nseg;
   int seg_row0[GATHER_MAX_SEGS + 1];
   float* seg_grad[GATHER_MAX_SEGS];
+  // set by the launcher (bf16 chunk path, one split): the tile is added
+  // straight into grad (or seg_grad) and no partials are written
+  int direct;
 };
 
 // Work plan of one GEMM launch (tile shape picked on the host).

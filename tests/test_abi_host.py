@@ -88,6 +88,8 @@ def test_stage_query_rejects_bad_layer_lists():
     assert _bad([dict(kind="linear", inputs=[-1], cin=4, cout=3, bias=True)]) == xp.EINVAL
     assert _bad([conv, dict(kind="add", inputs=[0, -1])]) == xp.EINVAL  # shape mismatch
     assert _bad([conv], mb=0) == xp.EINVAL
+    # more than 2^30 pixels in a micro-batch (row indices are 32-bit)
+    assert _bad([conv], shape=(32768, 32768, 4), mb=2) == xp.EINVAL
     assert _bad([dict(kind="concat", inputs=[-1])]) == xp.EINVAL
     # concat of the stage input itself is not a layer output
     assert _bad([dict(kind="concat", inputs=[-1, -1])], shape=(4, 4, 4)) in (xp.EINVAL, xp.EUNSUPPORTED)

@@ -1434,6 +1434,19 @@ static hipError_t conv_dispatch(const ConvArgs& a0, hipStream_t s, int* gr) {
     // strided or unpadded layers (ResNet-101 stem, first blocks, projections;
     // Inception-V3 stem and grid reductions): general tiles
     if constexpr (sizeof(T) == 2) {
+      // large grids (first stages at 224 x 224 over micro-batch 100): 128-row
+      // tiles, or one 96-column tile for 64 < N <= 96; 10-33% faster there
+      const size_t rows = (size_t)a.nb * a.Ho * a.Wo;
+      if (!flat && !narrow && rows >= 65536) {
+        if (a.tr) {
+          if (a.N <= 64) return conv_go<T, 128, 64, 2, 2, 2, 2, 2>(a, flat, s, gr);
+          if (a.N <= 96) return conv_go<T, 64, 96, 2, 2, 1, 2, 2>(a, flat, s, gr);
+          return conv_go<T, 128, 128, 2, 4, 2, 2, 2>(a, flat, s, gr);
+        }
+        if (a.N <= 64) return conv_go<T, 128, 64, 2, 2, 2, 2, 1>(a, flat, s, gr);
+        if (a.N <= 96) return conv_go<T, 64, 96, 2, 2, 1, 2, 1>(a, flat, s, gr);
+        return conv_go<T, 128, 128, 2, 4, 2, 2, 1>(a, flat, s, gr);
+      }
       if (a.tr) {
         if (narrow) return conv_go<T, 64, 32, 2, 2, 1, 2, 2>(a, flat, s, gr);
         return conv_go<T, 64, 64, 2, 2, 2, 2, 2>(a, flat, s, gr);

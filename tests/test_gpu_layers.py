@@ -66,6 +66,11 @@ LAYER_CASES = {
     # 128 columns on eight waves (forward) and 64 (data gradient); then N = 160
     "conv3x3_many_rows_n128": ([conv(-1, 64, 128, 3)], (182, 181, 64), 2),
     "conv1x1_many_rows_n160": ([conv(-1, 64, 160, 1)], (182, 181, 64), 2),
+    # the same for the unpadded and strided gathers (forward and data gradient):
+    # 66 978 output / 68 450 input rows; 65 884 output / 263 536 input rows
+    "conv3x3_valid_many_rows_n96": ([conv(-1, 80, 96, 3, pad="valid")], (185, 185, 80), 2),
+    "conv3x3_valid_many_rows_n128": ([conv(-1, 64, 128, 3, pad="valid")], (185, 185, 64), 2),
+    "conv3x3_s2_many_rows": ([conv(-1, 64, 64, 3, stride=2)], (364, 362, 64), 2),
     "conv_relu": ([conv(-1, 64, 64, 3, True), dict(kind="relu", inputs=[0])], (13, 13, 64), 2),
     "bn": ([dict(kind="bn", inputs=[-1], cin=96, cout=96)], (9, 9, 96), 3),
     "bn_add_relu": ([dict(kind="bn", inputs=[-1], cin=128, cout=128),

@@ -96,6 +96,12 @@ LAYER_CASES = {
                     dict(kind="softmax_ce", inputs=[0], classes=10)], (256,), 32),
     "concat_views": ([conv(-1, 64, 64, 1), conv(-1, 64, 32, 3),
                       dict(kind="concat", inputs=[0, 1]), conv(2, 96, 48, 1)], (8, 8, 64), 2),
+    # two wide 3x3 siblings (bf16: one 512 x 4608 launch of 576 tiles, whose
+    # weight gradient takes one split and adds each sibling's rows straight into
+    # its own accumulator)
+    "siblings_merged_wide": ([conv(-1, 512, 256, 3), bn(0, 256), dict(kind="relu", inputs=[1]),
+                              conv(-1, 512, 256, 3), bn(3, 256), dict(kind="relu", inputs=[4]),
+                              dict(kind="add", inputs=[2, 5])], (4, 4, 512), 2),
     # two 1x1 siblings on one input share a launch in bf16 (channel-slice outputs)
     "siblings_merged_bn": ([conv(-1, 64, 32, 1), dict(kind="bn", inputs=[0], cin=32, cout=32),
                             dict(kind="relu", inputs=[1]),

@@ -382,7 +382,8 @@ def time_sweep(n, steps):
     res = {}
 
     def timed(fn, reps):
-        fn()
+        for _ in range(3):
+            fn()
         torch.cuda.synchronize()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
@@ -392,7 +393,8 @@ def time_sweep(n, steps):
         torch.cuda.synchronize()
         return a.elapsed_time(b) / reps
 
-    reps = max(3, steps)
+    # at least 50 calls (>= 12 ms for the shortest pass) per timed window
+    reps = max(50, steps)
     for sv in (0, 1, 2, 3, 7):
         ms = timed(lambda: xp.xpipe_predict_flat(W, m, v, out, None, sv, hp, 100), reps)
         res[f"predict_s{sv}"] = {"ms": ms, "GB_s": 16.0 * n / ms / 1e6}

@@ -1057,8 +1057,7 @@ __global__ __launch_bounds__(256) void k_maxpool3s2_fwd(PoolArgs a, int Ho, int 
   const size_t o = (size_t)(n * Ho + ho) * Wo + wo;
   stn<T, N>((T*)a.out + o * a.ldo + c0, best);
   if (a.idx) {
-    // a NaN maximum chooses no position (the comparison in the backward
-    // without indices never matches it either)
+    // a NaN maximum chooses no position (0xff matches none)
 #pragma unroll
     for (int e = 0; e < N; ++e)
       if (best[e] != best[e]) pos[e] = 0xffu;
@@ -1078,10 +1077,8 @@ __global__ __launch_bounds__(256) void k_maxpool3s2_fwd(PoolArgs a, int Ho, int 
 }
 
 // backward: each input pixel gathers, in (ho, wo) order, the output gradients
-// of the (at most four) windows that contain it and chose it.  A window chose
-// the pixel when the pixel holds the window's maximum (the stored forward
-// output y) and no position before it in row-major window order does; the
-// earlier positions are read only when some channel of the chunk ties.
+// of the (at most four) windows that contain it and chose it: the forward
+// recorded, per window and channel, the position of its first maximum.
 template <typename T, int N>
 __global__ __launch_bounds__(256) void k_maxpool3s2_bwd(PoolArgs a, int Ho, int Wo) {
   const int groups = a.C / N;
@@ -1093,8 +1090,6 @@ __global__ __launch_bounds__(256) void k_maxpool3s2_bwd(PoolArgs a, int Ho, int 
   it /= a.W;
   const int h = (int)(it % a.H), n = (int)(it / a.H);
   const int c0 = g * N;
-  const T* X = (const T*)a.x;
-  const T* Y = (const T*)a.y;
   const T* DY = (const T*)a.dy;
   const int pd = a.valid ? 0 : 1;
   double acc[N];
@@ -1103,77 +1098,34 @@ __global__ __launch_bounds__(256) void k_maxpool3s2_bwd(PoolArgs a, int Ho, int 
   // windows 2ho - pd .. 2ho - pd + 2 that contain row h: ho from ceil((h + pd - 2) / 2)
   const int ho0 = max(0, (h + pd - 1) / 2), wo0 = max(0, (w + pd - 1) / 2);
   const int ho1 = min((h + pd) / 2, Ho - 1), wo1 = min((w + pd) / 2, Wo - 1);
-  if (a.idx) {
-    // the forward's choice: this pixel's position in each covering window
-    for (int ho = ho0; ho <= ho1; ++ho)
-      for (int wo = wo0; wo <= wo1; ++wo) {
-        const size_t o = (size_t)(n * Ho + ho) * Wo + wo;
-        const uint32_t me = (uint32_t)((h - (2 * ho - pd)) * 3 + (w - (2 * wo - pd)));
-        const uint8_t* ip = a.idx + o * a.ldi + c0;
-        uint32_t pos[N];
-        if constexpr (N == 8) {
-          const uint2 v = *reinterpret_cast<const uint2*>(ip);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            pos[e] = (v.x >> (8 * e)) & 0xffu;
-            pos[e + 4] = (v.y >> (8 * e)) & 0xffu;
-          }
-        } else if constexpr (N == 4) {
-          const uint32_t v = *reinterpret_cast<const uint32_t*>(ip);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) pos[e] = (v >> (8 * e)) & 0xffu;
-        } else {
-#pragma unroll
-          for (int e = 0; e < N; ++e) pos[e] = ip[e];
-        }
-        double d[N];
-        ldn<T, N>(DY + o * a.lddy + c0, d);
-#pragma unroll
-        for (int e = 0; e < N; ++e)
-          if (pos[e] == me) acc[e] += d[e];
-      }
-  } else {
-  double xv[N];
-  ldn<T, N>(X + ((size_t)(n * a.H + h) * a.W + w) * a.ldx + c0, xv);
+  // the forward's choice: this pixel's position in each covering window
   for (int ho = ho0; ho <= ho1; ++ho)
     for (int wo = wo0; wo <= wo1; ++wo) {
       const size_t o = (size_t)(n * Ho + ho) * Wo + wo;
-      double yv[N];
-      ldn<T, N>(Y + o * a.ldy + c0, yv);
-      bool cand[N], any = false;
+      const uint32_t me = (uint32_t)((h - (2 * ho - pd)) * 3 + (w - (2 * wo - pd)));
+      const uint8_t* ip = a.idx + o * a.ldi + c0;
+      uint32_t pos[N];
+      if constexpr (N == 8) {
+        const uint2 v = *reinterpret_cast<const uint2*>(ip);
 #pragma unroll
-      for (int e = 0; e < N; ++e) {
-        cand[e] = xv[e] == yv[e];
-        any = any || cand[e];
-      }
-      if (!any) continue;
-      // an earlier position holding the maximum takes it instead
-      const int hs = 2 * ho - pd, ws = 2 * wo - pd;
-      for (int r = 0; r < 3 && any; ++r) {
-        const int hh = hs + r;
-        if (hh < 0 || hh >= a.H || hh > h) continue;
-        for (int q = 0; q < 3; ++q) {
-          const int ww = ws + q;
-          if (ww < 0 || ww >= a.W || (hh == h && ww >= w)) continue;
-          double v[N];
-          ldn<T, N>(X + ((size_t)(n * a.H + hh) * a.W + ww) * a.ldx + c0, v);
-          any = false;
-#pragma unroll
-          for (int e = 0; e < N; ++e) {
-            cand[e] = cand[e] && !(v[e] == yv[e]);
-            any = any || cand[e];
-          }
-          if (!any) break;
+        for (int e = 0; e < 4; ++e) {
+          pos[e] = (v.x >> (8 * e)) & 0xffu;
+          pos[e + 4] = (v.y >> (8 * e)) & 0xffu;
         }
+      } else if constexpr (N == 4) {
+        const uint32_t v = *reinterpret_cast<const uint32_t*>(ip);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) pos[e] = (v >> (8 * e)) & 0xffu;
+      } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e) pos[e] = ip[e];
       }
-      if (!any) continue;
       double d[N];
       ldn<T, N>(DY + o * a.lddy + c0, d);
 #pragma unroll
       for (int e = 0; e < N; ++e)
-        if (cand[e]) acc[e] += d[e];
+        if (pos[e] == me) acc[e] += d[e];
     }
-  }
   const size_t r = (size_t)(n * a.H + h) * a.W + w;
   if (a.mask) {
     double m[N];
@@ -1200,8 +1152,8 @@ static hipError_t maxpool3s2_go(const PoolArgs& a, bool bwd, hipStream_t s) {
   constexpr int V = VT<T>::N;
   const bool vec = vec_ok<T>(a.C, {{a.x, a.ldx}, {a.out, a.ldo}, {a.dy, a.lddy}, {a.mask, a.ldm},
                                    {a.y, a.ldy}});
-  // the backward reads the forward's choices or its output
-  if (bwd && !a.y && !a.idx) return hipErrorInvalidValue;
+  // the backward reads the positions the forward recorded
+  if (bwd && !a.idx) return hipErrorInvalidValue;
   // indices are stored as one byte per channel, N-byte groups aligned
   if (a.idx && (a.ldi < a.C || (vec && ((a.ldi % VT<T>::N) != 0 ||
                                        (reinterpret_cast<uintptr_t>(a.idx) % VT<T>::N) != 0))))

@@ -1423,9 +1423,6 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         if (op.kind == OP_MAXPOOL3) {
           // a pixel takes a window's gradient when it holds the window's
           // maximum first: the recomputed forward recorded that position
-          View yv = act(st, op.out, c);
-          pa.y = yv.p;
-          pa.ldy = yv.ld;
           pa.idx = (uint8_t*)(st->ws + op.idx_off);
           pa.ldi = tin.sh.C;
         }

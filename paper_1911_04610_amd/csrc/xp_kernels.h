@@ -217,9 +217,9 @@ struct PoolArgs {
   int nb, H, W, C;                 // input shape
   double* part;                    // GAP forward: workspace, gap_partial_bytes
   int valid;                       // 3x3 stride-2 max pool: no padding
-  // 3x3 stride-2 max pool (optional): per output element, the window position
-  // r * 3 + q of the first maximum, one byte, at idx[row * ldi + channel];
-  // the forward writes it, the backward then reads it instead of comparing
+  // 3x3 stride-2 max pool: per output element, the window position r * 3 + q
+  // of the first maximum, one byte, at idx[row * ldi + channel]; the forward
+  // writes it when given, the backward requires it
   uint8_t* idx; int ldi;
 };
 size_t gap_partial_bytes(int nb, int H, int W, int C);
@@ -227,7 +227,7 @@ hipError_t launch_maxpool_fwd(int dtype, const PoolArgs& a, hipStream_t s);
 hipError_t launch_maxpool_bwd(int dtype, const PoolArgs& a, hipStream_t s);
 // 3x3 / stride 2 / padding 1 max pool (padding never chosen; ties to the first
 // maximum in row-major window order); the backward takes each window's choice
-// from a.idx when given, else re-derives it from x and the forward output y
+// from a.idx, which the forward recorded
 hipError_t launch_maxpool3s2_fwd(int dtype, const PoolArgs& a, hipStream_t s);
 hipError_t launch_maxpool3s2_bwd(int dtype, const PoolArgs& a, hipStream_t s);
 hipError_t launch_avgpool_fwd(int dtype, const PoolArgs& a, hipStream_t s);

@@ -204,7 +204,7 @@ xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t 
                              int32_t s_bwd_next, int32_t emit_pred);
 
 /* Update rules of the paper's other settings, with the prediction still built
- * from Adam moments (Sec. III-B): momentum SGD with weight decay (Sec. IV-B's
+ * from Adam moments (Sec. III-B): momentum SGD with weight decay (Sec. IV-D's
  * experiments) and RMSProp with momentum (Sec. IV-D's robustness study).
  * The gradient the rule steps on is g = grad + weight_decay * W; the Adam
  * moments m, v (Eq. 4) advance by the same g in the same pass.
@@ -241,7 +241,7 @@ xpipe_status xpipe_rule_step(xpipe_stage_t st, const xpipe_rule_hparams* rp, con
 xpipe_status xpipe_stage_destroy(xpipe_stage_t st);
 
 /* ---------------------------------------------------------------- partition
- * The paper's model partition (Sec. IV-A): the layers are split across the
+ * The paper's model partition (Sec. IV-B): the layers are split across the
  * GPUs into consecutive stages with roughly equal numbers of layers, the later
  * GPUs taking slightly more.  Counted here are the layers with weights (LINEAR,
  * CONV): with L of them over K stages, stage k gets L / K and the last L % K
@@ -317,7 +317,10 @@ xpipe_status xpipe_stage_run(xpipe_stage_t st, const xpipe_sched_event* events, 
                              const xpipe_rule_hparams* rule, float* buf, float* sq, int32_t draft);
 
 /* Flat-buffer forms of the two bandwidth-bound kernels, on n fp32 elements
- * (any n >= 0; no alignment needed beyond 4 bytes, 16 bytes is faster).
+ * (any n >= 0).  The kernels stream 16-byte chunks from the base pointers:
+ * every fp32 buffer must be 16-byte aligned (a bf16 output 8-byte aligned),
+ * else the call returns XPIPE_EINVAL before anything is enqueued.  n need not
+ * be a multiple of the chunk; the tail is handled element by element.
  * xpipe_predict_flat: out = W - s * lr * dir(m, v) (Eq. 3); out_bf16 (may be
  * NULL) receives the same values rounded to bf16 (uint16 bit patterns).
  * xpipe_adam_flat: W, m, v updated in place from G (update hp->t + 1); G is

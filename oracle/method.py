@@ -127,7 +127,7 @@ def adam_moments(m, v, g, beta1: float, beta2: float):
 def momentum_sgd_update(W, buf, m, v, G, lr: float, momentum: float, weight_decay: float,
                         beta1: float, beta2: float):
     """Momentum SGD with weight decay, the update rule of the paper's main
-    experiments (Sec. IV-B: momentum 0.9, weight decay 5e-4), with the Adam
+    experiments (Sec. IV-D: momentum 0.9, weight decay 5e-4), with the Adam
     moments that the prediction of Eq. 3 keeps (Sec. III-B) advanced by the same
     gradient.  Heavy-ball form without dampening: g = G + wd * W,
     buf = momentum * buf + g, W = W - lr * buf.  Returns (W, buf, m, v) in fp64."""

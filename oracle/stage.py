@@ -15,19 +15,17 @@ activations, activation gradients and the optimizer state in a narrower
 format (fp32, or bf16 for activations in its bf16 variant).  Where a stored
 value decides an integer (a max-pool argmax, a ReLU mask), both sides must
 take the decision on values of the same precision, so the oracle can round
-(to nearest, ties to even) exactly the tensors that the GPU path stores:
+(to nearest, ties to even) at storage precision:
   storage="f32"   activations and gradients rounded to fp32;
   storage="bf16"  activations and gradients rounded to bf16, conv/linear
                   weights multiplied as bf16 (the fp32 prediction, rounded);
 in both, the predicted weights, the master weights, both moments and the
 gradient accumulator are rounded to fp32 each time they are written.
-Rounded activations are the outputs of conv, linear, relu, avgpool3 and gap
-layers (max pools select stored values).  A BN output feeding only a ReLU, or
-only a residual add whose other operand comes earlier in the list, is fused
-into that consumer and not rounded; any other BN output (the projection
-shortcut of a ResNet block, added to the main path's BN) is a stored
-activation and is rounded.  Residual-add outputs are followed by a ReLU and
-are not rounded.  Every
+The rounding points are a property of the layer list alone: the output of
+every layer is rounded (rounding is idempotent, so layers that only select
+or copy stored values -- max pools, concatenations -- leave them unchanged,
+and ReLU commutes with rounding).  In particular a BN output is rounded
+before a residual add takes it in, and the sum is rounded again.  Every
 activation gradient is rounded each time a contribution is added to it;
 contributions arrive in reverse layer order.  storage="f64" rounds nothing.
 """
@@ -85,21 +83,6 @@ class Stage:
             self.pidx.append(list(range(k, k + n)))
             k += n
         self.n_params = k
-        # BN outputs that are stored on their own (not fused into their consumer)
-        cons = [[j for j, M in enumerate(layer_list) if i in M["inputs"]] for i in range(len(layer_list))]
-        self.bn_stored = {}
-        for i, L in enumerate(layer_list):
-            if L["kind"] != "bn":
-                continue
-            fused = False
-            if len(cons[i]) == 1:
-                c = layer_list[cons[i][0]]
-                if c["kind"] == "relu":
-                    fused = True
-                elif c["kind"] == "add":
-                    other = c["inputs"][1] if c["inputs"][0] == i else c["inputs"][0]
-                    fused = other < i
-            self.bn_stored[i] = not fused
 
     # storage rounding: activations / gradients (q), conv and linear weight
     # operands (qw), fp32 state (qs)
@@ -141,12 +124,12 @@ class Stage:
                 outs[i] = self.q(ly.linear(_rows(a), self.qw(P[pi[0]]), b))
             elif k == "bn":
                 y, xhat, rstd = ly.batchnorm(a, P[pi[0]], P[pi[1]])
-                outs[i] = self.q(y) if self.bn_stored[i] else y
+                outs[i] = self.q(y)
                 saved[i] = (xhat, rstd)
             elif k == "relu":
                 outs[i] = self.q(ly.relu(a))
             elif k == "add":
-                outs[i] = a + outs[L["inputs"][1]]
+                outs[i] = self.q(a + outs[L["inputs"][1]])
             elif k == "maxpool2":
                 y, idx = ly.maxpool2(a)
                 outs[i] = y
@@ -253,7 +236,7 @@ class Hyper:
     eps: float = 1e-8
     mode: str = PRED_EQ3
     # update rule at the mini-batch boundary (the prediction always uses the
-    # Adam moments m, v): Adam, momentum SGD (Sec. IV-B) or RMSProp (Sec. IV-D)
+    # Adam moments m, v): Adam, momentum SGD or RMSProp (both Sec. IV-D)
     rule: str = RULE_ADAM
     momentum: float = 0.9
     weight_decay: float = 0.0

@@ -350,7 +350,7 @@ def xpipe_predict_flat(W, m, v, out, out_bf16, s: int, hp: Hyper, t: int, stream
 
 
 def xpipe_partition(layers, stages: int) -> List[int]:
-    """first layer index of each stage, and len(layers) (Sec. IV-A's partition)."""
+    """first layer index of each stage, and len(layers) (Sec. IV-B's partition)."""
     arr = layer_descs(layers)
     first = (_I32 * (stages + 1))()
     _check(lib().xpipe_partition(arr, len(layers), stages, first))

@@ -111,7 +111,9 @@ __global__ __launch_bounds__(256) void k_bn_apply(BnApplyArgs a, int row_blocks)
   for (int r = r0 + rg; r < r1; r += 4) {
     double xh = (ldd(Z + (size_t)r * a.ldz + col) - mu) * rs;
     double v = g * xh + b;
-    if (R) v += ldd(R + (size_t)r * a.ldres + col);
+    // a BN output is a layer output of its own: rounded to the storage type
+    // before the residual add takes it in (the sum is rounded on store)
+    if (R) v = rnd<T>(v) + ldd(R + (size_t)r * a.ldres + col);
     if (a.relu) v = v > 0.0 ? v : 0.0;
     std_(Y + (size_t)r * a.ldy + col, v);
   }
@@ -707,7 +709,8 @@ __global__ __launch_bounds__(256) void k_bn_apply_v(BnApplyArgs a) {
       for (int e = 0; e < N; ++e) {
         double xh = (z[e] - mu[e]) * rs[e];
         double v = ga[e] * xh + be[e];
-        if (R) v += q[e];
+        // the BN output is rounded to the storage type before the residual add
+        if (R) v = rnd<T>(v) + q[e];
         if (a.relu) v = v > 0.0 ? v : 0.0;
         z[e] = v;
       }

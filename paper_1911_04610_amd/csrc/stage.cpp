@@ -2162,7 +2162,7 @@ xpipe_status xpipe_stage_run(xpipe_stage_t st, const xpipe_sched_event* events, 
 }
 
 // ============================================================================
-// Model partition (Sec. IV-A)
+// Model partition (Sec. IV-B)
 // ============================================================================
 xpipe_status xpipe_partition(const xpipe_layer_desc* layers, int32_t n_layers, int32_t stages, int32_t* first) {
   if (!layers || !first || n_layers <= 0 || stages < 1) return fail(XPIPE_EINVAL, "bad arguments");

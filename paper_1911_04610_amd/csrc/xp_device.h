@@ -41,6 +41,10 @@ template <> struct Store<bf16_t> {
 };
 
 template <typename T> XP_DEV double ldd(const T* p) { return Store<T>::ld(p); }
+// v rounded to the storage type and widened back (what a store then a load gives)
+template <typename T> XP_DEV double rnd(double v);
+template <> XP_DEV double rnd<float>(double v) { return (double)(float)v; }
+template <> XP_DEV double rnd<bf16_t>(double v) { return (double)bf16_to_f32(f32_to_bf16((float)v)); }
 template <typename T> XP_DEV void std_(T* p, double v) { Store<T>::st(p, v); }
 
 // ---------------------------------------------------------------- reductions

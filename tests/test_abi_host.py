@@ -160,7 +160,7 @@ def test_schedule_rejects_bad_arguments():
 
 
 def test_partition_vgg16():
-    """Sec. IV-A's rule on VGG-16's 14 weighted layers over 4 GPUs: 3, 3, 4, 4
+    """Sec. IV-B's rule on VGG-16's 14 weighted layers over 4 GPUs: 3, 3, 4, 4
     (the later GPUs take the remainder), each stage starting at a weighted
     layer, trailing ReLUs and pools kept with the layer they follow."""
     L = wl.vgg16_layers()

@@ -5,7 +5,8 @@ under a minute.
 
 fp32 storage: every tensor (outputs, loss, input gradient, accumulated weight
 gradient, predictions, W, m, v after the update) within 2e-4 of the oracle's
-fp32-storage model.  bf16 storage: the stage forward within 2e-2 of the
+fp32-storage model; against the exact fp64 oracle, the forward within 2e-4 and
+the rest within the bound stated in the test.  bf16 storage: the stage forward within 2e-2 of the
 oracle's bf16-storage model, or no further from the exact (fp64) forward than
 that bf16 model is (x1.25) where bf16 storage alone moves the output by more
 than the bar (measured: 2.6e-2 for the 24-layer ResNet stage)."""
@@ -28,10 +29,30 @@ def test_fullsize_fp32_step_matches_oracle(name):
     inp = wl.stage_inputs(w, act_dtype="f32", moment_init="paper")
     need_dx = w.rank > 0
     gpu, _ = run_stage(w, inp, xp.F32, xp.Hyper(), w.s_fwd, w.s_bwd, need_dx=need_dx)
-    ref = oracle.train_stage(oracle.Stage(w.layers, "f32"), inp.params, inp.m, inp.v, inp.xs,
-                             w.s_fwd, w.s_bwd, oracle.Hyper(), labels=inp.labels, dys=inp.dys,
-                             need_dx=need_dx)
-    g, r = gpu[0], ref[0]
+    args = (inp.params, inp.m, inp.v, inp.xs, w.s_fwd, w.s_bwd, oracle.Hyper())
+    kw = dict(labels=inp.labels, dys=inp.dys, need_dx=need_dx)
+    r32 = oracle.train_stage(oracle.Stage(w.layers, "f32"), *args, **kw)[0]
+    r64 = oracle.train_stage(oracle.Stage(w.layers, "f64"), *args, **kw)[0]
+    e = _errs(gpu[0], r32, need_dx)
+    worst = max(e, key=e.get)
+    print(f"{name} full size fp32 vs oracle-f32: worst {worst} = {e[worst]:.2e} over {len(e)} tensors")
+    bad = {k: v for k, v in e.items() if not v <= 2e-4}
+    assert not bad, bad
+    # Against the exact oracle: the forward within 2e-4; every other tensor
+    # within 2e-4, or -- where fp32 storage alone moves it further (a ReLU mask
+    # of a value within fp32 rounding of zero, whose effect the 24 BN layers
+    # of the ResNet stage spread through every gradient) -- no further than
+    # 1.25x the fp32-storage model's own distance, and never above 2e-2.
+    e64, model = _errs(gpu[0], r64, need_dx), _errs(r32, r64, need_dx)
+    worst = max(e64, key=e64.get)
+    print(f"{name} full size fp32 vs oracle-f64: worst {worst} = {e64[worst]:.2e} "
+          f"(fp32-storage model {model[worst]:.2e})")
+    assert e64["y"] <= 2e-4
+    bad = {k: (v, model[k]) for k, v in e64.items() if not (v <= 2e-4 or (v <= 1.25 * model[k] and v <= 2e-2))}
+    assert not bad, bad
+
+
+def _errs(g, r, need_dx):
     errs = {"y": rel_l2(g.ys[0], r.ys[0])}
     if need_dx:
         errs["dx"] = rel_l2(g.dxs[0], r.dxs[0])
@@ -40,10 +61,7 @@ def test_fullsize_fp32_step_matches_oracle(name):
     for field in ("grad", "w_pred_fwd", "w_pred_bwd", "W", "m", "v"):
         for k, (a, b) in enumerate(zip(getattr(g, field), getattr(r, field))):
             errs[f"{field}[{k}]"] = rel_l2(a, b)
-    worst = max(errs, key=errs.get)
-    print(f"{name} full size fp32: worst {worst} = {errs[worst]:.2e} over {len(errs)} tensors")
-    bad = {k: v for k, v in errs.items() if not v <= 2e-4}
-    assert not bad, bad
+    return errs
 
 
 @pytest.mark.parametrize("name", FULL)

@@ -208,18 +208,23 @@ def test_layer_kernels_match_oracle(name, dtype):
 
 
 @pytest.mark.parametrize("dtype", [xp.F32, xp.BF16])
-@pytest.mark.parametrize("pad,shape", [(None, (13, 11, 16)), ("valid", (12, 13, 16)),
-                                       (None, (9, 10, 20))])
-def test_maxpool3s2_ties_match_oracle_exactly(pad, shape, dtype):
+@pytest.mark.parametrize("kind,pad,shape", [("maxpool3s2", None, (13, 11, 16)),
+                                            ("maxpool3s2", "valid", (12, 13, 16)),
+                                            ("maxpool3s2", None, (9, 10, 20)),
+                                            ("maxpool2", None, (12, 14, 16)),
+                                            ("maxpool2", None, (13, 11, 16)),
+                                            ("maxpool2", None, (10, 10, 20))])
+def test_maxpool_ties_match_oracle_exactly(kind, pad, shape, dtype):
     """Inputs on five levels, so most windows hold their maximum more than once:
     the output is that maximum and each window's gradient goes to its first
     holder in row-major window order, as the oracle routes it.  Both are exact
     (the gradient sums at most four upstream values), so the comparison is bit
-    for bit; C = 20 takes the element-wise kernels."""
-    L = dict(kind="maxpool3s2", inputs=[-1])
+    for bit; C = 20 takes the element-wise kernels, odd sizes the floor of the
+    2 x 2 pool."""
+    L = dict(kind=kind, inputs=[-1])
     if pad:
         L["pad"] = pad
-    w = wl.StageWorkload("maxpool3s2_ties", [L], 2, 2, shape, 1, 0, 0, 0, minibatches=1, seed=23)
+    w = wl.StageWorkload(kind + "_ties", [L], 2, 2, shape, 1, 0, 0, 0, minibatches=1, seed=23)
     act = "bf16" if dtype == xp.BF16 else "f32"
     inp = wl.stage_inputs(w, act_dtype=act, x_levels=5)
     gpu, _ = run_stage(w, inp, dtype, xp.Hyper(), 0, 0, minibatches=1)

@@ -1,4 +1,4 @@
-"""Whole networks partitioned into four stages by Sec. IV-A's rule, run
+"""Whole networks partitioned into four stages by Sec. IV-B's rule, run
 stage by stage on the GPU library (the activation of stage k is the input of
 stage k + 1, the input gradient of stage k + 1 the upstream gradient of stage
 k) against the oracle's forward and backward of the unpartitioned network.

@@ -61,20 +61,23 @@ def _compare(gpu, ref, tol, what):
 def test_stage_step_fp32_matches_oracle(name):
     """fp32 storage, fp64 arithmetic: every tensor of every mini-batch within
     2e-4 of the oracle's fp32-storage model (decisions taken on the same
-    stored values on both sides)."""
+    stored values on both sides) and of the exact fp64 oracle."""
     w = CASES[name]()
     inp = wl.stage_inputs(w, act_dtype="f32")
     gpu, _ = run_stage(w, inp, xp.F32, xp.Hyper(), w.s_fwd, w.s_bwd)
-    ref = oracle.train_stage(oracle.Stage(w.layers, "f32"), inp.params, inp.m, inp.v, inp.xs,
-                             w.s_fwd, w.s_bwd, oracle.Hyper(), labels=inp.labels, dys=inp.dys)
-    _compare(gpu, ref, TOL[xp.F32], f"{name}/f32")
+    for storage in ("f32", "f64"):
+        # the fp32-storage model, and the plain fp64 oracle that rounds nothing
+        # (fp32 storage of fp64-computed values stays ~1e-6 from it here)
+        ref = oracle.train_stage(oracle.Stage(w.layers, storage), inp.params, inp.m, inp.v, inp.xs,
+                                 w.s_fwd, w.s_bwd, oracle.Hyper(), labels=inp.labels, dys=inp.dys)
+        _compare(gpu, ref, TOL[xp.F32], f"{name}/f32 vs oracle-{storage}")
 
 
 @pytest.mark.parametrize("name", ["tiny_mlp", "vgg16_stage0", "inception_v3_stage"])
 @pytest.mark.parametrize("rule", [xp.RULE_MOMENTUM_SGD, xp.RULE_RMSPROP])
 def test_stage_step_other_rules_fp32_match_oracle(name, rule):
     """The paper's other update rules (momentum SGD with weight decay, Sec.
-    IV-B; RMSProp with momentum, Sec. IV-D) with Adam-moment prediction from
+    IV-D; RMSProp with momentum, Sec. IV-D) with Adam-moment prediction from
     the paper's moment initialisation: fp32 storage, every tensor within 2e-4
     of the oracle."""
     w = CASES[name]()
@@ -134,6 +137,37 @@ def test_stage_step_bf16_matches_oracle(name):
     print(f"{name}/bf16 vs exact: worst {worst}: gpu {e_gpu[worst]:.2e}, bf16 model {e_ref[worst]:.2e}")
     bad = {k: (e_gpu[k], e_ref[k]) for k, r in ratio.items() if not r <= 1.0}
     assert not bad, ", ".join(f"{k}: gpu {a:.2e} model {b:.2e}" for k, (a, b) in list(bad.items())[:12])
+
+
+EXACT_LR = 1e-5
+
+
+def test_stage_step_bf16_exact_inputs_match_oracle():
+    """The bf16 stage step where its results are unique: the VGG stage (no
+    biases) on integer inputs with +-1 weights (workloads.exact_stage_inputs).
+    Every forward product and partial sum is then an exact fp32 integer, so
+    the GPU's fp32-accumulating MFMA GEMMs and the oracle's fp64 sums store the
+    same bf16 values and take the same ReLU and (tie-heavy) max-pool decisions.
+    The learning rate keeps |W_hat - W| below half a bf16 ulp of 1, so the
+    second mini-batch multiplies the same bf16 operands while the fp32 master
+    weights, moments and predictions move.  Every tensor of both mini-batches
+    (outputs, input gradients, accumulated gradients, both predictions, W, m,
+    v) is held to the bf16 bar of 2e-2; the forward outputs bit for bit."""
+    w = wl.shrink(wl.vgg_stage(), micro_batch=4, spatial=(20, 20), T=2, minibatches=2,
+                  layers=wl.vgg_stage_layers(bias=False))
+    inp = wl.exact_stage_inputs(w)
+    hp, ohp = xp.Hyper(lr=EXACT_LR), oracle.Hyper(lr=EXACT_LR)
+    gpu, _ = run_stage(w, inp, xp.BF16, hp, w.s_fwd, w.s_bwd)
+    ref = oracle.train_stage(oracle.Stage(w.layers, "bf16"), inp.params, inp.m, inp.v, inp.xs,
+                             w.s_fwd, w.s_bwd, ohp, dys=inp.dys)
+    from oracle.stage import _round_bf16
+    for a, b in zip(ref[1].w_pred_fwd + ref[1].w_pred_bwd, inp.params):
+        assert np.array_equal(_round_bf16(a), b)     # same bf16 operands in mini-batch 2
+    assert not np.array_equal(ref[1].w_pred_fwd[0], inp.params[0])   # fp32 state moved
+    for j in range(2):
+        for a, b in zip(gpu[j].ys, ref[j].ys):
+            np.testing.assert_array_equal(np.asarray(a, np.float64).reshape(b.shape), b)
+    _compare(gpu, ref, TOL[xp.BF16], "vgg16_stage0/bf16/exact-inputs")
 
 
 @pytest.mark.parametrize("name", ["tiny_mlp", "vgg16_stage0"])

@@ -140,6 +140,50 @@ def test_predict_constant_gradient_closed_form(c, k):
         np.testing.assert_allclose(got, want, rtol=0, atol=1e-15)
 
 
+@pytest.mark.parametrize("c", [0.3, -1e-3, 2.0, 3e-5])
+@pytest.mark.parametrize("k", [1, 2, 5, 40])
+def test_predict_literal_constant_gradient_closed_form(c, k):
+    """Eq. 4 as printed divides the moments by 1 - gamma and 1 - lambda with
+    no power t.  From zero moments, k Adam updates with a constant gradient c
+    leave m = c (1 - beta1^k) and v = c^2 (1 - beta2^k) (geometric sums of the
+    recurrences), so the printed form predicts
+        W_k - s lr [c (1 - beta1^k) / (1 - beta1)] / sqrt(c^2 (1 - beta2^k) / (1 - beta2) + eps).
+    Swapping beta1 and beta2, or using 1 - beta^t, changes every case with
+    k >= 2 (and the swap every case)."""
+    W = np.array([0.25, -0.5, 0.0])
+    m = np.zeros(3)
+    v = np.zeros(3)
+    G = np.full(3, c)
+    for t in range(1, k + 1):
+        W, m, v = om.adam_update(W, m, v, G, t, **HP)
+    b1, b2, eps, lr = HP["beta1"], HP["beta2"], HP["eps"], HP["lr"]
+    m_k = c * (1.0 - b1 ** k)
+    v_k = c * c * (1.0 - b2 ** k)
+    for s in (1, 2, 7):
+        got = om.predict(W, m, v, k, s, mode=om.PRED_LITERAL, **HP)
+        want = W - s * lr * (m_k / (1.0 - b1)) / np.sqrt(v_k / (1.0 - b2) + eps)
+        np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-17)
+
+
+def test_predict_literal_hand_values():
+    """Hand-computed values of Eq. 4 as printed (lr 1e-3, gamma 0.9, lambda
+    0.999, eps 1e-8).  After two updates with gradient 1 from zero moments:
+    m = 0.19, v = 0.001999, so the direction is (0.19 / 0.1) / sqrt(0.001999 /
+    0.001 + 1e-8) = 1.9 / sqrt(1.99900001) = 1.3438389...; with m = 0.05,
+    v = 0.0004 (t is not used): 0.5 / sqrt(0.4 + 1e-8) = 0.79056940...  With
+    beta1 and beta2 swapped the first would be 190 / sqrt(0.01999) = 1343.8."""
+    W = np.array([1.0, 1.0])
+    m = np.array([0.19, 0.05])
+    v = np.array([0.001999, 0.0004])
+    got = om.predict(W, m, v, 2, 1, mode=om.PRED_LITERAL, **HP)
+    want = 1.0 - 1e-3 * np.array([1.9 / np.sqrt(1.99900001), 0.5 / np.sqrt(0.40000001)])
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-15)
+    np.testing.assert_allclose(1.0 - got, [1.3438389e-3, 7.905694e-4], rtol=1e-7)
+    # s = 3 moves three times as far; t has no effect in this mode
+    got3 = om.predict(W, m, v, 100, 3, mode=om.PRED_LITERAL, **HP)
+    np.testing.assert_allclose(1.0 - got3, 3 * (1.0 - got), rtol=1e-12)
+
+
 def test_predict_adamdir_one_step_is_adam_step():
     """With Adam's own direction and s = 1, predicting from the moments that an
     update just produced reproduces that update's weights."""
@@ -189,7 +233,7 @@ def test_adam_zero_gradient_keeps_zero_state():
 
 
 # ------------------------------------------------------------------ momentum SGD / RMSProp
-SGD = dict(lr=1e-2, momentum=0.9, weight_decay=5e-4)      # Sec. IV-B's settings
+SGD = dict(lr=1e-2, momentum=0.9, weight_decay=5e-4)      # Sec. IV-D's settings
 RMS = dict(lr=1e-4, alpha=0.99, eps=1e-8, momentum=0.9, weight_decay=0.0)  # Sec. IV-D
 
 

@@ -108,17 +108,32 @@ def test_full_inception_v3_matches_torch():
     assert worst < 1e-10, worst
 
 
-def test_projection_bn_output_is_stored():
-    """A BN output that is not fused into a ReLU or into a later residual add
-    (the projection shortcut's BN) is a stored activation: rounded to the
-    storage type; the main path's last BN, which takes in the shortcut, is not."""
-    layers = wl.resnet101_layers(blocks=(1, 1, 1, 1))
-    st = oracle.Stage(layers, "bf16")
-    stored = sorted(i for i, v in st.bn_stored.items() if v)
-    proj = [i for i, L in enumerate(layers) if L["kind"] == "bn" and layers[L["inputs"][0]]["kind"] == "conv"
-            and layers[L["inputs"][0]]["k"] == 1 and
-            any(M["kind"] == "add" and M["inputs"][1] == i for M in layers)]
-    assert stored == proj and len(proj) == 4
+@pytest.mark.parametrize("storage", ["f32", "bf16"])
+def test_every_layer_output_is_rounded(storage):
+    """The storage model rounds the output of every layer of the list,
+    whatever kernels a GPU plan would fuse: a ResNet-101 block's BN outputs
+    (those feeding a ReLU, the one feeding the residual add, and the
+    projection shortcut's) and the residual sums are all storage values, and
+    the add takes in the rounded BN output."""
+    from oracle.stage import _round_bf16, _round_f32
+    rnd = _round_bf16 if storage == "bf16" else _round_f32
+    layers = wl.resnet101_layers(blocks=(1, 1, 1, 1))[:16]   # stem, pool, first block
+    assert [L["kind"] for L in layers[-3:]] == ["bn", "add", "relu"]
+    w = wl.StageWorkload("resnet_head", layers, 2, 1, (16, 16, 3), 4, 0, 0, 0, minibatches=1)
+    inp = wl.stage_inputs(w)
+    st = oracle.Stage(layers, storage)
+    _, _, (outs, _) = st.forward(inp.params, inp.xs[0][0])
+    for i in range(len(layers)):
+        assert np.array_equal(outs[i], rnd(outs[i])), (i, layers[i]["kind"])
+    add = len(layers) - 2
+    a, b = layers[add]["inputs"]
+    # the sum is the rounding of the two stored operands' exact sum
+    assert np.array_equal(outs[add], rnd(outs[a] + outs[b]))
+    # and differs from rounding the unrounded BN output plus the shortcut
+    ly_ = __import__("oracle.layers", fromlist=["batchnorm"])
+    P = [np.asarray(p, np.float64) for p in inp.params]
+    bn_raw, _, _ = ly_.batchnorm(outs[layers[a]["inputs"][0]], P[st.pidx[a][0]], P[st.pidx[a][1]])
+    assert not np.array_equal(rnd(bn_raw + outs[b]), outs[add])
 
 
 @pytest.mark.parametrize("name", ["tiny_mlp", "vgg16_stage0"])
@@ -222,9 +237,9 @@ def test_prediction_changes_the_step_once_moments_exist():
 
 
 def test_f32_storage_stays_close_to_exact():
-    """Rounding activations, gradients and state to fp32 perturbs the step by
-    about fp32 precision; ReLU masks that flip where a pre-activation is within
-    rounding of zero add a little more (about 1e-4 here), nothing larger."""
+    """Rounding activations, gradients and state to fp32 (values computed in
+    fp64) perturbs the step by about fp32 precision: measured 3e-7 on the
+    gradients here, held to 1e-5."""
     w = _small("vgg16_stage0", T=2, minibatches=2)
     inp = wl.stage_inputs(w)
     hp = oracle.Hyper()
@@ -236,7 +251,7 @@ def test_f32_storage_stays_close_to_exact():
         for a, b in zip(got[j].ys, ref[j].ys):
             assert rel_l2(a, b) < 1e-5
         for a, b in zip(got[j].grad, ref[j].grad):
-            assert rel_l2(a, b) < 1e-3
+            assert rel_l2(a, b) < 1e-5
     y = got[0].ys[0]
     assert np.array_equal(y, y.astype(np.float32).astype(np.float64))
 
@@ -262,3 +277,37 @@ def test_bf16_storage_forward_close_to_exact():
 def ostage_round(a):
     from oracle.stage import _round_bf16
     return _round_bf16(a)
+
+
+def test_bf16_whole_stage_gradients_are_not_unique():
+    """Why the deep BN stages' bf16 gradients are held to a bar relative to the
+    exact result rather than element by element to the bf16 model: two
+    evaluations of the oracle's own bf16 model that differ only by a relative
+    2^-24 sqrt(K) perturbation of each convolution before it is rounded (what
+    fp32 accumulation in another order does) disagree on the ResNet stage's
+    accumulated gradients by more than twice the 2e-2 bar, while their forward
+    outputs stay within it.  Each rounding difference moves a BN channel's
+    statistics, which moves the bf16 rounding of other elements, and so on
+    through the layers.  No bf16 implementation can be held to 2e-2 on these
+    gradients against any other."""
+    from oracle import layers as ly
+    w = wl.shrink(wl.resnet_stage(), micro_batch=2, T=2, minibatches=1,
+                  layers=wl.resnet_stage_layers(blocks=2), in_shape=(9, 9, 512))
+    inp = wl.stage_inputs(w, act_dtype="bf16", moment_init="paper")
+    args = (inp.params, inp.m, inp.v, inp.xs, w.s_fwd, w.s_bwd, oracle.Hyper())
+    ref = oracle.train_stage(oracle.Stage(w.layers, "bf16"), *args, dys=inp.dys)
+    rng = np.random.default_rng(5)
+    conv = ly.conv2d
+
+    def noisy(x, wt, b=None, stride=1, valid=False):
+        y = conv(x, wt, None, stride, valid)
+        y = y * (1 + 2.0 ** -24 * np.sqrt(wt[0].size) * rng.standard_normal(y.shape))
+        return y if b is None else y + b
+
+    ly.conv2d = noisy
+    try:
+        alt = oracle.train_stage(oracle.Stage(w.layers, "bf16"), *args, dys=inp.dys)
+    finally:
+        ly.conv2d = conv
+    assert max(rel_l2(a, b) for a, b in zip(alt[0].ys, ref[0].ys)) < 2e-2
+    assert max(rel_l2(a, b) for a, b in zip(alt[0].grad, ref[0].grad)) > 4e-2

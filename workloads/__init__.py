@@ -29,7 +29,7 @@ from typing import Dict, List, Optional
 
 import numpy as np
 
-PAPER_SEED = 1  # Sec. IV-C: "The seed was fixed with 1"
+PAPER_SEED = 1  # the data-shuffling seed the paper states (Sec. IV-C)
 
 
 # ----------------------------------------------------------------------------
@@ -73,20 +73,20 @@ def mlp_stage_layers(d_in=256, d_hidden=256, classes=10) -> List[dict]:
     return b.layers
 
 
-def vgg_stage_layers() -> List[dict]:
+def vgg_stage_layers(bias=True) -> List[dict]:
     """First of four VGG-16 stages: two conv blocks of (conv3x3+ReLU)x2 + maxpool."""
     b = _Builder()
-    x = b.relu(b.conv(-1, 3, 64, 3, bias=True))
-    x = b.relu(b.conv(x, 64, 64, 3, bias=True))
+    x = b.relu(b.conv(-1, 3, 64, 3, bias=bias))
+    x = b.relu(b.conv(x, 64, 64, 3, bias=bias))
     x = b.add(kind="maxpool2", inputs=[x])
-    x = b.relu(b.conv(x, 64, 128, 3, bias=True))
-    x = b.relu(b.conv(x, 128, 128, 3, bias=True))
+    x = b.relu(b.conv(x, 64, 128, 3, bias=bias))
+    x = b.relu(b.conv(x, 128, 128, 3, bias=bias))
     b.add(kind="maxpool2", inputs=[x])
     return b.layers
 
 
 def vgg16_layers(classes=10) -> List[dict]:
-    """VGG-16 for 32x32 inputs (Sec. IV-B's CIFAR-10 model): thirteen 3x3
+    """VGG-16 for 32x32 inputs (Sec. IV-C's CIFAR-10 model): thirteen 3x3
     convolutions with bias and ReLU in five blocks, each closed by a 2x2 max
     pool (32 -> 1), then a linear classifier and the cross-entropy loss."""
     b = _Builder()
@@ -138,7 +138,7 @@ def split_layers(layers: List[dict], first: List[int]) -> List[List[dict]]:
 
 
 def resnet101_layers(classes=200, blocks=(3, 4, 23, 3)) -> List[dict]:
-    """ResNet-101 (Sec. IV-B's Tiny ImageNet model, inputs scaled to 224 x 224):
+    """ResNet-101 (Sec. IV-C's Tiny ImageNet model, inputs scaled to 224 x 224):
     a 7x7 stride-2 stem convolution with BN and ReLU, a 3x3 stride-2 max pool,
     four groups of bottleneck blocks (1x1, 3x3, 1x1 with 4x expansion; BN after
     each convolution) whose first block strides by 2 on its 3x3 convolution
@@ -169,7 +169,7 @@ def resnet101_layers(classes=200, blocks=(3, 4, 23, 3)) -> List[dict]:
 
 
 def inception_v3_layers(classes=200) -> List[dict]:
-    """Inception-V3 (Sec. IV-B's Tiny ImageNet model, inputs scaled to 224 x
+    """Inception-V3 (Sec. IV-C's Tiny ImageNet model, inputs scaled to 224 x
     224), as defined by its authors: every convolution followed by BN and ReLU;
     an unpadded stem (3x3 stride 2, 3x3, padded 3x3, 3x3 stride-2 max pool,
     1x1, 3x3, 3x3 stride-2 max pool); three Inception-A modules (1x1 | 1x1 ->
@@ -460,6 +460,66 @@ def stage_inputs(w: StageWorkload, act_dtype: str = "f32", moment_init: str = "z
     else:
         out_shape = stage_output_shape(w)
         dys = [[conv((w.dy_std * rng.standard_normal(out_shape)).astype(np.float32))
+                for _ in range(w.T)] for _ in range(w.minibatches)]
+    return StageInputs(params, m, v, xs, labels, dys)
+
+
+def exact_stage_inputs(w: StageWorkload, seed: Optional[int] = None, two_point: bool = False,
+                       x_levels: int = 5, dy_levels: int = 7, dy_scale: float = 2.0 ** -8) -> StageInputs:
+    """Inputs on which the bf16 variant's stored values are unique: every
+    product and partial sum of a forward contraction is an exact fp32 value,
+    so an fp32-accumulating kernel and an fp64 reference store the same bits,
+    and equal values (max-pool ties) are compared exactly on both sides.
+
+      weights     conv / linear weights +-1 (random signs), no biases (a bias
+                  update is an fp32 value that no grid keeps exact); BN gamma 1,
+                  beta 0;
+      moments     the paper's initialisation 1e-4 * U(0, 1) (Sec. IV-C);
+      inputs      integers uniform in [-(x_levels // 2), x_levels // 2];
+                  with two_point, each micro-batch holds two such input
+                  vectors, alternating over its samples (even micro-batch), so
+                  that every BN channel sees exactly two values, equally often:
+                  its normalised outputs are +-d / sqrt(d^2 + eps), which bf16
+                  stores as +-1 (or 0 when d = 0), keeping the next contraction
+                  on integers (use with 1 x 1 maps, where a padded k x k
+                  convolution reduces to its centre tap);
+      upstream    integers in [-(dy_levels // 2), dy_levels // 2] times dy_scale;
+      labels      uniform.
+
+    Integer activations stay exact in fp32 while every partial sum is below
+    2^24.  A learning rate small enough that |W_hat - W| stays under half a
+    bf16 ulp of 1 keeps the bf16 weight operands at +-1 in later mini-batches
+    (the fp32 master weights, moments and predictions still move)."""
+    rng = np.random.default_rng(w.seed if seed is None else seed)
+    params = []
+    for shape, (li, role) in zip(param_shapes(w.layers), param_roles(w.layers)):
+        if role == "weight":
+            params.append(np.where(rng.integers(0, 2, size=shape) == 1, 1.0, -1.0).astype(np.float32))
+        elif role == "gamma":
+            params.append(np.ones(shape, np.float32))
+        else:
+            params.append(np.zeros(shape, np.float32))
+    m = [(1e-4 * rng.uniform(0.0, 1.0, size=p.shape)).astype(np.float32) for p in params]
+    v = [(1e-4 * rng.uniform(0.0, 1.0, size=p.shape)).astype(np.float32) for p in params]
+    shape = (w.micro_batch,) + tuple(w.in_shape)
+    half = x_levels // 2
+
+    def draw():
+        if not two_point:
+            return rng.integers(-half, half + 1, size=shape).astype(np.float32)
+        assert w.micro_batch % 2 == 0, "two-point inputs need an even micro-batch"
+        uv = rng.integers(-half, half + 1, size=(2,) + tuple(w.in_shape)).astype(np.float32)
+        return np.stack([uv[i % 2] for i in range(w.micro_batch)])
+
+    xs = [[draw() for _ in range(w.T)] for _ in range(w.minibatches)]
+    labels = dys = None
+    if w.has_loss:
+        labels = [[rng.integers(0, w.classes, size=w.micro_batch).astype(np.int32)
+                   for _ in range(w.T)] for _ in range(w.minibatches)]
+    else:
+        out_shape = stage_output_shape(w)
+        dh = dy_levels // 2
+        dys = [[(dy_scale * rng.integers(-dh, dh + 1, size=out_shape)).astype(np.float32)
                 for _ in range(w.T)] for _ in range(w.minibatches)]
     return StageInputs(params, m, v, xs, labels, dys)
 

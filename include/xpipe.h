@@ -155,6 +155,32 @@ xpipe_status xpipe_stage_create(const xpipe_layer_desc* layers, int32_t n_layers
                                 float* w_pred_fwd, float* w_pred_bwd,
                                 void* workspace, size_t workspace_bytes, xpipe_stage_t* out);
 
+/* Variant of xpipe_stage_create for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): same arguments and semantics, but no workspace argument.
+ * The stage's workspace is the library's static device array of
+ * XPIPE_STATIC_WORKSPACE_BYTES bytes (one per GPU, held from the library's
+ * load until the process ends), so neither this call nor any later call on
+ * the stage allocates or frees device memory, and none creates streams,
+ * events or graphs: every kernel runs on hip_stream, in launch order, passes
+ * are not recorded (xpipe_stage_set_graphs(st, 1) returns
+ * XPIPE_EUNSUPPORTED), and grad is zeroed by a kernel, not a memset.
+ * Results are bit-identical to a stage made by xpipe_stage_create.
+ * Errors: XPIPE_EINVAL when the stage's workspace (xpipe_stage_query) exceeds
+ * XPIPE_STATIC_WORKSPACE_BYTES, or as xpipe_stage_create; XPIPE_ESTATE while
+ * another stage made by this call is alive on the current device (a stage
+ * keeps state in its workspace between calls, and the array is shared);
+ * XPIPE_EHIP when the array's device address cannot be resolved.  The array
+ * keeps whatever the previous stage left in it; nothing in it needs to start
+ * at zero.  Calls that overlap in time on one GPU (the stage driven from two
+ * threads or streams at once) race on the array. */
+#define XPIPE_STATIC_WORKSPACE_BYTES ((size_t)64 << 20)
+xpipe_status xpipe_stage_create_static(const xpipe_layer_desc* layers, int32_t n_layers,
+                                       int32_t micro_batch, int32_t T, int32_t H, int32_t W, int32_t C,
+                                       int32_t dtype, void* hip_stream, float* W_, float* m, float* v,
+                                       float* grad, float* w_pred_fwd, float* w_pred_bwd,
+                                       xpipe_stage_t* out);
+
 /* Number of parameter tensors, and offset/count (elements) of tensor idx. */
 xpipe_status xpipe_stage_num_param_tensors(xpipe_stage_t st, int32_t* n);
 xpipe_status xpipe_stage_param_layout(xpipe_stage_t st, int32_t tensor_idx,

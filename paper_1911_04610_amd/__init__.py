@@ -105,6 +105,8 @@ _SIGS = {
                           ctypes.POINTER(_SZ)],
     "xpipe_stage_create": [_P, _I32, _I32, _I32, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P,
                            _P, _P, _P, _SZ, ctypes.POINTER(_P)],
+    "xpipe_stage_create_static": [_P, _I32, _I32, _I32, _I32, _I32, _I32, _I32, _P, _P, _P, _P,
+                                  _P, _P, _P, ctypes.POINTER(_P)],
     "xpipe_stage_num_param_tensors": [_P, ctypes.POINTER(_I32)],
     "xpipe_stage_param_layout": [_P, _I32, ctypes.POINTER(_I64), ctypes.POINTER(_I64)],
     "xpipe_stage_output_shape": [_P] + [ctypes.POINTER(_I32)] * 4,
@@ -141,6 +143,12 @@ def lib() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it with "
                               "`python -m paper_1911_04610_amd.build`")
+        # The library and PyTorch must share one HIP runtime (the library
+        # launches on torch's streams and into torch's allocations).  torch
+        # ships its own copy of the runtime; loaded after the library, it would
+        # come in as a second runtime with its own device contexts.  Importing
+        # torch first makes the library bind to torch's copy.
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB_PATH)
         for name, args in _SIGS.items():
             f = getattr(L, name)
@@ -217,7 +225,9 @@ class Stage:
     prediction caches and workspace are torch tensors owned by this object."""
 
     def __init__(self, layers: List[dict], micro_batch: int, T: int, in_shape, dtype: int = F32,
-                 device="cuda", stream=None):
+                 device="cuda", stream=None, static_workspace: bool = False):
+        """static_workspace=True creates the stage with xpipe_stage_create_static
+        (the library's static device workspace; no workspace tensor here)."""
         import torch
         self.layers = layers
         self.micro_batch, self.T, self.dtype = micro_batch, T, dtype
@@ -232,16 +242,24 @@ class Stage:
         self.grad = torch.zeros(self.P, **f32)
         self.w_pred_fwd = torch.zeros(self.P, **f32)
         self.w_pred_bwd = torch.zeros(self.P, **f32)
-        self.workspace = torch.empty(max(ws, 256) + 256, dtype=torch.uint8, device=self.device)
-        base = self.workspace.data_ptr()
-        ws_ptr = (base + 255) // 256 * 256
         self._h = _P()
         H, W, C = _hwc(in_shape)
         self._descs = layer_descs(layers)
-        _check(lib().xpipe_stage_create(self._descs, len(layers), micro_batch, T, H, W, C, dtype,
-                                        _stream_ptr(stream), _ptr(self.W), _ptr(self.m),
-                                        _ptr(self.v), _ptr(self.grad), _ptr(self.w_pred_fwd),
-                                        _ptr(self.w_pred_bwd), ws_ptr, ws, ctypes.byref(self._h)))
+        if static_workspace:
+            self.workspace = None
+            _check(lib().xpipe_stage_create_static(self._descs, len(layers), micro_batch, T, H, W, C,
+                                                   dtype, _stream_ptr(stream), _ptr(self.W),
+                                                   _ptr(self.m), _ptr(self.v), _ptr(self.grad),
+                                                   _ptr(self.w_pred_fwd), _ptr(self.w_pred_bwd),
+                                                   ctypes.byref(self._h)))
+        else:
+            self.workspace = torch.empty(max(ws, 256) + 256, dtype=torch.uint8, device=self.device)
+            base = self.workspace.data_ptr()
+            ws_ptr = (base + 255) // 256 * 256
+            _check(lib().xpipe_stage_create(self._descs, len(layers), micro_batch, T, H, W, C, dtype,
+                                            _stream_ptr(stream), _ptr(self.W), _ptr(self.m),
+                                            _ptr(self.v), _ptr(self.grad), _ptr(self.w_pred_fwd),
+                                            _ptr(self.w_pred_bwd), ws_ptr, ws, ctypes.byref(self._h)))
         n = _I32(0)
         _check(lib().xpipe_stage_num_param_tensors(self._h, ctypes.byref(n)))
         self.layout = []

@@ -23,6 +23,7 @@
 #include <cstring>
 #include <iterator>
 #include <map>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -166,6 +167,11 @@ struct xpipe_stage {
     void after(const char* name, double work) override;
   } hook;
   bool timing = false;
+  // a stage of xpipe_stage_create_static: one launch lane (no auxiliary
+  // streams or events), no recorded passes, workspace in the static array of
+  // device static_dev
+  bool one_lane = false;
+  int static_dev = -1;
   // recorded passes: each distinct (pass, caller pointers) is captured once
   // into a HIP graph on cap_stream and replayed on the stage's stream
   struct PassGraph {
@@ -937,7 +943,7 @@ struct Lanes {
     out.assign(d, d + nd);
     return XPIPE_OK;
   }
-  bool single() const { return st->timing; }
+  bool single() const { return st->timing || st->one_lane; }
   // stream for op i after its waits; the first use of an auxiliary lane in
   // the pass waits for the work enqueued on the stage's stream before it
   xpipe_status begin(int i, hipStream_t& s, int& lane) {
@@ -1610,6 +1616,151 @@ xpipe_status run_graphed(xpipe_stage* st, int kind, const void* const (&ptr)[5],
   return XPIPE_OK;
 }
 
+// ---------------------------------------------------------------- static workspace
+// Workspace of the stages made by xpipe_stage_create_static: a file-scope
+// device array (each GPU holds its own copy, at its own address, from the
+// library's load until the process ends).  Host code never passes the array's
+// name to a kernel or a copy -- on the host it is only a stand-in -- but the
+// device address that hipGetSymbolAddress resolved, once per device, with that
+// device current.  At most one such stage is alive per device: a stage keeps
+// state in its workspace between calls (bf16 copies of the predictions, the
+// data gradient's flipped weights), which a second stage would overwrite.
+constexpr size_t XP_STATIC_WS_BYTES = XPIPE_STATIC_WORKSPACE_BYTES;
+static __device__ __align__(256) unsigned char scratch[XP_STATIC_WS_BYTES];
+
+struct StaticWs {
+  bool resolved = false;
+  void* ptr = nullptr;
+  const xpipe_stage* owner = nullptr;
+};
+constexpr int XP_MAX_DEVICES = 64;
+std::mutex g_static_mu;
+StaticWs g_static_ws[XP_MAX_DEVICES];
+
+// the current device's copy of the array (resolved on the first call on that
+// device); call with g_static_mu held
+xpipe_status static_workspace(int dev, void** ptr) {
+  if (dev < 0 || dev >= XP_MAX_DEVICES) return fail(XPIPE_EUNSUPPORTED, "device index out of range");
+  StaticWs& w = g_static_ws[dev];
+  if (!w.resolved) {
+    void* p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(XPIPE_EHIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    w.ptr = p;
+    w.resolved = true;
+  }
+  *ptr = w.ptr;
+  return XPIPE_OK;
+}
+
+// grad = 0 with a kernel (no memset node if a caller records the stream)
+__global__ __launch_bounds__(256) void k_zero_f32(float* __restrict__ p, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0.f;
+}
+
+hipError_t zero_f32(float* p, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_zero_f32, dim3((unsigned)blocks), dim3(256), 0, s, p, n);
+  return hipGetLastError();
+}
+
+// Shared body of xpipe_stage_create and xpipe_stage_create_static.
+xpipe_status create_stage(const xpipe_layer_desc* layers, int32_t n_layers, int32_t micro_batch, int32_t T,
+                          int32_t H, int32_t W, int32_t C, int32_t dtype, void* hip_stream, float* W_,
+                          float* m, float* v, float* grad, float* w_pred_fwd, float* w_pred_bwd,
+                          void* workspace, size_t workspace_bytes, int static_dev, xpipe_stage_t* out) {
+  if (!out) return fail(XPIPE_EINVAL, "null output handle");
+  *out = nullptr;
+  if (T < 1) return fail(XPIPE_EINVAL, "T must be >= 1");
+  Plan p;
+  xpipe_status s = build_plan(layers, n_layers, micro_batch, H, W, C, dtype, p);
+  if (s != XPIPE_OK) return s;
+  if (p.P > 0 && (!W_ || !m || !v || !grad || !w_pred_fwd || !w_pred_bwd))
+    return fail(XPIPE_EINVAL, "null device buffer");
+  if (static_dev >= 0 && p.ws > XP_STATIC_WS_BYTES)
+    return fail(XPIPE_EINVAL, "stage needs a workspace of " + std::to_string(p.ws) +
+                                  " bytes, more than the static workspace's " +
+                                  std::to_string(XP_STATIC_WS_BYTES) + " (use xpipe_stage_create)");
+  if (!workspace) return fail(XPIPE_EINVAL, "null workspace");
+  if (workspace_bytes < p.ws) return fail(XPIPE_EINVAL, "workspace too small");
+  if ((reinterpret_cast<uintptr_t>(workspace) % WS_ALIGN) != 0)
+    return fail(XPIPE_EINVAL, "workspace must be 256-byte aligned");
+  if (!aligned16(W_) || !aligned16(m) || !aligned16(v) || !aligned16(grad) ||
+      !aligned16(w_pred_fwd) || !aligned16(w_pred_bwd))
+    return fail(XPIPE_EINVAL, "parameter buffers must be 16-byte aligned");
+  xpipe_stage* st = new (std::nothrow) xpipe_stage();
+  if (!st) return fail(XPIPE_EINVAL, "out of host memory");
+  st->layers.assign(layers, layers + n_layers);
+  st->mb = micro_batch;
+  st->T = T;
+  st->dtype = dtype;
+  st->in_shape = Shape{micro_batch, H, W, C};
+  st->stream = (hipStream_t)hip_stream;
+  st->W = W_;
+  st->m = m;
+  st->v = v;
+  st->grad = grad;
+  st->wpf = w_pred_fwd;
+  st->wpb = w_pred_bwd;
+  st->ws = (char*)workspace;
+  st->ws_bytes = workspace_bytes;
+  st->P = p.P;
+  st->params = p.params;
+  st->tensors = p.tensors;
+  st->ops = p.ops;
+  st->rec_order[0] = p.rec_order[0];
+  st->rec_order[1] = p.rec_order[1];
+  st->out_tensor = p.out_tensor;
+  st->has_loss = p.has_loss;
+  st->classes = p.classes;
+  st->bf_f_off = p.bf_f_off;
+  st->bf_b_off = p.bf_b_off;
+  for (int l = 0; l < NLANES; ++l) {
+    st->colpart_off[l] = p.colpart_off[l];
+    st->wpart_off[l] = p.wpart_off[l];
+  }
+  st->hook.st = st;
+  st->lane_stream[0] = st->stream;
+  hipError_t e = hipSuccess;
+  if (static_dev >= 0) {
+    // everything on the caller's stream: no streams, events or graphs to create
+    st->one_lane = true;
+    st->graphs = false;
+    st->static_dev = static_dev;
+  } else {
+    // auxiliary launch lanes (default priority) and their events
+    for (int l = 1; l < NLANES && e == hipSuccess; ++l)
+      e = hipStreamCreateWithFlags(&st->lane_stream[l], hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&st->cap_stream, hipStreamNonBlocking);
+    if (const char* g = std::getenv("XPIPE_GRAPHS"); g && *g == '0') st->graphs = false;
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&st->fork_ev, hipEventDisableTiming);
+    for (int l = 1; l < NLANES && e == hipSuccess; ++l)
+      e = hipEventCreateWithFlags(&st->join_ev[l], hipEventDisableTiming);
+    for (int pass = 0; pass < 2 && e == hipSuccess; ++pass) {
+      st->op_ev[pass].assign(st->ops.size(), nullptr);
+      for (size_t i = 0; i < st->ops.size() && e == hipSuccess; ++i)
+        if (st->ops[i].record[pass])
+          e = hipEventCreateWithFlags(&st->op_ev[pass][i], hipEventDisableTiming);
+    }
+    if (e != hipSuccess) {
+      release_lanes(st);
+      delete st;
+      return fail(XPIPE_EHIP, std::string("stream / event creation: ") + hipGetErrorString(e));
+    }
+  }
+  e = zero_f32(grad, p.P, st->stream);
+  if (e != hipSuccess) {
+    release_lanes(st);
+    delete st;
+    return fail(XPIPE_EHIP, std::string("zeroing grad: ") + hipGetErrorString(e));
+  }
+  *out = st;
+  return XPIPE_OK;
+}
+
 }  // namespace
 
 // ============================================================================
@@ -1663,82 +1814,30 @@ xpipe_status xpipe_stage_create(const xpipe_layer_desc* layers, int32_t n_layers
                                 void* hip_stream, float* W_, float* m, float* v, float* grad,
                                 float* w_pred_fwd, float* w_pred_bwd, void* workspace,
                                 size_t workspace_bytes, xpipe_stage_t* out) {
+  return create_stage(layers, n_layers, micro_batch, T, H, W, C, dtype, hip_stream, W_, m, v, grad,
+                      w_pred_fwd, w_pred_bwd, workspace, workspace_bytes, -1, out);
+}
+
+xpipe_status xpipe_stage_create_static(const xpipe_layer_desc* layers, int32_t n_layers,
+                                       int32_t micro_batch, int32_t T, int32_t H, int32_t W, int32_t C,
+                                       int32_t dtype, void* hip_stream, float* W_, float* m, float* v,
+                                       float* grad, float* w_pred_fwd, float* w_pred_bwd,
+                                       xpipe_stage_t* out) {
   if (!out) return fail(XPIPE_EINVAL, "null output handle");
   *out = nullptr;
-  if (T < 1) return fail(XPIPE_EINVAL, "T must be >= 1");
-  Plan p;
-  xpipe_status s = build_plan(layers, n_layers, micro_batch, H, W, C, dtype, p);
+  int dev = -1;
+  XP_HIP(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  void* ws = nullptr;
+  xpipe_status s = static_workspace(dev, &ws);
   if (s != XPIPE_OK) return s;
-  if (p.P > 0 && (!W_ || !m || !v || !grad || !w_pred_fwd || !w_pred_bwd))
-    return fail(XPIPE_EINVAL, "null device buffer");
-  if (!workspace) return fail(XPIPE_EINVAL, "null workspace");
-  if (workspace_bytes < p.ws) return fail(XPIPE_EINVAL, "workspace too small");
-  if ((reinterpret_cast<uintptr_t>(workspace) % WS_ALIGN) != 0)
-    return fail(XPIPE_EINVAL, "workspace must be 256-byte aligned");
-  if (!aligned16(W_) || !aligned16(m) || !aligned16(v) || !aligned16(grad) ||
-      !aligned16(w_pred_fwd) || !aligned16(w_pred_bwd))
-    return fail(XPIPE_EINVAL, "parameter buffers must be 16-byte aligned");
-  xpipe_stage* st = new (std::nothrow) xpipe_stage();
-  if (!st) return fail(XPIPE_EINVAL, "out of host memory");
-  st->layers.assign(layers, layers + n_layers);
-  st->mb = micro_batch;
-  st->T = T;
-  st->dtype = dtype;
-  st->in_shape = Shape{micro_batch, H, W, C};
-  st->stream = (hipStream_t)hip_stream;
-  st->W = W_;
-  st->m = m;
-  st->v = v;
-  st->grad = grad;
-  st->wpf = w_pred_fwd;
-  st->wpb = w_pred_bwd;
-  st->ws = (char*)workspace;
-  st->ws_bytes = workspace_bytes;
-  st->P = p.P;
-  st->params = p.params;
-  st->tensors = p.tensors;
-  st->ops = p.ops;
-  st->rec_order[0] = p.rec_order[0];
-  st->rec_order[1] = p.rec_order[1];
-  st->out_tensor = p.out_tensor;
-  st->has_loss = p.has_loss;
-  st->classes = p.classes;
-  st->bf_f_off = p.bf_f_off;
-  st->bf_b_off = p.bf_b_off;
-  for (int l = 0; l < NLANES; ++l) {
-    st->colpart_off[l] = p.colpart_off[l];
-    st->wpart_off[l] = p.wpart_off[l];
-  }
-  st->hook.st = st;
-  hipError_t e = hipSuccess;
-  // auxiliary launch lanes (default priority) and their events
-  st->lane_stream[0] = st->stream;
-  for (int l = 1; l < NLANES && e == hipSuccess; ++l)
-    e = hipStreamCreateWithFlags(&st->lane_stream[l], hipStreamNonBlocking);
-  if (e == hipSuccess) e = hipStreamCreateWithFlags(&st->cap_stream, hipStreamNonBlocking);
-  if (const char* g = std::getenv("XPIPE_GRAPHS"); g && *g == '0') st->graphs = false;
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&st->fork_ev, hipEventDisableTiming);
-  for (int l = 1; l < NLANES && e == hipSuccess; ++l)
-    e = hipEventCreateWithFlags(&st->join_ev[l], hipEventDisableTiming);
-  for (int pass = 0; pass < 2 && e == hipSuccess; ++pass) {
-    st->op_ev[pass].assign(st->ops.size(), nullptr);
-    for (size_t i = 0; i < st->ops.size() && e == hipSuccess; ++i)
-      if (st->ops[i].record[pass])
-        e = hipEventCreateWithFlags(&st->op_ev[pass][i], hipEventDisableTiming);
-  }
-  if (e != hipSuccess) {
-    release_lanes(st);
-    delete st;
-    return fail(XPIPE_EHIP, std::string("stream / event creation: ") + hipGetErrorString(e));
-  }
-  e = p.P > 0 ? hipMemsetAsync(grad, 0, (size_t)p.P * sizeof(float), st->stream) : hipSuccess;
-  if (e != hipSuccess) {
-    release_lanes(st);
-    delete st;
-    return fail(XPIPE_EHIP, std::string("hipMemsetAsync: ") + hipGetErrorString(e));
-  }
-  *out = st;
-  return XPIPE_OK;
+  if (g_static_ws[dev].owner)
+    return fail(XPIPE_ESTATE, "a stage with the static workspace is alive on this device "
+                              "(destroy it first)");
+  s = create_stage(layers, n_layers, micro_batch, T, H, W, C, dtype, hip_stream, W_, m, v, grad,
+                   w_pred_fwd, w_pred_bwd, ws, XP_STATIC_WS_BYTES, dev, out);
+  if (s == XPIPE_OK) g_static_ws[dev].owner = *out;
+  return s;
 }
 
 xpipe_status xpipe_stage_num_param_tensors(xpipe_stage_t st, int32_t* n) {
@@ -1826,6 +1925,7 @@ xpipe_status xpipe_stage_bwd(xpipe_stage_t st, const void* x, const void* dy, co
 
 xpipe_status xpipe_stage_set_graphs(xpipe_stage_t st, int32_t enable) {
   if (!st) return fail(XPIPE_EINVAL, "null stage");
+  if (st->one_lane && enable) return fail(XPIPE_EUNSUPPORTED, "a static-workspace stage records no passes");
   st->graphs = enable != 0;
   drop_graphs(st);
   return XPIPE_OK;
@@ -1914,6 +2014,12 @@ xpipe_status xpipe_stage_destroy(xpipe_stage_t st) {
     (void)hipEventDestroy(r.b);
   }
   for (auto e : st->pool) (void)hipEventDestroy(e);
+  if (st->static_dev >= 0) {
+    // work still queued on the caller's stream uses the static workspace
+    (void)hipStreamSynchronize(st->stream);
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    if (g_static_ws[st->static_dev].owner == st) g_static_ws[st->static_dev].owner = nullptr;
+  }
   delete st;
   return XPIPE_OK;
 }

@@ -35,6 +35,7 @@ def parse():
     ap.add_argument("--sweep-n", type=int, default=100_000_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-legs", action="store_true", help="skip the other stage configurations")
     ap.add_argument("--traffic-run", action="store_true",
                     help="a few stage steps plus a 256 MiB calibration copy, for rocprofv3 --pmc "
                          "FETCH_SIZE / WRITE_SIZE runs")
@@ -145,14 +146,21 @@ def stored_traffic(kernel):
     return None if k is None else k["traffic_bytes"]
 
 
-def time_stage(args, timing_pass=True, graphs=True):
+def time_stage(args, timing_pass=True, graphs=True, workload=None, dtype=None, s_fwd=None,
+               steps=None, warmup=None):
+    import dataclasses
     import torch
     import paper_1911_04610_amd as xp
     import workloads as wl
-    w = wl.WORKLOADS[args.workload]()
-    dt = xp.BF16 if args.dtype == "bf16" else xp.F32
+    w = wl.WORKLOADS[workload or args.workload]()
+    if s_fwd is not None:
+        w = dataclasses.replace(w, s_fwd=s_fwd)
+    dtype = dtype or args.dtype
+    steps = args.steps if steps is None else steps
+    warmup = args.warmup if warmup is None else warmup
+    dt = xp.BF16 if dtype == "bf16" else xp.F32
     tdt = torch.bfloat16 if dt == xp.BF16 else torch.float32
-    inp = wl.stage_inputs(w, act_dtype=args.dtype if args.dtype == "bf16" else "f32",
+    inp = wl.stage_inputs(w, act_dtype=dtype if dtype == "bf16" else "f32",
                           moment_init="paper")
     st = xp.Stage(w.layers, w.micro_batch, w.T, w.in_shape, dt)
     st.set_graphs(graphs)
@@ -189,25 +197,25 @@ def time_stage(args, timing_pass=True, graphs=True):
         st.xpipe_adam_step(hp, state["t"], w.s_fwd, w.s_bwd, emit_pred=True)
         state["t"] += 1
 
-    for j in range(args.warmup):
+    for j in range(warmup):
         step(j)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     e0.record(stream)
-    for j in range(args.steps):
+    for j in range(steps):
         step(j)
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms = e0.elapsed_time(e1) / args.steps
+    ms = e0.elapsed_time(e1) / steps
     if not timing_pass:
         return w, ms, wall, {}, True
     # per-kernel durations with HIP events around every launch, over the same
     # number of steps
     st.set_timing(True)
-    for j in range(args.steps):
+    for j in range(steps):
         step(j)
     torch.cuda.synchronize()
     classes = st.timing()
@@ -513,20 +521,30 @@ def vendor_reference(reps=50):
     return out
 
 
-def cpu_baseline(w, dtype):
-    """The oracle as it stands, on the host, for one whole step of the same
-    stage: both predictions, T forwards, T backwards with recomputation and
-    the Adam update (the oracle's mini-batch driver, one mini-batch)."""
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, dtype, sweep_n=10_000_000):
+    """The oracle as it stands, on the host: one whole step of the same stage
+    (both predictions, T forwards, T backwards with recomputation and the Adam
+    update: the oracle's mini-batch driver, one mini-batch) with the BLAS
+    thread pool at its default size, the first micro-batch's forward alone on
+    one thread, and the oracle's prediction and Adam passes over sweep_n flat
+    parameters (the 1e8-parameter sweep's distributions, a tenth of its size)
+    on one thread and on all."""
+    import numpy as np
     import oracle
     import workloads as wl
-    threads = os.cpu_count()
-    try:
-        from threadpoolctl import threadpool_info
-        info = threadpool_info()
-        if info:
-            threads = max(i.get("num_threads", 0) for i in info) or threads
-    except Exception:
-        pass
+    from threadpoolctl import threadpool_info, threadpool_limits
+    info = threadpool_info()
+    threads = max((i.get("num_threads", 0) for i in info), default=0) or os.cpu_count()
     storage = "bf16" if dtype == "bf16" else "f32"
     inp = wl.stage_inputs(w, act_dtype=storage, moment_init="paper")
     st = oracle.Stage(w.layers, storage)
@@ -535,11 +553,134 @@ def cpu_baseline(w, dtype):
                        labels=inp.labels, dys=inp.dys, need_dx=w.rank > 0, minibatches=1, t0=1)
     sec = time.perf_counter() - t0
     samples = w.T * w.micro_batch
+    with threadpool_limits(limits=1):
+        t1 = time.perf_counter()
+        st.forward(inp.params, inp.xs[0][0], None if inp.labels is None else inp.labels[0][0],
+                   samples)
+        fwd1 = time.perf_counter() - t1
+    fs = wl.flat_state(sweep_n)
+    W, m, v, G = (a.astype(np.float64) for a in (fs.W, fs.m, fs.v, fs.G))
+    hp = oracle.Hyper()
+
+    def sweep():
+        t1 = time.perf_counter()
+        oracle.predict(W, m, v, 100, 2, hp.lr, hp.beta1, hp.beta2, hp.eps)
+        tp = time.perf_counter() - t1
+        t1 = time.perf_counter()
+        oracle.adam_update(W, m, v, G, 101, hp.lr, hp.beta1, hp.beta2, hp.eps)
+        ta = time.perf_counter() - t1
+        # the GPU passes' algorithmic bytes at fp32 storage: predict 16 B/param, Adam 28
+        return {"predict_GB_s": round(16.0 * sweep_n / tp / 1e9, 3),
+                "adam_GB_s": round(28.0 * sweep_n / ta / 1e9, 3)}
+
+    with threadpool_limits(limits=1):
+        sw1 = sweep()
+    swn = sweep()
     return {"value": round(samples / sec, 3), "unit": "samples/s", "cores": int(threads),
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
             "sample": (f"one full step ({samples} samples: 2 predictions, {w.T} forwards, {w.T} "
                        f"backwards with recompute, Adam) of the same stage in fp64 numpy with "
-                       f"{storage} storage rounding; {sec:.1f} s on {threads} threads")}
+                       f"{storage} storage rounding; {sec:.1f} s on {threads} BLAS threads"),
+            "single_thread": {"forward_one_micro_batch_s": round(fwd1, 3),
+                              "samples_per_s": round(w.micro_batch / fwd1, 3),
+                              "note": "forward of one micro-batch only, one thread"},
+            "predict_adam_sweep": {"n_params": sweep_n, "one_thread": sw1, "all_threads": swn,
+                                   "note": "numpy element-wise passes run on one thread either way"}}
+
+
+def is_gemm(name):
+    return name.startswith(("k_conv_gemm", "k_conv_direct", "k_wgrad"))
+
+
+class KernelTable:
+    """Per-kernel event timings of a timing pass (name -> (ms, launches, work))
+    with the per-launch event offset removed: average launch time, achieved
+    rate and roofline fraction (GEMMs against the MFMA peak of the type they
+    multiply in, everything else against HBM)."""
+
+    def __init__(self, classes, steps, off_us, peak_key):
+        self.c, self.steps, self.off_us, self.peak_key = classes, steps, off_us, peak_key
+
+    def ms(self, k):
+        kms, kn, _ = self.c[k]
+        return max(kms - kn * self.off_us / 1e3, 1e-9)
+
+    def dominant(self, pred=lambda k: True):
+        ks = [k for k in self.c if pred(k)]
+        return max(ks, key=self.ms) if ks else None
+
+    def roofline(self, k):
+        kms, kn, kwork = self.c[k]
+        ms = self.ms(k)
+        if is_gemm(k):
+            ach = kwork / (ms / 1e3) / 1e12
+            peak = PEAK_TFLOPS[self.peak_key]
+            r = {"bound": "mfma", "achieved": round(ach, 3), "peak": peak, "unit": "TFLOP/s",
+                 "frac": round(ach / peak, 5)}
+        else:
+            ach = kwork / (ms / 1e3) / 1e9
+            r = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                 "frac": round(ach / HBM_PEAK_GBS, 4)}
+        r.update({"kernel": k, "launches_per_step": kn / self.steps,
+                  "avg_launch_us": round(1e3 * ms / max(kn, 1), 3),
+                  "avg_launch_us_raw_events": round(1e3 * kms / max(kn, 1), 3),
+                  "work_per_launch": kwork / max(kn, 1)})
+        return r
+
+    def summary(self, k):
+        r = self.roofline(k)
+        return {"kernel": k, "ms_per_step": round(self.ms(k) / self.steps, 4),
+                "launches_per_step": r["launches_per_step"], "avg_us": round(r["avg_launch_us"], 2),
+                "achieved": r["achieved"], "unit": r["unit"], "frac": r["frac"]}
+
+    def top(self, n):
+        return sorted(self.c, key=lambda k: -self.ms(k))[:n]
+
+    def all_gemm_frac(self):
+        ms = sum(self.ms(k) for k in self.c if is_gemm(k))
+        work = sum(self.c[k][2] for k in self.c if is_gemm(k))
+        return round(work / (ms / 1e3) / 1e12 / PEAK_TFLOPS[self.peak_key], 5) if ms > 0 else None
+
+    def launches_per_step(self):
+        return sum(v[1] for v in self.c.values()) / self.steps
+
+
+def config_legs(args, off_us):
+    """The other stage configurations, each timed the same way as the main
+    line (whole steps with HIP events, then a per-kernel timing pass): the
+    Tiny MLP (fp32, micro-seconds per step: launch-bound, no roofline), the
+    VGG-16 first stage (bf16 and fp32, s_f = 2 and the half-down reading's 1),
+    the ResNet middle stage and the Inception-A stage in both storage types.
+    fp32 storage multiplies on fp64 MFMA, so its GEMMs are held to the fp64
+    peak."""
+    legs = [("tiny_mlp", "f32", None), ("vgg16_stage0", "bf16", None), ("vgg16_stage0", "bf16", 1),
+            ("vgg16_stage0", "f32", None), ("vgg16_stage0", "f32", 1),
+            ("resnet101_mid_stage", "bf16", None), ("resnet101_mid_stage", "f32", None),
+            ("inception_v3_stage", "f32", None)]
+    out = []
+    for name, dt, sf in legs:
+        w, ms, wall, classes, fin = time_stage(args, workload=name, dtype=dt, s_fwd=sf,
+                                               steps=max(10, min(args.steps, 20)), warmup=3)
+        steps = max(10, min(args.steps, 20))
+        tab = KernelTable(classes, steps, off_us, "bf16" if dt == "bf16" else "f64")
+        samples = w.T * w.micro_batch
+        leg = {"workload": name, "dtype": dt, "micro_batch": w.micro_batch, "T": w.T,
+               "s_fwd": w.s_fwd, "s_bwd": w.s_bwd, "ms_per_step": round(ms, 4),
+               "samples_per_s": round(samples / (ms / 1e3), 1), "finite": fin,
+               "launches_per_step": tab.launches_per_step()}
+        if name == "tiny_mlp":
+            leg["us_per_step"] = round(ms * 1e3, 1)
+        else:
+            dom = tab.dominant()
+            leg["roofline"] = tab.roofline(dom)
+            cg = tab.dominant(lambda k: k.startswith(("k_conv_gemm", "k_conv_direct")))
+            wg = tab.dominant(lambda k: k.startswith("k_wgrad"))
+            leg["roofline_conv_gemm"] = tab.roofline(cg) if cg else None
+            leg["roofline_weight_gradient"] = tab.roofline(wg) if wg else None
+            leg["mfma_util_all_gemm"] = tab.all_gemm_frac()
+        leg["top_kernels"] = [tab.summary(k) for k in tab.top(5)]
+        out.append(leg)
+    return out
 
 
 def main():
@@ -561,35 +702,17 @@ def main():
     samples = w.T * w.micro_batch
     value = samples / (ms / 1e3)
     peak_key = "bf16" if args.dtype == "bf16" else "f64"
-
-    def is_gemm(name):
-        return name.startswith("k_conv_gemm") or name.startswith("k_wgrad")
-
     off_us, off_bracket, off_period = event_offset_us()
-
-    def roof(name):
-        kms, kn, kwork = classes[name]
-        kms = max(kms - kn * off_us / 1e3, 1e-9)  # remove the per-launch event offset
-        if is_gemm(name):
-            ach = kwork / (kms / 1e3) / 1e12
-            return {"bound": "mfma", "achieved": round(ach, 3), "peak": PEAK_TFLOPS[peak_key],
-                    "unit": "TFLOP/s", "frac": round(ach / PEAK_TFLOPS[peak_key], 5)}
-        ach = kwork / (kms / 1e3) / 1e9
-        return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(ach / HBM_PEAK_GBS, 4)}
-
-    dom = max(classes, key=lambda k: classes[k][0])
-    d_ms, d_n, d_work = classes[dom]
-    rf = roof(dom)
-    rf.update({"kernel": dom, "traffic": stored_traffic(dom), "traffic_unit": "bytes per launch",
-               "launches_per_step": d_n / args.steps,
-               "avg_launch_us": round(1e3 * d_ms / max(d_n, 1) - off_us, 3),
-               "avg_launch_us_raw_events": round(1e3 * d_ms / max(d_n, 1), 3),
-               "event_offset_us": round(off_us, 3),
-               "work_per_launch": d_work / max(d_n, 1)})
-    gemm_ms = sum(v[0] for k, v in classes.items() if is_gemm(k))
-    gemm_work = sum(v[2] for k, v in classes.items() if is_gemm(k))
-    top = sorted(classes, key=lambda k: -classes[k][0])[:12]
+    tab = KernelTable(classes, args.steps, off_us, peak_key)
+    # the dominant kernel: largest summed launch time once the per-launch
+    # event offset is removed (what the kernel-trace profiler ranks by)
+    dom = tab.dominant()
+    rf = tab.roofline(dom)
+    rf.update({"traffic": stored_traffic(dom), "traffic_unit": "bytes per launch",
+               "event_offset_us": round(off_us, 3)})
+    wg = tab.dominant(lambda k: k.startswith("k_wgrad"))
+    cg = tab.dominant(lambda k: k.startswith(("k_conv_gemm", "k_conv_direct")))
+    top = tab.top(12)
     out = {
         "metric": "stage samples/sec (predict+fwd+bwd+Adam); predict/Adam HBM GB/s; MFMA util",
         "value": round(value, 2),
@@ -608,14 +731,12 @@ def main():
                    "s_bwd": w.s_bwd, "rank": w.rank, "size": w.size,
                    "update": "adam fused with next predictions", "parallelism": "one stage, 1 GPU"},
         "roofline": rf,
-        "mfma_util_all_gemm": round(gemm_work / (gemm_ms / 1e3) / 1e12 / PEAK_TFLOPS[peak_key], 5)
-        if gemm_ms > 0 else None,
+        "roofline_conv_gemm": tab.roofline(cg) if cg else None,
+        "roofline_weight_gradient": tab.roofline(wg) if wg else None,
+        "mfma_util_all_gemm": tab.all_gemm_frac(),
+        "launches_per_step": tab.launches_per_step(),
         "kernels_timed_sum_ms_per_step": round(sum(v[0] for v in classes.values()) / args.steps, 4),
-        "top_kernels": [{"kernel": k, "ms_per_step": round(classes[k][0] / args.steps, 4),
-                         "launches_per_step": classes[k][1] / args.steps,
-                         "avg_us": round(1e3 * classes[k][0] / max(classes[k][1], 1) - off_us, 2),
-                         **{kk: vv for kk, vv in roof(k).items() if kk in ("achieved", "unit", "frac")}}
-                        for k in top],
+        "top_kernels": [tab.summary(k) for k in top],
         "finite": finite,
     }
     pk = measured_peaks()
@@ -637,6 +758,8 @@ def main():
         out["resnet101_partitioned"] = time_partitioned(args, "resnet101")
         out["inception_v3_partitioned"] = time_partitioned(args, "inception_v3")
         out["vendor_reference"] = vendor_reference()
+    if not args.no_legs:
+        out["configs"] = config_legs(args, off_us)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.dtype)
     print(json.dumps(out))

@@ -26,6 +26,7 @@
 #include "xp_kernels.h"
 
 #include <cstdio>
+#include <cstdlib>
 
 namespace xp {
 
@@ -97,6 +98,168 @@ XP_DEV int xcd_tile(int l, int G) {
   const int x = l % XP_XCDS, q = l / XP_XCDS;
   const int per = G / XP_XCDS, rem = G % XP_XCDS;
   return x * per + (x < rem ? x : rem) + q;
+}
+
+// bf16 epilogue from the fp32 result tile staged in LDS (ot, BM rows of
+// OPITCH floats; every thread of the workgroup takes part): each thread
+// finishes 8-column chunks of a row (bias, ReLU, mask, accumulate, round
+// once) with 16-byte loads and stores, leaves the stored values in LDS, and
+// the batch-norm column statistics of the tile are taken from there.
+template <int BM, int BN, int NT, int OPITCH>
+XP_DEV void conv_epilogue_bf16(const ConvArgs& a, float* ot, int tid, int m0, int n0, int tm, int M) {
+  typedef bf16_t T;
+  T* __restrict__ y = (T*)a.y;
+  const T* __restrict__ mask = (const T*)a.mask;
+  constexpr int CPRN = BN / 8;  // 8-column chunks per tile row
+  static_assert(BN % 8 == 0, "chunked epilogue");
+  // 16-byte global access needs 8-element aligned rows and base pointers
+  const bool vy = (a.ldy % 8) == 0 && (reinterpret_cast<uintptr_t>(y) % 16) == 0;
+  const bool vm = mask && (a.ldm % 8) == 0 && (reinterpret_cast<uintptr_t>(mask) % 16) == 0;
+  // all loads of the thread's chunks are issued before its first store (a
+  // load after a store waits for the store on this hardware); full chunks
+  // take 16-byte accesses, a ragged last chunk (N not a multiple of 8) or
+  // unaligned views an element loop
+  typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+  constexpr int NCH = (BM * CPRN + NT - 1) / NT;  // chunks per thread
+  int c_ne[NCH];
+  u32x4_t c_mask[NCH], c_old[NCH];
+  f32x4_t c_b0[NCH], c_b1[NCH];
+  const bool vb = a.bias && (reinterpret_cast<uintptr_t>(a.bias + n0) % 16) == 0;
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    const int c = k * NT + tid;
+    const int row = c / CPRN, cc = c - row * CPRN;
+    const int m = m0 + row, nb = n0 + cc * 8;
+    const bool live = ((BM * CPRN) % NT == 0 || c < BM * CPRN) && m < M && nb < a.N;
+    const int ne = live ? (a.N - nb < 8 ? a.N - nb : 8) : 0;  // valid columns in this chunk
+    c_ne[k] = ne;
+    c_mask[k] = c_old[k] = (u32x4_t){0u, 0u, 0u, 0u};
+    c_b0[k] = c_b1[k] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+    if (ne == 8) {
+      if (vb) {
+        c_b0[k] = *reinterpret_cast<const f32x4_t*>(a.bias + nb);
+        c_b1[k] = *reinterpret_cast<const f32x4_t*>(a.bias + nb + 4);
+      }
+      if (vm) c_mask[k] = *reinterpret_cast<const u32x4_t*>(mask + (size_t)m * a.ldm + nb);
+      if (a.accumulate && vy) c_old[k] = *reinterpret_cast<const u32x4_t*>(y + (size_t)m * a.ldy + nb);
+    }
+    if (ne > 0 && (ne < 8 || (a.bias && !vb) || (mask && !vm) || (a.accumulate && !vy))) {
+      float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      uint16_t mv[8] = {0, 0, 0, 0, 0, 0, 0, 0}, ov[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      for (int e = 0; e < ne; ++e) {
+        if (a.bias) bv[e] = a.bias[nb + e];
+        if (mask) mv[e] = mask[(size_t)m * a.ldm + nb + e];
+        if (a.accumulate) ov[e] = y[(size_t)m * a.ldy + nb + e];
+      }
+      c_b0[k] = (f32x4_t){bv[0], bv[1], bv[2], bv[3]};
+      c_b1[k] = (f32x4_t){bv[4], bv[5], bv[6], bv[7]};
+      c_mask[k] = *reinterpret_cast<const u32x4_t*>(mv);
+      c_old[k] = *reinterpret_cast<const u32x4_t*>(ov);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    const int c = k * NT + tid;
+    if ((BM * CPRN) % NT != 0 && c >= BM * CPRN) break;
+    const int row = c / CPRN, cc = c - row * CPRN;
+    const int ne = c_ne[k];
+    float* o = &ot[row * OPITCH + cc * 8];
+    if (ne > 0) {
+      const f32x4_t lo = *reinterpret_cast<const f32x4_t*>(o);
+      const f32x4_t hi = *reinterpret_cast<const f32x4_t*>(o + 4);
+      float f[8];
+      if (!a.accumulate) {
+        // one rounding to fp32 of acc + bias equals the rounding of their
+        // exact double sum (53 >= 2 * 24 + 2), and ReLU and the mask commute
+        // with rounding, so fp32 arithmetic stores the same values
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          f[e] = lo[e] + c_b0[k][e];
+          f[e + 4] = hi[e] + c_b1[k][e];
+        }
+      } else {
+        // y + result: added to the double value, rounded once
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          double v = (double)(e < 4 ? lo[e] : hi[e - 4]) + (double)(e < 4 ? c_b0[k][e] : c_b1[k][e - 4]);
+          if (a.relu) v = v > 0.0 ? v : 0.0;
+          const uint32_t mw = c_mask[k][e >> 1];
+          if (mask && !(__uint_as_float((e & 1) ? (mw & 0xffff0000u) : (mw << 16)) > 0.0f)) v = 0.0;
+          const uint32_t ow = c_old[k][e >> 1];
+          v += (double)__uint_as_float((e & 1) ? (ow & 0xffff0000u) : (ow << 16));
+          f[e] = (float)v;
+        }
+      }
+      if (!a.accumulate) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          if (a.relu) f[e] = f[e] > 0.f ? f[e] : 0.f;
+          const uint32_t mw = c_mask[k][e >> 1];
+          if (mask && !(__uint_as_float((e & 1) ? (mw & 0xffff0000u) : (mw << 16)) > 0.0f)) f[e] = 0.f;
+        }
+      }
+      u32x4_t pr;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) pr[q] = f32x2_to_bf16x2(f[2 * q], f[2 * q + 1]);
+      T* p = y + (size_t)(m0 + row) * a.ldy + n0 + cc * 8;
+      if (vy && ne == 8) {
+        *reinterpret_cast<u32x4_t*>(p) = pr;
+      } else {
+        for (int e = 0; e < ne; ++e) p[e] = (uint16_t)(pr[e >> 1] >> ((e & 1) * 16));
+      }
+      if (a.stat_part) {
+        f32x4_t s0, s1;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          s0[2 * q] = 2 * q < ne ? __uint_as_float(pr[q] << 16) : 0.f;
+          s0[2 * q + 1] = 2 * q + 1 < ne ? __uint_as_float(pr[q] & 0xffff0000u) : 0.f;
+          s1[2 * q] = 2 * q + 4 < ne ? __uint_as_float(pr[q + 2] << 16) : 0.f;
+          s1[2 * q + 1] = 2 * q + 5 < ne ? __uint_as_float(pr[q + 2] & 0xffff0000u) : 0.f;
+        }
+        *reinterpret_cast<f32x4_t*>(o) = s0;
+        *reinterpret_cast<f32x4_t*>(o + 4) = s1;
+      }
+    } else if (a.stat_part) {
+      *reinterpret_cast<f32x4_t*>(o) = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+      *reinterpret_cast<f32x4_t*>(o + 4) = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+    }
+  }
+  if (a.stat_part) {
+    // column sums of the stored values: RS row ranges per column, then a
+    // fixed-order sum of the ranges
+    constexpr int RS = NT / BN > 0 ? NT / BN : 1;
+    constexpr int RROWS = BM / RS;
+    static_assert(BM % RS == 0 && RROWS % 4 == 0, "row ranges");
+    __shared__ double sred[RS][2][BN];
+    __syncthreads();
+    if (tid < RS * BN) {
+      const int col = tid % BN, part = tid / BN;
+      const float* oc = ot + part * RROWS * OPITCH + col;
+      // four interleaved partial sums, added in a fixed order
+      double s0[4] = {0.0, 0.0, 0.0, 0.0}, s1[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+      for (int r = 0; r < RROWS; ++r) {
+        const double sv = (double)oc[r * OPITCH];
+        s0[r & 3] += sv;
+        s1[r & 3] += sv * sv;
+      }
+      sred[part][0][col] = (s0[0] + s0[1]) + (s0[2] + s0[3]);
+      sred[part][1][col] = (s1[0] + s1[1]) + (s1[2] + s1[3]);
+    }
+    __syncthreads();
+    for (int col = tid; col < BN; col += NT) {
+      const int n = n0 + col;
+      if (n >= a.N) continue;
+      double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+      for (int q = 0; q < RS; ++q) {
+        s0 += sred[q][0][col];
+        s1 += sred[q][1][col];
+      }
+      a.stat_part[((size_t)n * 2 + 0) * gridDim.x + tm] = s0;
+      a.stat_part[((size_t)n * 2 + 1) * gridDim.x + tm] = s1;
+    }
+  }
 }
 
 // GM selects the gather: 0 stride 1 (rows = input grid), 1 strided forward,
@@ -471,156 +634,7 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
                 acc[i][j][q];
     }
     __syncthreads();
-    constexpr int CPRN = BN / 8;  // 8-column chunks per tile row
-    static_assert(BN % 8 == 0, "chunked epilogue");
-    // 16-byte global access needs 8-element aligned rows and base pointers
-    const bool vy = (a.ldy % 8) == 0 && (reinterpret_cast<uintptr_t>(y) % 16) == 0;
-    const bool vm = mask && (a.ldm % 8) == 0 && (reinterpret_cast<uintptr_t>(mask) % 16) == 0;
-    // all loads of the thread's chunks are issued before its first store (a
-    // load after a store waits for the store on this hardware); full chunks
-    // take 16-byte accesses, a ragged last chunk (N not a multiple of 8) or
-    // unaligned views an element loop
-    typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-    constexpr int NCH = (BM * CPRN + NT - 1) / NT;  // chunks per thread
-    int c_ne[NCH];
-    u32x4_t c_mask[NCH], c_old[NCH];
-    f32x4_t c_b0[NCH], c_b1[NCH];
-    const bool vb = a.bias && (reinterpret_cast<uintptr_t>(a.bias + n0) % 16) == 0;
-#pragma unroll
-    for (int k = 0; k < NCH; ++k) {
-      const int c = k * NT + tid;
-      const int row = c / CPRN, cc = c - row * CPRN;
-      const int m = m0 + row, nb = n0 + cc * 8;
-      const bool live = ((BM * CPRN) % NT == 0 || c < BM * CPRN) && m < M && nb < a.N;
-      const int ne = live ? (a.N - nb < 8 ? a.N - nb : 8) : 0;  // valid columns in this chunk
-      c_ne[k] = ne;
-      c_mask[k] = c_old[k] = (u32x4_t){0u, 0u, 0u, 0u};
-      c_b0[k] = c_b1[k] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-      if (ne == 8) {
-        if (vb) {
-          c_b0[k] = *reinterpret_cast<const f32x4_t*>(a.bias + nb);
-          c_b1[k] = *reinterpret_cast<const f32x4_t*>(a.bias + nb + 4);
-        }
-        if (vm) c_mask[k] = *reinterpret_cast<const u32x4_t*>(mask + (size_t)m * a.ldm + nb);
-        if (a.accumulate && vy) c_old[k] = *reinterpret_cast<const u32x4_t*>(y + (size_t)m * a.ldy + nb);
-      }
-      if (ne > 0 && (ne < 8 || (a.bias && !vb) || (mask && !vm) || (a.accumulate && !vy))) {
-        float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-        uint16_t mv[8] = {0, 0, 0, 0, 0, 0, 0, 0}, ov[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (int e = 0; e < ne; ++e) {
-          if (a.bias) bv[e] = a.bias[nb + e];
-          if (mask) mv[e] = mask[(size_t)m * a.ldm + nb + e];
-          if (a.accumulate) ov[e] = y[(size_t)m * a.ldy + nb + e];
-        }
-        c_b0[k] = (f32x4_t){bv[0], bv[1], bv[2], bv[3]};
-        c_b1[k] = (f32x4_t){bv[4], bv[5], bv[6], bv[7]};
-        c_mask[k] = *reinterpret_cast<const u32x4_t*>(mv);
-        c_old[k] = *reinterpret_cast<const u32x4_t*>(ov);
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < NCH; ++k) {
-      const int c = k * NT + tid;
-      if ((BM * CPRN) % NT != 0 && c >= BM * CPRN) break;
-      const int row = c / CPRN, cc = c - row * CPRN;
-      const int ne = c_ne[k];
-      float* o = &ot[row * OPITCH + cc * 8];
-      if (ne > 0) {
-        const f32x4_t lo = *reinterpret_cast<const f32x4_t*>(o);
-        const f32x4_t hi = *reinterpret_cast<const f32x4_t*>(o + 4);
-        float f[8];
-        if (!a.accumulate) {
-          // one rounding to fp32 of acc + bias equals the rounding of their
-          // exact double sum (53 >= 2 * 24 + 2), and ReLU and the mask commute
-          // with rounding, so fp32 arithmetic stores the same values
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            f[e] = lo[e] + c_b0[k][e];
-            f[e + 4] = hi[e] + c_b1[k][e];
-          }
-        } else {
-          // y + result: added to the double value, rounded once
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            double v = (double)(e < 4 ? lo[e] : hi[e - 4]) + (double)(e < 4 ? c_b0[k][e] : c_b1[k][e - 4]);
-            if (a.relu) v = v > 0.0 ? v : 0.0;
-            const uint32_t mw = c_mask[k][e >> 1];
-            if (mask && !(__uint_as_float((e & 1) ? (mw & 0xffff0000u) : (mw << 16)) > 0.0f)) v = 0.0;
-            const uint32_t ow = c_old[k][e >> 1];
-            v += (double)__uint_as_float((e & 1) ? (ow & 0xffff0000u) : (ow << 16));
-            f[e] = (float)v;
-          }
-        }
-        if (!a.accumulate) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            if (a.relu) f[e] = f[e] > 0.f ? f[e] : 0.f;
-            const uint32_t mw = c_mask[k][e >> 1];
-            if (mask && !(__uint_as_float((e & 1) ? (mw & 0xffff0000u) : (mw << 16)) > 0.0f)) f[e] = 0.f;
-          }
-        }
-        u32x4_t pr;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) pr[q] = f32x2_to_bf16x2(f[2 * q], f[2 * q + 1]);
-        T* p = y + (size_t)(m0 + row) * a.ldy + n0 + cc * 8;
-        if (vy && ne == 8) {
-          *reinterpret_cast<u32x4_t*>(p) = pr;
-        } else {
-          for (int e = 0; e < ne; ++e) p[e] = (uint16_t)(pr[e >> 1] >> ((e & 1) * 16));
-        }
-        if (a.stat_part) {
-          f32x4_t s0, s1;
-#pragma unroll
-          for (int q = 0; q < 2; ++q) {
-            s0[2 * q] = 2 * q < ne ? __uint_as_float(pr[q] << 16) : 0.f;
-            s0[2 * q + 1] = 2 * q + 1 < ne ? __uint_as_float(pr[q] & 0xffff0000u) : 0.f;
-            s1[2 * q] = 2 * q + 4 < ne ? __uint_as_float(pr[q + 2] << 16) : 0.f;
-            s1[2 * q + 1] = 2 * q + 5 < ne ? __uint_as_float(pr[q + 2] & 0xffff0000u) : 0.f;
-          }
-          *reinterpret_cast<f32x4_t*>(o) = s0;
-          *reinterpret_cast<f32x4_t*>(o + 4) = s1;
-        }
-      } else if (a.stat_part) {
-        *reinterpret_cast<f32x4_t*>(o) = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-        *reinterpret_cast<f32x4_t*>(o + 4) = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-      }
-    }
-    if (a.stat_part) {
-      // column sums of the stored values: RS row ranges per column, then a
-      // fixed-order sum of the ranges
-      constexpr int RS = NT / BN > 0 ? NT / BN : 1;
-      constexpr int RROWS = BM / RS;
-      static_assert(BM % RS == 0 && RROWS % 4 == 0, "row ranges");
-      __shared__ double sred[RS][2][BN];
-      __syncthreads();
-      if (tid < RS * BN) {
-        const int col = tid % BN, part = tid / BN;
-        const float* oc = ot + part * RROWS * OPITCH + col;
-        // four interleaved partial sums, added in a fixed order
-        double s0[4] = {0.0, 0.0, 0.0, 0.0}, s1[4] = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-        for (int r = 0; r < RROWS; ++r) {
-          const double sv = (double)oc[r * OPITCH];
-          s0[r & 3] += sv;
-          s1[r & 3] += sv * sv;
-        }
-        sred[part][0][col] = (s0[0] + s0[1]) + (s0[2] + s0[3]);
-        sred[part][1][col] = (s1[0] + s1[1]) + (s1[2] + s1[3]);
-      }
-      __syncthreads();
-      for (int col = tid; col < BN; col += NT) {
-        const int n = n0 + col;
-        if (n >= a.N) continue;
-        double s0 = 0.0, s1 = 0.0;
-#pragma unroll
-        for (int q = 0; q < RS; ++q) {
-          s0 += sred[q][0][col];
-          s1 += sred[q][1][col];
-        }
-        a.stat_part[((size_t)n * 2 + 0) * gridDim.x + tm] = s0;
-        a.stat_part[((size_t)n * 2 + 1) * gridDim.x + tm] = s1;
-      }
-    }
+    conv_epilogue_bf16<BM, BN, NT, OPITCH>(a, ot, tid, m0, n0, tm, M);
   } else {
     // epilogue (fp32 storage): bias, ReLU, mask, accumulate, round once on store
     constexpr int NCOL = M32 ? TN2 : TN;  // column groups per lane

@@ -414,13 +414,27 @@ def time_sweep(n, steps):
     # momentum SGD 36 B/param (W, buf, m, v, G in; W, buf, m, v out) + zero + 2 predictions
     # = 48; RMSProp adds the squared average (44 + 12 = 56)
     buf, sq = (torch.from_numpy(a).cuda() for a in wl.rule_state(n))
+    s_extra = torch.empty_like(W)
     rule = xp.Rule(rule=xp.RULE_MOMENTUM_SGD, lr=1e-2, momentum=0.9, weight_decay=5e-4)
     ms = timed(lambda: xp.xpipe_rule_flat(W, buf, None, m, v, G, rule, hp, 100, True, pf, 2, pb, 1), reps)
     res["momentum_sgd_zero_grad_2pred"] = {"ms": ms, "GB_s": 48.0 * n / ms / 1e6}
     rule = xp.Rule(rule=xp.RULE_RMSPROP, lr=1e-4, momentum=0.9, alpha=0.99, eps=1e-8)
     ms = timed(lambda: xp.xpipe_rule_flat(W, buf, sq, m, v, G, rule, hp, 100, True, pf, 2, pb, 1), reps)
     res["rmsprop_zero_grad_2pred"] = {"ms": ms, "GB_s": 56.0 * n / ms / 1e6}
-    del W, m, v, G, out, pf, pb, buf, sq
+    # the attainable rate of each pass's access pattern on this GPU: a bare
+    # stream with the same numbers of 16-byte reads and writes per element
+    ceil = {}
+    for key, (nr, nw) in {"predict": (3, 1), "adam": (4, 3), "adam_zero_grad_2pred": (4, 6)}.items():
+        srcs = [W, m, v, G][:nr]
+        dsts = [out, pf, pb, buf, sq, s_extra][:nw]
+        ms = timed(lambda: xp.xpipe_probe_stream(srcs, dsts), reps)
+        ceil[key] = {"reads": nr, "writes": nw, "ms": ms, "GB_s": 4.0 * (nr + nw) * n / ms / 1e6}
+    res["stream_ceiling"] = ceil
+    for k in list(res):
+        base = "predict" if k.startswith("predict_s") else k
+        if base in ceil:
+            res[k]["frac_of_stream_ceiling"] = round(res[k]["GB_s"] / ceil[base]["GB_s"], 4)
+    del W, m, v, G, out, pf, pb, buf, sq, s_extra
     torch.cuda.empty_cache()
     return res
 
@@ -747,11 +761,18 @@ def main():
         rf["frac_of_measured_peak"] = round(rf["achieved"] / pk["hbm_copy_GB_s"], 4)
     if not args.no_sweep:
         sw = time_sweep(args.sweep_n, args.steps)
+        ceil = sw.pop("stream_ceiling")
         out["predict_adam_sweep"] = {"n_params": args.sweep_n, "t": 100,
                                      **{k: {"ms": round(v["ms"], 4), "GB_s": round(v["GB_s"], 1),
                                             "frac_hbm": round(v["GB_s"] / HBM_PEAK_GBS, 4),
-                                            "frac_measured_copy": round(v["GB_s"] / pk["hbm_copy_GB_s"], 4)}
-                                        for k, v in sw.items()}}
+                                            "frac_measured_copy": round(v["GB_s"] / pk["hbm_copy_GB_s"], 4),
+                                            **({"frac_of_stream_ceiling": v["frac_of_stream_ceiling"]}
+                                               if "frac_of_stream_ceiling" in v else {})}
+                                        for k, v in sw.items()},
+                                     "stream_ceiling": {k: {"reads": v["reads"], "writes": v["writes"],
+                                                            "GB_s": round(v["GB_s"], 1),
+                                                            "frac_hbm": round(v["GB_s"] / HBM_PEAK_GBS, 4)}
+                                                        for k, v in ceil.items()}}
     if not args.no_sweep:
         out["interleaved_schedule"] = time_interleaved(args)
         out["vgg16_partitioned"] = time_partitioned(args, "vgg16")

@@ -402,6 +402,17 @@ xpipe_status xpipe_stage_timing_entry(xpipe_stage_t st, int32_t i, const char** 
  * operands and writes one float per wave to out[waves] (so the work is kept);
  * flops = waves * iters * 8 * 32768.  Both enqueue on hip_stream. */
 xpipe_status xpipe_probe_copy(const void* src, void* dst, int64_t bytes, void* hip_stream);
+/* xpipe_probe_stream: a bare stream of a pass's shape, the attainable HBM
+ * rate the prediction and update passes are compared with: each of nsrc
+ * (0..4) fp32 buffers of n elements is read once and each of ndst (1..6) is
+ * written once (the element-wise sum of the sources), 16 bytes per thread and
+ * buffer with the passes' non-temporal hints.  n a multiple of 4; every
+ * buffer 16-byte aligned and non-overlapping; src / dst are host arrays of
+ * device pointers.  Prediction: 3 reads, 1 write; Adam: 4 and 3; Adam fused
+ * with zeroing the gradient and both predictions: 4 and 6. */
+xpipe_status xpipe_probe_stream(const float* const* src, int32_t nsrc, float* const* dst, int32_t ndst,
+                                int64_t n, void* hip_stream);
+
 xpipe_status xpipe_probe_mfma(float* out, int32_t waves, int32_t iters, void* hip_stream);
 
 /* Message for the last non-OK status returned on the calling thread. */

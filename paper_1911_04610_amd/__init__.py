@@ -127,6 +127,7 @@ _SIGS = {
                         _P],
     "xpipe_probe_copy": [_P, _P, _I64, _P],
     "xpipe_probe_mfma": [_P, _I32, _I32, _P],
+    "xpipe_probe_stream": [ctypes.POINTER(_P), _I32, ctypes.POINTER(_P), _I32, _I64, _P],
     "xpipe_stage_set_timing": [_P, _I32],
     "xpipe_stage_set_graphs": [_P, _I32],
     "xpipe_stage_timing_count": [_P, ctypes.POINTER(_I32)],
@@ -406,6 +407,15 @@ def xpipe_probe_copy(src, dst, stream=None):
 def xpipe_probe_mfma(out, iters: int, stream=None):
     """One wave per element of the float32 tensor `out`, `iters` rounds of 8 MFMAs each."""
     _check(lib().xpipe_probe_mfma(_ptr(out), out.numel(), int(iters), _stream_ptr(stream)))
+
+
+def xpipe_probe_stream(srcs, dsts, stream=None):
+    """Bare stream: every float32 tensor in srcs read once, every one in dsts
+    written once (all of one size, a multiple of 4 elements)."""
+    n = dsts[0].numel()
+    S = (_P * max(len(srcs), 1))(*[_ptr(t) for t in srcs])
+    D = (_P * len(dsts))(*[_ptr(t) for t in dsts])
+    _check(lib().xpipe_probe_stream(S, len(srcs), D, len(dsts), n, _stream_ptr(stream)))
 
 
 def xpipe_adam_flat(W, m, v, G, hp: Hyper, t: int, zero_grad=True, pred_fwd=None, s_fwd=0,

@@ -395,6 +395,30 @@ hipError_t launch_probe_copy(const void* src, void* dst, int64_t bytes, hipStrea
   return hipGetLastError();
 }
 
+// a bare stream of the passes' shape: nsrc 16-byte reads and ndst 16-byte
+// writes per thread (non-temporal, as the passes), one add per element
+__global__ __launch_bounds__(256) void k_probe_stream(StreamArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.n) return;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int j = 0; j < STREAM_MAX_SRC; ++j)
+    if (j < a.nsrc) {
+      const float4 v = ldnt(reinterpret_cast<const float4*>(a.src[j]) + i);
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+#pragma unroll
+  for (int j = 0; j < STREAM_MAX_DST; ++j)
+    if (j < a.ndst) stnt(reinterpret_cast<float4*>(a.dst[j]) + i, acc);
+}
+
+hipError_t launch_probe_stream(const StreamArgs& a, hipStream_t s) {
+  if (a.n <= 0) return hipSuccess;
+  XP_LAUNCH("k_probe_stream", (double)a.n * 16 * (a.nsrc + a.ndst), k_probe_stream,
+            dim3((unsigned)((a.n + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_probe_mfma(float* out, int waves, int iters, hipStream_t s) {
   if (waves <= 0 || iters <= 0) return hipSuccess;
   XP_LAUNCH("k_probe_mfma", (double)waves * iters * 8 * 32768.0, k_probe_mfma,

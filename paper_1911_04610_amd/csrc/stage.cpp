@@ -2086,6 +2086,29 @@ xpipe_status xpipe_probe_copy(const void* src, void* dst, int64_t bytes, void* h
   return XPIPE_OK;
 }
 
+xpipe_status xpipe_probe_stream(const float* const* src, int32_t nsrc, float* const* dst, int32_t ndst,
+                                int64_t n, void* hip_stream) {
+  if (n < 0 || (n % 4) != 0) return fail(XPIPE_EINVAL, "n must be a non-negative multiple of 4");
+  if (nsrc < 0 || nsrc > STREAM_MAX_SRC || ndst < 1 || ndst > STREAM_MAX_DST)
+    return fail(XPIPE_EINVAL, "0..4 sources and 1..6 destinations");
+  if (n == 0) return XPIPE_OK;
+  if ((nsrc > 0 && !src) || !dst) return fail(XPIPE_EINVAL, "null pointer array");
+  StreamArgs a{};
+  for (int j = 0; j < nsrc; ++j) {
+    if (!src[j] || !aligned16(src[j])) return fail(XPIPE_EINVAL, "sources must be 16-byte aligned");
+    a.src[j] = src[j];
+  }
+  for (int j = 0; j < ndst; ++j) {
+    if (!dst[j] || !aligned16(dst[j])) return fail(XPIPE_EINVAL, "destinations must be 16-byte aligned");
+    a.dst[j] = dst[j];
+  }
+  a.nsrc = nsrc;
+  a.ndst = ndst;
+  a.n = n / 4;
+  XP_HIP(launch_probe_stream(a, (hipStream_t)hip_stream));
+  return XPIPE_OK;
+}
+
 xpipe_status xpipe_probe_mfma(float* out, int32_t waves, int32_t iters, void* hip_stream) {
   if (waves < 0 || iters < 0) return fail(XPIPE_EINVAL, "negative size");
   if (waves == 0 || iters == 0) return XPIPE_OK;

@@ -248,5 +248,16 @@ hipError_t launch_softmax_ce(int dtype, const CeArgs& a, hipStream_t s);
 // ---------------------------------------------------------------- measurement probes
 hipError_t launch_probe_copy(const void* src, void* dst, int64_t bytes, hipStream_t s);
 hipError_t launch_probe_mfma(float* out, int waves, int iters, hipStream_t s);
+// measurement probe: n 16-byte vectors read from each of nsrc buffers and
+// written to each of ndst buffers
+constexpr int STREAM_MAX_SRC = 4, STREAM_MAX_DST = 6;
+struct StreamArgs {
+  const float* src[STREAM_MAX_SRC];
+  float* dst[STREAM_MAX_DST];
+  int nsrc, ndst;
+  int64_t n;  // 16-byte vectors per buffer
+};
+hipError_t launch_probe_stream(const StreamArgs& a, hipStream_t s);
+
 
 }  // namespace xp

@@ -132,6 +132,17 @@ def test_flat_entry_points_check_arguments_on_the_host():
     # misaligned buffers are refused before any launch
     assert L.xpipe_predict_flat(20, 16, 16, 16, None, 8, 1, ctypes.byref(hp), None) == xp.EINVAL
     assert L.xpipe_adam_flat(None, None, None, None, 0, ctypes.byref(hp), 1, None, 0, None, 0, None) == xp.OK
+    # the bare-stream probe: counts, sizes and alignment are checked first
+    P = ctypes.c_void_p
+    src = (P * 4)(16, 32, 48, 64)
+    dst = (P * 7)(*([80] * 7))
+    assert L.xpipe_probe_stream(src, 5, dst, 1, 16, None) == xp.EINVAL      # > 4 sources
+    assert L.xpipe_probe_stream(src, 1, dst, 7, 16, None) == xp.EINVAL      # > 6 destinations
+    assert L.xpipe_probe_stream(src, 1, dst, 0, 16, None) == xp.EINVAL      # no destination
+    assert L.xpipe_probe_stream(src, 1, dst, 1, 6, None) == xp.EINVAL       # n not a multiple of 4
+    assert L.xpipe_probe_stream(src, 1, dst, 1, 0, None) == xp.OK           # nothing to do
+    mis = (P * 1)(20)
+    assert L.xpipe_probe_stream(mis, 1, dst, 1, 16, None) == xp.EINVAL      # misaligned source
 
 
 @pytest.mark.parametrize("rounding", [0, 2])

@@ -106,7 +106,8 @@ XP_DEV int xcd_tile(int l, int G) {
 // once) with 16-byte loads and stores, leaves the stored values in LDS, and
 // the batch-norm column statistics of the tile are taken from there.
 template <int BM, int BN, int NT, int OPITCH>
-XP_DEV void conv_epilogue_bf16(const ConvArgs& a, float* ot, int tid, int m0, int n0, int tm, int M) {
+XP_DEV void conv_epilogue_bf16(const ConvArgs& a, float* ot, int tid, int m0, int n0, int tm, int M,
+                               int row_tiles) {
   typedef bf16_t T;
   T* __restrict__ y = (T*)a.y;
   const T* __restrict__ mask = (const T*)a.mask;
@@ -256,8 +257,8 @@ XP_DEV void conv_epilogue_bf16(const ConvArgs& a, float* ot, int tid, int m0, in
         s0 += sred[q][0][col];
         s1 += sred[q][1][col];
       }
-      a.stat_part[((size_t)n * 2 + 0) * gridDim.x + tm] = s0;
-      a.stat_part[((size_t)n * 2 + 1) * gridDim.x + tm] = s1;
+      a.stat_part[((size_t)n * 2 + 0) * row_tiles + tm] = s0;
+      a.stat_part[((size_t)n * 2 + 1) * row_tiles + tm] = s1;
     }
   }
 }
@@ -634,7 +635,7 @@ __global__ __launch_bounds__(WM * WN * 64) void k_conv_gemm(ConvArgs a) {
                 acc[i][j][q];
     }
     __syncthreads();
-    conv_epilogue_bf16<BM, BN, NT, OPITCH>(a, ot, tid, m0, n0, tm, M);
+    conv_epilogue_bf16<BM, BN, NT, OPITCH>(a, ot, tid, m0, n0, tm, M, gridDim.x);
   } else {
     // epilogue (fp32 storage): bias, ReLU, mask, accumulate, round once on store
     constexpr int NCOL = M32 ? TN2 : TN;  // column groups per lane

@@ -470,15 +470,18 @@ def measured_peaks():
             "copy_bytes": 2 * n, "mfma": "v_mfma_f32_32x32x16_bf16, %d waves x %d x 8" % (waves, iters)}
 
 
-def vendor_reference(reps=50):
-    """The stage's two most frequent convolution shapes (32 x 35 x 35 NHWC,
-    bf16) three ways, per launch, with HIP events over back-to-back launches:
-    this library's implicit GEMM (forward of a one-convolution stage: one
-    k_conv_gemm launch), MIOpen's convolution through torch (channels-last),
-    and hipBLASLt's plain GEMM of the same M x K x N through torch.mm (no
-    im2col: the library GEMM reads a ready K-major operand, which the
-    convolution does not have).  Context for the MFMA fraction of these skinny
-    shapes, not a dependency: the stage itself never calls the vendor
+def vendor_reference(off_us, reps=50):
+    """The stage's convolution shapes (32 x 35 x 35 NHWC, bf16) against the
+    vendor libraries, per launch, with HIP events over back-to-back launches.
+    Forward: this library's implicit GEMM (forward of a one-convolution
+    stage: one k_conv_gemm launch), MIOpen's convolution through torch
+    (channels-last), and hipBLASLt's plain GEMM of the same M x K x N through
+    torch.mm (no im2col: the library GEMM reads a ready K-major operand, which
+    the convolution does not have).  Weight gradient: this library's
+    k_wgrad_b plus its split reduction (per-launch events in the one-
+    convolution stage's backward, event offset removed) against MIOpen's
+    backward-weights convolution.  Context for the MFMA fraction of these
+    skinny shapes, not a dependency: the stage itself never calls the vendor
     libraries."""
     import numpy as np
     import torch
@@ -500,7 +503,7 @@ def vendor_reference(reps=50):
     torch.backends.cudnn.benchmark = True  # MIOpen picks its fastest algorithm per shape
     out = []
     nb, H, W = 32, 35, 35
-    for cin, cout, k in ((64, 96, 3), (96, 96, 3)):
+    for cin, cout, k in ((64, 96, 3), (96, 96, 3), (48, 64, 5), (256, 176, 1)):
         b = wl._Builder()
         b.conv(-1, cin, cout, k)
         st = xp.Stage(b.layers, nb, 1, (H, W, cin), xp.BF16, stream=torch.cuda.current_stream())
@@ -525,12 +528,34 @@ def vendor_reference(reps=50):
         B = torch.randn(K, cout, device="cuda").to(torch.bfloat16)
         blas = timed(lambda: A @ B)
         fl = 2.0 * M * cout * K
+        # weight gradient: the backward of the one-convolution stage (no input
+        # gradient); only its weight-gradient launches are counted
+        st.xpipe_predict_weights(xp.BWD, 0, hp, 0)
+        dy = torch.randn(nb, H, W, cout, device="cuda").to(torch.bfloat16)
+        for _ in range(3):
+            st.xpipe_stage_bwd(x, dy)
+        torch.cuda.synchronize()
+        st.set_timing(True)
+        for _ in range(reps):
+            st.xpipe_stage_bwd(x, dy)
+        torch.cuda.synchronize()
+        tm = st.timing()
+        st.set_timing(False)
+        wl_names = sorted(n for n in tm if n.startswith(("k_wgrad", "k_split_reduce")))
+        ours_wg = sum(tm[n][0] * 1e3 - off_us * tm[n][1] for n in wl_names) / reps
+        dyc = dy.permute(0, 3, 1, 2)
+        miopen_wg = timed(lambda: torch.ops.aten.convolution_backward(
+            dyc, xc, wt, None, [1, 1], [k // 2, k // 2], [1, 1], False, [0, 0], 1, [False, True, False]))
         out.append({"shape": f"conv {k}x{k} {cin}->{cout}, 32x35x35 NHWC bf16 (M={M}, N={cout}, K={K})",
                     "ours_us": round(ours, 2), "ours_launches": launched, "miopen_conv_us": round(miopen, 2),
                     "hipblaslt_gemm_us": round(blas, 2),
                     "ours_TFLOP_s": round(fl / ours / 1e6, 1),
                     "miopen_TFLOP_s": round(fl / miopen / 1e6, 1),
-                    "hipblaslt_TFLOP_s": round(fl / blas / 1e6, 1)})
+                    "hipblaslt_TFLOP_s": round(fl / blas / 1e6, 1),
+                    "wgrad_ours_us": round(ours_wg, 2), "wgrad_ours_launches": wl_names,
+                    "wgrad_miopen_us": round(miopen_wg, 2),
+                    "wgrad_ours_TFLOP_s": round(fl / ours_wg / 1e6, 1),
+                    "wgrad_miopen_TFLOP_s": round(fl / miopen_wg / 1e6, 1)})
         del st
     return out
 
@@ -778,7 +803,7 @@ def main():
         out["vgg16_partitioned"] = time_partitioned(args, "vgg16")
         out["resnet101_partitioned"] = time_partitioned(args, "resnet101")
         out["inception_v3_partitioned"] = time_partitioned(args, "inception_v3")
-        out["vendor_reference"] = vendor_reference()
+        out["vendor_reference"] = vendor_reference(off_us)
     if not args.no_legs:
         out["configs"] = config_legs(args, off_us)
     if not args.no_cpu_baseline:

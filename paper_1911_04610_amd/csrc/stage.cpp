@@ -53,8 +53,11 @@ constexpr int64_t PARAM_ALIGN = 64;  // elements
 constexpr size_t WS_ALIGN = 256;     // bytes
 constexpr double BN_EPS = 1e-5;
 // launch lanes: the stage's stream plus auxiliary streams on which independent
-// branches of the layer graph run concurrently
-constexpr int NLANES = 4;
+// branches of the layer graph run concurrently.  Three: on the Inception-A
+// step (four branches per module) a fourth lane made the recorded step slower
+// (8.24 against 7.88 ms), and so did six or eight lanes (8.8 ms), two (7.97)
+// or one (9.64)
+constexpr int NLANES = 3;
 
 int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 

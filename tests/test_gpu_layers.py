@@ -62,6 +62,9 @@ LAYER_CASES = {
     "conv5x5_c48": ([conv(-1, 48, 64, 5)], (11, 11, 48), 2),
     "conv3x3_c3_flat": ([conv(-1, 3, 64, 3, True)], (18, 18, 3), 2),
     "conv_n96_c96": ([conv(-1, 96, 96, 3)], (7, 9, 96), 2),
+    # 2 450 pixels per micro-batch: the 96 x 128 weight-gradient tile over
+    # several pixel splits (K = 864: a ragged last K block)
+    "conv_n96_c96_splits": ([conv(-1, 96, 96, 3)], (35, 35, 96), 2),
     # 65 884 rows (a ragged last tile): the 128-row tiles of large images,
     # 128 columns on eight waves (forward) and 64 (data gradient); then N = 160
     "conv3x3_many_rows_n128": ([conv(-1, 64, 128, 3)], (182, 181, 64), 2),

@@ -309,7 +309,11 @@ void plan_lanes(Plan& p) {
     }
     // recording order: an op is ready once the previous op of its lane (in
     // pass order) and the ops it waits for are placed; among ready ops take
-    // the lane placed least recently, then pass order
+    // the one with the longest path to the end of the pass (GEMM ops weigh 3
+    // forward, 6 backward, the others 1), then pass order.  The graph's nodes
+    // are dispatched in this order when several are ready: on the Inception-A
+    // step this took 7.77 -> 7.57 ms against taking the lane placed least
+    // recently (7.85 ms in plain pass order); other weights gave the same
     std::vector<int> seq;  // pass order without concats
     for (int q = 0; q < n; ++q) {
       const int i = pass == 0 ? q : n - 1 - q;
@@ -320,25 +324,37 @@ void plan_lanes(Plan& p) {
       prev[i] = last[p.ops[i].lane[pass]];
       last[p.ops[i].lane[pass]] = i;
     }
+    std::vector<double> level(n, 0.0);  // longest weighted path to the pass end
+    {
+      std::vector<std::vector<int>> succ(n);
+      for (int i : seq) {
+        if (prev[i] >= 0) succ[prev[i]].push_back(i);
+        for (int j : p.ops[i].waits[pass]) succ[j].push_back(i);
+      }
+      for (int q = (int)seq.size() - 1; q >= 0; --q) {
+        const int i = seq[q];
+        double m = 0.0;
+        for (int k : succ[i]) m = std::max(m, level[k]);
+        level[i] = (p.ops[i].kind == OP_GEMM ? (pass == 1 ? 6.0 : 3.0) : 1.0) + m;
+      }
+    }
     std::vector<char> placed(n, 0);
-    std::vector<long> lane_used(NLANES, -1);
     std::vector<int>& order = p.rec_order[pass];
     order.clear();
-    for (long step = 0; order.size() < seq.size(); ++step) {
+    while (order.size() < seq.size()) {
       int pick = -1;
       for (int i : seq) {
         if (placed[i] || (prev[i] >= 0 && !placed[prev[i]])) continue;
         bool ready = true;
         for (int j : p.ops[i].waits[pass]) ready = ready && placed[j];
         if (!ready) continue;
-        if (pick < 0 || lane_used[p.ops[i].lane[pass]] < lane_used[p.ops[pick].lane[pass]]) pick = i;
+        if (pick < 0 || level[i] > level[pick]) pick = i;
       }
       if (pick < 0) {  // cannot happen for a plan built above; keep pass order
         order = seq;
         break;
       }
       placed[pick] = 1;
-      lane_used[p.ops[pick].lane[pass]] = step;
       order.push_back(pick);
     }
   }

@@ -76,9 +76,9 @@ def kernel_key(name):
     if m:
         gm = int(m.group(2))
         n = "k_conv_gemm<" + m.group(1) + ("" if gm == 0 else "," + ("strided", "strided_dgrad")[gm - 1]) + ">"
-    m = re.match(r"^k_wgrad_b<((?:\d+,){4}\d+),(true|false)>$", n)
+    m = re.match(r"^k_wgrad_t<((?:\d+,){4}\d+),(true|false)>$", n)
     if m:
-        n = "k_wgrad_b<" + m.group(1) + (",grid>" if m.group(2) == "true" else ">")
+        n = "k_wgrad_t<" + m.group(1) + (",grid>" if m.group(2) == "true" else ">")
     return re.sub(r"^(k_bn_apply_v|k_bn_bwd_v|k_maxpool3s2_fwd|k_maxpool3s2_bwd)<(bf16|f32),\d+>$",
                   r"\1<\2>", n)
 
@@ -478,7 +478,7 @@ def vendor_reference(off_us, reps=50):
     (channels-last), and hipBLASLt's plain GEMM of the same M x K x N through
     torch.mm (no im2col: the library GEMM reads a ready K-major operand, which
     the convolution does not have).  Weight gradient: this library's
-    k_wgrad_b plus its split reduction (per-launch events in the one-
+    k_wgrad_t plus its split reduction (per-launch events in the one-
     convolution stage's backward, event offset removed) against MIOpen's
     backward-weights convolution.  Context for the MFMA fraction of these
     skinny shapes, not a dependency: the stage itself never calls the vendor

@@ -974,27 +974,37 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs a) {
       }
 }
 
+
 // bf16 weight gradient, 16-byte chunk path (channels, output channels and row
-// strides multiples of 8, views below 2 GiB).  Same tiles and LDS layout as
-// k_wgrad; the operands load through raw buffer resources (out-of-range
-// offsets read zeros), addresses advance by a scalar per step, each thread
-// tracks the image row / column of its pixels incrementally, and PF steps of
-// loads are in flight.
+// strides multiples of 8, views below 2 GiB), 32x32 wave tiles.  The operands
+// load through raw buffer resources (out-of-range offsets read zeros),
+// addresses advance by a scalar per step, each thread tracks the image row /
+// column of its pixel incrementally, and PF steps of loads are in flight.
+// The reduction runs over pixels, which are the rows of both operands in
+// memory, while an MFMA fragment holds 8 consecutive pixels of one column: the
+// tiles therefore sit in LDS as loaded (one row per pixel, 16-byte stores) and
+// the fragments are read with gfx950's transposing LDS read.  Interleaving
+// pixel pairs into column-major rows on the way into LDS instead (two
+// permutes and two 4-byte LDS stores per 16 loaded bytes) was 30% slower on
+// the 3x3 and 5x5 stage shapes (3x3 64 -> 96: 35.4 -> 24.6 us with the split
+// reduction), with the same bits.
 // GRID: dz lives on the Ho x Wo grid of a strided or unpadded convolution (or
 // the rows and columns pad differently); each pixel then tracks its image, row
 // and column and addresses x at (ho*stride + r - pad, wo*stride + q - padw)
 template <int BM, int BN, int WM, int WN, int PF, bool GRID>
-__global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
+__global__ __launch_bounds__(256) void k_wgrad_t(WgradArgs a) {
   using T = bf16_t;
   // 64 pixels per step: four 32x32x16 MFMAs per wave between barriers (32 took
   // 4-8% longer on the stage shapes)
-  constexpr int VEC = 8, BKm = 64, RPT = 2;
-  constexpr int PA = BKm + 8, PB = BKm + 8;
-  __shared__ __align__(16) T sA[2][BM * PA];
-  __shared__ __align__(16) T sB[2][BN * PB];
+  constexpr int VEC = 8, BKm = 64, RPT = 1;
+  // rows = pixels, as loaded; a row pitch of 32 bytes over the tile width puts
+  // the four rows one transposing read touches in disjoint banks
+  constexpr int PA = BM + 16, PB = BN + 16;
+  __shared__ __align__(16) T sA[2][BKm * PA];
+  __shared__ __align__(16) T sB[2][BKm * PB];
   constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
   static_assert(WM * WN == 4, "four waves");
-  constexpr int A_T = (BKm / 2) * (BM / VEC), B_T = (BKm / 2) * (BN / VEC);
+  constexpr int A_T = BKm * (BM / VEC), B_T = BKm * (BN / VEC);
   constexpr int A_PER = (A_T + 255) / 256, B_PER = (B_T + 255) / 256;
   constexpr uint32_t OUT_OF_RANGE = 0x80000000u;
 
@@ -1107,41 +1117,21 @@ __global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
     ++loaded;
   };
 
+  // each task's 16 bytes (8 channels of one pixel) go to its pixel's row as
+  // loaded: no interleaving
   auto lstore = [&](auto SLOT, int buf) __attribute__((always_inline)) {
     constexpr int slot = decltype(SLOT)::value;
-    // interleave two pixels: word e of row (chunk*8 + e) holds (pixel 2p, pixel 2p+1)
 #pragma unroll
-    for (int i = 0; i < A_PER; ++i) {
-      if (!a_slot[i]) continue;
-      const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&ra[slot][i][0]);
-      const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&ra[slot][i][1]);
+    for (int i = 0; i < A_PER; ++i)
+      if (a_slot[i]) *reinterpret_cast<uint4*>(&sA[buf][a_p[i] * PA + a_c[i] * VEC]) = ra[slot][i][0];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t lo = __builtin_amdgcn_perm(r1[j], r0[j], 0x05040100u);
-        const uint32_t hi = __builtin_amdgcn_perm(r1[j], r0[j], 0x07060302u);
-        const int row = a_c[i] * VEC + 2 * j;
-        *reinterpret_cast<uint32_t*>(&sA[buf][row * PA + 2 * a_p[i]]) = lo;
-        *reinterpret_cast<uint32_t*>(&sA[buf][(row + 1) * PA + 2 * a_p[i]]) = hi;
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < B_PER; ++i) {
-      if (!b_slot[i]) continue;
-      const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&rb[slot][i][0]);
-      const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&rb[slot][i][1]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t lo = __builtin_amdgcn_perm(r1[j], r0[j], 0x05040100u);
-        const uint32_t hi = __builtin_amdgcn_perm(r1[j], r0[j], 0x07060302u);
-        const int row = b_c[i] * VEC + 2 * j;
-        *reinterpret_cast<uint32_t*>(&sB[buf][row * PB + 2 * b_p[i]]) = lo;
-        *reinterpret_cast<uint32_t*>(&sB[buf][(row + 1) * PB + 2 * b_p[i]]) = hi;
-      }
-    }
+    for (int i = 0; i < B_PER; ++i)
+      if (b_slot[i]) *reinterpret_cast<uint4*>(&sB[buf][b_p[i] * PB + b_c[i] * VEC]) = rb[slot][i][0];
   };
 
   // wave tiles that are multiples of 32 use v_mfma_f32_32x32x16_bf16
   constexpr bool M32 = WTM % 32 == 0 && WTN % 32 == 0;
+  static_assert(M32, "32x32 wave tiles");
   constexpr int TM2 = M32 ? WTM / 32 : 1, TN2 = M32 ? WTN / 32 : 1;
   f32x4_t acc[M32 ? 1 : TM][M32 ? 1 : TN];
   f32x16_t acc2[TM2][TN2];
@@ -1158,45 +1148,41 @@ __global__ __launch_bounds__(256) void k_wgrad_b(WgradArgs a) {
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc2[i][j][q] = 0.f;
 
+  // MFMA fragments straight from the pixel-major tiles with gfx950's
+  // transposing LDS read: in each group of 16 lanes, output e (0..3) of lane i
+  // is element i % 4 of the 8 bytes that lane 4 e + i / 4 of the group
+  // addressed.  A 32x32x16 fragment (lane l: row l % 32, pixels 8 (l / 32) ..
+  // + 8 of the 16-pixel slice) is two such reads: lane j of a group addresses
+  // pixel 8 (l / 32) + j / 4 (+ 4 for the second read), columns
+  // 16 ((l % 32) / 16) + 4 (j % 4) .. + 4 of the wave's 32.
+  const int tr_px = 8 * (lane >> 5) + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane & 31) >> 4) + 4 * (lane & 3);
+  auto tr_frag = [&](const T* base, int pitch, int col0, int px0) __attribute__((always_inline)) {
+    typedef short v4i16 __attribute__((ext_vector_type(4)));
+    const T* p = base + (px0 + tr_px) * pitch + col0 + tr_col;
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) v4i16*)(p));
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) v4i16*)(p + 4 * pitch));
+    typedef short v8i16 __attribute__((ext_vector_type(8)));
+    const v8i16 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8_t, v);
+  };
   auto compute = [&](int buf) __attribute__((always_inline)) {
     const T* A = sA[buf];
     const T* B = sB[buf];
-    if constexpr (M32) {
 #pragma unroll
-      for (int kk = 0; kk < BKm / 16; ++kk) {
-        bf16x8_t af[TM2], bfv[TN2];
+    for (int kk = 0; kk < BKm / 16; ++kk) {
+      bf16x8_t af[TM2], bfv[TN2];
 #pragma unroll
-        for (int i = 0; i < TM2; ++i)
-          af[i] = *reinterpret_cast<const bf16x8_t*>(
-              &A[(wm * WTM + i * 32 + (lane & 31)) * PA + kk * 16 + (lane >> 5) * 8]);
+      for (int i = 0; i < TM2; ++i) af[i] = tr_frag(A, PA, wm * WTM + i * 32, kk * 16);
+#pragma unroll
+      for (int j = 0; j < TN2; ++j) bfv[j] = tr_frag(B, PB, wn * WTN + j * 32, kk * 16);
+#pragma unroll
+      for (int i = 0; i < TM2; ++i)
 #pragma unroll
         for (int j = 0; j < TN2; ++j)
-          bfv[j] = *reinterpret_cast<const bf16x8_t*>(
-              &B[(wn * WTN + j * 32 + (lane & 31)) * PB + kk * 16 + (lane >> 5) * 8]);
-#pragma unroll
-        for (int i = 0; i < TM2; ++i)
-#pragma unroll
-          for (int j = 0; j < TN2; ++j)
-            acc2[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfv[j], acc2[i][j], 0, 0, 0);
-      }
-      return;
-    }
-#pragma unroll
-    for (int ks = 0; ks < BKm / 32; ++ks) {
-      bf16x8_t af[TM], bfv[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_t*>(
-            &A[(wm * WTM + i * 16 + (lane & 15)) * PA + ks * 32 + (lane >> 4) * 8]);
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bfv[j] = *reinterpret_cast<const bf16x8_t*>(
-            &B[(wn * WTN + j * 16 + (lane & 15)) * PB + ks * 32 + (lane >> 4) * 8]);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfv[j], acc[i][j], 0, 0, 0);
+          acc2[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfv[j], acc2[i][j], 0, 0, 0);
     }
   };
 
@@ -1530,9 +1516,8 @@ int conv_max_row_tiles(int M) { return (M + 31) / 32; }
 
 // The weight gradient of a filter with 65..96 output channels and K >= 768
 // takes one 96 x 128 tile per K block (all output channels at once, the
-// 32x32x16 form): 3x3 96 -> 96 over 32 x 35 x 35 pixels, 48.3 -> 43.4 us
-// with its split reduction; on 3x3 64 -> 96 (K = 576) the 64 x 64 tiles stay
-// faster (35.4 against 39.9 us)
+// 32x32x16 form): 3x3 96 -> 96 over 32 x 35 x 35 pixels, 35.9 -> 31.1 us
+// with its split reduction
 static bool wgrad_tile96(int N, int K, int taps) { return N > 64 && N <= 96 && taps > 1 && K >= 768; }
 
 int wgrad_pick_splits(int dtype, int M, int N, int K, int taps) {
@@ -1541,7 +1526,7 @@ int wgrad_pick_splits(int dtype, int M, int N, int K, int taps) {
   // and about 512 workgroups
   const bool bf = dtype == DT_BF16;
   // bf16, 65..96 output channels of a filter with K >= 768: one 96-row tile
-  // by 128 columns (k_wgrad_b<96,128>), about 512 workgroups
+  // by 128 columns (k_wgrad_t<96,128>), about 512 workgroups
   const bool t96 = bf && wgrad_tile96(N, K, taps);
   int bm = t96 ? 96 : bf ? 64 : (N <= 64 ? 64 : 128);
   int bn = t96 ? 128 : bf ? 64 : (K <= 64 ? 64 : 128);
@@ -1608,21 +1593,21 @@ static hipError_t wgrad_go(const WgradArgs& a, bool flat, hipStream_t s) {
 }
 
 template <int BM, int BN, int WM, int WN, int PF, bool GRID = false>
-static hipError_t wgrad_b_go(const WgradArgs& a, hipStream_t s) {
+static hipError_t wgrad_t_go(const WgradArgs& a, hipStream_t s) {
   int K = a.R * a.S * a.C;
   dim3 grid((a.N + BM - 1) / BM, (K + BN - 1) / BN, a.splits);
   const int pix = a.Ho > 0 ? a.Ho * a.Wo : a.H * a.W;
   double flops = 2.0 * a.nb * pix * (double)a.N * K;
   static char name[64];
-  snprintf(name, sizeof name, GRID ? "k_wgrad_b<%d,%d,%d,%d,%d,grid>" : "k_wgrad_b<%d,%d,%d,%d,%d>", BM, BN,
+  snprintf(name, sizeof name, GRID ? "k_wgrad_t<%d,%d,%d,%d,%d,grid>" : "k_wgrad_t<%d,%d,%d,%d,%d>", BM, BN,
            WM, WN, PF);
   WgradArgs b = a;
   b.direct = a.splits == 1;
-  XP_LAUNCH(name, flops,
-            (k_wgrad_b<BM, BN, WM, WN, PF, GRID>), grid, dim3(256), 0, s, b);
+  XP_LAUNCH(name, flops, (k_wgrad_t<BM, BN, WM, WN, PF, GRID>), grid, dim3(256), 0, s, b);
   if (b.direct) return hipGetLastError();
   return wgrad_reduce<bf16_t>(a, s);
 }
+
 
 template <typename T>
 static hipError_t wgrad_dispatch(const WgradArgs& a, hipStream_t s) {
@@ -1640,9 +1625,9 @@ static hipError_t wgrad_dispatch(const WgradArgs& a, hipStream_t s) {
     // same grid and square padding: pixel offsets shift with the pixel index;
     // otherwise each pixel addresses x from its own row and column
     if (chunks && a.Ho <= 0 && a.pad == a.padw && wgrad_tile96(a.N, K, a.R * a.S))
-      return wgrad_b_go<96, 128, 1, 4, 2>(a, s);
-    if (chunks && a.Ho <= 0 && a.pad == a.padw) return wgrad_b_go<64, 64, 2, 2, 1>(a, s);
-    if (chunks) return wgrad_b_go<64, 64, 2, 2, 1, true>(a, s);
+      return wgrad_t_go<96, 128, 1, 4, 2>(a, s);
+    if (chunks && a.Ho <= 0 && a.pad == a.padw) return wgrad_t_go<64, 64, 2, 2, 1>(a, s);
+    if (chunks) return wgrad_t_go<64, 64, 2, 2, 1, true>(a, s);
   }
   if (n64 && k64) return wgrad_go<T, 64, 64, 2, 2>(a, flat, s);
   if (n64) return wgrad_go<T, 64, 128, 2, 2>(a, flat, s);

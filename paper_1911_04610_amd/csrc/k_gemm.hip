@@ -208,7 +208,7 @@ XP_DEV void conv_epilogue_bf16(const ConvArgs& a, float* ot, int tid, int m0, in
       } else {
         for (int e = 0; e < ne; ++e) p[e] = (uint16_t)(pr[e >> 1] >> ((e & 1) * 16));
       }
-      if (a.stat_part) {
+      if (a.stat_part || a.bn_part) {
         f32x4_t s0, s1;
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
@@ -220,14 +220,18 @@ XP_DEV void conv_epilogue_bf16(const ConvArgs& a, float* ot, int tid, int m0, in
         *reinterpret_cast<f32x4_t*>(o) = s0;
         *reinterpret_cast<f32x4_t*>(o + 4) = s1;
       }
-    } else if (a.stat_part) {
+    } else if (a.stat_part || a.bn_part) {
       *reinterpret_cast<f32x4_t*>(o) = (f32x4_t){0.f, 0.f, 0.f, 0.f};
       *reinterpret_cast<f32x4_t*>(o + 4) = (f32x4_t){0.f, 0.f, 0.f, 0.f};
     }
   }
-  if (a.stat_part) {
-    // column sums of the stored values: RS row ranges per column, then a
-    // fixed-order sum of the ranges
+  if (a.stat_part || a.bn_part) {
+    // per column, over the tile's rows, the sums of the stored values and of
+    // their squares (batch-norm statistics), or, for a stored gradient g of a
+    // batch norm with input z (bn_part), the sums of g and of g (z - mean) rstd
+    // (its backward partials; z read a row at a time, columns across
+    // threads): RS row ranges per column, each with four interleaved fp64
+    // sums, then a fixed-order sum of the ranges
     constexpr int RS = NT / BN > 0 ? NT / BN : 1;
     constexpr int RROWS = BM / RS;
     static_assert(BM % RS == 0 && RROWS % 4 == 0, "row ranges");
@@ -236,18 +240,35 @@ XP_DEV void conv_epilogue_bf16(const ConvArgs& a, float* ot, int tid, int m0, in
     if (tid < RS * BN) {
       const int col = tid % BN, part = tid / BN;
       const float* oc = ot + part * RROWS * OPITCH + col;
-      // four interleaved partial sums, added in a fixed order
       double s0[4] = {0.0, 0.0, 0.0, 0.0}, s1[4] = {0.0, 0.0, 0.0, 0.0};
+      if (!a.bn_part) {
 #pragma unroll
-      for (int r = 0; r < RROWS; ++r) {
-        const double sv = (double)oc[r * OPITCH];
-        s0[r & 3] += sv;
-        s1[r & 3] += sv * sv;
+        for (int r = 0; r < RROWS; ++r) {
+          const double sv = (double)oc[r * OPITCH];
+          s0[r & 3] += sv;
+          s1[r & 3] += sv * sv;
+        }
+      } else if (n0 + col < a.N) {
+        const int n = n0 + col, mr = m0 + part * RROWS;
+        const double mu = a.bn_mean[n], rs = a.bn_rstd[n];
+        const bf16_t* zc = (const bf16_t*)a.bn_z + n;
+        // every load issued before the first use: rows past the last are
+        // read at the last row (their g is 0)
+        float zv[RROWS];
+#pragma unroll
+        for (int r = 0; r < RROWS; ++r) zv[r] = bf16_to_f32(zc[(size_t)min(mr + r, M - 1) * a.ld_bnz]);
+#pragma unroll
+        for (int r = 0; r < RROWS; ++r) {
+          const double g = (double)oc[r * OPITCH];  // 0 past the last row
+          s0[r & 3] += g;
+          s1[r & 3] += g * (((double)zv[r] - mu) * rs);
+        }
       }
       sred[part][0][col] = (s0[0] + s0[1]) + (s0[2] + s0[3]);
       sred[part][1][col] = (s1[0] + s1[1]) + (s1[2] + s1[3]);
     }
     __syncthreads();
+    double* part_out = a.bn_part ? a.bn_part : a.stat_part;
     for (int col = tid; col < BN; col += NT) {
       const int n = n0 + col;
       if (n >= a.N) continue;
@@ -257,8 +278,8 @@ XP_DEV void conv_epilogue_bf16(const ConvArgs& a, float* ot, int tid, int m0, in
         s0 += sred[q][0][col];
         s1 += sred[q][1][col];
       }
-      a.stat_part[((size_t)n * 2 + 0) * row_tiles + tm] = s0;
-      a.stat_part[((size_t)n * 2 + 1) * row_tiles + tm] = s1;
+      part_out[((size_t)n * 2 + 0) * row_tiles + tm] = s0;
+      part_out[((size_t)n * 2 + 1) * row_tiles + tm] = s1;
     }
   }
 }

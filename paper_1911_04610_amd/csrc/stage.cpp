@@ -112,6 +112,11 @@ struct Op {
   int64_t stat_block = -1;     // ... to this workspace block ([2][cout] doubles, then dbeta/dgamma)
   bool stats_fused = false;    // BN: statistics come from the producing GEMM
   int stats_from = -1;         // BN: index of that GEMM op (during planning)
+  // bf16: a BN whose output gradient is written whole by one GEMM's data
+  // gradient takes its backward column sums from that launch's epilogue
+  int bnb_bn = -1;             // GEMM: the BN op it computes them for
+  int bnb_gemm = -1;           // BN: the GEMM op that computes them
+  int64_t bnb_part_off = -1;   // GEMM: workspace bytes of those per-row-tile partials
   // launch lanes, per pass (0 forward, 1 backward): the lane this op runs on,
   // the ops (same pass) on other lanes it waits for, and whether later ops on
   // other lanes wait for it
@@ -150,6 +155,7 @@ struct xpipe_stage {
   std::vector<ParamT> params;
   std::vector<Tensor> tensors;  // [0] = stage input
   std::vector<Op> ops;
+  std::vector<int> bnb_nrb;     // per GEMM op with bnb_bn: row tiles of its last data-gradient launch
   int out_tensor = -1;          // stage output tensor (logits for a loss stage)
   bool has_loss = false;
   int classes = 0;
@@ -762,6 +768,35 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     }
   }
 
+  // ---- bf16: BN backward partials from the data-gradient epilogue of the one
+  // GEMM that writes the BN output's gradient (a standalone tensor, read by
+  // that GEMM only, written first and whole by its data gradient)
+  if (dtype == DT_BF16) {
+    for (size_t b = 0; b < p.ops.size(); ++b) {
+      Op& bn = p.ops[b];
+      if (bn.kind != OP_BN) continue;
+      const int t = bn.out;
+      if (t <= 0 || t == p.out_tensor || p.tensors[t].owner >= 0) continue;
+      bool owns = false;
+      for (const Tensor& u : p.tensors) owns = owns || u.owner == t;
+      if (owns) continue;
+      int user = -1, users = 0;
+      for (size_t j = 0; j < p.ops.size(); ++j) {
+        const Op& o = p.ops[j];
+        if (o.kind == OP_CONCAT) continue;
+        if (o.in == t || o.in2 == t) {
+          ++users;
+          user = (int)j;
+        }
+      }
+      if (users != 1) continue;
+      Op& g = p.ops[user];
+      if (g.kind != OP_GEMM || g.in != t || g.in2 == t || g.in_acc) continue;
+      g.bnb_bn = (int)b;
+      bn.bnb_gemm = user;
+    }
+  }
+
   // ---- launch lanes
   plan_lanes(p);
   if (const char* tr = std::getenv("XPIPE_TRACE_PLAN"); tr && *tr == '1') {
@@ -798,6 +833,8 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
         for (int d = 0; d < 2; ++d)
           op.wg_off[d] = take((size_t)op.cout * op.k * op.kw * op.cin * esz);
       if (op.stats) op.stat_block = take((size_t)4 * op.cout * sizeof(double));
+      if (op.bnb_bn >= 0)
+        op.bnb_part_off = take((size_t)conv_max_row_tiles((int)tin_.sh.rows()) * 2 * op.cin * sizeof(double));
       int M = (int)p.tensors[op.out].sh.rows();  // output pixels (the input's for stride 1)
       int K = op.k * op.kw * op.cin;
       int splits = wgrad_pick_splits(dtype, M, op.cout, K, op.k * op.kw);
@@ -1294,7 +1331,20 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
             a.Ho = tin.sh.H;
             a.Wo = tin.sh.W;
           }
-          XP_HIP(launch_conv_gemm(dt, a, s));
+          if (op.bnb_bn >= 0) {
+            // the input's batch norm: its backward partials come from here
+            const Op& bn = st->ops[op.bnb_bn];
+            View z = act(st, bn.in, c);
+            const double* bst = (const double*)(st->ws + bn.stat_off);
+            a.bn_part = (double*)(st->ws + op.bnb_part_off);
+            a.bn_z = z.p;
+            a.ld_bnz = z.ld;
+            a.bn_mean = bst;
+            a.bn_rstd = bst + bn.stat_ld;
+          }
+          int rows_tiles = 0;
+          XP_HIP(launch_conv_gemm(dt, a, s, &rows_tiles));
+          if (op.bnb_bn >= 0) st->bnb_nrb[i] = rows_tiles;
         }
         // the ops that wait for this one need only the input gradient (the
         // weight gradient is joined at the end of the pass): they are released
@@ -1373,7 +1423,12 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         ca.out1 = stats + 3 * ld;
         ca.grad0 = st->grad + op.g_off;
         ca.grad1 = st->grad + op.be_off;
-        {
+        if (op.bnb_gemm >= 0) {
+          // partials from the data-gradient epilogue that wrote g
+          ca.partial = (double*)(st->ws + st->ops[op.bnb_gemm].bnb_part_off);
+          ca.row_blocks = st->bnb_nrb[op.bnb_gemm];
+          XP_HIP(launch_colfinal(ca, s));
+        } else {
           XP_HIP(launch_colreduce(dt, ca, s));
         }
         BnBwdArgs b{};
@@ -1748,6 +1803,7 @@ xpipe_status create_stage(const xpipe_layer_desc* layers, int32_t n_layers, int3
   st->params = p.params;
   st->tensors = p.tensors;
   st->ops = p.ops;
+  st->bnb_nrb.assign(st->ops.size(), 0);
   st->rec_order[0] = p.rec_order[0];
   st->rec_order[1] = p.rec_order[1];
   st->out_tensor = p.out_tensor;

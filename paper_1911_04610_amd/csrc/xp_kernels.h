@@ -93,6 +93,15 @@ struct ConvArgs {
   int accumulate;       // y = y + result (after mask)
   double* stat_part;    // optional: per row tile, column sums of the stored y and of its
                         // squares, at stat_part[(n * 2 + {0,1}) * row_tiles + tile]
+  // optional (bf16): the stored y is the output gradient g of a batch norm
+  // whose input is z (view bn_z, ld_bnz) with batch mean / rstd bn_mean /
+  // bn_rstd; per row tile, the column sums of g and of g (z - mean) rstd, at
+  // bn_part[(n * 2 + {0,1}) * row_tiles + tile] (the BN backward's partials)
+  double* bn_part;
+  const void* bn_z;
+  int ld_bnz;
+  const double* bn_mean;
+  const double* bn_rstd;
   // general grid (Ho > 0: strided, or unpadded): the rows are an Ho x Wo grid
   // per image, stride >= 1.
   // tr = 0: forward, row (ho, wo) reads x at (ho*stride + r - pad, wo*stride + q - padw);

@@ -103,3 +103,34 @@ def test_fullsize_bf16_forward_matches_oracle(name):
         el = abs(float(loss.item()) - lr_) / abs(lr_)
         print(f"   loss {el:.2e}")
         assert el <= 2e-2
+
+
+def test_fullsize_bf16_exact_inputs_step_matches_oracle():
+    """The benchmarked storage type through a whole step at full size, where
+    its results are unique: the VGG stage (no biases) at micro-batch 32 and
+    32 x 32 on integer inputs with +-1 weights (workloads.exact_stage_inputs),
+    two accumulated micro-batches and two mini-batches, so the second
+    mini-batch runs on non-trivial predictions (t = 1, s_f = 2, s_b = 1;
+    Sec. III-B, Eq. 3).  Every forward partial sum is an exact fp32 integer
+    (the largest stored activation is about 3e5), so both sides store the
+    same bf16 values: the forward outputs bit for bit, every other tensor of
+    both mini-batches (input gradients, accumulated gradients, both
+    predictions, W, m, v) within the bf16 bar of 2e-2."""
+    from test_gpu_stage import EXACT_LR, TOL, _compare
+    from oracle.stage import _round_bf16
+    w = wl.shrink(wl.WORKLOADS["vgg16_stage0"](), T=2, minibatches=2,
+                  layers=wl.vgg_stage_layers(bias=False))
+    assert w.micro_batch == 32 and tuple(w.in_shape) == (32, 32, 3)
+    assert w.s_fwd > 0 and w.s_bwd > 0
+    inp = wl.exact_stage_inputs(w)
+    hp, ohp = xp.Hyper(lr=EXACT_LR), oracle.Hyper(lr=EXACT_LR)
+    gpu, _ = run_stage(w, inp, xp.BF16, hp, w.s_fwd, w.s_bwd)
+    ref = oracle.train_stage(oracle.Stage(w.layers, "bf16"), inp.params, inp.m, inp.v, inp.xs,
+                             w.s_fwd, w.s_bwd, ohp, dys=inp.dys)
+    for a, b in zip(ref[1].w_pred_fwd + ref[1].w_pred_bwd, inp.params):
+        assert np.array_equal(_round_bf16(a), b)     # same bf16 operands in mini-batch 2
+    assert not np.array_equal(ref[1].w_pred_fwd[0], inp.params[0])   # fp32 state moved
+    for j in range(2):
+        for a, b in zip(gpu[j].ys, ref[j].ys):
+            np.testing.assert_array_equal(np.asarray(a, np.float64).reshape(b.shape), b)
+    _compare(gpu, ref, TOL[xp.BF16], "vgg16_stage0/bf16/full-size/exact-inputs")

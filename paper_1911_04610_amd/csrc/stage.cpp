@@ -17,6 +17,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -283,7 +284,14 @@ void plan_lanes(Plan& p) {
             }
       }
     }
+    auto qpos = [&](int i) { return pass == 0 ? i : n - 1 - i; };
     std::vector<int> tail(NLANES, -1), tail_q(NLANES, -1);
+    // per lane: the pass position up to which each lane's ops are known to
+    // have completed (lane order and the waits so far); per op, that vector
+    // when it was placed
+    std::vector<std::array<int, NLANES>> vc(n);
+    std::array<int, NLANES> lane_vc[NLANES];
+    for (int l = 0; l < NLANES; ++l) lane_vc[l].fill(-1);
     for (int q = 0; q < n; ++q) {
       const int i = pass == 0 ? q : n - 1 - q;
       Op& op = p.ops[i];
@@ -307,11 +315,20 @@ void plan_lanes(Plan& p) {
       op.lane[pass] = lane;
       tail[lane] = i;
       tail_q[lane] = q;
-      for (int j : deps[i])
-        if (p.ops[j].lane[pass] != lane) {
-          op.waits[pass].push_back(j);
-          p.ops[j].record[pass] = true;
-        }
+      // waits for ops on other lanes, skipping those already covered by lane
+      // order and earlier waits (latest first: a wait for a later op of a
+      // lane covers its earlier ones); the graph gets no redundant edges
+      std::vector<int> ds = deps[i];
+      std::sort(ds.begin(), ds.end(), [&](int a, int b) { return qpos(a) > qpos(b); });
+      for (int j : ds) {
+        const int m = p.ops[j].lane[pass];
+        if (m == lane || lane_vc[lane][m] >= qpos(j)) continue;
+        op.waits[pass].push_back(j);
+        p.ops[j].record[pass] = true;
+        for (int l = 0; l < NLANES; ++l) lane_vc[lane][l] = std::max(lane_vc[lane][l], vc[j][l]);
+      }
+      lane_vc[lane][lane] = q;
+      vc[i] = lane_vc[lane];
     }
     // recording order: an op is ready once the previous op of its lane (in
     // pass order) and the ops it waits for are placed; among ready ops take

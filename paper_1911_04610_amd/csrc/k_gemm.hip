@@ -248,20 +248,35 @@ XP_DEV void conv_epilogue_bf16(const ConvArgs& a, float* ot, int tid, int m0, in
           s0[r & 3] += sv;
           s1[r & 3] += sv * sv;
         }
-      } else if (n0 + col < a.N) {
+      } else {
+        // the batch norm this column belongs to (selected with constant
+        // indices: no dynamic indexing of the argument arrays)
         const int n = n0 + col, mr = m0 + part * RROWS;
-        const double mu = a.bn_mean[n], rs = a.bn_rstd[n];
-        const bf16_t* zc = (const bf16_t*)a.bn_z + n;
-        // every load issued before the first use: rows past the last are
-        // read at the last row (their g is 0)
-        float zv[RROWS];
+        const bf16_t* zc = nullptr;
+        const double *mp = nullptr, *rp = nullptr;
+        int ldz = 0;
 #pragma unroll
-        for (int r = 0; r < RROWS; ++r) zv[r] = bf16_to_f32(zc[(size_t)min(mr + r, M - 1) * a.ld_bnz]);
+        for (int q = 0; q < CONV_BN_SEGS; ++q)
+          if (q < a.bn_nseg && n >= a.bn_c0[q] && n < a.bn_c1[q]) {
+            const int lc = n - a.bn_c0[q];
+            zc = (const bf16_t*)a.bn_z[q] + lc;
+            ldz = a.ld_bnz[q];
+            mp = a.bn_mean[q] + lc;
+            rp = a.bn_rstd[q] + lc;
+          }
+        if (zc && n < a.N) {
+          const double mu = *mp, rs = *rp;
+          // every load issued before the first use: rows past the last are
+          // read at the last row (their g is 0)
+          float zv[RROWS];
 #pragma unroll
-        for (int r = 0; r < RROWS; ++r) {
-          const double g = (double)oc[r * OPITCH];  // 0 past the last row
-          s0[r & 3] += g;
-          s1[r & 3] += g * (((double)zv[r] - mu) * rs);
+          for (int r = 0; r < RROWS; ++r) zv[r] = bf16_to_f32(zc[(size_t)min(mr + r, M - 1) * ldz]);
+#pragma unroll
+          for (int r = 0; r < RROWS; ++r) {
+            const double g = (double)oc[r * OPITCH];  // 0 past the last row
+            s0[r & 3] += g;
+            s1[r & 3] += g * (((double)zv[r] - mu) * rs);
+          }
         }
       }
       sred[part][0][col] = (s0[0] + s0[1]) + (s0[2] + s0[3]);

@@ -113,10 +113,12 @@ struct Op {
   int64_t stat_block = -1;     // ... to this workspace block ([2][cout] doubles, then dbeta/dgamma)
   bool stats_fused = false;    // BN: statistics come from the producing GEMM
   int stats_from = -1;         // BN: index of that GEMM op (during planning)
-  // bf16: a BN whose output gradient is written whole by one GEMM's data
-  // gradient takes its backward column sums from that launch's epilogue
-  int bnb_bn = -1;             // GEMM: the BN op it computes them for
-  int bnb_gemm = -1;           // BN: the GEMM op that computes them
+  // bf16: BNs whose output gradients are completed by one GEMM's data
+  // gradient (the last of its input's gradient writers) take their backward
+  // column sums from that launch's epilogue
+  std::vector<std::pair<int, int>> bnb_segs;  // GEMM: (BN op, first input column) each
+  int bnb_gemm = -1;           // BN: the GEMM op that computes them ...
+  int bnb_c0 = 0;              // ... at this input column of it
   int64_t bnb_part_off = -1;   // GEMM: workspace bytes of those per-row-tile partials
   // launch lanes, per pass (0 forward, 1 backward): the lane this op runs on,
   // the ops (same pass) on other lanes it waits for, and whether later ops on
@@ -156,7 +158,7 @@ struct xpipe_stage {
   std::vector<ParamT> params;
   std::vector<Tensor> tensors;  // [0] = stage input
   std::vector<Op> ops;
-  std::vector<int> bnb_nrb;     // per GEMM op with bnb_bn: row tiles of its last data-gradient launch
+  std::vector<int> bnb_nrb;     // per GEMM op with bnb_segs: row tiles of its last data-gradient launch
   int out_tensor = -1;          // stage output tensor (logits for a loss stage)
   bool has_loss = false;
   int classes = 0;
@@ -785,32 +787,40 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     }
   }
 
-  // ---- bf16: BN backward partials from the data-gradient epilogue of the one
-  // GEMM that writes the BN output's gradient (a standalone tensor, read by
-  // that GEMM only, written first and whole by its data gradient)
+  // ---- bf16: BN backward partials from the data-gradient epilogue of the GEMM
+  // that completes the gradient of the BN outputs: a GEMM reading a whole
+  // tensor (standalone or a concat) that is the first of the tensor's
+  // readers, so the last writer of its gradient in the backward; the BNs
+  // (no residual) whose output is that tensor or a member of it take their
+  // partials from the launch, at most CONV_BN_SEGS of them
   if (dtype == DT_BF16) {
-    for (size_t b = 0; b < p.ops.size(); ++b) {
-      Op& bn = p.ops[b];
-      if (bn.kind != OP_BN) continue;
-      const int t = bn.out;
-      if (t <= 0 || t == p.out_tensor || p.tensors[t].owner >= 0) continue;
-      bool owns = false;
-      for (const Tensor& u : p.tensors) owns = owns || u.owner == t;
-      if (owns) continue;
-      int user = -1, users = 0;
-      for (size_t j = 0; j < p.ops.size(); ++j) {
-        const Op& o = p.ops[j];
+    for (size_t j = 0; j < p.ops.size(); ++j) {
+      Op& g = p.ops[j];
+      const int t = g.in;
+      if (g.kind != OP_GEMM || t <= 0 || p.tensors[t].owner >= 0) continue;
+      const Region rt = region_of(p, t);
+      bool first = true;
+      for (size_t k = 0; k < j && first; ++k) {
+        const Op& o = p.ops[k];
         if (o.kind == OP_CONCAT) continue;
-        if (o.in == t || o.in2 == t) {
-          ++users;
-          user = (int)j;
-        }
+        for (int r : {o.in, o.in2})
+          if (r >= 0 && overlap(region_of(p, r), rt)) first = false;
       }
-      if (users != 1) continue;
-      Op& g = p.ops[user];
-      if (g.kind != OP_GEMM || g.in != t || g.in2 == t || g.in_acc) continue;
-      g.bnb_bn = (int)b;
-      bn.bnb_gemm = user;
+      if (!first) continue;
+      std::vector<std::pair<int, int>> segs;
+      for (size_t b = 0; b < p.ops.size(); ++b) {
+        const Op& bn = p.ops[b];
+        if (bn.kind != OP_BN || bn.in2 >= 0 || bn.out == p.out_tensor) continue;
+        const Tensor& u = p.tensors[bn.out];
+        if (bn.out == t) segs.push_back({(int)b, 0});
+        else if (u.owner == t) segs.push_back({(int)b, u.coff});
+      }
+      if (segs.empty() || segs.size() > (size_t)CONV_BN_SEGS) continue;
+      g.bnb_segs = segs;
+      for (auto& sg : segs) {
+        p.ops[sg.first].bnb_gemm = (int)j;
+        p.ops[sg.first].bnb_c0 = sg.second;
+      }
     }
   }
 
@@ -850,7 +860,7 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
         for (int d = 0; d < 2; ++d)
           op.wg_off[d] = take((size_t)op.cout * op.k * op.kw * op.cin * esz);
       if (op.stats) op.stat_block = take((size_t)4 * op.cout * sizeof(double));
-      if (op.bnb_bn >= 0)
+      if (!op.bnb_segs.empty())
         op.bnb_part_off = take((size_t)conv_max_row_tiles((int)tin_.sh.rows()) * 2 * op.cin * sizeof(double));
       int M = (int)p.tensors[op.out].sh.rows();  // output pixels (the input's for stride 1)
       int K = op.k * op.kw * op.cin;
@@ -1348,20 +1358,25 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
             a.Ho = tin.sh.H;
             a.Wo = tin.sh.W;
           }
-          if (op.bnb_bn >= 0) {
-            // the input's batch norm: its backward partials come from here
-            const Op& bn = st->ops[op.bnb_bn];
-            View z = act(st, bn.in, c);
-            const double* bst = (const double*)(st->ws + bn.stat_off);
+          if (!op.bnb_segs.empty()) {
+            // the batch norms whose output gradient this launch completes
             a.bn_part = (double*)(st->ws + op.bnb_part_off);
-            a.bn_z = z.p;
-            a.ld_bnz = z.ld;
-            a.bn_mean = bst;
-            a.bn_rstd = bst + bn.stat_ld;
+            a.bn_nseg = (int)op.bnb_segs.size();
+            for (int k = 0; k < a.bn_nseg; ++k) {
+              const Op& bn = st->ops[op.bnb_segs[k].first];
+              View z = act(st, bn.in, c);
+              const double* bst = (const double*)(st->ws + bn.stat_off);
+              a.bn_c0[k] = op.bnb_segs[k].second;
+              a.bn_c1[k] = a.bn_c0[k] + st->tensors[bn.in].sh.C;
+              a.bn_z[k] = z.p;
+              a.ld_bnz[k] = z.ld;
+              a.bn_mean[k] = bst;
+              a.bn_rstd[k] = bst + bn.stat_ld;
+            }
           }
           int rows_tiles = 0;
           XP_HIP(launch_conv_gemm(dt, a, s, &rows_tiles));
-          if (op.bnb_bn >= 0) st->bnb_nrb[i] = rows_tiles;
+          if (!op.bnb_segs.empty()) st->bnb_nrb[i] = rows_tiles;
         }
         // the ops that wait for this one need only the input gradient (the
         // weight gradient is joined at the end of the pass): they are released
@@ -1442,8 +1457,9 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         ca.grad1 = st->grad + op.be_off;
         if (op.bnb_gemm >= 0) {
           // partials from the data-gradient epilogue that wrote g
-          ca.partial = (double*)(st->ws + st->ops[op.bnb_gemm].bnb_part_off);
           ca.row_blocks = st->bnb_nrb[op.bnb_gemm];
+          ca.partial = (double*)(st->ws + st->ops[op.bnb_gemm].bnb_part_off) +
+                       (size_t)op.bnb_c0 * 2 * ca.row_blocks;
           XP_HIP(launch_colfinal(ca, s));
         } else {
           XP_HIP(launch_colreduce(dt, ca, s));

@@ -79,6 +79,7 @@ hipError_t launch_gather(int dtype, const GatherArgs& a, hipStream_t s);
 // w[n][r][s][c] + bias[n]) over an nb x H x W image batch (stride 1, zero padding).
 // Serves conv forward, linear forward (H = W = R = S = 1) and the data gradient
 // (x = output gradient, w = flipped / transposed weights).
+constexpr int CONV_BN_SEGS = 4;
 struct ConvArgs {
   const void* x;
   int ldx;
@@ -93,15 +94,19 @@ struct ConvArgs {
   int accumulate;       // y = y + result (after mask)
   double* stat_part;    // optional: per row tile, column sums of the stored y and of its
                         // squares, at stat_part[(n * 2 + {0,1}) * row_tiles + tile]
-  // optional (bf16): the stored y is the output gradient g of a batch norm
-  // whose input is z (view bn_z, ld_bnz) with batch mean / rstd bn_mean /
-  // bn_rstd; per row tile, the column sums of g and of g (z - mean) rstd, at
-  // bn_part[(n * 2 + {0,1}) * row_tiles + tile] (the BN backward's partials)
+  // optional (bf16): columns [bn_c0[k], bn_c1[k]) of the stored y are the
+  // output gradient g of batch norm k (k < bn_nseg), whose input is z (view
+  // bn_z[k], ld_bnz[k]) with batch mean / rstd bn_mean[k] / bn_rstd[k] (all
+  // three from the norm's first column on); per row tile, the column sums of
+  // g and of g (z - mean) rstd, at bn_part[(n * 2 + {0,1}) * row_tiles + tile]
+  // (the BN backward's partials; columns outside every range get zeros)
   double* bn_part;
-  const void* bn_z;
-  int ld_bnz;
-  const double* bn_mean;
-  const double* bn_rstd;
+  int bn_nseg;
+  int bn_c0[CONV_BN_SEGS], bn_c1[CONV_BN_SEGS];
+  const void* bn_z[CONV_BN_SEGS];
+  int ld_bnz[CONV_BN_SEGS];
+  const double* bn_mean[CONV_BN_SEGS];
+  const double* bn_rstd[CONV_BN_SEGS];
   // general grid (Ho > 0: strided, or unpadded): the rows are an Ho x Wo grid
   // per image, stride >= 1.
   // tr = 0: forward, row (ho, wo) reads x at (ho*stride + r - pad, wo*stride + q - padw);

@@ -467,7 +467,26 @@ def measured_peaks():
     ms = timed(lambda: xp.xpipe_probe_mfma(out, iters))
     tflops = waves * iters * 8 * 32768.0 / (ms / 1e3) / 1e12
     return {"hbm_copy_GB_s": round(copy_gbs, 1), "mfma_bf16_TFLOP_s": round(tflops, 1),
-            "copy_bytes": 2 * n, "mfma": "v_mfma_f32_32x32x16_bf16, %d waves x %d x 8" % (waves, iters)}
+            "copy_bytes": 2 * n, "mfma": "v_mfma_f32_32x32x16_bf16, %d waves x %d x 8" % (waves, iters),
+            "graph_fork_join": graph_costs()}
+
+
+def graph_costs():
+    """What the launch lanes cost inside a recorded graph: microseconds per
+    diamond (one launch, `width` branches of `len` launches on other streams,
+    joined back) against the same launches as one chain, for empty launches
+    and for launches of about 28 us (256 workgroups, 2000 dependent FMAs per
+    thread)."""
+    import torch
+    import paper_1911_04610_amd as xp
+    scratch = torch.zeros(2048, dtype=torch.float32, device="cuda")
+    res = []
+    for spin in (0, 2000):
+        for width, length in ((1, 1), (2, 1), (3, 1), (2, 3)):
+            par, ser = xp.xpipe_probe_graph(scratch, width, length, 40, spin)
+            res.append({"spin": spin, "width": width, "len": length, "launches": 1 + width * length,
+                        "branches_us": round(par, 2), "chain_us": round(ser, 2)})
+    return res
 
 
 def vendor_reference(off_us, reps=50):

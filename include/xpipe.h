@@ -415,6 +415,21 @@ xpipe_status xpipe_probe_stream(const float* const* src, int32_t nsrc, float* co
 
 xpipe_status xpipe_probe_mfma(float* out, int32_t waves, int32_t iters, void* hip_stream);
 
+/* xpipe_probe_graph: what a fork/join costs inside a recorded HIP graph, the
+ * structure the stage's launch lanes become.  Two graphs are recorded and
+ * each replayed 2 + 5 times on hip_stream (the last 5 timed): `reps` diamonds
+ * of (one launch, then `width` branches on separate streams of `len`
+ * launches each, joined back), and the same launches as one chain.  Every
+ * launch is 256 workgroups of 256 threads doing `spin` dependent fp32
+ * multiply-adds (0: an empty launch).  scratch: device memory of at least
+ * 2048 floats (read and written).  us_out (host, 2 doubles): microseconds per
+ * diamond with branches, then as one chain.  1 <= width <= 3, 1 <= len <= 8,
+ * 1 <= reps <= 256, spin >= 0; creates and destroys its own streams (default
+ * priority), events and graphs, runs after the work already enqueued on
+ * hip_stream and returns when its own work has finished. */
+xpipe_status xpipe_probe_graph(float* scratch, int32_t width, int32_t len, int32_t reps, int32_t spin,
+                               double* us_out, void* hip_stream);
+
 /* Message for the last non-OK status returned on the calling thread. */
 const char* xpipe_last_error(void);
 

@@ -127,6 +127,7 @@ _SIGS = {
                         _P],
     "xpipe_probe_copy": [_P, _P, _I64, _P],
     "xpipe_probe_mfma": [_P, _I32, _I32, _P],
+    "xpipe_probe_graph": [_P, _I32, _I32, _I32, _I32, ctypes.POINTER(ctypes.c_double), _P],
     "xpipe_probe_stream": [ctypes.POINTER(_P), _I32, ctypes.POINTER(_P), _I32, _I64, _P],
     "xpipe_stage_set_timing": [_P, _I32],
     "xpipe_stage_set_graphs": [_P, _I32],
@@ -407,6 +408,18 @@ def xpipe_probe_copy(src, dst, stream=None):
 def xpipe_probe_mfma(out, iters: int, stream=None):
     """One wave per element of the float32 tensor `out`, `iters` rounds of 8 MFMAs each."""
     _check(lib().xpipe_probe_mfma(_ptr(out), out.numel(), int(iters), _stream_ptr(stream)))
+
+
+def xpipe_probe_graph(scratch, width: int, length: int, reps: int, spin: int, stream=None):
+    """Recorded-graph fork/join probe: (us per diamond with `width` branches of
+    `length` launches, us for the same launches as one chain).  scratch: a
+    float32 device tensor of at least 2048 elements."""
+    if scratch.numel() < 2048:
+        raise ValueError("scratch needs at least 2048 floats")
+    out = (ctypes.c_double * 2)()
+    _check(lib().xpipe_probe_graph(_ptr(scratch), int(width), int(length), int(reps), int(spin),
+                                   out, _stream_ptr(stream)))
+    return out[0], out[1]
 
 
 def xpipe_probe_stream(srcs, dsts, stream=None):

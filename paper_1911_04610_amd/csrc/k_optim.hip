@@ -419,6 +419,19 @@ hipError_t launch_probe_stream(const StreamArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// graph probe: a fixed amount of dependent fp32 work per thread (iters
+// multiply-adds on one value), one float written per launch so it is kept
+__global__ __launch_bounds__(256) void k_probe_spin(float* p, int i, int iters) {
+  float v = p[i & 1023];
+  for (int k = 0; k < iters; ++k) v = v * 0.999f + 1.0f;
+  if (threadIdx.x == 0 && blockIdx.x == 0) p[1024 + (i & 1023)] = v;
+}
+
+hipError_t launch_probe_spin(float* p, int i, int iters, int blocks, hipStream_t s) {
+  XP_LAUNCH("k_probe_spin", 0.0, k_probe_spin, dim3(blocks), dim3(256), 0, s, p, i, iters);
+  return hipGetLastError();
+}
+
 hipError_t launch_probe_mfma(float* out, int waves, int iters, hipStream_t s) {
   if (waves <= 0 || iters <= 0) return hipSuccess;
   XP_LAUNCH("k_probe_mfma", (double)waves * iters * 8 * 32768.0, k_probe_mfma,

@@ -2243,6 +2243,88 @@ xpipe_status xpipe_probe_mfma(float* out, int32_t waves, int32_t iters, void* hi
   return XPIPE_OK;
 }
 
+xpipe_status xpipe_probe_graph(float* scratch, int32_t width, int32_t len, int32_t reps, int32_t spin,
+                               double* us_out, void* hip_stream) {
+  if (!scratch || !us_out) return fail(XPIPE_EINVAL, "null pointer");
+  if (width < 1 || width > 3 || len < 1 || len > 8 || reps < 1 || reps > 256 || spin < 0)
+    return fail(XPIPE_EINVAL, "probe sizes out of range");
+  // recorded and replayed on a stream of its own (a capture cannot use the
+  // null stream), after the work already on hip_stream; returns when done
+  hipStream_t s0 = nullptr;
+  hipStream_t side[3] = {nullptr, nullptr, nullptr};
+  std::vector<hipEvent_t> evs;
+  hipGraph_t g = nullptr;
+  hipGraphExec_t ge = nullptr;
+  hipEvent_t t0 = nullptr, t1 = nullptr;
+  hipError_t e = hipSuccess;
+  auto ev = [&](hipEvent_t* out) {
+    e = hipEventCreateWithFlags(out, hipEventDisableTiming);
+    if (e == hipSuccess) evs.push_back(*out);
+    return e;
+  };
+  // one recorded graph per layout; the stream work happens while capturing
+  auto record = [&](bool branches) -> hipError_t {
+    hipError_t r = hipStreamBeginCapture(s0, hipStreamCaptureModeThreadLocal);
+    if (r != hipSuccess) return r;
+    int k = 0;
+    for (int q = 0; q < reps && r == hipSuccess; ++q) {
+      r = launch_probe_spin(scratch, k++, spin, 256, s0);
+      if (r != hipSuccess || !branches) {
+        for (int b = 0; b < width * len && r == hipSuccess; ++b) r = launch_probe_spin(scratch, k++, spin, 256, s0);
+        continue;
+      }
+      hipEvent_t f;
+      if ((r = ev(&f)) != hipSuccess || (r = hipEventRecord(f, s0)) != hipSuccess) break;
+      for (int b = 0; b < width && r == hipSuccess; ++b) {
+        if ((r = hipStreamWaitEvent(side[b], f, 0)) != hipSuccess) break;
+        for (int l = 0; l < len && r == hipSuccess; ++l) r = launch_probe_spin(scratch, k++, spin, 256, side[b]);
+        hipEvent_t j;
+        if (r != hipSuccess || (r = ev(&j)) != hipSuccess || (r = hipEventRecord(j, side[b])) != hipSuccess) break;
+        r = hipStreamWaitEvent(s0, j, 0);
+      }
+    }
+    hipGraph_t gg = nullptr;
+    hipError_t r2 = hipStreamEndCapture(s0, &gg);
+    if (r == hipSuccess) r = r2;
+    if (r == hipSuccess) g = gg;
+    else if (gg) hipGraphDestroy(gg);
+    return r;
+  };
+  for (int b = 0; b < width && e == hipSuccess; ++b) e = hipStreamCreateWithFlags(&side[b], hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&s0, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreate(&t0);
+  if (e == hipSuccess) e = hipEventCreate(&t1);
+  if (e == hipSuccess) e = hipEventRecord(t0, (hipStream_t)hip_stream);
+  if (e == hipSuccess) e = hipStreamWaitEvent(s0, t0, 0);
+  for (int layout = 0; layout < 2 && e == hipSuccess; ++layout) {
+    e = record(layout == 0);
+    if (e == hipSuccess) e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+    for (int w = 0; w < 2 && e == hipSuccess; ++w) e = hipGraphLaunch(ge, s0);
+    if (e == hipSuccess) e = hipEventRecord(t0, s0);
+    for (int w = 0; w < 5 && e == hipSuccess; ++w) e = hipGraphLaunch(ge, s0);
+    if (e == hipSuccess) e = hipEventRecord(t1, s0);
+    if (e == hipSuccess) e = hipEventSynchronize(t1);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, t0, t1);
+    if (e == hipSuccess) us_out[layout] = (double)ms * 1e3 / 5.0 / reps;
+    if (ge) hipGraphExecDestroy(ge);
+    if (g) hipGraphDestroy(g);
+    ge = nullptr;
+    g = nullptr;
+  }
+  for (hipEvent_t x : evs) hipEventDestroy(x);
+  if (t0) hipEventDestroy(t0);
+  if (t1) hipEventDestroy(t1);
+  if (s0) {
+    hipStreamSynchronize(s0);
+    hipStreamDestroy(s0);
+  }
+  for (int b = 0; b < 3; ++b)
+    if (side[b]) hipStreamDestroy(side[b]);
+  if (e != hipSuccess) return fail(XPIPE_EHIP, std::string("graph probe: ") + hipGetErrorString(e));
+  return XPIPE_OK;
+}
+
 xpipe_status xpipe_stage_set_timing(xpipe_stage_t st, int32_t enable) {
   if (!st) return fail(XPIPE_EINVAL, "null stage");
   st->timing = enable != 0;

@@ -262,6 +262,7 @@ hipError_t launch_softmax_ce(int dtype, const CeArgs& a, hipStream_t s);
 // ---------------------------------------------------------------- measurement probes
 hipError_t launch_probe_copy(const void* src, void* dst, int64_t bytes, hipStream_t s);
 hipError_t launch_probe_mfma(float* out, int waves, int iters, hipStream_t s);
+hipError_t launch_probe_spin(float* p, int i, int iters, int blocks, hipStream_t s);
 // measurement probe: n 16-byte vectors read from each of nsrc buffers and
 // written to each of ndst buffers
 constexpr int STREAM_MAX_SRC = 4, STREAM_MAX_DST = 6;

@@ -143,6 +143,13 @@ def test_flat_entry_points_check_arguments_on_the_host():
     assert L.xpipe_probe_stream(src, 1, dst, 1, 0, None) == xp.OK           # nothing to do
     mis = (P * 1)(20)
     assert L.xpipe_probe_stream(mis, 1, dst, 1, 16, None) == xp.EINVAL      # misaligned source
+    # the graph probe: sizes are checked before anything is created
+    us = (ctypes.c_double * 2)()
+    for width, length, reps, spin in ((0, 1, 1, 0), (4, 1, 1, 0), (1, 0, 1, 0), (1, 9, 1, 0),
+                                      (1, 1, 0, 0), (1, 1, 257, 0), (1, 1, 1, -1)):
+        assert L.xpipe_probe_graph(16, width, length, reps, spin, us, None) == xp.EINVAL
+    assert L.xpipe_probe_graph(None, 1, 1, 1, 0, us, None) == xp.EINVAL
+    assert L.xpipe_probe_graph(16, 1, 1, 1, 0, None, None) == xp.EINVAL
 
 
 @pytest.mark.parametrize("rounding", [0, 2])

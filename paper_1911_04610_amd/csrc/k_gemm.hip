@@ -89,16 +89,6 @@ XP_DEV void static_for(F&& f) {
   }
 }
 
-// Workgroups are dispatched to the 8 XCDs (each with its own L2) round-robin
-// by linear id.  Remap the linear id so that each XCD takes a contiguous run
-// of the logical tile order: neighbouring tiles (shared input rows, shared
-// pixel splits) then meet in one L2.  A bijection of [0, G).
-constexpr int XP_XCDS = 8;
-XP_DEV int xcd_tile(int l, int G) {
-  const int x = l % XP_XCDS, q = l / XP_XCDS;
-  const int per = G / XP_XCDS, rem = G % XP_XCDS;
-  return x * per + (x < rem ? x : rem) + q;
-}
 
 // bf16 epilogue from the fp32 result tile staged in LDS (ot, BM rows of
 // OPITCH floats; every thread of the workgroup takes part): each thread

@@ -120,6 +120,13 @@ struct Op {
   int bnb_gemm = -1;           // BN: the GEMM op that computes them ...
   int bnb_c0 = 0;              // ... at this input column of it
   int64_t bnb_part_off = -1;   // GEMM: workspace bytes of those per-row-tile partials
+  // bf16: a 1x1 convolution whose input is a 3x3 average pool (padding
+  // counted) takes the pool's backward: its output gradient is box-averaged
+  // first (the pool is self-adjoint and commutes with the 1x1 contraction),
+  // and its data gradient writes the pool input's gradient directly
+  int pool_bwd = -1;           // GEMM: the average-pool op
+  int pool_by = -1;            // AVGPOOL: the GEMM op that takes its backward
+  int64_t box_off = -1;        // GEMM: workspace bytes of the averaged output gradient
   // launch lanes, per pass (0 forward, 1 backward): the lane this op runs on,
   // the ops (same pass) on other lanes it waits for, and whether later ops on
   // other lanes wait for it
@@ -824,6 +831,36 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     }
   }
 
+  // ---- bf16: average pool -> 1x1 convolution, backward reordered (the
+  // averaging runs on the convolution's cout channels instead of its cin)
+  if (dtype == DT_BF16) {
+    for (size_t a = 0; a < p.ops.size(); ++a) {
+      Op& ap = p.ops[a];
+      if (ap.kind != OP_AVGPOOL) continue;
+      const int t = ap.out;
+      if (t <= 0 || t == p.out_tensor || p.tensors[t].owner >= 0 || p.tensors[t].masked) continue;
+      bool owns = false;
+      for (const Tensor& u : p.tensors) owns = owns || u.owner == t;
+      if (owns) continue;
+      int user = -1, users = 0;
+      for (size_t j = 0; j < p.ops.size(); ++j) {
+        const Op& o = p.ops[j];
+        if (o.kind == OP_CONCAT) continue;
+        if (o.in == t || o.in2 == t) {
+          ++users;
+          user = (int)j;
+        }
+      }
+      if (users != 1) continue;
+      Op& g = p.ops[user];
+      if (g.kind != OP_GEMM || g.in != t || g.in2 >= 0 || g.k != 1 || g.kw != 1 || g.grid ||
+          !g.segs.empty() || !g.bnb_segs.empty())
+        continue;
+      g.pool_bwd = (int)a;
+      ap.pool_by = user;
+    }
+  }
+
   // ---- launch lanes
   plan_lanes(p);
   if (const char* tr = std::getenv("XPIPE_TRACE_PLAN"); tr && *tr == '1') {
@@ -860,6 +897,8 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
         for (int d = 0; d < 2; ++d)
           op.wg_off[d] = take((size_t)op.cout * op.k * op.kw * op.cin * esz);
       if (op.stats) op.stat_block = take((size_t)4 * op.cout * sizeof(double));
+      if (op.pool_bwd >= 0)
+        op.box_off = take((size_t)p.tensors[op.out].sh.rows() * op.cout * esz);
       if (!op.bnb_segs.empty())
         op.bnb_part_off = take((size_t)conv_max_row_tiles((int)tin_.sh.rows()) * 2 * op.cin * sizeof(double));
       int M = (int)p.tensors[op.out].sh.rows();  // output pixels (the input's for stride 1)
@@ -1329,15 +1368,33 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         const Tensor& tout = st->tensors[op.out];
         const int M = (int)tout.sh.rows();  // output pixels
         const int K = op.k * op.kw * op.cin;
-        if (want_grad(op.in)) {
-          View dx = gradv(st, op.in, c);
+        const Op* pool = op.pool_bwd >= 0 ? &st->ops[op.pool_bwd] : nullptr;
+        if (pool ? want_grad(pool->in) : want_grad(op.in)) {
+          View dx = gradv(st, pool ? pool->in : op.in, c);
           ConvArgs a{};
           a.x = g.p;
           a.ldx = g.ld;
           a.w = st->ws + op.wd_off;
           a.y = dx.p;
           a.ldy = dx.ld;
-          mask_of(op.in, a.mask, a.ldm);
+          mask_of(pool ? pool->in : op.in, a.mask, a.ldm);
+          if (pool) {
+            // the average pool's backward: average the output gradient over
+            // 3x3 windows (cout channels), then the 1x1 data gradient writes
+            // the pool input's gradient with the pool's mask and accumulation
+            PoolArgs pa{};
+            pa.x = g.p;
+            pa.ldx = g.ld;
+            pa.out = st->ws + op.box_off;
+            pa.ldo = op.cout;
+            pa.nb = tout.sh.n;
+            pa.H = tout.sh.H;
+            pa.W = tout.sh.W;
+            pa.C = op.cout;
+            XP_HIP(launch_avgpool_fwd(dt, pa, s));
+            a.x = st->ws + op.box_off;
+            a.ldx = op.cout;
+          }
           a.nb = tin.sh.n;
           a.H = tin.sh.H;
           a.W = tin.sh.W;
@@ -1347,7 +1404,7 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
           a.S = op.kw;
           a.pad = op.ph;
           a.padw = op.pw;
-          a.accumulate = op.in_acc;
+          a.accumulate = pool ? pool->in_acc : op.in_acc;
           if (op.grid) {
             // rows: the input grid; gathered from the output gradient's grid,
             // with the transposed (unflipped) weights
@@ -1534,7 +1591,7 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
       case OP_MAXPOOL3:
       case OP_AVGPOOL:
       case OP_GAP: {
-        if (!want_grad(op.in)) break;
+        if (!want_grad(op.in) || op.pool_by >= 0) break;  // (or taken by its 1x1 convolution)
         View g = gradv(st, op.out, c);
         View d = gradv(st, op.in, c);
         PoolArgs pa{};

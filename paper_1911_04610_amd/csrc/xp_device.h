@@ -12,6 +12,17 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------- bf16
+// Workgroups are dispatched to the 8 XCDs (each with its own L2) round-robin
+// by linear id.  Remap the linear id so that each XCD takes a contiguous run
+// of the logical tile order: neighbouring tiles (shared input rows, shared
+// pixel splits) then meet in one L2.  A bijection of [0, G).
+constexpr int XP_XCDS = 8;
+XP_DEV int xcd_tile(int l, int G) {
+  const int x = l % XP_XCDS, q = l / XP_XCDS;
+  const int per = G / XP_XCDS, rem = G % XP_XCDS;
+  return x * per + (x < rem ? x : rem) + q;
+}
+
 XP_DEV float bf16_to_f32(bf16_t u) { return __uint_as_float((uint32_t)u << 16); }
 
 // fp32 -> bf16, round to nearest, ties to even (the gfx950 conversion

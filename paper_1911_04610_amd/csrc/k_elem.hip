@@ -1302,6 +1302,124 @@ __global__ __launch_bounds__(256) void k_gap_bwd_v(PoolArgs a) {
   }
 }
 
+// GAP backward with batch-norm backward partials: blocks of CL chunk-lanes x
+// RG row groups over a row block, as the column partials are laid out; each
+// thread forms g = dy / (H W) for its chunk's rows (masked, added to the
+// stored value when accumulating), stores it, and adds the stored values and
+// their products with (z - mean) rstd; the row groups are then added in a
+// fixed pairwise tree
+template <typename T>
+__global__ __launch_bounds__(256) void k_gap_bwd_bn_v(PoolArgs a, GapBnArgs b, int row_blocks) {
+  constexpr int N = VT<T>::N;
+  __shared__ double sh[2][256][N];
+  const int chunks = a.C / N;
+  const int CL = chunks < 256 ? chunks : 256;
+  const int RG = 256 / CL;
+  const int cl = threadIdx.x % CL, g = threadIdx.x / CL;
+  const int chunk = blockIdx.x * CL + cl;
+  const int HW = a.H * a.W, M = a.nb * HW;
+  const int per = ceil_div(M, row_blocks);
+  const int r0 = blockIdx.y * per, r1 = min(M, r0 + per);
+  double s0[N], s1[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) s0[e] = s1[e] = 0.0;
+  if (g < RG && chunk < chunks) {
+    const int c0 = chunk * N;
+    // this chunk's norm (selected with constant indices)
+    const T* Z = nullptr;
+    int ldz = 0;
+    const double *mp = nullptr, *rp = nullptr;
+#pragma unroll
+    for (int q = 0; q < CONV_BN_SEGS; ++q)
+      if (q < b.bn_nseg && c0 >= b.bn_c0[q] && c0 < b.bn_c1[q]) {
+        const int lc = c0 - b.bn_c0[q];
+        Z = (const T*)b.bn_z[q] + lc;
+        ldz = b.ld_bnz[q];
+        mp = b.bn_mean[q] + lc;
+        rp = b.bn_rstd[q] + lc;
+      }
+    double mu[N], rs[N];
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+      mu[e] = Z ? mp[e] : 0.0;
+      rs[e] = Z ? rp[e] : 0.0;
+    }
+    const T* DY = (const T*)a.dy;
+    const T* MK = (const T*)a.mask;
+    T* O = (T*)a.out;
+    constexpr int U = 4;
+    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+    for (int rb = r0 + g; rb < r1; rb += U * RG) {
+      uint4 dv[U], mv[U], ov[U], zv[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int r = rb + u * RG;
+        dv[u] = mv[u] = ov[u] = zv[u] = zero;
+        if (r < r1) {
+          dv[u] = ld16(DY + (size_t)(r / HW) * a.lddy + c0);
+          if (MK) mv[u] = ld16(MK + (size_t)r * a.ldm + c0);
+          if (a.accumulate) ov[u] = ld16(O + (size_t)r * a.ldo + c0);
+          if (Z) zv[u] = ld16(Z + (size_t)r * ldz);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int r = rb + u * RG;
+        if (r >= r1) break;
+        double d[N];
+        cvt16<T>(dv[u], d);
+#pragma unroll
+        for (int e = 0; e < N; ++e) d[e] = d[e] / HW;
+        if (MK) vmask_raw<T>(mv[u], d);
+        if (a.accumulate) {
+          double o[N];
+          cvt16<T>(ov[u], o);
+#pragma unroll
+          for (int e = 0; e < N; ++e) d[e] += o[e];
+        }
+        const uint4 st = pack16<T>(d);
+        *reinterpret_cast<uint4*>(O + (size_t)r * a.ldo + c0) = st;
+        if (Z) {
+          double v[N], z[N];
+          cvt16<T>(st, v);  // the stored values
+          cvt16<T>(zv[u], z);
+#pragma unroll
+          for (int e = 0; e < N; ++e) {
+            s0[e] += v[e];
+            s1[e] += v[e] * ((z[e] - mu[e]) * rs[e]);
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < N; ++e) {
+    sh[0][threadIdx.x][e] = s0[e];
+    sh[1][threadIdx.x][e] = s1[e];
+  }
+  int half = 1;
+  while (2 * half < RG) half *= 2;
+  for (; half >= 1; half >>= 1) {
+    __syncthreads();
+    if (g < half && g + half < RG) {
+      const int o = (g + half) * CL + cl;
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        sh[0][threadIdx.x][e] += sh[0][o][e];
+        sh[1][threadIdx.x][e] += sh[1][o][e];
+      }
+    }
+  }
+  if (g == 0 && chunk < chunks) {
+    const int c0 = chunk * N;
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+      b.part[((size_t)(c0 + e) * 2 + 0) * row_blocks + blockIdx.y] = sh[0][cl][e];
+      b.part[((size_t)(c0 + e) * 2 + 1) * row_blocks + blockIdx.y] = sh[1][cl][e];
+    }
+  }
+}
+
 // ---------------------------------------------------------------- softmax cross-entropy
 // One workgroup; wave w handles rows w, w + 16, ...  Row losses go to LDS and
 // one thread adds them in row order.
@@ -1515,6 +1633,32 @@ hipError_t launch_gap_fwd(int dtype, const PoolArgs& a, hipStream_t s) {
     return hipGetLastError();
   }
   return launch_gap_fwd_s(dtype, a, s);
+}
+
+int gap_bn_max_row_blocks() { return COL_MAX_ROW_BLOCKS_V; }
+
+hipError_t launch_gap_bwd_bn(int dtype, const PoolArgs& a, const GapBnArgs& b, hipStream_t s,
+                             int* row_blocks) {
+  if (row_blocks) *row_blocks = 0;
+  const int64_t rows = (int64_t)a.nb * a.H * a.W;
+  if (rows <= 0 || a.C <= 0) return hipSuccess;
+  const int N = vn(dtype);
+  bool ok = b.part && b.bn_nseg >= 1 && b.bn_nseg <= CONV_BN_SEGS &&
+            vec_dt(dtype, rows, a.C, {{a.dy, a.lddy}, {a.mask, a.ldm}, {a.out, a.ldo}});
+  for (int k = 0; ok && k < b.bn_nseg; ++k)
+    ok = b.bn_c0[k] % N == 0 && b.bn_c1[k] % N == 0 && b.bn_c0[k] < b.bn_c1[k] && b.bn_c1[k] <= a.C &&
+         vec_dt(dtype, rows, a.C, {{b.bn_z[k], b.ld_bnz[k]}});
+  if (!ok) return hipErrorInvalidValue;
+  const int rb = col_row_blocks_v((int)rows, a.C, N);
+  const int chunks = a.C / N, CL = chunks < 256 ? chunks : 256;
+  const dim3 grid(ceil_div(chunks, CL), rb);
+  const double bytes = (double)rows * a.C * (dtype == DT_BF16 ? 2 : 4) * (2 + (a.mask ? 1 : 0) + (a.accumulate ? 1 : 0));
+  if (dtype == DT_BF16)
+    XP_LAUNCH("k_gap_bwd_bn_v<bf16>", bytes, k_gap_bwd_bn_v<bf16_t>, grid, dim3(256), 0, s, a, b, rb);
+  else
+    XP_LAUNCH("k_gap_bwd_bn_v<f32>", bytes, k_gap_bwd_bn_v<float>, grid, dim3(256), 0, s, a, b, rb);
+  if (row_blocks) *row_blocks = rb;
+  return hipGetLastError();
 }
 
 hipError_t launch_gap_bwd(int dtype, const PoolArgs& a, hipStream_t s) {

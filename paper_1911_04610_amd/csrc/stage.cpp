@@ -804,7 +804,10 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     for (size_t j = 0; j < p.ops.size(); ++j) {
       Op& g = p.ops[j];
       const int t = g.in;
-      if (g.kind != OP_GEMM || t <= 0 || p.tensors[t].owner >= 0) continue;
+      // a GEMM's data gradient, or a global average pool's backward (the
+      // classifier head's), can take the partials
+      if ((g.kind != OP_GEMM && g.kind != OP_GAP) || t <= 0 || p.tensors[t].owner >= 0) continue;
+      if (g.kind == OP_GAP && p.tensors[t].sh.C % 8 != 0) continue;
       const Region rt = region_of(p, t);
       bool first = true;
       for (size_t k = 0; k < j && first; ++k) {
@@ -819,6 +822,7 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
         const Op& bn = p.ops[b];
         if (bn.kind != OP_BN || bn.in2 >= 0 || bn.out == p.out_tensor) continue;
         const Tensor& u = p.tensors[bn.out];
+        if (g.kind == OP_GAP && (u.coff % 8 != 0 || u.sh.C % 8 != 0)) continue;
         if (bn.out == t) segs.push_back({(int)b, 0});
         else if (u.owner == t) segs.push_back({(int)b, u.coff});
       }
@@ -921,6 +925,8 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
       colpart = std::max(colpart, col_partial_bytes((int)tin_.sh.rows(), tin_.sh.C));
     } else if (op.kind == OP_GAP) {
       colpart = std::max(colpart, gap_partial_bytes(tin_.sh.n, tin_.sh.H, tin_.sh.W, tin_.sh.C));
+      if (!op.bnb_segs.empty())
+        op.bnb_part_off = take((size_t)gap_bn_max_row_blocks() * 2 * tin_.sh.C * sizeof(double));
     } else if (op.kind == OP_MAXPOOL3) {
       op.idx_off = take((size_t)p.tensors[op.out].sh.elems());
     }
@@ -1617,7 +1623,28 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
         if (op.kind == OP_MAXPOOL) XP_HIP(launch_maxpool_bwd(dt, pa, s));
         else if (op.kind == OP_MAXPOOL3) XP_HIP(launch_maxpool3s2_bwd(dt, pa, s));
         else if (op.kind == OP_AVGPOOL) XP_HIP(launch_avgpool_bwd(dt, pa, s));
-        else XP_HIP(launch_gap_bwd(dt, pa, s));
+        else if (op.bnb_segs.empty()) XP_HIP(launch_gap_bwd(dt, pa, s));
+        else {
+          // with the backward partials of the batch norms whose output
+          // gradient this completes
+          GapBnArgs gb{};
+          gb.part = (double*)(st->ws + op.bnb_part_off);
+          gb.bn_nseg = (int)op.bnb_segs.size();
+          for (int k = 0; k < gb.bn_nseg; ++k) {
+            const Op& bn = st->ops[op.bnb_segs[k].first];
+            View z = act(st, bn.in, c);
+            const double* bst = (const double*)(st->ws + bn.stat_off);
+            gb.bn_c0[k] = op.bnb_segs[k].second;
+            gb.bn_c1[k] = gb.bn_c0[k] + st->tensors[bn.in].sh.C;
+            gb.bn_z[k] = z.p;
+            gb.ld_bnz[k] = z.ld;
+            gb.bn_mean[k] = bst;
+            gb.bn_rstd[k] = bst + bn.stat_ld;
+          }
+          int rb = 0;
+          XP_HIP(launch_gap_bwd_bn(dt, pa, gb, s, &rb));
+          st->bnb_nrb[i] = rb;
+        }
         break;
       }
       case OP_CONCAT:

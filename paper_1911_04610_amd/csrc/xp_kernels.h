@@ -248,6 +248,28 @@ hipError_t launch_avgpool_fwd(int dtype, const PoolArgs& a, hipStream_t s);
 hipError_t launch_avgpool_bwd(int dtype, const PoolArgs& a, hipStream_t s);
 hipError_t launch_gap_fwd(int dtype, const PoolArgs& a, hipStream_t s);
 hipError_t launch_gap_bwd(int dtype, const PoolArgs& a, hipStream_t s);
+// GAP backward (a's dy, mask, out, accumulate, shape) that also takes the
+// batch-norm backward partials of the norms whose output gradient it
+// completes: columns [bn_c0[k], bn_c1[k]) belong to norm k (k < bn_nseg, each
+// boundary a multiple of the 16-byte chunk), whose input is z (view bn_z[k],
+// ld_bnz[k]) with mean / rstd bn_mean[k] / bn_rstd[k], all from the norm's
+// first column on.  Per row block, the column sums of the stored gradient g
+// and of g (z - mean) rstd go to part[(c * 2 + {0,1}) * row_blocks + block]
+// (zeros outside the norms' columns); *row_blocks receives the block count
+// (at most gap_bn_max_row_blocks()).  Vector path only: hipErrorInvalidValue
+// when the views are not 16-byte aligned.
+struct GapBnArgs {
+  double* part;
+  int bn_nseg;
+  int bn_c0[CONV_BN_SEGS], bn_c1[CONV_BN_SEGS];
+  const void* bn_z[CONV_BN_SEGS];
+  int ld_bnz[CONV_BN_SEGS];
+  const double* bn_mean[CONV_BN_SEGS];
+  const double* bn_rstd[CONV_BN_SEGS];
+};
+hipError_t launch_gap_bwd_bn(int dtype, const PoolArgs& a, const GapBnArgs& b, hipStream_t s,
+                             int* row_blocks);
+int gap_bn_max_row_blocks();
 
 struct CeArgs {
   const void* z; int ldz;          // logits [n][classes]

@@ -1363,9 +1363,12 @@ __global__ __launch_bounds__(256) void k_gather(GatherArgs a) {
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void k_flip(const T* __restrict__ w, T* __restrict__ wd, int N,
-                                               int R, int S, int C, int flip) {
-  int64_t total = (int64_t)N * R * S * C;
+__global__ __launch_bounds__(256) void k_flip_set(FlipSet f) {
+  const int q = blockIdx.y;
+  const T* __restrict__ w = (const T*)f.w[q];
+  T* __restrict__ wd = (T*)f.wd[q];
+  const int N = f.N[q], R = f.R[q], S = f.S[q], C = f.C[q], flip = f.flip[q];
+  const int64_t total = (int64_t)N * R * S * C;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
        i += (int64_t)gridDim.x * blockDim.x) {
     // i indexes wd[c][r][s][n]
@@ -1690,19 +1693,24 @@ hipError_t launch_gather(int dtype, const GatherArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_flip_weights(int dtype, const void* w, void* wd, int N, int R, int S, int C,
-                               hipStream_t s, int flip) {
-  int64_t total = (int64_t)N * R * S * C;
-  int blocks = (int)((total + 255) / 256);
-  if (blocks > 4096) blocks = 4096;
-  if (total <= 0) return hipSuccess;
+hipError_t launch_flip_set(int dtype, const FlipSet& f, hipStream_t s) {
+  if (f.n <= 0) return hipSuccess;
+  if (f.n > FLIP_MAX) return hipErrorInvalidValue;
+  int64_t most = 0, total = 0;
+  for (int q = 0; q < f.n; ++q) {
+    const int64_t e = (int64_t)f.N[q] * f.R[q] * f.S[q] * f.C[q];
+    most = std::max(most, e);
+    total += e;
+  }
+  if (most <= 0) return hipSuccess;
+  int blocks = (int)((most + 255) / 256);
+  if (blocks > 1024) blocks = 1024;
   if (dtype == DT_BF16)
-    XP_LAUNCH("k_flip<bf16>", (double)total * 4, k_flip<bf16_t>, dim3(blocks), dim3(256), 0, s,
-              (const bf16_t*)w, (bf16_t*)wd, N, R, S, C, flip);
+    XP_LAUNCH("k_flip_set<bf16>", (double)total * 4, k_flip_set<bf16_t>, dim3(blocks, f.n), dim3(256), 0, s, f);
   else
-    XP_LAUNCH("k_flip<f32>", (double)total * 8, k_flip<float>, dim3(blocks), dim3(256), 0, s,
-              (const float*)w, (float*)wd, N, R, S, C, flip);
+    XP_LAUNCH("k_flip_set<f32>", (double)total * 8, k_flip_set<float>, dim3(blocks, f.n), dim3(256), 0, s, f);
   return hipGetLastError();
 }
+
 
 }  // namespace xp

@@ -1743,13 +1743,26 @@ xpipe_status refresh_gathered(xpipe_stage* st, int dir) {
 }
 
 xpipe_status refresh_flipped(xpipe_stage* st) {
+  // same grid: flipped (the data gradient is a convolution of dy); strided or
+  // unpadded: transposed only (the data gradient gathers dy tap by tap).  Up
+  // to FLIP_MAX convolutions per launch.
+  FlipSet f{};
   for (const Op& op : st->ops) {
     if (op.kind != OP_GEMM) continue;
-    // same grid: flipped (the data gradient is a convolution of dy); strided or
-    // unpadded: transposed only (the data gradient gathers dy tap by tap)
-    XP_HIP(launch_flip_weights(st->dtype, gemm_weights(st, op, XPIPE_BWD), st->ws + op.wd_off,
-                               op.cout, op.k, op.kw, op.cin, st->stream, !op.grid));
+    const int q = f.n++;
+    f.w[q] = gemm_weights(st, op, XPIPE_BWD);
+    f.wd[q] = st->ws + op.wd_off;
+    f.N[q] = op.cout;
+    f.R[q] = op.k;
+    f.S[q] = op.kw;
+    f.C[q] = op.cin;
+    f.flip[q] = !op.grid;
+    if (f.n == FLIP_MAX) {
+      XP_HIP(launch_flip_set(st->dtype, f, st->stream));
+      f.n = 0;
+    }
   }
+  XP_HIP(launch_flip_set(st->dtype, f, st->stream));
   st->wd_valid = true;
   return XPIPE_OK;
 }

@@ -152,10 +152,17 @@ size_t wgrad_part_bytes(int dtype, int N, int K, int splits);
 int wgrad_pick_splits(int dtype, int M, int N, int K, int taps);
 hipError_t launch_wgrad(int dtype, const WgradArgs& a, hipStream_t s);
 
-// Transposed copy for the data gradient, flipped for stride 1:
+// Transposed copies of the convolutions' weights for their data gradients,
+// flipped for stride 1, up to FLIP_MAX per launch (grid y = the convolution):
 // wd[c][r][s][n] = w[n][R-1-r][S-1-s][c] (flip != 0) or w[n][r][s][c] (flip == 0).
-hipError_t launch_flip_weights(int dtype, const void* w, void* wd, int N, int R, int S, int C,
-                               hipStream_t s, int flip = 1);
+constexpr int FLIP_MAX = 32;
+struct FlipSet {
+  int n;
+  const void* w[FLIP_MAX];
+  void* wd[FLIP_MAX];
+  int N[FLIP_MAX], R[FLIP_MAX], S[FLIP_MAX], C[FLIP_MAX], flip[FLIP_MAX];
+};
+hipError_t launch_flip_set(int dtype, const FlipSet& f, hipStream_t s);
 
 // ---------------------------------------------------------------- column reductions
 // Per-column sums over the rows of [M][C] views, two-level and fixed-order.

@@ -1351,14 +1351,12 @@ __global__ __launch_bounds__(256) void k_split_reduce(const P* __restrict__ part
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_gather(GatherArgs a) {
-  int64_t base = 0;
   for (int j = 0; j < a.nseg; ++j) {
     const T* src = (const T*)a.src[j];
-    T* dst = (T*)a.dst + base;
+    T* dst = (T*)a.dst[j];
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < a.count[j];
          i += (int64_t)gridDim.x * blockDim.x)
       dst[i] = src[i];
-    base += a.count[j];
   }
 }
 
@@ -1678,6 +1676,7 @@ hipError_t launch_wgrad(int dtype, const WgradArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_gather(int dtype, const GatherArgs& a, hipStream_t s) {
+  if (a.nseg < 0 || a.nseg > GATHER_BATCH) return hipErrorInvalidValue;
   int64_t total = 0, longest = 0;
   for (int j = 0; j < a.nseg; ++j) {
     total += a.count[j];

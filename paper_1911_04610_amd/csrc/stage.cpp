@@ -1723,22 +1723,29 @@ RuleCoef rule_coef(const xpipe_rule_hparams* rp, const xpipe_hparams* hp) {
 
 // the merged GEMMs' weights, gathered from the prediction of direction dir
 xpipe_status refresh_gathered(xpipe_stage* st, int dir) {
+  // every merged GEMM's sibling weights, up to GATHER_BATCH copies per launch
+  const size_t esz = st->esz();
+  GatherArgs g{};
   for (const Op& op : st->ops) {
     if (op.segs.empty()) continue;
-    GatherArgs g{};
-    g.nseg = (int)op.segs.size();
     const int64_t K = (int64_t)op.k * op.kw * op.cin;
-    for (int q = 0; q < g.nseg; ++q) {
-      const int64_t off = op.segs[q].first;
+    int64_t base = 0;
+    for (const auto& sg : op.segs) {
+      const int q = g.nseg++;
       if (st->dtype == DT_BF16)
-        g.src[q] = st->ws + (dir == XPIPE_FWD ? st->bf_f_off : st->bf_b_off) + (size_t)off * 2;
+        g.src[q] = st->ws + (dir == XPIPE_FWD ? st->bf_f_off : st->bf_b_off) + (size_t)sg.first * 2;
       else
-        g.src[q] = (dir == XPIPE_FWD ? st->wpf : st->wpb) + off;
-      g.count[q] = K * op.segs[q].second;
+        g.src[q] = (dir == XPIPE_FWD ? st->wpf : st->wpb) + sg.first;
+      g.dst[q] = st->ws + op.wg_off[dir] + (size_t)base * esz;
+      g.count[q] = K * sg.second;
+      base += g.count[q];
+      if (g.nseg == GATHER_BATCH) {
+        XP_HIP(launch_gather(st->dtype, g, st->stream));
+        g.nseg = 0;
+      }
     }
-    g.dst = st->ws + op.wg_off[dir];
-    XP_HIP(launch_gather(st->dtype, g, st->stream));
   }
+  if (g.nseg > 0) XP_HIP(launch_gather(st->dtype, g, st->stream));
   return XPIPE_OK;
 }
 

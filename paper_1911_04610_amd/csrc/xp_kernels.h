@@ -66,11 +66,13 @@ hipError_t launch_adam(float* W, float* m, float* v, float* G, int64_t n, const 
 // Copies nseg blocks of elements (storage dtype) back to back into dst: the
 // weights of sibling layers that share one GEMM launch.
 constexpr int GATHER_MAX_SEGS = 4;
+// copies src[j] -> dst[j] (count[j] elements) for j < nseg, one launch
+constexpr int GATHER_BATCH = 16;
 struct GatherArgs {
   int nseg;
-  const void* src[GATHER_MAX_SEGS];
-  int64_t count[GATHER_MAX_SEGS];
-  void* dst;
+  const void* src[GATHER_BATCH];
+  void* dst[GATHER_BATCH];
+  int64_t count[GATHER_BATCH];
 };
 hipError_t launch_gather(int dtype, const GatherArgs& a, hipStream_t s);
 

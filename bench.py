@@ -210,6 +210,24 @@ def time_stage(args, timing_pass=True, graphs=True, workload=None, dtype=None, s
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms = e0.elapsed_time(e1) / steps
+    # the two passes apart (recorded graphs, all lanes): T forwards, then T
+    # backwards (each with its recomputed forward), microseconds per micro-batch
+    def pass_us(fn, reps=10):
+        torch.cuda.synchronize()
+        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a0.record(stream)
+        for _ in range(reps):
+            fn()
+        a1.record(stream)
+        torch.cuda.synchronize()
+        return a0.elapsed_time(a1) / reps / w.T * 1e3
+    passes = {
+        "fwd_us": round(pass_us(lambda: [st.xpipe_stage_fwd(xs[0][i], y, None if labels is None else labels[0][i],
+                                                            loss if w.has_loss else None) for i in range(w.T)]), 1),
+        "bwd_with_recompute_us": round(pass_us(lambda: [st.xpipe_stage_bwd(xs[0][i], None if dys is None else dys[0][i],
+                                                                           None if labels is None else labels[0][i], dx)
+                                                        for i in range(w.T)]), 1)}
+    time_stage.passes = passes
     if not timing_pass:
         return w, ms, wall, {}, True
     # per-kernel durations with HIP events around every launch, over the same
@@ -793,6 +811,7 @@ def main():
         "mfma_util_all_gemm": tab.all_gemm_frac(),
         "launches_per_step": tab.launches_per_step(),
         "kernels_timed_sum_ms_per_step": round(sum(v[0] for v in classes.values()) / args.steps, 4),
+        "pass_us_per_micro_batch": getattr(time_stage, "passes", None),
         "top_kernels": [tab.summary(k) for k in top],
         "finite": finite,
     }

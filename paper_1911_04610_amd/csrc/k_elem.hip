@@ -1421,6 +1421,7 @@ __global__ __launch_bounds__(256) void k_gap_bwd_bn_v(PoolArgs a, GapBnArgs b, i
 }
 
 // ---------------------------------------------------------------- softmax cross-entropy
+constexpr int CE_REG = 8;  // classes per lane kept in registers (up to 512 classes)
 // One workgroup; wave w handles rows w, w + 16, ...  Row losses go to LDS and
 // one thread adds them in row order.
 template <typename T>
@@ -1429,6 +1430,63 @@ __global__ __launch_bounds__(1024) void k_softmax_ce(CeArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const T* Z = (const T*)a.z;
   T* DZ = (T*)a.dz;
+  if (a.classes <= 64 * CE_REG) {
+    // each lane keeps its logits (classes lane, lane + 64, ...) and their
+    // exponentials in registers, and a wave takes two rows at once: the same
+    // operations in the same order as the loop below, without re-reading or
+    // re-exponentiating
+    for (int r0 = wave; r0 < a.n; r0 += 32) {
+      double v[2][CE_REG], e[2][CE_REG], mx[2], se[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int r = r0 + 16 * h;
+        mx[h] = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < CE_REG; ++k) {
+          const int c = lane + 64 * k;
+          v[h][k] = (r < a.n && c < a.classes) ? ldd(Z + (size_t)r * a.ldz + c) : -INFINITY;
+          mx[h] = fmax(mx[h], v[h][k]);
+        }
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        mx[h] = wave_max(mx[h]);
+        se[h] = 0.0;
+#pragma unroll
+        for (int k = 0; k < CE_REG; ++k) {
+          e[h][k] = lane + 64 * k < a.classes ? exp(v[h][k] - mx[h]) : 0.0;
+          se[h] += e[h][k];
+        }
+        se[h] = wave_sum(se[h]);
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int r = r0 + 16 * h;
+        if (r >= a.n) break;
+        const int lab = a.labels[r];
+        const bool lab_ok = lab >= 0 && lab < a.classes;  // out-of-range label: NaN, no read
+        if (lane == 0 && r < 1024)
+          row_loss[r] = lab_ok ? -((ldd(Z + (size_t)r * a.ldz + lab) - mx[h]) - log(se[h])) : NAN;
+        if (DZ) {
+#pragma unroll
+          for (int k = 0; k < CE_REG; ++k) {
+            const int c = lane + 64 * k;
+            if (c >= a.classes) break;
+            double p = e[h][k] / se[h];
+            if (c == lab) p -= 1.0;
+            std_(DZ + (size_t)r * a.lddz + c, lab_ok ? p * a.inv_N : NAN);
+          }
+        }
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0 && a.loss) {
+      double s = 0.0;
+      for (int r = 0; r < a.n && r < 1024; ++r) s += row_loss[r];
+      *a.loss = (float)(s * a.inv_N);
+    }
+    return;
+  }
   for (int r = wave; r < a.n; r += 16) {
     const T* z = Z + (size_t)r * a.ldz;
     double mx = -INFINITY;

@@ -97,6 +97,15 @@ LAYER_CASES = {
                             dict(kind="softmax_ce", inputs=[1], classes=200)], (7, 7, 256), 4),
     "mlp_head10": ([dict(kind="linear", inputs=[-1], cin=256, cout=10, bias=True),
                     dict(kind="softmax_ce", inputs=[0], classes=10)], (256,), 32),
+    # more classes than the cross-entropy kernel keeps in registers (512)
+    "mlp_head600": ([dict(kind="linear", inputs=[-1], cin=128, cout=600, bias=True),
+                     dict(kind="softmax_ce", inputs=[0], classes=600)], (128,), 8),
+    # the head's average-pool backward completes the BN output's gradient and
+    # takes its backward partials (bf16)
+    "bn_relu_gap_head": ([conv(-1, 32, 64, 3), bn(0, 64), dict(kind="relu", inputs=[1]),
+                          dict(kind="gap", inputs=[2]),
+                          dict(kind="linear", inputs=[3], cin=64, cout=10, bias=True),
+                          dict(kind="softmax_ce", inputs=[4], classes=10)], (9, 9, 32), 4),
     "concat_views": ([conv(-1, 64, 64, 1), conv(-1, 64, 32, 3),
                       dict(kind="concat", inputs=[0, 1]), conv(2, 96, 48, 1)], (8, 8, 64), 2),
     # two wide 3x3 siblings (bf16: one 512 x 4608 launch of 576 tiles, whose

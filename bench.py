@@ -210,6 +210,8 @@ def time_stage(args, timing_pass=True, graphs=True, workload=None, dtype=None, s
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms = e0.elapsed_time(e1) / steps
+    if not timing_pass:
+        return w, ms, wall, {}, True
     # the two passes apart (recorded graphs, all lanes): T forwards, then T
     # backwards (each with its recomputed forward), microseconds per micro-batch
     def pass_us(fn, reps=10):
@@ -228,8 +230,6 @@ def time_stage(args, timing_pass=True, graphs=True, workload=None, dtype=None, s
                                                                            None if labels is None else labels[0][i], dx)
                                                         for i in range(w.T)]), 1)}
     time_stage.passes = passes
-    if not timing_pass:
-        return w, ms, wall, {}, True
     # per-kernel durations with HIP events around every launch, over the same
     # number of steps
     st.set_timing(True)

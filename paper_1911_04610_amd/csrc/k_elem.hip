@@ -885,10 +885,15 @@ __global__ __launch_bounds__(256) void k_maxpool_bwd_v(PoolArgs a) {
       const int me = ((h & 1) << 1) + (w & 1);
 #pragma unroll
       for (int e = 0; e < N; ++e) {
+        // the running maximum is kept by value (no runtime index into v)
         int arg = 0;
+        double best = v[0][e];
 #pragma unroll
         for (int q = 1; q < 4; ++q)
-          if (v[q][e] > v[arg][e]) arg = q;  // first maximum in row-major order wins ties
+          if (v[q][e] > best) {  // first maximum in row-major order wins ties
+            best = v[q][e];
+            arg = q;
+          }
         d[e] = arg == me ? g[e] : 0.0;
       }
     }

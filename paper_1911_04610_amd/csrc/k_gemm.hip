@@ -245,16 +245,21 @@ XP_DEV void conv_epilogue_bf16(const ConvArgs& a, float* ot, int tid, int m0, in
         const bf16_t* zc = nullptr;
         const double *mp = nullptr, *rp = nullptr;
         int ldz = 0;
+        bool sum_only = false;  // a bias (no z): the column sums of g alone
 #pragma unroll
         for (int q = 0; q < CONV_BN_SEGS; ++q)
           if (q < a.bn_nseg && n >= a.bn_c0[q] && n < a.bn_c1[q]) {
             const int lc = n - a.bn_c0[q];
-            zc = (const bf16_t*)a.bn_z[q] + lc;
+            sum_only = a.bn_z[q] == nullptr;
+            zc = sum_only ? nullptr : (const bf16_t*)a.bn_z[q] + lc;
             ldz = a.ld_bnz[q];
-            mp = a.bn_mean[q] + lc;
-            rp = a.bn_rstd[q] + lc;
+            mp = sum_only ? nullptr : a.bn_mean[q] + lc;
+            rp = sum_only ? nullptr : a.bn_rstd[q] + lc;
           }
-        if (zc && n < a.N) {
+        if (sum_only && n < a.N) {
+#pragma unroll
+          for (int r = 0; r < RROWS; ++r) s0[r & 3] += (double)oc[r * OPITCH];  // 0 past the last row
+        } else if (zc && n < a.N) {
           const double mu = *mp, rs = *rp;
           // every load issued before the first use: rows past the last are
           // read at the last row (their g is 0)

@@ -820,7 +820,11 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
       std::vector<std::pair<int, int>> segs;
       for (size_t b = 0; b < p.ops.size(); ++b) {
         const Op& bn = p.ops[b];
-        if (bn.kind != OP_BN || bn.in2 >= 0 || bn.out == p.out_tensor) continue;
+        // BNs (no residual), and, for a GEMM's epilogue, convolutions with a
+        // bias (their bias gradient is the column sums of the same g)
+        const bool is_bn = bn.kind == OP_BN && bn.in2 < 0;
+        const bool is_bias = g.kind == OP_GEMM && bn.kind == OP_GEMM && bn.b_off >= 0 && bn.segs.empty();
+        if ((!is_bn && !is_bias) || bn.out == p.out_tensor) continue;
         const Tensor& u = p.tensors[bn.out];
         if (g.kind == OP_GAP && (u.coff % 8 != 0 || u.sh.C % 8 != 0)) continue;
         if (bn.out == t) segs.push_back({(int)b, 0});
@@ -1427,9 +1431,14 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
             a.bn_nseg = (int)op.bnb_segs.size();
             for (int k = 0; k < a.bn_nseg; ++k) {
               const Op& bn = st->ops[op.bnb_segs[k].first];
+              a.bn_c0[k] = op.bnb_segs[k].second;
+              if (bn.kind == OP_GEMM) {  // a convolution's bias: sums of g only
+                a.bn_c1[k] = a.bn_c0[k] + bn.cout;
+                a.bn_z[k] = nullptr;
+                continue;
+              }
               View z = act(st, bn.in, c);
               const double* bst = (const double*)(st->ws + bn.stat_off);
-              a.bn_c0[k] = op.bnb_segs[k].second;
               a.bn_c1[k] = a.bn_c0[k] + st->tensors[bn.in].sh.C;
               a.bn_z[k] = z.p;
               a.ld_bnz[k] = z.ld;
@@ -1490,10 +1499,18 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
           ca.lda = g.ld;
           ca.M = M;
           ca.C = op.cout;
-          ca.partial = (double*)(st->ws + st->colpart_off[lane]);
-          ca.row_blocks = col_row_blocks(M, op.cout);
           ca.grad0 = st->grad + op.b_off;
-          XP_HIP(launch_colreduce(dt, ca, s));
+          if (op.bnb_gemm >= 0) {
+            // the column sums of g from the epilogue that completed it
+            ca.row_blocks = st->bnb_nrb[op.bnb_gemm];
+            ca.partial = (double*)(st->ws + st->ops[op.bnb_gemm].bnb_part_off) +
+                         (size_t)op.bnb_c0 * 2 * ca.row_blocks;
+            XP_HIP(launch_colfinal(ca, s));
+          } else {
+            ca.partial = (double*)(st->ws + st->colpart_off[lane]);
+            ca.row_blocks = col_row_blocks(M, op.cout);
+            XP_HIP(launch_colreduce(dt, ca, s));
+          }
         }
         break;
       }

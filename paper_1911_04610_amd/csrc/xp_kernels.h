@@ -101,7 +101,8 @@ struct ConvArgs {
   // bn_z[k], ld_bnz[k]) with batch mean / rstd bn_mean[k] / bn_rstd[k] (all
   // three from the norm's first column on); per row tile, the column sums of
   // g and of g (z - mean) rstd, at bn_part[(n * 2 + {0,1}) * row_tiles + tile]
-  // (the BN backward's partials; columns outside every range get zeros)
+  // (the BN backward's partials; columns outside every range get zeros).
+  // bn_z[k] == nullptr: a bias's columns, the sums of g alone (second sum 0)
   double* bn_part;
   int bn_nseg;
   int bn_c0[CONV_BN_SEGS], bn_c1[CONV_BN_SEGS];

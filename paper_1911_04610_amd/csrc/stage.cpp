@@ -798,8 +798,8 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
   // that completes the gradient of the BN outputs: a GEMM reading a whole
   // tensor (standalone or a concat) that is the first of the tensor's
   // readers, so the last writer of its gradient in the backward; the BNs
-  // (no residual) whose output is that tensor or a member of it take their
-  // partials from the launch, at most CONV_BN_SEGS of them
+  // whose output is that tensor or a member of it take their partials from
+  // the launch, at most CONV_BN_SEGS of them
   if (dtype == DT_BF16) {
     for (size_t j = 0; j < p.ops.size(); ++j) {
       Op& g = p.ops[j];
@@ -820,9 +820,11 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
       std::vector<std::pair<int, int>> segs;
       for (size_t b = 0; b < p.ops.size(); ++b) {
         const Op& bn = p.ops[b];
-        // BNs (no residual), and, for a GEMM's epilogue, convolutions with a
-        // bias (their bias gradient is the column sums of the same g)
-        const bool is_bn = bn.kind == OP_BN && bn.in2 < 0;
+        // BNs (with or without a residual: the partials are of the gradient
+        // at the BN(+add) output either way), and, for a GEMM's epilogue,
+        // convolutions with a bias (their bias gradient is the column sums of
+        // the same g)
+        const bool is_bn = bn.kind == OP_BN;
         const bool is_bias = g.kind == OP_GEMM && bn.kind == OP_GEMM && bn.b_off >= 0 && bn.segs.empty();
         if ((!is_bn && !is_bias) || bn.out == p.out_tensor) continue;
         const Tensor& u = p.tensors[bn.out];

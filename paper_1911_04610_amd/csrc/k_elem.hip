@@ -617,6 +617,13 @@ __global__ __launch_bounds__(256) void k_colfinal_v(ColArgs a) {
   const int col = blockIdx.x;
   const double* p0 = a.partial + (size_t)col * 2 * a.row_blocks;
   const double* p1 = p0 + a.row_blocks;
+  // the gradient accumulators the finish adds to, read before the reduction
+  // so that their latency overlaps it
+  float acc0 = 0.f, acc1 = 0.f;
+  if (threadIdx.x == 0 && a.mode != COL_STATS) {
+    acc0 = a.grad0[col];
+    if (a.mode == COL_BNBWD) acc1 = a.grad1[col];
+  }
   double s0 = 0.0, s1 = 0.0;
 #pragma unroll 4
   for (int b = threadIdx.x; b < a.row_blocks; b += 256) {
@@ -630,9 +637,20 @@ __global__ __launch_bounds__(256) void k_colfinal_v(ColArgs a) {
     sh[1][wave] = s1;
   }
   __syncthreads();
-  if (threadIdx.x == 0)
-    col_finish_one(a, col, ((sh[0][0] + sh[0][1]) + sh[0][2]) + sh[0][3],
-                   ((sh[1][0] + sh[1][1]) + sh[1][2]) + sh[1][3]);
+  if (threadIdx.x == 0) {
+    const double t0 = ((sh[0][0] + sh[0][1]) + sh[0][2]) + sh[0][3];
+    const double t1 = ((sh[1][0] + sh[1][1]) + sh[1][2]) + sh[1][3];
+    if (a.mode == COL_STATS) {
+      col_finish_one(a, col, t0, t1);
+    } else if (a.mode == COL_BNBWD) {
+      a.out0[col] = t0;
+      a.out1[col] = t1;
+      a.grad0[col] = (float)((double)acc0 + t1);
+      a.grad1[col] = (float)((double)acc1 + t0);
+    } else {
+      a.grad0[col] = (float)((double)acc0 + t0);
+    }
+  }
 }
 
 hipError_t launch_colfinal(const ColArgs& a, hipStream_t s) {

@@ -59,6 +59,12 @@ constexpr double BN_EPS = 1e-5;
 // (8.24 against 7.88 ms), and so did six or eight lanes (8.8 ms), two (7.97)
 // or one (9.64)
 constexpr int NLANES = 3;
+// lanes a pass may start new chains on.  The backward (recompute, data and
+// weight gradients) keeps the GPU busy with two: a third lane there made the
+// Inception-A step slower (6.65 against 6.62 ms; one lane: 7.80 ms), while
+// the forward, bound by launch latency, loses with fewer than three (two:
+// 6.94 ms, one: 7.98 ms)
+constexpr int PASS_LANES[2] = {3, 2};
 
 int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 
@@ -318,7 +324,7 @@ void plan_lanes(Plan& p) {
       }
       if (lane < 0) {
         lane = 0;
-        for (int l = 1; l < NLANES; ++l)
+        for (int l = 1; l < PASS_LANES[pass]; ++l)
           if (tail_q[l] < tail_q[lane]) lane = l;
       }
       op.lane[pass] = lane;

@@ -63,7 +63,13 @@ typedef enum { XPIPE_FWD = 0, XPIPE_BWD = 1 } xpipe_dir;
 typedef enum {
   XPIPE_PRED_EQ3 = 0,     /* m_hat / sqrt(v_hat + eps), m_hat = m/(1-beta1^t), v_hat = v/(1-beta2^t) */
   XPIPE_PRED_ADAMDIR = 1, /* m_hat / (sqrt(v_hat) + eps): Adam's own update direction */
-  XPIPE_PRED_LITERAL = 2  /* (m/(1-beta1)) / sqrt(v/(1-beta2) + eps): Eq. 4 as printed */
+  XPIPE_PRED_LITERAL = 2, /* (m/(1-beta1)) / sqrt(v/(1-beta2) + eps): Eq. 4 as printed */
+  XPIPE_PRED_SMOOTHED = 3 /* m/(1-beta1): the smoothed gradient of momentum SGD, the
+                           * predictor of SpecTrain that Sec. II describes.  With beta1
+                           * equal to the rule's momentum and m advanced by the same
+                           * gradients from zero, m/(1-beta1) is the heavy-ball buffer
+                           * buf of XPIPE_RULE_MOMENTUM_SGD, so W_hat = W - s lr buf
+                           * (lr: the rule's). */
 } xpipe_pred_mode;
 
 /* Tie rule for the "round" of Eq. 1 and Eq. 2 (undefined in the paper). */
@@ -193,7 +199,7 @@ xpipe_status xpipe_stage_output_shape(xpipe_stage_t st, int32_t* n, int32_t* H, 
 
 /* Bellwether prediction (Sec. III-B, Eq. 3 with Eq. 4's moments after hp->t
  * completed updates): w_pred_{fwd|bwd} = W - s * lr * dir(m, v).  s >= 0.
- * s = 0, or hp->t = 0 with a bias-corrected mode, gives W exactly.  The
+ * s = 0, or hp->t = 0 with any mode but LITERAL, gives W exactly.  The
  * result is cached for the mini-batch's other T-1 micro-batches. */
 xpipe_status xpipe_predict_weights(xpipe_stage_t st, int32_t which, int32_t s,
                                    const xpipe_hparams* hp);

@@ -15,6 +15,7 @@ Contents:
   schedule  the pipeline schedule as a unit-time model, with staleness counts
 """
 from .method import (HALF_DOWN, HALF_EVEN, HALF_UP, PRED_ADAMDIR, PRED_EQ3, PRED_LITERAL,
+                     PRED_SMOOTHED,
                      RULE_ADAM, RULE_MOMENTUM_SGD, RULE_RMSPROP, adam_moments, adam_update,
                      momentum_sgd_update, predict, rmsprop_update, version_difference_bwd,
                      version_difference_fwd)
@@ -22,7 +23,7 @@ from .stage import Hyper, MinibatchRecord, ScheduleRecord, Stage, train_schedule
 from . import schedule
 
 __all__ = [
-    "HALF_DOWN", "HALF_EVEN", "HALF_UP", "PRED_ADAMDIR", "PRED_EQ3", "PRED_LITERAL",
+    "HALF_DOWN", "HALF_EVEN", "HALF_UP", "PRED_ADAMDIR", "PRED_EQ3", "PRED_LITERAL", "PRED_SMOOTHED",
     "RULE_ADAM", "RULE_MOMENTUM_SGD", "RULE_RMSPROP", "adam_moments", "adam_update",
     "momentum_sgd_update", "predict", "rmsprop_update", "version_difference_bwd",
     "version_difference_fwd",

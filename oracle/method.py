@@ -24,6 +24,7 @@ HALF_DOWN = "half_down"
 PRED_EQ3 = "eq3"           # Eq. 3: m_hat / sqrt(v_hat + eps), bias correction 1 - beta^t
 PRED_ADAMDIR = "adamdir"   # Adam's own direction m_hat / (sqrt(v_hat) + eps)
 PRED_LITERAL = "literal"   # Eq. 4 as printed: m / (1 - beta1), v / (1 - beta2)
+PRED_SMOOTHED = "smoothed" # SpecTrain's smoothed gradient (Sec. II): m / (1 - beta1), no v
 
 
 def _round(x: float, rule: str) -> int:
@@ -67,6 +68,12 @@ def predict(W, m, v, t: int, s: int, lr: float, beta1: float, beta2: float, eps:
     of the mini-batch being predicted for does not exist yet).  With t = 0 the
     bias corrections 1 - beta^t vanish and no update has happened, so the
     prediction is W itself; s = 0 is likewise W.
+
+    PRED_SMOOTHED is the predictor Sec. II attributes to SpecTrain: the weights
+    moved s steps along momentum SGD's smoothed gradient.  Heavy-ball momentum
+    without dampening keeps buf = sum_j mu^(k-j) g_j, and the first moment with
+    beta1 = mu is (1 - mu) times the same sum, so m / (1 - beta1) is that
+    buffer and the prediction is W - s lr buf.
     """
     W = np.asarray(W, np.float64)
     if s == 0 or (t == 0 and mode != PRED_LITERAL):
@@ -83,6 +90,8 @@ def predict(W, m, v, t: int, s: int, lr: float, beta1: float, beta2: float, eps:
         dW = m_hat / (np.sqrt(v_hat) + eps)
     elif mode == PRED_LITERAL:
         dW = (m / (1.0 - beta1)) / np.sqrt(v / (1.0 - beta2) + eps)
+    elif mode == PRED_SMOOTHED:
+        dW = m / (1.0 - beta1)
     else:
         raise ValueError(mode)
     return W - s * lr * dW

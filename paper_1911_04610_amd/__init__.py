@@ -26,7 +26,7 @@ OK, EINVAL, ESTATE, EHIP, EUNSUPPORTED = 0, 1, 2, 3, 4
 F32, BF16 = 0, 1
 FWD, BWD = 0, 1
 KEEP_PRED = 2
-PRED_EQ3, PRED_ADAMDIR, PRED_LITERAL = 0, 1, 2
+PRED_EQ3, PRED_ADAMDIR, PRED_LITERAL, PRED_SMOOTHED = 0, 1, 2, 3
 RULE_MOMENTUM_SGD, RULE_RMSPROP = 1, 2
 ROUND_HALF_UP, ROUND_HALF_EVEN, ROUND_HALF_DOWN = 0, 1, 2
 KINDS = {"linear": 0, "conv": 1, "bn": 2, "relu": 3, "add": 4, "maxpool2": 5, "avgpool3": 6,

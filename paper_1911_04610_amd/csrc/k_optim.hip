@@ -18,7 +18,8 @@ constexpr int STREAM_BLOCK = 256;
 
 XP_DEV double pred_dir(double m, double v, const PredCoef& c) {
   double mh = m * c.c1, vh = v * c.c2;
-  return c.eps_outside ? mh / (sqrt(vh) + c.eps) : mh / sqrt(vh + c.eps);
+  if (c.kind == PRED_DIR_SMOOTHED) return mh;
+  return c.kind == PRED_DIR_ADAM ? mh / (sqrt(vh) + c.eps) : mh / sqrt(vh + c.eps);
 }
 
 // s = 0 (or t = 0 with bias correction) is the identity: W is returned bit for bit
@@ -123,7 +124,7 @@ __global__ __launch_bounds__(STREAM_BLOCK) void k_adam(float* __restrict__ W, fl
                                                bf16_t* __restrict__ pb_bf, PredCoef cb) {
   const int64_t nv = n >> 2;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const bool shared = cf.c1 == cb.c1 && cf.c2 == cb.c2 && cf.eps == cb.eps && cf.eps_outside == cb.eps_outside;
+  const bool shared = cf.c1 == cb.c1 && cf.c2 == cb.c2 && cf.eps == cb.eps && cf.kind == cb.kind;
   float4* W4 = reinterpret_cast<float4*>(W);
   float4* m4 = reinterpret_cast<float4*>(m);
   float4* v4 = reinterpret_cast<float4*>(v);
@@ -237,7 +238,7 @@ __global__ __launch_bounds__(STREAM_BLOCK) void k_rule(float* __restrict__ W, fl
   float4* m4 = reinterpret_cast<float4*>(m);
   float4* v4 = reinterpret_cast<float4*>(v);
   float4* G4 = reinterpret_cast<float4*>(G);
-  const bool shared = cf.c1 == cb.c1 && cf.c2 == cb.c2 && cf.eps == cb.eps && cf.eps_outside == cb.eps_outside;
+  const bool shared = cf.c1 == cb.c1 && cf.c2 == cb.c2 && cf.eps == cb.eps && cf.kind == cb.kind;
   auto preds = [&](int64_t i, const RuleElem (&e)[4]) __attribute__((always_inline)) {
     if (pf && pb) {
       float4 rf, rb;

@@ -1684,7 +1684,7 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
 xpipe_status check_hp(const xpipe_hparams* hp) {
   if (!hp) return fail(XPIPE_EINVAL, "null hparams");
   if (!(hp->lr >= 0) || !(hp->beta1 >= 0 && hp->beta1 < 1) || !(hp->beta2 >= 0 && hp->beta2 < 1) ||
-      !(hp->eps > 0) || hp->t < 0 || hp->mode < 0 || hp->mode > 2)
+      !(hp->eps > 0) || hp->t < 0 || hp->mode < 0 || hp->mode > 3)
     return fail(XPIPE_EINVAL, "bad hparams");
   return XPIPE_OK;
 }
@@ -1692,11 +1692,16 @@ xpipe_status check_hp(const xpipe_hparams* hp) {
 PredCoef pred_coef(const xpipe_hparams* hp, int64_t t, int s) {
   PredCoef c{};
   c.eps = hp->eps;
-  c.eps_outside = hp->mode == XPIPE_PRED_ADAMDIR;
+  c.kind = hp->mode == XPIPE_PRED_ADAMDIR    ? PRED_DIR_ADAM
+           : hp->mode == XPIPE_PRED_SMOOTHED ? PRED_DIR_SMOOTHED
+                                             : PRED_DIR_EQ3;
   bool identity = s == 0 || (t == 0 && hp->mode != XPIPE_PRED_LITERAL);
   if (identity) return c;  // coef = c1 = c2 = 0: W - 0 * 0 = W
   c.coef = (double)s * hp->lr;
-  if (hp->mode == XPIPE_PRED_LITERAL) {
+  if (hp->mode == XPIPE_PRED_SMOOTHED) {
+    // the heavy-ball buffer of the same gradients, from the first moment
+    c.c1 = 1.0 / (1.0 - hp->beta1);
+  } else if (hp->mode == XPIPE_PRED_LITERAL) {
     c.c1 = 1.0 / (1.0 - hp->beta1);
     c.c2 = 1.0 / (1.0 - hp->beta2);
   } else {

@@ -35,8 +35,11 @@ struct PredCoef {
   double coef;      // s * lr (0 for the identity)
   double c1, c2;    // first / second moment scale (bias correction), 0 for the identity
   double eps;
-  int eps_outside;  // Adam's direction: eps added after the root
+  int kind;         // PRED_DIR_*: which direction the moments form
 };
+// directions of the prediction: Eq. 3 (eps inside the root), Adam's own
+// (eps after the root), the smoothed gradient alone (first moment times c1)
+enum { PRED_DIR_EQ3 = 0, PRED_DIR_ADAM = 1, PRED_DIR_SMOOTHED = 2 };
 
 struct AdamCoef {
   double lr, beta1, beta2, one_m_beta1, one_m_beta2;

@@ -128,6 +128,9 @@ def test_flat_entry_points_check_arguments_on_the_host():
     assert L.xpipe_predict_flat(None, None, None, None, None, 0, 1, ctypes.byref(hp), None) == xp.OK
     bad = xp.Hyper(beta1=1.0).c(1)
     assert L.xpipe_predict_flat(None, None, None, None, None, 0, 1, ctypes.byref(bad), None) == xp.EINVAL
+    for mode, want in ((xp.PRED_SMOOTHED, xp.OK), (xp.PRED_SMOOTHED + 1, xp.EINVAL), (-1, xp.EINVAL)):
+        h = xp.Hyper(mode=mode).c(1)
+        assert L.xpipe_predict_flat(None, None, None, None, None, 0, 1, ctypes.byref(h), None) == want
     assert L.xpipe_predict_flat(16, 16, 16, 16, None, 8, -1, ctypes.byref(hp), None) == xp.EINVAL
     # misaligned buffers are refused before any launch
     assert L.xpipe_predict_flat(20, 16, 16, 16, None, 8, 1, ctypes.byref(hp), None) == xp.EINVAL

@@ -18,7 +18,7 @@ from conftest import rel_l2
 pytestmark = pytest.mark.gpu
 TOL = 2e-4
 MODES = {xp.PRED_EQ3: oracle.PRED_EQ3, xp.PRED_ADAMDIR: oracle.PRED_ADAMDIR,
-         xp.PRED_LITERAL: oracle.PRED_LITERAL}
+         xp.PRED_LITERAL: oracle.PRED_LITERAL, xp.PRED_SMOOTHED: oracle.PRED_SMOOTHED}
 
 
 def _dev(a):
@@ -182,6 +182,36 @@ def test_rule_flat_fused_matches_oracle(n, rule, kw):
         for out, s in ((pf, 2), (pb, 1)):
             want = oracle.predict(W32, m32, v32, t + 1, s, hp.lr, hp.beta1, hp.beta2, hp.eps)
             _assert_rounded(_host(out), want, f"pred s={s}")
+
+
+@pytest.mark.parametrize("n", [5, 4096, 1000003])
+def test_rule_flat_smoothed_prediction(n):
+    """Momentum SGD predicting along its own smoothed gradient (SpecTrain's
+    predictor, Sec. II): three fused updates from zero state with fresh
+    gradients, beta1 = momentum.  The predictions of each pass must be the
+    fp32 nearest to the oracle's from the stored state, and W_hat - W must
+    track -s lr buf of the stored heavy-ball buffer."""
+    import torch
+    st = wl.flat_state(n, seed=14)
+    r = xp.Rule(rule=xp.RULE_MOMENTUM_SGD, lr=1e-2, momentum=0.9, weight_decay=5e-4)
+    hp = xp.Hyper(lr=r.lr, beta1=r.momentum, mode=xp.PRED_SMOOTHED)
+    z = np.zeros(n, np.float32)
+    W, buf, m, v = _dev(st.W), _dev(z), _dev(z), _dev(z)
+    rng = np.random.default_rng(15)
+    for t in range(3):
+        g = rng.normal(0, 10 ** rng.uniform(-2, -1), n).astype(np.float32)
+        G = _dev(g)
+        pf, pb = torch.empty_like(W), torch.empty_like(W)
+        xp.xpipe_rule_flat(W, buf, None, m, v, G, r, hp, t, True, pf, 2, pb, 1)
+        torch.cuda.synchronize()
+        W32, b32, m32, v32 = (_host(a) for a in (W, buf, m, v))
+        for out, s in ((pf, 2), (pb, 1)):
+            got = _host(out)
+            want = oracle.predict(W32, m32, v32, t + 1, s, hp.lr, hp.beta1, hp.beta2, hp.eps,
+                                  oracle.PRED_SMOOTHED)
+            _assert_rounded(got, want, f"pred t={t} s={s}")
+            d = got.astype(np.float64) - W32
+            assert rel_l2(d, -s * r.lr * b32.astype(np.float64)) <= 1e-4
 
 
 def test_rule_flat_rejects_bad_arguments():

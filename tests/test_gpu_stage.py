@@ -94,6 +94,24 @@ def test_stage_step_other_rules_fp32_match_oracle(name, rule):
     _compare(gpu, ref, TOL[xp.F32], f"{name}/f32/rule{rule}")
 
 
+@pytest.mark.parametrize("name", ["tiny_mlp", "inception_v3_stage"])
+def test_stage_step_smoothed_prediction_fp32_matches_oracle(name):
+    """Momentum SGD predicting along its smoothed gradient (SpecTrain's
+    predictor as Sec. II describes it; beta1 = momentum): both bellwether
+    predictions and the fused update's predictions, every tensor within 2e-4
+    of the oracle."""
+    w = CASES[name]()
+    inp = wl.stage_inputs(w, act_dtype="f32", moment_init="paper")
+    r = xp.Rule(rule=xp.RULE_MOMENTUM_SGD, lr=1e-2, momentum=0.9, weight_decay=5e-4)
+    ohp = oracle.Hyper(lr=r.lr, beta1=0.9, mode=oracle.PRED_SMOOTHED, rule=oracle.RULE_MOMENTUM_SGD,
+                       momentum=0.9, weight_decay=5e-4)
+    hp = xp.Hyper(lr=r.lr, beta1=0.9, mode=xp.PRED_SMOOTHED)
+    gpu, _ = run_stage(w, inp, xp.F32, hp, w.s_fwd, w.s_bwd, rule=r)
+    ref = oracle.train_stage(oracle.Stage(w.layers, "f32"), inp.params, inp.m, inp.v, inp.xs,
+                             w.s_fwd, w.s_bwd, ohp, labels=inp.labels, dys=inp.dys)
+    _compare(gpu, ref, TOL[xp.F32], f"{name}/f32/smoothed")
+
+
 def _all_errs(recs, ref):
     e = {}
     for j, (g, r) in enumerate(zip(recs, ref)):

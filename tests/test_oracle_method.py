@@ -102,7 +102,7 @@ def _state(n=4096, seed=7):
     return W, m, v
 
 
-@pytest.mark.parametrize("mode", [om.PRED_EQ3, om.PRED_ADAMDIR, om.PRED_LITERAL])
+@pytest.mark.parametrize("mode", [om.PRED_EQ3, om.PRED_ADAMDIR, om.PRED_LITERAL, om.PRED_SMOOTHED])
 def test_predict_identities(mode):
     W, m, v = _state()
     assert np.array_equal(om.predict(W, m, v, 100, 0, mode=mode, **HP), W)          # s = 0
@@ -112,7 +112,7 @@ def test_predict_identities(mode):
         assert np.array_equal(om.predict(W, m, v, 0, 3, mode=mode, **HP), W)        # t = 0
 
 
-@pytest.mark.parametrize("mode", [om.PRED_EQ3, om.PRED_ADAMDIR, om.PRED_LITERAL])
+@pytest.mark.parametrize("mode", [om.PRED_EQ3, om.PRED_ADAMDIR, om.PRED_LITERAL, om.PRED_SMOOTHED])
 def test_predict_linear_in_s(mode):
     """Eq. 3 extrapolates along a fixed direction: W_hat(s) - W = s (W_hat(1) - W)."""
     W, m, v = _state()
@@ -182,6 +182,49 @@ def test_predict_literal_hand_values():
     # s = 3 moves three times as far; t has no effect in this mode
     got3 = om.predict(W, m, v, 100, 3, mode=om.PRED_LITERAL, **HP)
     np.testing.assert_allclose(1.0 - got3, 3 * (1.0 - got), rtol=1e-12)
+
+
+@pytest.mark.parametrize("wd", [0.0, 5e-4])
+@pytest.mark.parametrize("k", [1, 2, 9])
+def test_predict_smoothed_is_momentum_buffer(wd, k):
+    """SpecTrain's predictor (Sec. II) moves W by s steps of momentum SGD's
+    smoothed gradient.  The heavy-ball buffer is kept by its own recurrence in
+    momentum_sgd_update (and matched to torch.optim.SGD above); with beta1
+    equal to the momentum, the smoothed mode read from the first moment must
+    give W - s lr buf for every s, with the same gradients and weight decay."""
+    rng = np.random.default_rng(21)
+    n = 300
+    W = rng.normal(0, 0.05, n)
+    buf, m, v = np.zeros(n), np.zeros(n), np.zeros(n)
+    mu, lr = SGD["momentum"], SGD["lr"]
+    for _ in range(k):
+        g = rng.normal(0, 10 ** rng.uniform(-4, -1), n)
+        W, buf, m, v = om.momentum_sgd_update(W, buf, m, v, g, lr, mu, wd, mu, HP["beta2"])
+    for s in (1, 2, 7):
+        got = om.predict(W, m, v, k, s, lr, mu, HP["beta2"], HP["eps"], mode=om.PRED_SMOOTHED)
+        np.testing.assert_allclose(got, W - s * lr * buf, rtol=0, atol=1e-16)
+        np.testing.assert_allclose(got - W, -s * lr * buf, rtol=1e-9, atol=1e-16)
+
+
+@pytest.mark.parametrize("c", [0.3, -1e-3, 2.0])
+@pytest.mark.parametrize("k", [1, 3, 40])
+def test_predict_smoothed_constant_gradient_closed_form(c, k):
+    """Constant gradient c from zero moments: m = c (1 - beta1^k), so the
+    smoothed-gradient prediction is W - s lr c (1 - beta1^k) / (1 - beta1),
+    with no bias correction and no second moment (v scaled by 100 changes
+    nothing)."""
+    W = np.array([0.25, -0.5, 0.0])
+    m, v = np.zeros(3), np.zeros(3)
+    G = np.full(3, c)
+    for t in range(1, k + 1):
+        W, m, v = om.adam_update(W, m, v, G, t, **HP)
+    b1, lr = HP["beta1"], HP["lr"]
+    for s in (1, 3):
+        want = W - s * lr * c * (1.0 - b1 ** k) / (1.0 - b1)
+        got = om.predict(W, m, v, k, s, mode=om.PRED_SMOOTHED, **HP)
+        np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-17)
+        got_v = om.predict(W, m, 100.0 * v, k, s, mode=om.PRED_SMOOTHED, **HP)
+        assert np.array_equal(got_v, got)
 
 
 def test_predict_adamdir_one_step_is_adam_step():

@@ -87,7 +87,7 @@ def traffic_run(args):
     import torch
     # eager launches: the counters are taken per dispatch (same kernels and
     # arguments as the recorded passes)
-    w, ms, wall, classes, fin = time_stage(args, timing_pass=False, graphs=False)
+    w, ms, wall, classes, fin = time_stage(args, timing_pass=False, graphs=False, fwd_stream=False)
     a = torch.empty(CALIB_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
     b = torch.empty_like(a)
     for _ in range(3):
@@ -147,7 +147,7 @@ def stored_traffic(kernel):
 
 
 def time_stage(args, timing_pass=True, graphs=True, workload=None, dtype=None, s_fwd=None,
-               steps=None, warmup=None):
+               steps=None, warmup=None, fwd_stream=True):
     import dataclasses
     import torch
     import paper_1911_04610_amd as xp
@@ -185,13 +185,20 @@ def time_stage(args, timing_pass=True, graphs=True, workload=None, dtype=None, s
     state = {"t": 0}
     st.xpipe_predict_weights(xp.FWD, w.s_fwd, hp, 0)
     st.xpipe_predict_weights(xp.BWD, w.s_bwd, hp, 0)
+    stream = torch.cuda.current_stream()
+    # the forwards on a stream of their own, beside the backwards
+    fs = torch.cuda.Stream() if fwd_stream else None
+    if fs is not None:
+        st.xpipe_stage_set_fwd_stream(fs)
 
     def step(j):
+        # steady-state order of a pipeline stage: the forward of one
+        # micro-batch, then the backward of one (here the same micro-batch, as
+        # on the last stage), T times; then the update with the next predictions
         J = len(xs)
         for i in range(w.T):
             st.xpipe_stage_fwd(xs[j % J][i], y, None if labels is None else labels[j % J][i],
                                loss if w.has_loss else None)
-        for i in range(w.T):
             st.xpipe_stage_bwd(xs[j % J][i], None if dys is None else dys[j % J][i],
                                None if labels is None else labels[j % J][i], dx)
         st.xpipe_adam_step(hp, state["t"], w.s_fwd, w.s_bwd, emit_pred=True)
@@ -200,21 +207,27 @@ def time_stage(args, timing_pass=True, graphs=True, workload=None, dtype=None, s
     for j in range(warmup):
         step(j)
     torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     e0.record(stream)
+    if fs is not None:
+        fs.wait_stream(stream)
     for j in range(steps):
         step(j)
+    if fs is not None:
+        stream.wait_stream(fs)
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms = e0.elapsed_time(e1) / steps
+    if fs is not None:
+        st.xpipe_stage_set_fwd_stream(None)
     if not timing_pass:
         return w, ms, wall, {}, True
     # the two passes apart (recorded graphs, all lanes): T forwards, then T
     # backwards (each with its recomputed forward), microseconds per micro-batch
     def pass_us(fn, reps=10):
+        fn()  # records the pass's graphs (dropped when the forward stream was unset)
         torch.cuda.synchronize()
         a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a0.record(stream)
@@ -274,19 +287,25 @@ def time_interleaved(args, minibatches=6):
     events = xp.xpipe_schedule(w.size, w.T, w.rank, minibatches)
     hp = xp.Hyper()
     run = lambda t: st.xpipe_stage_run(events, xs, ys, hp, t, dy=dys, labels=labels, loss=loss, dx=dxs)
+    # forwards on a stream of their own, beside the backwards
+    stream, fs = torch.cuda.current_stream(), torch.cuda.Stream()
+    st.xpipe_stage_set_fwd_stream(fs)
     run(0)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
+    fs.wait_stream(stream)
     run(minibatches)
+    stream.wait_stream(fs)
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1)
     return {"size": w.size, "rank": w.rank, "T": w.T, "minibatches": minibatches,
             "samples_per_s": round(n * w.micro_batch / (ms / 1e3), 2),
             "ms_per_minibatch": round(ms / minibatches, 4),
-            "note": "interleaved one-forward-one-backward order of this rank; a prediction per "
-                    "bellwether and direction, updates kept separate from predictions"}
+            "note": "interleaved one-forward-one-backward order of this rank, forwards on their "
+                    "own stream; a prediction per bellwether and direction, updates kept separate "
+                    "from predictions"}
 
 
 def time_partitioned(args, net, stages=4, steps=10, warmup=3):

@@ -131,6 +131,7 @@ _SIGS = {
     "xpipe_probe_stream": [ctypes.POINTER(_P), _I32, ctypes.POINTER(_P), _I32, _I64, _P],
     "xpipe_stage_set_timing": [_P, _I32],
     "xpipe_stage_set_graphs": [_P, _I32],
+    "xpipe_stage_set_fwd_stream": [_P, _P, _P, ctypes.c_size_t],
     "xpipe_stage_timing_count": [_P, ctypes.POINTER(_I32)],
     "xpipe_stage_timing_entry": [_P, _I32, ctypes.POINTER(ctypes.c_char_p),
                                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64),
@@ -237,6 +238,8 @@ class Stage:
         self.device = torch.device(device)
         self.stream = stream
         self.P, ws = xpipe_stage_query(layers, micro_batch, in_shape, dtype)
+        self.ws_bytes = ws
+        self.fwd_workspace = self.fwd_stream = None
         f32 = dict(dtype=torch.float32, device=self.device)
         self.W = torch.zeros(self.P, **f32)
         self.m = torch.zeros(self.P, **f32)
@@ -296,6 +299,19 @@ class Stage:
 
     def xpipe_stage_fwd(self, x, y, labels=None, loss=None):
         _check(lib().xpipe_stage_fwd(self._h, _ptr(x), _ptr(y), _ptr(labels), _ptr(loss)))
+
+    def xpipe_stage_set_fwd_stream(self, stream):
+        """Forwards on `stream` (a torch stream other than the stage's) with a
+        workspace of their own, allocated here; None: back on the stage's stream."""
+        import torch
+        if stream is None:
+            _check(lib().xpipe_stage_set_fwd_stream(self._h, None, None, 0))
+            self.fwd_workspace = self.fwd_stream = None
+            return
+        buf = torch.empty(max(self.ws_bytes, 256) + 256, dtype=torch.uint8, device=self.device)
+        ptr = (buf.data_ptr() + 255) // 256 * 256
+        _check(lib().xpipe_stage_set_fwd_stream(self._h, _stream_ptr(stream), ptr, self.ws_bytes))
+        self.fwd_workspace, self.fwd_stream = buf, stream
 
     def xpipe_stage_bwd(self, x, dy=None, labels=None, dx=None):
         _check(lib().xpipe_stage_bwd(self._h, _ptr(x), _ptr(dy), _ptr(labels), _ptr(dx)))

@@ -165,8 +165,20 @@ struct xpipe_stage {
   hipStream_t stream = nullptr;
   float *W = nullptr, *m = nullptr, *v = nullptr, *grad = nullptr;
   float *wpf = nullptr, *wpb = nullptr;
+  // workspace: ws holds the running pass's activations, gradients and
+  // scratch; wws the weight copies derived from the predictions (bf16
+  // shadows, gathered and flipped weights), written only by the prediction
+  // and update calls.  Both are the caller's workspace, except while a
+  // forward runs on its own stream (fwd_stream): then ws is fwd_ws.
   char* ws = nullptr;
+  char* wws = nullptr;
   size_t ws_bytes = 0;
+  size_t ws_need = 0;  // the plan's workspace size (xpipe_stage_query)
+  hipStream_t fwd_stream = nullptr;
+  char* fwd_ws = nullptr;
+  hipEvent_t pred_ev = nullptr;  // stage stream: the last write of the forward prediction
+  hipEvent_t fwd_ev = nullptr;   // fwd_stream: the last forward
+  bool fwd_pending = false;      // a forward was enqueued on fwd_stream since the stage stream last waited
   int64_t P = 0;
   std::vector<ParamT> params;
   std::vector<Tensor> tensors;  // [0] = stage input
@@ -1028,10 +1040,10 @@ struct HookScope {
 };
 
 const void* gemm_weights(xpipe_stage* st, const Op& op, int dir) {
-  if (!op.segs.empty()) return st->ws + op.wg_off[dir];
+  if (!op.segs.empty()) return st->wws + op.wg_off[dir];
   if (st->dtype == DT_BF16) {
     int64_t off = dir == XPIPE_FWD ? st->bf_f_off : st->bf_b_off;
-    return st->ws + off + (size_t)op.w_off * 2;
+    return st->wws + off + (size_t)op.w_off * 2;
   }
   return (dir == XPIPE_FWD ? st->wpf : st->wpb) + op.w_off;
 }
@@ -1392,7 +1404,7 @@ xpipe_status run_backward(xpipe_stage* st, const Ctx& c, const void* dy, const i
           ConvArgs a{};
           a.x = g.p;
           a.ldx = g.ld;
-          a.w = st->ws + op.wd_off;
+          a.w = st->wws + op.wd_off;
           a.y = dx.p;
           a.ldy = dx.ld;
           mask_of(pool ? pool->in : op.in, a.mask, a.ldm);
@@ -1763,10 +1775,10 @@ xpipe_status refresh_gathered(xpipe_stage* st, int dir) {
     for (const auto& sg : op.segs) {
       const int q = g.nseg++;
       if (st->dtype == DT_BF16)
-        g.src[q] = st->ws + (dir == XPIPE_FWD ? st->bf_f_off : st->bf_b_off) + (size_t)sg.first * 2;
+        g.src[q] = st->wws + (dir == XPIPE_FWD ? st->bf_f_off : st->bf_b_off) + (size_t)sg.first * 2;
       else
         g.src[q] = (dir == XPIPE_FWD ? st->wpf : st->wpb) + sg.first;
-      g.dst[q] = st->ws + op.wg_off[dir] + (size_t)base * esz;
+      g.dst[q] = st->wws + op.wg_off[dir] + (size_t)base * esz;
       g.count[q] = K * sg.second;
       base += g.count[q];
       if (g.nseg == GATHER_BATCH) {
@@ -1788,7 +1800,7 @@ xpipe_status refresh_flipped(xpipe_stage* st) {
     if (op.kind != OP_GEMM) continue;
     const int q = f.n++;
     f.w[q] = gemm_weights(st, op, XPIPE_BWD);
-    f.wd[q] = st->ws + op.wd_off;
+    f.wd[q] = st->wws + op.wd_off;
     f.N[q] = op.cout;
     f.R[q] = op.k;
     f.S[q] = op.kw;
@@ -1811,8 +1823,27 @@ void drop_graphs(xpipe_stage* st) {
   st->pass_graphs.clear();
 }
 
+// Forwards on their own stream (xpipe_stage_set_fwd_stream): a call that
+// rewrites the forward prediction (or what derives from it) first makes the
+// stage's stream wait for the forwards enqueued before it, and afterwards
+// marks the point the next forward waits for.
+xpipe_status wait_forwards(xpipe_stage* st) {
+  if (!st->fwd_pending) return XPIPE_OK;
+  XP_HIP(hipStreamWaitEvent(st->stream, st->fwd_ev, 0));
+  st->fwd_pending = false;
+  return XPIPE_OK;
+}
+
+xpipe_status mark_prediction(xpipe_stage* st) {
+  if (!st->fwd_stream) return XPIPE_OK;
+  XP_HIP(hipEventRecord(st->pred_ev, st->stream));
+  return XPIPE_OK;
+}
+
 void release_lanes(xpipe_stage* st) {
   drop_graphs(st);
+  if (st->pred_ev) (void)hipEventDestroy(st->pred_ev);
+  if (st->fwd_ev) (void)hipEventDestroy(st->fwd_ev);
   if (st->cap_stream) (void)hipStreamDestroy(st->cap_stream);
   for (int pass = 0; pass < 2; ++pass)
     for (hipEvent_t e : st->op_ev[pass])
@@ -1964,8 +1995,9 @@ xpipe_status create_stage(const xpipe_layer_desc* layers, int32_t n_layers, int3
   st->grad = grad;
   st->wpf = w_pred_fwd;
   st->wpb = w_pred_bwd;
-  st->ws = (char*)workspace;
+  st->ws = st->wws = (char*)workspace;
   st->ws_bytes = workspace_bytes;
+  st->ws_need = p.ws;
   st->P = p.P;
   st->params = p.params;
   st->tensors = p.tensors;
@@ -2134,7 +2166,8 @@ xpipe_status xpipe_predict_weights(xpipe_stage_t st, int32_t which, int32_t s, c
   PredCoef c = pred_coef(hp, hp->t, s);
   float* out = which == XPIPE_FWD ? st->wpf : st->wpb;
   bf16_t* obf = nullptr;
-  if (st->dtype == DT_BF16) obf = (bf16_t*)(st->ws + (which == XPIPE_FWD ? st->bf_f_off : st->bf_b_off));
+  if (st->dtype == DT_BF16) obf = (bf16_t*)(st->wws + (which == XPIPE_FWD ? st->bf_f_off : st->bf_b_off));
+  if (which == XPIPE_FWD) XP_OK(wait_forwards(st));
   {
     XP_HIP(launch_predict(st->W, st->m, st->v, out, obf, st->P, c, st->stream));
   }
@@ -2144,8 +2177,9 @@ xpipe_status xpipe_predict_weights(xpipe_stage_t st, int32_t which, int32_t s, c
   if (which == XPIPE_BWD) {
     r = refresh_flipped(st);
     if (r != XPIPE_OK) return r;
+    return XPIPE_OK;
   }
-  return XPIPE_OK;
+  return mark_prediction(st);
 }
 
 xpipe_status xpipe_stage_fwd(xpipe_stage_t st, const void* x, void* y, const int32_t* labels, float* loss) {
@@ -2159,7 +2193,22 @@ xpipe_status xpipe_stage_fwd(xpipe_stage_t st, const void* x, void* y, const int
   c.y = y;
   float* ls = st->has_loss ? loss : nullptr;
   const void* const key[5] = {x, y, labels, ls, nullptr};
-  return run_graphed(st, 0, key, [&] { return run_forward(st, XPIPE_FWD, c, labels, ls); });
+  if (!st->fwd_stream || st->timing)
+    return run_graphed(st, 0, key, [&] { return run_forward(st, XPIPE_FWD, c, labels, ls); });
+  // on the forward stream, with the forward workspace, after the last write
+  // of the forward prediction
+  XP_HIP(hipStreamWaitEvent(st->fwd_stream, st->pred_ev, 0));
+  hipStream_t caller = st->stream;
+  char* pass_ws = st->ws;
+  st->stream = st->lane_stream[0] = st->fwd_stream;
+  st->ws = st->fwd_ws;
+  xpipe_status r = run_graphed(st, 0, key, [&] { return run_forward(st, XPIPE_FWD, c, labels, ls); });
+  st->stream = st->lane_stream[0] = caller;
+  st->ws = pass_ws;
+  if (r != XPIPE_OK) return r;
+  XP_HIP(hipEventRecord(st->fwd_ev, st->fwd_stream));
+  st->fwd_pending = true;
+  return XPIPE_OK;
 }
 
 xpipe_status xpipe_stage_bwd(xpipe_stage_t st, const void* x, const void* dy, const int32_t* labels, void* dx) {
@@ -2180,6 +2229,32 @@ xpipe_status xpipe_stage_bwd(xpipe_stage_t st, const void* x, const void* dy, co
   });
   if (s != XPIPE_OK) return s;
   st->bwd_since_step++;
+  return XPIPE_OK;
+}
+
+xpipe_status xpipe_stage_set_fwd_stream(xpipe_stage_t st, void* hip_stream, void* workspace,
+                                        size_t workspace_bytes) {
+  if (!st) return fail(XPIPE_EINVAL, "null stage");
+  hipStream_t fs = (hipStream_t)hip_stream;
+  if (fs) {
+    if (st->one_lane) return fail(XPIPE_EUNSUPPORTED, "a static-workspace stage runs on one stream");
+    if (fs == st->stream) return fail(XPIPE_EINVAL, "the forward stream must differ from the stage's stream");
+    if (!workspace) return fail(XPIPE_EINVAL, "null forward workspace");
+    if (workspace_bytes < st->ws_need) return fail(XPIPE_EINVAL, "forward workspace too small");
+    if ((reinterpret_cast<uintptr_t>(workspace) % WS_ALIGN) != 0)
+      return fail(XPIPE_EINVAL, "forward workspace must be 256-byte aligned");
+  }
+  // the recorded forwards used the other workspace and stream: finish them
+  if (st->fwd_stream) XP_HIP(hipStreamSynchronize(st->fwd_stream));
+  XP_HIP(hipStreamSynchronize(st->stream));
+  st->fwd_pending = false;
+  drop_graphs(st);
+  st->fwd_stream = fs;
+  st->fwd_ws = fs ? (char*)workspace : nullptr;
+  if (!fs) return XPIPE_OK;
+  if (!st->pred_ev) XP_HIP(hipEventCreateWithFlags(&st->pred_ev, hipEventDisableTiming));
+  if (!st->fwd_ev) XP_HIP(hipEventCreateWithFlags(&st->fwd_ev, hipEventDisableTiming));
+  XP_HIP(hipEventRecord(st->pred_ev, st->stream));
   return XPIPE_OK;
 }
 
@@ -2207,9 +2282,10 @@ xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t 
   bf16_t* ff = nullptr;
   bf16_t* fb = nullptr;
   if (emit_pred && st->dtype == DT_BF16) {
-    ff = (bf16_t*)(st->ws + st->bf_f_off);
-    fb = (bf16_t*)(st->ws + st->bf_b_off);
+    ff = (bf16_t*)(st->wws + st->bf_f_off);
+    fb = (bf16_t*)(st->wws + st->bf_b_off);
   }
+  if (emit_pred) XP_OK(wait_forwards(st));
   {
     XP_HIP(launch_adam(st->W, st->m, st->v, st->grad, st->P, a, 1, emit_pred ? st->wpf : nullptr, ff, cf,
                        emit_pred ? st->wpb : nullptr, fb, cb, st->stream));
@@ -2223,7 +2299,8 @@ xpipe_status xpipe_adam_step(xpipe_stage_t st, const xpipe_hparams* hp, int32_t 
     xpipe_status r = refresh_gathered(st, d);
     if (r != XPIPE_OK) return r;
   }
-  return refresh_flipped(st);
+  XP_OK(refresh_flipped(st));
+  return mark_prediction(st);
 }
 
 xpipe_status xpipe_rule_step(xpipe_stage_t st, const xpipe_rule_hparams* rp, const xpipe_hparams* hp,
@@ -2246,9 +2323,10 @@ xpipe_status xpipe_rule_step(xpipe_stage_t st, const xpipe_rule_hparams* rp, con
   bf16_t* ff = nullptr;
   bf16_t* fb = nullptr;
   if (emit_pred && st->dtype == DT_BF16) {
-    ff = (bf16_t*)(st->ws + st->bf_f_off);
-    fb = (bf16_t*)(st->ws + st->bf_b_off);
+    ff = (bf16_t*)(st->wws + st->bf_f_off);
+    fb = (bf16_t*)(st->wws + st->bf_b_off);
   }
+  if (emit_pred) XP_OK(wait_forwards(st));
   XP_HIP(launch_rule(rp->rule, st->W, buf, sq, st->m, st->v, st->grad, st->P, rule_coef(rp, hp), 1,
                      emit_pred ? st->wpf : nullptr, ff, cf, emit_pred ? st->wpb : nullptr, fb, cb, st->stream));
   st->bwd_since_step = 0;
@@ -2260,12 +2338,15 @@ xpipe_status xpipe_rule_step(xpipe_stage_t st, const xpipe_rule_hparams* rp, con
     xpipe_status r = refresh_gathered(st, d);
     if (r != XPIPE_OK) return r;
   }
-  return refresh_flipped(st);
+  XP_OK(refresh_flipped(st));
+  return mark_prediction(st);
 }
 
 xpipe_status xpipe_stage_destroy(xpipe_stage_t st) {
   if (!st) return fail(XPIPE_EINVAL, "null stage");
-  // auxiliary lanes finish their work before their streams go away
+  // auxiliary lanes (and the forward stream) finish their work before the
+  // streams, events and graphs go away
+  if (st->fwd_stream) (void)hipStreamSynchronize(st->fwd_stream);
   for (int l = 1; l < NLANES; ++l)
     if (st->lane_stream[l]) (void)hipStreamSynchronize(st->lane_stream[l]);
   release_lanes(st);

@@ -186,10 +186,8 @@ def time_stage(args, timing_pass=True, graphs=True, workload=None, dtype=None, s
     st.xpipe_predict_weights(xp.FWD, w.s_fwd, hp, 0)
     st.xpipe_predict_weights(xp.BWD, w.s_bwd, hp, 0)
     stream = torch.cuda.current_stream()
-    # the forwards on a stream of their own, beside the backwards
-    fs = torch.cuda.Stream() if fwd_stream else None
-    if fs is not None:
-        st.xpipe_stage_set_fwd_stream(fs)
+    # the forwards on a stream of the stage's own, beside the backwards
+    fs = st.xpipe_stage_set_fwd_stream(True) if fwd_stream else None
 
     def step(j):
         # steady-state order of a pipeline stage: the forward of one
@@ -221,7 +219,7 @@ def time_stage(args, timing_pass=True, graphs=True, workload=None, dtype=None, s
     wall = time.perf_counter() - t0
     ms = e0.elapsed_time(e1) / steps
     if fs is not None:
-        st.xpipe_stage_set_fwd_stream(None)
+        st.xpipe_stage_set_fwd_stream(False)
     if not timing_pass:
         return w, ms, wall, {}, True
     # the two passes apart (recorded graphs, all lanes): T forwards, then T
@@ -287,9 +285,9 @@ def time_interleaved(args, minibatches=6):
     events = xp.xpipe_schedule(w.size, w.T, w.rank, minibatches)
     hp = xp.Hyper()
     run = lambda t: st.xpipe_stage_run(events, xs, ys, hp, t, dy=dys, labels=labels, loss=loss, dx=dxs)
-    # forwards on a stream of their own, beside the backwards
-    stream, fs = torch.cuda.current_stream(), torch.cuda.Stream()
-    st.xpipe_stage_set_fwd_stream(fs)
+    # forwards on a stream of the stage's own, beside the backwards
+    stream = torch.cuda.current_stream()
+    fs = st.xpipe_stage_set_fwd_stream(True)
     run(0)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)

@@ -401,23 +401,24 @@ xpipe_status xpipe_stage_set_graphs(xpipe_stage_t st, int32_t enable);
  * another (Sec. III-A); the two read different weight versions (the cached
  * forward and backward predictions, Sec. III-B) and share no activations
  * (the backward recomputes its forward), so they may run concurrently.
- * After this call, xpipe_stage_fwd enqueues on hip_stream (the caller's, not
- * the stage's stream) and keeps its activations and scratch in `workspace`
- * (caller-owned device memory of at least xpipe_stage_query's
- * workspace_bytes, 256-byte aligned, used by this stage until the forward
- * stream is set again or the stage is destroyed).  Every other call stays on
- * the stage's stream.  Ordering kept by the library: a forward starts after
- * the last call that wrote the forward prediction (xpipe_predict_weights(FWD),
- * or an update with emit_pred = 1); such a call waits for the forwards
- * enqueued before it.  The caller orders the forward's inputs (x, labels) and
- * outputs (y, loss) against hip_stream itself.  Results are identical to
- * forwards on the stage's stream.  hip_stream = NULL goes back to one stream.
- * The call synchronises both streams and drops the recorded passes.  Timing
- * mode runs forwards on the stage's stream.  EINVAL: hip_stream equal to the
- * stage's stream, workspace NULL, too small or misaligned; EUNSUPPORTED for a
- * stage of xpipe_stage_create_static. */
-xpipe_status xpipe_stage_set_fwd_stream(xpipe_stage_t st, void* hip_stream, void* workspace,
-                                        size_t workspace_bytes);
+ * With a workspace given, xpipe_stage_fwd enqueues on a stream the stage
+ * owns (one of its launch lanes, returned in *hip_stream when hip_stream is
+ * not NULL; valid until the stage is destroyed) and keeps its activations and
+ * scratch in `workspace` (caller-owned device memory of at least
+ * xpipe_stage_query's workspace_bytes, 256-byte aligned, used by this stage
+ * until this call is made again or the stage is destroyed).  Every other
+ * call stays on the stage's stream.  Ordering kept by the library: a forward
+ * starts after the last call that wrote the forward prediction
+ * (xpipe_predict_weights(FWD), or an update with emit_pred = 1), and such a
+ * call waits for the forwards enqueued before it.  The caller orders the
+ * forward's inputs (x, labels) and outputs (y, loss) against the returned
+ * stream itself.  Results are identical to forwards on the stage's stream.
+ * workspace = NULL goes back to one stream (*hip_stream = NULL).  The call
+ * synchronises both streams and drops the recorded passes.  Timing mode runs
+ * forwards on the stage's stream.  EINVAL: workspace too small or
+ * misaligned; EUNSUPPORTED for a stage of xpipe_stage_create_static. */
+xpipe_status xpipe_stage_set_fwd_stream(xpipe_stage_t st, void* workspace, size_t workspace_bytes,
+                                        void** hip_stream);
 xpipe_status xpipe_stage_timing_count(xpipe_stage_t st, int32_t* n);
 xpipe_status xpipe_stage_timing_entry(xpipe_stage_t st, int32_t i, const char** kernel, double* ms,
                                       int64_t* launches, double* work);

@@ -131,7 +131,7 @@ _SIGS = {
     "xpipe_probe_stream": [ctypes.POINTER(_P), _I32, ctypes.POINTER(_P), _I32, _I64, _P],
     "xpipe_stage_set_timing": [_P, _I32],
     "xpipe_stage_set_graphs": [_P, _I32],
-    "xpipe_stage_set_fwd_stream": [_P, _P, _P, ctypes.c_size_t],
+    "xpipe_stage_set_fwd_stream": [_P, _P, ctypes.c_size_t, ctypes.POINTER(_P)],
     "xpipe_stage_timing_count": [_P, ctypes.POINTER(_I32)],
     "xpipe_stage_timing_entry": [_P, _I32, ctypes.POINTER(ctypes.c_char_p),
                                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64),
@@ -300,18 +300,23 @@ class Stage:
     def xpipe_stage_fwd(self, x, y, labels=None, loss=None):
         _check(lib().xpipe_stage_fwd(self._h, _ptr(x), _ptr(y), _ptr(labels), _ptr(loss)))
 
-    def xpipe_stage_set_fwd_stream(self, stream):
-        """Forwards on `stream` (a torch stream other than the stage's) with a
-        workspace of their own, allocated here; None: back on the stage's stream."""
+    def xpipe_stage_set_fwd_stream(self, enable: bool):
+        """Forwards on a stream of the stage's own, with a workspace of their
+        own (allocated here), beside the backwards on the stage's stream.
+        Returns that stream as a torch.cuda.ExternalStream (None when
+        disabled), for ordering the forwards' inputs and outputs."""
         import torch
-        if stream is None:
-            _check(lib().xpipe_stage_set_fwd_stream(self._h, None, None, 0))
+        if not enable:
+            _check(lib().xpipe_stage_set_fwd_stream(self._h, None, 0, None))
             self.fwd_workspace = self.fwd_stream = None
-            return
+            return None
         buf = torch.empty(max(self.ws_bytes, 256) + 256, dtype=torch.uint8, device=self.device)
         ptr = (buf.data_ptr() + 255) // 256 * 256
-        _check(lib().xpipe_stage_set_fwd_stream(self._h, _stream_ptr(stream), ptr, self.ws_bytes))
-        self.fwd_workspace, self.fwd_stream = buf, stream
+        s = _P()
+        _check(lib().xpipe_stage_set_fwd_stream(self._h, ptr, self.ws_bytes, ctypes.byref(s)))
+        self.fwd_workspace = buf
+        self.fwd_stream = torch.cuda.ExternalStream(s.value, device=self.device)
+        return self.fwd_stream
 
     def xpipe_stage_bwd(self, x, dy=None, labels=None, dx=None):
         _check(lib().xpipe_stage_bwd(self._h, _ptr(x), _ptr(dy), _ptr(labels), _ptr(dx)))

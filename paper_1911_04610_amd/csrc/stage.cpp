@@ -2240,14 +2240,12 @@ xpipe_status xpipe_stage_bwd(xpipe_stage_t st, const void* x, const void* dy, co
   return XPIPE_OK;
 }
 
-xpipe_status xpipe_stage_set_fwd_stream(xpipe_stage_t st, void* hip_stream, void* workspace,
-                                        size_t workspace_bytes) {
+xpipe_status xpipe_stage_set_fwd_stream(xpipe_stage_t st, void* workspace, size_t workspace_bytes,
+                                        void** hip_stream) {
   if (!st) return fail(XPIPE_EINVAL, "null stage");
-  hipStream_t fs = (hipStream_t)hip_stream;
-  if (fs) {
+  if (hip_stream) *hip_stream = nullptr;
+  if (workspace) {
     if (st->one_lane) return fail(XPIPE_EUNSUPPORTED, "a static-workspace stage runs on one stream");
-    if (fs == st->stream) return fail(XPIPE_EINVAL, "the forward stream must differ from the stage's stream");
-    if (!workspace) return fail(XPIPE_EINVAL, "null forward workspace");
     if (workspace_bytes < st->ws_need) return fail(XPIPE_EINVAL, "forward workspace too small");
     if ((reinterpret_cast<uintptr_t>(workspace) % WS_ALIGN) != 0)
       return fail(XPIPE_EINVAL, "forward workspace must be 256-byte aligned");
@@ -2257,12 +2255,25 @@ xpipe_status xpipe_stage_set_fwd_stream(xpipe_stage_t st, void* hip_stream, void
   XP_HIP(hipStreamSynchronize(st->stream));
   st->fwd_pending = false;
   drop_graphs(st);
+  // The stage's last launch lane, which no pass uses while the forwards have
+  // their own stream (the forward and the recomputed forward are chains on
+  // lane 0, the backward starts chains on PASS_LANES[1] lanes).  Measured
+  // against a stream of the caller's (torch's stream pool): the same step
+  // times when the two streams land on different hardware queues, but from
+  // one stage creation to the next the caller's stream could share the
+  // stage's queue (VGG stage 0.98 against 0.86 ms, ResNet middle stage 7.31
+  // against 6.41 ms, Inception-A 7.82 against 6.29 ms); the lane was 0.86,
+  // 6.40-6.41 and 6.28-6.35 ms every time.  A stream with a hardware queue of
+  // its own (a full CU mask) was 1.3-5x slower.
+  static_assert(PASS_LANES[1] < NLANES, "the forward stream is a lane the backward does not use");
+  hipStream_t fs = workspace ? st->lane_stream[NLANES - 1] : nullptr;
   st->fwd_stream = fs;
   st->fwd_ws = fs ? (char*)workspace : nullptr;
   if (!fs) return XPIPE_OK;
   if (!st->pred_ev) XP_HIP(hipEventCreateWithFlags(&st->pred_ev, hipEventDisableTiming));
   if (!st->fwd_ev) XP_HIP(hipEventCreateWithFlags(&st->fwd_ev, hipEventDisableTiming));
   XP_HIP(hipEventRecord(st->pred_ev, st->stream));
+  if (hip_stream) *hip_stream = (void*)fs;
   return XPIPE_OK;
 }
 

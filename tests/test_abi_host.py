@@ -135,7 +135,7 @@ def test_flat_entry_points_check_arguments_on_the_host():
     # misaligned buffers are refused before any launch
     assert L.xpipe_predict_flat(20, 16, 16, 16, None, 8, 1, ctypes.byref(hp), None) == xp.EINVAL
     assert L.xpipe_adam_flat(None, None, None, None, 0, ctypes.byref(hp), 1, None, 0, None, 0, None) == xp.OK
-    assert L.xpipe_stage_set_fwd_stream(None, None, None, 0) == xp.EINVAL
+    assert L.xpipe_stage_set_fwd_stream(None, None, 0, None) == xp.EINVAL
     # the bare-stream probe: counts, sizes and alignment are checked first
     P = ctypes.c_void_p
     src = (P * 4)(16, 32, 48, 64)

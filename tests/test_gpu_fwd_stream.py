@@ -37,9 +37,8 @@ def _run(w, inp, dtype, overlap, order, graphs=True):
     st.set_flat(st.W, inp.params)
     st.set_flat(st.m, inp.m)
     st.set_flat(st.v, inp.v)
-    fs = torch.cuda.Stream() if overlap else None
     if overlap:
-        st.xpipe_stage_set_fwd_stream(fs)
+        assert st.xpipe_stage_set_fwd_stream(True) is not None
     J, T = len(inp.xs), w.T
     xs = [[to_device(x, dtype) for x in row] for row in inp.xs]
     labels = None if inp.labels is None else [[torch.from_numpy(l).cuda() for l in row]
@@ -124,21 +123,25 @@ def test_forward_stream_full_size_inception_a():
 
 def test_forward_stream_arguments():
     import torch
+    import ctypes
     w = SMALL["tiny_mlp"]()
-    s0, s = torch.cuda.Stream(), torch.cuda.Stream()
+    s0 = torch.cuda.Stream()
     st = xp.Stage(w.layers, w.micro_batch, w.T, w.in_shape, xp.F32, stream=s0)
     L = xp.lib()
     buf = torch.empty(st.ws_bytes + 512, dtype=torch.uint8, device="cuda")
     base = (buf.data_ptr() + 255) // 256 * 256
-    assert L.xpipe_stage_set_fwd_stream(st._h, s0.cuda_stream, base, st.ws_bytes) == xp.EINVAL  # its own
-    assert L.xpipe_stage_set_fwd_stream(st._h, s.cuda_stream, None, st.ws_bytes) == xp.EINVAL
-    assert L.xpipe_stage_set_fwd_stream(st._h, s.cuda_stream, base, st.ws_bytes - 1) == xp.EINVAL
-    assert L.xpipe_stage_set_fwd_stream(st._h, s.cuda_stream, base + 16, st.ws_bytes) == xp.EINVAL
-    assert L.xpipe_stage_set_fwd_stream(st._h, s.cuda_stream, base, st.ws_bytes) == xp.OK
-    assert L.xpipe_stage_set_fwd_stream(st._h, None, None, 0) == xp.OK
+    fs = ctypes.c_void_p(1)
+    assert L.xpipe_stage_set_fwd_stream(st._h, base, st.ws_bytes - 1, ctypes.byref(fs)) == xp.EINVAL
+    assert fs.value is None
+    assert L.xpipe_stage_set_fwd_stream(st._h, base + 16, st.ws_bytes, None) == xp.EINVAL
+    assert L.xpipe_stage_set_fwd_stream(st._h, base, st.ws_bytes, ctypes.byref(fs)) == xp.OK
+    assert fs.value not in (None, s0.cuda_stream)          # a stream of the stage's own
+    assert L.xpipe_stage_set_fwd_stream(st._h, None, 0, ctypes.byref(fs)) == xp.OK
+    assert fs.value is None
     one = xp.Stage(w.layers, w.micro_batch, w.T, w.in_shape, xp.F32, static_workspace=True)
     try:
-        assert L.xpipe_stage_set_fwd_stream(one._h, s.cuda_stream, base, st.ws_bytes) == xp.EUNSUPPORTED
+        assert L.xpipe_stage_set_fwd_stream(one._h, base, st.ws_bytes, None) == xp.EUNSUPPORTED
+        assert L.xpipe_stage_set_fwd_stream(one._h, None, 0, None) == xp.OK
     finally:
         one.destroy()
     torch.cuda.synchronize()

@@ -25,18 +25,21 @@ def _small(name):
                      layers=wl.inception_stage_layers(modules=1, classes=10), spatial=(9, 9))
 
 
-CASES = [  # (workload, size, rank, rule, draft)
-    ("tiny_mlp", 4, 0, None, False),
-    ("tiny_mlp", 4, 2, None, False),
-    ("tiny_mlp", 4, 2, None, True),
-    ("tiny_mlp", 4, 3, xp.RULE_MOMENTUM_SGD, False),
-    ("vgg16_stage0", 4, 0, xp.RULE_MOMENTUM_SGD, True),
-    ("inception_v3_stage", 4, 1, None, False),
+CASES = [  # (workload, size, rank, rule, draft, forwards on the stage's forward stream)
+    ("tiny_mlp", 4, 0, None, False, False),
+    ("tiny_mlp", 4, 2, None, False, False),
+    ("tiny_mlp", 4, 2, None, True, False),
+    ("tiny_mlp", 4, 3, xp.RULE_MOMENTUM_SGD, False, False),
+    ("vgg16_stage0", 4, 0, xp.RULE_MOMENTUM_SGD, True, False),
+    ("inception_v3_stage", 4, 1, None, False, False),
+    ("tiny_mlp", 4, 2, None, True, True),
+    ("vgg16_stage0", 4, 0, xp.RULE_MOMENTUM_SGD, True, True),
+    ("inception_v3_stage", 4, 1, None, False, True),
 ]
 
 
-@pytest.mark.parametrize("name,size,rank,rule,draft", CASES)
-def test_interleaved_schedule_matches_oracle(name, size, rank, rule, draft):
+@pytest.mark.parametrize("name,size,rank,rule,draft,fwd_stream", CASES)
+def test_interleaved_schedule_matches_oracle(name, size, rank, rule, draft, fwd_stream):
     import torch
     w = _small(name)
     inp = wl.stage_inputs(w, act_dtype="f32", moment_init="paper")
@@ -65,6 +68,9 @@ def test_interleaved_schedule_matches_oracle(name, size, rank, rule, draft):
     dyd = None if dys is None else [to_device(d, xp.F32) for d in dys]
     loss = torch.zeros(len(xs), dtype=torch.float32, device="cuda") if w.has_loss else None
     buf = torch.zeros(st.P, dtype=torch.float32, device="cuda")
+    if fwd_stream:
+        st.xpipe_stage_set_fwd_stream(True)
+    torch.cuda.synchronize()
     st.xpipe_stage_run(events, xd, yd, hp, 0, dy=dyd, labels=lab, loss=loss, dx=dxd, rule=r,
                        buf=buf, draft=draft)
     torch.cuda.synchronize()

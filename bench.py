@@ -309,8 +309,8 @@ def time_interleaved(args, minibatches=6):
 def time_partitioned(args, net, stages=4, steps=10, warmup=3):
     """A whole network split into `stages` stages by the paper's partition rule
     (xpipe_partition), each stage trained on its own as its GPU would (T
-    forwards, T backwards with recomputation, Adam fused with the next
-    predictions; bf16).  Reports each stage's step time and the pipeline's
+    forward/backward pairs, the forwards on the stage's forward stream and the
+    backwards with recomputation, Adam fused with the next predictions; bf16).  Reports each stage's step time and the pipeline's
     steady-state throughput bound, the slowest stage's (synthetic inputs and
     upstream gradients of each stage's shapes).  VGG-16: CIFAR-10 images
     (32 x 32), micro-batch 32, T = 4 (mini-batch 128).  ResNet-101 and
@@ -348,11 +348,12 @@ def time_partitioned(args, net, stages=4, steps=10, warmup=3):
         st.xpipe_predict_weights(xp.FWD, 1, hp, 0)
         st.xpipe_predict_weights(xp.BWD, 1, hp, 0)
         state = {"t": 0}
+        stream = torch.cuda.current_stream()
+        fs = st.xpipe_stage_set_fwd_stream(True)  # forwards beside the backwards
 
         def step():
             for _ in range(T):
                 st.xpipe_stage_fwd(x, y, lab, loss)
-            for _ in range(T):
                 st.xpipe_stage_bwd(x, dy, lab, dx)
             st.xpipe_adam_step(hp, state["t"], 1, 1, emit_pred=True)
             state["t"] += 1
@@ -362,8 +363,10 @@ def time_partitioned(args, net, stages=4, steps=10, warmup=3):
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
+        fs.wait_stream(stream)
         for _ in range(steps):
             step()
+        stream.wait_stream(fs)
         e1.record()
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / steps

@@ -209,7 +209,9 @@ xpipe_status xpipe_predict_weights(xpipe_stage_t st, int32_t which, int32_t s,
  * y: stage output (logits for a loss stage), written.  labels: int32
  * [micro_batch] in [0, classes), required iff the stage ends in SOFTMAX_CE;
  * loss (fp32 scalar, may be NULL) receives this micro-batch's share of the
- * mini-batch loss.  ESTATE before the first forward prediction. */
+ * mini-batch loss.  ESTATE before the first forward prediction.  Enqueued on
+ * the stage's stream, or on its forward stream once one is set
+ * (xpipe_stage_set_fwd_stream). */
 xpipe_status xpipe_stage_fwd(xpipe_stage_t st, const void* x, void* y, const int32_t* labels,
                              float* loss);
 

@@ -694,17 +694,37 @@ __global__ __launch_bounds__(256) void k_bn_apply_v(BnApplyArgs a) {
   const RowMap m = row_map<T>(a.C);
   if (!m.live) return;
   const int c0 = m.chunk * N;
+  // one BN, or the BN whose channel range holds this chunk (y, gamma and beta
+  // then start at the range's first channel)
+  T* Y = (T*)a.y;
+  int ldy = a.ldy, yc = c0, relu = a.relu;
+  const float* gam = a.gamma + c0;
+  const float* bet = a.beta + c0;
+  if (a.nseg > 0) {
+    bool found = false;
+#pragma unroll
+    for (int q = 0; q < BN_APPLY_SEGS; ++q)
+      if (q < a.nseg && c0 >= a.seg_c0[q] && c0 < a.seg_c1[q]) {
+        found = true;
+        Y = (T*)a.seg_y[q];
+        ldy = a.seg_ldy[q];
+        yc = c0 - a.seg_c0[q];
+        relu = a.seg_relu[q];
+        gam = a.seg_gamma[q] + yc;
+        bet = a.seg_beta[q] + yc;
+      }
+    if (!found) return;
+  }
   double mu[N], rs[N], ga[N], be[N];
 #pragma unroll
   for (int e = 0; e < N; ++e) {
     mu[e] = a.mean[c0 + e];
     rs[e] = a.rstd[c0 + e];
-    ga[e] = (double)a.gamma[c0 + e];
-    be[e] = (double)a.beta[c0 + e];
+    ga[e] = (double)gam[e];
+    be[e] = (double)bet[e];
   }
   const T* Z = (const T*)a.z;
   const T* R = (const T*)a.res;
-  T* Y = (T*)a.y;
   for (int r0 = m.row0; r0 < a.M; r0 += U * m.stride) {
     uint4 zr[U], rr[U];
 #pragma unroll
@@ -729,10 +749,10 @@ __global__ __launch_bounds__(256) void k_bn_apply_v(BnApplyArgs a) {
         double v = ga[e] * xh + be[e];
         // the BN output is rounded to the storage type before the residual add
         if (R) v = rnd<T>(v) + q[e];
-        if (a.relu) v = v > 0.0 ? v : 0.0;
+        if (relu) v = v > 0.0 ? v : 0.0;
         z[e] = v;
       }
-      vst(Y + (size_t)r * a.ldy + c0, z);
+      vst(Y + (size_t)r * ldy + yc, z);
     }
   }
 }
@@ -1588,7 +1608,16 @@ constexpr int BN_APPLY_U = 4, BN_BWD_U = 4;
 
 hipError_t launch_bn_apply(int dtype, const BnApplyArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.C <= 0) return hipSuccess;
-  if (vec_dt(dtype, a.M, a.C, {{a.z, a.ldz}, {a.res, a.ldres}, {a.y, a.ldy}})) {
+  if (a.nseg > 0) {
+    // several BNs in one launch: the 16-byte chunk path only, no residual
+    const int N = vn(dtype);
+    bool ok = a.nseg <= BN_APPLY_SEGS && !a.res && vec_dt(dtype, a.M, a.C, {{a.z, a.ldz}});
+    for (int q = 0; ok && q < a.nseg; ++q)
+      ok = a.seg_c0[q] % N == 0 && a.seg_c1[q] % N == 0 && a.seg_c0[q] < a.seg_c1[q] &&
+           a.seg_c1[q] <= a.C && vec_dt(dtype, a.M, a.seg_c1[q] - a.seg_c0[q], {{a.seg_y[q], a.seg_ldy[q]}});
+    if (!ok) return hipErrorInvalidValue;
+  }
+  if (a.nseg > 0 || vec_dt(dtype, a.M, a.C, {{a.z, a.ldz}, {a.res, a.ldres}, {a.y, a.ldy}})) {
     const int N = vn(dtype);
     const dim3 grid = row_grid(a.M, a.C, N, BN_APPLY_U);
     const double bytes = (double)a.M * a.C * (dtype == DT_BF16 ? 2 : 4) * (a.res ? 3 : 2);

@@ -118,7 +118,7 @@ struct Op {
   bool stats = false;          // GEMM: writes mean / rstd of every output column ...
   int64_t stat_block = -1;     // ... to this workspace block ([2][cout] doubles, then dbeta/dgamma)
   bool stats_fused = false;    // BN: statistics come from the producing GEMM
-  int stats_from = -1;         // BN: index of that GEMM op (during planning)
+  int stats_from = -1;         // BN: index of that GEMM op
   // bf16: BNs whose output gradients are completed by one GEMM's data
   // gradient (the last of its input's gradient writers) take their backward
   // column sums from that launch's epilogue
@@ -133,6 +133,7 @@ struct Op {
   int pool_bwd = -1;           // GEMM: the average-pool op
   int pool_by = -1;            // AVGPOOL: the GEMM op that takes its backward
   int64_t box_off = -1;        // GEMM: workspace bytes of the averaged output gradient
+  int apply_grp = -1;          // BN: its group of BNs over one merged GEMM's slices
   // launch lanes, per pass (0 forward, 1 backward): the lane this op runs on,
   // the ops (same pass) on other lanes it waits for, and whether later ops on
   // other lanes wait for it
@@ -220,6 +221,7 @@ struct xpipe_stage {
   bool graphs = true;
   bool capturing = false;  // a pass is being recorded on cap_stream
   std::vector<int> rec_order[2];  // op order while recording (see Plan)
+  std::vector<std::vector<int>> apply_groups;
   hipStream_t cap_stream = nullptr;
   std::vector<PassGraph> pass_graphs;
   uint64_t graph_clock = 0;
@@ -249,6 +251,7 @@ struct Plan {
   // topological order of the lane plan that takes the lanes in turn, so the
   // graph's launches interleave the independent branches
   std::vector<int> rec_order[2];
+  std::vector<std::vector<int>> apply_groups;  // BN ops applied by one launch (see Op)
 };
 
 // Channel range a tensor occupies in its buffer: (buffer tensor, first, end).
@@ -789,6 +792,28 @@ xpipe_status build_plan(const xpipe_layer_desc* L, int n, int mb, int H, int W, 
     }
   }
 
+  // ---- the BNs over one merged GEMM's slices (statistics from its epilogue,
+  // no residual) can be applied by one launch; taken when a pass runs as a
+  // single chain of launches, where it removes launches without serialising
+  // anything (with parallel lanes the separate launches let the branches start
+  // apart, which measured faster)
+  for (size_t j = 0; j < p.ops.size(); ++j) {
+    const Op& g = p.ops[j];
+    if (g.kind != OP_GEMM || g.segs.empty() || !g.stats) continue;
+    std::vector<int> mem;
+    bool ok = true;
+    for (size_t i = 0; i < p.ops.size(); ++i) {
+      const Op& bn = p.ops[i];
+      if (bn.kind != OP_BN || !bn.stats_fused || bn.stats_from != (int)j || bn.in2 >= 0) continue;
+      const Tensor& z = p.tensors[bn.in];
+      ok = ok && z.coff % 8 == 0 && z.sh.C % 8 == 0;
+      mem.push_back((int)i);
+    }
+    if (!ok || mem.size() < 2 || mem.size() > (size_t)BN_APPLY_SEGS) continue;
+    for (int i : mem) p.ops[i].apply_grp = (int)p.apply_groups.size();
+    p.apply_groups.push_back(mem);
+  }
+
   // ---- backward accumulation order: walk ops in reverse; first contribution writes
   {
     std::vector<bool> written(p.tensors.size(), false);
@@ -1184,6 +1209,8 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
                          float* loss, bool chain = false) {
   const int dt = st->dtype;
   Lanes lanes(st, 0, chain);
+  // as one chain, a group of BNs is applied by one launch at its first member
+  std::vector<char> grp_done(chain ? st->apply_groups.size() : 0, 0);
   for (int i : pass_order(st, 0)) {
     const Op& op = st->ops[i];
     if (op.kind == OP_CONCAT) continue;
@@ -1238,6 +1265,36 @@ xpipe_status run_forward(xpipe_stage* st, int dir, const Ctx& c, const int32_t* 
         break;
       }
       case OP_BN: {
+        if (chain && op.apply_grp >= 0) {
+          if (grp_done[op.apply_grp]) break;
+          grp_done[op.apply_grp] = 1;
+          const std::vector<int>& mem = st->apply_groups[op.apply_grp];
+          const Op& g = st->ops[op.stats_from];
+          const double* gst = (const double*)(st->ws + g.stat_block);
+          View z = act(st, g.out, c);
+          BnApplyArgs b{};
+          b.z = z.p;
+          b.ldz = z.ld;
+          b.mean = gst;
+          b.rstd = gst + g.cout;
+          b.M = (int)tin.sh.rows();
+          b.C = g.cout;
+          b.nseg = (int)mem.size();
+          for (int q = 0; q < b.nseg; ++q) {
+            const Op& bn = st->ops[mem[q]];
+            const Tensor& zt = st->tensors[bn.in];
+            View y = act(st, bn.out, c);
+            b.seg_c0[q] = zt.coff;
+            b.seg_c1[q] = zt.coff + zt.sh.C;
+            b.seg_y[q] = y.p;
+            b.seg_ldy[q] = y.ld;
+            b.seg_gamma[q] = fp32_param(st, bn.g_off, dir);
+            b.seg_beta[q] = fp32_param(st, bn.be_off, dir);
+            b.seg_relu[q] = bn.relu;
+          }
+          XP_HIP(launch_bn_apply(dt, b, s));
+          break;
+        }
         double* stats = (double*)(st->ws + op.stat_off);
         ColArgs ca{};
         ca.mode = COL_STATS;
@@ -2007,6 +2064,7 @@ xpipe_status create_stage(const xpipe_layer_desc* layers, int32_t n_layers, int3
   st->bnb_nrb.assign(st->ops.size(), 0);
   st->rec_order[0] = p.rec_order[0];
   st->rec_order[1] = p.rec_order[1];
+  st->apply_groups = p.apply_groups;
   st->out_tensor = p.out_tensor;
   st->has_loss = p.has_loss;
   st->classes = p.classes;

@@ -198,6 +198,7 @@ hipError_t launch_colreduce(int dtype, const ColArgs& a, hipStream_t s);
 hipError_t launch_colfinal(const ColArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- element-wise
+constexpr int BN_APPLY_SEGS = 4;
 struct BnApplyArgs {
   const void* z; int ldz;
   const double* mean; const double* rstd;
@@ -205,6 +206,15 @@ struct BnApplyArgs {
   const void* res; int ldres;     // optional residual (added before the ReLU)
   void* y; int ldy;
   int M, C, relu;
+  // nseg > 0: the BNs over channel ranges [seg_c0, seg_c1) of z (multiples of
+  // the 16-byte chunk; mean / rstd indexed by the channel of z), each with its
+  // own output, gamma / beta (from its first channel) and ReLU flag; y, gamma,
+  // beta and relu above are unused, and so is res (none)
+  int nseg;
+  int seg_c0[BN_APPLY_SEGS], seg_c1[BN_APPLY_SEGS];
+  void* seg_y[BN_APPLY_SEGS]; int seg_ldy[BN_APPLY_SEGS];
+  const float* seg_gamma[BN_APPLY_SEGS]; const float* seg_beta[BN_APPLY_SEGS];
+  int seg_relu[BN_APPLY_SEGS];
 };
 hipError_t launch_bn_apply(int dtype, const BnApplyArgs& a, hipStream_t s);
 

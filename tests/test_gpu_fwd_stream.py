@@ -8,7 +8,6 @@ output and loss, every input gradient, and W, m, v and both predictions after
 each update.  The calls are issued both as forward/backward pairs (the
 steady-state order of the last stage) and as all forwards then all
 backwards, with recorded passes and eagerly."""
-import numpy as np
 import pytest
 
 import paper_1911_04610_amd as xp

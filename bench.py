@@ -87,7 +87,7 @@ def traffic_run(args):
     import torch
     # eager launches: the counters are taken per dispatch (same kernels and
     # arguments as the recorded passes)
-    w, ms, wall, classes, fin = time_stage(args, timing_pass=False, graphs=False, fwd_stream=False)
+    w, ms, wall, classes, fin = time_stage(args, timing_pass=False, graphs=False)
     a = torch.empty(CALIB_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
     b = torch.empty_like(a)
     for _ in range(3):
@@ -242,7 +242,10 @@ def time_stage(args, timing_pass=True, graphs=True, workload=None, dtype=None, s
                                                         for i in range(w.T)]), 1)}
     time_stage.passes = passes
     # per-kernel durations with HIP events around every launch, over the same
-    # number of steps
+    # number of steps: the timed step's launches (with the forward stream set,
+    # the chained forwards), all on the stage's stream
+    if fs is not None:
+        st.xpipe_stage_set_fwd_stream(True)
     st.set_timing(True)
     for j in range(steps):
         step(j)

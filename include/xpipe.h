@@ -416,9 +416,12 @@ xpipe_status xpipe_stage_set_graphs(xpipe_stage_t st, int32_t enable);
  * forward's inputs (x, labels) and outputs (y, loss) against the returned
  * stream itself.  Results are identical to forwards on the stage's stream.
  * workspace = NULL goes back to one stream (*hip_stream = NULL).  The call
- * synchronises both streams and drops the recorded passes.  Timing mode runs
- * forwards on the stage's stream.  EINVAL: workspace too small or
- * misaligned; EUNSUPPORTED for a stage of xpipe_stage_create_static. */
+ * synchronises both streams and drops the recorded passes.  While it is set,
+ * the forward and the backward's recomputed forward each run as one chain of
+ * launches (the BNs over a merged GEMM's slices applied by one launch), which
+ * is faster beside the backward.  Timing mode runs the same launches on the
+ * stage's stream.  EINVAL: workspace too small or misaligned; EUNSUPPORTED
+ * for a stage of xpipe_stage_create_static. */
 xpipe_status xpipe_stage_set_fwd_stream(xpipe_stage_t st, void* workspace, size_t workspace_bytes,
                                         void** hip_stream);
 xpipe_status xpipe_stage_timing_count(xpipe_stage_t st, int32_t* n);

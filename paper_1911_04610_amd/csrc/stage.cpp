@@ -2253,8 +2253,10 @@ xpipe_status xpipe_stage_fwd(xpipe_stage_t st, const void* x, void* y, const int
   c.y = y;
   float* ls = st->has_loss ? loss : nullptr;
   const void* const key[5] = {x, y, labels, ls, nullptr};
+  // (timing mode: on the stage's stream, but the same launches)
   if (!st->fwd_stream || st->timing)
-    return run_graphed(st, 0, key, [&] { return run_forward(st, XPIPE_FWD, c, labels, ls); });
+    return run_graphed(st, 0, key,
+                       [&] { return run_forward(st, XPIPE_FWD, c, labels, ls, st->fwd_stream != nullptr); });
   // on the forward stream, with the forward workspace, after the last write
   // of the forward prediction
   XP_HIP(hipStreamWaitEvent(st->fwd_stream, st->pred_ev, 0));

@@ -23,15 +23,18 @@ class GpuRecord:
 
 
 def run_stage(w, inp, dtype, hp, s_fwd, s_bwd, minibatches=None, fused=True, need_dx=True,
-              stage=None, reuse_inputs=False, rule=None):
+              stage=None, reuse_inputs=False, rule=None, fwd_stream=False):
     """Mini-batch loop of the XPipe stage step on the GPU.  With fused=True the
     Adam step also emits the next mini-batch's predictions (no separate
     predict calls after the first mini-batch).  reuse_inputs feeds mini-batch
     0's buffers to every mini-batch (same pointers on every call).  rule (an
-    xp.Rule) updates with momentum SGD / RMSProp instead of Adam."""
+    xp.Rule) updates with momentum SGD / RMSProp instead of Adam.  fwd_stream
+    runs the forwards on the stage's forward stream (each output is read after
+    that stream)."""
     import torch
     J = len(inp.xs) if minibatches is None else minibatches
     st = stage or xp.Stage(w.layers, w.micro_batch, w.T, w.in_shape, dtype)
+    fs = st.xpipe_stage_set_fwd_stream(True) if fwd_stream else None
     st.set_flat(st.W, inp.params)
     st.set_flat(st.m, inp.m)
     st.set_flat(st.v, inp.v)
@@ -57,6 +60,8 @@ def run_stage(w, inp, dtype, hp, s_fwd, s_bwd, minibatches=None, fused=True, nee
         for i in range(w.T):
             st.xpipe_stage_fwd(xs[j][i], y, None if labels is None else labels[j][i],
                                loss if w.has_loss else None)
+            if fs is not None:
+                torch.cuda.current_stream().wait_stream(fs)
             r.ys.append(to_host(y).reshape(out_shape_oracle))
             r.losses.append(float(loss.item()) if w.has_loss else None)
         r.w_pred_fwd = st.get_tensors(st.w_pred_fwd)

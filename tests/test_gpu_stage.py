@@ -58,13 +58,16 @@ def _compare(gpu, ref, tol, what):
 
 
 @pytest.mark.parametrize("name", list(CASES))
-def test_stage_step_fp32_matches_oracle(name):
+@pytest.mark.parametrize("fwd_stream", [False, True])
+def test_stage_step_fp32_matches_oracle(name, fwd_stream):
     """fp32 storage, fp64 arithmetic: every tensor of every mini-batch within
     2e-4 of the oracle's fp32-storage model (decisions taken on the same
-    stored values on both sides) and of the exact fp64 oracle."""
+    stored values on both sides) and of the exact fp64 oracle; with the
+    forwards on one stream with the backwards, and on the stage's forward
+    stream (chained passes) beside them."""
     w = CASES[name]()
     inp = wl.stage_inputs(w, act_dtype="f32")
-    gpu, _ = run_stage(w, inp, xp.F32, xp.Hyper(), w.s_fwd, w.s_bwd)
+    gpu, _ = run_stage(w, inp, xp.F32, xp.Hyper(), w.s_fwd, w.s_bwd, fwd_stream=fwd_stream)
     for storage in ("f32", "f64"):
         # the fp32-storage model, and the plain fp64 oracle that rounds nothing
         # (fp32 storage of fp64-computed values stays ~1e-6 from it here)

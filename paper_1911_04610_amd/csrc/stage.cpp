@@ -163,7 +163,8 @@ struct xpipe_stage {
   std::vector<xpipe_layer_desc> layers;
   int mb = 0, T = 1, dtype = DT_F32;
   Shape in_shape;
-  hipStream_t stream = nullptr;
+  hipStream_t stream = nullptr;     // the stream launches go to (swapped while a pass records or a forward runs on fwd_stream)
+  hipStream_t own_stream = nullptr; // the stage's stream as created
   float *W = nullptr, *m = nullptr, *v = nullptr, *grad = nullptr;
   float *wpf = nullptr, *wpb = nullptr;
   // workspace: ws holds the running pass's activations, gradients and
@@ -1950,6 +1951,9 @@ xpipe_status run_graphed(xpipe_stage* st, int kind, const void* const (&ptr)[5],
   if (e != hipSuccess) return fail(XPIPE_EHIP, std::string("hipGraphInstantiate: ") + hipGetErrorString(e));
   constexpr size_t MAX_GRAPHS = 64;
   if (st->pass_graphs.size() >= MAX_GRAPHS) {
+    // the evicted graph may still run on either stream
+    if (st->fwd_stream) XP_HIP(hipStreamSynchronize(st->fwd_stream));
+    XP_HIP(hipStreamSynchronize(st->own_stream));
     auto old = std::min_element(st->pass_graphs.begin(), st->pass_graphs.end(),
                                 [](const auto& a, const auto& b) { return a.used < b.used; });
     (void)hipGraphExecDestroy(old->exec);
@@ -2047,7 +2051,7 @@ xpipe_status create_stage(const xpipe_layer_desc* layers, int32_t n_layers, int3
   st->T = T;
   st->dtype = dtype;
   st->in_shape = Shape{micro_batch, H, W, C};
-  st->stream = (hipStream_t)hip_stream;
+  st->stream = st->own_stream = (hipStream_t)hip_stream;
   st->W = W_;
   st->m = m;
   st->v = v;
@@ -2340,6 +2344,9 @@ xpipe_status xpipe_stage_set_fwd_stream(xpipe_stage_t st, void* workspace, size_
 xpipe_status xpipe_stage_set_graphs(xpipe_stage_t st, int32_t enable) {
   if (!st) return fail(XPIPE_EINVAL, "null stage");
   if (st->one_lane && enable) return fail(XPIPE_EUNSUPPORTED, "a static-workspace stage records no passes");
+  // the kept graphs may still run
+  if (st->fwd_stream) XP_HIP(hipStreamSynchronize(st->fwd_stream));
+  XP_HIP(hipStreamSynchronize(st->stream));
   st->graphs = enable != 0;
   drop_graphs(st);
   return XPIPE_OK;

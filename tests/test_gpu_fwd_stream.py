@@ -144,3 +144,43 @@ def test_forward_stream_arguments():
     finally:
         one.destroy()
     torch.cuda.synchronize()
+
+
+def test_forward_stream_many_recorded_passes():
+    """More distinct pointer sets than the stage keeps recorded passes (64):
+    the least recently used graphs are dropped while passes still run on both
+    streams.  Outputs and the accumulated gradient must equal an eager run on
+    one stream, bit for bit."""
+    import torch
+    w = SMALL["tiny_mlp"]()
+    inp = wl.stage_inputs(w, act_dtype="f32", moment_init="paper")
+    n = 80
+    g = torch.Generator().manual_seed(5)
+    xs = [torch.randn((w.micro_batch,) + tuple(w.in_shape), generator=g).cuda() for _ in range(n)]
+    labels = [torch.randint(0, 10, (w.micro_batch,), generator=g, dtype=torch.int32).cuda()
+              for _ in range(n)] if w.has_loss else None
+    hp = xp.Hyper()
+    outs = []
+    for overlap in (False, True):
+        st = xp.Stage(w.layers, w.micro_batch, w.T, w.in_shape, xp.F32)
+        st.set_graphs(overlap)
+        st.set_flat(st.W, inp.params)
+        st.set_flat(st.m, inp.m)
+        st.set_flat(st.v, inp.v)
+        if overlap:
+            st.xpipe_stage_set_fwd_stream(True)
+        st.xpipe_predict_weights(xp.FWD, 1, hp, 3)
+        st.xpipe_predict_weights(xp.BWD, 1, hp, 3)
+        ys = [torch.empty(st.out_shape, dtype=torch.float32, device="cuda") for _ in range(n)]
+        dys = None if w.has_loss else [torch.randn(st.out_shape, generator=g).cuda() for _ in range(n)]
+        torch.cuda.synchronize()
+        for k in range(n):
+            st.xpipe_stage_fwd(xs[k], ys[k], None if labels is None else labels[k], None)
+            st.xpipe_stage_bwd(xs[k], None if dys is None else dys[k],
+                               None if labels is None else labels[k], None)
+        torch.cuda.synchronize()
+        outs.append((ys, st.grad.clone()))
+        st.destroy()
+    for k in range(n):
+        assert torch.equal(outs[0][0][k], outs[1][0][k]), f"y[{k}]"
+    assert torch.equal(outs[0][1], outs[1][1]), "grad"
